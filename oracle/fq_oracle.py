@@ -1,0 +1,258 @@
+"""CPU float64 oracle for FrameQuant's per-layer quantization pass.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the package smoke check and the benchmark's
+CPU-baseline leg may import this module.  It shares no code with the device library and
+never calls it.
+
+Plain numpy/LAPACK in float64.  Inputs are the exact values the device consumed (rounded
+once to the device dtype, upcast exactly).  Each function follows the passage of the
+paper (FrameQuant, Adepu et al., ICML 2024) named in its docstring; where the paper
+defers to OPTQ/GPTQ (Frantar et al. 2023), the published algorithm is written out step by
+step.  Readings of silent or garbled passages are listed where they are used:
+
+* Alg. 1 step 3 prints "D = 2 sigma clip(...)"; read as the clip alone at
+  mu +/- clip_sigmas * sigma, mu and sigma scalars over all of D, sigma with N - 1.
+* The quantization grid is OPTQ's asymmetric per-row min/max grid (the paper stores a
+  per-row scale and bias, appendix "Storage benefits"): lo = min(0, min row),
+  hi = max(0, max row), lo = hi = 0 -> (-1, 1); scale = (hi - lo) / (2^bits - 1),
+  rounded to float32 (the stored precision); zero = round-half-even(-lo / scale).
+* H is the unscaled X^T X; OPTQ's damping is relative (damp * mean of the diagonal) and
+  its updates are scale-free, so a constant factor on H changes nothing.
+* OPTQ with act-order off, one group per row, dead columns (zero diagonal) get a unit
+  diagonal and zero weights; damping damp * mean(diag) is added to the diagonal.
+* Rounding is half-to-even everywhere.
+
+Parity unpinned: the grid variant, sigma's N - 1, the rotation law of the frames and the
+act-order choice are readings; the paper prints no quantized layer to pin them against.
+"""
+from __future__ import annotations
+
+import numpy as np
+import scipy.linalg as sla
+
+TIE_EPS = 1e-6
+
+
+# --------------------------------------------------------------------------- stage 1
+def hessian(X_chunks) -> np.ndarray:
+    """Calibration Hessian H = X^T X = A_prev A_prev^T (Sec. 3, proxy loss: the FF-space
+    Hessian is C C^T with C = P_prev^T A_prev, so C C^T = P_prev^T (X^T X) P_prev).
+
+    X_chunks: one (n x d_in) array or an iterable of row chunks; summed in float64.
+    """
+    if isinstance(X_chunks, np.ndarray):
+        X_chunks = [X_chunks]
+    H = None
+    for X in X_chunks:
+        X = np.asarray(X, dtype=np.float64)
+        G = X.T @ X
+        H = G if H is None else H + G
+    return H
+
+
+# --------------------------------------------------------------------------- stage 2
+def frame_analysis(W, P_out, P_in, H):
+    """FF-space weights and Hessian (Sec. 3; Alg. 1 step 1):
+    D = P_l^T Theta P_prev and H~ = P_prev^T H P_prev (= C_prev C_prev^T)."""
+    W = np.asarray(W, dtype=np.float64)
+    P_out = np.asarray(P_out, dtype=np.float64)
+    P_in = np.asarray(P_in, dtype=np.float64)
+    D = P_out.T @ W @ P_in
+    Ht = None if H is None else P_in.T @ np.asarray(H, dtype=np.float64) @ P_in
+    return D, Ht
+
+
+# --------------------------------------------------------------------------- stage 3a
+def clip_bounds(D, clip_sigmas: float = 2.0):
+    """mu = mean(D), sigma = std(D) (ddof 1) over the whole matrix; the clip interval
+    [mu - c sigma, mu + c sigma] (Alg. 1 steps 2-3; Sec. 3, clipping at 2 sigma)."""
+    D = np.asarray(D, dtype=np.float64)
+    mu = D.mean()
+    sigma = D.std(ddof=1) if D.size > 1 else 0.0
+    return mu, sigma, mu - clip_sigmas * sigma, mu + clip_sigmas * sigma
+
+
+def apply_clip(D, lo_b: float, hi_b: float):
+    return np.minimum(np.maximum(np.asarray(D, dtype=np.float64), lo_b), hi_b)
+
+
+def row_grid(D, bits: int = 2):
+    """Per-row asymmetric min/max grid (OPTQ's quantizer; per-row scale and bias stored
+    with the codes, appendix "Storage benefits").  Returns (scale, zero) as float64
+    holding the float32 scale and the integer zero point."""
+    D = np.asarray(D, dtype=np.float64)
+    maxq = 2 ** bits - 1
+    lo = np.minimum(D.min(axis=1), 0.0)
+    hi = np.maximum(D.max(axis=1), 0.0)
+    both0 = (lo == 0) & (hi == 0)
+    lo = np.where(both0, -1.0, lo)
+    hi = np.where(both0, 1.0, hi)
+    scale = ((hi - lo) / maxq).astype(np.float32).astype(np.float64)
+    zero = np.round(-lo / scale)
+    return scale, zero
+
+
+def rtn_codes(x, scale, zero, bits: int = 2):
+    """Round to nearest on the grid: code = clamp(rne(x / scale) + zero, 0, 2^bits - 1).
+    Also returns the pre-rounding value t = x / scale in code units."""
+    maxq = 2 ** bits - 1
+    t = x / scale
+    q = np.clip(np.round(t) + zero, 0, maxq)
+    return q, t
+
+
+def near_tie(t, eps: float = TIE_EPS):
+    """|frac(t) - 1/2| < eps: t lies within eps of a rounding boundary."""
+    return np.abs((t - np.floor(t)) - 0.5) < eps
+
+
+# --------------------------------------------------------------------------- stage 3b
+def gptq_prepare(Ht, damp: float = 0.01):
+    """OPTQ preparation on the FF Hessian (Sec. 3, "quantize(D, C, B) // modified GPTQ"):
+    dead columns (H~_jj = 0) get H~_jj = 1; H~ += damp * mean(diag H~) I;
+    U = upper Cholesky factor of H~^{-1} (U^T U = H~^{-1}).
+    Returns (U, dead mask, damped H~).  Raises numpy.linalg.LinAlgError when the damped
+    H~ is not positive definite."""
+    H = np.array(Ht, dtype=np.float64, copy=True)
+    dead = np.diag(H) == 0
+    H[dead, dead] = 1.0
+    lam = damp * np.mean(np.diag(H))
+    H[np.diag_indices_from(H)] += lam
+    L = np.linalg.cholesky(H)                       # H = L L^T
+    Linv = sla.solve_triangular(L, np.eye(H.shape[0]), lower=True)
+    Hinv = Linv.T @ Linv                            # H^{-1}
+    Hinv = 0.5 * (Hinv + Hinv.T)
+    U = np.linalg.cholesky(Hinv).T                  # U^T U = H^{-1}
+    return U, dead, H
+
+
+# --------------------------------------------------------------------------- stage 3c/3d
+def gptq(D, U, scale, zero, bits: int = 2, block: int = 128, dead=None,
+         forced_codes=None, tie_eps: float = TIE_EPS):
+    """OPTQ's column-sequential rounding with Cholesky error feedback and lazy block
+    updates (Alg. 1 step 4).  For each block [i1, i2) of width `block`, for each column j
+    in order: q = grid-round(w_j); err = (w_j - dq) / U_jj; later columns of the block
+    w_l -= err * U_jl; after the block, columns >= i2 get -= E_block @ U[i1:i2, i2:].
+
+    forced_codes (same shape as D): where the pre-rounding value is within tie_eps of a
+    rounding boundary, adopt that code instead of the oracle's own (teacher forcing).
+    Returns dict(codes, t, tie, E)."""
+    W = np.array(D, dtype=np.float64, copy=True)
+    if dead is not None:
+        W[:, dead] = 0.0
+    rows, n = W.shape
+    maxq = 2 ** bits - 1
+    codes = np.zeros((rows, n), dtype=np.int64)
+    tvals = np.zeros((rows, n))
+    ties = np.zeros((rows, n), dtype=bool)
+    E = np.zeros((rows, n))
+    for i1 in range(0, n, block):
+        i2 = min(i1 + block, n)
+        W1 = W[:, i1:i2].copy()
+        E1 = np.zeros((rows, i2 - i1))
+        for jj in range(i2 - i1):
+            j = i1 + jj
+            w = W1[:, jj]
+            q, t = rtn_codes(w, scale, zero, bits)
+            tie = near_tie(t, tie_eps)
+            if forced_codes is not None:
+                q = np.where(tie, forced_codes[:, j], q)
+            q = np.clip(q, 0, maxq)
+            dq = scale * (q - zero)
+            err = (w - dq) / U[j, j]
+            W1[:, jj:] -= np.outer(err, U[j, j:i2])
+            E1[:, jj] = err
+            codes[:, j] = q
+            tvals[:, j] = t
+            ties[:, j] = tie
+        W[:, i2:] -= E1 @ U[i1:i2, i2:]
+        E[:, i1:i2] = E1
+    return {"codes": codes, "t": tvals, "tie": ties, "E": E}
+
+
+def gptq_obs(D, Hd, scale, zero, bits: int = 2, dead=None):
+    """Second, independent formulation (optimal brain surgeon form): for column j the
+    inverse S of the trailing damped Hessian block H[j:, j:] gives err = (w - dq) / S_00
+    and the update D[:, j:] -= err * S[0, :]; S is downdated by one Schur step."""
+    W = np.array(D, dtype=np.float64, copy=True)
+    if dead is not None:
+        W[:, dead] = 0.0
+    n = W.shape[1]
+    S = np.linalg.inv(np.asarray(Hd, dtype=np.float64))
+    codes = np.zeros(W.shape, dtype=np.int64)
+    for j in range(n):
+        w = W[:, j]
+        q, _ = rtn_codes(w, scale, zero, bits)
+        dq = scale * (q - zero)
+        err = (w - dq) / S[0, 0]
+        W[:, j:] -= np.outer(err, S[0, :])
+        codes[:, j] = q
+        S = S[1:, 1:] - np.outer(S[1:, 0], S[0, 1:]) / S[0, 0]
+    return codes
+
+
+def dequant(codes, scale, zero):
+    """D^ = scale * (q - zero) per row (appendix "Storage benefits": codes plus a
+    per-row scale and bias)."""
+    return np.asarray(scale)[:, None] * (np.asarray(codes, dtype=np.float64) - np.asarray(zero)[:, None])
+
+
+def proxy_loss(D, Dhat, H):
+    """L(D^) = tr((D - D^) H (D - D^)^T) (Sec. 3, proxy loss in FF space)."""
+    R = np.asarray(D, dtype=np.float64) - np.asarray(Dhat, dtype=np.float64)
+    return float(np.einsum("ij,jk,ik->", R, H, R))
+
+
+# --------------------------------------------------------------------------- stage 3e
+def pack2(codes) -> np.ndarray:
+    """2-bit codes -> uint32 words, 16 codes per word, row-major; column j sits in bits
+    2*(j mod 16) .. 2*(j mod 16)+1 of word floor(j / 16); pad bits are zero."""
+    c = np.asarray(codes, dtype=np.uint64)
+    rows, n = c.shape
+    nw = (n + 15) // 16
+    padded = np.zeros((rows, nw * 16), dtype=np.uint64)
+    padded[:, :n] = c
+    padded = padded.reshape(rows, nw, 16)
+    shifts = (2 * np.arange(16, dtype=np.uint64))[None, None, :]
+    return np.bitwise_or.reduce(padded << shifts, axis=2).astype(np.uint32)
+
+
+def unpack2(words, n: int) -> np.ndarray:
+    w = np.asarray(words, dtype=np.uint64)
+    shifts = (2 * np.arange(16, dtype=np.uint64))[None, None, :]
+    c = (w[:, :, None] >> shifts) & np.uint64(3)
+    return c.reshape(w.shape[0], -1)[:, :n].astype(np.int64)
+
+
+# --------------------------------------------------------------------------- stage 4
+def synthesis(codes, scale, zero, P_out, P_in):
+    """Reconstructed weights Theta^ = P_l D^ P_prev^T (Alg. 1 return value without the
+    activations; appendix "Computational Complexity during Inference")."""
+    Dhat = dequant(codes, scale, zero)
+    return np.asarray(P_out, dtype=np.float64) @ Dhat @ np.asarray(P_in, dtype=np.float64).T
+
+
+# --------------------------------------------------------------------------- pipeline
+def quantize_frames(D, Ht, bits=2, block=128, damp=0.01, clip_sigmas=2.0,
+                    forced_codes=None, tie_eps=TIE_EPS):
+    """Alg. 1 steps 2-4 on FF-space inputs: clip, per-row grid, OPTQ rounding."""
+    mu, sigma, lo_b, hi_b = clip_bounds(D, clip_sigmas)
+    Dc = apply_clip(D, lo_b, hi_b)
+    scale, zero = row_grid(Dc, bits)
+    U, dead, Hd = gptq_prepare(Ht, damp)
+    r = gptq(Dc, U, scale, zero, bits, block, dead, forced_codes, tie_eps)
+    r.update(scale=scale, zero=zero, mu=mu, sigma=sigma, Dc=Dc, U=U, dead=dead, Hd=Hd)
+    return r
+
+
+def quantize_layer(W, X_chunks, P_out, P_in, bits=2, block=128, damp=0.01,
+                   clip_sigmas=2.0, H=None):
+    """The whole per-layer pass (Alg. 1): H, analysis, clip, OPTQ, pack, synthesis."""
+    if H is None:
+        H = hessian(X_chunks)
+    D, Ht = frame_analysis(W, P_out, P_in, H)
+    r = quantize_frames(D, Ht, bits, block, damp, clip_sigmas)
+    r["H"], r["D"], r["Ht"] = H, D, Ht
+    r["packed"] = pack2(r["codes"])
+    r["W_hat"] = synthesis(r["codes"], r["scale"], r["zero"], P_out, P_in)
+    return r

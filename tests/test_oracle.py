@@ -1,0 +1,268 @@
+"""Pins for the CPU oracle: closed forms, invariants, special cases and brute force.
+
+Each check is chosen so that a plausible slip in the oracle (a dropped term, a wrong
+sign or index, a transposed operand) fails at least one of them.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from fq_inputs import tff
+import oracle as O
+
+
+def _rng(s=0):
+    return np.random.default_rng(s)
+
+
+# ----------------------------------------------------------------------------- H
+def test_hessian_brute_force_and_chunks():
+    rng = _rng(1)
+    X = rng.standard_normal((7, 5))
+    H = O.hessian(X)
+    for i in range(5):
+        for j in range(5):
+            s = 0.0
+            for t in range(7):
+                s += X[t, i] * X[t, j]
+            assert abs(H[i, j] - s) < 1e-13
+    np.testing.assert_allclose(O.hessian([X[:3], X[3:]]), H, atol=1e-13)
+    np.testing.assert_array_equal(O.hessian(np.eye(4)), np.eye(4))
+
+
+# ----------------------------------------------------------------------------- analysis
+def _frames(d_out, d_in, r_out_k, r_in_k, seed=0, rho=4):
+    P_out = tff.parseval_frame(r_out_k, rho, d_out, np.random.SeedSequence(seed))
+    P_in = tff.parseval_frame(r_in_k, rho, d_in, np.random.SeedSequence(seed + 1))
+    return P_out, P_in
+
+
+def test_analysis_exact_recovery_and_shapes():
+    P_out, P_in = _frames(24, 16, 7, 5)                # K_out = 28, K_in = 20
+    W = _rng(2).standard_normal((24, 16))
+    D, _ = O.frame_analysis(W, P_out, P_in, None)
+    assert D.shape == (28, 20)
+    np.testing.assert_allclose(P_out @ D @ P_in.T, W, atol=1e-13)
+
+
+def test_ff_hessian_equals_C_Ct():
+    """H~ from H via P_prev^T H P_prev equals C C^T with C = P_prev^T A_prev computed
+    directly from the activations (Sec. 3, proxy loss)."""
+    _, P_in = _frames(8, 16, 3, 5)
+    X = _rng(3).standard_normal((40, 16))
+    H = O.hessian(X)
+    _, Ht = O.frame_analysis(np.zeros((8, 16)), np.eye(8), P_in, H)
+    C = P_in.T @ X.T
+    np.testing.assert_allclose(Ht, C @ C.T, atol=1e-11)
+    # rank(H~) <= d_in < K_in: singular without damping when r > 1
+    assert np.linalg.matrix_rank(Ht, tol=1e-9) <= 16 < Ht.shape[0]
+
+
+# ----------------------------------------------------------------------------- clip + grid
+def test_clip_bounds_hand_case():
+    D = np.array([[1.0, 2.0, 3.0], [4.0, 5.0, 30.0]])
+    mu, sigma, lo, hi = O.clip_bounds(D, 2.0)
+    # mean 7.5; squared deviations 42.25+30.25+20.25+12.25+6.25+506.25 = 617.5;
+    # sigma = sqrt(617.5 / (6 - 1))
+    assert mu == pytest.approx(7.5, abs=1e-15)
+    assert sigma == pytest.approx(np.sqrt(123.5), abs=1e-13)
+    Dc = O.apply_clip(D, lo, hi)
+    assert Dc[1, 2] == pytest.approx(7.5 + 2 * np.sqrt(123.5), abs=1e-13)
+    np.testing.assert_array_equal(Dc[0], D[0])
+
+
+def test_row_grid_hand_cases():
+    D = np.array([[-0.3, 0.0, 0.6],      # lo=-0.3 hi=0.6 -> scale 0.3, zero 1
+                  [0.2, 0.5, 0.9],       # lo=0 (min with 0) hi=0.9 -> scale .3, zero 0
+                  [-0.9, -0.3, -0.6],    # lo=-0.9 hi=0 -> scale .3, zero 3
+                  [0.0, 0.0, 0.0]])      # all zero -> (-1, 1) -> scale fl32(2/3)
+    # fl32(2/3) = 0.66666668653..., slightly above 2/3, so -lo/scale = 1.4999999... and
+    # the zero point rounds to 1 (with the exact 2/3 it would be the tie 1.5 -> 2).
+    s, z = O.row_grid(D, 2)
+    np.testing.assert_allclose(s, np.float32([0.3, 0.3, 0.3, 2 / 3]).astype(np.float64), rtol=0)
+    np.testing.assert_array_equal(z, [1, 0, 3, 1])
+    q, t = O.rtn_codes(np.array([-0.3, 0.0, 0.6]), s[0], z[0])
+    np.testing.assert_array_equal(q, [0, 1, 3])
+    # clamping at the grid edges
+    q, _ = O.rtn_codes(np.array([-5.0, 5.0]), s[0], z[0])
+    np.testing.assert_array_equal(q, [0, 3])
+    # half-to-even at an exact tie: t = 0.5 rounds to 0, t = 1.5 to 2
+    q, _ = O.rtn_codes(np.array([0.5, 1.5]), 1.0, 0.0)
+    np.testing.assert_array_equal(q, [0, 2])
+
+
+# ----------------------------------------------------------------------------- GPTQ
+def _problem(rows=6, n=9, seed=4, damp=0.01):
+    rng = _rng(seed)
+    D = rng.standard_normal((rows, n)) * 0.1 + 0.01
+    X = rng.standard_normal((3 * n, n)) @ rng.standard_normal((n, n))
+    Ht = O.hessian(X)
+    s, z = O.row_grid(D)
+    U, dead, Hd = O.gptq_prepare(Ht, damp)
+    return D, Ht, s, z, U, dead, Hd
+
+
+def test_U_is_cholesky_of_inverse_and_ul_identity():
+    _, _, _, _, U, _, Hd = _problem()
+    np.testing.assert_allclose(U.T @ U, np.linalg.inv(Hd), rtol=1e-10, atol=1e-12)
+    assert np.allclose(np.tril(U, -1), 0)
+    # upper-from-bottom route: M = chol(J H J), U = J M^{-1} J
+    J = np.eye(Hd.shape[0])[::-1]
+    M = np.linalg.cholesky(J @ Hd @ J)
+    np.testing.assert_allclose(J @ np.linalg.inv(M) @ J, U, rtol=1e-9, atol=1e-12)
+
+
+def test_identity_hessian_is_rtn():
+    rng = _rng(5)
+    D = rng.standard_normal((5, 12))
+    s, z = O.row_grid(D)
+    U, dead, _ = O.gptq_prepare(np.eye(12), 0.01)
+    r = O.gptq(D, U, s, z, 2, 4, dead)
+    q, _ = O.rtn_codes(D, s[:, None], z[:, None])
+    np.testing.assert_array_equal(r["codes"], q)
+
+
+def test_single_column_is_rtn():
+    rng = _rng(6)
+    D = rng.standard_normal((8, 1))
+    s, z = O.row_grid(D)
+    U, dead, _ = O.gptq_prepare(np.array([[3.7]]), 0.01)
+    r = O.gptq(D, U, s, z, 2, 128, dead)
+    q, _ = O.rtn_codes(D[:, 0], s, z)
+    np.testing.assert_array_equal(r["codes"][:, 0], q)
+
+
+def test_obs_form_and_block_invariance():
+    D, Ht, s, z, U, dead, Hd = _problem(rows=10, n=13, seed=7)
+    ref = O.gptq(D, U, s, z, 2, 13, dead)["codes"]
+    np.testing.assert_array_equal(O.gptq_obs(D, Hd, s, z, 2, dead), ref)
+    for B in (1, 4, 7, 128):
+        np.testing.assert_array_equal(O.gptq(D, U, s, z, 2, B, dead)["codes"], ref)
+
+
+def _levels(scale, zero, bits=2):
+    return scale * (np.arange(2 ** bits) - zero)
+
+
+def test_sequential_conditional_optimality_brute_force():
+    """At every column, the chosen level minimises the damped proxy loss over the 4
+    levels, with earlier columns fixed at their chosen levels and later columns free
+    (continuous least squares) -- OPTQ's greedy step, checked without any Cholesky."""
+    for seed in range(4):
+        D, Ht, s, z, U, dead, Hd = _problem(rows=3, n=6, seed=10 + seed)
+        codes = O.gptq(D, U, s, z, 2, 128, dead)["codes"]
+        n = D.shape[1]
+        for r in range(D.shape[0]):
+            lv = _levels(s[r], z[r])
+            fixed = lv[codes[r]]
+            for j in range(n):
+                best, arg = None, None
+                for c in range(4):
+                    head = np.concatenate([fixed[:j], [lv[c]]])
+                    # minimise (d - v)^T H (d - v) over v[j+1:]
+                    e_head = D[r, :j + 1] - head
+                    Hff = Hd[j + 1:, j + 1:]
+                    Hfh = Hd[j + 1:, :j + 1]
+                    if n - j - 1 > 0:
+                        e_tail = -np.linalg.solve(Hff, Hfh @ e_head)
+                        e = np.concatenate([e_head, e_tail])
+                    else:
+                        e = e_head
+                    loss = e @ Hd @ e
+                    if best is None or loss < best - 1e-12:
+                        best, arg = loss, c
+                assert arg == codes[r, j], (seed, r, j)
+
+
+def test_exhaustive_minimum_not_above_gptq():
+    D, Ht, s, z, U, dead, Hd = _problem(rows=2, n=4, seed=20)
+    res = O.gptq(D, U, s, z, 2, 128, dead)
+    for r in range(2):
+        lv = _levels(s[r], z[r])
+        g = O.proxy_loss(D[r:r + 1], lv[res["codes"][r]][None], Hd)
+        best = min(O.proxy_loss(D[r:r + 1], lv[list(c)][None], Hd)
+                   for c in itertools.product(range(4), repeat=4))
+        assert best <= g + 1e-15
+        # and GPTQ beats plain round-to-nearest on the damped proxy loss
+        q, _ = O.rtn_codes(D[r], s[r], z[r])
+        assert g <= O.proxy_loss(D[r:r + 1], lv[q.astype(int)][None], Hd) + 1e-15
+
+
+def test_dead_column_and_forced_ties():
+    rng = _rng(8)
+    D = rng.standard_normal((4, 5))
+    Ht = O.hessian(rng.standard_normal((20, 5)))
+    Ht[2, :] = 0
+    Ht[:, 2] = 0
+    s, z = O.row_grid(D)
+    U, dead, Hd = O.gptq_prepare(Ht, 0.01)
+    assert dead.tolist() == [False, False, True, False, False]
+    r = O.gptq(D, U, s, z, 2, 2, dead)
+    # the dead column is quantized from zero
+    np.testing.assert_array_equal(r["codes"][:, 2], O.rtn_codes(np.zeros(4), s, z)[0])
+    # forcing codes only bites at near ties
+    forced = (r["codes"] + 1) % 4
+    r2 = O.gptq(D, U, s, z, 2, 2, dead, forced_codes=forced)
+    np.testing.assert_array_equal(r2["codes"], r["codes"])
+    r3 = O.gptq(D, U, s, z, 2, 2, dead, forced_codes=forced, tie_eps=0.6)
+    np.testing.assert_array_equal(r3["codes"], forced)
+
+
+def test_not_positive_definite_without_damping():
+    _, P_in = _frames(8, 16, 3, 5)
+    H = O.hessian(_rng(9).standard_normal((40, 16)))
+    _, Ht = O.frame_analysis(np.zeros((8, 16)), np.eye(8), P_in, H)
+    with pytest.raises(np.linalg.LinAlgError):
+        Hz = Ht.copy()
+        Hz[np.diag_indices_from(Hz)] -= 1e-9 * np.abs(Hz).max()  # make it indefinite
+        O.gptq_prepare(Hz, 0.0)
+
+
+# ----------------------------------------------------------------------------- pack
+def test_pack_layout_hand_case():
+    codes = np.zeros((2, 18), dtype=np.int64)
+    codes[0, 0] = 3            # bits 0-1 of word 0
+    codes[0, 15] = 2           # bits 30-31 of word 0
+    codes[0, 16] = 1           # bits 0-1 of word 1
+    codes[1, 1] = 1            # bits 2-3
+    codes[1, 17] = 3           # bits 2-3 of word 1
+    w = O.pack2(codes)
+    assert w.dtype == np.uint32 and w.shape == (2, 2)
+    assert w[0, 0] == 3 | (2 << 30) and w[0, 1] == 1
+    assert w[1, 0] == 1 << 2 and w[1, 1] == 3 << 2
+    rc = _rng(1).integers(0, 4, size=(5, 37))
+    np.testing.assert_array_equal(O.unpack2(O.pack2(rc), 37), rc)
+
+
+# ----------------------------------------------------------------------------- synthesis
+def test_synthesis_inverts_analysis_at_r1():
+    """With r = 1 both frames are orthogonal, so analysis(synthesis(D^)) = D^ exactly."""
+    P_out = tff.parseval_frame(6, 4, 24, np.random.SeedSequence(1))   # K = d = 24
+    P_in = tff.parseval_frame(4, 4, 16, np.random.SeedSequence(2))
+    rng = _rng(11)
+    codes = rng.integers(0, 4, size=(24, 16))
+    scale = rng.uniform(0.1, 1.0, 24)
+    zero = rng.integers(0, 4, 24).astype(float)
+    Wh = O.synthesis(codes, scale, zero, P_out, P_in)
+    D2, _ = O.frame_analysis(Wh, P_out, P_in, None)
+    np.testing.assert_allclose(D2, O.dequant(codes, scale, zero), atol=1e-12)
+
+
+def test_output_loss_bound_and_pipeline():
+    """||(Theta - Theta^) X^T|| <= ||(D - D^) C|| for the unclipped D; equality at
+    r_out = 1 (P_l has unit singular values)."""
+    rng = _rng(12)
+    W = rng.standard_normal((16, 16)) * 0.05
+    X = rng.standard_normal((64, 16))
+    for k_out in (4, 5):                           # r_out = 1 and 1.25
+        P_out, P_in = _frames(16, 16, k_out, 5, seed=k_out)
+        r = O.quantize_layer(W, X, P_out, P_in, block=4)
+        C = P_in.T @ X.T
+        lhs = np.linalg.norm((W - r["W_hat"]) @ X.T)
+        Dh = O.dequant(r["codes"], r["scale"], r["zero"])
+        rhs = np.linalg.norm((r["D"] - Dh) @ C)
+        assert lhs <= rhs * (1 + 1e-12)
+        if k_out == 4:
+            assert lhs == pytest.approx(rhs, rel=1e-10)
+        np.testing.assert_array_equal(O.unpack2(r["packed"], r["codes"].shape[1]), r["codes"])
