@@ -1,0 +1,147 @@
+/*
+ * fq.h -- C ABI of libfq, FrameQuant's per-layer quantization pass on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * FrameQuant (Adepu, Zeng, Zhang, Singh, ICML 2024) quantizes one linear layer Theta
+ * (d_out x d_in) in the representation of two tight fusion frames: P_l (d_out x K_out)
+ * on the output side and P_prev (d_in x K_in) on the input side (Sec. 3, Alg. 1).  The
+ * pass has four calls, made in this order:
+ *
+ *   fq_hessian_accumulate  H   = X^T X over calibration tokens (Sec. 3, proxy loss)
+ *   fq_frame_analysis      D   = P_l^T Theta P_prev,  H~ = P_prev^T H P_prev (Alg. 1 step 1)
+ *   fq_quantize_frames     2-bit codes of D with OPTQ-style Hessian-aware rounding and
+ *                          Cholesky error feedback after a mu +/- c*sigma clip
+ *                          (Alg. 1 steps 2-5)
+ *   fq_frame_synthesis     Theta^ = P_l D^ P_prev^T (Alg. 1 return value; appendix
+ *                          "Computational Complexity during Inference")
+ *
+ * Conventions shared by every call
+ *  - Matrices are row-major.  Every array argument is a DEVICE pointer owned by the
+ *    caller; the library never allocates device memory.  Each call that needs scratch
+ *    space takes a caller-provided workspace `ws` of at least the size returned by its
+ *    *_workspace_bytes query (16-byte aligned).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are stream-ordered and
+ *    asynchronous, except fq_quantize_frames, which synchronizes `stream` once at its end
+ *    to report the positive-definiteness and finiteness checks.
+ *  - Arguments are validated before anything is launched; on failure the call returns
+ *    FQ_ERR_INVALID_ARG (or FQ_ERR_UNSUPPORTED / FQ_ERR_WORKSPACE_TOO_SMALL) and
+ *    fq_last_error() describes the problem.  No exception crosses the boundary.
+ *  - Calls are thread-safe for distinct buffers and streams; fq_last_error is per thread.
+ *  - Sizes may be zero (the call then does nothing, except that fq_hessian_accumulate
+ *    with accumulate = 0 still writes H = 0).
+ */
+#ifndef FQ_H
+#define FQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FQ_OK = 0,
+  FQ_ERR_INVALID_ARG = 1,           /* bad shape, leading dimension, pointer or scalar */
+  FQ_ERR_UNSUPPORTED = 2,           /* valid request the library does not implement */
+  FQ_ERR_NOT_POSITIVE_DEFINITE = 3, /* damped H~ has a non-positive Cholesky pivot */
+  FQ_ERR_NONFINITE = 4,             /* NaN or Inf in D or H~ */
+  FQ_ERR_WORKSPACE_TOO_SMALL = 5,
+  FQ_ERR_HIP = 6                    /* a HIP runtime call failed */
+} fq_status;
+
+typedef enum { FQ_F32 = 0, FQ_F16 = 1, FQ_BF16 = 2 } fq_dtype;
+
+/*
+ * H (+)= X^T X  -- the calibration Hessian (Sec. 3: the FF-space Hessian H~ = C C^T with
+ * C = P_prev^T A_prev equals P_prev^T (X^T X) P_prev; A_prev = X^T).
+ *   X        device, n_tokens x d_in, element type xt, row stride ldx >= d_in (elements).
+ *            f16/bf16 products are exact in fp32; f32 X is split into two bf16 terms
+ *            (relative error about 2^-17 per product).
+ *   H        device fp32, d_in x d_in, row-major, written in full (exactly symmetric).
+ *   accumulate  0: H = X^T X;  1: H += X^T X (chunked calibration sets).
+ *   Cross-chunk sums are reduced in fp64 and rounded once to fp32.
+ */
+fq_status fq_hessian_accumulate(void* stream, const void* X, int xt, int64_t n_tokens,
+                                int64_t d_in, int64_t ldx, float* H, int accumulate,
+                                void* ws, size_t ws_bytes);
+size_t fq_hessian_workspace_bytes(int xt, int64_t n_tokens, int64_t d_in);
+
+/*
+ * FF-space weights and Hessian (Alg. 1 step 1; Sec. 3 "What are analogous calculations
+ * in FF space?"):
+ *   D  = P_out^T W P_in      (K_out x K_in, fp32)      -- skipped when D  == NULL
+ *   Ht = P_in^T  H P_in      (K_in x K_in, fp32, exactly symmetric) -- skipped when Ht == NULL
+ *   W      device, d_out x d_in, type wt, row stride d_in.
+ *   P_out  device fp32, d_out x K_out (columns [P_1 ... P_k], weights absorbed).
+ *   P_in   device fp32, d_in  x K_in.
+ *   H      device fp32, d_in x d_in symmetric (may be NULL when Ht == NULL).
+ * The contractions run on bf16 MFMA with each fp32 operand split into a bf16 pair; the
+ * relative error of every product is about 2^-17.
+ */
+fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, int64_t d_in,
+                            const float* P_out, int64_t K_out, const float* P_in, int64_t K_in,
+                            const float* H, float* D, float* Ht, void* ws, size_t ws_bytes);
+size_t fq_frame_analysis_workspace_bytes(int wt, int64_t d_out, int64_t d_in, int64_t K_out,
+                                         int64_t K_in);
+
+/*
+ * Quantize the FF-space weights (Alg. 1 steps 2-5, with the OPTQ procedure the paper
+ * applies to D and H~, Sec. 3 "Details of the quantization procedure"):
+ *  1. mu = mean(D), sigma = std(D) (N - 1) over all of D; D <- clip(D, mu +/- clip_sigmas*sigma).
+ *  2. Per-row asymmetric grid from the clipped D: lo = min(0, row min), hi = max(0, row max)
+ *     ((lo, hi) = (-1, 1) for an all-zero row); scale = fp32((hi - lo) / (2^bits - 1));
+ *     zero = round-half-even(-lo / scale).
+ *  3. OPTQ: dead columns (H~_jj == 0) get H~_jj = 1 and D[:, j] = 0; H~ += damp *
+ *     mean(diag H~) I; columns are rounded in order with Cholesky error feedback, in
+ *     lazy blocks of `block` columns; code = clamp(rne(w / scale) + zero, 0, 2^bits - 1).
+ *     All of step 3 runs in fp64.
+ *   D       device fp32 K_out x K_in (read only).
+ *   Ht      device fp32 K_in x K_in symmetric (the lower triangle is read).
+ *   bits    2 (other widths return FQ_ERR_UNSUPPORTED).
+ *   block   >= 1.
+ *   codes   device uint32, K_out x ceil(K_in / 16): column j of row i sits in bits
+ *           2*(j mod 16) .. 2*(j mod 16)+1 of word floor(j / 16) of row i; pad bits are 0.
+ *   scale, zero  device fp32, K_out each (zero is integer valued; bias = -scale * zero).
+ * Returns FQ_ERR_NOT_POSITIVE_DEFINITE when the damped H~ is not positive definite
+ * (e.g. damp = 0 with K_in > rank H~) and FQ_ERR_NONFINITE when D or H~ holds NaN/Inf;
+ * outputs are then unspecified.
+ */
+fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int64_t K_out,
+                             int64_t K_in, int bits, int block, double damp,
+                             double clip_sigmas, uint32_t* codes, float* scale, float* zero,
+                             void* ws, size_t ws_bytes);
+size_t fq_quantize_frames_workspace_bytes(int64_t K_out, int64_t K_in, int block);
+
+/*
+ * Synthesis of the dequantized layer (Alg. 1 return value; appendix "Computational
+ * Complexity during Inference"):  W_hat = P_out * diag(scale) * (codes - zero) * P_in^T.
+ *   codes/scale/zero  as produced by fq_quantize_frames.
+ *   P_out  device fp32 d_out x K_out;  P_in device fp32 d_in x K_in.
+ *   W_hat  device fp32 d_out x d_in.
+ */
+fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* scale,
+                             const float* zero, int64_t K_out, int64_t K_in,
+                             const float* P_out, int64_t d_out, const float* P_in,
+                             int64_t d_in, float* W_hat, void* ws, size_t ws_bytes);
+size_t fq_frame_synthesis_workspace_bytes(int64_t K_out, int64_t K_in, int64_t d_out,
+                                          int64_t d_in);
+
+/* Status text and the calling thread's last error message (never NULL). */
+const char* fq_status_string(int status);
+const char* fq_last_error(void);
+
+/*
+ * Kernel timing (tracing).  While enabled, every kernel the library launches is
+ * bracketed with HIP events on the stream it runs on.  fq_profile_query synchronizes
+ * those events and returns the launch count and total milliseconds of kernels whose name
+ * starts with `prefix` (all kernels for ""), since the last reset.  Not thread-safe.
+ */
+void fq_profile_enable(int on);
+void fq_profile_reset(void);
+int fq_profile_query(const char* prefix, int* count, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FQ_H */

@@ -1,0 +1,524 @@
+// C ABI of libfq: argument validation, workspace layout and the launch sequence of each
+// call of the FrameQuant per-layer pass (see include/fq.h for the contract).
+#include "fq_internal.h"
+#include "../../include/fq.h"
+
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+#include <string>
+#include <vector>
+#include <mutex>
+
+namespace fq {
+
+// ---------------------------------------------------------------- errors
+static thread_local std::string g_last_error;
+
+static fq_status fail(fq_status st, const char* msg) {
+  g_last_error = msg;
+  return st;
+}
+
+static fq_status hip_fail(hipError_t e, const char* where) {
+  std::string m = std::string(where) + ": " + hipGetErrorString(e);
+  g_last_error = m;
+  return FQ_ERR_HIP;
+}
+
+hipError_t last_launch_error() { return hipGetLastError(); }
+
+// ---------------------------------------------------------------- kernel timer
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+static bool g_prof_on = false;
+static std::vector<ProfRec> g_prof;
+static std::vector<hipEvent_t> g_pool;
+static std::mutex g_prof_mu;
+
+static hipEvent_t take_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void prof_begin(hipStream_t s, const char* name) {
+  if (!g_prof_on) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfRec r{name, take_event(), take_event()};
+  if (r.a) hipEventRecord(r.a, s);
+  g_prof.push_back(r);
+}
+
+void prof_end(hipStream_t s) {
+  if (!g_prof_on) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof.empty() && g_prof.back().b) hipEventRecord(g_prof.back().b, s);
+}
+
+// ---------------------------------------------------------------- workspace carving
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  template <typename T>
+  T* take(size_t count) {
+    off = (off + 255) & ~(size_t)255;
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+static int64_t rup8(int64_t x) { return (x + 7) / 8 * 8; }
+static const int64_t DIM_MAX = (int64_t)1 << 30;
+
+static bool dim_ok(int64_t v) { return v >= 0 && v < DIM_MAX; }
+
+static int hessian_ksplit(int64_t n, int64_t d, int npass) {
+  const int t = (int)((d + 255) / 256);
+  const int ntiles = t * (t + 1) / 2;
+  const int64_t ktiles = (n + 63) / 64;
+  int ks = (int)((2048 + ntiles / 2) / (ntiles > 0 ? ntiles : 1));
+  if (ks < 1) ks = 1;
+  if (ks > ktiles) ks = (int)(ktiles > 0 ? ktiles : 1);
+  (void)npass;
+  return ks;
+}
+
+struct HessLayout {
+  u16* xhi; u16* xlo; float* part; int ksplit; int64_t ldp;
+};
+
+static size_t hessian_layout(int xt, int64_t n, int64_t d, void* ws, HessLayout* L) {
+  Carver c(ws);
+  HessLayout l{};
+  l.ldp = rup8(d);
+  if (xt == FQ_F32) {
+    l.xhi = c.take<u16>((size_t)n * l.ldp);
+    l.xlo = c.take<u16>((size_t)n * l.ldp);
+  }
+  l.ksplit = hessian_ksplit(n, d, xt == FQ_F32 ? 3 : 1);
+  l.part = c.take<float>(gemm_partial_bytes((int)d, l.ksplit) / sizeof(float));
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+struct AnaLayout {
+  u16 *po_hi, *po_lo, *pi_hi, *pi_lo, *w_hi, *w_lo, *t_hi, *t_lo, *h_hi, *h_lo, *g_hi, *g_lo;
+  int64_t ldko, ldki, ldi;
+};
+
+static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out, int64_t K_in,
+                              void* ws, AnaLayout* L) {
+  Carver c(ws);
+  AnaLayout l{};
+  l.ldko = rup8(K_out);
+  l.ldki = rup8(K_in);
+  l.ldi = rup8(d_in);
+  l.po_hi = c.take<u16>((size_t)d_out * l.ldko);
+  l.po_lo = c.take<u16>((size_t)d_out * l.ldko);
+  l.pi_hi = c.take<u16>((size_t)d_in * l.ldki);
+  l.pi_lo = c.take<u16>((size_t)d_in * l.ldki);
+  if (wt != FQ_BF16) {
+    l.w_hi = c.take<u16>((size_t)d_out * l.ldi);
+    l.w_lo = c.take<u16>((size_t)d_out * l.ldi);
+  }
+  l.t_hi = c.take<u16>((size_t)K_out * l.ldi);
+  l.t_lo = c.take<u16>((size_t)K_out * l.ldi);
+  l.h_hi = c.take<u16>((size_t)d_in * l.ldi);
+  l.h_lo = c.take<u16>((size_t)d_in * l.ldi);
+  l.g_hi = c.take<u16>((size_t)d_in * l.ldki);
+  l.g_lo = c.take<u16>((size_t)d_in * l.ldki);
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+static int64_t res_width(int64_t K_in, int block) {
+  int64_t w = block < K_in ? block : K_in;
+  return w > 0 ? w : 1;
+}
+
+static size_t quant_layout(int64_t K_out, int64_t K_in, int block, void* ws, QuantScratch* Q) {
+  Carver c(ws);
+  QuantScratch q{};
+  q.Y = c.take<double>((size_t)K_out * K_in);
+  q.A = c.take<double>((size_t)K_in * K_in);
+  q.R = c.take<double>((size_t)K_in * K_in);
+  q.res = c.take<double>((size_t)K_out * res_width(K_in, block));
+  q.codes8 = c.take<uint8_t>((size_t)K_out * K_in);
+  q.red = c.take<double>(1024);
+  q.scal = c.take<double>(8);
+  q.scale64 = c.take<double>((size_t)K_out);
+  q.zero64 = c.take<double>((size_t)K_out);
+  q.inv_rdiag = c.take<double>((size_t)2 * K_in);
+  q.dead = c.take<uint8_t>((size_t)K_in);
+  q.flags = c.take<int>(4);
+  if (Q) *Q = q;
+  return c.off + 256;
+}
+
+struct SynLayout {
+  u16 *q, *pl_hi, *pl_lo, *pi_hi, *pi_lo, *n_hi, *n_lo;
+  int64_t ldko, ldki;
+};
+
+static size_t synthesis_layout(int64_t K_out, int64_t K_in, int64_t d_out, int64_t d_in,
+                               void* ws, SynLayout* L) {
+  Carver c(ws);
+  SynLayout l{};
+  l.ldko = rup8(K_out);
+  l.ldki = rup8(K_in);
+  l.q = c.take<u16>((size_t)K_out * l.ldki);
+  l.pl_hi = c.take<u16>((size_t)d_out * l.ldko);
+  l.pl_lo = c.take<u16>((size_t)d_out * l.ldko);
+  l.pi_hi = c.take<u16>((size_t)d_in * l.ldki);
+  l.pi_lo = c.take<u16>((size_t)d_in * l.ldki);
+  l.n_hi = c.take<u16>((size_t)d_out * l.ldki);
+  l.n_lo = c.take<u16>((size_t)d_out * l.ldki);
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+__global__ void k_zero_i32(int* p, int n) {
+  if ((int)threadIdx.x < n) p[threadIdx.x] = 0;
+}
+
+}  // namespace fq
+
+using namespace fq;
+
+extern "C" {
+
+const char* fq_status_string(int st) {
+  switch (st) {
+    case FQ_OK: return "FQ_OK";
+    case FQ_ERR_INVALID_ARG: return "FQ_ERR_INVALID_ARG";
+    case FQ_ERR_UNSUPPORTED: return "FQ_ERR_UNSUPPORTED";
+    case FQ_ERR_NOT_POSITIVE_DEFINITE: return "FQ_ERR_NOT_POSITIVE_DEFINITE";
+    case FQ_ERR_NONFINITE: return "FQ_ERR_NONFINITE";
+    case FQ_ERR_WORKSPACE_TOO_SMALL: return "FQ_ERR_WORKSPACE_TOO_SMALL";
+    case FQ_ERR_HIP: return "FQ_ERR_HIP";
+  }
+  return "FQ_UNKNOWN_STATUS";
+}
+
+const char* fq_last_error(void) { return g_last_error.c_str(); }
+
+void fq_profile_enable(int on) { g_prof_on = on != 0; }
+
+void fq_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& r : g_prof) {
+    if (r.a) { hipEventSynchronize(r.a); g_pool.push_back(r.a); }
+    if (r.b) { hipEventSynchronize(r.b); g_pool.push_back(r.b); }
+  }
+  g_prof.clear();
+}
+
+int fq_profile_query(const char* prefix, int* count, double* total_ms) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  const size_t pl = prefix ? strlen(prefix) : 0;
+  int n = 0;
+  double t = 0.0;
+  for (auto& r : g_prof) {
+    if (pl && strncmp(r.name, prefix, pl) != 0) continue;
+    if (!r.a || !r.b) continue;
+    if (hipEventSynchronize(r.b) != hipSuccess) return -1;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return -1;
+    ++n;
+    t += ms;
+  }
+  if (count) *count = n;
+  if (total_ms) *total_ms = t;
+  return 0;
+}
+
+// ================================================================ S1: Hessian
+size_t fq_hessian_workspace_bytes(int xt, int64_t n_tokens, int64_t d_in) {
+  if (!dim_ok(n_tokens) || !dim_ok(d_in) || xt < 0 || xt > 2) return 0;
+  return hessian_layout(xt, n_tokens, d_in, nullptr, nullptr);
+}
+
+fq_status fq_hessian_accumulate(void* stream, const void* X, int xt, int64_t n_tokens,
+                                int64_t d_in, int64_t ldx, float* H, int accumulate, void* ws,
+                                size_t ws_bytes) {
+  if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (!dim_ok(n_tokens) || !dim_ok(d_in)) return fail(FQ_ERR_INVALID_ARG, "n_tokens and d_in must be in [0, 2^30)");
+  if (ldx < d_in) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d_in");
+  if (d_in == 0) return FQ_OK;
+  if (!H) return fail(FQ_ERR_INVALID_ARG, "H is NULL");
+  if (n_tokens > 0 && !X) return fail(FQ_ERR_INVALID_ARG, "X is NULL");
+  const size_t need = hessian_layout(xt, n_tokens, d_in, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_hessian_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  // align the carve base to 256 bytes inside the provided workspace
+  char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+  HessLayout L;
+  hessian_layout(xt, n_tokens, d_in, base, &L);
+  hipError_t e;
+  GemmDesc g;
+  g.M = (int)d_in; g.N = (int)d_in; g.K = (int)n_tokens;
+  g.a_kmajor = false; g.b_kmajor = false;
+  g.epi = EPI_PARTIAL;
+  g.ksplit = L.ksplit;
+  if (xt == FQ_F32) {
+    e = split_bf16(X, 0, ldx, (int)n_tokens, (int)d_in, nullptr, L.xhi, L.xlo, L.ldp, s);
+    if (e != hipSuccess) return hip_fail(e, "split X");
+    g.a[0] = L.xhi; g.a[1] = L.xlo; g.b[0] = L.xhi; g.b[1] = L.xlo;
+    g.lda = g.ldb = L.ldp;
+    g.npass = 3;
+    g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
+  } else {
+    g.a[0] = (const u16*)X; g.b[0] = (const u16*)X;
+    g.lda = g.ldb = ldx;
+    g.npass = 1;
+    g.f16 = (xt == FQ_F16);
+  }
+  e = gemm_run(g, L.part, s);
+  if (e != hipSuccess) return hip_fail(e, "hessian gemm");
+  e = syrk_reduce(L.part, (int)d_in, L.ksplit, H, d_in, accumulate, s);
+  if (e != hipSuccess) return hip_fail(e, "hessian reduce");
+  return FQ_OK;
+}
+
+// ================================================================ S2: analysis
+size_t fq_frame_analysis_workspace_bytes(int wt, int64_t d_out, int64_t d_in, int64_t K_out,
+                                         int64_t K_in) {
+  if (wt < 0 || wt > 2 || !dim_ok(d_out) || !dim_ok(d_in) || !dim_ok(K_out) || !dim_ok(K_in)) return 0;
+  return analysis_layout(wt, d_out, d_in, K_out, K_in, nullptr, nullptr);
+}
+
+fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, int64_t d_in,
+                            const float* P_out, int64_t K_out, const float* P_in, int64_t K_in,
+                            const float* H, float* D, float* Ht, void* ws, size_t ws_bytes) {
+  if (wt < FQ_F32 || wt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "wt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (!dim_ok(d_out) || !dim_ok(d_in) || !dim_ok(K_out) || !dim_ok(K_in))
+    return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
+  if (K_out < d_out || K_in < d_in)
+    return fail(FQ_ERR_INVALID_ARG, "a frame needs K >= d (K_out >= d_out, K_in >= d_in)");
+  if (D && (!W || !P_out || !P_in) && d_out > 0 && d_in > 0)
+    return fail(FQ_ERR_INVALID_ARG, "W, P_out and P_in are required for D");
+  if (Ht && (!H || !P_in) && d_in > 0) return fail(FQ_ERR_INVALID_ARG, "H and P_in are required for Ht");
+  const size_t need = analysis_layout(wt, d_out, d_in, K_out, K_in, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_analysis_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+  AnaLayout L;
+  analysis_layout(wt, d_out, d_in, K_out, K_in, base, &L);
+  hipError_t e;
+  if (d_in > 0 && K_in > 0) {
+    e = split_bf16(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ldki, s);
+    if (e != hipSuccess) return hip_fail(e, "split P_in");
+  }
+  if (D && K_out > 0 && K_in > 0) {
+    if (d_out == 0 || d_in == 0) {
+      e = fill_zero_f32(D, (int)K_out, (int)K_in, K_in, s);
+      if (e != hipSuccess) return hip_fail(e, "zero D");
+    } else {
+      e = split_bf16(P_out, 0, K_out, (int)d_out, (int)K_out, nullptr, L.po_hi, L.po_lo, L.ldko, s);
+      if (e != hipSuccess) return hip_fail(e, "split P_out");
+      const u16* w0;
+      const u16* w1 = nullptr;
+      int64_t ldw;
+      if (wt == FQ_BF16) {
+        w0 = (const u16*)W;
+        ldw = d_in;
+      } else {
+        e = split_bf16(W, wt == FQ_F16 ? 1 : 0, d_in, (int)d_out, (int)d_in, nullptr, L.w_hi,
+                       L.w_lo, L.ldi, s);
+        if (e != hipSuccess) return hip_fail(e, "split W");
+        w0 = L.w_hi;
+        w1 = L.w_lo;
+        ldw = L.ldi;
+      }
+      // T = P_out^T W  (K_out x d_in), emitted as a bf16 pair
+      GemmDesc g;
+      g.M = (int)K_out; g.N = (int)d_in; g.K = (int)d_out;
+      g.a[0] = L.po_hi; g.a[1] = L.po_lo; g.lda = L.ldko; g.a_kmajor = false;
+      g.b[0] = w0; g.b[1] = w1; g.ldb = ldw; g.b_kmajor = false;
+      if (w1) {
+        g.npass = 3;
+        g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
+      } else {
+        g.npass = 2;
+        g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
+      }
+      g.epi = EPI_SPLIT; g.c_hi = L.t_hi; g.c_lo = L.t_lo; g.ldc = L.ldi;
+      e = gemm_run(g, nullptr, s);
+      if (e != hipSuccess) return hip_fail(e, "analysis gemm 1");
+      // D = T P_in  (K_out x K_in)
+      GemmDesc g2;
+      g2.M = (int)K_out; g2.N = (int)K_in; g2.K = (int)d_in;
+      g2.a[0] = L.t_hi; g2.a[1] = L.t_lo; g2.lda = L.ldi; g2.a_kmajor = true;
+      g2.b[0] = L.pi_hi; g2.b[1] = L.pi_lo; g2.ldb = L.ldki; g2.b_kmajor = false;
+      g2.npass = 3;
+      g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
+      g2.epi = EPI_F32; g2.c = D; g2.ldc = K_in;
+      e = gemm_run(g2, nullptr, s);
+      if (e != hipSuccess) return hip_fail(e, "analysis gemm 2");
+    }
+  }
+  if (Ht && K_in > 0) {
+    if (d_in == 0) {
+      e = fill_zero_f32(Ht, (int)K_in, (int)K_in, K_in, s);
+      if (e != hipSuccess) return hip_fail(e, "zero Ht");
+    } else {
+      e = split_bf16(H, 0, d_in, (int)d_in, (int)d_in, nullptr, L.h_hi, L.h_lo, L.ldi, s);
+      if (e != hipSuccess) return hip_fail(e, "split H");
+      // G = H P_in  (d_in x K_in)
+      GemmDesc g;
+      g.M = (int)d_in; g.N = (int)K_in; g.K = (int)d_in;
+      g.a[0] = L.h_hi; g.a[1] = L.h_lo; g.lda = L.ldi; g.a_kmajor = true;
+      g.b[0] = L.pi_hi; g.b[1] = L.pi_lo; g.ldb = L.ldki; g.b_kmajor = false;
+      g.npass = 3;
+      g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
+      g.epi = EPI_SPLIT; g.c_hi = L.g_hi; g.c_lo = L.g_lo; g.ldc = L.ldki;
+      e = gemm_run(g, nullptr, s);
+      if (e != hipSuccess) return hip_fail(e, "analysis gemm 3");
+      // Ht = P_in^T G  (K_in x K_in, upper tiles mirrored)
+      GemmDesc g2;
+      g2.M = (int)K_in; g2.N = (int)K_in; g2.K = (int)d_in;
+      g2.a[0] = L.pi_hi; g2.a[1] = L.pi_lo; g2.lda = L.ldki; g2.a_kmajor = false;
+      g2.b[0] = L.g_hi; g2.b[1] = L.g_lo; g2.ldb = L.ldki; g2.b_kmajor = false;
+      g2.npass = 3;
+      g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
+      g2.epi = EPI_SYM; g2.c = Ht; g2.ldc = K_in;
+      e = gemm_run(g2, nullptr, s);
+      if (e != hipSuccess) return hip_fail(e, "analysis gemm 4");
+    }
+  }
+  return FQ_OK;
+}
+
+// ================================================================ S3: quantize
+size_t fq_quantize_frames_workspace_bytes(int64_t K_out, int64_t K_in, int block) {
+  if (!dim_ok(K_out) || !dim_ok(K_in) || block < 1) return 0;
+  return quant_layout(K_out, K_in, block, nullptr, nullptr);
+}
+
+fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int64_t K_out,
+                             int64_t K_in, int bits, int block, double damp, double clip_sigmas,
+                             uint32_t* codes, float* scale, float* zero, void* ws,
+                             size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (bits != 2) return fail(FQ_ERR_UNSUPPORTED, "only bits = 2 is implemented");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (!(damp >= 0.0) || !isfinite(damp)) return fail(FQ_ERR_INVALID_ARG, "damp must be finite and >= 0");
+  if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!D || !Ht || !codes || !scale || !zero) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  const size_t need = quant_layout(K_out, K_in, block, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_quantize_frames_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+  QuantScratch Q;
+  quant_layout(K_out, K_in, block, base, &Q);
+  hipError_t e;
+  prof_begin(s, "q_init");
+  hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, Q.flags, 4);
+  prof_end(s);
+  if ((e = q_stats(D, K_out, K_in, clip_sigmas, Q, s)) != hipSuccess) return hip_fail(e, "stats");
+  if ((e = q_hdiag_build(Ht, K_in, damp, Q, s)) != hipSuccess) return hip_fail(e, "hessian prep");
+  if ((e = q_cholesky(Q.A, K_in, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
+  if ((e = q_reverse_upper(Q.A, K_in, Q.R, Q.inv_rdiag, s)) != hipSuccess) return hip_fail(e, "reverse");
+  if ((e = q_clip_grid(D, K_out, K_in, bits, Q, scale, zero, s)) != hipSuccess) return hip_fail(e, "clip/grid");
+  const int64_t ldr = res_width(K_in, block);
+  for (int64_t o1 = 0; o1 < K_in; o1 += block) {
+    const int64_t o2 = (o1 + block < K_in) ? o1 + block : K_in;
+    for (int64_t i1 = o1; i1 < o2; i1 += 128) {
+      const int64_t i2 = (i1 + 128 < o2) ? i1 + 128 : o2;
+      if ((e = q_gptq_block(D, K_out, K_in, (int)i1, (int)i2, (int)o1, ldr, bits, Q, s)) != hipSuccess)
+        return hip_fail(e, "rounding block");
+      if (i2 < o2) {
+        e = dgemm(K_out, o2 - i2, i2 - i1, 1.0, Q.res + (i1 - o1), ldr, Q.R + i1 * K_in + i2, K_in,
+                  false, Q.Y + i2, K_in, false, s);
+        if (e != hipSuccess) return hip_fail(e, "in-block update");
+      }
+    }
+    if (o2 < K_in) {
+      e = dgemm(K_out, K_in - o2, o2 - o1, 1.0, Q.res, ldr, Q.R + o1 * K_in + o2, K_in, false,
+                Q.Y + o2, K_in, false, s);
+      if (e != hipSuccess) return hip_fail(e, "lazy update");
+    }
+  }
+  if ((e = q_pack2(Q.codes8, K_out, K_in, codes, s)) != hipSuccess) return hip_fail(e, "pack");
+  int flags[4] = {0, 0, 0, 0};
+  if ((e = hipMemcpyAsync(flags, Q.flags, sizeof(flags), hipMemcpyDeviceToHost, s)) != hipSuccess)
+    return hip_fail(e, "flag copy");
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(e, "stream sync");
+  if (flags[1]) return fail(FQ_ERR_NONFINITE, "D or Ht holds NaN or Inf");
+  if (flags[0]) return fail(FQ_ERR_NOT_POSITIVE_DEFINITE, "damped Ht is not positive definite");
+  return FQ_OK;
+}
+
+// ================================================================ S4: synthesis
+size_t fq_frame_synthesis_workspace_bytes(int64_t K_out, int64_t K_in, int64_t d_out,
+                                          int64_t d_in) {
+  if (!dim_ok(K_out) || !dim_ok(K_in) || !dim_ok(d_out) || !dim_ok(d_in)) return 0;
+  return synthesis_layout(K_out, K_in, d_out, d_in, nullptr, nullptr);
+}
+
+fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* scale,
+                             const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
+                             int64_t d_out, const float* P_in, int64_t d_in, float* W_hat,
+                             void* ws, size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in) || !dim_ok(d_out) || !dim_ok(d_in))
+    return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
+  if (K_out < d_out || K_in < d_in)
+    return fail(FQ_ERR_INVALID_ARG, "a frame needs K >= d (K_out >= d_out, K_in >= d_in)");
+  if (d_out == 0 || d_in == 0) return FQ_OK;
+  if (!W_hat || !P_out || !P_in) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  if (K_out > 0 && K_in > 0 && (!codes || !scale || !zero)) return fail(FQ_ERR_INVALID_ARG, "NULL codes/scale/zero");
+  const size_t need = synthesis_layout(K_out, K_in, d_out, d_in, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_synthesis_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+  if (K_out == 0 || K_in == 0) {
+    e = fill_zero_f32(W_hat, (int)d_out, (int)d_in, d_in, s);
+    return e == hipSuccess ? FQ_OK : hip_fail(e, "zero W_hat");
+  }
+  char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+  SynLayout L;
+  synthesis_layout(K_out, K_in, d_out, d_in, base, &L);
+  if ((e = dequant_bf16(codes, zero, K_out, K_in, L.q, L.ldki, s)) != hipSuccess) return hip_fail(e, "dequant");
+  if ((e = split_bf16(P_out, 0, K_out, (int)d_out, (int)K_out, scale, L.pl_hi, L.pl_lo, L.ldko, s)) != hipSuccess)
+    return hip_fail(e, "split P_out");
+  if ((e = split_bf16(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ldki, s)) != hipSuccess)
+    return hip_fail(e, "split P_in");
+  // N = (P_out diag(scale)) (codes - zero)   (d_out x K_in), bf16 pair
+  GemmDesc g;
+  g.M = (int)d_out; g.N = (int)K_in; g.K = (int)K_out;
+  g.a[0] = L.pl_hi; g.a[1] = L.pl_lo; g.lda = L.ldko; g.a_kmajor = true;
+  g.b[0] = L.q; g.ldb = L.ldki; g.b_kmajor = false;
+  g.npass = 2;
+  g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
+  g.epi = EPI_SPLIT; g.c_hi = L.n_hi; g.c_lo = L.n_lo; g.ldc = L.ldki;
+  if ((e = gemm_run(g, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 1");
+  // W_hat = N P_in^T  (d_out x d_in)
+  GemmDesc g2;
+  g2.M = (int)d_out; g2.N = (int)d_in; g2.K = (int)K_in;
+  g2.a[0] = L.n_hi; g2.a[1] = L.n_lo; g2.lda = L.ldki; g2.a_kmajor = true;
+  g2.b[0] = L.pi_hi; g2.b[1] = L.pi_lo; g2.ldb = L.ldki; g2.b_kmajor = true;
+  g2.npass = 3;
+  g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
+  g2.epi = EPI_F32; g2.c = W_hat; g2.ldc = d_in;
+  if ((e = gemm_run(g2, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 2");
+  return FQ_OK;
+}
+
+}  // extern "C"

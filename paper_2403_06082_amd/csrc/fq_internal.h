@@ -1,0 +1,100 @@
+// Internal declarations shared by the libfq translation units (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace fq {
+
+typedef uint16_t u16;
+
+// ---------------------------------------------------------------- launch bookkeeping
+// Every launch goes through prof_begin/prof_end so that the optional kernel timer can
+// bracket it with events on the launch stream.
+void prof_begin(hipStream_t s, const char* name);
+void prof_end(hipStream_t s);
+hipError_t last_launch_error();
+
+// ---------------------------------------------------------------- bf16 MFMA GEMM engine
+// C = sum over passes p of A[pa[p]] * B[pb[p]], fp32 accumulation, where A is M x K and
+// B is K x N, both given as 16-bit planes (bf16, or f16 for the Hessian of f16 inputs).
+//   a_kmajor: A(m, k) at a[m * lda + k]   else at a[k * lda + m]
+//   b_kmajor: B(k, n) at b[n * ldb + k]   else at b[k * ldb + n]
+enum Epilogue {
+  EPI_F32 = 0,      // c[row * ldc + col] = acc
+  EPI_SPLIT = 1,    // c_hi/c_lo[row * ldc + col] = bf16 pair of acc
+  EPI_SYM = 2,      // upper tiles only; c[row][col] and c[col][row] for row <= col
+  EPI_PARTIAL = 3   // upper tiles only, split over K; fp32 partial tiles, tile-major
+};
+
+struct GemmDesc {
+  int M = 0, N = 0, K = 0;
+  const u16* a[2] = {nullptr, nullptr};
+  const u16* b[2] = {nullptr, nullptr};
+  int64_t lda = 0, ldb = 0;
+  int npass = 1;
+  int pa[3] = {0, 0, 0}, pb[3] = {0, 0, 0};
+  bool a_kmajor = true, b_kmajor = true;
+  bool f16 = false;              // operands are IEEE half instead of bf16
+  int epi = EPI_F32;
+  float* c = nullptr;
+  int64_t ldc = 0;
+  u16* c_hi = nullptr;
+  u16* c_lo = nullptr;
+  int ksplit = 1;                // EPI_PARTIAL only
+};
+
+// Workspace bytes needed by EPI_PARTIAL for an N x N symmetric product split ksplit ways.
+size_t gemm_partial_bytes(int N, int ksplit);
+int gemm_sym_tiles(int N);
+hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s);
+// H (+)= sum of the ksplit partial tiles (fp64), mirrored to full symmetric storage.
+hipError_t syrk_reduce(const float* partial, int N, int ksplit, float* H, int64_t ldh,
+                       int accumulate, hipStream_t s);
+
+// fp32 / f16 -> bf16 (hi, lo) planes with out[r * ld_out + c]; optional column scale
+// (applied in fp32 before the split).  Element type: 0 = f32, 1 = f16.
+hipError_t split_bf16(const void* in, int in_type, int64_t ld_in, int rows, int cols,
+                      const float* col_scale, u16* hi, u16* lo, int64_t ld_out, hipStream_t s);
+hipError_t fill_zero_f32(float* p, int rows, int cols, int64_t ld, hipStream_t s);
+
+// ---------------------------------------------------------------- fp64 path
+struct QuantScratch {
+  double* Y;          // K_out x K_in working matrix (scaled pre-rounding values)
+  double* A;          // K_in x K_in: reversed damped H~, factored in place (lower)
+  double* R;          // K_in x K_in: upper factor, H~_damped = R R^T
+  double* res;        // K_out x block residuals D - D^ of the current block
+  uint8_t* codes8;    // K_out x K_in codes
+  double* red;        // reduction partials
+  double* scal;       // device scalars: [0] mu [1] sigma [2] lo [3] hi [4] lambda
+  double* scale64;    // K_out
+  double* zero64;     // K_out
+  double* inv_rdiag;  // K_in
+  uint8_t* dead;      // K_in
+  int* flags;         // [0] not PD, [1] non-finite
+};
+
+hipError_t q_stats(const float* D, int64_t rows, int64_t cols, double clip_sigmas,
+                   QuantScratch& w, hipStream_t s);
+hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& w,
+                         hipStream_t s);
+hipError_t q_cholesky(double* A, int64_t K, int* flags, hipStream_t s);
+hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rdiag,
+                           hipStream_t s);
+hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, QuantScratch& w,
+                       float* scale, float* zero, hipStream_t s);
+hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int i2, int o1,
+                        int64_t ld_res, int bits, QuantScratch& w, hipStream_t s);
+// C[M x N] += alpha * A[M x K] * op(B)   (fp64 MFMA)
+//   b_trans: op(B)(k, n) = B[n * ldb + k]  else B[k * ldb + n]
+//   lower_only: only tiles with tile_row >= tile_col (for the Cholesky update)
+hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, const double* A, int64_t lda,
+                 const double* B, int64_t ldb, bool b_trans, double* C, int64_t ldc,
+                 bool lower_only, hipStream_t s);
+hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* out,
+                   hipStream_t s);
+hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
+                        u16* out, int64_t ld_out, hipStream_t s);
+
+}  // namespace fq

@@ -1,0 +1,543 @@
+// bf16 / f16 MFMA GEMM engine for gfx950 (CDNA4) and the small elementwise kernels that
+// feed it.  Used for the calibration Hessian (H = X^T X, upper tiles, split over tokens),
+// the frame analysis (D = P_l^T W P_prev, H~ = P_prev^T H P_prev) and the synthesis
+// (W^ = P_l D^ P_prev^T).
+//
+// Design
+//  * Work-group tile 256 x 256, K step 64, 256 threads = 4 wave64s in a 2 x 2 grid; each
+//    wave owns a 128 x 128 sub-tile as 4 x 4 v_mfma_f32_32x32x16 (bf16 or f16) blocks.
+//  * Both operands are staged through LDS as [row][k] with the 16-byte k-chunks of each
+//    row XOR-swizzled (chunk c of row r lives at slot c ^ ((r>>1 ^ r>>3) & 7)), which
+//    keeps the MFMA fragment reads conflict-free without padding.  Two stages (128 KiB)
+//    double-buffer the global loads: the next stage is fetched into registers while the
+//    current one feeds the MFMAs, with one barrier per stage.
+//  * An operand stored with M (or N) contiguous is transposed on the way into LDS: each
+//    thread loads an 8 x 8 block (eight 16-byte rows) and transposes it in registers
+//    with byte permutes, so every global load stays a coalesced 16-byte access.
+//  * fp32 operands enter as bf16 (hi, lo) pairs; a "pass" is one (A plane, B plane)
+//    product and all passes accumulate into the same fp32 registers.
+//  * Work-group ids are remapped so that consecutive tiles land on the same XCD (ids are
+//    dealt round-robin over the 8 XCDs), and tiles are walked in groups of 8 tile-rows
+//    for L2 reuse.
+#include "fq_internal.h"
+
+namespace fq {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 64, NT = 256;
+constexpr int TILE_ELEMS = BM * BK;          // u16 elements per operand per stage
+
+struct KParams {
+  int M, N, K;
+  const u16* a0; const u16* a1;
+  const u16* b0; const u16* b1;
+  int64_t lda, ldb;
+  int npass;
+  int pa0, pa1, pa2, pb0, pb1, pb2;
+  float* c; int64_t ldc;
+  u16* c_hi; u16* c_lo;
+  int aligned_a, aligned_b;
+  int tiles_m, tiles_n, ntiles;
+  int ksplit, k_per_split;
+  float* part;
+};
+
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
+
+__device__ __forceinline__ uint32_t bf16_rne_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// ------------------------------------------------------------------ operand staging
+// K-major operand: element (mn, k) at base[mn * ld + k].  Thread t stages chunks
+// c = t + 256 i (i < 8): row c >> 3, 16-byte k-chunk c & 7.
+__device__ __forceinline__ void load_kmajor(const u16* __restrict__ base, int64_t ld, int mn0,
+                                            int k0, int MN, int K, bool aligned, uint4 (&r)[8],
+                                            int tid) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = tid + NT * i;
+    const int row = c >> 3;
+    const int kc = c & 7;
+    const int m = mn0 + row;
+    const int k = k0 + kc * 8;
+    if (m < MN && k + 8 <= K && aligned) {
+      r[i] = *reinterpret_cast<const uint4*>(base + (int64_t)m * ld + k);
+    } else {
+      uint32_t w[4] = {0, 0, 0, 0};
+      if (m < MN) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (k + e < K) {
+            uint32_t v = base[(int64_t)m * ld + k + e];
+            w[e >> 1] |= v << ((e & 1) * 16);
+          }
+        }
+      }
+      r[i] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
+__device__ __forceinline__ void store_kmajor(u16* sm, const uint4 (&r)[8], int tid) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int c = tid + NT * i;
+    const int row = c >> 3;
+    const int kc = c & 7;
+    *reinterpret_cast<uint4*>(sm + row * BK + ((kc ^ swz(row)) << 3)) = r[i];
+  }
+}
+
+// MN-major operand: element (mn, k) at base[k * ld + mn].  Thread t loads the 8 x 8 block
+// k in [k0 + 8 kb, +8), mn in [mn0 + 8 mb, +8) with kb = t >> 5, mb = t & 31.
+__device__ __forceinline__ void load_mnmajor(const u16* __restrict__ base, int64_t ld, int mn0,
+                                             int k0, int MN, int K, bool aligned, uint4 (&r)[8],
+                                             int tid) {
+  const int kb = tid >> 5;
+  const int mb = tid & 31;
+  const int m = mn0 + mb * 8;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int k = k0 + kb * 8 + i;
+    if (k < K && m + 8 <= MN && aligned) {
+      r[i] = *reinterpret_cast<const uint4*>(base + (int64_t)k * ld + m);
+    } else {
+      uint32_t w[4] = {0, 0, 0, 0};
+      if (k < K) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (m + e < MN) {
+            uint32_t v = base[(int64_t)k * ld + m + e];
+            w[e >> 1] |= v << ((e & 1) * 16);
+          }
+        }
+      }
+      r[i] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t dw(const uint4& v, int i) {
+  return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
+}
+
+// Transpose the 8 x 8 block of 16-bit values and store row mb*8 + j, chunk kb.
+__device__ __forceinline__ void store_mnmajor(u16* sm, const uint4 (&r)[8], int tid) {
+  const int kb = tid >> 5;
+  const int mb = tid & 31;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    uint32_t o[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint32_t lo = dw(r[2 * kk], j >> 1);
+      const uint32_t hi = dw(r[2 * kk + 1], j >> 1);
+      // low half of the output dword from row 2kk, high half from row 2kk+1
+      o[kk] = (j & 1) ? __builtin_amdgcn_perm(hi, lo, 0x07060302u)
+                      : __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+    }
+    const int row = mb * 8 + j;
+    *reinterpret_cast<uint4*>(sm + row * BK + ((kb ^ swz(row)) << 3)) =
+        make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+template <bool AK, bool BKM>
+__device__ __forceinline__ void load_stage(const KParams& p, int s, int nkt, int kbeg, int m0,
+                                           int n0, uint4 (&ra)[8], uint4 (&rb)[8], int tid) {
+  const int pass = s / nkt;
+  const int kt = s - pass * nkt;
+  const int pa = pass == 0 ? p.pa0 : (pass == 1 ? p.pa1 : p.pa2);
+  const int pb = pass == 0 ? p.pb0 : (pass == 1 ? p.pb1 : p.pb2);
+  const u16* A = pa ? p.a1 : p.a0;
+  const u16* B = pb ? p.b1 : p.b0;
+  const int k0 = kbeg + kt * BK;
+  if (AK) load_kmajor(A, p.lda, m0, k0, p.M, p.K, p.aligned_a, ra, tid);
+  else load_mnmajor(A, p.lda, m0, k0, p.M, p.K, p.aligned_a, ra, tid);
+  if (BKM) load_kmajor(B, p.ldb, n0, k0, p.N, p.K, p.aligned_b, rb, tid);
+  else load_mnmajor(B, p.ldb, n0, k0, p.N, p.K, p.aligned_b, rb, tid);
+}
+
+template <bool AK, bool BKM>
+__device__ __forceinline__ void store_stage(u16* sA, u16* sB, const uint4 (&ra)[8],
+                                            const uint4 (&rb)[8], int tid) {
+  if (AK) store_kmajor(sA, ra, tid); else store_mnmajor(sA, ra, tid);
+  if (BKM) store_kmajor(sB, rb, tid); else store_mnmajor(sB, rb, tid);
+}
+
+__device__ __forceinline__ uint4 frag(const u16* sm, int row, int chunk) {
+  return *reinterpret_cast<const uint4*>(sm + row * BK + ((chunk ^ swz(row)) << 3));
+}
+
+template <bool F16>
+__device__ __forceinline__ floatx16 mfma(uint4 a, uint4 b, floatx16 c) {
+  if constexpr (F16) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
+                                                 __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+  }
+}
+
+// Work-group id -> (split, tm, tn).
+__device__ __forceinline__ void tile_coords(const KParams& p, bool sym, int& split, int& tm,
+                                            int& tn) {
+  const int nb = gridDim.x;
+  const int b = blockIdx.x;
+  // consecutive remapped ids share an XCD (ids are dealt round-robin to 8 XCDs)
+  const int per = nb / 8, rem = nb % 8;
+  const int xcd = b % 8, idx = b / 8;
+  const int bb = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+  split = bb / p.ntiles;
+  int t = bb - split * p.ntiles;
+  if (sym) {
+    int row = 0, cnt = p.tiles_n;
+    while (t >= cnt) { t -= cnt; ++row; --cnt; }
+    tm = row;
+    tn = row + t;
+  } else {
+    const int G = 8;
+    const int per_group = G * p.tiles_n;
+    const int g = t / per_group;
+    const int first = g * G;
+    const int gs = min(G, p.tiles_m - first);
+    const int in = t - g * per_group;
+    tm = first + in % gs;
+    tn = in / gs;
+  }
+}
+
+template <bool AK, bool BKM, bool F16, int EPI>
+__global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
+  __shared__ __attribute__((aligned(16))) u16 smem[2 * 2 * TILE_ELEMS];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  constexpr bool SYM = (EPI == EPI_SYM || EPI == EPI_PARTIAL);
+
+  int split, tm, tn;
+  tile_coords(p, SYM, split, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  int kbeg = 0, kend = p.K;
+  if (EPI == EPI_PARTIAL) {
+    kbeg = split * p.k_per_split;
+    kend = min(p.K, kbeg + p.k_per_split);
+  }
+  const int nkt = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  const int nstage = nkt * p.npass;
+
+  floatx16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  uint4 ra[8], rb[8];
+  if (nstage > 0) {
+    load_stage<AK, BKM>(p, 0, nkt, kbeg, m0, n0, ra, rb, tid);
+    store_stage<AK, BKM>(smem, smem + TILE_ELEMS, ra, rb, tid);
+  }
+  __syncthreads();
+
+  for (int s = 0; s < nstage; ++s) {
+    const int buf = s & 1;
+    const u16* sA = smem + buf * 2 * TILE_ELEMS;
+    const u16* sB = sA + TILE_ELEMS;
+    const bool more = (s + 1) < nstage;
+    if (more) load_stage<AK, BKM>(p, s + 1, nkt, kbeg, m0, n0, ra, rb, tid);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int chunk = kk * 2 + (lane >> 5);
+      uint4 af[4], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = frag(sA, wm * 128 + i * 32 + (lane & 31), chunk);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bfr[j] = frag(sB, wn * 128 + j * 32 + (lane & 31), chunk);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma<F16>(af[i], bfr[j], acc[i][j]);
+    }
+    if (more) {
+      u16* nA = smem + (buf ^ 1) * 2 * TILE_ELEMS;
+      store_stage<AK, BKM>(nA, nA + TILE_ELEMS, ra, rb, tid);
+    }
+    __syncthreads();
+  }
+
+  // ---------------------------------------------------------------- epilogue
+  // 32x32 accumulator layout: value v of lane l is row 8*(v/4) + 4*(l/32) + v%4,
+  // column l%32 of its 32 x 32 block.
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int rl = wm * 128 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+        const int cl = wn * 128 + j * 32 + (lane & 31);
+        const int row = m0 + rl, col = n0 + cl;
+        const float x = acc[i][j][v];
+        if (EPI == EPI_PARTIAL) {
+          float* dst = p.part + (int64_t)split * p.ntiles * (BM * BN);
+          // tile-major: tile index of (tm, tn) in the upper triangle
+          const int tidx = tm * p.tiles_n - (tm * (tm - 1)) / 2 + (tn - tm);
+          dst[(int64_t)tidx * (BM * BN) + rl * BN + cl] = x;
+        } else if (row < p.M && col < p.N) {
+          if (EPI == EPI_F32) {
+            p.c[(int64_t)row * p.ldc + col] = x;
+          } else if (EPI == EPI_SPLIT) {
+            const uint32_t h = bf16_rne_bits(x);
+            const float hf = __uint_as_float(h << 16);
+            const uint32_t l = bf16_rne_bits(x - hf);
+            p.c_hi[(int64_t)row * p.ldc + col] = (u16)h;
+            p.c_lo[(int64_t)row * p.ldc + col] = (u16)l;
+          } else {  // EPI_SYM
+            if (row <= col) {
+              p.c[(int64_t)row * p.ldc + col] = x;
+              p.c[(int64_t)col * p.ldc + row] = x;
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ split-K reduction
+// One work-group per (upper tile, 64 x 64 sub-block).  Sums the partial tiles in fp64,
+// adds the old H when accumulating, writes H[i][j] and (through LDS) H[j][i], i <= j.
+__global__ __launch_bounds__(256) void k_syrk_reduce(const float* __restrict__ part, int N,
+                                                     int tiles, int ntiles, int ksplit,
+                                                     float* __restrict__ H, int64_t ldh,
+                                                     int accumulate) {
+  __shared__ float tr[64][65];
+  const int sub = blockIdx.x & 15;
+  int t = blockIdx.x >> 4;
+  const int sr = sub >> 2, sc = sub & 3;
+  int tm = 0, cnt = tiles;
+  while (t >= cnt) { t -= cnt; ++tm; --cnt; }
+  const int tn = tm + t;
+  const int tidx = blockIdx.x >> 4;
+  const int i0 = tm * BM + sr * 64, j0 = tn * BN + sc * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int r = ty; r < 64; r += 4) {
+    const int i = i0 + r, j = j0 + tx;
+    double sum = 0.0;
+    const int64_t off = (int64_t)tidx * (BM * BN) + (int64_t)(sr * 64 + r) * BN + sc * 64 + tx;
+    for (int s = 0; s < ksplit; ++s) sum += (double)part[(int64_t)s * ntiles * (BM * BN) + off];
+    float v = 0.f;
+    if (i < N && j < N) {
+      const int ii = i <= j ? i : j, jj = i <= j ? j : i;
+      if (accumulate) sum += (double)H[(int64_t)ii * ldh + jj];
+      v = (float)sum;
+      if (i <= j) H[(int64_t)i * ldh + j] = v;
+    }
+    tr[r][tx] = v;
+  }
+  __syncthreads();
+  // transposed write: element (i0 + c, j0 + r') -> H[j0 + r'][i0 + c]
+  for (int r = ty; r < 64; r += 4) {
+    const int j = j0 + r, i = i0 + tx;
+    if (i < N && j < N && i <= j) H[(int64_t)j * ldh + i] = tr[tx][r];
+  }
+}
+
+// ------------------------------------------------------------------ elementwise
+template <typename T>
+__device__ __forceinline__ float ld_f(const T* p) { return (float)*p; }
+
+template <typename T>
+__global__ void k_split(const T* __restrict__ in, int64_t ld_in, int rows, int cols,
+                        const float* __restrict__ col_scale, u16* __restrict__ hi,
+                        u16* __restrict__ lo, int64_t ld_out) {
+  const int64_t total = (int64_t)rows * cols;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(e / cols), c = (int)(e - (int64_t)r * cols);
+    float x = ld_f(in + (int64_t)r * ld_in + c);
+    if (col_scale) x *= col_scale[c];
+    const uint32_t h = bf16_rne_bits(x);
+    const float hf = __uint_as_float(h << 16);
+    hi[(int64_t)r * ld_out + c] = (u16)h;
+    if (lo) lo[(int64_t)r * ld_out + c] = (u16)bf16_rne_bits(x - hf);
+  }
+}
+
+// 4-wide variant for fp32 rows with cols % 4 == 0 and 16-byte aligned rows.
+__global__ void k_split4(const float* __restrict__ in, int64_t ld_in, int rows, int cols,
+                         const float* __restrict__ col_scale, u16* __restrict__ hi,
+                         u16* __restrict__ lo, int64_t ld_out) {
+  const int c4 = cols >> 2;
+  const int64_t total = (int64_t)rows * c4;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(e / c4), c = (int)(e - (int64_t)r * c4) * 4;
+    float4 x = *reinterpret_cast<const float4*>(in + (int64_t)r * ld_in + c);
+    if (col_scale) {
+      const float4 sc = *reinterpret_cast<const float4*>(col_scale + c);
+      x.x *= sc.x; x.y *= sc.y; x.z *= sc.z; x.w *= sc.w;
+    }
+    const float xs[4] = {x.x, x.y, x.z, x.w};
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      h[q] = bf16_rne_bits(xs[q]);
+      l[q] = bf16_rne_bits(xs[q] - __uint_as_float(h[q] << 16));
+    }
+    *reinterpret_cast<uint2*>(hi + (int64_t)r * ld_out + c) =
+        make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    if (lo)
+      *reinterpret_cast<uint2*>(lo + (int64_t)r * ld_out + c) =
+          make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
+  }
+}
+
+__global__ void k_fill_zero(float* p, int rows, int cols, int64_t ld) {
+  const int64_t total = (int64_t)rows * cols;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int r = (int)(e / cols), c = (int)(e - (int64_t)r * cols);
+    p[(int64_t)r * ld + c] = 0.f;
+  }
+}
+
+int grid_for(int64_t n, int per_block) {
+  int64_t g = (n + per_block - 1) / per_block;
+  if (g > 65536) g = 65536;
+  if (g < 1) g = 1;
+  return (int)g;
+}
+
+template <bool AK, bool BKM, bool F16, int EPI>
+void launch(const KParams& p, int grid, hipStream_t s) {
+  hipLaunchKernelGGL((k_gemm<AK, BKM, F16, EPI>), dim3(grid), dim3(NT), 0, s, p);
+}
+
+template <bool AK, bool BKM, bool F16>
+bool dispatch_epi(const KParams& p, int epi, int grid, hipStream_t s) {
+  switch (epi) {
+    case EPI_F32: launch<AK, BKM, F16, EPI_F32>(p, grid, s); return true;
+    case EPI_SPLIT: launch<AK, BKM, F16, EPI_SPLIT>(p, grid, s); return true;
+    case EPI_SYM: launch<AK, BKM, F16, EPI_SYM>(p, grid, s); return true;
+    case EPI_PARTIAL: launch<AK, BKM, F16, EPI_PARTIAL>(p, grid, s); return true;
+  }
+  return false;
+}
+
+}  // namespace
+
+int gemm_sym_tiles(int N) {
+  const int t = (N + BN - 1) / BN;
+  return t * (t + 1) / 2;
+}
+
+size_t gemm_partial_bytes(int N, int ksplit) {
+  return (size_t)gemm_sym_tiles(N) * ksplit * BM * BN * sizeof(float);
+}
+
+hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
+  if (d.M <= 0 || d.N <= 0) return hipSuccess;
+  KParams p{};
+  p.M = d.M; p.N = d.N; p.K = d.K;
+  p.a0 = d.a[0]; p.a1 = d.a[1] ? d.a[1] : d.a[0];
+  p.b0 = d.b[0]; p.b1 = d.b[1] ? d.b[1] : d.b[0];
+  p.lda = d.lda; p.ldb = d.ldb;
+  p.npass = d.npass;
+  p.pa0 = d.pa[0]; p.pa1 = d.pa[1]; p.pa2 = d.pa[2];
+  p.pb0 = d.pb[0]; p.pb1 = d.pb[1]; p.pb2 = d.pb[2];
+  p.c = d.c; p.ldc = d.ldc; p.c_hi = d.c_hi; p.c_lo = d.c_lo;
+  auto al = [](const u16* q, int64_t ld) {
+    return ((reinterpret_cast<uintptr_t>(q) & 15) == 0) && (ld % 8 == 0);
+  };
+  p.aligned_a = al(p.a0, d.lda) && al(p.a1, d.lda);
+  p.aligned_b = al(p.b0, d.ldb) && al(p.b1, d.ldb);
+  p.tiles_m = (d.M + BM - 1) / BM;
+  p.tiles_n = (d.N + BN - 1) / BN;
+  const bool sym = d.epi == EPI_SYM || d.epi == EPI_PARTIAL;
+  p.ntiles = sym ? p.tiles_n * (p.tiles_n + 1) / 2 : p.tiles_m * p.tiles_n;
+  p.ksplit = d.epi == EPI_PARTIAL ? d.ksplit : 1;
+  const int kt_total = (d.K + BK - 1) / BK;
+  const int kt_per = (kt_total + p.ksplit - 1) / p.ksplit;
+  p.k_per_split = kt_per * BK;
+  p.part = partial;
+  const int grid = p.ntiles * p.ksplit;
+  const char* name = d.epi == EPI_PARTIAL ? "gemm_syrk" : (d.epi == EPI_SYM ? "gemm_sym" : "gemm");
+  prof_begin(s, name);
+  bool ok;
+  if (d.a_kmajor && d.b_kmajor) {
+    ok = d.f16 ? dispatch_epi<true, true, true>(p, d.epi, grid, s)
+               : dispatch_epi<true, true, false>(p, d.epi, grid, s);
+  } else if (d.a_kmajor && !d.b_kmajor) {
+    ok = d.f16 ? dispatch_epi<true, false, true>(p, d.epi, grid, s)
+               : dispatch_epi<true, false, false>(p, d.epi, grid, s);
+  } else if (!d.a_kmajor && !d.b_kmajor) {
+    ok = d.f16 ? dispatch_epi<false, false, true>(p, d.epi, grid, s)
+               : dispatch_epi<false, false, false>(p, d.epi, grid, s);
+  } else {
+    ok = false;
+  }
+  prof_end(s);
+  if (!ok) return hipErrorInvalidValue;
+  return last_launch_error();
+}
+
+hipError_t syrk_reduce(const float* partial, int N, int ksplit, float* H, int64_t ldh,
+                       int accumulate, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  const int tiles = (N + BN - 1) / BN;
+  const int ntiles = tiles * (tiles + 1) / 2;
+  prof_begin(s, "syrk_reduce");
+  hipLaunchKernelGGL(k_syrk_reduce, dim3(ntiles * 16), dim3(256), 0, s, partial, N, tiles,
+                     ntiles, ksplit, H, ldh, accumulate);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t split_bf16(const void* in, int in_type, int64_t ld_in, int rows, int cols,
+                      const float* col_scale, u16* hi, u16* lo, int64_t ld_out, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  prof_begin(s, "split_bf16");
+  if (in_type == 0) {
+    const bool vec = (cols % 4 == 0) && (ld_in % 4 == 0) && (ld_out % 4 == 0) &&
+                     ((reinterpret_cast<uintptr_t>(in) & 15) == 0) &&
+                     ((reinterpret_cast<uintptr_t>(hi) & 7) == 0) &&
+                     (!lo || (reinterpret_cast<uintptr_t>(lo) & 7) == 0) &&
+                     (!col_scale || (reinterpret_cast<uintptr_t>(col_scale) & 15) == 0);
+    if (vec) {
+      hipLaunchKernelGGL(k_split4, dim3(grid_for((int64_t)rows * cols / 4, 256)), dim3(256), 0, s,
+                         (const float*)in, ld_in, rows, cols, col_scale, hi, lo, ld_out);
+    } else {
+      hipLaunchKernelGGL(k_split<float>, dim3(grid_for((int64_t)rows * cols, 256)), dim3(256), 0,
+                         s, (const float*)in, ld_in, rows, cols, col_scale, hi, lo, ld_out);
+    }
+  } else {
+    hipLaunchKernelGGL(k_split<_Float16>, dim3(grid_for((int64_t)rows * cols, 256)), dim3(256),
+                       0, s, (const _Float16*)in, ld_in, rows, cols, col_scale, hi, lo, ld_out);
+  }
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t fill_zero_f32(float* p, int rows, int cols, int64_t ld, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  prof_begin(s, "fill_zero");
+  hipLaunchKernelGGL(k_fill_zero, dim3(grid_for((int64_t)rows * cols, 256)), dim3(256), 0, s, p,
+                     rows, cols, ld);
+  prof_end(s);
+  return last_launch_error();
+}
+
+}  // namespace fq

@@ -1,0 +1,215 @@
+"""Thin Python binding of libfq (the C ABI in include/fq.h).
+
+Argument marshalling only: every function here checks tensor placement, shape and dtype,
+turns tensors into device pointers, allocates the caller-side workspace with torch when
+none is given, and calls the library.  All arithmetic of the pass runs in libfq's HIP
+kernels; nothing here falls back to another implementation.  Loading fails loudly when
+libfq.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfq.so")
+
+FQ_F32, FQ_F16, FQ_BF16 = 0, 1, 2
+STATUS = {0: "FQ_OK", 1: "FQ_ERR_INVALID_ARG", 2: "FQ_ERR_UNSUPPORTED",
+          3: "FQ_ERR_NOT_POSITIVE_DEFINITE", 4: "FQ_ERR_NONFINITE",
+          5: "FQ_ERR_WORKSPACE_TOO_SMALL", 6: "FQ_ERR_HIP"}
+
+# exported symbols of include/fq.h: name -> (restype, argtypes)
+_vp, _i64, _i, _sz, _d = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t, ctypes.c_double
+SIGNATURES = {
+    "fq_hessian_accumulate": (_i, [_vp, _vp, _i, _i64, _i64, _i64, _vp, _i, _vp, _sz]),
+    "fq_hessian_workspace_bytes": (_sz, [_i, _i64, _i64]),
+    "fq_frame_analysis": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp, _vp,
+                               _vp, _sz]),
+    "fq_frame_analysis_workspace_bytes": (_sz, [_i, _i64, _i64, _i64, _i64]),
+    "fq_quantize_frames": (_i, [_vp, _vp, _vp, _i64, _i64, _i, _i, _d, _d, _vp, _vp, _vp, _vp,
+                                _sz]),
+    "fq_quantize_frames_workspace_bytes": (_sz, [_i64, _i64, _i]),
+    "fq_frame_synthesis": (_i, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp,
+                                _sz]),
+    "fq_frame_synthesis_workspace_bytes": (_sz, [_i64, _i64, _i64, _i64]),
+    "fq_status_string": (ctypes.c_char_p, [_i]),
+    "fq_last_error": (ctypes.c_char_p, []),
+    "fq_profile_enable": (None, [_i]),
+    "fq_profile_reset": (None, []),
+    "fq_profile_query": (_i, [ctypes.c_char_p, ctypes.POINTER(_i), ctypes.POINTER(_d)]),
+}
+
+_lib = None
+
+
+class FQError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libfq.so (raises ImportError when it is missing)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it first "
+                              "(python -m paper_2403_06082_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise FQError(status, lib().fq_last_error().decode())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dt(t) -> int:
+    torch = _torch()
+    return {torch.float32: FQ_F32, torch.float16: FQ_F16, torch.bfloat16: FQ_BF16}[t.dtype]
+
+
+def _dev(t, name, dtype=None, shape=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ws(nbytes, ws, device):
+    torch = _torch()
+    if ws is None:
+        ws = torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    return ws, ctypes.c_void_p(ws.data_ptr()), ws.numel() * ws.element_size()
+
+
+# ------------------------------------------------------------------ workspace queries
+def fq_hessian_workspace_bytes(xt: int, n_tokens: int, d_in: int) -> int:
+    return lib().fq_hessian_workspace_bytes(xt, n_tokens, d_in)
+
+
+def fq_frame_analysis_workspace_bytes(wt, d_out, d_in, K_out, K_in) -> int:
+    return lib().fq_frame_analysis_workspace_bytes(wt, d_out, d_in, K_out, K_in)
+
+
+def fq_quantize_frames_workspace_bytes(K_out, K_in, block) -> int:
+    return lib().fq_quantize_frames_workspace_bytes(K_out, K_in, block)
+
+
+def fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in) -> int:
+    return lib().fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in)
+
+
+# ------------------------------------------------------------------ the four calls
+def fq_hessian_accumulate(X, H, accumulate: bool = False, ws=None, stream=None):
+    """H (+)= X^T X.  X: (n, d_in) f32/f16/bf16 device tensor, H: (d_in, d_in) f32."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D with unit column stride")
+    n, d = X.shape
+    _dev(H, "H", torch.float32, (d, d))
+    ws, wp, wb = _ws(fq_hessian_workspace_bytes(_dt(X), n, d), ws, X.device)
+    _check(lib().fq_hessian_accumulate(_stream(stream), _ptr(X), _dt(X), n, d, X.stride(0),
+                                       _ptr(H), int(bool(accumulate)), wp, wb))
+    return H
+
+
+def fq_frame_analysis(W, P_out, P_in, H=None, D=None, Ht=None, ws=None, stream=None):
+    """D = P_out^T W P_in and Ht = P_in^T H P_in (each optional)."""
+    torch = _torch()
+    d_out, d_in = W.shape
+    _dev(W, "W")
+    _dev(P_out, "P_out", torch.float32)
+    _dev(P_in, "P_in", torch.float32)
+    K_out, K_in = P_out.shape[1], P_in.shape[1]
+    if P_out.shape[0] != d_out or P_in.shape[0] != d_in:
+        raise ValueError("frame shapes do not match W")
+    _dev(H, "H", torch.float32, (d_in, d_in))
+    _dev(D, "D", torch.float32, (K_out, K_in))
+    _dev(Ht, "Ht", torch.float32, (K_in, K_in))
+    ws, wp, wb = _ws(fq_frame_analysis_workspace_bytes(_dt(W), d_out, d_in, K_out, K_in), ws,
+                     W.device)
+    _check(lib().fq_frame_analysis(_stream(stream), _ptr(W), _dt(W), d_out, d_in, _ptr(P_out),
+                                   K_out, _ptr(P_in), K_in, _ptr(H), _ptr(D), _ptr(Ht), wp, wb))
+    return D, Ht
+
+
+def fq_quantize_frames(D, Ht, codes, scale, zero, bits: int = 2, block: int = 128,
+                       damp: float = 0.01, clip_sigmas: float = 2.0, ws=None, stream=None):
+    """2-bit codes (K_out, ceil(K_in/16)) int32 view of uint32 words, scale/zero (K_out,)."""
+    torch = _torch()
+    K_out, K_in = D.shape
+    _dev(D, "D", torch.float32)
+    _dev(Ht, "Ht", torch.float32, (K_in, K_in))
+    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    ws, wp, wb = _ws(fq_quantize_frames_workspace_bytes(K_out, K_in, block), ws, D.device)
+    _check(lib().fq_quantize_frames(_stream(stream), _ptr(D), _ptr(Ht), K_out, K_in, bits, block,
+                                    float(damp), float(clip_sigmas), _ptr(codes), _ptr(scale),
+                                    _ptr(zero), wp, wb))
+    return codes, scale, zero
+
+
+def fq_frame_synthesis(codes, scale, zero, P_out, P_in, W_hat, ws=None, stream=None):
+    """W_hat = P_out diag(scale) (codes - zero) P_in^T."""
+    torch = _torch()
+    K_out, K_in = P_out.shape[1], P_in.shape[1]
+    d_out, d_in = P_out.shape[0], P_in.shape[0]
+    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    _dev(P_out, "P_out", torch.float32)
+    _dev(P_in, "P_in", torch.float32)
+    _dev(W_hat, "W_hat", torch.float32, (d_out, d_in))
+    ws, wp, wb = _ws(fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in), ws,
+                     W_hat.device)
+    _check(lib().fq_frame_synthesis(_stream(stream), _ptr(codes), _ptr(scale), _ptr(zero), K_out,
+                                    K_in, _ptr(P_out), d_out, _ptr(P_in), d_in, _ptr(W_hat), wp,
+                                    wb))
+    return W_hat
+
+
+# ------------------------------------------------------------------ kernel timer
+def fq_profile_enable(on: bool = True):
+    lib().fq_profile_enable(int(bool(on)))
+
+
+def fq_profile_reset():
+    lib().fq_profile_reset()
+
+
+def fq_profile_query(prefix: str = ""):
+    n = ctypes.c_int(0)
+    ms = ctypes.c_double(0.0)
+    if lib().fq_profile_query(prefix.encode(), ctypes.byref(n), ctypes.byref(ms)) != 0:
+        raise FQError(6, "event query failed")
+    return n.value, ms.value
