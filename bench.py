@@ -1,0 +1,285 @@
+"""Benchmark: FrameQuant's per-layer quantization pass on one MI355X.
+
+One step = the whole pass on one layer with its inputs resident in HBM:
+    H = X^T X (262,144 tokens)  ->  D = P_l^T W P_prev, H~ = P_prev^T H P_prev
+    ->  clip + grid + OPTQ 2-bit rounding (fp64)  ->  W^ = P_l D^ P_prev^T
+on the Llama-2-7B-shaped up_proj layer (11008 x 4096 bf16, X 262,144 x 4096 bf16,
+frames r = 1.1: K_out x K_in = 12112 x 4512, block 128).  Inputs are synthetic and
+seeded (fq_inputs).
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Prints one JSON line.  value = quantized weights per second (d_out * d_in / step time).
+"roofline" is the dominant kernel's algorithmic throughput against its MFMA peak, timed
+with HIP events on its own launch stream inside the timed region; "kernels" lists every
+kernel group the same way.  "cpu_baseline" is the float64 CPU oracle timed on a bounded
+sample of the same workload on this host, extrapolated stage by stage.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "quantized weights/sec per layer (Llama-7B-shaped 11008×4096); MFMA % of peak"
+PEAK = {"bf16": 2500.0, "f64": 78.6, "hbm": 8000.0}    # TFLOP/s, TFLOP/s, GB/s
+
+
+def algorithmic_work(n, d_out, d_in, K_out, K_in, block):
+    """Algorithmic flops (bytes for the memory-bound kernels) per launch group and step."""
+    gptq_upd = 0
+    for o1 in range(0, K_in, block):
+        o2 = min(o1 + block, K_in)
+        for i1 in range(o1, o2, 128):
+            i2 = min(i1 + 128, o2)
+            gptq_upd += 2 * K_out * (i2 - i1) * (o2 - i2)
+        gptq_upd += 2 * K_out * (o2 - o1) * (K_in - o2)
+    chol = 0
+    for k0 in range(0, K_in, 64):
+        kb = min(64, K_in - k0)
+        rest = K_in - k0 - kb
+        chol += rest * (rest + 1) * kb          # lower-triangle rank-kb update, 2 flops/FMA
+    return {
+        "gemm_hessian": ("bf16", n * d_in * (d_in + 1)),
+        "gemm_analysis_w1": ("bf16", 2 * K_out * d_out * d_in),
+        "gemm_analysis_w2": ("bf16", 2 * K_out * d_in * K_in),
+        "gemm_analysis_h1": ("bf16", 2 * d_in * d_in * K_in),
+        "gemm_analysis_h2": ("bf16", K_in * (K_in + 1) * d_in),
+        "gemm_synthesis_1": ("bf16", 2 * d_out * K_out * K_in),
+        "gemm_synthesis_2": ("bf16", 2 * d_out * K_in * d_in),
+        "gptq_update": ("f64", gptq_upd),
+        "chol_syrk": ("f64", chol),
+        "gptq_block": ("f64", K_out * K_in * 128),     # in-block FMAs (upper bound)
+        "pack2": ("hbm", K_out * K_in + K_out * ((K_in + 15) // 16) * 4),
+    }
+
+
+KERNEL_GROUPS = ["gemm_hessian", "gemm_analysis_w1", "gemm_analysis_w2", "gemm_analysis_h1",
+                 "gemm_analysis_h2", "gemm_synthesis_1", "gemm_synthesis_2", "gptq_update",
+                 "gptq_block", "chol_syrk", "chol_potrf", "chol_trsm", "q_", "split_bf16",
+                 "syrk_reduce", "dequant", "pack2"]
+
+
+def make_inputs(wl, li):
+    import torch
+    from fq_inputs import gen
+    L = wl.layers[li]
+    t0 = time.time()
+    Xs = gen.make_x(wl, L.d_in)
+    Ws = gen.make_weight(wl, li)
+    Po64, Pi64 = gen.make_frames(wl, li)
+    Po, Pi = gen.frame_f32(Po64), gen.frame_f32(Pi64)
+    del Po64, Pi64
+
+    def up(a, dt):
+        t = torch.from_numpy(a)
+        if dt == "bf16":
+            t = t.view(torch.bfloat16)
+        return t.cuda()
+
+    dev = dict(X=up(Xs, wl.x_dtype), W=up(Ws, wl.w_dtype), P_out=up(Po, "f32"),
+               P_in=up(Pi, "f32"))
+    host = dict(X=Xs, W=Ws, P_out=Po, P_in=Pi)
+    print(f"[bench] inputs generated and uploaded in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
+    return dev, host
+
+
+def cpu_baseline(wl, li, host, budget_rows=1024, sample_tokens=8192):
+    """Time the oracle on a bounded sample of the same layer and extrapolate per stage:
+    H over one 8,192-token chunk (x n / 8192); D, OPTQ and W^ on `budget_rows` sampled
+    rows (x rows / budget_rows); H~ and the factor U in full."""
+    import oracle as O
+    from fq_inputs import gen
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    L = wl.layers[li]
+    n = wl.n_tokens
+    X = host["X"]
+    W64 = gen.storage_to_f32(host["W"], wl.w_dtype).astype(np.float64)
+    Po = host["P_out"].astype(np.float64)
+    Pi = host["P_in"].astype(np.float64)
+    K_out, K_in = Po.shape[1], Pi.shape[1]
+    rng = np.random.default_rng(0)
+    t = {}
+    s0 = time.perf_counter()
+    Xc = gen.storage_to_f32(X[:sample_tokens], wl.x_dtype).astype(np.float64)
+    H = O.hessian(Xc) * (n / sample_tokens)
+    t["hessian"] = (time.perf_counter() - s0) * (n / sample_tokens)
+    rows = np.sort(rng.choice(K_out, size=min(budget_rows, K_out), replace=False))
+    s0 = time.perf_counter()
+    D_rows = (Po[:, rows].T @ W64) @ Pi
+    t["analysis_D"] = (time.perf_counter() - s0) * (K_out / len(rows))
+    s0 = time.perf_counter()
+    _, Ht = O.frame_analysis(np.zeros((1, L.d_in)), np.zeros((1, 1)), Pi, H)
+    t["analysis_Ht"] = time.perf_counter() - s0
+    s0 = time.perf_counter()
+    U, dead, _ = O.gptq_prepare(Ht, wl.damp)
+    t["factor"] = time.perf_counter() - s0
+    s0 = time.perf_counter()
+    mu, sigma, lo, hi = O.clip_bounds(D_rows, wl.clip_sigmas)
+    Dc = O.apply_clip(D_rows, lo, hi)
+    sc, z = O.row_grid(Dc)
+    r = O.gptq(Dc, U, sc, z, wl.bits, wl.block, dead)
+    O.pack2(r["codes"])
+    t["gptq"] = (time.perf_counter() - s0) * (K_out / len(rows))
+    orow = np.sort(rng.choice(L.d_out, size=min(budget_rows, L.d_out), replace=False))
+    Dh = O.dequant(r["codes"], sc, z)
+    # rows of W^ = (P_l[rows, :] D^) P_prev^T; the sampled rows of D^ stand in for all of it
+    s0 = time.perf_counter()
+    Mr = Po[orow][:, rows] @ Dh
+    t["synthesis_1"] = (time.perf_counter() - s0) * (L.d_out / len(orow)) * (K_out / len(rows))
+    s0 = time.perf_counter()
+    _ = Mr @ Pi.T
+    t["synthesis_2"] = (time.perf_counter() - s0) * (L.d_out / len(orow))
+    total = sum(t.values())
+    return {"value": L.d_out * L.d_in / total, "unit": "weights/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"float64 numpy oracle: H on {sample_tokens} of {n} tokens (x{n // sample_tokens}); "
+                       f"D, OPTQ and synthesis on {len(rows)} of {K_out} FF rows (scaled to all rows); "
+                       f"H~ and its Cholesky factor in full; extrapolated total {total:.1f} s"),
+            "stage_seconds": {k: round(v, 3) for k, v in t.items()}}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="llama7b")
+    ap.add_argument("--layer", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the per-layer pass runs on a single device in this "
+              "build (no multi-GPU path); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2403_06082_amd as fq
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    from fq_inputs import WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    fq.lib()
+    wl = WORKLOADS[args.workload]
+    li = args.layer
+    L = wl.layers[li]
+    dev, host = make_inputs(wl, li)
+    K_out, K_in = dev["P_out"].shape[1], dev["P_in"].shape[1]
+    n = dev["X"].shape[0]
+    bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], bufs, block=wl.block,
+                       damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream)
+
+    for i in range(args.warmup):
+        step()
+        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    fq.fq_profile_reset()
+    fq.fq_profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    fq.fq_profile_enable(False)
+    ms = (t1 - t0) * 1000.0 / args.steps
+    print(f"[bench] {args.steps} timed steps: {ms:.2f} ms/step", file=sys.stderr, flush=True)
+
+    work = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block)
+    kernels = {}
+    for name in KERNEL_GROUPS:
+        cnt, tot = fq.fq_profile_query(name)
+        if cnt == 0:
+            continue
+        e = {"launches_per_step": cnt / args.steps, "ms_per_step": round(tot / args.steps, 4)}
+        if name in work:
+            kind, amount = work[name]
+            per_step_s = tot / args.steps / 1000.0
+            if kind == "hbm":
+                e["GB/s"] = round(amount / per_step_s / 1e9, 1)
+                e["frac_of_peak"] = round(amount / per_step_s / 1e9 / PEAK["hbm"], 4)
+            else:
+                e["TFLOP/s"] = round(amount / per_step_s / 1e12, 2)
+                e["frac_of_peak"] = round(amount / per_step_s / 1e12 / PEAK[kind], 4)
+                e["peak"] = kind
+        kernels[name] = e
+    cnt_all, tot_all = fq.fq_profile_query("")
+    fq.fq_profile_reset()
+
+    # dominant kernel with a defined algorithmic count
+    dom = max((k for k in kernels if k in work), key=lambda k: kernels[k]["ms_per_step"])
+    kind, amount = work[dom]
+    launches = kernels[dom]["launches_per_step"]
+    avg_ms = kernels[dom]["ms_per_step"] / launches
+    per_launch = amount / launches
+    if kind == "hbm":
+        roof = {"bound": "hbm", "achieved": round(per_launch / (avg_ms / 1e3) / 1e9, 1),
+                "peak": PEAK["hbm"], "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": round(per_launch / (avg_ms / 1e3) / 1e12, 2),
+                "peak": PEAK[kind], "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["avg_launch_ms"] = round(avg_ms, 4)
+    roof["algorithmic_per_launch"] = per_launch
+
+    # spec contraction fraction: Hessian + analysis contractions at bf16 peak
+    contr = [k for k in kernels if k.startswith("gemm_hessian") or k.startswith("gemm_analysis")]
+    c_flops = sum(work[k][1] for k in contr)
+    c_ms = sum(kernels[k]["ms_per_step"] for k in contr)
+    contraction_frac = c_flops / (c_ms / 1e3) / 1e12 / PEAK["bf16"] if c_ms > 0 else None
+
+    out = {
+        "metric": METRIC,
+        "value": round(L.d_out * L.d_in / (ms / 1e3), 1),
+        "unit": "weights/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 MFMA (fp32 acc) + fp64",
+        "data": "synthetic (seeded; Gaussian weights with 1% x10 outliers, Gaussian "
+                "activations with 8 channels x100)",
+        "config": {"workload": f"{wl.key} {L.name}_proj: W {L.d_out}x{L.d_in} {wl.w_dtype}, "
+                               f"X {n}x{L.d_in} {wl.x_dtype}, frames K {K_out}x{K_in} "
+                               f"(r={wl.r}, rho={wl.rho}), {wl.bits}-bit, block {wl.block}, "
+                               f"damp {wl.damp}, clip {wl.clip_sigmas} sigma",
+                   "d_out": L.d_out, "d_in": L.d_in, "n_tokens": n, "K_out": K_out,
+                   "K_in": K_in},
+        "roofline": roof,
+        "contraction_mfma_frac": None if contraction_frac is None else round(contraction_frac, 4),
+        "kernels": kernels,
+        "kernel_ms_total_per_step": round(tot_all / args.steps, 3),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, li, host)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

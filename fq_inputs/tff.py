@@ -199,12 +199,13 @@ def rotation_factors(d: int, seed_seq) -> tuple[np.ndarray, np.ndarray]:
 
 def apply_rotation(R1: np.ndarray, R2: np.ndarray, T: np.ndarray) -> np.ndarray:
     """(R1 (x) R2) @ T without forming the Kronecker product: each column t of T is
-    reshaped row-major to d1 x d2 and mapped to R1 t R2^T."""
+    reshaped row-major to d1 x d2 and mapped to R1 t R2^T (two large matrix products)."""
     d1, d2 = R1.shape[0], R2.shape[0]
     K = T.shape[1]
-    M = T.T.reshape(K, d1, d2)
-    out = np.matmul(np.matmul(R1[None], M), R2.T[None])
-    return out.reshape(K, d1 * d2).T
+    M = np.ascontiguousarray(T.T).reshape(K, d1, d2)
+    A = np.tensordot(R1, M, axes=([1], [1]))                 # (d1, K, d2)
+    B = (A.reshape(d1 * K, d2) @ R2.T).reshape(d1, K, d2)
+    return np.ascontiguousarray(B.transpose(1, 0, 2).reshape(K, d1 * d2).T)
 
 
 def parseval_frame(k: int, rho: int, d: int, seed_seq=None, rotate: bool = True) -> np.ndarray:

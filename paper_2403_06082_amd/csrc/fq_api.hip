@@ -273,6 +273,7 @@ fq_status fq_hessian_accumulate(void* stream, const void* X, int xt, int64_t n_t
   g.a_kmajor = false; g.b_kmajor = false;
   g.epi = EPI_PARTIAL;
   g.ksplit = L.ksplit;
+  g.name = "gemm_hessian";
   if (xt == FQ_F32) {
     e = split_bf16(X, 0, ldx, (int)n_tokens, (int)d_in, nullptr, L.xhi, L.xlo, L.ldp, s);
     if (e != hipSuccess) return hip_fail(e, "split X");
@@ -357,6 +358,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
         g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
       }
       g.epi = EPI_SPLIT; g.c_hi = L.t_hi; g.c_lo = L.t_lo; g.ldc = L.ldi;
+      g.name = "gemm_analysis_w1";
       e = gemm_run(g, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 1");
       // D = T P_in  (K_out x K_in)
@@ -367,6 +369,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       g2.npass = 3;
       g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
       g2.epi = EPI_F32; g2.c = D; g2.ldc = K_in;
+      g2.name = "gemm_analysis_w2";
       e = gemm_run(g2, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 2");
     }
@@ -386,6 +389,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       g.npass = 3;
       g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
       g.epi = EPI_SPLIT; g.c_hi = L.g_hi; g.c_lo = L.g_lo; g.ldc = L.ldki;
+      g.name = "gemm_analysis_h1";
       e = gemm_run(g, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 3");
       // Ht = P_in^T G  (K_in x K_in, upper tiles mirrored)
@@ -396,6 +400,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       g2.npass = 3;
       g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
       g2.epi = EPI_SYM; g2.c = Ht; g2.ldc = K_in;
+      g2.name = "gemm_analysis_h2";
       e = gemm_run(g2, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 4");
     }
@@ -508,6 +513,7 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   g.npass = 2;
   g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
   g.epi = EPI_SPLIT; g.c_hi = L.n_hi; g.c_lo = L.n_lo; g.ldc = L.ldki;
+  g.name = "gemm_synthesis_1";
   if ((e = gemm_run(g, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 1");
   // W_hat = N P_in^T  (d_out x d_in)
   GemmDesc g2;
@@ -517,6 +523,7 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   g2.npass = 3;
   g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
   g2.epi = EPI_F32; g2.c = W_hat; g2.ldc = d_in;
+  g2.name = "gemm_synthesis_2";
   if ((e = gemm_run(g2, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 2");
   return FQ_OK;
 }

@@ -43,6 +43,7 @@ struct GemmDesc {
   u16* c_hi = nullptr;
   u16* c_lo = nullptr;
   int ksplit = 1;                // EPI_PARTIAL only
+  const char* name = "gemm";     // kernel-timer label
 };
 
 // Workspace bytes needed by EPI_PARTIAL for an N x N symmetric product split ksplit ways.

@@ -474,8 +474,7 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
   p.k_per_split = kt_per * BK;
   p.part = partial;
   const int grid = p.ntiles * p.ksplit;
-  const char* name = d.epi == EPI_PARTIAL ? "gemm_syrk" : (d.epi == EPI_SYM ? "gemm_sym" : "gemm");
-  prof_begin(s, name);
+  prof_begin(s, d.name);
   bool ok;
   if (d.a_kmajor && d.b_kmajor) {
     ok = d.f16 ? dispatch_epi<true, true, true>(p, d.epi, grid, s)
