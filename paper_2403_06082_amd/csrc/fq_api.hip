@@ -5,6 +5,7 @@
 
 #include <math.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 #include <string>
 #include <vector>
@@ -27,6 +28,13 @@ static fq_status hip_fail(hipError_t e, const char* where) {
 }
 
 hipError_t last_launch_error() { return hipGetLastError(); }
+
+// tile edge of the fp64 update GEMM (FQ_DGEMM_TILE=64|128 overrides, for tuning)
+static int dgemm_tile_from_env() {
+  const char* v = getenv("FQ_DGEMM_TILE");
+  return (v && atoi(v) == 128) ? 128 : 64;
+}
+static int g_dgemm_tile = dgemm_tile_from_env();
 
 // ---------------------------------------------------------------- kernel timer
 struct ProfRec {
@@ -141,8 +149,18 @@ static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out
   return c.off + 256;
 }
 
+// Columns are rounded in chunks of min(block, 128) by the sequential kernel; the
+// residuals of consecutive chunks are applied to the columns right of them in spans of
+// at least 512 columns (a whole number of blocks): inside a span after every chunk,
+// beyond it once per span.  This regroups OPTQ's lazy block updates; every column still
+// receives exactly the sum of the residual terms of all earlier columns.
+static int64_t chunk_width(int block) { return block < 128 ? block : 128; }
+static int64_t span_width(int block) {
+  const int64_t b = block;
+  return b * ((512 + b - 1) / b);
+}
 static int64_t res_width(int64_t K_in, int block) {
-  int64_t w = block < K_in ? block : K_in;
+  int64_t w = span_width(block) < K_in ? span_width(block) : K_in;
   return w > 0 ? w : 1;
 }
 
@@ -442,21 +460,22 @@ fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int6
   if ((e = q_reverse_upper(Q.A, K_in, Q.R, Q.inv_rdiag, s)) != hipSuccess) return hip_fail(e, "reverse");
   if ((e = q_clip_grid(D, K_out, K_in, bits, Q, scale, zero, s)) != hipSuccess) return hip_fail(e, "clip/grid");
   const int64_t ldr = res_width(K_in, block);
-  for (int64_t o1 = 0; o1 < K_in; o1 += block) {
-    const int64_t o2 = (o1 + block < K_in) ? o1 + block : K_in;
-    for (int64_t i1 = o1; i1 < o2; i1 += 128) {
-      const int64_t i2 = (i1 + 128 < o2) ? i1 + 128 : o2;
-      if ((e = q_gptq_block(D, K_out, K_in, (int)i1, (int)i2, (int)o1, ldr, bits, Q, s)) != hipSuccess)
+  const int64_t cw = chunk_width(block), sw = span_width(block);
+  for (int64_t s1 = 0; s1 < K_in; s1 += sw) {
+    const int64_t s2 = (s1 + sw < K_in) ? s1 + sw : K_in;
+    for (int64_t i1 = s1; i1 < s2; i1 += cw) {
+      const int64_t i2 = (i1 + cw < s2) ? i1 + cw : s2;
+      if ((e = q_gptq_block(D, K_out, K_in, (int)i1, (int)i2, (int)s1, ldr, bits, Q, s)) != hipSuccess)
         return hip_fail(e, "rounding block");
-      if (i2 < o2) {
-        e = dgemm(K_out, o2 - i2, i2 - i1, 1.0, Q.res + (i1 - o1), ldr, Q.R + i1 * K_in + i2, K_in,
-                  false, Q.Y + i2, K_in, false, s);
-        if (e != hipSuccess) return hip_fail(e, "in-block update");
+      if (i2 < s2) {
+        e = dgemm(K_out, s2 - i2, i2 - i1, 1.0, 1.0, Q.res + (i1 - s1), ldr, Q.R + i1 * K_in + i2,
+                  K_in, false, Q.Y + i2, K_in, false, s, "gptq_update", g_dgemm_tile);
+        if (e != hipSuccess) return hip_fail(e, "in-span update");
       }
     }
-    if (o2 < K_in) {
-      e = dgemm(K_out, K_in - o2, o2 - o1, 1.0, Q.res, ldr, Q.R + o1 * K_in + o2, K_in, false,
-                Q.Y + o2, K_in, false, s);
+    if (s2 < K_in) {
+      e = dgemm(K_out, K_in - s2, s2 - s1, 1.0, 1.0, Q.res, ldr, Q.R + s1 * K_in + s2, K_in, false,
+                Q.Y + s2, K_in, false, s, "gptq_update", g_dgemm_tile);
       if (e != hipSuccess) return hip_fail(e, "lazy update");
     }
   }

@@ -80,6 +80,7 @@ hipError_t q_stats(const float* D, int64_t rows, int64_t cols, double clip_sigma
                    QuantScratch& w, hipStream_t s);
 hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& w,
                          hipStream_t s);
+// Blocked lower Cholesky of A (K x K, in place).
 hipError_t q_cholesky(double* A, int64_t K, int* flags, hipStream_t s);
 hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rdiag,
                            hipStream_t s);
@@ -87,12 +88,13 @@ hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, Qua
                        float* scale, float* zero, hipStream_t s);
 hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int i2, int o1,
                         int64_t ld_res, int bits, QuantScratch& w, hipStream_t s);
-// C[M x N] += alpha * A[M x K] * op(B)   (fp64 MFMA)
+// C[M x N] = beta * C + alpha * A[M x K] * op(B)   (fp64 MFMA; beta is 0 or 1)
 //   b_trans: op(B)(k, n) = B[n * ldb + k]  else B[k * ldb + n]
 //   lower_only: only tiles with tile_row >= tile_col (for the Cholesky update)
-hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, const double* A, int64_t lda,
-                 const double* B, int64_t ldb, bool b_trans, double* C, int64_t ldc,
-                 bool lower_only, hipStream_t s);
+//   tile: 64 or 128 (work-group tile edge)
+hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, const double* A,
+                 int64_t lda, const double* B, int64_t ldb, bool b_trans, double* C, int64_t ldc,
+                 bool lower_only, hipStream_t s, const char* name, int tile);
 hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* out,
                    hipStream_t s);
 hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,

@@ -140,71 +140,134 @@ __global__ __launch_bounds__(256) void k_build_rev(const float* __restrict__ Ht,
 }
 
 // ------------------------------------------------------------------ Cholesky
-// Factor the kb x kb diagonal block at (k0, k0) in place (lower), one wave64: lane r
-// holds row r of the block (padded with identity rows beyond kb).
-__global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
-                                                int kb, int* flags) {
-  const int r = threadIdx.x;
-  double a[64];
-#pragma unroll
-  for (int c = 0; c < 64; ++c) {
-    double v = (r == c) ? 1.0 : 0.0;
-    if (r < kb && c < kb && c <= r) v = A[(k0 + r) * lda + k0 + c];
-    a[c] = v;
-  }
-  bool notpd = false;
-#pragma unroll
-  for (int c = 0; c < 64; ++c) {
-    double piv = bcast_lane(a[c], c);
+// 1 / sqrt(x) to full double precision: hardware estimate plus two Newton steps.
+__device__ __forceinline__ double rsqrt_d(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+  double h = 0.5 * x;
+  y = y * fma(-h * y, y, 1.5);
+  y = y * fma(-h * y, y, 1.5);
+  return y;
+}
+
+// One column of the in-register factorization (column index C is a compile-time
+// constant so that the row stays in registers).
+template <int C>
+__device__ __forceinline__ void potrf_cols(double (&a)[64], double (*col)[64], int r,
+                                           bool& notpd) {
+  if constexpr (C < 64) {
+    double piv = bcast_lane(a[C], C);
     if (!(piv > 0.0)) {
       notpd = true;
       piv = 1.0;
     }
-    const double d = sqrt(piv);
-    const double inv = 1.0 / d;
-    if (r > c) a[c] *= inv;
-    else if (r == c) a[c] = d;
-    const double lc = a[c];
+    const double inv = rsqrt_d(piv);
+    a[C] = (r == C) ? piv * inv : a[C] * inv;
+    col[C & 1][r] = a[C];
+    __syncthreads();               // one barrier per column: col is double-buffered
+    const double lc = a[C];
 #pragma unroll
-    for (int cc = c + 1; cc < 64; ++cc) {
-      const double l2 = bcast_lane(lc, cc);
-      if (r >= cc) a[cc] -= lc * l2;
+    for (int cc0 = (C + 1) & ~7; cc0 < 64; cc0 += 8) {
+      // the 8 broadcast values of a group are read together (4 x 16 bytes), then used
+      const double2* cp = reinterpret_cast<const double2*>(&col[C & 1][cc0]);
+      double2 v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = cp[q];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (cc0 + q > C) a[cc0 + q] -= lc * ((q & 1) ? v[q >> 1].y : v[q >> 1].x);
+      // pin the group's results here: without it the compiler sinks every update to the
+      // column's own step and keeps all broadcast values alive
+      asm volatile("" : "+v"(a[cc0]), "+v"(a[cc0 + 1]), "+v"(a[cc0 + 2]), "+v"(a[cc0 + 3]),
+                   "+v"(a[cc0 + 4]), "+v"(a[cc0 + 5]), "+v"(a[cc0 + 6]), "+v"(a[cc0 + 7]));
     }
+    potrf_cols<C + 1>(a, col, r, notpd);
   }
-  if (notpd && r == 0) flags[0] = 1;
-  if (r < kb) {
+}
+
+// Factor the kb x kb diagonal block at (k0, k0) in place (lower).  One wave64: lane r
+// holds row r of the block in registers, staged through LDS with zeros above the
+// diagonal (identity rows beyond kb); each finished column is broadcast through LDS.
+// Entries above the diagonal pick up finite values that are never written back, which
+// keeps the update loop free of per-lane masks.
+__global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
+                                                int kb, int* flags) {
+  __shared__ double Ls[64][65];
+  __shared__ __attribute__((aligned(16))) double col[2][64];
+  const int r = threadIdx.x;
+  // all 64 loads of a thread in flight at once (the block is read row by row, coalesced)
 #pragma unroll
-    for (int c = 0; c < 64; ++c)
-      if (c <= r && c < kb) A[(k0 + r) * lda + k0 + c] = a[c];
+  for (int i = 0; i < 64; ++i) {
+    double v = (i == r) ? 1.0 : 0.0;
+    if (i < kb && r <= i) v = A[(k0 + i) * lda + k0 + r];
+    Ls[i][r] = v;
+  }
+  __syncthreads();
+  double a[64];
+#pragma unroll
+  for (int c = 0; c < 64; ++c) a[c] = Ls[r][c];
+  bool notpd = false;
+  potrf_cols<0>(a, col, r, notpd);
+  if (notpd && r == 0) flags[0] = 1;
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < 64; ++c) Ls[r][c] = a[c];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 64; ++i)
+    if (i < kb && r <= i) A[(k0 + i) * lda + k0 + r] = Ls[i][r];
+}
+
+// Forward substitution of one panel row against L_kk (x L^T = a), column C of x.
+template <int C>
+__device__ __forceinline__ void trsm_cols(double (&x)[64], const double (*L)[66],
+                                          const double* invd) {
+  if constexpr (C < 64) {
+    double s0 = x[C], s1 = 0.0;
+#pragma unroll
+    for (int m0 = 0; m0 < C; m0 += 8) {
+      const double2* lp = reinterpret_cast<const double2*>(&L[C][m0]);
+      double2 v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = lp[q];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (m0 + q < C) {
+          const double l = (q & 1) ? v[q >> 1].y : v[q >> 1].x;
+          if (q & 1) s1 -= x[m0 + q] * l;
+          else s0 -= x[m0 + q] * l;
+        }
+    }
+    x[C] = (s0 + s1) * invd[C];
+    asm volatile("" : "+v"(x[C]));
+    trsm_cols<C + 1>(x, L, invd);
   }
 }
 
 // Panel below the diagonal block: rows i in [k0+kb, K), X = A[i, k0:k0+kb] L_kk^{-T}
-// (forward substitution, one row per thread; the rows and L_kk live in LDS).
-__global__ __launch_bounds__(64) void k_trsm64(double* __restrict__ A, int64_t lda, int64_t K,
-                                               int64_t k0, int kb) {
-  __shared__ double L[64][65];
-  __shared__ double X[64][65];
-  const int t = threadIdx.x;
-  const int64_t i0 = k0 + kb + (int64_t)blockIdx.x * 64;
-  for (int e = t; e < 64 * 64; e += 64) {
+// (forward substitution, one row per thread in registers; L_kk broadcast from LDS).
+__global__ __launch_bounds__(256) void k_trsm64(double* __restrict__ A, int64_t lda, int64_t K,
+                                                int64_t k0, int kb) {
+  __shared__ __attribute__((aligned(16))) double L[64][66];
+  __shared__ double invd[64];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    const int e = threadIdx.x + 256 * q;
     const int r = e >> 6, c = e & 63;
     L[r][c] = (r < kb && c < kb && c <= r) ? A[(k0 + r) * lda + k0 + c] : (r == c ? 1.0 : 0.0);
-    const int64_t gi = i0 + r;
-    X[r][c] = (gi < K && c < kb) ? A[gi * lda + k0 + c] : 0.0;
   }
   __syncthreads();
-  for (int c = 0; c < kb; ++c) {
-    double v = X[t][c];
-    for (int m = 0; m < c; ++m) v -= X[t][m] * L[c][m];
-    X[t][c] = v / L[c][c];
-  }
+  if (threadIdx.x < 64) invd[threadIdx.x] = 1.0 / L[threadIdx.x][threadIdx.x];
   __syncthreads();
-  for (int e = t; e < 64 * 64; e += 64) {
-    const int r = e >> 6, c = e & 63;
-    const int64_t gi = i0 + r;
-    if (gi < K && c < kb) A[gi * lda + k0 + c] = X[r][c];
-  }
+  const int64_t i = k0 + kb + (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= K) return;
+  double x[64];
+  double* row = A + i * lda + k0;
+#pragma unroll
+  for (int c = 0; c < 64; ++c) x[c] = (c < kb) ? row[c] : 0.0;
+  trsm_cols<0>(x, L, invd);
+#pragma unroll
+  for (int c = 0; c < 64; ++c)
+    if (c < kb) row[c] = x[c];
 }
 
 // R[i][j] = M[K-1-i][K-1-j] (upper), rdiag / inv_rdiag.
@@ -279,14 +342,88 @@ __global__ __launch_bounds__(256) void k_clip_grid(const float* __restrict__ D, 
 }
 
 // ------------------------------------------------------------------ rounding block
-// Columns [i1, i2) (at most 128) of every row.  512 threads = 8 waves; a wave is four
-// groups of 16 lanes; a group owns 2 rows and lane g of the group holds columns
-// 8g .. 8g+7 of the block for both rows.  Column j is decided by its owner lane, its
-// residual D_j - D^_j is broadcast to the group, and every lane folds it into its own
-// columns with the R row from LDS.
+// Columns [i1, i1 + b) (b <= 128) of every row.  512 threads = 8 waves; each wave is four
+// 16-lane DPP rows ("groups"); a group owns 2 rows of D and lane g of the group holds
+// columns 8g .. 8g+7 of the block for both rows.  At column j every lane evaluates the
+// rounding on its own copy of column j, the owner lane (g = j / 8) keeps the code and
+// the residual D_j - D^_j, the residual is broadcast inside the group with a DPP row
+// broadcast, and every lane folds it into its columns with row j of R (from LDS).
 constexpr int GB = 128;
-constexpr int GTH = 512;
-constexpr int GROWS = GTH / 16 * 2;   // 64 rows per work-group
+constexpr int GTH = 384;
+constexpr int GROWS = GTH / 16 * 2;   // 48 rows per work-group (253 groups for 12112 rows)
+
+template <int O>
+__device__ __forceinline__ double row_bcast(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xffffffffll), 0x150 + O, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), 0x150 + O, 0xf, 0xf, false);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+struct RoundState {
+  double y[2][8], d0[2][8], rr[2][8];
+  uint32_t q[2][2];            // the 8 codes of each row, one byte each
+  double s[2], is[2], z[2];
+};
+
+template <int O>
+__device__ __forceinline__ void round_owner_cols(RoundState& st, const double* __restrict__ Rs,
+                                                 const double* __restrict__ ird, int b, int g,
+                                                 double maxq) {
+  // the 8 inverse pivots of this group and the first R row are read ahead of use
+  double irv[8];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const double2 t = reinterpret_cast<const double2*>(ird + O * 8)[q];
+    irv[2 * q] = t.x;
+    irv[2 * q + 1] = t.y;
+  }
+  double2 rn[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) rn[q] = reinterpret_cast<const double2*>(Rs + (O * 8) * GB + g * 8)[q];
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) {
+    const int j = O * 8 + jj;
+    if (j >= b) return;
+    const double2 rc[4] = {rn[0], rn[1], rn[2], rn[3]};
+    if (jj + 1 < 8) {   // prefetch row j + 1 of R while column j is rounded
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        rn[q] = reinterpret_cast<const double2*>(Rs + (j + 1) * GB + g * 8)[q];
+    }
+    const double ir = irv[jj];
+    double e[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      // t = w / scale in code units; the code relative to the zero point is
+      // clamp(rne(t), -zero, maxq - zero) (the zero point is an integer)
+      const double t = st.y[k][jj] * (ir * st.is[k]);
+      const double qz = fmin(fmax(rint(t), -st.z[k]), maxq - st.z[k]);
+      const double ek = fma(-st.s[k], qz, st.d0[k][jj]);
+      if (g == O) {
+        st.rr[k][jj] = ek;
+        st.q[k][jj >> 2] |= (uint32_t)(qz + st.z[k]) << (8 * (jj & 3));
+      }
+      e[k] = row_bcast<O>(ek);
+    }
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) {
+      const double rv = (cc & 1) ? rc[cc >> 1].y : rc[cc >> 1].x;
+      st.y[0][cc] += e[0] * rv;
+      st.y[1][cc] += e[1] * rv;
+    }
+  }
+}
+
+template <int O>
+__device__ __forceinline__ void round_all(RoundState& st, const double* Rs, const double* ird,
+                                          int b, int g, double maxq) {
+  if constexpr (O < 16) {
+    if (O * 8 >= b) return;
+    round_owner_cols<O>(st, Rs, ird, b, g, maxq);
+    round_all<O + 1>(st, Rs, ird, b, g, maxq);
+  }
+}
 
 __global__ __launch_bounds__(GTH) void k_gptq_block(
     const float* __restrict__ D, int64_t rows, int64_t cols, int i1, int b, int64_t res_col0,
@@ -294,77 +431,43 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     const double* __restrict__ R, const double* __restrict__ inv_rdiag,
     const double* __restrict__ scale64, const double* __restrict__ zero64,
     const double* __restrict__ Y, uint8_t* __restrict__ codes8, double* __restrict__ res) {
-  __shared__ double Rs[GB * GB];
+  __shared__ __attribute__((aligned(16))) double Rs[GB * GB];
+  __shared__ __attribute__((aligned(16))) double ird[GB];
   for (int e = threadIdx.x; e < GB * GB; e += GTH) {
     const int rr = e / GB, cc = e % GB;
     Rs[e] = (rr < b && cc < b) ? R[(int64_t)(i1 + rr) * cols + i1 + cc] : 0.0;
   }
-  __shared__ double ird[GB];
   if (threadIdx.x < GB) ird[threadIdx.x] = threadIdx.x < b ? inv_rdiag[i1 + threadIdx.x] : 0.0;
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  const int g = lane & 15;                         // position inside the group
-  const int grp = (threadIdx.x >> 4);              // group index in the work-group
-  const int gbase = lane & ~15;                    // first lane of the group
+  const int g = lane & 15;                         // position inside the 16-lane group
+  const int grp = threadIdx.x >> 4;                // group index in the work-group
   const int64_t r0 = (int64_t)blockIdx.x * GROWS + grp * 2;
   const double lo_b = scal[2], hi_b = scal[3];
 
-  double y[2][8], d0[2][8], rr_[2][8];
-  uint8_t q8[2][8];
-  double s[2], is[2], z[2];
+  RoundState st;
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const int64_t r = r0 + k;
     const bool ok = r < rows;
-    s[k] = ok ? scale64[r] : 1.0;
-    is[k] = 1.0 / s[k];
-    z[k] = ok ? zero64[r] : 0.0;
+    st.s[k] = ok ? scale64[r] : 1.0;
+    st.is[k] = 1.0 / st.s[k];
+    st.z[k] = ok ? zero64[r] : 0.0;
+    st.q[k][0] = st.q[k][1] = 0;
 #pragma unroll
     for (int cc = 0; cc < 8; ++cc) {
       const int c = g * 8 + cc;
       const bool in = ok && c < b;
-      y[k][cc] = in ? Y[r * cols + i1 + c] : 0.0;
+      st.y[k][cc] = in ? Y[r * cols + i1 + c] : 0.0;
       double x = 0.0;
       if (in && !dead[i1 + c]) x = fmin(fmax((double)D[r * cols + i1 + c], lo_b), hi_b);
-      d0[k][cc] = x;
-      rr_[k][cc] = 0.0;
-      q8[k][cc] = 0;
+      st.d0[k][cc] = x;
+      st.rr[k][cc] = 0.0;
     }
   }
 
-  for (int o = 0; o < 16; ++o) {
-    if (o * 8 >= b) break;
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      const int j = o * 8 + jj;
-      if (j >= b) break;
-      double res_own[2] = {0.0, 0.0};
-      if (g == o) {
-        const double ir = ird[j];
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          const double w = y[k][jj] * ir;
-          const double t = w * is[k];
-          const double q = fmin(fmax(rint(t) + z[k], 0.0), (double)maxq);
-          const double dq = s[k] * (q - z[k]);
-          const double e = d0[k][jj] - dq;
-          res_own[k] = e;
-          rr_[k][jj] = e;
-          q8[k][jj] = (uint8_t)q;
-        }
-      }
-      const double e0 = shfl_d(res_own[0], gbase + o);
-      const double e1 = shfl_d(res_own[1], gbase + o);
-      const double* Rrow = Rs + j * GB + g * 8;
-#pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-        const double rv = Rrow[cc];
-        y[0][cc] += e0 * rv;
-        y[1][cc] += e1 * rv;
-      }
-    }
-  }
+  round_all<0>(st, Rs, ird, b, g, (double)maxq);
 
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
@@ -374,89 +477,145 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     for (int cc = 0; cc < 8; ++cc) {
       const int c = g * 8 + cc;
       if (c < b) {
-        codes8[r * cols + i1 + c] = q8[k][cc];
-        res[r * ld_res + res_col0 + c] = rr_[k][cc];
+        codes8[r * cols + i1 + c] = (uint8_t)(st.q[k][cc >> 2] >> (8 * (cc & 3)));
+        res[r * ld_res + res_col0 + c] = st.rr[k][cc];
       }
     }
   }
 }
 
 // ------------------------------------------------------------------ fp64 MFMA GEMM
-// C[M x N] += alpha * A[M x K] * op(B).  Tile 64 x 64, K step 16, 256 threads (2 x 2
-// waves of 32 x 32, each 2 x 2 v_mfma_f64_16x16x4 blocks).
-constexpr int DT = 64, DK = 16;
+// C[M x N] = beta * C + alpha * A[M x K] * op(B).  Tile 128 x 128, K step 16, 256
+// threads = 2 x 2 waves of 64 x 64 (4 x 4 v_mfma_f64_16x16x4 blocks each).  Operands are
+// staged k-major in LDS ([k][m], [k][n]) and the next K step is fetched into registers
+// while the current one is multiplied.  A and C may alias when every tile reads only
+// the rows it writes (the in-place triangular solve of the Cholesky panel).
+constexpr int DK = 16, DPAD = 4;
 
-__global__ __launch_bounds__(256) void k_dgemm(int64_t M, int64_t N, int64_t K, double alpha,
-                                               const double* __restrict__ A, int64_t lda,
-                                               const double* __restrict__ B, int64_t ldb,
-                                               int b_trans, double* __restrict__ C, int64_t ldc,
-                                               int lower_only, int tiles_n) {
-  __shared__ double As[DT][DK + 1];
-  __shared__ double Bs[DK][DT + 1];
+struct DgemmArgs {
+  int64_t M, N, K;
+  double alpha, beta;
+  const double* A; int64_t lda;
+  const double* B; int64_t ldb;
+  double* C; int64_t ldc;
+  int b_trans, lower_only, tiles_n;
+};
+
+// Tile DT x DT with 256 threads; each wave owns a (DT/2) x (DT/2) quarter built from
+// WT x WT blocks of 16 x 16 (WT = DT / 32).
+template <int DT>
+__device__ __forceinline__ void dg_load(const DgemmArgs& p, int64_t m0, int64_t n0, int64_t k0,
+                                        double (&ra)[DT / 16], double (&rb)[DT / 16], int tid) {
+  constexpr int PER = DT / 16;             // doubles per thread per operand
+  constexpr int TPR = 16 / PER;            // threads per 16-wide k row
+  {  // A: row m0 + tid / TPR, k0 + PER * (tid % TPR)
+    const int64_t gm = m0 + tid / TPR;
+    const int64_t gk = k0 + PER * (tid % TPR);
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+      ra[q] = (gm < p.M && gk + q < p.K) ? p.A[gm * p.lda + gk + q] : 0.0;
+  }
+  if (p.b_trans) {  // op(B)(k, n) = B[n * ldb + k]
+    const int64_t gn = n0 + tid / TPR;
+    const int64_t gk = k0 + PER * (tid % TPR);
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+      rb[q] = (gn < p.N && gk + q < p.K) ? p.B[gn * p.ldb + gk + q] : 0.0;
+  } else {          // B[k * ldb + n]: row k0 + tid / (DT / PER), n0 + PER * (tid % (DT / PER))
+    constexpr int TPN = DT / PER;
+    const int64_t gk = k0 + tid / TPN;
+    const int64_t gn = n0 + PER * (tid % TPN);
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+      rb[q] = (gk < p.K && gn + q < p.N) ? p.B[gk * p.ldb + gn + q] : 0.0;
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void dg_store(const DgemmArgs& p, double (*As)[DT + DPAD],
+                                         double (*Bs)[DT + DPAD], const double (&ra)[DT / 16],
+                                         const double (&rb)[DT / 16], int tid) {
+  constexpr int PER = DT / 16;
+  constexpr int TPR = 16 / PER;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) As[PER * (tid % TPR) + q][tid / TPR] = ra[q];
+  if (p.b_trans) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) Bs[PER * (tid % TPR) + q][tid / TPR] = rb[q];
+  } else {
+    constexpr int TPN = DT / PER;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) Bs[tid / TPN][PER * (tid % TPN) + q] = rb[q];
+  }
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_dgemm(DgemmArgs p) {
+  constexpr int WT = DT / 32;
+  __shared__ double As[2][DK][DT + DPAD];
+  __shared__ double Bs[2][DK][DT + DPAD];
   int tm, tn;
-  if (lower_only) {
+  if (p.lower_only) {
     int t = blockIdx.x, row = 0;
     while (t > row) { t -= row + 1; ++row; }
     tm = row;
     tn = t;
   } else {
-    tm = blockIdx.x / tiles_n;
-    tn = blockIdx.x - tm * tiles_n;
+    tm = blockIdx.x / p.tiles_n;
+    tn = blockIdx.x - tm * p.tiles_n;
   }
   const int64_t m0 = (int64_t)tm * DT, n0 = (int64_t)tn * DT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  doublex4 acc[2][2];
+  doublex4 acc[WT][WT];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < WT; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = (doublex4){0.0, 0.0, 0.0, 0.0};
+    for (int j = 0; j < WT; ++j) acc[i][j] = (doublex4){0.0, 0.0, 0.0, 0.0};
 
-  for (int64_t k0 = 0; k0 < K; k0 += DK) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + q * 256;
-      {  // A tile: 64 rows x 16 k, row-major
-        const int r = e >> 4, c = e & 15;
-        const int64_t gm = m0 + r, gk = k0 + c;
-        As[r][c] = (gm < M && gk < K) ? A[gm * lda + gk] : 0.0;
-      }
-      if (b_trans) {  // op(B)(k, n) = B[n * ldb + k]
-        const int n = e >> 4, c = e & 15;
-        const int64_t gn = n0 + n, gk = k0 + c;
-        Bs[c][n] = (gn < N && gk < K) ? B[gn * ldb + gk] : 0.0;
-      } else {        // B[k * ldb + n]
-        const int c = e >> 6, n = e & 63;
-        const int64_t gn = n0 + n, gk = k0 + c;
-        Bs[c][n] = (gn < N && gk < K) ? B[gk * ldb + gn] : 0.0;
-      }
-    }
-    __syncthreads();
+  double ra[DT / 16], rb[DT / 16];
+  const int nk = (int)((p.K + DK - 1) / DK);
+  if (nk > 0) {
+    dg_load<DT>(p, m0, n0, 0, ra, rb, tid);
+    dg_store<DT>(p, As[0], Bs[0], ra, rb, tid);
+  }
+  __syncthreads();
+  for (int s = 0; s < nk; ++s) {
+    const int buf = s & 1;
+    const bool more = s + 1 < nk;
+    if (more) dg_load<DT>(p, m0, n0, (int64_t)(s + 1) * DK, ra, rb, tid);
 #pragma unroll
     for (int kk = 0; kk < DK; kk += 4) {
-      double af[2], bfv[2];
+      double af[WT], bfv[WT];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) af[i] = As[wm * 32 + i * 16 + (lane & 15)][kk + (lane >> 4)];
+      for (int i = 0; i < WT; ++i)
+        af[i] = As[buf][kk + (lane >> 4)][wm * (DT / 2) + i * 16 + (lane & 15)];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bfv[j] = Bs[kk + (lane >> 4)][wn * 32 + j * 16 + (lane & 15)];
+      for (int j = 0; j < WT; ++j)
+        bfv[j] = Bs[buf][kk + (lane >> 4)][wn * (DT / 2) + j * 16 + (lane & 15)];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < WT; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WT; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
     }
+    if (more) dg_store<DT>(p, As[buf ^ 1], Bs[buf ^ 1], ra, rb, tid);
     __syncthreads();
   }
   // 16x16 f64 accumulator layout: value v of lane l is row l/16 + 4*v, column l%16.
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < WT; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < WT; ++j)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int64_t row = m0 + wm * 32 + i * 16 + (lane >> 4) + 4 * v;
-        const int64_t col = n0 + wn * 32 + j * 16 + (lane & 15);
-        if (row < M && col < N) C[row * ldc + col] += alpha * acc[i][j][v];
+        const int64_t row = m0 + wm * (DT / 2) + i * 16 + (lane >> 4) + 4 * v;
+        const int64_t col = n0 + wn * (DT / 2) + j * 16 + (lane & 15);
+        if (row < p.M && col < p.N) {
+          double* c = p.C + row * p.ldc + col;
+          const double x = p.alpha * acc[i][j][v];
+          *c = (p.beta == 0.0) ? x : p.beta * *c + x;
+        }
       }
 }
 
@@ -550,11 +709,12 @@ hipError_t q_cholesky(double* A, int64_t K, int* flags, hipStream_t s) {
     const int64_t rest = K - k0 - kb;
     if (rest > 0) {
       prof_begin(s, "chol_trsm");
-      hipLaunchKernelGGL(k_trsm64, dim3(grid_for(rest, 64, 1 << 30)), dim3(64), 0, s, A, K, K, k0, kb);
+      hipLaunchKernelGGL(k_trsm64, dim3(grid_for(rest, 256, 1 << 30)), dim3(256), 0, s, A, K, K,
+                         k0, kb);
       prof_end(s);
       const double* P = A + (k0 + kb) * K + k0;
-      hipError_t e = dgemm(rest, rest, kb, -1.0, P, K, P, K, true, A + (k0 + kb) * K + (k0 + kb),
-                           K, true, s);
+      hipError_t e = dgemm(rest, rest, kb, -1.0, 1.0, P, K, P, K, true,
+                           A + (k0 + kb) * K + (k0 + kb), K, true, s, "chol_syrk", 64);
       if (e != hipSuccess) return e;
     }
   }
@@ -592,15 +752,23 @@ hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int 
   return last_launch_error();
 }
 
-hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, const double* A, int64_t lda,
-                 const double* B, int64_t ldb, bool b_trans, double* C, int64_t ldc,
-                 bool lower_only, hipStream_t s) {
-  if (M <= 0 || N <= 0 || K <= 0) return hipSuccess;
+hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, const double* A,
+                 int64_t lda, const double* B, int64_t ldb, bool b_trans, double* C, int64_t ldc,
+                 bool lower_only, hipStream_t s, const char* name, int tile) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  DgemmArgs p;
+  p.M = M; p.N = N; p.K = K < 0 ? 0 : K;
+  p.alpha = alpha; p.beta = beta;
+  p.A = A; p.lda = lda; p.B = B; p.ldb = ldb; p.C = C; p.ldc = ldc;
+  p.b_trans = (int)b_trans;
+  p.lower_only = (int)lower_only;
+  const int DT = tile == 128 ? 128 : 64;
   const int tiles_m = (int)((M + DT - 1) / DT), tiles_n = (int)((N + DT - 1) / DT);
+  p.tiles_n = tiles_n;
   const int64_t grid = lower_only ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
-  prof_begin(s, lower_only ? "chol_syrk" : "gptq_update");
-  hipLaunchKernelGGL(k_dgemm, dim3((unsigned)grid), dim3(256), 0, s, M, N, K, alpha, A, lda, B,
-                     ldb, (int)b_trans, C, ldc, (int)lower_only, tiles_n);
+  prof_begin(s, name);
+  if (DT == 128) hipLaunchKernelGGL(k_dgemm<128>, dim3((unsigned)grid), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL(k_dgemm<64>, dim3((unsigned)grid), dim3(256), 0, s, p);
   prof_end(s);
   return last_launch_error();
 }
