@@ -119,32 +119,36 @@ static size_t hessian_layout(int xt, int64_t n, int64_t d, void* ws, HessLayout*
   return c.off + 256;
 }
 
+static int64_t rup32(int64_t x) { return (x + 31) / 32 * 32; }
+
+// Operand planes of the analysis, every one stored K-contiguous and zero-padded in K to a
+// multiple of 32 (the layout the asynchronous MFMA kernel reads):
+//   pot  = P_out^T  [K_out x pad(d_out)]    wt = W^T  [d_in x pad(d_out)]
+//   t    = P_out^T W [K_out x pad(d_in)]    pit = P_in^T [K_in x pad(d_in)]
+//   h    = H [d_in x pad(d_in)]             gt = P_in^T H [K_in x pad(d_in)]
 struct AnaLayout {
-  u16 *po_hi, *po_lo, *pi_hi, *pi_lo, *w_hi, *w_lo, *t_hi, *t_lo, *h_hi, *h_lo, *g_hi, *g_lo;
-  int64_t ldko, ldki, ldi;
+  u16 *pot_hi, *pot_lo, *pit_hi, *pit_lo, *wt_hi, *wt_lo, *t_hi, *t_lo, *h_hi, *h_lo, *gt_hi, *gt_lo;
+  int64_t lo_, li_;   // pad(d_out), pad(d_in)
 };
 
 static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out, int64_t K_in,
                               void* ws, AnaLayout* L) {
   Carver c(ws);
   AnaLayout l{};
-  l.ldko = rup8(K_out);
-  l.ldki = rup8(K_in);
-  l.ldi = rup8(d_in);
-  l.po_hi = c.take<u16>((size_t)d_out * l.ldko);
-  l.po_lo = c.take<u16>((size_t)d_out * l.ldko);
-  l.pi_hi = c.take<u16>((size_t)d_in * l.ldki);
-  l.pi_lo = c.take<u16>((size_t)d_in * l.ldki);
-  if (wt != FQ_BF16) {
-    l.w_hi = c.take<u16>((size_t)d_out * l.ldi);
-    l.w_lo = c.take<u16>((size_t)d_out * l.ldi);
-  }
-  l.t_hi = c.take<u16>((size_t)K_out * l.ldi);
-  l.t_lo = c.take<u16>((size_t)K_out * l.ldi);
-  l.h_hi = c.take<u16>((size_t)d_in * l.ldi);
-  l.h_lo = c.take<u16>((size_t)d_in * l.ldi);
-  l.g_hi = c.take<u16>((size_t)d_in * l.ldki);
-  l.g_lo = c.take<u16>((size_t)d_in * l.ldki);
+  l.lo_ = rup32(d_out);
+  l.li_ = rup32(d_in);
+  l.pot_hi = c.take<u16>((size_t)K_out * l.lo_);
+  l.pot_lo = c.take<u16>((size_t)K_out * l.lo_);
+  l.pit_hi = c.take<u16>((size_t)K_in * l.li_);
+  l.pit_lo = c.take<u16>((size_t)K_in * l.li_);
+  l.wt_hi = c.take<u16>((size_t)d_in * l.lo_);
+  if (wt != FQ_BF16) l.wt_lo = c.take<u16>((size_t)d_in * l.lo_);
+  l.t_hi = c.take<u16>((size_t)K_out * l.li_);
+  l.t_lo = c.take<u16>((size_t)K_out * l.li_);
+  l.h_hi = c.take<u16>((size_t)d_in * l.li_);
+  l.h_lo = c.take<u16>((size_t)d_in * l.li_);
+  l.gt_hi = c.take<u16>((size_t)K_in * l.li_);
+  l.gt_lo = c.take<u16>((size_t)K_in * l.li_);
   if (L) *L = l;
   return c.off + 256;
 }
@@ -183,24 +187,27 @@ static size_t quant_layout(int64_t K_out, int64_t K_in, int block, void* ws, Qua
   return c.off + 256;
 }
 
+// Synthesis planes (K-contiguous, zero-padded in K):
+//   qt  = (codes - zero)^T [K_in x pad(K_out)]   pl = P_out diag(scale) [d_out x pad(K_out)]
+//   n   = pl (codes - zero) [d_out x pad(K_in)]  pi = P_in [d_in x pad(K_in)]
 struct SynLayout {
-  u16 *q, *pl_hi, *pl_lo, *pi_hi, *pi_lo, *n_hi, *n_lo;
-  int64_t ldko, ldki;
+  u16 *qt, *pl_hi, *pl_lo, *pi_hi, *pi_lo, *n_hi, *n_lo;
+  int64_t ko, ki;   // pad(K_out), pad(K_in)
 };
 
 static size_t synthesis_layout(int64_t K_out, int64_t K_in, int64_t d_out, int64_t d_in,
                                void* ws, SynLayout* L) {
   Carver c(ws);
   SynLayout l{};
-  l.ldko = rup8(K_out);
-  l.ldki = rup8(K_in);
-  l.q = c.take<u16>((size_t)K_out * l.ldki);
-  l.pl_hi = c.take<u16>((size_t)d_out * l.ldko);
-  l.pl_lo = c.take<u16>((size_t)d_out * l.ldko);
-  l.pi_hi = c.take<u16>((size_t)d_in * l.ldki);
-  l.pi_lo = c.take<u16>((size_t)d_in * l.ldki);
-  l.n_hi = c.take<u16>((size_t)d_out * l.ldki);
-  l.n_lo = c.take<u16>((size_t)d_out * l.ldki);
+  l.ko = rup32(K_out);
+  l.ki = rup32(K_in);
+  l.qt = c.take<u16>((size_t)K_in * l.ko);
+  l.pl_hi = c.take<u16>((size_t)d_out * l.ko);
+  l.pl_lo = c.take<u16>((size_t)d_out * l.ko);
+  l.pi_hi = c.take<u16>((size_t)d_in * l.ki);
+  l.pi_lo = c.take<u16>((size_t)d_in * l.ki);
+  l.n_hi = c.take<u16>((size_t)d_out * l.ki);
+  l.n_lo = c.take<u16>((size_t)d_out * l.ki);
   if (L) *L = l;
   return c.off + 256;
 }
@@ -338,8 +345,12 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
   AnaLayout L;
   analysis_layout(wt, d_out, d_in, K_out, K_in, base, &L);
   hipError_t e;
+  auto three = [](GemmDesc& g) {
+    g.npass = 3;
+    g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
+  };
   if (d_in > 0 && K_in > 0) {
-    e = split_bf16(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ldki, s);
+    e = split_bf16_t(P_in, 0, K_in, (int)d_in, (int)K_in, L.pit_hi, L.pit_lo, L.li_, s);
     if (e != hipSuccess) return hip_fail(e, "split P_in");
   }
   if (D && K_out > 0 && K_in > 0) {
@@ -347,45 +358,34 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       e = fill_zero_f32(D, (int)K_out, (int)K_in, K_in, s);
       if (e != hipSuccess) return hip_fail(e, "zero D");
     } else {
-      e = split_bf16(P_out, 0, K_out, (int)d_out, (int)K_out, nullptr, L.po_hi, L.po_lo, L.ldko, s);
+      e = split_bf16_t(P_out, 0, K_out, (int)d_out, (int)K_out, L.pot_hi, L.pot_lo, L.lo_, s);
       if (e != hipSuccess) return hip_fail(e, "split P_out");
-      const u16* w0;
-      const u16* w1 = nullptr;
-      int64_t ldw;
-      if (wt == FQ_BF16) {
-        w0 = (const u16*)W;
-        ldw = d_in;
-      } else {
-        e = split_bf16(W, wt == FQ_F16 ? 1 : 0, d_in, (int)d_out, (int)d_in, nullptr, L.w_hi,
-                       L.w_lo, L.ldi, s);
-        if (e != hipSuccess) return hip_fail(e, "split W");
-        w0 = L.w_hi;
-        w1 = L.w_lo;
-        ldw = L.ldi;
-      }
+      // W^T: bf16 weights are exact in one plane; f16/f32 weights take a bf16 pair
+      const int in_t = wt == FQ_BF16 ? 2 : (wt == FQ_F16 ? 1 : 0);
+      e = split_bf16_t(W, in_t, d_in, (int)d_out, (int)d_in, L.wt_hi, wt == FQ_BF16 ? nullptr : L.wt_lo,
+                       L.lo_, s);
+      if (e != hipSuccess) return hip_fail(e, "split W");
       // T = P_out^T W  (K_out x d_in), emitted as a bf16 pair
       GemmDesc g;
-      g.M = (int)K_out; g.N = (int)d_in; g.K = (int)d_out;
-      g.a[0] = L.po_hi; g.a[1] = L.po_lo; g.lda = L.ldko; g.a_kmajor = false;
-      g.b[0] = w0; g.b[1] = w1; g.ldb = ldw; g.b_kmajor = false;
-      if (w1) {
-        g.npass = 3;
-        g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
+      g.M = (int)K_out; g.N = (int)d_in; g.K = (int)L.lo_;
+      g.a[0] = L.pot_hi; g.a[1] = L.pot_lo; g.lda = L.lo_; g.a_kmajor = true;
+      g.b[0] = L.wt_hi; g.b[1] = L.wt_lo; g.ldb = L.lo_; g.b_kmajor = true;
+      if (wt != FQ_BF16) {
+        three(g);
       } else {
         g.npass = 2;
         g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
       }
-      g.epi = EPI_SPLIT; g.c_hi = L.t_hi; g.c_lo = L.t_lo; g.ldc = L.ldi;
+      g.epi = EPI_SPLIT; g.c_hi = L.t_hi; g.c_lo = L.t_lo; g.ldc = L.li_; g.ldc_pad = L.li_;
       g.name = "gemm_analysis_w1";
       e = gemm_run(g, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 1");
       // D = T P_in  (K_out x K_in)
       GemmDesc g2;
-      g2.M = (int)K_out; g2.N = (int)K_in; g2.K = (int)d_in;
-      g2.a[0] = L.t_hi; g2.a[1] = L.t_lo; g2.lda = L.ldi; g2.a_kmajor = true;
-      g2.b[0] = L.pi_hi; g2.b[1] = L.pi_lo; g2.ldb = L.ldki; g2.b_kmajor = false;
-      g2.npass = 3;
-      g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
+      g2.M = (int)K_out; g2.N = (int)K_in; g2.K = (int)L.li_;
+      g2.a[0] = L.t_hi; g2.a[1] = L.t_lo; g2.lda = L.li_; g2.a_kmajor = true;
+      g2.b[0] = L.pit_hi; g2.b[1] = L.pit_lo; g2.ldb = L.li_; g2.b_kmajor = true;
+      three(g2);
       g2.epi = EPI_F32; g2.c = D; g2.ldc = K_in;
       g2.name = "gemm_analysis_w2";
       e = gemm_run(g2, nullptr, s);
@@ -397,26 +397,24 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       e = fill_zero_f32(Ht, (int)K_in, (int)K_in, K_in, s);
       if (e != hipSuccess) return hip_fail(e, "zero Ht");
     } else {
-      e = split_bf16(H, 0, d_in, (int)d_in, (int)d_in, nullptr, L.h_hi, L.h_lo, L.ldi, s);
+      e = split_bf16_pad(H, 0, d_in, (int)d_in, (int)d_in, nullptr, L.h_hi, L.h_lo, L.li_, s);
       if (e != hipSuccess) return hip_fail(e, "split H");
-      // G = H P_in  (d_in x K_in)
+      // G^T = P_in^T H  (K_in x d_in; H is symmetric, so row i of H is column i)
       GemmDesc g;
-      g.M = (int)d_in; g.N = (int)K_in; g.K = (int)d_in;
-      g.a[0] = L.h_hi; g.a[1] = L.h_lo; g.lda = L.ldi; g.a_kmajor = true;
-      g.b[0] = L.pi_hi; g.b[1] = L.pi_lo; g.ldb = L.ldki; g.b_kmajor = false;
-      g.npass = 3;
-      g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
-      g.epi = EPI_SPLIT; g.c_hi = L.g_hi; g.c_lo = L.g_lo; g.ldc = L.ldki;
+      g.M = (int)K_in; g.N = (int)d_in; g.K = (int)L.li_;
+      g.a[0] = L.pit_hi; g.a[1] = L.pit_lo; g.lda = L.li_; g.a_kmajor = true;
+      g.b[0] = L.h_hi; g.b[1] = L.h_lo; g.ldb = L.li_; g.b_kmajor = true;
+      three(g);
+      g.epi = EPI_SPLIT; g.c_hi = L.gt_hi; g.c_lo = L.gt_lo; g.ldc = L.li_; g.ldc_pad = L.li_;
       g.name = "gemm_analysis_h1";
       e = gemm_run(g, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 3");
       // Ht = P_in^T G  (K_in x K_in, upper tiles mirrored)
       GemmDesc g2;
-      g2.M = (int)K_in; g2.N = (int)K_in; g2.K = (int)d_in;
-      g2.a[0] = L.pi_hi; g2.a[1] = L.pi_lo; g2.lda = L.ldki; g2.a_kmajor = false;
-      g2.b[0] = L.g_hi; g2.b[1] = L.g_lo; g2.ldb = L.ldki; g2.b_kmajor = false;
-      g2.npass = 3;
-      g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
+      g2.M = (int)K_in; g2.N = (int)K_in; g2.K = (int)L.li_;
+      g2.a[0] = L.pit_hi; g2.a[1] = L.pit_lo; g2.lda = L.li_; g2.a_kmajor = true;
+      g2.b[0] = L.gt_hi; g2.b[1] = L.gt_lo; g2.ldb = L.li_; g2.b_kmajor = true;
+      three(g2);
       g2.epi = EPI_SYM; g2.c = Ht; g2.ldc = K_in;
       g2.name = "gemm_analysis_h2";
       e = gemm_run(g2, nullptr, s);
@@ -519,26 +517,26 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
   SynLayout L;
   synthesis_layout(K_out, K_in, d_out, d_in, base, &L);
-  if ((e = dequant_bf16(codes, zero, K_out, K_in, L.q, L.ldki, s)) != hipSuccess) return hip_fail(e, "dequant");
-  if ((e = split_bf16(P_out, 0, K_out, (int)d_out, (int)K_out, scale, L.pl_hi, L.pl_lo, L.ldko, s)) != hipSuccess)
+  if ((e = dequant_bf16_t(codes, zero, K_out, K_in, L.qt, L.ko, s)) != hipSuccess) return hip_fail(e, "dequant");
+  if ((e = split_bf16_pad(P_out, 0, K_out, (int)d_out, (int)K_out, scale, L.pl_hi, L.pl_lo, L.ko, s)) != hipSuccess)
     return hip_fail(e, "split P_out");
-  if ((e = split_bf16(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ldki, s)) != hipSuccess)
+  if ((e = split_bf16_pad(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ki, s)) != hipSuccess)
     return hip_fail(e, "split P_in");
   // N = (P_out diag(scale)) (codes - zero)   (d_out x K_in), bf16 pair
   GemmDesc g;
-  g.M = (int)d_out; g.N = (int)K_in; g.K = (int)K_out;
-  g.a[0] = L.pl_hi; g.a[1] = L.pl_lo; g.lda = L.ldko; g.a_kmajor = true;
-  g.b[0] = L.q; g.ldb = L.ldki; g.b_kmajor = false;
+  g.M = (int)d_out; g.N = (int)K_in; g.K = (int)L.ko;
+  g.a[0] = L.pl_hi; g.a[1] = L.pl_lo; g.lda = L.ko; g.a_kmajor = true;
+  g.b[0] = L.qt; g.ldb = L.ko; g.b_kmajor = true;
   g.npass = 2;
   g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
-  g.epi = EPI_SPLIT; g.c_hi = L.n_hi; g.c_lo = L.n_lo; g.ldc = L.ldki;
+  g.epi = EPI_SPLIT; g.c_hi = L.n_hi; g.c_lo = L.n_lo; g.ldc = L.ki; g.ldc_pad = L.ki;
   g.name = "gemm_synthesis_1";
   if ((e = gemm_run(g, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 1");
   // W_hat = N P_in^T  (d_out x d_in)
   GemmDesc g2;
-  g2.M = (int)d_out; g2.N = (int)d_in; g2.K = (int)K_in;
-  g2.a[0] = L.n_hi; g2.a[1] = L.n_lo; g2.lda = L.ldki; g2.a_kmajor = true;
-  g2.b[0] = L.pi_hi; g2.b[1] = L.pi_lo; g2.ldb = L.ldki; g2.b_kmajor = true;
+  g2.M = (int)d_out; g2.N = (int)d_in; g2.K = (int)L.ki;
+  g2.a[0] = L.n_hi; g2.a[1] = L.n_lo; g2.lda = L.ki; g2.a_kmajor = true;
+  g2.b[0] = L.pi_hi; g2.b[1] = L.pi_lo; g2.ldb = L.ki; g2.b_kmajor = true;
   g2.npass = 3;
   g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
   g2.epi = EPI_F32; g2.c = W_hat; g2.ldc = d_in;

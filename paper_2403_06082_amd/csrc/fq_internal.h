@@ -44,6 +44,7 @@ struct GemmDesc {
   u16* c_lo = nullptr;
   int ksplit = 1;                // EPI_PARTIAL only
   const char* name = "gemm";     // kernel-timer label
+  int64_t ldc_pad = 0;           // EPI_SPLIT: output columns [N, ldc_pad) are zeroed
 };
 
 // Workspace bytes needed by EPI_PARTIAL for an N x N symmetric product split ksplit ways.
@@ -58,6 +59,14 @@ hipError_t syrk_reduce(const float* partial, int N, int ksplit, float* H, int64_
 // (applied in fp32 before the split).  Element type: 0 = f32, 1 = f16.
 hipError_t split_bf16(const void* in, int in_type, int64_t ld_in, int rows, int cols,
                       const float* col_scale, u16* hi, u16* lo, int64_t ld_out, hipStream_t s);
+// Same with zero padding: out has ld_out >= cols columns, [cols, ld_out) are 0.
+// Element type 2 = bf16.
+hipError_t split_bf16_pad(const void* in, int in_type, int64_t ld_in, int rows, int cols,
+                          const float* col_scale, u16* hi, u16* lo, int64_t ld_out,
+                          hipStream_t s);
+// Transposing split: out[c * ld_out + r] for r < rows, zero for rows <= r < ld_out.
+hipError_t split_bf16_t(const void* in, int in_type, int64_t ld_in, int rows, int cols, u16* hi,
+                        u16* lo, int64_t ld_out, hipStream_t s);
 hipError_t fill_zero_f32(float* p, int rows, int cols, int64_t ld, hipStream_t s);
 
 // ---------------------------------------------------------------- fp64 path
@@ -99,5 +108,9 @@ hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* 
                    hipStream_t s);
 hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
                         u16* out, int64_t ld_out, hipStream_t s);
+// Transposed dequantization: out[c * ld_out + r] = code[r][c] - zero[r] (bf16), zero for
+// rows <= r < ld_out.
+hipError_t dequant_bf16_t(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
+                          u16* out, int64_t ld_out, hipStream_t s);
 
 }  // namespace fq

@@ -215,6 +215,57 @@ __device__ __forceinline__ void tile_coords(const KParams& p, bool sym, int& spl
   }
 }
 
+// Byte offsets, fixed for the whole tile, of a thread's global loads relative to the
+// stage base (operand origin of the tile at the stage's first k), of its LDS stores and
+// of its MFMA fragment reads.
+template <bool KM>
+__device__ __forceinline__ void load_offsets(int64_t ld, uint32_t (&g)[8], uint32_t (&st)[8],
+                                             int tid) {
+  if (KM) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + NT * i;
+      const int row = c >> 3, kc = c & 7;
+      g[i] = (uint32_t)(((int64_t)row * ld + kc * 8) * 2);
+      st[i] = (uint32_t)((row * BK + ((kc ^ swz(row)) << 3)) * 2);
+    }
+  } else {
+    const int kb = tid >> 5, mb = tid & 31;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      g[i] = (uint32_t)(((int64_t)(kb * 8 + i) * ld + mb * 8) * 2);
+      const int row = mb * 8 + i;   // store row of output vector i after the transpose
+      st[i] = (uint32_t)((row * BK + ((kb ^ swz(row)) << 3)) * 2);
+    }
+  }
+}
+
+__device__ __forceinline__ void fast_load(const char* base, const uint32_t (&g)[8], uint4 (&r)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = *reinterpret_cast<const uint4*>(base + g[i]);
+}
+
+template <bool KM>
+__device__ __forceinline__ void fast_store(char* sm, const uint32_t (&st)[8], const uint4 (&r)[8]) {
+  if (KM) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint4*>(sm + st[i]) = r[i];
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      uint32_t o[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const uint32_t lo = dw(r[2 * kk], j >> 1);
+        const uint32_t hi = dw(r[2 * kk + 1], j >> 1);
+        o[kk] = (j & 1) ? __builtin_amdgcn_perm(hi, lo, 0x07060302u)
+                        : __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+      }
+      *reinterpret_cast<uint4*>(sm + st[j]) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
 template <bool AK, bool BKM, bool F16, int EPI>
 __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
   __shared__ __attribute__((aligned(16))) u16 smem[2 * 2 * TILE_ELEMS];
@@ -235,6 +286,25 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
   }
   const int nkt = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   const int nstage = nkt * p.npass;
+  // interior tiles with 16-byte aligned operands take the check-free loaders for every
+  // full K step
+  const bool interior = (m0 + BM <= p.M) && (n0 + BN <= p.N) && p.aligned_a && p.aligned_b;
+
+  uint32_t ga[8], gb[8], sa[8], sb[8];
+  load_offsets<AK>(p.lda, ga, sa, tid);
+  load_offsets<BKM>(p.ldb, gb, sb, tid);
+  // fragment offsets (bytes) for the 4 row blocks x 4 k16 sub-steps of each operand
+  uint32_t fa[4][4], fb[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int chunk = kk * 2 + (lane >> 5);
+      const int ra = wm * 128 + i * 32 + (lane & 31);
+      const int rb = wn * 128 + i * 32 + (lane & 31);
+      fa[i][kk] = (uint32_t)((ra * BK + ((chunk ^ swz(ra)) << 3)) * 2);
+      fb[i][kk] = (uint32_t)((rb * BK + ((chunk ^ swz(rb)) << 3)) * 2);
+    }
 
   floatx16 acc[4][4];
 #pragma unroll
@@ -244,35 +314,74 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // stage s -> (pass, k0); the stage's operand origins
+  auto stage_k0 = [&](int s, int& pass) {
+    pass = s / nkt;
+    return kbeg + (s - pass * nkt) * BK;
+  };
+  auto origin = [&](int pass, int k0, const char*& A, const char*& B) {
+    const int pa = pass == 0 ? p.pa0 : (pass == 1 ? p.pa1 : p.pa2);
+    const int pb = pass == 0 ? p.pb0 : (pass == 1 ? p.pb1 : p.pb2);
+    const u16* a = pa ? p.a1 : p.a0;
+    const u16* b = pb ? p.b1 : p.b0;
+    A = reinterpret_cast<const char*>(AK ? a + (int64_t)m0 * p.lda + k0 : a + (int64_t)k0 * p.lda + m0);
+    B = reinterpret_cast<const char*>(BKM ? b + (int64_t)n0 * p.ldb + k0 : b + (int64_t)k0 * p.ldb + n0);
+  };
+
   uint4 ra[8], rb[8];
+  auto fetch = [&](int s) {
+    int pass;
+    const int k0 = stage_k0(s, pass);
+    if (interior && k0 + BK <= kend) {
+      const char* A;
+      const char* B;
+      origin(pass, k0, A, B);
+      fast_load(A, ga, ra);
+      fast_load(B, gb, rb);
+    } else {
+      load_stage<AK, BKM>(p, s, nkt, kbeg, m0, n0, ra, rb, tid);
+    }
+  };
+  auto put = [&](int s, char* sA, char* sB) {
+    int pass;
+    const int k0 = stage_k0(s, pass);
+    if (interior && k0 + BK <= kend) {
+      fast_store<AK>(sA, sa, ra);
+      fast_store<BKM>(sB, sb, rb);
+    } else {
+      store_stage<AK, BKM>(reinterpret_cast<u16*>(sA), reinterpret_cast<u16*>(sB), ra, rb, tid);
+    }
+  };
+
+  char* sm = reinterpret_cast<char*>(smem);
+  constexpr int OPB = TILE_ELEMS * 2;      // bytes per operand per stage
   if (nstage > 0) {
-    load_stage<AK, BKM>(p, 0, nkt, kbeg, m0, n0, ra, rb, tid);
-    store_stage<AK, BKM>(smem, smem + TILE_ELEMS, ra, rb, tid);
+    fetch(0);
+    put(0, sm, sm + OPB);
   }
   __syncthreads();
 
   for (int s = 0; s < nstage; ++s) {
     const int buf = s & 1;
-    const u16* sA = smem + buf * 2 * TILE_ELEMS;
-    const u16* sB = sA + TILE_ELEMS;
+    const char* sA = sm + buf * 2 * OPB;
+    const char* sB = sA + OPB;
     const bool more = (s + 1) < nstage;
-    if (more) load_stage<AK, BKM>(p, s + 1, nkt, kbeg, m0, n0, ra, rb, tid);
+    if (more) fetch(s + 1);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int chunk = kk * 2 + (lane >> 5);
       uint4 af[4], bfr[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = frag(sA, wm * 128 + i * 32 + (lane & 31), chunk);
+      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const uint4*>(sA + fa[i][kk]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bfr[j] = frag(sB, wn * 128 + j * 32 + (lane & 31), chunk);
+      for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const uint4*>(sB + fb[j][kk]);
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = mfma<F16>(af[i], bfr[j], acc[i][j]);
     }
     if (more) {
-      u16* nA = smem + (buf ^ 1) * 2 * TILE_ELEMS;
-      store_stage<AK, BKM>(nA, nA + TILE_ELEMS, ra, rb, tid);
+      char* nA = sm + (buf ^ 1) * 2 * OPB;
+      put(s + 1, nA, nA + OPB);
     }
     __syncthreads();
   }
@@ -309,6 +418,253 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
               p.c[(int64_t)row * p.ldc + col] = x;
               p.c[(int64_t)col * p.ldc + row] = x;
             }
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ async GEMM
+// Global tiles go straight to LDS with global_load_lds_dwordx4 (no register staging)
+// through a 4-stage ring of 256 x 32 tiles fetched three stages ahead; one barrier per
+// stage.  K must be a multiple of 32 (operand planes are zero-padded in K).
+//  * K-major operand (X(r, k) at x[r * ld + k]): LDS rows r of 4 chunks of 8 k-values,
+//    chunk c stored in slot c ^ ((r >> 2) & 3); fragments are plain 16-byte reads.
+//    Rows beyond M (N) are read from the last valid row; their results are discarded.
+//  * M/N-major operand (X(r, k) at x[k * ld + r]): LDS rows k of 32 chunks of 8 r-values,
+//    chunk x stored in slot x ^ (2 (k & 3)); fragments come from two
+//    ds_read_b64_tr_b16 per MFMA operand (inside a group of 16 lanes, lane j supplies
+//    4 values of k-row j / 4 and lane i receives the 4 k-values of column i).  Requires
+//    M (N) to be a multiple of 8; columns beyond are read from the last valid chunk.
+// All fragment reads are bank-conflict free.
+constexpr int ABK = 32, ANST = 4;
+constexpr int ATILE = BM * ABK;                  // u16 elements per operand per stage
+
+struct AParams {
+  int M, N, K;
+  const u16* a0; const u16* a1;
+  const u16* b0; const u16* b1;
+  int64_t lda, ldb;
+  int npass;
+  int pa0, pa1, pa2, pb0, pb1, pb2;
+  float* c; int64_t ldc;
+  u16* c_hi; u16* c_lo;
+  int ldc_pad;          // EPI_SPLIT: columns [N, ldc_pad) of the output are written as 0
+  int tiles_m, tiles_n, ntiles;
+  int ksplit, k_per_split;
+  float* part;
+};
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// s_waitcnt immediate that waits for vmcnt <= n and leaves expcnt / lgkmcnt alone
+constexpr unsigned waitcnt_vm(unsigned n) {
+  return (n & 15u) | ((n >> 4) << 14) | (7u << 4) | (15u << 8);
+}
+
+// Per-lane DMA byte offsets (relative to the stage origin) of the 4 chunks a lane moves
+// per operand and stage.
+template <bool MN>
+__device__ __forceinline__ void dma_offsets(int64_t ld, int r0, int R, int wave, int lane,
+                                            uint32_t (&g)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int slot = (wave * 4 + i) * 64 + lane;
+    if (MN) {
+      const int k = slot >> 5;
+      const int x = (slot & 31) ^ ((k & 3) << 1);
+      const int r = min(r0 + 8 * x, R - 8) - r0;
+      g[i] = (uint32_t)(((int64_t)k * ld + r) * 2);
+    } else {
+      const int row = slot >> 2;
+      const int c = (slot & 3) ^ ((row >> 2) & 3);
+      const int r = min(r0 + row, R - 1) - r0;
+      g[i] = (uint32_t)(((int64_t)r * ld + c * 8) * 2);
+    }
+  }
+}
+
+// Fragment read base offsets: for K-major operands f[i][kk] are full byte offsets; for
+// M/N-major ones f[i][0] is the offset of the first transpose read of row block i (the
+// other three reads of the block sit at fixed immediate distances).
+template <bool MN>
+__device__ __forceinline__ void frag_offsets(int wblk, int lane, uint32_t (&f)[4][2]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (MN) {
+      const int j = lane & 15;
+      const int g = lane >> 5;
+      const int mb = 16 * ((lane >> 4) & 1);
+      const int m = wblk * 128 + i * 32 + mb + 4 * (j & 3);
+      const int k = 8 * g + (j >> 2);
+      const int x = (m >> 3) ^ ((k & 3) << 1);
+      f[i][0] = (uint32_t)(k * 512 + x * 16 + (m & 7) * 2);
+      f[i][1] = 0;
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int chunk = kk * 2 + (lane >> 5);
+        const int r = wblk * 128 + i * 32 + (lane & 31);
+        f[i][kk] = (uint32_t)(r * 64 + ((chunk ^ ((r >> 2) & 3)) << 4));
+      }
+    }
+  }
+}
+
+template <bool MN>
+__device__ __forceinline__ uint4 afrag(const char* base, const uint32_t (&f)[4][2], int i, int kk) {
+  if (MN) {
+    // k rows 16 kk + 8 g + (0..3) and + 4 .. 7: two transpose reads 4 k-rows apart
+    const char* p0 = base + f[i][0] + kk * 16 * 512;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 4 * 512));
+    uint4 r;
+    r.x = ((uint32_t)(uint16_t)lo[0]) | ((uint32_t)(uint16_t)lo[1] << 16);
+    r.y = ((uint32_t)(uint16_t)lo[2]) | ((uint32_t)(uint16_t)lo[3] << 16);
+    r.z = ((uint32_t)(uint16_t)hi[0]) | ((uint32_t)(uint16_t)hi[1] << 16);
+    r.w = ((uint32_t)(uint16_t)hi[2]) | ((uint32_t)(uint16_t)hi[3] << 16);
+    return r;
+  } else {
+    return *reinterpret_cast<const uint4*>(base + f[i][kk]);
+  }
+}
+
+template <bool AMN, bool BMN, bool F16, int EPI>
+__global__ __launch_bounds__(NT, 1) void k_gemm_async(AParams p) {
+  // one LDS object per ring stage, so that the compiler can tell the DMA writes of the
+  // stages in flight from the reads of the stage being consumed
+  __shared__ __attribute__((aligned(16))) u16 st0[2 * ATILE];
+  __shared__ __attribute__((aligned(16))) u16 st1[2 * ATILE];
+  __shared__ __attribute__((aligned(16))) u16 st2[2 * ATILE];
+  __shared__ __attribute__((aligned(16))) u16 st3[2 * ATILE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  constexpr bool SYM = (EPI == EPI_SYM || EPI == EPI_PARTIAL);
+
+  int split, tm, tn;
+  {
+    KParams kp{};
+    kp.tiles_m = p.tiles_m; kp.tiles_n = p.tiles_n; kp.ntiles = p.ntiles;
+    tile_coords(kp, SYM, split, tm, tn);
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
+  int kbeg = 0, kend = p.K;
+  if (EPI == EPI_PARTIAL) {
+    kbeg = split * p.k_per_split;
+    kend = min(p.K, kbeg + p.k_per_split);
+  }
+  const int nkt = kend > kbeg ? (kend - kbeg) / ABK : 0;
+  const int nstage = nkt * p.npass;
+
+  uint32_t ga[4], gb[4];
+  dma_offsets<AMN>(p.lda, m0, p.M, wave, lane, ga);
+  dma_offsets<BMN>(p.ldb, n0, p.N, wave, lane, gb);
+  uint32_t fa[4][2], fb[4][2];
+  frag_offsets<AMN>(wm, lane, fa);
+  frag_offsets<BMN>(wn, lane, fb);
+
+  floatx16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  constexpr int OPB = ATILE * 2;                 // bytes per operand per stage
+  auto issue = [&](int s, char* dst) {
+    const int pass = s / nkt;
+    const int k0 = kbeg + (s - pass * nkt) * ABK;
+    const int pa = pass == 0 ? p.pa0 : (pass == 1 ? p.pa1 : p.pa2);
+    const int pb = pass == 0 ? p.pb0 : (pass == 1 ? p.pb1 : p.pb2);
+    const u16* a = pa ? p.a1 : p.a0;
+    const u16* b = pb ? p.b1 : p.b0;
+    const char* A = reinterpret_cast<const char*>(AMN ? a + (int64_t)k0 * p.lda + m0
+                                                      : a + (int64_t)m0 * p.lda + k0);
+    const char* B = reinterpret_cast<const char*>(BMN ? b + (int64_t)k0 * p.ldb + n0
+                                                      : b + (int64_t)n0 * p.ldb + k0);
+    char* dA = dst + wave * 4 * 1024;
+    char* dB = dA + OPB;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(A + ga[i]), (lds_void*)(dA + i * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(B + gb[i]), (lds_void*)(dB + i * 1024), 16, 0, 0);
+  };
+  auto compute = [&](const char* sA) {
+    const char* sB = sA + OPB;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint4 af[4], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = afrag<AMN>(sA, fa, i, kk);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bfr[j] = afrag<BMN>(sB, fb, j, kk);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma<F16>(af[i], bfr[j], acc[i][j]);
+    }
+  };
+  // one ring step with compile-time slots: wait for stage s, refill the slot freed by
+  // stage s - 1 with stage s + 3, multiply stage s
+  auto step = [&](int s, char* cur, char* nxt) {
+    const int ahead = nstage - 1 - s;
+    if (ahead >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(16));
+    else if (ahead == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __syncthreads();
+    if (s + ANST - 1 < nstage) issue(s + ANST - 1, nxt);
+    compute(cur);
+  };
+
+  if (nstage > 0) issue(0, reinterpret_cast<char*>(st0));
+  if (nstage > 1) issue(1, reinterpret_cast<char*>(st1));
+  if (nstage > 2) issue(2, reinterpret_cast<char*>(st2));
+  for (int s = 0; s < nstage; s += 4) {
+    step(s, reinterpret_cast<char*>(st0), reinterpret_cast<char*>(st3));
+    if (s + 1 < nstage) step(s + 1, reinterpret_cast<char*>(st1), reinterpret_cast<char*>(st0));
+    if (s + 2 < nstage) step(s + 2, reinterpret_cast<char*>(st2), reinterpret_cast<char*>(st1));
+    if (s + 3 < nstage) step(s + 3, reinterpret_cast<char*>(st3), reinterpret_cast<char*>(st2));
+  }
+
+  // 32x32 accumulator layout: value v of lane l is row 8*(v/4) + 4*(l/32) + v%4,
+  // column l%32 of its 32 x 32 block.
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int rl = wm * 128 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+      const int row = m0 + rl;
+      if (EPI != EPI_PARTIAL && row >= p.M) continue;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int cl = wn * 128 + j * 32 + (lane & 31);
+        const int col = n0 + cl;
+        const float x = acc[i][j][v];
+        if (EPI == EPI_PARTIAL) {
+          const int tidx = tm * p.tiles_n - (tm * (tm - 1)) / 2 + (tn - tm);
+          p.part[((int64_t)split * p.ntiles + tidx) * (BM * BN) + rl * BN + cl] = x;
+        } else if (EPI == EPI_F32) {
+          if (col < p.N) p.c[(int64_t)row * p.ldc + col] = x;
+        } else if (EPI == EPI_SPLIT) {
+          if (col < p.ldc_pad) {
+            const bool in = col < p.N;
+            const uint32_t h = in ? bf16_rne_bits(x) : 0u;
+            const uint32_t l = in ? bf16_rne_bits(x - __uint_as_float(h << 16)) : 0u;
+            p.c_hi[(int64_t)row * p.ldc + col] = (u16)h;
+            p.c_lo[(int64_t)row * p.ldc + col] = (u16)l;
+          }
+        } else {  // EPI_SYM
+          if (col < p.N && row <= col) {
+            p.c[(int64_t)row * p.ldc + col] = x;
+            p.c[(int64_t)col * p.ldc + row] = x;
           }
         }
       }
@@ -358,6 +714,8 @@ __global__ __launch_bounds__(256) void k_syrk_reduce(const float* __restrict__ p
 // ------------------------------------------------------------------ elementwise
 template <typename T>
 __device__ __forceinline__ float ld_f(const T* p) { return (float)*p; }
+template <>
+__device__ __forceinline__ float ld_f<u16>(const u16* p) { return __uint_as_float((uint32_t)*p << 16); }
 
 template <typename T>
 __global__ void k_split(const T* __restrict__ in, int64_t ld_in, int rows, int cols,
@@ -414,6 +772,57 @@ __global__ void k_fill_zero(float* p, int rows, int cols, int64_t ld) {
   }
 }
 
+// out[r * ld_out + c] = bf16 pair of in[r][c] (times col_scale[c]) for c < cols and 0 for
+// cols <= c < ld_out (K padding).
+template <typename T>
+__global__ void k_split_pad(const T* __restrict__ in, int64_t ld_in, int rows, int cols,
+                            const float* __restrict__ col_scale, u16* __restrict__ hi,
+                            u16* __restrict__ lo, int64_t ld_out) {
+  const int64_t total = (int64_t)rows * ld_out;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t r = e / ld_out;
+    const int c = (int)(e - r * ld_out);
+    uint32_t h = 0, l = 0;
+    if (c < cols) {
+      float x = ld_f(in + r * ld_in + c);
+      if (col_scale) x *= col_scale[c];
+      h = bf16_rne_bits(x);
+      l = bf16_rne_bits(x - __uint_as_float(h << 16));
+    }
+    hi[e] = (u16)h;
+    if (lo) lo[e] = (u16)l;
+  }
+}
+
+// Transposing split: out[c * ld_out + r] = bf16 pair of in[r][c] for r < rows, 0 for
+// rows <= r < ld_out.  64 x 64 tiles through LDS; grid (ceil(cols/64), ceil(ld_out/64)).
+template <typename T>
+__global__ __launch_bounds__(256) void k_split_t(const T* __restrict__ in, int64_t ld_in, int rows,
+                                                 int cols, u16* __restrict__ hi,
+                                                 u16* __restrict__ lo, int64_t ld_out) {
+  __shared__ float tile[64][65];
+  const int c0 = blockIdx.x * 64;
+  const int64_t r0 = (int64_t)blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int r = ty; r < 64; r += 4) {
+    const int64_t gr = r0 + r;
+    const int gc = c0 + tx;
+    tile[r][tx] = (gr < rows && gc < cols) ? ld_f(in + gr * ld_in + gc) : 0.f;
+  }
+  __syncthreads();
+  for (int c = ty; c < 64; c += 4) {
+    const int gc = c0 + c;
+    const int64_t gr = r0 + tx;
+    if (gc < cols && gr < ld_out) {
+      const float x = tile[tx][c];
+      const uint32_t h = bf16_rne_bits(x);
+      hi[(int64_t)gc * ld_out + gr] = (u16)h;
+      if (lo) lo[(int64_t)gc * ld_out + gr] = (u16)bf16_rne_bits(x - __uint_as_float(h << 16));
+    }
+  }
+}
+
 int grid_for(int64_t n, int per_block) {
   int64_t g = (n + per_block - 1) / per_block;
   if (g > 65536) g = 65536;
@@ -459,8 +868,10 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
   p.pa0 = d.pa[0]; p.pa1 = d.pa[1]; p.pa2 = d.pa[2];
   p.pb0 = d.pb[0]; p.pb1 = d.pb[1]; p.pb2 = d.pb[2];
   p.c = d.c; p.ldc = d.ldc; p.c_hi = d.c_hi; p.c_lo = d.c_lo;
+  // 16-byte aligned rows; per-thread byte offsets inside a 256-row (or 64-row) stage
+  // must fit in 32 bits
   auto al = [](const u16* q, int64_t ld) {
-    return ((reinterpret_cast<uintptr_t>(q) & 15) == 0) && (ld % 8 == 0);
+    return ((reinterpret_cast<uintptr_t>(q) & 15) == 0) && (ld % 8 == 0) && ld < (1 << 22);
   };
   p.aligned_a = al(p.a0, d.lda) && al(p.a1, d.lda);
   p.aligned_b = al(p.b0, d.ldb) && al(p.b1, d.ldb);
@@ -474,6 +885,37 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
   p.k_per_split = kt_per * BK;
   p.part = partial;
   const int grid = p.ntiles * p.ksplit;
+  // asynchronous path: K a multiple of 32 (of each K-split), 16-byte aligned operands,
+  // M/N-major operands with rows a multiple of 8
+  const bool kp_ok = (p.k_per_split % ABK == 0) && (d.K % ABK == 0);
+  const bool mn_ok = (d.a_kmajor || d.M % 8 == 0) && (d.b_kmajor || d.N % 8 == 0);
+  if (kp_ok && mn_ok && p.aligned_a && p.aligned_b && d.a_kmajor == d.b_kmajor) {
+    AParams q{};
+    q.M = d.M; q.N = d.N; q.K = d.K;
+    q.a0 = p.a0; q.a1 = p.a1; q.b0 = p.b0; q.b1 = p.b1; q.lda = d.lda; q.ldb = d.ldb;
+    q.npass = d.npass;
+    q.pa0 = p.pa0; q.pa1 = p.pa1; q.pa2 = p.pa2; q.pb0 = p.pb0; q.pb1 = p.pb1; q.pb2 = p.pb2;
+    q.c = d.c; q.ldc = d.ldc; q.c_hi = d.c_hi; q.c_lo = d.c_lo; q.ldc_pad = (int)d.ldc_pad;
+    q.tiles_m = p.tiles_m; q.tiles_n = p.tiles_n; q.ntiles = p.ntiles;
+    q.ksplit = p.ksplit; q.k_per_split = p.k_per_split; q.part = partial;
+    prof_begin(s, d.name);
+    const dim3 gr(grid), bl(NT);
+#define FQ_LAUNCH_ASYNC(AMN, BMN, F16)                                                          \
+    switch (d.epi) {                                                                             \
+      case EPI_F32: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_F32>), gr, bl, 0, s, q); break;      \
+      case EPI_SPLIT: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SPLIT>), gr, bl, 0, s, q); break;  \
+      case EPI_SYM: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SYM>), gr, bl, 0, s, q); break;      \
+      default: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_PARTIAL>), gr, bl, 0, s, q); break;       \
+    }
+    if (d.a_kmajor && d.b_kmajor) {
+      if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true) } else { FQ_LAUNCH_ASYNC(false, false, false) }
+    } else {
+      if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true) } else { FQ_LAUNCH_ASYNC(true, true, false) }
+    }
+#undef FQ_LAUNCH_ASYNC
+    prof_end(s);
+    return last_launch_error();
+  }
   prof_begin(s, d.name);
   bool ok;
   if (d.a_kmajor && d.b_kmajor) {
@@ -526,6 +968,43 @@ hipError_t split_bf16(const void* in, int in_type, int64_t ld_in, int rows, int 
     hipLaunchKernelGGL(k_split<_Float16>, dim3(grid_for((int64_t)rows * cols, 256)), dim3(256),
                        0, s, (const _Float16*)in, ld_in, rows, cols, col_scale, hi, lo, ld_out);
   }
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t split_bf16_pad(const void* in, int in_type, int64_t ld_in, int rows, int cols,
+                          const float* col_scale, u16* hi, u16* lo, int64_t ld_out,
+                          hipStream_t s) {
+  if (rows <= 0 || ld_out <= 0) return hipSuccess;
+  prof_begin(s, "split_bf16");
+  const dim3 g(grid_for((int64_t)rows * ld_out, 256));
+  if (in_type == 0)
+    hipLaunchKernelGGL(k_split_pad<float>, g, dim3(256), 0, s, (const float*)in, ld_in, rows, cols,
+                       col_scale, hi, lo, ld_out);
+  else if (in_type == 1)
+    hipLaunchKernelGGL(k_split_pad<_Float16>, g, dim3(256), 0, s, (const _Float16*)in, ld_in, rows,
+                       cols, col_scale, hi, lo, ld_out);
+  else
+    hipLaunchKernelGGL(k_split_pad<u16>, g, dim3(256), 0, s, (const u16*)in, ld_in, rows, cols,
+                       col_scale, hi, lo, ld_out);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t split_bf16_t(const void* in, int in_type, int64_t ld_in, int rows, int cols, u16* hi,
+                        u16* lo, int64_t ld_out, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  prof_begin(s, "split_bf16");
+  const dim3 g((cols + 63) / 64, (unsigned)((ld_out + 63) / 64));
+  if (in_type == 0)
+    hipLaunchKernelGGL(k_split_t<float>, g, dim3(256), 0, s, (const float*)in, ld_in, rows, cols, hi,
+                       lo, ld_out);
+  else if (in_type == 1)
+    hipLaunchKernelGGL(k_split_t<_Float16>, g, dim3(256), 0, s, (const _Float16*)in, ld_in, rows,
+                       cols, hi, lo, ld_out);
+  else
+    hipLaunchKernelGGL(k_split_t<u16>, g, dim3(256), 0, s, (const u16*)in, ld_in, rows, cols, hi, lo,
+                       ld_out);
   prof_end(s);
   return last_launch_error();
 }

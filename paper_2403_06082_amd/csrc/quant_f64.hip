@@ -675,6 +675,41 @@ __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ co
   }
 }
 
+// Transposed dequantization: out[c * ld_out + r] = code[r][c] - zero[r] as bf16 (small
+// integers, exact); rows r in [rows, ld_out) are written as 0.  64 x 64 tiles.
+__global__ __launch_bounds__(256) void k_dequant_t(const uint32_t* __restrict__ codes,
+                                                   const float* __restrict__ zero, int64_t rows,
+                                                   int64_t cols, u16* __restrict__ out,
+                                                   int64_t ld_out) {
+  __shared__ u16 tile[64][66];
+  const int64_t r0 = (int64_t)blockIdx.y * 64;
+  const int64_t c0 = (int64_t)blockIdx.x * 64;   // multiple of 16
+  const int64_t nw = (cols + 15) / 16;
+  // 64 rows x 4 words of 16 codes
+  {
+    const int r = threadIdx.x >> 2, w = threadIdx.x & 3;
+    const int64_t gr = r0 + r, gw = c0 / 16 + w;
+    uint32_t word = 0;
+    float z = 0.f;
+    const bool ok = gr < rows && gw < nw;
+    if (ok) {
+      word = codes[gr * nw + gw];
+      z = zero[gr];
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float v = ok ? (float)((word >> (2 * k)) & 3u) - z : 0.f;
+      tile[r][w * 16 + k] = (u16)(__float_as_uint(v) >> 16);
+    }
+  }
+  __syncthreads();
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int c = ty; c < 64; c += 4) {
+    const int64_t gc = c0 + c, gr = r0 + tx;
+    if (gc < cols && gr < ld_out) out[gc * ld_out + gr] = (gr < rows) ? tile[tx][c] : (u16)0;
+  }
+}
+
 }  // namespace
 
 // ====================================================================== launchers
@@ -769,6 +804,16 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
   prof_begin(s, name);
   if (DT == 128) hipLaunchKernelGGL(k_dgemm<128>, dim3((unsigned)grid), dim3(256), 0, s, p);
   else hipLaunchKernelGGL(k_dgemm<64>, dim3((unsigned)grid), dim3(256), 0, s, p);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t dequant_bf16_t(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
+                          u16* out, int64_t ld_out, hipStream_t s) {
+  if (cols <= 0 || ld_out <= 0) return hipSuccess;
+  prof_begin(s, "dequant");
+  hipLaunchKernelGGL(k_dequant_t, dim3((unsigned)((cols + 63) / 64), (unsigned)((ld_out + 63) / 64)),
+                     dim3(256), 0, s, codes, zero, rows, cols, out, ld_out);
   prof_end(s);
   return last_launch_error();
 }

@@ -31,7 +31,7 @@ def _rand_storage(rng, shape, dtype, scale=1.0):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
-@pytest.mark.parametrize("n,d", [(77, 100), (512, 256), (1000, 520), (3000, 264)])
+@pytest.mark.parametrize("n,d", [(77, 100), (512, 256), (1000, 520), (3000, 264), (2048, 264), (4096, 520)])
 def test_hessian_parity(dtype, n, d):
     torch = need_gpu()
     fq = _fq()
