@@ -21,6 +21,8 @@
 //    for L2 reuse.
 #include "fq_internal.h"
 
+#include <stdlib.h>
+
 namespace fq {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -433,7 +435,7 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
 //    chunk c stored in slot c ^ ((r >> 2) & 3); fragments are plain 16-byte reads.
 //    Rows beyond M (N) are read from the last valid row; their results are discarded.
 //  * M/N-major operand (X(r, k) at x[k * ld + r]): LDS rows k of 32 chunks of 8 r-values,
-//    chunk x stored in slot x ^ (2 (k & 3)); fragments come from two
+//    chunk x stored in slot x ^ (4 (k & 3)); fragments come from two
 //    ds_read_b64_tr_b16 per MFMA operand (inside a group of 16 lanes, lane j supplies
 //    4 values of k-row j / 4 and lane i receives the 4 k-values of column i).  Requires
 //    M (N) to be a multiple of 8; columns beyond are read from the last valid chunk.
@@ -465,17 +467,29 @@ constexpr unsigned waitcnt_vm(unsigned n) {
   return (n & 15u) | ((n >> 4) << 14) | (7u << 4) | (15u << 8);
 }
 
-// Per-lane DMA byte offsets (relative to the stage origin) of the 4 chunks a lane moves
-// per operand and stage.
-template <bool MN>
+// One 16-byte-per-lane DMA from global memory (wave-uniform base + per-lane offset) into
+// 1 KiB of LDS at lds + 16 * lane.  Issued as inline assembly so that the compiler's wait
+// insertion does not treat every later LDS read as dependent on it: completion is
+// tracked by the explicit vmcnt waits of the ring.
+__device__ __forceinline__ void dma16(const char* base, uint32_t off, char* lds) {
+  const uint32_t l = (uint32_t)(uintptr_t)(lds_void*)lds;
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(l)
+               : "memory", "m0");
+}
+
+// Per-lane DMA byte offsets (relative to the stage origin) of the NI chunks a lane moves
+// per operand and stage (NI = 1024 chunks / (64 lanes x waves)).
+template <bool MN, int NI>
 __device__ __forceinline__ void dma_offsets(int64_t ld, int r0, int R, int wave, int lane,
-                                            uint32_t (&g)[4]) {
+                                            uint32_t (&g)[NI]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int slot = (wave * 4 + i) * 64 + lane;
+  for (int i = 0; i < NI; ++i) {
+    const int slot = (wave * NI + i) * 64 + lane;
     if (MN) {
       const int k = slot >> 5;
-      const int x = (slot & 31) ^ ((k & 3) << 1);
+      const int x = (slot & 31) ^ ((k & 3) << 2);
       const int r = min(r0 + 8 * x, R - 8) - r0;
       g[i] = (uint32_t)(((int64_t)k * ld + r) * 2);
     } else {
@@ -487,35 +501,35 @@ __device__ __forceinline__ void dma_offsets(int64_t ld, int r0, int R, int wave,
   }
 }
 
-// Fragment read base offsets: for K-major operands f[i][kk] are full byte offsets; for
-// M/N-major ones f[i][0] is the offset of the first transpose read of row block i (the
-// other three reads of the block sit at fixed immediate distances).
-template <bool MN>
-__device__ __forceinline__ void frag_offsets(int wblk, int lane, uint32_t (&f)[4][2]) {
+// Fragment read offsets of the NB row blocks (32 rows each) a wave owns, starting at row
+// r0w of the tile.  K-major: f[i][kk] are full byte offsets; M/N-major: f[i][0] is the
+// first of the block's transpose reads (the others sit at fixed immediate distances).
+template <bool MN, int NB>
+__device__ __forceinline__ void frag_offsets(int r0w, int lane, uint32_t (&f)[NB][2]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < NB; ++i) {
     if (MN) {
       const int j = lane & 15;
       const int g = lane >> 5;
       const int mb = 16 * ((lane >> 4) & 1);
-      const int m = wblk * 128 + i * 32 + mb + 4 * (j & 3);
+      const int m = r0w + i * 32 + mb + 4 * (j & 3);
       const int k = 8 * g + (j >> 2);
-      const int x = (m >> 3) ^ ((k & 3) << 1);
+      const int x = (m >> 3) ^ ((k & 3) << 2);
       f[i][0] = (uint32_t)(k * 512 + x * 16 + (m & 7) * 2);
       f[i][1] = 0;
     } else {
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         const int chunk = kk * 2 + (lane >> 5);
-        const int r = wblk * 128 + i * 32 + (lane & 31);
+        const int r = r0w + i * 32 + (lane & 31);
         f[i][kk] = (uint32_t)(r * 64 + ((chunk ^ ((r >> 2) & 3)) << 4));
       }
     }
   }
 }
 
-template <bool MN>
-__device__ __forceinline__ uint4 afrag(const char* base, const uint32_t (&f)[4][2], int i, int kk) {
+template <bool MN, int NB>
+__device__ __forceinline__ uint4 afrag(const char* base, const uint32_t (&f)[NB][2], int i, int kk) {
   if (MN) {
     // k rows 16 kk + 8 g + (0..3) and + 4 .. 7: two transpose reads 4 k-rows apart
     const char* p0 = base + f[i][0] + kk * 16 * 512;
@@ -532,8 +546,14 @@ __device__ __forceinline__ uint4 afrag(const char* base, const uint32_t (&f)[4][
   }
 }
 
-template <bool AMN, bool BMN, bool F16, int EPI>
-__global__ __launch_bounds__(NT, 1) void k_gemm_async(AParams p) {
+// WAVES = 4: 2 x 2 waves of 128 x 128.  WAVES = 8: 2 x 4 waves of 128 x 64 (two waves per
+// SIMD, so one wave's memory waits overlap the other's MFMAs).
+template <bool AMN, bool BMN, bool F16, int EPI, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
+  constexpr int NBM = 4;                         // 32-row blocks per wave in m
+  constexpr int NBN = WAVES == 4 ? 4 : 2;        // 32-col blocks per wave in n
+  constexpr int WN = WAVES == 4 ? 2 : 4;         // waves along n
+  constexpr int NI = 1024 / (64 * WAVES);        // DMA chunks per lane per operand and stage
   // one LDS object per ring stage, so that the compiler can tell the DMA writes of the
   // stages in flight from the reads of the stage being consumed
   __shared__ __attribute__((aligned(16))) u16 st0[2 * ATILE];
@@ -543,7 +563,7 @@ __global__ __launch_bounds__(NT, 1) void k_gemm_async(AParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   constexpr bool SYM = (EPI == EPI_SYM || EPI == EPI_PARTIAL);
 
   int split, tm, tn;
@@ -561,91 +581,133 @@ __global__ __launch_bounds__(NT, 1) void k_gemm_async(AParams p) {
   const int nkt = kend > kbeg ? (kend - kbeg) / ABK : 0;
   const int nstage = nkt * p.npass;
 
-  uint32_t ga[4], gb[4];
-  dma_offsets<AMN>(p.lda, m0, p.M, wave, lane, ga);
-  dma_offsets<BMN>(p.ldb, n0, p.N, wave, lane, gb);
-  uint32_t fa[4][2], fb[4][2];
-  frag_offsets<AMN>(wm, lane, fa);
-  frag_offsets<BMN>(wn, lane, fb);
+  uint32_t ga[NI], gb[NI];
+  dma_offsets<AMN, NI>(p.lda, m0, p.M, wave, lane, ga);
+  dma_offsets<BMN, NI>(p.ldb, n0, p.N, wave, lane, gb);
+  uint32_t fa[NBM][2], fb[NBN][2];
+  frag_offsets<AMN, NBM>(wm * 128, lane, fa);
+  frag_offsets<BMN, NBN>(wn * 32 * NBN, lane, fb);
 
-  floatx16 acc[4][4];
+  floatx16 acc[NBM][NBN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < NBM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NBN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // Operand origins of each pass for this work-group's K range; inside a pass the stage
+  // origin advances by a fixed byte step, so the issue path is pointer increments only.
+  auto a_origin = [&](int sel) {
+    const u16* a = sel ? p.a1 : p.a0;
+    return reinterpret_cast<const char*>(AMN ? a + (int64_t)kbeg * p.lda + m0
+                                             : a + (int64_t)m0 * p.lda + kbeg);
+  };
+  auto b_origin = [&](int sel) {
+    const u16* b = sel ? p.b1 : p.b0;
+    return reinterpret_cast<const char*>(BMN ? b + (int64_t)kbeg * p.ldb + n0
+                                             : b + (int64_t)n0 * p.ldb + kbeg);
+  };
+  const char* const oa1 = a_origin(p.pa1);
+  const char* const oa2 = a_origin(p.pa2);
+  const char* const ob1 = b_origin(p.pb1);
+  const char* const ob2 = b_origin(p.pb2);
+  const int64_t astep = AMN ? (int64_t)ABK * p.lda * 2 : (int64_t)ABK * 2;
+  const int64_t bstep = BMN ? (int64_t)ABK * p.ldb * 2 : (int64_t)ABK * 2;
+  const char* iA = a_origin(p.pa0);
+  const char* iB = b_origin(p.pb0);
+  int ikt = 0, ipass = 0;
   constexpr int OPB = ATILE * 2;                 // bytes per operand per stage
-  auto issue = [&](int s, char* dst) {
-    const int pass = s / nkt;
-    const int k0 = kbeg + (s - pass * nkt) * ABK;
-    const int pa = pass == 0 ? p.pa0 : (pass == 1 ? p.pa1 : p.pa2);
-    const int pb = pass == 0 ? p.pb0 : (pass == 1 ? p.pb1 : p.pb2);
-    const u16* a = pa ? p.a1 : p.a0;
-    const u16* b = pb ? p.b1 : p.b0;
-    const char* A = reinterpret_cast<const char*>(AMN ? a + (int64_t)k0 * p.lda + m0
-                                                      : a + (int64_t)m0 * p.lda + k0);
-    const char* B = reinterpret_cast<const char*>(BMN ? b + (int64_t)k0 * p.ldb + n0
-                                                      : b + (int64_t)n0 * p.ldb + k0);
-    char* dA = dst + wave * 4 * 1024;
+  // DMA of the next stage in issue order into ring slot dst
+  auto issue = [&](char* dst) {
+    char* dA = dst + wave * NI * 1024;
     char* dB = dA + OPB;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(A + ga[i]), (lds_void*)(dA + i * 1024), 16, 0, 0);
+    for (int i = 0; i < NI; ++i) dma16(iA, ga[i], dA + i * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(B + gb[i]), (lds_void*)(dB + i * 1024), 16, 0, 0);
-  };
-  auto compute = [&](const char* sA) {
-    const char* sB = sA + OPB;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      uint4 af[4], bfr[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = afrag<AMN>(sA, fa, i, kk);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bfr[j] = afrag<BMN>(sB, fb, j, kk);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma<F16>(af[i], bfr[j], acc[i][j]);
+    for (int i = 0; i < NI; ++i) dma16(iB, gb[i], dB + i * 1024);
+    iA += astep;
+    iB += bstep;
+    if (++ikt == nkt) {
+      ikt = 0;
+      ++ipass;
+      iA = ipass == 1 ? oa1 : oa2;
+      iB = ipass == 1 ? ob1 : ob2;
     }
   };
-  // one ring step with compile-time slots: wait for stage s, refill the slot freed by
-  // stage s - 1 with stage s + 3, multiply stage s
-  auto step = [&](int s, char* cur, char* nxt) {
-    const int ahead = nstage - 1 - s;
-    if (ahead >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(16));
-    else if (ahead == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(8));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
-    __syncthreads();
-    if (s + ANST - 1 < nstage) issue(s + ANST - 1, nxt);
-    compute(cur);
+  auto load = [&](const char* sA, int kk, uint4 (&af)[NBM], uint4 (&bf)[NBN]) {
+    const char* sB = sA + OPB;
+#pragma unroll
+    for (int i = 0; i < NBM; ++i) af[i] = afrag<AMN, NBM>(sA, fa, i, kk);
+#pragma unroll
+    for (int j = 0; j < NBN; ++j) bf[j] = afrag<BMN, NBN>(sB, fb, j, kk);
+  };
+  auto mma = [&](const uint4 (&af)[NBM], const uint4 (&bf)[NBN]) {
+#pragma unroll
+    for (int i = 0; i < NBM; ++i)
+#pragma unroll
+      for (int j = 0; j < NBN; ++j) acc[i][j] = mfma<F16>(af[i], bf[j], acc[i][j]);
+  };
+  // Work-group barrier without a memory fence: the only cross-wave traffic is LDS, made
+  // safe by the explicit vmcnt waits (DMA landed) and by register dependencies (reads
+  // done); a fenced barrier would wait for every DMA in flight.
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   };
 
-  if (nstage > 0) issue(0, reinterpret_cast<char*>(st0));
-  if (nstage > 1) issue(1, reinterpret_cast<char*>(st1));
-  if (nstage > 2) issue(2, reinterpret_cast<char*>(st2));
+  // Software pipeline over a 4-slot ring with stages s + 1 and s + 2 in flight while
+  // stage s is multiplied; fragments of the next k-slice are read from LDS while the
+  // current one is in the matrix cores.
+  constexpr unsigned PER = 2 * NI;               // DMA instructions per stage and wave
+  uint4 a0[NBM], b0[NBN], a1[NBM], b1[NBN];
+  auto step = [&](int s, const char* cur, const char* nxt, char* refill) {
+    load(cur, 1, a1, b1);
+    mma(a0, b0);
+    if (s + 1 < nstage) {
+      if (s + 2 < nstage) __builtin_amdgcn_s_waitcnt(waitcnt_vm(PER));
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+      barrier();
+      if (s + 3 < nstage) issue(refill);
+      load(nxt, 0, a0, b0);
+    }
+    mma(a1, b1);
+  };
+
+  char* const r0 = reinterpret_cast<char*>(st0);
+  char* const r1 = reinterpret_cast<char*>(st1);
+  char* const r2 = reinterpret_cast<char*>(st2);
+  char* const r3 = reinterpret_cast<char*>(st3);
+  if (nstage > 0) {
+    issue(r0);
+    if (nstage > 1) issue(r1);
+    if (nstage > 2) issue(r2);
+    if (nstage > 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * PER));
+    else if (nstage > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(PER));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    barrier();
+    load(r0, 0, a0, b0);
+  }
   for (int s = 0; s < nstage; s += 4) {
-    step(s, reinterpret_cast<char*>(st0), reinterpret_cast<char*>(st3));
-    if (s + 1 < nstage) step(s + 1, reinterpret_cast<char*>(st1), reinterpret_cast<char*>(st0));
-    if (s + 2 < nstage) step(s + 2, reinterpret_cast<char*>(st2), reinterpret_cast<char*>(st1));
-    if (s + 3 < nstage) step(s + 3, reinterpret_cast<char*>(st3), reinterpret_cast<char*>(st2));
+    step(s, r0, r1, r3);
+    if (s + 1 < nstage) step(s + 1, r1, r2, r0);
+    if (s + 2 < nstage) step(s + 2, r2, r3, r1);
+    if (s + 3 < nstage) step(s + 3, r3, r0, r2);
   }
 
   // 32x32 accumulator layout: value v of lane l is row 8*(v/4) + 4*(l/32) + v%4,
   // column l%32 of its 32 x 32 block.
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < NBM; ++i) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int rl = wm * 128 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
       const int row = m0 + rl;
       if (EPI != EPI_PARTIAL && row >= p.M) continue;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int cl = wn * 128 + j * 32 + (lane & 31);
+      for (int j = 0; j < NBN; ++j) {
+        const int cl = wn * 32 * NBN + j * 32 + (lane & 31);
         const int col = n0 + cl;
         const float x = acc[i][j][v];
         if (EPI == EPI_PARTIAL) {
@@ -846,6 +908,13 @@ bool dispatch_epi(const KParams& p, int epi, int grid, hipStream_t s) {
   return false;
 }
 
+// waves per work-group of the asynchronous GEMM (FQ_ASYNC_WAVES=4|8 overrides, for tuning)
+int async_waves_from_env() {
+  const char* v = getenv("FQ_ASYNC_WAVES");
+  return (v && atoi(v) == 4) ? 4 : 8;
+}
+int g_async_waves = async_waves_from_env();
+
 }  // namespace
 
 int gemm_sym_tiles(int N) {
@@ -899,18 +968,26 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     q.tiles_m = p.tiles_m; q.tiles_n = p.tiles_n; q.ntiles = p.ntiles;
     q.ksplit = p.ksplit; q.k_per_split = p.k_per_split; q.part = partial;
     prof_begin(s, d.name);
-    const dim3 gr(grid), bl(NT);
-#define FQ_LAUNCH_ASYNC(AMN, BMN, F16)                                                          \
-    switch (d.epi) {                                                                             \
-      case EPI_F32: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_F32>), gr, bl, 0, s, q); break;      \
-      case EPI_SPLIT: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SPLIT>), gr, bl, 0, s, q); break;  \
-      case EPI_SYM: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SYM>), gr, bl, 0, s, q); break;      \
-      default: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_PARTIAL>), gr, bl, 0, s, q); break;       \
+    const dim3 gr(grid);
+#define FQ_LAUNCH_ASYNC(AMN, BMN, F16, W)                                                                  \
+    switch (d.epi) {                                                                                        \
+      case EPI_F32: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_F32, W>), gr, dim3(64 * W), 0, s, q); break;     \
+      case EPI_SPLIT: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SPLIT, W>), gr, dim3(64 * W), 0, s, q); break; \
+      case EPI_SYM: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SYM, W>), gr, dim3(64 * W), 0, s, q); break;     \
+      default: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_PARTIAL, W>), gr, dim3(64 * W), 0, s, q); break;      \
     }
-    if (d.a_kmajor && d.b_kmajor) {
-      if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true) } else { FQ_LAUNCH_ASYNC(false, false, false) }
+    if (g_async_waves == 8) {
+      if (d.a_kmajor && d.b_kmajor) {
+        if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true, 8) } else { FQ_LAUNCH_ASYNC(false, false, false, 8) }
+      } else {
+        if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true, 8) } else { FQ_LAUNCH_ASYNC(true, true, false, 8) }
+      }
     } else {
-      if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true) } else { FQ_LAUNCH_ASYNC(true, true, false) }
+      if (d.a_kmajor && d.b_kmajor) {
+        if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true, 4) } else { FQ_LAUNCH_ASYNC(false, false, false, 4) }
+      } else {
+        if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true, 4) } else { FQ_LAUNCH_ASYNC(true, true, false, 4) }
+      }
     }
 #undef FQ_LAUNCH_ASYNC
     prof_end(s);
