@@ -124,18 +124,18 @@ def make_x(wl: Workload, d_in: int, n_tokens: int | None = None, out: np.ndarray
     return out
 
 
-def make_frame(wl: Workload, d: int, tag: int, index: int = 0) -> np.ndarray:
-    """Dense Parseval frame P (d x K) for dimension d, float64."""
+def make_frame(wl: Workload, d: int, tag: int, index: int = 0, dtype=np.float64) -> np.ndarray:
+    """Dense Parseval frame P (d x K) for dimension d (float64, or its float32 rounding)."""
     k = frame_k(wl, d)
     ss = np.random.SeedSequence([wl.seed, tag, index])
-    return tff.parseval_frame(k, wl.rho, d, ss)
+    return tff.parseval_frame(k, wl.rho, d, ss, dtype=dtype)
 
 
-def make_frames(wl: Workload, li: int):
+def make_frames(wl: Workload, li: int, dtype=np.float64):
     """(P_out, P_in) for layer li; P_in is shared by all layers of the workload."""
     L = wl.layers[li]
-    P_out = make_frame(wl, L.d_out, TAG_POUT, li)
-    P_in = make_frame(wl, L.d_in, TAG_PIN, 0)
+    P_out = make_frame(wl, L.d_out, TAG_POUT, li, dtype)
+    P_in = make_frame(wl, L.d_in, TAG_PIN, 0, dtype)
     return P_out, P_in
 
 

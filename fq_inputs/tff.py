@@ -20,10 +20,15 @@ Nothing here is arithmetic of the quantization method itself; the frame is an in
 """
 from __future__ import annotations
 
+from concurrent.futures import ThreadPoolExecutor
 from fractions import Fraction
 import math
+import os
+import threading
 
 import numpy as np
+
+_BLAS_LOCK = threading.Lock()
 
 
 def t_block(x: float) -> np.ndarray:
@@ -106,21 +111,28 @@ def modulation_is_tight(F: np.ndarray, k: int) -> bool:
     return True
 
 
-def complex_tff(k: int, rho_c: int, d_c: int) -> np.ndarray:
-    """Complex (k, rho_c, d_c) TFF: array B[s] (d_c x rho_c), orthonormal columns.
-
-    Subspace s is spanned by the rows of F modulated by (w^(j*s))_j, w = exp(2*pi*i/k),
-    each divided by sqrt(d_c/rho_c) to make it unit norm.
-    """
+def _base_frame(k: int, rho_c: int, d_c: int) -> np.ndarray:
     F = spectral_tetris(rho_c, d_c) if d_c != rho_c else np.eye(rho_c)
     if not modulation_is_tight(F, k):
         raise ValueError(f"no tight modulation for (k={k}, rho={rho_c}, d={d_c})")
+    return F
+
+
+def complex_tff(k: int, rho_c: int, d_c: int, subspaces=None) -> np.ndarray:
+    """Complex (k, rho_c, d_c) TFF: array B[s] (d_c x rho_c), orthonormal columns.
+
+    Subspace s is spanned by the rows of F modulated by (w^(j*s))_j, w = exp(2*pi*i/k),
+    each divided by sqrt(d_c/rho_c) to make it unit norm.  subspaces: optional range of
+    s to build (default all k).
+    """
+    F = _base_frame(k, rho_c, d_c)
     j = np.arange(d_c)
     norm = math.sqrt(d_c / rho_c)
-    B = np.empty((k, d_c, rho_c), dtype=np.complex128)
-    for s in range(k):
+    ss = range(k) if subspaces is None else subspaces
+    B = np.empty((len(ss), d_c, rho_c), dtype=np.complex128)
+    for i, s in enumerate(ss):
         w = np.exp(2j * np.pi * s * j / k)
-        B[s] = (F * w[None, :]).T / norm
+        B[i] = (F * w[None, :]).T / norm
     return B
 
 
@@ -137,15 +149,16 @@ def realify(B: np.ndarray) -> np.ndarray:
     return out
 
 
-def real_tff_basis(k: int, rho: int, d: int) -> np.ndarray:
+def real_tff_basis(k: int, rho: int, d: int, subspaces=None) -> np.ndarray:
     """Real (k, rho, d) TFF as a d x (k*rho) matrix T = [T_1 ... T_k], each T_i with
     orthonormal columns; sum_i T_i T_i^T = (k*rho/d) I_d.  rho and d must be even
-    (realification of a complex (k, rho/2, d/2) TFF)."""
+    (realification of a complex (k, rho/2, d/2) TFF).  subspaces: optional range of i
+    (the matching column blocks only)."""
     if rho % 2 or d % 2:
         raise ValueError("the real construction needs even rho and d")
-    B = complex_tff(k, rho // 2, d // 2)
-    R = realify(B)  # k x d x rho
-    return np.concatenate(list(R), axis=1)
+    B = complex_tff(k, rho // 2, d // 2, subspaces)
+    R = realify(B)  # n x d x rho
+    return np.ascontiguousarray(R.transpose(1, 0, 2).reshape(d, R.shape[0] * rho))
 
 
 def valid_k_for(rho: int, d: int, k: int) -> bool:
@@ -203,20 +216,44 @@ def apply_rotation(R1: np.ndarray, R2: np.ndarray, T: np.ndarray) -> np.ndarray:
     d1, d2 = R1.shape[0], R2.shape[0]
     K = T.shape[1]
     M = np.ascontiguousarray(T.T).reshape(K, d1, d2)
-    A = np.tensordot(R1, M, axes=([1], [1]))                 # (d1, K, d2)
-    B = (A.reshape(d1 * K, d2) @ R2.T).reshape(d1, K, d2)
+    with _BLAS_LOCK:      # the BLAS is threaded itself and not safe for concurrent callers
+        A = np.tensordot(R1, M, axes=([1], [1]))             # (d1, K, d2)
+        B = (A.reshape(d1 * K, d2) @ R2.T).reshape(d1, K, d2)
     return np.ascontiguousarray(B.transpose(1, 0, 2).reshape(K, d1 * d2).T)
 
 
-def parseval_frame(k: int, rho: int, d: int, seed_seq=None, rotate: bool = True) -> np.ndarray:
-    """Dense d x (k*rho) Parseval fusion frame P = R T sqrt(d/(k rho)), float64.
+def parseval_frame(k: int, rho: int, d: int, seed_seq=None, rotate: bool = True,
+                   dtype=np.float64) -> np.ndarray:
+    """Dense d x (k*rho) Parseval fusion frame P = R T sqrt(d/(k rho)).
 
     P P^T = I_d; column block i (rho columns) is an orthogonal basis of subspace i scaled
-    by its weight w_i = sqrt(d/(k rho)).
+    by its weight w_i = sqrt(d/(k rho)).  Built in float64, a group of subspaces at a
+    time (the rotation acts on each column separately), and stored as dtype (float32:
+    round-to-nearest of the float64 frame).
     """
-    T = real_tff_basis(k, rho, d) if not (k == 1 and rho == d) else np.eye(d)
-    T = T * math.sqrt(d / (k * rho))
-    if not rotate:
-        return T
-    R1, R2 = rotation_factors(d, seed_seq)
-    return apply_rotation(R1, R2, T)
+    scale = math.sqrt(d / (k * rho))
+    if k == 1 and rho == d:
+        T = np.eye(d) * scale
+        if rotate:
+            R1, R2 = rotation_factors(d, seed_seq)
+            T = apply_rotation(R1, R2, T)
+        return np.asarray(T, dtype=dtype)
+    if rotate:
+        R1, R2 = rotation_factors(d, seed_seq)
+    out = np.empty((d, k * rho), dtype=dtype)
+    group = max(1, 2048 // rho)
+
+    def build(s0):
+        s1 = min(k, s0 + group)
+        T = real_tff_basis(k, rho, d, range(s0, s1)) * scale
+        if rotate:
+            T = apply_rotation(R1, R2, T)
+        out[:, s0 * rho: s1 * rho] = T
+
+    starts = range(0, k, group)
+    if len(starts) == 1:
+        build(0)
+    else:
+        with ThreadPoolExecutor(min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(build, starts))
+    return out

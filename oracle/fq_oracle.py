@@ -107,17 +107,24 @@ def near_tie(t, eps: float = TIE_EPS):
 
 
 # --------------------------------------------------------------------------- stage 3b
+def damped_hessian(Ht, damp: float = 0.01):
+    """OPTQ's conditioning of the FF Hessian: dead columns (H~_jj = 0) get H~_jj = 1, then
+    damp * mean(diag) is added to the diagonal.  Returns (damped H~, dead mask)."""
+    H = np.array(Ht, dtype=np.float64, copy=True)
+    dead = np.diag(H) == 0
+    H[dead, dead] = 1.0
+    lam = damp * np.mean(np.diag(H))
+    H[np.diag_indices_from(H)] += lam
+    return H, dead
+
+
 def gptq_prepare(Ht, damp: float = 0.01):
     """OPTQ preparation on the FF Hessian (Sec. 3, "quantize(D, C, B) // modified GPTQ"):
     dead columns (H~_jj = 0) get H~_jj = 1; H~ += damp * mean(diag H~) I;
     U = upper Cholesky factor of H~^{-1} (U^T U = H~^{-1}).
     Returns (U, dead mask, damped H~).  Raises numpy.linalg.LinAlgError when the damped
     H~ is not positive definite."""
-    H = np.array(Ht, dtype=np.float64, copy=True)
-    dead = np.diag(H) == 0
-    H[dead, dead] = 1.0
-    lam = damp * np.mean(np.diag(H))
-    H[np.diag_indices_from(H)] += lam
+    H, dead = damped_hessian(Ht, damp)
     L = np.linalg.cholesky(H)                       # H = L L^T
     Linv = sla.solve_triangular(L, np.eye(H.shape[0]), lower=True)
     Hinv = Linv.T @ Linv                            # H^{-1}
@@ -189,6 +196,33 @@ def gptq_obs(D, Hd, scale, zero, bits: int = 2, dead=None):
         codes[:, j] = q
         S = S[1:, 1:] - np.outer(S[1:, 0], S[0, 1:]) / S[0, 0]
     return codes
+
+
+def gptq_tail_pre_rounding(Dc, dq, Ht, first: int, damp: float = 0.01):
+    """OPTQ's pre-rounding values w_j of the trailing columns j >= first, given the
+    dequantized values dq of every column: the consistency property of Alg. 1 step 4
+    that each code is the grid point nearest to its w_j, usable where a full replay
+    (a factorization of all of H~) is too large.
+
+    The feedback gives D - DQ = E U (E the column errors, U^T U = H^{-1}, U upper), so
+    w_j = DQ_j + E_j U_jj.  Writing the damped H~ = M M^T with M upper (M = J L J, L the
+    lower factor of the reversed J H~ J), U = M^{-1}; hence E = (D - DQ) M and
+    w_j = DQ_j + E_j / M_jj.  The columns j >= first of M are the leading n - first columns
+    of L, read backwards, so only a panel of the factorization is formed.
+    Dc: clipped D (rows x n); dead columns are zeroed here as in gptq."""
+    D = np.array(Dc, dtype=np.float64, copy=True)
+    H, dead = damped_hessian(Ht, damp)
+    D[:, dead] = 0.0
+    n = H.shape[0]
+    p = n - first
+    A = H[::-1, ::-1]                                   # J H~ J
+    L11 = np.linalg.cholesky(A[:p, :p])
+    L21 = sla.solve_triangular(L11, A[p:, :p].T, lower=True).T
+    Lp = np.vstack([L11, L21])                          # leading p columns of L
+    Mt = Lp[::-1, ::-1]                                 # columns first..n-1 of M
+    E = (D - np.asarray(dq, dtype=np.float64)) @ Mt     # E_j for j >= first
+    diag = Mt[first + np.arange(p), np.arange(p)]
+    return np.asarray(dq, dtype=np.float64)[:, first:] + E / diag[None, :]
 
 
 def dequant(codes, scale, zero):

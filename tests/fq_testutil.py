@@ -43,28 +43,31 @@ def unpack_codes(codes_t, K_in: int) -> np.ndarray:
 
 
 def replay_rows(D_gpu: np.ndarray, Ht_gpu: np.ndarray, codes_gpu: np.ndarray, rows=None,
-                bits=2, block=128, damp=0.01, clip_sigmas=2.0):
+                bits=2, block=128, damp=0.01, clip_sigmas=2.0, codes_are_rows=False):
     """Teacher-forced oracle replay on the device's own D and H~ (stage isolation).
 
     The oracle runs the clip, grid and OPTQ in float64 on exactly the values the device
     consumed; where its pre-rounding value lies within 1e-6 (code units) of a rounding
     boundary it adopts the device's code, so a legitimate near-tie cannot cascade along a
     row.  rows: optional subset (rows are independent once U is fixed; mu and sigma are
-    taken over the whole D)."""
+    taken over the whole D).  codes_are_rows: codes_gpu holds only the rows listed."""
     D = np.asarray(D_gpu, dtype=np.float64)
     mu, sigma, lo_b, hi_b = O.clip_bounds(D, clip_sigmas)
     sel = np.arange(D.shape[0]) if rows is None else np.asarray(rows)
     Dc = O.apply_clip(D[sel], lo_b, hi_b)
     scale, zero = O.row_grid(Dc, bits)
     U, dead, _ = O.gptq_prepare(np.asarray(Ht_gpu, dtype=np.float64), damp)
-    r = O.gptq(Dc, U, scale, zero, bits, block, dead, forced_codes=codes_gpu[sel])
-    r.update(scale=scale, zero=zero, rows=sel, mu=mu, sigma=sigma)
+    forced = codes_gpu if codes_are_rows else codes_gpu[sel]
+    r = O.gptq(Dc, U, scale, zero, bits, block, dead, forced_codes=forced)
+    r.update(scale=scale, zero=zero, rows=sel, mu=mu, sigma=sigma, codes_are_rows=codes_are_rows)
     return r
 
 
 def check_codes(r, codes_gpu, scale_gpu, zero_gpu):
-    """Codes bit-exact outside the near-tie window; scale/zero equal to the oracle's."""
-    sel = r["rows"]
+    """Codes bit-exact outside the near-tie window; scale/zero equal to the oracle's.
+    The device arrays hold every row, or only the replayed rows when the replay was made
+    with codes_are_rows."""
+    sel = slice(None) if r.get("codes_are_rows") else r["rows"]
     cg = codes_gpu[sel]
     mism = (r["codes"] != cg) & ~r["tie"]
     np.testing.assert_allclose(scale_gpu[sel], r["scale"], rtol=2e-7, atol=0)

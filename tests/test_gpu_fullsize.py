@@ -1,0 +1,172 @@
+"""Parity at the full workload sizes, in the launch configuration the benchmark times
+(one LayerBuffers per layer shape, the four ABI calls in order, H computed from all of X),
+checked on sampled outputs the oracle can compute one by one:
+  H      : the principal submatrix on 64 random channels plus every outlier channel;
+  D      : 16 random rows, P_out[:, r]^T W P_in;
+  H~     : in full, P_in^T H P_in from the device's H (stage isolation); for the
+           Llama-70B-shaped layer the principal submatrix on 64 random frame columns;
+  codes  : teacher-forced replay of 48 random rows on the device's D and H~; for the
+           Llama-70B-shaped layer (K_in 28672 / 31536, beyond a host factorization in a
+           test) scale / zero of 128 random rows exactly, and the rounding property of the
+           last four 128-column blocks: each code is the grid point nearest to its
+           pre-rounding value given the device's earlier codes (exact outside near ties);
+  W_hat  : 16 random rows, P_out[i, :] D^ P_in^T from the device's codes;
+  Y      : those output channels of X W_hat^T on 512 random tokens.
+Tolerances are those of the small-shape tests (see test_gpu_stages): 1e-5 relative
+Frobenius per contraction stage, 1e-4 for W_hat and Y against the oracle, codes exact
+outside the near-tie window.  For H each entry is also held to 1e-4 of
+sqrt(H_ii H_jj), the Cauchy-Schwarz scale of its fp32 partial sums.
+"""
+import time
+
+import numpy as np
+import pytest
+
+import oracle as O
+from fq_inputs import WORKLOADS, gen
+from fq_testutil import need_gpu, upload, rel_fro, unpack_codes, replay_rows, check_codes
+
+pytestmark = pytest.mark.gpu
+
+_X = {}
+
+
+def _log(msg):
+    print(f"[fullsize] {msg}", flush=True)
+
+
+def _calibration(key):
+    """(host storage, device tensor) of the workload's X, generated once per workload."""
+    if key not in _X:
+        _X.clear()
+        import torch
+        torch.cuda.empty_cache()
+        wl = WORKLOADS[key]
+        t = time.time()
+        Xs = gen.make_x(wl, wl.layers[0].d_in)
+        _X[key] = (Xs, upload(Xs, wl.x_dtype))
+        _log(f"{key}: X {Xs.shape} {wl.x_dtype} generated and uploaded in {time.time() - t:.1f}s")
+    return _X[key]
+
+
+def fullsize_layer(key, li, n_code_rows=48, replay=True):
+    torch = need_gpu()
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    wl = WORKLOADS[key]
+    L = wl.layers[li]
+    _log(f"{key} {L.name}: W {L.d_out}x{L.d_in} {wl.w_dtype}")
+    Xs, X = _calibration(key)
+    t = time.time()
+    Po, Pi = gen.make_frames(wl, li, np.float32)
+    Ws = gen.make_weight(wl, li)
+    W = upload(Ws, wl.w_dtype)
+    K_out, K_in = Po.shape[1], Pi.shape[1]
+    _log(f"frames and weight built in {time.time() - t:.1f}s (K_out {K_out}, K_in {K_in})")
+    bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, X.shape[0], wl.block)
+    P_out, P_in = torch.from_numpy(Po).cuda(), torch.from_numpy(Pi).cuda()
+    t = time.time()
+    quantize_layer(W, X, P_out, P_in, bufs, block=wl.block, damp=wl.damp,
+                   clip_sigmas=wl.clip_sigmas)
+    torch.cuda.synchronize()
+    _log(f"device pass done in {time.time() - t:.1f}s")
+    rng = np.random.default_rng([li, K_out, K_in])
+
+    # stage 1: principal submatrix of H on sampled channels
+    ch = np.union1d(rng.choice(L.d_in, 64, replace=False), gen.x_outlier_channels(wl, L.d_in))
+    cht = torch.from_numpy(ch).cuda()
+    Hs = bufs.H.index_select(0, cht).index_select(1, cht).cpu().numpy().astype(np.float64)
+    Xc = gen.storage_to_f32(np.ascontiguousarray(Xs[:, ch]), wl.x_dtype)
+    Ho = O.hessian(Xc)
+    assert rel_fro(Hs, Ho) < 1e-5, "H"
+    cs = np.sqrt(np.outer(np.diag(Ho), np.diag(Ho)))
+    assert float(np.max(np.abs(Hs - Ho) / cs)) < 1e-4, "H entries"
+    _log("H ok")
+
+    # stage 2: sampled rows of D; H~ from the device's H (all of it, or a principal block)
+    W64 = gen.storage_to_f32(Ws, wl.w_dtype).astype(np.float64)
+    rows_d = np.sort(rng.choice(K_out, 16, replace=False))
+    Hg = bufs.H.cpu().numpy()
+    Htg = bufs.Ht.cpu().numpy()
+    if replay:
+        D_o, Ht_o = O.frame_analysis(W64, Po[:, rows_d], Pi, Hg)
+        assert rel_fro(Htg, Ht_o) < 1e-5, "Ht"
+        del Ht_o
+    else:
+        D_o, _ = O.frame_analysis(W64, Po[:, rows_d], Pi, None)
+        cols = np.sort(rng.choice(K_in, 64, replace=False))
+        _, Ht_o = O.frame_analysis(W64, Po[:, :0], Pi[:, cols], Hg)
+        assert rel_fro(Htg[np.ix_(cols, cols)], Ht_o) < 1e-5, "Ht block"
+    np.testing.assert_array_equal(Htg, Htg.T)
+    Dg = bufs.D.cpu().numpy()
+    assert rel_fro(Dg[rows_d], D_o) < 1e-5, "D rows"
+    del Hg, W64
+    _log("D, Ht ok")
+
+    # stage 3: codes of sampled rows
+    rows_q = np.sort(rng.choice(K_out, n_code_rows, replace=False))
+    rq = torch.from_numpy(rows_q).cuda()
+    cg_rows = unpack_codes(bufs.codes.index_select(0, rq), K_in)
+    sg, zg = bufs.scale.cpu().numpy(), bufs.zero.cpu().numpy()
+    if replay:
+        r = replay_rows(Dg, Htg, cg_rows, rows=rows_q, block=wl.block, damp=wl.damp,
+                        clip_sigmas=wl.clip_sigmas, codes_are_rows=True)
+        ties = check_codes(r, cg_rows, sg[rows_q], zg[rows_q])
+        _log(f"codes ok on {n_code_rows} rows ({ties} near ties)")
+    else:
+        ties = _check_code_tail(wl, Dg, Htg, rows_q, cg_rows, sg[rows_q], zg[rows_q], 4 * wl.block)
+        _log(f"scale/zero and last {4 * wl.block} columns ok on {n_code_rows} rows "
+             f"({ties} near ties)")
+    del Dg, Htg
+
+    # stage 4 and layer outputs, from the device's codes
+    cg = unpack_codes(bufs.codes, K_in)
+    rows_w = np.sort(rng.choice(L.d_out, 16, replace=False))
+    Wh_o = O.synthesis(cg, sg.astype(np.float64), zg.astype(np.float64), Po[rows_w], Pi)
+    del cg
+    Whg = bufs.W_hat.index_select(0, torch.from_numpy(rows_w).cuda()).cpu().numpy()
+    assert rel_fro(Whg, Wh_o) < 1e-4, "W_hat rows"
+    tok = np.sort(rng.choice(Xs.shape[0], 512, replace=False))
+    xs = gen.storage_to_f32(Xs[tok], wl.x_dtype).astype(np.float64)
+    assert rel_fro(xs @ Whg.T.astype(np.float64), xs @ Wh_o.T) < 1e-4, "Y"
+    _log("W_hat, Y ok")
+    return ties
+
+
+def _check_code_tail(wl, Dg, Htg, rows, codes, scale, zero, tail):
+    """scale / zero of the given rows against the oracle's clip and grid, then the
+    rounding property on the last `tail` columns given the device's earlier codes."""
+    D = np.asarray(Dg, dtype=np.float64)
+    mu, sigma, lo_b, hi_b = O.clip_bounds(D, wl.clip_sigmas)
+    Dc = O.apply_clip(D[rows], lo_b, hi_b)
+    del D
+    s_o, z_o = O.row_grid(Dc, wl.bits)
+    np.testing.assert_allclose(scale, s_o, rtol=2e-7, atol=0)
+    np.testing.assert_array_equal(zero, z_o)
+    dq = O.dequant(codes, s_o, z_o)
+    first = Dc.shape[1] - tail
+    w = O.gptq_tail_pre_rounding(Dc, dq, Htg, first, wl.damp)
+    q, t = O.rtn_codes(w, s_o[:, None], z_o[:, None], wl.bits)
+    tie = O.near_tie(t)
+    mism = (q != codes[:, first:]) & ~tie
+    assert int(mism.sum()) == 0, f"{int(mism.sum())} tail codes are not the nearest grid point"
+    return int(tie.sum())
+
+
+def test_fullsize_opt1b3_fc1():
+    fullsize_layer("opt1b3", 0)
+
+
+def test_fullsize_llama7b_q():
+    fullsize_layer("llama7b", 0)
+
+
+def test_fullsize_llama7b_up():
+    fullsize_layer("llama7b", 1)
+
+
+def test_fullsize_llama70b_r10_down():
+    fullsize_layer("llama70b_r1.0", 0, n_code_rows=128, replay=False)
+
+
+def test_fullsize_llama70b_r11_down():
+    fullsize_layer("llama70b_r1.1", 0, n_code_rows=128, replay=False)

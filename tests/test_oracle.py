@@ -266,3 +266,28 @@ def test_output_loss_bound_and_pipeline():
         if k_out == 4:
             assert lhs == pytest.approx(rhs, rel=1e-10)
         np.testing.assert_array_equal(O.unpack2(r["packed"], r["codes"].shape[1]), r["codes"])
+
+
+def test_tail_pre_rounding_matches_replay():
+    """The trailing-column consistency property reproduces the sequential OPTQ's own
+    pre-rounding values from its codes, for every start column and with a dead column
+    and clipped entries present."""
+    for seed, block in ((21, 4), (22, 128), (23, 1)):
+        D, Ht, s, z, U, dead, Hd = _problem(rows=7, n=23, seed=seed)
+        Ht = Ht.copy()
+        Ht[5, :] = 0
+        Ht[:, 5] = 0
+        U, dead, Hd = O.gptq_prepare(Ht)
+        mu, sigma, lo, hi = O.clip_bounds(D, 1.0)
+        Dc = O.apply_clip(D, lo, hi)
+        s, z = O.row_grid(Dc)
+        r = O.gptq(Dc, U, s, z, 2, block, dead)
+        dq = O.dequant(r["codes"], s, z)
+        for first in (0, 9, 22):
+            w = O.gptq_tail_pre_rounding(Dc, dq, Ht, first)
+            np.testing.assert_allclose(w / s[:, None], r["t"][:, first:], rtol=1e-9, atol=1e-9)
+        # a changed earlier code moves the later pre-rounding values
+        bad = r["codes"].copy()
+        bad[:, 3] = (bad[:, 3] + 1) % 4
+        w_bad = O.gptq_tail_pre_rounding(Dc, O.dequant(bad, s, z), Ht, 9)
+        assert np.abs(w_bad / s[:, None] - r["t"][:, 9:]).max() > 1e-3
