@@ -126,9 +126,18 @@ static int64_t rup32(int64_t x) { return (x + 31) / 32 * 32; }
 //   pot  = P_out^T  [K_out x pad(d_out)]    wt = W^T  [d_in x pad(d_out)]
 //   t    = P_out^T W [K_out x pad(d_in)]    pit = P_in^T [K_in x pad(d_in)]
 //   h    = H [d_in x pad(d_in)]             gt = P_in^T H [K_in x pad(d_in)]
+// Analysis planes.  Every product reads both operands with the reduction index as the
+// row (row-contiguous in the other index), so each operand is the caller's array as laid
+// out, split into bf16 planes with rows and columns zero-padded:
+//   po  = P_out [pad(d_out) x pad8(K_out)]     wn = W [pad(d_out) x pad(d_in)]
+//   pi  = P_in  [pad(d_in) x pad8(K_in)]       h  = H [pad(d_in) x pad(d_in)]
+//   tt  = T^T = W^T P_out [pad(d_in) x pad8(K_out)]   g = H P_in [pad(d_in) x pad8(K_in)]
+// D = T P_in and H~ = P_in^T G then need no transposed copy.  bf16 weights whose shape
+// needs no padding are read in place.
 struct AnaLayout {
-  u16 *pot_hi, *pot_lo, *pit_hi, *pit_lo, *wt_hi, *wt_lo, *t_hi, *t_lo, *h_hi, *h_lo, *gt_hi, *gt_lo;
-  int64_t lo_, li_;   // pad(d_out), pad(d_in)
+  u16 *po_hi, *po_lo, *pi_hi, *pi_lo, *wn_hi, *wn_lo, *tt_hi, *tt_lo, *h_hi, *h_lo, *g_hi, *g_lo;
+  int64_t lo_, li_;   // pad(d_out), pad(d_in): multiples of 32
+  int64_t ko8, ki8;   // pad8(K_out), pad8(K_in)
 };
 
 static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out, int64_t K_in,
@@ -137,18 +146,20 @@ static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out
   AnaLayout l{};
   l.lo_ = rup32(d_out);
   l.li_ = rup32(d_in);
-  l.pot_hi = c.take<u16>((size_t)K_out * l.lo_);
-  l.pot_lo = c.take<u16>((size_t)K_out * l.lo_);
-  l.pit_hi = c.take<u16>((size_t)K_in * l.li_);
-  l.pit_lo = c.take<u16>((size_t)K_in * l.li_);
-  l.wt_hi = c.take<u16>((size_t)d_in * l.lo_);
-  if (wt != FQ_BF16) l.wt_lo = c.take<u16>((size_t)d_in * l.lo_);
-  l.t_hi = c.take<u16>((size_t)K_out * l.li_);
-  l.t_lo = c.take<u16>((size_t)K_out * l.li_);
-  l.h_hi = c.take<u16>((size_t)d_in * l.li_);
-  l.h_lo = c.take<u16>((size_t)d_in * l.li_);
-  l.gt_hi = c.take<u16>((size_t)K_in * l.li_);
-  l.gt_lo = c.take<u16>((size_t)K_in * l.li_);
+  l.ko8 = (K_out + 7) / 8 * 8;
+  l.ki8 = (K_in + 7) / 8 * 8;
+  l.po_hi = c.take<u16>((size_t)l.lo_ * l.ko8);
+  l.po_lo = c.take<u16>((size_t)l.lo_ * l.ko8);
+  l.pi_hi = c.take<u16>((size_t)l.li_ * l.ki8);
+  l.pi_lo = c.take<u16>((size_t)l.li_ * l.ki8);
+  l.wn_hi = c.take<u16>((size_t)l.lo_ * l.li_);
+  if (wt != FQ_BF16) l.wn_lo = c.take<u16>((size_t)l.lo_ * l.li_);
+  l.tt_hi = c.take<u16>((size_t)l.li_ * l.ko8);
+  l.tt_lo = c.take<u16>((size_t)l.li_ * l.ko8);
+  l.h_hi = c.take<u16>((size_t)l.li_ * l.li_);
+  l.h_lo = c.take<u16>((size_t)l.li_ * l.li_);
+  l.g_hi = c.take<u16>((size_t)l.li_ * l.ki8);
+  l.g_lo = c.take<u16>((size_t)l.li_ * l.ki8);
   if (L) *L = l;
   return c.off + 256;
 }
@@ -181,18 +192,23 @@ static size_t quant_layout(int64_t K_out, int64_t K_in, int block, void* ws, Qua
   q.scale64 = c.take<double>((size_t)K_out);
   q.zero64 = c.take<double>((size_t)K_out);
   q.inv_rdiag = c.take<double>((size_t)2 * K_in);
+  q.linv = c.take<double>(64 * 64);
   q.dead = c.take<uint8_t>((size_t)K_in);
   q.flags = c.take<int>(4);
   if (Q) *Q = q;
   return c.off + 256;
 }
 
-// Synthesis planes (K-contiguous, zero-padded in K):
-//   qt  = (codes - zero)^T [K_in x pad(K_out)]   pl = P_out diag(scale) [d_out x pad(K_out)]
-//   n   = pl (codes - zero) [d_out x pad(K_in)]  pi = P_in [d_in x pad(K_in)]
+// Synthesis planes (zero-padded):
+//   q  = codes - zero           [pad(K_out) x pad(K_in)]   (natural layout, exact in bf16)
+//   pl = P_out diag(scale)      [d_out x pad(K_out)]       pi = P_in [d_in x pad(K_in)]
+//   nt = (pl q)^T = q^T pl^T    [pad(K_in) x pad8(d_out)]  (rows beyond K_in come out 0)
+// W^ = pl q P_in^T is then nt^T P_in^T: the first product reads q with the reduction
+// index as the row and pl with it as the column, the second nt and P_in likewise.
 struct SynLayout {
-  u16 *qt, *pl_hi, *pl_lo, *pi_hi, *pi_lo, *n_hi, *n_lo;
-  int64_t ko, ki;   // pad(K_out), pad(K_in)
+  u16 *q, *pl_hi, *pl_lo, *pi_hi, *pi_lo, *nt_hi, *nt_lo;
+  int64_t ko, ki;   // pad(K_out), pad(K_in): multiples of 32
+  int64_t do8;      // pad8(d_out)
 };
 
 static size_t synthesis_layout(int64_t K_out, int64_t K_in, int64_t d_out, int64_t d_in,
@@ -201,13 +217,14 @@ static size_t synthesis_layout(int64_t K_out, int64_t K_in, int64_t d_out, int64
   SynLayout l{};
   l.ko = rup32(K_out);
   l.ki = rup32(K_in);
-  l.qt = c.take<u16>((size_t)K_in * l.ko);
+  l.do8 = (d_out + 7) / 8 * 8;
+  l.q = c.take<u16>((size_t)l.ko * l.ki);
   l.pl_hi = c.take<u16>((size_t)d_out * l.ko);
   l.pl_lo = c.take<u16>((size_t)d_out * l.ko);
   l.pi_hi = c.take<u16>((size_t)d_in * l.ki);
   l.pi_lo = c.take<u16>((size_t)d_in * l.ki);
-  l.n_hi = c.take<u16>((size_t)d_out * l.ki);
-  l.n_lo = c.take<u16>((size_t)d_out * l.ki);
+  l.nt_hi = c.take<u16>((size_t)l.ki * l.do8);
+  l.nt_lo = c.take<u16>((size_t)l.ki * l.do8);
   if (L) *L = l;
   return c.off + 256;
 }
@@ -349,8 +366,18 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
     g.npass = 3;
     g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1; g.pa[2] = 1; g.pb[2] = 0;
   };
+  // C (+ or SPLIT / SYM) = A B with A(m, k) at a[k * lda + m] and B(k, n) at b[k * ldb + n]
+  auto mn_gemm = [](int M, int N, int K, const u16* a0, const u16* a1, int64_t lda,
+                    const u16* b0, const u16* b1, int64_t ldb) {
+    GemmDesc g;
+    g.M = M; g.N = N; g.K = K;
+    g.a[0] = a0; g.a[1] = a1; g.lda = lda; g.a_kmajor = false;
+    g.b[0] = b0; g.b[1] = b1; g.ldb = ldb; g.b_kmajor = false;
+    return g;
+  };
   if (d_in > 0 && K_in > 0) {
-    e = split_bf16_t(P_in, 0, K_in, (int)d_in, (int)K_in, L.pit_hi, L.pit_lo, L.li_, s);
+    e = split_bf16_pad(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ki8,
+                       (int)L.li_, s);
     if (e != hipSuccess) return hip_fail(e, "split P_in");
   }
   if (D && K_out > 0 && K_in > 0) {
@@ -358,33 +385,39 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       e = fill_zero_f32(D, (int)K_out, (int)K_in, K_in, s);
       if (e != hipSuccess) return hip_fail(e, "zero D");
     } else {
-      e = split_bf16_t(P_out, 0, K_out, (int)d_out, (int)K_out, L.pot_hi, L.pot_lo, L.lo_, s);
+      e = split_bf16_pad(P_out, 0, K_out, (int)d_out, (int)K_out, nullptr, L.po_hi, L.po_lo, L.ko8,
+                         (int)L.lo_, s);
       if (e != hipSuccess) return hip_fail(e, "split P_out");
-      // W^T: bf16 weights are exact in one plane; f16/f32 weights take a bf16 pair
+      // W: bf16 weights are exact in one plane and are read in place when no padding is
+      // needed; otherwise a zero-padded copy (f16 / f32 weights take a bf16 pair)
       const int in_t = wt == FQ_BF16 ? 2 : (wt == FQ_F16 ? 1 : 0);
-      e = split_bf16_t(W, in_t, d_in, (int)d_out, (int)d_in, L.wt_hi, wt == FQ_BF16 ? nullptr : L.wt_lo,
-                       L.lo_, s);
-      if (e != hipSuccess) return hip_fail(e, "split W");
-      // T = P_out^T W  (K_out x d_in), emitted as a bf16 pair
-      GemmDesc g;
-      g.M = (int)K_out; g.N = (int)d_in; g.K = (int)L.lo_;
-      g.a[0] = L.pot_hi; g.a[1] = L.pot_lo; g.lda = L.lo_; g.a_kmajor = true;
-      g.b[0] = L.wt_hi; g.b[1] = L.wt_lo; g.ldb = L.lo_; g.b_kmajor = true;
+      const u16* wb0 = L.wn_hi;
+      const u16* wb1 = L.wn_lo;
+      int64_t ldw = L.li_;
+      if (wt == FQ_BF16 && d_out == L.lo_ && d_in == L.li_ && aligned16(W)) {
+        wb0 = (const u16*)W;
+        ldw = d_in;
+      } else {
+        e = split_bf16_pad(W, in_t, d_in, (int)d_out, (int)d_in, nullptr, L.wn_hi,
+                           wt == FQ_BF16 ? nullptr : L.wn_lo, L.li_, (int)L.lo_, s);
+        if (e != hipSuccess) return hip_fail(e, "split W");
+      }
+      // T^T = W^T P_out  (pad(d_in) x K_out; rows beyond d_in come out zero), bf16 pair
+      GemmDesc g = mn_gemm((int)L.li_, (int)K_out, (int)L.lo_, wb0, wb1, ldw, L.po_hi, L.po_lo,
+                           L.ko8);
       if (wt != FQ_BF16) {
         three(g);
       } else {
         g.npass = 2;
-        g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
+        g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1;
       }
-      g.epi = EPI_SPLIT; g.c_hi = L.t_hi; g.c_lo = L.t_lo; g.ldc = L.li_; g.ldc_pad = L.li_;
+      g.epi = EPI_SPLIT; g.c_hi = L.tt_hi; g.c_lo = L.tt_lo; g.ldc = L.ko8; g.ldc_pad = L.ko8;
       g.name = "gemm_analysis_w1";
       e = gemm_run(g, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 1");
       // D = T P_in  (K_out x K_in)
-      GemmDesc g2;
-      g2.M = (int)K_out; g2.N = (int)K_in; g2.K = (int)L.li_;
-      g2.a[0] = L.t_hi; g2.a[1] = L.t_lo; g2.lda = L.li_; g2.a_kmajor = true;
-      g2.b[0] = L.pit_hi; g2.b[1] = L.pit_lo; g2.ldb = L.li_; g2.b_kmajor = true;
+      GemmDesc g2 = mn_gemm((int)K_out, (int)K_in, (int)L.li_, L.tt_hi, L.tt_lo, L.ko8, L.pi_hi,
+                            L.pi_lo, L.ki8);
       three(g2);
       g2.epi = EPI_F32; g2.c = D; g2.ldc = K_in;
       g2.name = "gemm_analysis_w2";
@@ -397,23 +430,20 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       e = fill_zero_f32(Ht, (int)K_in, (int)K_in, K_in, s);
       if (e != hipSuccess) return hip_fail(e, "zero Ht");
     } else {
-      e = split_bf16_pad(H, 0, d_in, (int)d_in, (int)d_in, nullptr, L.h_hi, L.h_lo, L.li_, s);
+      e = split_bf16_pad(H, 0, d_in, (int)d_in, (int)d_in, nullptr, L.h_hi, L.h_lo, L.li_,
+                         (int)L.li_, s);
       if (e != hipSuccess) return hip_fail(e, "split H");
-      // G^T = P_in^T H  (K_in x d_in; H is symmetric, so row i of H is column i)
-      GemmDesc g;
-      g.M = (int)K_in; g.N = (int)d_in; g.K = (int)L.li_;
-      g.a[0] = L.pit_hi; g.a[1] = L.pit_lo; g.lda = L.li_; g.a_kmajor = true;
-      g.b[0] = L.h_hi; g.b[1] = L.h_lo; g.ldb = L.li_; g.b_kmajor = true;
+      // G = H P_in  (pad(d_in) x K_in; H is symmetric, rows beyond d_in come out zero)
+      GemmDesc g = mn_gemm((int)L.li_, (int)K_in, (int)L.li_, L.h_hi, L.h_lo, L.li_, L.pi_hi,
+                           L.pi_lo, L.ki8);
       three(g);
-      g.epi = EPI_SPLIT; g.c_hi = L.gt_hi; g.c_lo = L.gt_lo; g.ldc = L.li_; g.ldc_pad = L.li_;
+      g.epi = EPI_SPLIT; g.c_hi = L.g_hi; g.c_lo = L.g_lo; g.ldc = L.ki8; g.ldc_pad = L.ki8;
       g.name = "gemm_analysis_h1";
       e = gemm_run(g, nullptr, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 3");
       // Ht = P_in^T G  (K_in x K_in, upper tiles mirrored)
-      GemmDesc g2;
-      g2.M = (int)K_in; g2.N = (int)K_in; g2.K = (int)L.li_;
-      g2.a[0] = L.pit_hi; g2.a[1] = L.pit_lo; g2.lda = L.li_; g2.a_kmajor = true;
-      g2.b[0] = L.gt_hi; g2.b[1] = L.gt_lo; g2.ldb = L.li_; g2.b_kmajor = true;
+      GemmDesc g2 = mn_gemm((int)K_in, (int)K_in, (int)L.li_, L.pi_hi, L.pi_lo, L.ki8, L.g_hi,
+                            L.g_lo, L.ki8);
       three(g2);
       g2.epi = EPI_SYM; g2.c = Ht; g2.ldc = K_in;
       g2.name = "gemm_analysis_h2";
@@ -454,7 +484,7 @@ fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int6
   prof_end(s);
   if ((e = q_stats(D, K_out, K_in, clip_sigmas, Q, s)) != hipSuccess) return hip_fail(e, "stats");
   if ((e = q_hdiag_build(Ht, K_in, damp, Q, s)) != hipSuccess) return hip_fail(e, "hessian prep");
-  if ((e = q_cholesky(Q.A, K_in, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
+  if ((e = q_cholesky(Q.A, K_in, Q.linv, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
   if ((e = q_reverse_upper(Q.A, K_in, Q.R, Q.inv_rdiag, s)) != hipSuccess) return hip_fail(e, "reverse");
   if ((e = q_clip_grid(D, K_out, K_in, bits, Q, scale, zero, s)) != hipSuccess) return hip_fail(e, "clip/grid");
   const int64_t ldr = res_width(K_in, block);
@@ -517,25 +547,26 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
   SynLayout L;
   synthesis_layout(K_out, K_in, d_out, d_in, base, &L);
-  if ((e = dequant_bf16_t(codes, zero, K_out, K_in, L.qt, L.ko, s)) != hipSuccess) return hip_fail(e, "dequant");
-  if ((e = split_bf16_pad(P_out, 0, K_out, (int)d_out, (int)K_out, scale, L.pl_hi, L.pl_lo, L.ko, s)) != hipSuccess)
+  if ((e = dequant_bf16(codes, zero, K_out, K_in, L.q, L.ki, L.ko, s)) != hipSuccess)
+    return hip_fail(e, "dequant");
+  if ((e = split_bf16_pad(P_out, 0, K_out, (int)d_out, (int)K_out, scale, L.pl_hi, L.pl_lo, L.ko, (int)d_out, s)) != hipSuccess)
     return hip_fail(e, "split P_out");
-  if ((e = split_bf16_pad(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ki, s)) != hipSuccess)
+  if ((e = split_bf16_pad(P_in, 0, K_in, (int)d_in, (int)K_in, nullptr, L.pi_hi, L.pi_lo, L.ki, (int)d_in, s)) != hipSuccess)
     return hip_fail(e, "split P_in");
-  // N = (P_out diag(scale)) (codes - zero)   (d_out x K_in), bf16 pair
+  // N^T = q^T (P_out diag(scale))^T   (pad(K_in) x d_out), bf16 pair
   GemmDesc g;
-  g.M = (int)d_out; g.N = (int)K_in; g.K = (int)L.ko;
-  g.a[0] = L.pl_hi; g.a[1] = L.pl_lo; g.lda = L.ko; g.a_kmajor = true;
-  g.b[0] = L.qt; g.ldb = L.ko; g.b_kmajor = true;
+  g.M = (int)L.ki; g.N = (int)d_out; g.K = (int)L.ko;
+  g.a[0] = L.q; g.lda = L.ki; g.a_kmajor = false;
+  g.b[0] = L.pl_hi; g.b[1] = L.pl_lo; g.ldb = L.ko; g.b_kmajor = true;
   g.npass = 2;
-  g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 1; g.pb[1] = 0;
-  g.epi = EPI_SPLIT; g.c_hi = L.n_hi; g.c_lo = L.n_lo; g.ldc = L.ki; g.ldc_pad = L.ki;
+  g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1;
+  g.epi = EPI_SPLIT; g.c_hi = L.nt_hi; g.c_lo = L.nt_lo; g.ldc = L.do8; g.ldc_pad = L.do8;
   g.name = "gemm_synthesis_1";
   if ((e = gemm_run(g, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 1");
   // W_hat = N P_in^T  (d_out x d_in)
   GemmDesc g2;
   g2.M = (int)d_out; g2.N = (int)d_in; g2.K = (int)L.ki;
-  g2.a[0] = L.n_hi; g2.a[1] = L.n_lo; g2.lda = L.ki; g2.a_kmajor = true;
+  g2.a[0] = L.nt_hi; g2.a[1] = L.nt_lo; g2.lda = L.do8; g2.a_kmajor = false;
   g2.b[0] = L.pi_hi; g2.b[1] = L.pi_lo; g2.ldb = L.ki; g2.b_kmajor = true;
   g2.npass = 3;
   g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;

@@ -59,14 +59,11 @@ hipError_t syrk_reduce(const float* partial, int N, int ksplit, float* H, int64_
 // (applied in fp32 before the split).  Element type: 0 = f32, 1 = f16.
 hipError_t split_bf16(const void* in, int in_type, int64_t ld_in, int rows, int cols,
                       const float* col_scale, u16* hi, u16* lo, int64_t ld_out, hipStream_t s);
-// Same with zero padding: out has ld_out >= cols columns, [cols, ld_out) are 0.
-// Element type 2 = bf16.
+// Same with zero padding: out has rows_out >= rows rows and ld_out >= cols columns; rows
+// [rows, rows_out) and columns [cols, ld_out) are 0.  Element type 2 = bf16.
 hipError_t split_bf16_pad(const void* in, int in_type, int64_t ld_in, int rows, int cols,
                           const float* col_scale, u16* hi, u16* lo, int64_t ld_out,
-                          hipStream_t s);
-// Transposing split: out[c * ld_out + r] for r < rows, zero for rows <= r < ld_out.
-hipError_t split_bf16_t(const void* in, int in_type, int64_t ld_in, int rows, int cols, u16* hi,
-                        u16* lo, int64_t ld_out, hipStream_t s);
+                          int rows_out, hipStream_t s);
 hipError_t fill_zero_f32(float* p, int rows, int cols, int64_t ld, hipStream_t s);
 
 // ---------------------------------------------------------------- fp64 path
@@ -81,6 +78,7 @@ struct QuantScratch {
   double* scale64;    // K_out
   double* zero64;     // K_out
   double* inv_rdiag;  // K_in
+  double* linv;       // 64 x 64: inverse of the current diagonal block of the factor
   uint8_t* dead;      // K_in
   int* flags;         // [0] not PD, [1] non-finite
 };
@@ -89,8 +87,8 @@ hipError_t q_stats(const float* D, int64_t rows, int64_t cols, double clip_sigma
                    QuantScratch& w, hipStream_t s);
 hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& w,
                          hipStream_t s);
-// Blocked lower Cholesky of A (K x K, in place).
-hipError_t q_cholesky(double* A, int64_t K, int* flags, hipStream_t s);
+// Blocked lower Cholesky of A (K x K, in place); Z: 64 x 64 doubles of scratch.
+hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s);
 hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rdiag,
                            hipStream_t s);
 hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, QuantScratch& w,
@@ -106,11 +104,9 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
                  bool lower_only, hipStream_t s, const char* name, int tile);
 hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* out,
                    hipStream_t s);
+// out[r * ld_out + c] = code[r][c] - zero[r] (bf16) on a rows_out x ld_out plane, zero
+// outside rows x cols; ld_out a multiple of 16 (and 16-byte aligned rows).
 hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
-                        u16* out, int64_t ld_out, hipStream_t s);
-// Transposed dequantization: out[c * ld_out + r] = code[r][c] - zero[r] (bf16), zero for
-// rows <= r < ld_out.
-hipError_t dequant_bf16_t(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
-                          u16* out, int64_t ld_out, hipStream_t s);
+                        u16* out, int64_t ld_out, int64_t rows_out, hipStream_t s);
 
 }  // namespace fq

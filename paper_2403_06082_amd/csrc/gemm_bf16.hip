@@ -43,6 +43,7 @@ struct KParams {
   int pa0, pa1, pa2, pb0, pb1, pb2;
   float* c; int64_t ldc;
   u16* c_hi; u16* c_lo;
+  int ldc_pad;          // EPI_SPLIT: columns [N, ldc_pad) of the output are written as 0
   int aligned_a, aligned_b;
   int tiles_m, tiles_n, ntiles;
   int ksplit, k_per_split;
@@ -406,15 +407,17 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
           // tile-major: tile index of (tm, tn) in the upper triangle
           const int tidx = tm * p.tiles_n - (tm * (tm - 1)) / 2 + (tn - tm);
           dst[(int64_t)tidx * (BM * BN) + rl * BN + cl] = x;
+        } else if (EPI == EPI_SPLIT) {
+          if (row < p.M && col < p.ldc_pad) {
+            const bool in = col < p.N;
+            const uint32_t h = in ? bf16_rne_bits(x) : 0u;
+            const uint32_t l = in ? bf16_rne_bits(x - __uint_as_float(h << 16)) : 0u;
+            p.c_hi[(int64_t)row * p.ldc + col] = (u16)h;
+            p.c_lo[(int64_t)row * p.ldc + col] = (u16)l;
+          }
         } else if (row < p.M && col < p.N) {
           if (EPI == EPI_F32) {
             p.c[(int64_t)row * p.ldc + col] = x;
-          } else if (EPI == EPI_SPLIT) {
-            const uint32_t h = bf16_rne_bits(x);
-            const float hf = __uint_as_float(h << 16);
-            const uint32_t l = bf16_rne_bits(x - hf);
-            p.c_hi[(int64_t)row * p.ldc + col] = (u16)h;
-            p.c_lo[(int64_t)row * p.ldc + col] = (u16)l;
           } else {  // EPI_SYM
             if (row <= col) {
               p.c[(int64_t)row * p.ldc + col] = x;
@@ -429,7 +432,7 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
 
 // ------------------------------------------------------------------ async GEMM
 // Global tiles go straight to LDS with global_load_lds_dwordx4 (no register staging)
-// through a 4-stage ring of 256 x 32 tiles fetched three stages ahead; one barrier per
+// through a 5-stage ring of 256 x 32 tiles (all 160 KiB of LDS) fetched four stages ahead; one barrier per
 // stage.  K must be a multiple of 32 (operand planes are zero-padded in K).
 //  * K-major operand (X(r, k) at x[r * ld + k]): LDS rows r of 4 chunks of 8 k-values,
 //    chunk c stored in slot c ^ ((r >> 2) & 3); fragments are plain 16-byte reads.
@@ -440,7 +443,7 @@ __global__ __launch_bounds__(NT, 1) void k_gemm(KParams p) {
 //    4 values of k-row j / 4 and lane i receives the 4 k-values of column i).  Requires
 //    M (N) to be a multiple of 8; columns beyond are read from the last valid chunk.
 // All fragment reads are bank-conflict free.
-constexpr int ABK = 32, ANST = 4;
+constexpr int ABK = 32, ANST = 5;
 constexpr int ATILE = BM * ABK;                  // u16 elements per operand per stage
 
 struct AParams {
@@ -560,6 +563,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
   __shared__ __attribute__((aligned(16))) u16 st1[2 * ATILE];
   __shared__ __attribute__((aligned(16))) u16 st2[2 * ATILE];
   __shared__ __attribute__((aligned(16))) u16 st3[2 * ATILE];
+  __shared__ __attribute__((aligned(16))) u16 st4[2 * ATILE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -657,43 +661,85 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
     asm volatile("" ::: "memory");
   };
 
-  // Software pipeline over a 4-slot ring with stages s + 1 and s + 2 in flight while
-  // stage s is multiplied; fragments of the next k-slice are read from LDS while the
+  // Software pipeline over a 5-slot ring (all of the LDS) with stages s + 1 .. s + 3 in
+  // flight while stage s is multiplied; fragments of the next k-slice are read from LDS while the
   // current one is in the matrix cores.
   constexpr unsigned PER = 2 * NI;               // DMA instructions per stage and wave
   uint4 a0[NBM], b0[NBN], a1[NBM], b1[NBN];
+  // LDS reads per fragment set and MFMAs per k-slice, for the interleaving hints
+  constexpr int NDS = (AMN ? 2 * NBM : NBM) + (BMN ? 2 * NBN : NBN);
+  constexpr int NMF = NBM * NBN;
+  auto interleave = [] {
+#pragma unroll
+    for (int i = 0; i < NMF; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                      // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, (NDS + NMF - 1) / NMF, 0);  // LDS reads
+    }
+  };
+  // wait until this wave's DMA of stage t has landed, given the last stage issued
+  auto wait_stage = [&](int t, int issued_last) {
+    const int ahead = issued_last - t;          // stages issued after t
+    if (ahead >= 3) __builtin_amdgcn_s_waitcnt(waitcnt_vm(3 * PER));
+    else if (ahead == 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * PER));
+    else if (ahead == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(PER));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  };
   auto step = [&](int s, const char* cur, const char* nxt, char* refill) {
     load(cur, 1, a1, b1);
     mma(a0, b0);
+    interleave();
     if (s + 1 < nstage) {
-      if (s + 2 < nstage) __builtin_amdgcn_s_waitcnt(waitcnt_vm(PER));
-      else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+      wait_stage(s + 1, min(nstage - 1, s + ANST - 2));
       barrier();
-      if (s + 3 < nstage) issue(refill);
+      if (s + ANST - 1 < nstage) issue(refill);
       load(nxt, 0, a0, b0);
     }
     mma(a1, b1);
+    interleave();
+  };
+
+  // steady-state step: stages s + 1 .. s + 3 issued, stage s + 4 exists; straight-line
+  // code, so that the wait counts before the MFMAs cover only the reads they need
+  auto step_full = [&](const char* cur, const char* nxt, char* refill) {
+    load(cur, 1, a1, b1);
+    mma(a0, b0);
+    interleave();
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * PER));
+    barrier();
+    issue(refill);
+    load(nxt, 0, a0, b0);
+    mma(a1, b1);
+    interleave();
   };
 
   char* const r0 = reinterpret_cast<char*>(st0);
   char* const r1 = reinterpret_cast<char*>(st1);
   char* const r2 = reinterpret_cast<char*>(st2);
   char* const r3 = reinterpret_cast<char*>(st3);
+  char* const r4 = reinterpret_cast<char*>(st4);
   if (nstage > 0) {
     issue(r0);
     if (nstage > 1) issue(r1);
     if (nstage > 2) issue(r2);
-    if (nstage > 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * PER));
-    else if (nstage > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(PER));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    if (nstage > 3) issue(r3);
+    wait_stage(0, min(nstage - 1, ANST - 2));
     barrier();
     load(r0, 0, a0, b0);
   }
-  for (int s = 0; s < nstage; s += 4) {
-    step(s, r0, r1, r3);
+  int s0 = 0;
+  for (; s0 + 8 < nstage; s0 += 5) {
+    step_full(r0, r1, r4);
+    step_full(r1, r2, r0);
+    step_full(r2, r3, r1);
+    step_full(r3, r4, r2);
+    step_full(r4, r0, r3);
+  }
+  for (int s = s0; s < nstage; s += 5) {
+    step(s, r0, r1, r4);
     if (s + 1 < nstage) step(s + 1, r1, r2, r0);
     if (s + 2 < nstage) step(s + 2, r2, r3, r1);
-    if (s + 3 < nstage) step(s + 3, r3, r0, r2);
+    if (s + 3 < nstage) step(s + 3, r3, r4, r2);
+    if (s + 4 < nstage) step(s + 4, r4, r0, r3);
   }
 
   // 32x32 accumulator layout: value v of lane l is row 8*(v/4) + 4*(l/32) + v%4,
@@ -839,14 +885,14 @@ __global__ void k_fill_zero(float* p, int rows, int cols, int64_t ld) {
 template <typename T>
 __global__ void k_split_pad(const T* __restrict__ in, int64_t ld_in, int rows, int cols,
                             const float* __restrict__ col_scale, u16* __restrict__ hi,
-                            u16* __restrict__ lo, int64_t ld_out) {
-  const int64_t total = (int64_t)rows * ld_out;
+                            u16* __restrict__ lo, int64_t ld_out, int rows_out) {
+  const int64_t total = (int64_t)rows_out * ld_out;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * blockDim.x) {
     const int64_t r = e / ld_out;
     const int c = (int)(e - r * ld_out);
     uint32_t h = 0, l = 0;
-    if (c < cols) {
+    if (c < cols && r < rows) {
       float x = ld_f(in + r * ld_in + c);
       if (col_scale) x *= col_scale[c];
       h = bf16_rne_bits(x);
@@ -854,34 +900,6 @@ __global__ void k_split_pad(const T* __restrict__ in, int64_t ld_in, int rows, i
     }
     hi[e] = (u16)h;
     if (lo) lo[e] = (u16)l;
-  }
-}
-
-// Transposing split: out[c * ld_out + r] = bf16 pair of in[r][c] for r < rows, 0 for
-// rows <= r < ld_out.  64 x 64 tiles through LDS; grid (ceil(cols/64), ceil(ld_out/64)).
-template <typename T>
-__global__ __launch_bounds__(256) void k_split_t(const T* __restrict__ in, int64_t ld_in, int rows,
-                                                 int cols, u16* __restrict__ hi,
-                                                 u16* __restrict__ lo, int64_t ld_out) {
-  __shared__ float tile[64][65];
-  const int c0 = blockIdx.x * 64;
-  const int64_t r0 = (int64_t)blockIdx.y * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    const int64_t gr = r0 + r;
-    const int gc = c0 + tx;
-    tile[r][tx] = (gr < rows && gc < cols) ? ld_f(in + gr * ld_in + gc) : 0.f;
-  }
-  __syncthreads();
-  for (int c = ty; c < 64; c += 4) {
-    const int gc = c0 + c;
-    const int64_t gr = r0 + tx;
-    if (gc < cols && gr < ld_out) {
-      const float x = tile[tx][c];
-      const uint32_t h = bf16_rne_bits(x);
-      hi[(int64_t)gc * ld_out + gr] = (u16)h;
-      if (lo) lo[(int64_t)gc * ld_out + gr] = (u16)bf16_rne_bits(x - __uint_as_float(h << 16));
-    }
   }
 }
 
@@ -908,12 +926,6 @@ bool dispatch_epi(const KParams& p, int epi, int grid, hipStream_t s) {
   return false;
 }
 
-// waves per work-group of the asynchronous GEMM (FQ_ASYNC_WAVES=4|8 overrides, for tuning)
-int async_waves_from_env() {
-  const char* v = getenv("FQ_ASYNC_WAVES");
-  return (v && atoi(v) == 4) ? 4 : 8;
-}
-int g_async_waves = async_waves_from_env();
 
 }  // namespace
 
@@ -937,6 +949,7 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
   p.pa0 = d.pa[0]; p.pa1 = d.pa[1]; p.pa2 = d.pa[2];
   p.pb0 = d.pb[0]; p.pb1 = d.pb[1]; p.pb2 = d.pb[2];
   p.c = d.c; p.ldc = d.ldc; p.c_hi = d.c_hi; p.c_lo = d.c_lo;
+  p.ldc_pad = (int)(d.ldc_pad > d.N ? d.ldc_pad : d.N);
   // 16-byte aligned rows; per-thread byte offsets inside a 256-row (or 64-row) stage
   // must fit in 32 bits
   auto al = [](const u16* q, int64_t ld) {
@@ -958,36 +971,34 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
   // M/N-major operands with rows a multiple of 8
   const bool kp_ok = (p.k_per_split % ABK == 0) && (d.K % ABK == 0);
   const bool mn_ok = (d.a_kmajor || d.M % 8 == 0) && (d.b_kmajor || d.N % 8 == 0);
-  if (kp_ok && mn_ok && p.aligned_a && p.aligned_b && d.a_kmajor == d.b_kmajor) {
+  if (kp_ok && mn_ok && p.aligned_a && p.aligned_b) {
     AParams q{};
     q.M = d.M; q.N = d.N; q.K = d.K;
     q.a0 = p.a0; q.a1 = p.a1; q.b0 = p.b0; q.b1 = p.b1; q.lda = d.lda; q.ldb = d.ldb;
     q.npass = d.npass;
     q.pa0 = p.pa0; q.pa1 = p.pa1; q.pa2 = p.pa2; q.pb0 = p.pb0; q.pb1 = p.pb1; q.pb2 = p.pb2;
-    q.c = d.c; q.ldc = d.ldc; q.c_hi = d.c_hi; q.c_lo = d.c_lo; q.ldc_pad = (int)d.ldc_pad;
+    q.c = d.c; q.ldc = d.ldc; q.c_hi = d.c_hi; q.c_lo = d.c_lo; q.ldc_pad = p.ldc_pad;
     q.tiles_m = p.tiles_m; q.tiles_n = p.tiles_n; q.ntiles = p.ntiles;
     q.ksplit = p.ksplit; q.k_per_split = p.k_per_split; q.part = partial;
     prof_begin(s, d.name);
     const dim3 gr(grid);
-#define FQ_LAUNCH_ASYNC(AMN, BMN, F16, W)                                                                  \
-    switch (d.epi) {                                                                                        \
-      case EPI_F32: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_F32, W>), gr, dim3(64 * W), 0, s, q); break;     \
-      case EPI_SPLIT: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SPLIT, W>), gr, dim3(64 * W), 0, s, q); break; \
-      case EPI_SYM: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SYM, W>), gr, dim3(64 * W), 0, s, q); break;     \
-      default: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_PARTIAL, W>), gr, dim3(64 * W), 0, s, q); break;      \
+#define FQ_LAUNCH_ASYNC(AMN, BMN, F16)                                                                  \
+    switch (d.epi) {                                                                                      \
+      case EPI_F32: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_F32, 8>), gr, dim3(512), 0, s, q); break;     \
+      case EPI_SPLIT: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SPLIT, 8>), gr, dim3(512), 0, s, q); break; \
+      case EPI_SYM: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SYM, 8>), gr, dim3(512), 0, s, q); break;     \
+      default: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_PARTIAL, 8>), gr, dim3(512), 0, s, q); break;      \
     }
-    if (g_async_waves == 8) {
-      if (d.a_kmajor && d.b_kmajor) {
-        if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true, 8) } else { FQ_LAUNCH_ASYNC(false, false, false, 8) }
-      } else {
-        if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true, 8) } else { FQ_LAUNCH_ASYNC(true, true, false, 8) }
-      }
+    // 8 waves (2 per SIMD, 128 x 64 wave tiles) measured ahead of 4 waves of 128 x 128
+    const bool amn = !d.a_kmajor, bmn = !d.b_kmajor;
+    if (amn && bmn) {
+      if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true) } else { FQ_LAUNCH_ASYNC(true, true, false) }
+    } else if (amn) {
+      if (d.f16) { FQ_LAUNCH_ASYNC(true, false, true) } else { FQ_LAUNCH_ASYNC(true, false, false) }
+    } else if (bmn) {
+      if (d.f16) { FQ_LAUNCH_ASYNC(false, true, true) } else { FQ_LAUNCH_ASYNC(false, true, false) }
     } else {
-      if (d.a_kmajor && d.b_kmajor) {
-        if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true, 4) } else { FQ_LAUNCH_ASYNC(false, false, false, 4) }
-      } else {
-        if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true, 4) } else { FQ_LAUNCH_ASYNC(true, true, false, 4) }
-      }
+      if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true) } else { FQ_LAUNCH_ASYNC(false, false, false) }
     }
 #undef FQ_LAUNCH_ASYNC
     prof_end(s);
@@ -1051,37 +1062,20 @@ hipError_t split_bf16(const void* in, int in_type, int64_t ld_in, int rows, int 
 
 hipError_t split_bf16_pad(const void* in, int in_type, int64_t ld_in, int rows, int cols,
                           const float* col_scale, u16* hi, u16* lo, int64_t ld_out,
-                          hipStream_t s) {
-  if (rows <= 0 || ld_out <= 0) return hipSuccess;
+                          int rows_out, hipStream_t s) {
+  if (rows_out < rows) rows_out = rows;
+  if (rows_out <= 0 || ld_out <= 0) return hipSuccess;
   prof_begin(s, "split_bf16");
-  const dim3 g(grid_for((int64_t)rows * ld_out, 256));
+  const dim3 g(grid_for((int64_t)rows_out * ld_out, 256));
   if (in_type == 0)
     hipLaunchKernelGGL(k_split_pad<float>, g, dim3(256), 0, s, (const float*)in, ld_in, rows, cols,
-                       col_scale, hi, lo, ld_out);
+                       col_scale, hi, lo, ld_out, rows_out);
   else if (in_type == 1)
     hipLaunchKernelGGL(k_split_pad<_Float16>, g, dim3(256), 0, s, (const _Float16*)in, ld_in, rows,
-                       cols, col_scale, hi, lo, ld_out);
+                       cols, col_scale, hi, lo, ld_out, rows_out);
   else
     hipLaunchKernelGGL(k_split_pad<u16>, g, dim3(256), 0, s, (const u16*)in, ld_in, rows, cols,
-                       col_scale, hi, lo, ld_out);
-  prof_end(s);
-  return last_launch_error();
-}
-
-hipError_t split_bf16_t(const void* in, int in_type, int64_t ld_in, int rows, int cols, u16* hi,
-                        u16* lo, int64_t ld_out, hipStream_t s) {
-  if (rows <= 0 || cols <= 0) return hipSuccess;
-  prof_begin(s, "split_bf16");
-  const dim3 g((cols + 63) / 64, (unsigned)((ld_out + 63) / 64));
-  if (in_type == 0)
-    hipLaunchKernelGGL(k_split_t<float>, g, dim3(256), 0, s, (const float*)in, ld_in, rows, cols, hi,
-                       lo, ld_out);
-  else if (in_type == 1)
-    hipLaunchKernelGGL(k_split_t<_Float16>, g, dim3(256), 0, s, (const _Float16*)in, ld_in, rows,
-                       cols, hi, lo, ld_out);
-  else
-    hipLaunchKernelGGL(k_split_t<u16>, g, dim3(256), 0, s, (const u16*)in, ld_in, rows, cols, hi, lo,
-                       ld_out);
+                       col_scale, hi, lo, ld_out, rows_out);
   prof_end(s);
   return last_launch_error();
 }

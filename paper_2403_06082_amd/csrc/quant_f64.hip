@@ -149,50 +149,115 @@ __device__ __forceinline__ double rsqrt_d(double x) {
   return y;
 }
 
-// One column of the in-register factorization (column index C is a compile-time
-// constant so that the row stays in registers).
-template <int C>
-__device__ __forceinline__ void potrf_cols(double (&a)[64], double (*col)[64], int r,
-                                           bool& notpd) {
-  if constexpr (C < 64) {
-    double piv = bcast_lane(a[C], C);
-    if (!(piv > 0.0)) {
-      notpd = true;
-      piv = 1.0;
+// ---- 64 x 64 diagonal-block factorization, one wave64, lane r holding row r in registers.
+// Column C: the pivot comes from lane C by readlane, every lane scales its entry of column
+// C and publishes it through LDS, then every lane applies the rank-1 update to its later
+// entries.  Ordering for latency: the update of column C is split into the 16 slots right
+// of C (applied first) and the rest; the pivot, scaling and broadcast of column C + 1 are
+// issued between the two, so the LDS round trip of column C + 1 overlaps the bulk of
+// column C's update.  Each slot still receives its updates in column order.
+
+// pin the listed slots: without it the compiler sinks updates into later columns and keeps
+// every broadcast value alive
+template <int LO, int HI>
+__device__ __forceinline__ void pin_slots(double (&a)[64]) {
+  if constexpr (LO < HI) {
+    if constexpr (HI - LO >= 4) {
+      asm volatile("" : "+v"(a[LO]), "+v"(a[LO + 1]), "+v"(a[LO + 2]), "+v"(a[LO + 3]));
+      pin_slots<LO + 4, HI>(a);
+    } else {
+      asm volatile("" : "+v"(a[LO]));
+      pin_slots<LO + 1, HI>(a);
     }
-    const double inv = rsqrt_d(piv);
-    a[C] = (r == C) ? piv * inv : a[C] * inv;
-    col[C & 1][r] = a[C];
-    __syncthreads();               // one barrier per column: col is double-buffered
-    const double lc = a[C];
-#pragma unroll
-    for (int cc0 = (C + 1) & ~7; cc0 < 64; cc0 += 8) {
-      // the 8 broadcast values of a group are read together (4 x 16 bytes), then used
-      const double2* cp = reinterpret_cast<const double2*>(&col[C & 1][cc0]);
-      double2 v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = cp[q];
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (cc0 + q > C) a[cc0 + q] -= lc * ((q & 1) ? v[q >> 1].y : v[q >> 1].x);
-      // pin the group's results here: without it the compiler sinks every update to the
-      // column's own step and keeps all broadcast values alive
-      asm volatile("" : "+v"(a[cc0]), "+v"(a[cc0 + 1]), "+v"(a[cc0 + 2]), "+v"(a[cc0 + 3]),
-                   "+v"(a[cc0 + 4]), "+v"(a[cc0 + 5]), "+v"(a[cc0 + 6]), "+v"(a[cc0 + 7]));
-    }
-    potrf_cols<C + 1>(a, col, r, notpd);
   }
 }
 
-// Factor the kb x kb diagonal block at (k0, k0) in place (lower).  One wave64: lane r
-// holds row r of the block in registers, staged through LDS with zeros above the
-// diagonal (identity rows beyond kb); each finished column is broadcast through LDS.
-// Entries above the diagonal pick up finite values that are never written back, which
-// keeps the update loop free of per-lane masks.
+// a[k] -= a[C] * v[k - LO] for LO <= k < HI, k > C (v: broadcast values of column C)
+template <int C, int LO, int HI, int NV>
+__device__ __forceinline__ void pf_update(double (&a)[64], const double2 (&v)[NV]) {
+  if constexpr (LO < HI) {
+    const double lc = a[C];
+#pragma unroll
+    for (int k = LO; k < HI; ++k)
+      if (k > C) a[k] -= lc * (((k - LO) & 1) ? v[(k - LO) >> 1].y : v[(k - LO) >> 1].x);
+    pin_slots<LO, HI>(a);
+  }
+}
+
+template <int LO, int HI, int NV>
+__device__ __forceinline__ void pf_read(const double* colC, double2 (&v)[NV]) {
+  const double2* cp = reinterpret_cast<const double2*>(colC + LO);
+#pragma unroll
+  for (int q = 0; q < (HI - LO) / 2; ++q) v[q] = cp[q];
+}
+
+// pivot of column C, scaled column entry of this lane, broadcast
+template <int C>
+__device__ __forceinline__ void pf_scale(double (&a)[64], double* colC, double* invd, int r,
+                                         bool& notpd) {
+  double piv = bcast_lane(a[C], C);
+  if (!(piv > 0.0)) {
+    notpd = true;
+    piv = 1.0;
+  }
+  const double inv = rsqrt_d(piv);
+  a[C] = (r == C) ? piv * inv : a[C] * inv;
+  colC[r] = a[C];
+  if (r == C) invd[C] = inv;       // 1 / L_CC
+}
+
+// entering: column C scaled and broadcast in col[C & 1], visible to the wave
+template <int C>
+__device__ __forceinline__ void pf_step(double (&a)[64], double (*col)[64], double* invd, int r,
+                                        bool& notpd) {
+  constexpr int G1 = (C + 1) & ~1;
+  constexpr int E1 = G1 + 16 < 64 ? G1 + 16 : 64;
+  constexpr int N1 = (E1 - G1) / 2 > 0 ? (E1 - G1) / 2 : 1;
+  constexpr int NB = (64 - E1) / 2 > 0 ? (64 - E1) / 2 : 1;
+  double2 v1[N1], vb[NB];
+  pf_read<G1, E1>(col[C & 1], v1);
+  pf_update<C, G1, E1>(a, v1);
+  pf_read<E1, 64>(col[C & 1], vb);
+  if constexpr (C + 1 < 64) pf_scale<C + 1>(a, col[(C + 1) & 1], invd, r, notpd);
+  pf_update<C, E1, 64>(a, vb);
+  if constexpr (C + 1 < 64) {
+    __syncthreads();
+    pf_step<C + 1>(a, col, invd, r, notpd);
+  }
+}
+
+// ---- inverse of the factor, Z = L^{-1}: lane j carries column j of Z, z = e_j initially;
+// for C = 0..63: z_C /= L_CC, then z_k -= L_kC z_C for k > C (column C of L read from
+// the transposed copy LT[C][k], the same for every lane and independent of z, so the reads
+// run ahead of the arithmetic).
+template <int C>
+__device__ __forceinline__ void zinv_step(double (&z)[64], const double (*LT)[64],
+                                          const double* invd) {
+  if constexpr (C < 64) {
+    z[C] *= invd[C];
+    constexpr int G = (C + 1) & ~1;
+    constexpr int NV = (64 - G) / 2 > 0 ? (64 - G) / 2 : 1;
+    if constexpr (G < 64) {
+      double2 v[NV];
+      pf_read<G, 64>(LT[C], v);
+      const double zc = z[C];
+#pragma unroll
+      for (int k = G; k < 64; ++k)
+        if (k > C) z[k] -= zc * (((k - G) & 1) ? v[(k - G) >> 1].y : v[(k - G) >> 1].x);
+    }
+    zinv_step<C + 1>(z, LT, invd);
+  }
+}
+
+// Factor the kb x kb diagonal block at (k0, k0) in place (lower) and write its inverse to
+// Z (64 x 64 row-major, lower; rows and columns beyond kb are the identity).  Rows of the
+// block beyond kb are identity rows.  Entries above the diagonal pick up finite values in
+// registers that are never written back, which keeps the update loop free of masks.
 __global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
-                                                int kb, int* flags) {
-  __shared__ double Ls[64][65];
+                                                int kb, double* __restrict__ Z, int* flags) {
+  __shared__ __attribute__((aligned(16))) double Ls[64][64];
   __shared__ __attribute__((aligned(16))) double col[2][64];
+  __shared__ double invd[64];
   const int r = threadIdx.x;
   // all 64 loads of a thread in flight at once (the block is read row by row, coalesced)
 #pragma unroll
@@ -206,68 +271,25 @@ __global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t 
 #pragma unroll
   for (int c = 0; c < 64; ++c) a[c] = Ls[r][c];
   bool notpd = false;
-  potrf_cols<0>(a, col, r, notpd);
+  pf_scale<0>(a, col[0], invd, r, notpd);
+  __syncthreads();
+  pf_step<0>(a, col, invd, r, notpd);
   if (notpd && r == 0) flags[0] = 1;
   __syncthreads();
+  // transposed copy: Ls[c][r] = L[r][c] (zero above the diagonal)
 #pragma unroll
-  for (int c = 0; c < 64; ++c) Ls[r][c] = a[c];
+  for (int c = 0; c < 64; ++c) Ls[c][r] = (c <= r) ? a[c] : 0.0;
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 64; ++i)
-    if (i < kb && r <= i) A[(k0 + i) * lda + k0 + r] = Ls[i][r];
-}
-
-// Forward substitution of one panel row against L_kk (x L^T = a), column C of x.
-template <int C>
-__device__ __forceinline__ void trsm_cols(double (&x)[64], const double (*L)[66],
-                                          const double* invd) {
-  if constexpr (C < 64) {
-    double s0 = x[C], s1 = 0.0;
+    if (i < kb && r <= i) A[(k0 + i) * lda + k0 + r] = Ls[r][i];
+  double z[64];
 #pragma unroll
-    for (int m0 = 0; m0 < C; m0 += 8) {
-      const double2* lp = reinterpret_cast<const double2*>(&L[C][m0]);
-      double2 v[4];
+  for (int k = 0; k < 64; ++k) z[k] = (k == r) ? 1.0 : 0.0;
+  zinv_step<0>(z, Ls, invd);
+  // Z[k][r] = z[k]: one row of Z per instruction across the wave (coalesced)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = lp[q];
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        if (m0 + q < C) {
-          const double l = (q & 1) ? v[q >> 1].y : v[q >> 1].x;
-          if (q & 1) s1 -= x[m0 + q] * l;
-          else s0 -= x[m0 + q] * l;
-        }
-    }
-    x[C] = (s0 + s1) * invd[C];
-    asm volatile("" : "+v"(x[C]));
-    trsm_cols<C + 1>(x, L, invd);
-  }
-}
-
-// Panel below the diagonal block: rows i in [k0+kb, K), X = A[i, k0:k0+kb] L_kk^{-T}
-// (forward substitution, one row per thread in registers; L_kk broadcast from LDS).
-__global__ __launch_bounds__(256) void k_trsm64(double* __restrict__ A, int64_t lda, int64_t K,
-                                                int64_t k0, int kb) {
-  __shared__ __attribute__((aligned(16))) double L[64][66];
-  __shared__ double invd[64];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const int e = threadIdx.x + 256 * q;
-    const int r = e >> 6, c = e & 63;
-    L[r][c] = (r < kb && c < kb && c <= r) ? A[(k0 + r) * lda + k0 + c] : (r == c ? 1.0 : 0.0);
-  }
-  __syncthreads();
-  if (threadIdx.x < 64) invd[threadIdx.x] = 1.0 / L[threadIdx.x][threadIdx.x];
-  __syncthreads();
-  const int64_t i = k0 + kb + (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= K) return;
-  double x[64];
-  double* row = A + i * lda + k0;
-#pragma unroll
-  for (int c = 0; c < 64; ++c) x[c] = (c < kb) ? row[c] : 0.0;
-  trsm_cols<0>(x, L, invd);
-#pragma unroll
-  for (int c = 0; c < 64; ++c)
-    if (c < kb) row[c] = x[c];
+  for (int k = 0; k < 64; ++k) Z[k * 64 + r] = z[k];
 }
 
 // R[i][j] = M[K-1-i][K-1-j] (upper), rdiag / inv_rdiag.
@@ -645,68 +667,36 @@ __global__ __launch_bounds__(256) void k_pack2(const uint8_t* __restrict__ c8, i
   }
 }
 
+// out[r * ld_out + c] = code[r][c] - zero[r] as bf16 (small integers, exact) for r < rows,
+// c < cols; every other entry of the rows_out x ld_out plane is 0.  ld_out is a multiple
+// of 16; one thread per 16-column group (one packed code word), two 16-byte stores.
 __global__ __launch_bounds__(256) void k_dequant(const uint32_t* __restrict__ codes,
                                                  const float* __restrict__ zero, int64_t rows,
                                                  int64_t cols, u16* __restrict__ out,
-                                                 int64_t ld_out) {
-  const int64_t nw = (cols + 15) / 16;
-  const int64_t total = rows * nw;
+                                                 int64_t ld_out, int64_t rows_out) {
+  const int64_t nw = (cols + 15) / 16;     // packed words per code row
+  const int64_t gw = ld_out / 16;          // 16-column groups per output row
+  const int64_t total = rows_out * gw;
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * 256) {
-    const int64_t r = e / nw, w = e - r * nw;
-    const uint32_t word = codes[e];
-    const float z = zero[r];
-    u16* dst = out + r * ld_out + w * 16;
+    const int64_t r = e / gw, w = e - r * gw;
     uint32_t h[16];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const float v = (float)((word >> (2 * k)) & 3u) - z;   // small integer, exact in bf16
-      h[k] = __float_as_uint(v) >> 16;
-    }
-    if (w * 16 + 16 <= cols && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
-      *reinterpret_cast<uint4*>(dst) = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16),
-                                                  h[4] | (h[5] << 16), h[6] | (h[7] << 16));
-      *reinterpret_cast<uint4*>(dst + 8) = make_uint4(h[8] | (h[9] << 16), h[10] | (h[11] << 16),
-                                                      h[12] | (h[13] << 16), h[14] | (h[15] << 16));
-    } else {
-      for (int k = 0; k < 16; ++k)
-        if (w * 16 + k < cols) dst[k] = (u16)h[k];
-    }
-  }
-}
-
-// Transposed dequantization: out[c * ld_out + r] = code[r][c] - zero[r] as bf16 (small
-// integers, exact); rows r in [rows, ld_out) are written as 0.  64 x 64 tiles.
-__global__ __launch_bounds__(256) void k_dequant_t(const uint32_t* __restrict__ codes,
-                                                   const float* __restrict__ zero, int64_t rows,
-                                                   int64_t cols, u16* __restrict__ out,
-                                                   int64_t ld_out) {
-  __shared__ u16 tile[64][66];
-  const int64_t r0 = (int64_t)blockIdx.y * 64;
-  const int64_t c0 = (int64_t)blockIdx.x * 64;   // multiple of 16
-  const int64_t nw = (cols + 15) / 16;
-  // 64 rows x 4 words of 16 codes
-  {
-    const int r = threadIdx.x >> 2, w = threadIdx.x & 3;
-    const int64_t gr = r0 + r, gw = c0 / 16 + w;
-    uint32_t word = 0;
-    float z = 0.f;
-    const bool ok = gr < rows && gw < nw;
-    if (ok) {
-      word = codes[gr * nw + gw];
-      z = zero[gr];
-    }
+    for (int k = 0; k < 16; ++k) h[k] = 0;
+    if (r < rows && w < nw) {
+      const uint32_t word = codes[r * nw + w];
+      const float z = zero[r];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const float v = ok ? (float)((word >> (2 * k)) & 3u) - z : 0.f;
-      tile[r][w * 16 + k] = (u16)(__float_as_uint(v) >> 16);
+      for (int k = 0; k < 16; ++k) {
+        const float v = (float)((word >> (2 * k)) & 3u) - z;   // small integer, exact in bf16
+        h[k] = (w * 16 + k < cols) ? (__float_as_uint(v) >> 16) : 0u;
+      }
     }
-  }
-  __syncthreads();
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int c = ty; c < 64; c += 4) {
-    const int64_t gc = c0 + c, gr = r0 + tx;
-    if (gc < cols && gr < ld_out) out[gc * ld_out + gr] = (gr < rows) ? tile[tx][c] : (u16)0;
+    u16* dst = out + r * ld_out + w * 16;
+    *reinterpret_cast<uint4*>(dst) = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16),
+                                                h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+    *reinterpret_cast<uint4*>(dst + 8) = make_uint4(h[8] | (h[9] << 16), h[10] | (h[11] << 16),
+                                                    h[12] | (h[13] << 16), h[14] | (h[15] << 16));
   }
 }
 
@@ -735,21 +725,22 @@ hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& 
   return last_launch_error();
 }
 
-hipError_t q_cholesky(double* A, int64_t K, int* flags, hipStream_t s) {
+hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s) {
   for (int64_t k0 = 0; k0 < K; k0 += 64) {
     const int kb = (int)((K - k0) < 64 ? (K - k0) : 64);
     prof_begin(s, "chol_potrf");
-    hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(64), 0, s, A, K, k0, kb, flags);
+    hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(64), 0, s, A, K, k0, kb, Z, flags);
     prof_end(s);
     const int64_t rest = K - k0 - kb;
     if (rest > 0) {
-      prof_begin(s, "chol_trsm");
-      hipLaunchKernelGGL(k_trsm64, dim3(grid_for(rest, 256, 1 << 30)), dim3(256), 0, s, A, K, K,
-                         k0, kb);
-      prof_end(s);
-      const double* P = A + (k0 + kb) * K + k0;
-      hipError_t e = dgemm(rest, rest, kb, -1.0, 1.0, P, K, P, K, true,
-                           A + (k0 + kb) * K + (k0 + kb), K, true, s, "chol_syrk", 64);
+      // panel below the block: X = A[k0+kb:, k0:k0+kb] L_kk^{-T}, in place (each output tile
+      // reads only its own rows of the panel, all of them before it writes)
+      double* P = A + (k0 + kb) * K + k0;
+      hipError_t e = dgemm(rest, kb, kb, 1.0, 0.0, P, K, Z, 64, true, P, K, false, s,
+                           "chol_trsm", 64);
+      if (e != hipSuccess) return e;
+      e = dgemm(rest, rest, kb, -1.0, 1.0, P, K, P, K, true, A + (k0 + kb) * K + (k0 + kb), K,
+                true, s, "chol_syrk", 64);
       if (e != hipSuccess) return e;
     }
   }
@@ -808,16 +799,6 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
   return last_launch_error();
 }
 
-hipError_t dequant_bf16_t(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
-                          u16* out, int64_t ld_out, hipStream_t s) {
-  if (cols <= 0 || ld_out <= 0) return hipSuccess;
-  prof_begin(s, "dequant");
-  hipLaunchKernelGGL(k_dequant_t, dim3((unsigned)((cols + 63) / 64), (unsigned)((ld_out + 63) / 64)),
-                     dim3(256), 0, s, codes, zero, rows, cols, out, ld_out);
-  prof_end(s);
-  return last_launch_error();
-}
-
 hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* out,
                    hipStream_t s) {
   const int64_t nw = rows * ((cols + 15) / 16);
@@ -829,12 +810,14 @@ hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* 
 }
 
 hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
-                        u16* out, int64_t ld_out, hipStream_t s) {
-  const int64_t nw = rows * ((cols + 15) / 16);
+                        u16* out, int64_t ld_out, int64_t rows_out, hipStream_t s) {
+  if (rows_out < rows) rows_out = rows;
+  if (ld_out % 16 != 0 || ld_out < cols) return hipErrorInvalidValue;
+  const int64_t nw = rows_out * (ld_out / 16);
   if (nw <= 0) return hipSuccess;
   prof_begin(s, "dequant");
   hipLaunchKernelGGL(k_dequant, dim3(grid_for(nw, 256)), dim3(256), 0, s, codes, zero, rows, cols,
-                     out, ld_out);
+                     out, ld_out, rows_out);
   prof_end(s);
   return last_launch_error();
 }

@@ -201,3 +201,51 @@ def test_quantize_errors():
     with pytest.raises(fq.FQError) as ei:
         _quantize(torch, fq, D, Ht, 128, bits=3)
     assert ei.value.status == 2
+
+
+@pytest.mark.parametrize("wt", ["bf16", "f32"])
+def test_poisoned_workspaces(wt):
+    """Every workspace filled with NaN bytes before the call: no output may depend on
+    workspace contents the call did not write itself (padding lanes and columns included)."""
+    torch = need_gpu()
+    fq = _fq()
+    rng = np.random.default_rng(77)
+    d_out, d_in, k_out, k_in = 520, 264, 143, 72     # ragged: fallback and padded paths
+    Po, Pi = _frames(d_out, d_in, k_out, k_in)
+    K_out, K_in = Po.shape[1], Pi.shape[1]
+    Ws = _rand_storage(rng, (d_out, d_in), wt, 0.02)
+    Xs = _rand_storage(rng, (300, d_in), wt)
+    X = upload(Xs, wt)
+    W, P_out, P_in = upload(Ws, wt), torch.from_numpy(Po).cuda(), torch.from_numpy(Pi).cuda()
+
+    def poisoned(nbytes):
+        return torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+
+    dt = {"bf16": fq.FQ_BF16, "f32": fq.FQ_F32}[wt]
+    H = torch.empty((d_in, d_in), dtype=torch.float32, device="cuda")
+    fq.fq_hessian_accumulate(X, H, ws=poisoned(fq.fq_hessian_workspace_bytes(dt, 300, d_in)))
+    D = torch.empty((K_out, K_in), dtype=torch.float32, device="cuda")
+    Ht = torch.empty((K_in, K_in), dtype=torch.float32, device="cuda")
+    fq.fq_frame_analysis(W, P_out, P_in, H, D, Ht,
+                         ws=poisoned(fq.fq_frame_analysis_workspace_bytes(dt, d_out, d_in, K_out, K_in)))
+    codes = torch.empty((K_out, (K_in + 15) // 16), dtype=torch.int32, device="cuda")
+    scale = torch.empty((K_out,), dtype=torch.float32, device="cuda")
+    zero = torch.empty((K_out,), dtype=torch.float32, device="cuda")
+    fq.fq_quantize_frames(D, Ht, codes, scale, zero,
+                          ws=poisoned(fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128)))
+    Wh = torch.empty((d_out, d_in), dtype=torch.float32, device="cuda")
+    fq.fq_frame_synthesis(codes, scale, zero, P_out, P_in, Wh,
+                          ws=poisoned(fq.fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in)))
+    torch.cuda.synchronize()
+    Ho = O.hessian(gen.storage_to_f32(Xs, wt).astype(np.float64))
+    Hg = H.cpu().numpy()
+    assert rel_fro(Hg, Ho) < 1e-5
+    Do, Hto = O.frame_analysis(gen.storage_to_f32(Ws, wt), Po, Pi, Hg)
+    Dg, Htg = D.cpu().numpy(), Ht.cpu().numpy()
+    assert rel_fro(Dg, Do) < 1e-5 and rel_fro(Htg, Hto) < 1e-5
+    cg = unpack_codes(codes, K_in)
+    r = replay_rows(Dg, Htg, cg)
+    check_codes(r, cg, scale.cpu().numpy(), zero.cpu().numpy())
+    Who = O.synthesis(cg, scale.cpu().numpy().astype(np.float64),
+                      zero.cpu().numpy().astype(np.float64), Po, Pi)
+    assert rel_fro(Wh.cpu().numpy(), Who) < 1e-5
