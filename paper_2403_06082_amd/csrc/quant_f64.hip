@@ -256,16 +256,18 @@ __device__ __forceinline__ void zinv_step(double (&z)[64], const double (*LT)[64
 __global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
                                                 int kb, double* __restrict__ Z, int* flags) {
   __shared__ __attribute__((aligned(16))) double Ls[64][64];
+  __shared__ double Lrow[64][65];      // row-major copy of the factor for the global store
   __shared__ __attribute__((aligned(16))) double col[2][64];
   __shared__ double invd[64];
   const int r = threadIdx.x;
-  // all 64 loads of a thread in flight at once (the block is read row by row, coalesced)
+  // all 64 loads of a thread in flight at once, unconditional (indices clamped into the
+  // block, the unwanted values replaced afterwards), coalesced row by row
+  const int rc = r < kb ? r : kb - 1;
+  double ld[64];
 #pragma unroll
-  for (int i = 0; i < 64; ++i) {
-    double v = (i == r) ? 1.0 : 0.0;
-    if (i < kb && r <= i) v = A[(k0 + i) * lda + k0 + r];
-    Ls[i][r] = v;
-  }
+  for (int i = 0; i < 64; ++i) ld[i] = A[(k0 + (i < kb ? i : kb - 1)) * lda + k0 + rc];
+#pragma unroll
+  for (int i = 0; i < 64; ++i) Ls[i][r] = (i < kb && r <= i) ? ld[i] : ((i == r) ? 1.0 : 0.0);
   __syncthreads();
   double a[64];
 #pragma unroll
@@ -276,13 +278,20 @@ __global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t 
   pf_step<0>(a, col, invd, r, notpd);
   if (notpd && r == 0) flags[0] = 1;
   __syncthreads();
-  // transposed copy: Ls[c][r] = L[r][c] (zero above the diagonal)
+  // transposed copy Ls[c][r] = L[r][c] for the inverse and a row-major copy for the store
+  // (zero above the diagonal); both written without bank conflicts
 #pragma unroll
-  for (int c = 0; c < 64; ++c) Ls[c][r] = (c <= r) ? a[c] : 0.0;
+  for (int c = 0; c < 64; ++c) {
+    const double v = (c <= r) ? a[c] : 0.0;
+    Ls[c][r] = v;
+    Lrow[r][c] = v;
+  }
   __syncthreads();
+  // row i of the factor, zeros above the diagonal (the upper triangle of a diagonal block
+  // is never read)
 #pragma unroll
   for (int i = 0; i < 64; ++i)
-    if (i < kb && r <= i) A[(k0 + i) * lda + k0 + r] = Ls[r][i];
+    if (i < kb && r < kb) A[(k0 + i) * lda + k0 + r] = Lrow[i][r];
   double z[64];
 #pragma unroll
   for (int k = 0; k < 64; ++k) z[k] = (k == r) ? 1.0 : 0.0;
