@@ -152,6 +152,24 @@ def cpu_baseline(wl, li, host, budget_rows=1024, sample_tokens=8192):
             "stage_seconds": {k: round(v, 3) for k, v in t.items()}}
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed byte-counter profile, or None when
+    there is none or the kernel source changed since it was taken."""
+    import hashlib
+    here = os.path.dirname(os.path.abspath(__file__))
+    try:
+        with open(os.path.join(here, "profiles", "traffic.json")) as f:
+            t = json.load(f)
+        if t.get("kernel") != kernel:
+            return None
+        with open(os.path.join(here, t["source"]), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != t["source_sha256"]:
+                return None
+        return t["hbm_bytes_per_launch"]
+    except (OSError, ValueError, KeyError):
+        return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -160,6 +178,9 @@ def main():
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--layer", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="device-to-device copy of this many MiB before the warmup, as the "
+                         "known-size reference for hardware byte counters")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -189,6 +210,15 @@ def main():
         quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], bufs, block=wl.block,
                        damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream)
 
+    if args.copy_probe_mib > 0:
+        nb = args.copy_probe_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(args.warmup):
         step()
         print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
@@ -250,7 +280,7 @@ def main():
         roof = {"bound": "mfma", "achieved": round(per_launch / (avg_ms / 1e3) / 1e12, 2),
                 "peak": PEAK[kind], "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dom)
     roof["kernel"] = dom
     roof["avg_launch_ms"] = round(avg_ms, 4)
     roof["algorithmic_per_launch"] = per_launch
