@@ -882,24 +882,62 @@ __global__ void k_fill_zero(float* p, int rows, int cols, int64_t ld) {
 
 // out[r * ld_out + c] = bf16 pair of in[r][c] (times col_scale[c]) for c < cols and 0 for
 // cols <= c < ld_out (K padding).
+// One thread per 4 output columns of a row (ld_out is a multiple of 4), rows across
+// blockIdx.y: vector loads where the source row allows them, 8-byte stores per plane.
 template <typename T>
-__global__ void k_split_pad(const T* __restrict__ in, int64_t ld_in, int rows, int cols,
-                            const float* __restrict__ col_scale, u16* __restrict__ hi,
-                            u16* __restrict__ lo, int64_t ld_out, int rows_out) {
-  const int64_t total = (int64_t)rows_out * ld_out;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t r = e / ld_out;
-    const int c = (int)(e - r * ld_out);
-    uint32_t h = 0, l = 0;
-    if (c < cols && r < rows) {
-      float x = ld_f(in + r * ld_in + c);
-      if (col_scale) x *= col_scale[c];
-      h = bf16_rne_bits(x);
-      l = bf16_rne_bits(x - __uint_as_float(h << 16));
+__device__ __forceinline__ void ld4(const T* src, float (&x)[4], bool vec) {
+  if constexpr (sizeof(T) == 4) {
+    if (vec) {
+      const float4 v = *reinterpret_cast<const float4*>(src);
+      x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+      return;
     }
-    hi[e] = (u16)h;
-    if (lo) lo[e] = (u16)l;
+  } else {
+    if (vec) {
+      const uint2 v = *reinterpret_cast<const uint2*>(src);
+      const T* e = reinterpret_cast<const T*>(&v);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = ld_f(e + q);
+      return;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) x[q] = ld_f(src + q);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_split_pad(const T* __restrict__ in, int64_t ld_in,
+                                                   int rows, int cols,
+                                                   const float* __restrict__ col_scale,
+                                                   u16* __restrict__ hi, u16* __restrict__ lo,
+                                                   int64_t ld_out, int rows_out) {
+  const int64_t c0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (c0 >= ld_out) return;
+  for (int64_t r = blockIdx.y; r < rows_out; r += gridDim.y) {
+    float x[4] = {0.f, 0.f, 0.f, 0.f};
+    if (r < rows && c0 < cols) {
+      const T* src = in + r * ld_in + c0;
+      if (c0 + 4 <= cols) {
+        const bool vec = (reinterpret_cast<uintptr_t>(src) & (4 * sizeof(T) - 1)) == 0;
+        ld4(src, x, vec);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) x[q] = (c0 + q < cols) ? ld_f(src + q) : 0.f;
+      }
+      if (col_scale) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) x[q] *= (c0 + q < cols) ? col_scale[c0 + q] : 0.f;
+      }
+    }
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      h[q] = bf16_rne_bits(x[q]);
+      l[q] = bf16_rne_bits(x[q] - __uint_as_float(h[q] << 16));
+    }
+    *reinterpret_cast<uint2*>(hi + r * ld_out + c0) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    if (lo)
+      *reinterpret_cast<uint2*>(lo + r * ld_out + c0) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
   }
 }
 
@@ -1065,8 +1103,12 @@ hipError_t split_bf16_pad(const void* in, int in_type, int64_t ld_in, int rows, 
                           int rows_out, hipStream_t s) {
   if (rows_out < rows) rows_out = rows;
   if (rows_out <= 0 || ld_out <= 0) return hipSuccess;
+  if (ld_out % 4 != 0 || ld_out < cols ||
+      (reinterpret_cast<uintptr_t>(hi) & 7) != 0 || (lo && (reinterpret_cast<uintptr_t>(lo) & 7) != 0))
+    return hipErrorInvalidValue;
   prof_begin(s, "split_bf16");
-  const dim3 g(grid_for((int64_t)rows_out * ld_out, 256));
+  // a few thousand work-groups, each thread walking rows_out / 512 rows
+  const dim3 g((unsigned)((ld_out + 1023) / 1024), (unsigned)(rows_out < 512 ? rows_out : 512));
   if (in_type == 0)
     hipLaunchKernelGGL(k_split_pad<float>, g, dim3(256), 0, s, (const float*)in, ld_in, rows, cols,
                        col_scale, hi, lo, ld_out, rows_out);

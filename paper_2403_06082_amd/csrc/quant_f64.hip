@@ -383,6 +383,12 @@ constexpr int GB = 128;
 constexpr int GTH = 384;
 constexpr int GROWS = GTH / 16 * 2;   // 48 rows per work-group (253 groups for 12112 rows)
 
+// Column-sequential rounding of one chunk of at most GB columns.  A group of 16 lanes
+// holds 2 rows; lane g owns columns g + 16 cc (cc < 8), so the lanes of a group read a
+// row of R as 16 consecutive doubles (no bank conflicts) and load / store rows of Y, D,
+// codes and residuals contiguously.  Column j is rounded by its owner lane j % 16, its
+// residual broadcast to the group with a DPP row broadcast, and every lane folds it into
+// its own later columns: y_c += e_j R_jc (R_jc = 0 for c < j).
 template <int O>
 __device__ __forceinline__ double row_bcast(double v) {
   const long long b = __double_as_longlong(v);
@@ -397,62 +403,47 @@ struct RoundState {
   double s[2], is[2], z[2];
 };
 
-template <int O>
-__device__ __forceinline__ void round_owner_cols(RoundState& st, const double* __restrict__ Rs,
-                                                 const double* __restrict__ ird, int b, int g,
-                                                 double maxq) {
-  // the 8 inverse pivots of this group and the first R row are read ahead of use
-  double irv[8];
+// column J; rn: row J of R at this lane's columns, irj: 1 / R_JJ
+template <int J>
+__device__ __forceinline__ void round_col(RoundState& st, const double* __restrict__ Rs,
+                                          const double* __restrict__ ird, int b, int g,
+                                          double maxq, const double (&rn)[8], double irj) {
+  if constexpr (J < GB) {
+    if (J >= b) return;
+    constexpr int O = J & 15, C = J >> 4;
+    double rnext[8];
+    double irn = 0.0;
+    if constexpr (J + 1 < GB) {   // next row of R and pivot, read while column J is rounded
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const double2 t = reinterpret_cast<const double2*>(ird + O * 8)[q];
-    irv[2 * q] = t.x;
-    irv[2 * q + 1] = t.y;
-  }
-  double2 rn[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) rn[q] = reinterpret_cast<const double2*>(Rs + (O * 8) * GB + g * 8)[q];
-#pragma unroll
-  for (int jj = 0; jj < 8; ++jj) {
-    const int j = O * 8 + jj;
-    if (j >= b) return;
-    const double2 rc[4] = {rn[0], rn[1], rn[2], rn[3]};
-    if (jj + 1 < 8) {   // prefetch row j + 1 of R while column j is rounded
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        rn[q] = reinterpret_cast<const double2*>(Rs + (j + 1) * GB + g * 8)[q];
+      for (int cc = 0; cc < 8; ++cc) rnext[cc] = Rs[(J + 1) * GB + g + 16 * cc];
+      irn = ird[J + 1];
     }
-    const double ir = irv[jj];
     double e[2];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       // t = w / scale in code units; the code relative to the zero point is
       // clamp(rne(t), -zero, maxq - zero) (the zero point is an integer)
-      const double t = st.y[k][jj] * (ir * st.is[k]);
+      const double t = st.y[k][C] * (irj * st.is[k]);
       const double qz = fmin(fmax(rint(t), -st.z[k]), maxq - st.z[k]);
-      const double ek = fma(-st.s[k], qz, st.d0[k][jj]);
+      const double ek = fma(-st.s[k], qz, st.d0[k][C]);
       if (g == O) {
-        st.rr[k][jj] = ek;
-        st.q[k][jj >> 2] |= (uint32_t)(qz + st.z[k]) << (8 * (jj & 3));
+        st.rr[k][C] = ek;
+        st.q[k][C >> 2] |= (uint32_t)(qz + st.z[k]) << (8 * (C & 3));
       }
       e[k] = row_bcast<O>(ek);
     }
 #pragma unroll
     for (int cc = 0; cc < 8; ++cc) {
-      const double rv = (cc & 1) ? rc[cc >> 1].y : rc[cc >> 1].x;
-      st.y[0][cc] += e[0] * rv;
-      st.y[1][cc] += e[1] * rv;
+      st.y[0][cc] += e[0] * rn[cc];
+      st.y[1][cc] += e[1] * rn[cc];
     }
-  }
-}
-
-template <int O>
-__device__ __forceinline__ void round_all(RoundState& st, const double* Rs, const double* ird,
-                                          int b, int g, double maxq) {
-  if constexpr (O < 16) {
-    if (O * 8 >= b) return;
-    round_owner_cols<O>(st, Rs, ird, b, g, maxq);
-    round_all<O + 1>(st, Rs, ird, b, g, maxq);
+    // pin the updated values here: otherwise the compiler sinks each update to the column
+    // that reads it and keeps every broadcast residual alive
+#pragma unroll
+    for (int cc = 0; cc < 8; cc += 2)
+      asm volatile("" : "+v"(st.y[0][cc]), "+v"(st.y[0][cc + 1]), "+v"(st.y[1][cc]),
+                   "+v"(st.y[1][cc + 1]));
+    if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, ird, b, g, maxq, rnext, irn);
   }
 }
 
@@ -464,12 +455,27 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     const double* __restrict__ Y, uint8_t* __restrict__ codes8, double* __restrict__ res) {
   __shared__ __attribute__((aligned(16))) double Rs[GB * GB];
   __shared__ __attribute__((aligned(16))) double ird[GB];
-  for (int e = threadIdx.x; e < GB * GB; e += GTH) {
-    const int rr = e / GB, cc = e % GB;
-    Rs[e] = (rr < b && cc < b) ? R[(int64_t)(i1 + rr) * cols + i1 + cc] : 0.0;
+  // R block: Rs[rr][cc] = R[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
+  // issued unconditionally from a clamped in-bounds address, all of a thread's at once
+  {
+    constexpr int NE = GB * GB, PER = (NE + GTH - 1) / GTH, BATCH = 16;
+#pragma unroll
+    for (int q0 = 0; q0 < PER; q0 += BATCH) {
+      double v[BATCH];
+#pragma unroll
+      for (int q = 0; q < BATCH; ++q) {
+        const int e = min((int)threadIdx.x + (q0 + q) * GTH, NE - 1);
+        const int rr = min(e / GB, b - 1), cc = min(e % GB, b - 1);
+        v[q] = R[(int64_t)(i1 + rr) * cols + i1 + cc];
+      }
+#pragma unroll
+      for (int q = 0; q < BATCH; ++q) {
+        const int e = (int)threadIdx.x + (q0 + q) * GTH;
+        if (q0 + q < PER && e < NE) Rs[e] = ((e / GB) < b && (e % GB) < b) ? v[q] : 0.0;
+      }
+    }
   }
   if (threadIdx.x < GB) ird[threadIdx.x] = threadIdx.x < b ? inv_rdiag[i1 + threadIdx.x] : 0.0;
-  __syncthreads();
 
   const int lane = threadIdx.x & 63;
   const int g = lane & 15;                         // position inside the 16-lane group
@@ -478,27 +484,46 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   const double lo_b = scal[2], hi_b = scal[3];
 
   RoundState st;
+  {
+    double yv[2][8];
+    float dv[2][8];
+    uint8_t dd[8];
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int64_t r = r0 + k;
-    const bool ok = r < rows;
-    st.s[k] = ok ? scale64[r] : 1.0;
-    st.is[k] = 1.0 / st.s[k];
-    st.z[k] = ok ? zero64[r] : 0.0;
-    st.q[k][0] = st.q[k][1] = 0;
+    for (int cc = 0; cc < 8; ++cc) dd[cc] = dead[i1 + min(g + 16 * cc, b - 1)];
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) {
-      const int c = g * 8 + cc;
-      const bool in = ok && c < b;
-      st.y[k][cc] = in ? Y[r * cols + i1 + c] : 0.0;
-      double x = 0.0;
-      if (in && !dead[i1 + c]) x = fmin(fmax((double)D[r * cols + i1 + c], lo_b), hi_b);
-      st.d0[k][cc] = x;
-      st.rr[k][cc] = 0.0;
+    for (int k = 0; k < 2; ++k) {
+      const int64_t r = min(r0 + k, rows - 1);
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        const int c = min(g + 16 * cc, b - 1);
+        yv[k][cc] = Y[r * cols + i1 + c];
+        dv[k][cc] = D[r * cols + i1 + c];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int64_t r = r0 + k;
+      const bool ok = r < rows;
+      const int64_t rc = ok ? r : rows - 1;
+      st.s[k] = ok ? scale64[rc] : 1.0;
+      st.is[k] = 1.0 / st.s[k];
+      st.z[k] = ok ? zero64[rc] : 0.0;
+      st.q[k][0] = st.q[k][1] = 0;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        const bool in = ok && g + 16 * cc < b;
+        st.y[k][cc] = in ? yv[k][cc] : 0.0;
+        st.d0[k][cc] = (in && !dd[cc]) ? fmin(fmax((double)dv[k][cc], lo_b), hi_b) : 0.0;
+        st.rr[k][cc] = 0.0;
+      }
     }
   }
+  __syncthreads();
 
-  round_all<0>(st, Rs, ird, b, g, (double)maxq);
+  double rn[8];
+#pragma unroll
+  for (int cc = 0; cc < 8; ++cc) rn[cc] = Rs[g + 16 * cc];
+  round_col<0>(st, Rs, ird, b, g, (double)maxq, rn, ird[0]);
 
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
@@ -506,7 +531,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     if (r >= rows) continue;
 #pragma unroll
     for (int cc = 0; cc < 8; ++cc) {
-      const int c = g * 8 + cc;
+      const int c = g + 16 * cc;
       if (c < b) {
         codes8[r * cols + i1 + c] = (uint8_t)(st.q[k][cc >> 2] >> (8 * (cc & 3)));
         res[r * ld_res + res_col0 + c] = st.rr[k][cc];
