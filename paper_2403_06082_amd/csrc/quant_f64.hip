@@ -226,26 +226,29 @@ __device__ __forceinline__ void pf_step(double (&a)[64], double (*col)[64], doub
   }
 }
 
-// ---- inverse of the factor, Z = L^{-1}: lane j carries column j of Z, z = e_j initially;
-// for C = 0..63: z_C /= L_CC, then z_k -= L_kC z_C for k > C (column C of L read from
-// the transposed copy LT[C][k], the same for every lane and independent of z, so the reads
-// run ahead of the arithmetic).
+// ---- inverse of the factor, Z = L^{-1}, formed by a second wave while the first factors:
+// lane j carries column j of Z, z = e_j initially; for C = 0..63, once column C of L and
+// 1 / L_CC are published: z_C /= L_CC, then z_k -= L_kC z_C for k > C.  It reads the same
+// broadcast buffer as the factorization and meets it at the same barrier per column, so
+// the buffer of column C is not reused before both waves are done with it.
 template <int C>
-__device__ __forceinline__ void zinv_step(double (&z)[64], const double (*LT)[64],
+__device__ __forceinline__ void zinv_step(double (&z)[64], const double (*col)[64],
                                           const double* invd) {
   if constexpr (C < 64) {
+    __syncthreads();                       // column C and 1 / L_CC are visible
     z[C] *= invd[C];
     constexpr int G = (C + 1) & ~1;
     constexpr int NV = (64 - G) / 2 > 0 ? (64 - G) / 2 : 1;
     if constexpr (G < 64) {
       double2 v[NV];
-      pf_read<G, 64>(LT[C], v);
+      pf_read<G, 64>(col[C & 1], v);
       const double zc = z[C];
 #pragma unroll
       for (int k = G; k < 64; ++k)
         if (k > C) z[k] -= zc * (((k - G) & 1) ? v[(k - G) >> 1].y : v[(k - G) >> 1].x);
+      pin_slots<G, 64>(z);
     }
-    zinv_step<C + 1>(z, LT, invd);
+    zinv_step<C + 1>(z, col, invd);
   }
 }
 
@@ -253,52 +256,54 @@ __device__ __forceinline__ void zinv_step(double (&z)[64], const double (*LT)[64
 // Z (64 x 64 row-major, lower; rows and columns beyond kb are the identity).  Rows of the
 // block beyond kb are identity rows.  Entries above the diagonal pick up finite values in
 // registers that are never written back, which keeps the update loop free of masks.
-__global__ __launch_bounds__(64) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
-                                                int kb, double* __restrict__ Z, int* flags) {
-  __shared__ __attribute__((aligned(16))) double Ls[64][64];
+// Two waves: wave 0 factors (one row per lane), wave 1 forms the inverse alongside.
+__global__ __launch_bounds__(128) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
+                                                 int kb, double* __restrict__ Z, int* flags) {
   __shared__ double Lrow[64][65];      // row-major copy of the factor for the global store
   __shared__ __attribute__((aligned(16))) double col[2][64];
   __shared__ double invd[64];
-  const int r = threadIdx.x;
-  // all 64 loads of a thread in flight at once, unconditional (indices clamped into the
-  // block, the unwanted values replaced afterwards), coalesced row by row
-  const int rc = r < kb ? r : kb - 1;
-  double ld[64];
+  const int r = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  if (wave == 0) {
+    // all 64 loads of a thread in flight at once, unconditional (indices clamped into the
+    // block, the unwanted values replaced afterwards), coalesced row by row
+    const int rc = r < kb ? r : kb - 1;
+    double ld[64];
 #pragma unroll
-  for (int i = 0; i < 64; ++i) ld[i] = A[(k0 + (i < kb ? i : kb - 1)) * lda + k0 + rc];
+    for (int i = 0; i < 64; ++i) ld[i] = A[(k0 + (i < kb ? i : kb - 1)) * lda + k0 + rc];
 #pragma unroll
-  for (int i = 0; i < 64; ++i) Ls[i][r] = (i < kb && r <= i) ? ld[i] : ((i == r) ? 1.0 : 0.0);
-  __syncthreads();
-  double a[64];
-#pragma unroll
-  for (int c = 0; c < 64; ++c) a[c] = Ls[r][c];
-  bool notpd = false;
-  pf_scale<0>(a, col[0], invd, r, notpd);
-  __syncthreads();
-  pf_step<0>(a, col, invd, r, notpd);
-  if (notpd && r == 0) flags[0] = 1;
-  __syncthreads();
-  // transposed copy Ls[c][r] = L[r][c] for the inverse and a row-major copy for the store
-  // (zero above the diagonal); both written without bank conflicts
-#pragma unroll
-  for (int c = 0; c < 64; ++c) {
-    const double v = (c <= r) ? a[c] : 0.0;
-    Ls[c][r] = v;
-    Lrow[r][c] = v;
+    for (int i = 0; i < 64; ++i) Lrow[i][r] = (i < kb && r <= i) ? ld[i] : ((i == r) ? 1.0 : 0.0);
   }
   __syncthreads();
-  // row i of the factor, zeros above the diagonal (the upper triangle of a diagonal block
-  // is never read)
+  if (wave == 0) {
+    double a[64];
 #pragma unroll
-  for (int i = 0; i < 64; ++i)
-    if (i < kb && r < kb) A[(k0 + i) * lda + k0 + r] = Lrow[i][r];
-  double z[64];
+    for (int c = 0; c < 64; ++c) a[c] = Lrow[r][c];
+    bool notpd = false;
+    pf_scale<0>(a, col[0], invd, r, notpd);
+    __syncthreads();                       // matches the first barrier of the inverse
+    pf_step<0>(a, col, invd, r, notpd);
+    if (notpd && r == 0) flags[0] = 1;
+    // row-major copy for the store (zero above the diagonal), written without conflicts
 #pragma unroll
-  for (int k = 0; k < 64; ++k) z[k] = (k == r) ? 1.0 : 0.0;
-  zinv_step<0>(z, Ls, invd);
-  // Z[k][r] = z[k]: one row of Z per instruction across the wave (coalesced)
+    for (int c = 0; c < 64; ++c) Lrow[r][c] = (c <= r) ? a[c] : 0.0;
+  } else {
+    double z[64];
 #pragma unroll
-  for (int k = 0; k < 64; ++k) Z[k * 64 + r] = z[k];
+    for (int k = 0; k < 64; ++k) z[k] = (k == r) ? 1.0 : 0.0;
+    zinv_step<0>(z, col, invd);
+    // Z[k][r] = z[k]: one row of Z per instruction across the wave (coalesced)
+#pragma unroll
+    for (int k = 0; k < 64; ++k) Z[k * 64 + r] = z[k];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // row i of the factor, zeros above the diagonal (the upper triangle of a diagonal
+    // block is never read)
+#pragma unroll
+    for (int i = 0; i < 64; ++i)
+      if (i < kb && r < kb) A[(k0 + i) * lda + k0 + r] = Lrow[i][r];
+  }
 }
 
 // R[i][j] = M[K-1-i][K-1-j] (upper), rdiag / inv_rdiag.
@@ -763,7 +768,7 @@ hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s
   for (int64_t k0 = 0; k0 < K; k0 += 64) {
     const int kb = (int)((K - k0) < 64 ? (K - k0) : 64);
     prof_begin(s, "chol_potrf");
-    hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(64), 0, s, A, K, k0, kb, Z, flags);
+    hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(128), 0, s, A, K, k0, kb, Z, flags);
     prof_end(s);
     const int64_t rest = K - k0 - kb;
     if (rest > 0) {
