@@ -3,6 +3,7 @@
 #include "fq_internal.h"
 #include "../../include/fq.h"
 
+#include <algorithm>
 #include <math.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -138,7 +139,12 @@ struct AnaLayout {
   u16 *po_hi, *po_lo, *pi_hi, *pi_lo, *wn_hi, *wn_lo, *tt_hi, *tt_lo, *h_hi, *h_lo, *g_hi, *g_lo;
   int64_t lo_, li_;   // pad(d_out), pad(d_in): multiples of 32
   int64_t ko8, ki8;   // pad8(K_out), pad8(K_in)
+  float* tailp;       // K-split scratch for a short last round of tiles (or null)
 };
+
+// Products with this many output tiles or fewer fill at most one round of the compute
+// units and never take the K-split tail; smaller layouts carry no scratch for it.
+static constexpr int64_t kTailMinTiles = 64;
 
 static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out, int64_t K_in,
                               void* ws, AnaLayout* L) {
@@ -160,6 +166,10 @@ static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out
   l.h_lo = c.take<u16>((size_t)l.li_ * l.li_);
   l.g_hi = c.take<u16>((size_t)l.li_ * l.ki8);
   l.g_lo = c.take<u16>((size_t)l.li_ * l.ki8);
+  const int64_t tiles = std::max({gemm_tiles(l.li_, K_out),
+                                  gemm_tiles(K_out, K_in),
+                                  gemm_tiles(l.li_, K_in)});
+  l.tailp = tiles > kTailMinTiles ? c.take<float>(gemm_tail_bytes() / sizeof(float)) : nullptr;
   if (L) *L = l;
   return c.off + 256;
 }
@@ -209,6 +219,7 @@ struct SynLayout {
   u16 *q, *pl_hi, *pl_lo, *pi_hi, *pi_lo, *nt_hi, *nt_lo;
   int64_t ko, ki;   // pad(K_out), pad(K_in): multiples of 32
   int64_t do8;      // pad8(d_out)
+  float* tailp;     // K-split scratch for a short last round of tiles (or null)
 };
 
 static size_t synthesis_layout(int64_t K_out, int64_t K_in, int64_t d_out, int64_t d_in,
@@ -225,6 +236,9 @@ static size_t synthesis_layout(int64_t K_out, int64_t K_in, int64_t d_out, int64
   l.pi_lo = c.take<u16>((size_t)d_in * l.ki);
   l.nt_hi = c.take<u16>((size_t)l.ki * l.do8);
   l.nt_lo = c.take<u16>((size_t)l.ki * l.do8);
+  const int64_t tiles = std::max(gemm_tiles(l.ki, d_out),
+                                 gemm_tiles(d_out, d_in));
+  l.tailp = tiles > kTailMinTiles ? c.take<float>(gemm_tail_bytes() / sizeof(float)) : nullptr;
   if (L) *L = l;
   return c.off + 256;
 }
@@ -413,7 +427,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       }
       g.epi = EPI_SPLIT; g.c_hi = L.tt_hi; g.c_lo = L.tt_lo; g.ldc = L.ko8; g.ldc_pad = L.ko8;
       g.name = "gemm_analysis_w1";
-      e = gemm_run(g, nullptr, s);
+      e = gemm_run(g, L.tailp, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 1");
       // D = T P_in  (K_out x K_in)
       GemmDesc g2 = mn_gemm((int)K_out, (int)K_in, (int)L.li_, L.tt_hi, L.tt_lo, L.ko8, L.pi_hi,
@@ -421,7 +435,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       three(g2);
       g2.epi = EPI_F32; g2.c = D; g2.ldc = K_in;
       g2.name = "gemm_analysis_w2";
-      e = gemm_run(g2, nullptr, s);
+      e = gemm_run(g2, L.tailp, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 2");
     }
   }
@@ -439,7 +453,7 @@ fq_status fq_frame_analysis(void* stream, const void* W, int wt, int64_t d_out, 
       three(g);
       g.epi = EPI_SPLIT; g.c_hi = L.g_hi; g.c_lo = L.g_lo; g.ldc = L.ki8; g.ldc_pad = L.ki8;
       g.name = "gemm_analysis_h1";
-      e = gemm_run(g, nullptr, s);
+      e = gemm_run(g, L.tailp, s);
       if (e != hipSuccess) return hip_fail(e, "analysis gemm 3");
       // Ht = P_in^T G  (K_in x K_in, upper tiles mirrored)
       GemmDesc g2 = mn_gemm((int)K_in, (int)K_in, (int)L.li_, L.pi_hi, L.pi_lo, L.ki8, L.g_hi,
@@ -562,7 +576,7 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1;
   g.epi = EPI_SPLIT; g.c_hi = L.nt_hi; g.c_lo = L.nt_lo; g.ldc = L.do8; g.ldc_pad = L.do8;
   g.name = "gemm_synthesis_1";
-  if ((e = gemm_run(g, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 1");
+  if ((e = gemm_run(g, L.tailp, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 1");
   // W_hat = N P_in^T  (d_out x d_in)
   GemmDesc g2;
   g2.M = (int)d_out; g2.N = (int)d_in; g2.K = (int)L.ki;
@@ -572,7 +586,7 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   g2.pa[0] = 0; g2.pb[0] = 0; g2.pa[1] = 0; g2.pb[1] = 1; g2.pa[2] = 1; g2.pb[2] = 0;
   g2.epi = EPI_F32; g2.c = W_hat; g2.ldc = d_in;
   g2.name = "gemm_synthesis_2";
-  if ((e = gemm_run(g2, nullptr, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 2");
+  if ((e = gemm_run(g2, L.tailp, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 2");
   return FQ_OK;
 }
 

@@ -25,7 +25,8 @@ enum Epilogue {
   EPI_F32 = 0,      // c[row * ldc + col] = acc
   EPI_SPLIT = 1,    // c_hi/c_lo[row * ldc + col] = bf16 pair of acc
   EPI_SYM = 2,      // upper tiles only; c[row][col] and c[col][row] for row <= col
-  EPI_PARTIAL = 3   // upper tiles only, split over K; fp32 partial tiles, tile-major
+  EPI_PARTIAL = 3,  // upper tiles only, split over K; fp32 partial tiles, tile-major
+  EPI_TAIL = 4      // internal: tiles of a short last round, split over K (fp32 partials)
 };
 
 struct GemmDesc {
@@ -50,7 +51,11 @@ struct GemmDesc {
 // Workspace bytes needed by EPI_PARTIAL for an N x N symmetric product split ksplit ways.
 size_t gemm_partial_bytes(int N, int ksplit);
 int gemm_sym_tiles(int N);
+int64_t gemm_tiles(int64_t M, int64_t N);   // output tiles of an M x N product
+// partial: EPI_PARTIAL's workspace, or (for EPI_F32 / EPI_SPLIT) an optional scratch of
+// gemm_tail_bytes() that lets a short last round of tiles be split over K.
 hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s);
+size_t gemm_tail_bytes();
 // H (+)= sum of the ksplit partial tiles (fp64), mirrored to full symmetric storage.
 hipError_t syrk_reduce(const float* partial, int N, int ksplit, float* H, int64_t ldh,
                        int accumulate, hipStream_t s);

@@ -459,6 +459,8 @@ struct AParams {
   int tiles_m, tiles_n, ntiles;
   int ksplit, k_per_split;
   float* part;
+  int tile0, tcount;    // this launch covers tiles [tile0, tile0 + tcount) (x ksplit)
+  int ra, rb;           // row extents the operand loads are clamped to (see gemm_run)
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -570,15 +572,36 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
   const int wm = wave / WN, wn = wave % WN;
   constexpr bool SYM = (EPI == EPI_SYM || EPI == EPI_PARTIAL);
 
-  int split, tm, tn;
+  // work-group id -> (split, tile): each XCD (ids dealt round-robin to 8) takes a
+  // contiguous range; symmetric products walk the upper triangle row by row, the others
+  // go down groups of 8 tile-rows column by column
+  int split, tm, tn, tloc;
   {
-    KParams kp{};
-    kp.tiles_m = p.tiles_m; kp.tiles_n = p.tiles_n; kp.ntiles = p.ntiles;
-    tile_coords(kp, SYM, split, tm, tn);
+    const int nb = gridDim.x, bid = blockIdx.x;
+    const int per = nb / 8, rem = nb % 8;
+    const int xcd = bid % 8, idx = bid / 8;
+    const int bb = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+    split = bb / p.tcount;
+    tloc = bb - split * p.tcount;
+    int t = p.tile0 + tloc;
+    if (SYM) {
+      int row = 0, cnt = p.tiles_n;
+      while (t >= cnt) { t -= cnt; ++row; --cnt; }
+      tm = row;
+      tn = row + t;
+    } else {
+      const int G = 8;
+      const int g = t / (G * p.tiles_n);
+      const int first = g * G;
+      const int gs = min(G, p.tiles_m - first);
+      const int in = t - g * G * p.tiles_n;
+      tm = first + in % gs;
+      tn = in / gs;
+    }
   }
   const int m0 = tm * BM, n0 = tn * BN;
   int kbeg = 0, kend = p.K;
-  if (EPI == EPI_PARTIAL) {
+  if (EPI == EPI_PARTIAL || EPI == EPI_TAIL) {
     kbeg = split * p.k_per_split;
     kend = min(p.K, kbeg + p.k_per_split);
   }
@@ -586,8 +609,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
   const int nstage = nkt * p.npass;
 
   uint32_t ga[NI], gb[NI];
-  dma_offsets<AMN, NI>(p.lda, m0, p.M, wave, lane, ga);
-  dma_offsets<BMN, NI>(p.ldb, n0, p.N, wave, lane, gb);
+  dma_offsets<AMN, NI>(p.lda, m0, p.ra, wave, lane, ga);
+  dma_offsets<BMN, NI>(p.ldb, n0, p.rb, wave, lane, gb);
   uint32_t fa[NBM][2], fb[NBN][2];
   frag_offsets<AMN, NBM>(wm * 128, lane, fa);
   frag_offsets<BMN, NBN>(wn * 32 * NBN, lane, fb);
@@ -750,7 +773,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
     for (int v = 0; v < 16; ++v) {
       const int rl = wm * 128 + i * 32 + (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
       const int row = m0 + rl;
-      if (EPI != EPI_PARTIAL && row >= p.M) continue;
+      if (EPI != EPI_PARTIAL && EPI != EPI_TAIL && row >= p.M) continue;
 #pragma unroll
       for (int j = 0; j < NBN; ++j) {
         const int cl = wn * 32 * NBN + j * 32 + (lane & 31);
@@ -759,6 +782,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
         if (EPI == EPI_PARTIAL) {
           const int tidx = tm * p.tiles_n - (tm * (tm - 1)) / 2 + (tn - tm);
           p.part[((int64_t)split * p.ntiles + tidx) * (BM * BN) + rl * BN + cl] = x;
+        } else if (EPI == EPI_TAIL) {
+          p.part[((int64_t)split * p.tcount + tloc) * (BM * BN) + rl * BN + cl] = x;
         } else if (EPI == EPI_F32) {
           if (col < p.N) p.c[(int64_t)row * p.ldc + col] = x;
         } else if (EPI == EPI_SPLIT) {
@@ -776,6 +801,49 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
           }
         }
       }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ tail reduction
+// Tiles [tile0, tile0 + tcount) of a non-symmetric product computed as ksplit K-slices:
+// sum the slices (fp64) and apply the product's epilogue.  One thread per 4 columns.
+__global__ __launch_bounds__(256) void k_tail_reduce(const float* __restrict__ part, int ksplit,
+                                                     int tile0, int tcount, int tiles_m,
+                                                     int tiles_n, int M, int N, int epi,
+                                                     float* __restrict__ c, int64_t ldc,
+                                                     u16* __restrict__ c_hi,
+                                                     u16* __restrict__ c_lo, int ldc_pad) {
+  const int tloc = blockIdx.y;
+  const int t = tile0 + tloc;
+  const int G = 8;
+  const int g = t / (G * tiles_n);
+  const int first = g * G;
+  const int gs = min(G, tiles_m - first);
+  const int in = t - g * G * tiles_n;
+  const int tm = first + in % gs, tn = in / gs;
+  const int e0 = (blockIdx.x * 256 + threadIdx.x) * 4;     // element of the 256 x 256 tile
+  if (e0 >= BM * BN) return;
+  const int rl = e0 / BN, cl = e0 % BN;
+  const int row = tm * BM + rl;
+  if (row >= M) return;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int sp = 0; sp < ksplit; ++sp) {
+    const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)sp * tcount + tloc) * (BM * BN) + e0);
+    acc[0] += v.x; acc[1] += v.y; acc[2] += v.z; acc[3] += v.w;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int col = tn * BN + cl + q;
+    const float x = (float)acc[q];
+    if (epi == EPI_F32) {
+      if (col < N) c[(int64_t)row * ldc + col] = x;
+    } else if (col < ldc_pad) {
+      const bool inb = col < N;
+      const uint32_t h = inb ? bf16_rne_bits(x) : 0u;
+      const uint32_t l = inb ? bf16_rne_bits(x - __uint_as_float(h << 16)) : 0u;
+      c_hi[(int64_t)row * ldc + col] = (u16)h;
+      c_lo[(int64_t)row * ldc + col] = (u16)l;
     }
   }
 }
@@ -965,7 +1033,25 @@ bool dispatch_epi(const KParams& p, int epi, int grid, hipStream_t s) {
 }
 
 
+// compute units of the current device (cached per device)
+int compute_units() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cache[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 }  // namespace
+
+size_t gemm_tail_bytes() { return (size_t)256 * BM * BN * sizeof(float); }
+
+int64_t gemm_tiles(int64_t M, int64_t N) { return ((M + BM - 1) / BM) * ((N + BN - 1) / BN); }
 
 int gemm_sym_tiles(int N) {
   const int t = (N + BN - 1) / BN;
@@ -1005,10 +1091,14 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
   p.k_per_split = kt_per * BK;
   p.part = partial;
   const int grid = p.ntiles * p.ksplit;
-  // asynchronous path: K a multiple of 32 (of each K-split), 16-byte aligned operands,
-  // M/N-major operands with rows a multiple of 8
+  // asynchronous path: K a multiple of 32 (of each K-split), 16-byte aligned operands;
+  // an M/N-major operand is loaded in 8-element pieces, so its extent must be a multiple
+  // of 8 or its rows must hold the extent rounded up to 8 (the extra elements only reach
+  // output rows / columns that are never stored)
   const bool kp_ok = (p.k_per_split % ABK == 0) && (d.K % ABK == 0);
-  const bool mn_ok = (d.a_kmajor || d.M % 8 == 0) && (d.b_kmajor || d.N % 8 == 0);
+  const int m8 = (d.M + 7) / 8 * 8, n8 = (d.N + 7) / 8 * 8;
+  const bool mn_ok = (d.a_kmajor || d.M % 8 == 0 || d.lda >= m8) &&
+                     (d.b_kmajor || d.N % 8 == 0 || d.ldb >= n8);
   if (kp_ok && mn_ok && p.aligned_a && p.aligned_b) {
     AParams q{};
     q.M = d.M; q.N = d.N; q.K = d.K;
@@ -1018,26 +1108,65 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     q.c = d.c; q.ldc = d.ldc; q.c_hi = d.c_hi; q.c_lo = d.c_lo; q.ldc_pad = p.ldc_pad;
     q.tiles_m = p.tiles_m; q.tiles_n = p.tiles_n; q.ntiles = p.ntiles;
     q.ksplit = p.ksplit; q.k_per_split = p.k_per_split; q.part = partial;
+    q.ra = d.a_kmajor ? d.M : m8;
+    q.rb = d.b_kmajor ? d.N : n8;
     prof_begin(s, d.name);
-    const dim3 gr(grid);
-#define FQ_LAUNCH_ASYNC(AMN, BMN, F16)                                                                  \
-    switch (d.epi) {                                                                                      \
-      case EPI_F32: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_F32, 8>), gr, dim3(512), 0, s, q); break;     \
-      case EPI_SPLIT: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SPLIT, 8>), gr, dim3(512), 0, s, q); break; \
-      case EPI_SYM: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_SYM, 8>), gr, dim3(512), 0, s, q); break;     \
-      default: hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, EPI_PARTIAL, 8>), gr, dim3(512), 0, s, q); break;      \
+#define FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, E, G)                                                        \
+    hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, E, 8>), dim3(G), dim3(512), 0, s, q);
+#define FQ_LAUNCH_ASYNC(AMN, BMN, F16, E, G)                                                           \
+    switch (E) {                                                                                        \
+      case EPI_F32: FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, EPI_F32, G) break;                                 \
+      case EPI_SPLIT: FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, EPI_SPLIT, G) break;                             \
+      case EPI_SYM: FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, EPI_SYM, G) break;                                 \
+      case EPI_TAIL: FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, EPI_TAIL, G) break;                               \
+      default: FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, EPI_PARTIAL, G) break;                                  \
     }
     // 8 waves (2 per SIMD, 128 x 64 wave tiles) measured ahead of 4 waves of 128 x 128
     const bool amn = !d.a_kmajor, bmn = !d.b_kmajor;
-    if (amn && bmn) {
-      if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true) } else { FQ_LAUNCH_ASYNC(true, true, false) }
-    } else if (amn) {
-      if (d.f16) { FQ_LAUNCH_ASYNC(true, false, true) } else { FQ_LAUNCH_ASYNC(true, false, false) }
-    } else if (bmn) {
-      if (d.f16) { FQ_LAUNCH_ASYNC(false, true, true) } else { FQ_LAUNCH_ASYNC(false, true, false) }
+    auto launch = [&](int epi, int g) {
+      if (amn && bmn) {
+        if (d.f16) { FQ_LAUNCH_ASYNC(true, true, true, epi, g) } else { FQ_LAUNCH_ASYNC(true, true, false, epi, g) }
+      } else if (amn) {
+        if (d.f16) { FQ_LAUNCH_ASYNC(true, false, true, epi, g) } else { FQ_LAUNCH_ASYNC(true, false, false, epi, g) }
+      } else if (bmn) {
+        if (d.f16) { FQ_LAUNCH_ASYNC(false, true, true, epi, g) } else { FQ_LAUNCH_ASYNC(false, true, false, epi, g) }
+      } else {
+        if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true, epi, g) } else { FQ_LAUNCH_ASYNC(false, false, false, epi, g) }
+      }
+    };
+    // A short last round of tiles (at most half the compute units busy) is split over K
+    // into fp32 partial tiles and reduced with the product's epilogue.
+    const int cus = compute_units();
+    const int rounds = (p.ntiles + cus - 1) / cus;
+    const int tail = p.ntiles - (rounds - 1) * cus;
+    const int ksteps = d.K / ABK;
+    int ts = (tail > 0) ? cus / tail : 0;
+    if (ts > ksteps / 4) ts = ksteps / 4;
+    const int kps = ts > 0 ? (ksteps + ts - 1) / ts : 0;   // k-steps per slice
+    if (kps > 0) ts = (ksteps + kps - 1) / kps;              // no empty slice
+    const bool use_tail = partial && rounds >= 2 && tail <= cus / 2 && ts >= 2 &&
+                          (d.epi == EPI_F32 || d.epi == EPI_SPLIT) &&
+                          (size_t)tail * ts * BM * BN * sizeof(float) <= gemm_tail_bytes();
+    if (use_tail) {
+      q.tile0 = 0;
+      q.tcount = p.ntiles - tail;
+      q.ksplit = 1;
+      launch(d.epi, q.tcount);
+      q.tile0 = p.ntiles - tail;
+      q.tcount = tail;
+      q.ksplit = ts;
+      q.k_per_split = kps * ABK;
+      q.part = partial;
+      launch(EPI_TAIL, tail * ts);
+      hipLaunchKernelGGL(k_tail_reduce, dim3(BM * BN / 1024, tail), dim3(256), 0, s, partial, ts,
+                         q.tile0, tail, p.tiles_m, p.tiles_n, d.M, d.N, d.epi, d.c, d.ldc,
+                         d.c_hi, d.c_lo, q.ldc_pad);
     } else {
-      if (d.f16) { FQ_LAUNCH_ASYNC(false, false, true) } else { FQ_LAUNCH_ASYNC(false, false, false) }
+      q.tile0 = 0;
+      q.tcount = p.ntiles;
+      launch(d.epi, grid);
     }
+#undef FQ_LAUNCH_ASYNC_E
 #undef FQ_LAUNCH_ASYNC
     prof_end(s);
     return last_launch_error();

@@ -249,3 +249,53 @@ def test_poisoned_workspaces(wt):
     Who = O.synthesis(cg, scale.cpu().numpy().astype(np.float64),
                       zero.cpu().numpy().astype(np.float64), Po, Pi)
     assert rel_fro(Wh.cpu().numpy(), Who) < 1e-5
+
+
+def _max_tile_rel(A, B, t=256):
+    """Largest relative Frobenius error over the 256 x 256 output tiles."""
+    worst = 0.0
+    for i in range(0, A.shape[0], t):
+        for j in range(0, A.shape[1], t):
+            worst = max(worst, rel_fro(A[i:i + t, j:j + t], B[i:i + t, j:j + t]))
+    return worst
+
+
+@pytest.mark.parametrize("d_out,d_in,wt", [(1000, 4100, "f32"), (4100, 1000, "bf16")])
+def test_short_last_round_products(d_out, d_in, wt):
+    """Products with 17 x 17 output tiles leave a last round of 33 tiles on 256 compute
+    units; those are computed as K-slices in a scratch area and reduced.  Every tile,
+    the reduced ones included, is checked, with NaN-filled workspaces."""
+    torch = need_gpu()
+    fq = _fq()
+    rng = np.random.default_rng(d_out + d_in)
+    k = 1050                                     # K_out = K_in = 4200: 17 tiles
+    Po, Pi = _frames(d_out, d_in, k, k)
+    K_out, K_in = Po.shape[1], Pi.shape[1]
+    Ws = _rand_storage(rng, (d_out, d_in), wt, 0.02)
+    Xs = _rand_storage(rng, (300, d_in), "f32")
+    Hn = O.hessian(Xs.astype(np.float64)).astype(np.float32)
+    W, P_out, P_in = upload(Ws, wt), torch.from_numpy(Po).cuda(), torch.from_numpy(Pi).cuda()
+    H = torch.from_numpy(Hn).cuda()
+    dt = {"bf16": fq.FQ_BF16, "f32": fq.FQ_F32}[wt]
+
+    def poisoned(nbytes):
+        return torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+
+    D = torch.empty((K_out, K_in), dtype=torch.float32, device="cuda")
+    Ht = torch.empty((K_in, K_in), dtype=torch.float32, device="cuda")
+    fq.fq_frame_analysis(W, P_out, P_in, H, D, Ht,
+                         ws=poisoned(fq.fq_frame_analysis_workspace_bytes(dt, d_out, d_in, K_out, K_in)))
+    codes = rng.integers(0, 4, size=(K_out, K_in))
+    scale = rng.uniform(0.01, 0.1, K_out).astype(np.float32)
+    zero = rng.integers(0, 4, K_out).astype(np.float32)
+    Wh = torch.empty((d_out, d_in), dtype=torch.float32, device="cuda")
+    fq.fq_frame_synthesis(torch.from_numpy(O.pack2(codes).view(np.int32)).cuda(),
+                          torch.from_numpy(scale).cuda(), torch.from_numpy(zero).cuda(), P_out,
+                          P_in, Wh,
+                          ws=poisoned(fq.fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in)))
+    torch.cuda.synchronize()
+    Do, Hto = O.frame_analysis(gen.storage_to_f32(Ws, wt), Po, Pi, Hn)
+    assert _max_tile_rel(D.cpu().numpy(), Do) < 1e-5
+    assert _max_tile_rel(Ht.cpu().numpy(), Hto) < 1e-5
+    Who = O.synthesis(codes, scale.astype(np.float64), zero.astype(np.float64), Po, Pi)
+    assert _max_tile_rel(Wh.cpu().numpy(), Who) < 1e-5
