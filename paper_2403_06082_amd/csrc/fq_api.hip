@@ -30,10 +30,12 @@ static fq_status hip_fail(hipError_t e, const char* where) {
 
 hipError_t last_launch_error() { return hipGetLastError(); }
 
-// tile edge of the fp64 update GEMM (FQ_DGEMM_TILE=64|128 overrides, for tuning)
+// kernel of the fp64 update GEMM: 0 = LDS ring where it applies (FQ_DGEMM_TILE=64|128
+// selects the register-staged kernel with that tile, for comparison)
 static int dgemm_tile_from_env() {
   const char* v = getenv("FQ_DGEMM_TILE");
-  return (v && atoi(v) == 128) ? 128 : 64;
+  const int t = v ? atoi(v) : 0;
+  return (t == 64 || t == 128) ? t : 0;
 }
 static int g_dgemm_tile = dgemm_tile_from_env();
 

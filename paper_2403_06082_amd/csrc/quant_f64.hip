@@ -546,12 +546,20 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
 }
 
 // ------------------------------------------------------------------ fp64 MFMA GEMM
-// C[M x N] = beta * C + alpha * A[M x K] * op(B).  Tile 128 x 128, K step 16, 256
-// threads = 2 x 2 waves of 64 x 64 (4 x 4 v_mfma_f64_16x16x4 blocks each).  Operands are
-// staged k-major in LDS ([k][m], [k][n]) and the next K step is fetched into registers
-// while the current one is multiplied.  A and C may alias when every tile reads only
-// the rows it writes (the in-place triangular solve of the Cholesky panel).
-constexpr int DK = 16, DPAD = 4;
+// C[M x N] = beta * C + alpha * A[M x K] * op(B).  Tile DT x DT (64 or 128), K step 16,
+// 256 threads = 2 x 2 waves of DT/2 x DT/2.  Operands are staged k-major in LDS ([k][m],
+// [k][n]) and the next K step is fetched into registers while the current one is
+// multiplied.  A and C may alias when every tile reads only the rows it writes (the
+// in-place triangular solve of the Cholesky panel).
+//
+// The products use v_mfma_f64_4x4x4f64, which on gfx950 sustains about 1.6x the fp64
+// rate of the 16x16x4 form.  One instruction is four independent 4 x 4 x 4 products
+// (blocks b = 0..3); lane l holds A_b[i][k] at l = 4b + i + 16k, B_b[k][j] at
+// l = 4b + j + 16k and D_b[i][j] at l = 4b + j + 16i.  The blocks are laid 2 x 2
+// (b = 2 bi + bj) over an 8 x 8 output sub-tile, so every A value feeds two blocks and
+// every B value two.
+constexpr int DK = 16, DPAD = 8;   // row pitch = DT + 8 doubles: the four k rows of a
+                                   // fragment read fall on disjoint banks
 
 struct DgemmArgs {
   int64_t M, N, K;
@@ -562,8 +570,8 @@ struct DgemmArgs {
   int b_trans, lower_only, tiles_n;
 };
 
-// Tile DT x DT with 256 threads; each wave owns a (DT/2) x (DT/2) quarter built from
-// WT x WT blocks of 16 x 16 (WT = DT / 32).
+// One K step (16) of the DT x DT tile's operands: each of the 256 threads fetches DT / 16
+// doubles of A and of op(B) (zero outside the matrices).
 template <int DT>
 __device__ __forceinline__ void dg_load(const DgemmArgs& p, int64_t m0, int64_t n0, int64_t k0,
                                         double (&ra)[DT / 16], double (&rb)[DT / 16], int tid) {
@@ -612,7 +620,6 @@ __device__ __forceinline__ void dg_store(const DgemmArgs& p, double (*As)[DT + D
 
 template <int DT>
 __global__ __launch_bounds__(256) void k_dgemm(DgemmArgs p) {
-  constexpr int WT = DT / 32;
   __shared__ double As[2][DK][DT + DPAD];
   __shared__ double Bs[2][DK][DT + DPAD];
   int tm, tn;
@@ -628,11 +635,15 @@ __global__ __launch_bounds__(256) void k_dgemm(DgemmArgs p) {
   const int64_t m0 = (int64_t)tm * DT, n0 = (int64_t)tn * DT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  doublex4 acc[WT][WT];
+  constexpr int WS = DT / 16;           // 8 x 8 sub-tiles per wave side
+  double acc[WS][WS];
 #pragma unroll
-  for (int i = 0; i < WT; ++i)
+  for (int i = 0; i < WS; ++i)
 #pragma unroll
-    for (int j = 0; j < WT; ++j) acc[i][j] = (doublex4){0.0, 0.0, 0.0, 0.0};
+    for (int j = 0; j < WS; ++j) acc[i][j] = 0.0;
+  const int blk = (lane >> 2) & 3, bi = blk >> 1, bj = blk & 1, q4 = lane & 3, kq = lane >> 4;
+  const int arow = wm * (DT / 2) + 4 * bi + q4;     // fragment row of sub-tile 0
+  const int bcol = wn * (DT / 2) + 4 * bj + q4;     // fragment column of sub-tile 0
 
   double ra[DT / 16], rb[DT / 16];
   const int nk = (int)((p.K + DK - 1) / DK);
@@ -647,37 +658,205 @@ __global__ __launch_bounds__(256) void k_dgemm(DgemmArgs p) {
     if (more) dg_load<DT>(p, m0, n0, (int64_t)(s + 1) * DK, ra, rb, tid);
 #pragma unroll
     for (int kk = 0; kk < DK; kk += 4) {
-      double af[WT], bfv[WT];
+      double af[WS], bfv[WS];
 #pragma unroll
-      for (int i = 0; i < WT; ++i)
-        af[i] = As[buf][kk + (lane >> 4)][wm * (DT / 2) + i * 16 + (lane & 15)];
+      for (int i = 0; i < WS; ++i) af[i] = As[buf][kk + kq][arow + 8 * i];
 #pragma unroll
-      for (int j = 0; j < WT; ++j)
-        bfv[j] = Bs[buf][kk + (lane >> 4)][wn * (DT / 2) + j * 16 + (lane & 15)];
+      for (int j = 0; j < WS; ++j) bfv[j] = Bs[buf][kk + kq][bcol + 8 * j];
 #pragma unroll
-      for (int i = 0; i < WT; ++i)
+      for (int i = 0; i < WS; ++i)
 #pragma unroll
-        for (int j = 0; j < WT; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < WS; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
     }
     if (more) dg_store<DT>(p, As[buf ^ 1], Bs[buf ^ 1], ra, rb, tid);
     __syncthreads();
   }
-  // 16x16 f64 accumulator layout: value v of lane l is row l/16 + 4*v, column l%16.
+  // lane l holds row 4 bi + l / 16, column 4 bj + l % 4 of each 8 x 8 sub-tile; C is
+  // read a sub-tile row at a time, every read before the stores (clamped addresses)
+  const int64_t r0 = m0 + wm * (DT / 2) + 4 * bi + kq;
+  const int64_t c0 = n0 + wn * (DT / 2) + 4 * bj + q4;
 #pragma unroll
-  for (int i = 0; i < WT; ++i)
+  for (int i = 0; i < WS; ++i) {
+    const int64_t row = r0 + 8 * i;
+    double cv[WS];
 #pragma unroll
-    for (int j = 0; j < WT; ++j)
+    for (int j = 0; j < WS; ++j)
+      cv[j] = p.beta != 0.0 ? p.C[min(row, p.M - 1) * p.ldc + min(c0 + 8 * j, p.N - 1)] : 0.0;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int64_t row = m0 + wm * (DT / 2) + i * 16 + (lane >> 4) + 4 * v;
-        const int64_t col = n0 + wn * (DT / 2) + j * 16 + (lane & 15);
-        if (row < p.M && col < p.N) {
-          double* c = p.C + row * p.ldc + col;
-          const double x = p.alpha * acc[i][j][v];
-          *c = (p.beta == 0.0) ? x : p.beta * *c + x;
-        }
-      }
+    for (int j = 0; j < WS; ++j) cv[j] = p.beta * cv[j] + p.alpha * acc[i][j];
+#pragma unroll
+    for (int j = 0; j < WS; j += 2) asm volatile("" : "+v"(cv[j]), "+v"(cv[j + 1]));
+    if (row < p.M) {
+#pragma unroll
+      for (int j = 0; j < WS; ++j)
+        if (c0 + 8 * j < p.N) p.C[row * p.ldc + c0 + 8 * j] = cv[j];
+    }
+  }
+}
+
+// ------------------------------------------------------------------ fp64 GEMM, LDS ring
+// C = beta C + alpha A B for row-major A (M x K, rows 16-byte aligned) and B (K x N),
+// K a multiple of 16: the trailing updates of the rounding.  Tile 128 x 128, 8 waves of
+// 32 x 64 built from 8 x 8 sub-tiles of the 2 x 2 block arrangement above; two
+// work-groups per CU (four waves per SIMD).  The waves copy each K step of 16 straight
+// from global memory into LDS (A in 16-byte pieces, rows clamped to M; B one dword per
+// lane, columns clamped to N element by element), without a pass through registers,
+// into two slots: the copy of step s + 1 runs while step s is multiplied.
+//   A slot: row r at byte 128 r, k stored at position k ^ 2 (r & 7)
+//   B slot: k-row kr at byte 1024 kr, column n stored at position n ^ 8 (kr & 3)
+// so that the 8 rows (A, one k) and 8 columns (B, one k) that a group of 16 lanes
+// reads fall on distinct banks (A pairs k = 2c, 2c + 1 stay together for the 16-byte
+// copies).
+constexpr int RT = 128, RK = 16, RST = 2;
+constexpr int RA_BYTES = RT * RK * 8;               // A part of a slot
+constexpr int RSLOT = 2 * RA_BYTES;
+constexpr int RWAVES = 8;
+constexpr int RA_PER = RA_BYTES / 1024 / RWAVES;     // 16-byte copies per wave and step (2)
+constexpr int RB_PER = RA_BYTES / 256 / RWAVES;      // dword copies per wave and step (8)
+static_assert(RA_PER == 2 && RB_PER == 8, "copy layout below assumes 8 waves");
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Global -> LDS copies (wave-uniform base + per-lane byte offset; lane l lands at
+// lds + 16 l or lds + 4 l).  Inline assembly, so that the compiler does not make every
+// later LDS read wait for them: completion is tracked by the explicit vmcnt wait.
+__device__ __forceinline__ void lds_copy16(const char* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+__device__ __forceinline__ void lds_copy4(const char* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
+               : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+
+__global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
+  __shared__ __attribute__((aligned(16))) char ring[RST * RSLOT];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;          // 32-row group, 64-column half
+  // work-group -> tile: contiguous ranges per XCD (ids are dealt round-robin to 8), then
+  // groups of 8 tile-rows walked column by column
+  int tm, tn;
+  {
+    const int nb = gridDim.x, b = blockIdx.x;
+    const int per = nb / 8, rem = nb % 8;
+    const int xcd = b % 8, idx = b / 8;
+    const int t = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+    const int tiles_m = (int)((p.M + RT - 1) / RT);
+    const int g = t / (8 * p.tiles_n);
+    const int first = g * 8;
+    const int gs = min(8, tiles_m - first);
+    const int in = t - g * 8 * p.tiles_n;
+    tm = first + in % gs;
+    tn = in / gs;
+  }
+  const int64_t m0 = (int64_t)tm * RT, n0 = (int64_t)tn * RT;
+  const int nst = (int)(p.K / RK);
+
+  // A copy i (i = 0, 1) of this wave: rows 8 (2 wave + i) + lane / 8, k pair c ^ (r & 7)
+  // at chunk c = lane % 8.  B copy i: k-row 2 wave + i / 4, columns 32 (i % 4) + 0..31,
+  // column n at position n ^ 8 (k-row & 3); offsets clamp at the last column.
+  uint32_t ga[2], gb[2], gl[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = 8 * (2 * wave + i) + (lane >> 3), c = lane & 7;
+    const int64_t gr = min(m0 + r, p.M - 1) - m0;
+    ga[i] = (uint32_t)((gr * p.lda + 2 * (c ^ (r & 7))) * 8);
+    const int kr = 2 * wave + i;
+    const int nl = (lane >> 1) ^ (8 * (kr & 3));
+    gb[i] = (uint32_t)((kr * p.ldb + nl) * 8 + 4 * (lane & 1));
+    gl[i] = (uint32_t)((kr * p.ldb + (p.N - 1 - n0)) * 8 + 4 * (lane & 1));
+  }
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void*)ring;
+  const char* srcA = reinterpret_cast<const char*>(p.A + m0 * p.lda);
+  const char* srcB = reinterpret_cast<const char*>(p.B + n0);
+  const int64_t stepA = RK * 8, stepB = (int64_t)RK * p.ldb * 8;
+  auto issue = [&](int s) {
+    const uint32_t slot = ring_lds + (uint32_t)((s & 1) * RSLOT);
+    const char* a = srcA + s * stepA;
+    const char* b = srcB + s * stepB;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) lds_copy16(a, ga[i], slot + (2 * wave + i) * 1024);
+    // the clamped offsets are formed here at every step (opaque copies of the bases keep
+    // the compiler from holding all eight in registers)
+    uint32_t b0 = gb[0], b1 = gb[1], l0 = gl[0], l1 = gl[1];
+    asm volatile("" : "+v"(b0), "+v"(b1), "+v"(l0), "+v"(l1));
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      lds_copy4(b, min((i < 4 ? b0 : b1) + 256 * (i & 3), i < 4 ? l0 : l1),
+                slot + RA_BYTES + (8 * wave + i) * 256);
+  };
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // fragment read offsets: A sub-tile i adds 1024 i, k group t uses xa[t]; B sub-tile j
+  // uses xb[j % 4] + 256 (j / 4), k group t adds 4096 t
+  const int blk = (lane >> 2) & 3, bi = blk >> 1, bj = blk & 1, q4 = lane & 3, kq = lane >> 4;
+  const int ra7 = 4 * bi + q4;                      // fragment row mod 8
+  const uint32_t base_a = (uint32_t)((wm * 32 + ra7) * 128);
+  uint32_t xa[4], xb[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) xa[t] = base_a + 8 * ((4 * t + kq) ^ (2 * ra7));
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    xb[j] = (uint32_t)(RA_BYTES + kq * 1024 + (wn * 64 + 4 * bj + q4) * 8 + 64 * (j ^ kq));
+
+  double acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
+
+  if (nst > 0) issue(0);
+  for (int s = 0; s < nst; ++s) {
+    // step s landed (own copies, then everyone's); step s - 1 read by every wave
+    __builtin_amdgcn_s_waitcnt(0x0F70);               // vmcnt(0): lgkmcnt, expcnt untouched
+    barrier();
+    if (s + 1 < nst) issue(s + 1);
+    const char* slot = ring + (s & 1) * RSLOT;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      double af[4], bfv[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const double*>(slot + xa[t] + 1024 * i);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        bfv[j] = *reinterpret_cast<const double*>(slot + xb[j & 3] + 256 * (j >> 2) + 4096 * t);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // lane l holds row 4 bi + l / 16, column 4 bj + l % 4 of each 8 x 8 sub-tile.  C is
+  // read a sub-tile row (8 values) at a time, all reads before the stores (clamped
+  // addresses; values outside the matrix are discarded).
+  const int64_t r0 = m0 + wm * 32 + 4 * bi + kq;
+  const int64_t c0 = n0 + wn * 64 + 4 * bj + q4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t row = r0 + 8 * i;
+    double cv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      cv[j] = p.beta != 0.0 ? p.C[min(row, p.M - 1) * p.ldc + min(c0 + 8 * j, p.N - 1)] : 0.0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cv[j] = p.beta * cv[j] + p.alpha * acc[i][j];
+    // formed before the first store: otherwise each value is computed inside its store's
+    // branch, behind a wait for every earlier store
+#pragma unroll
+    for (int j = 0; j < 8; j += 2) asm volatile("" : "+v"(cv[j]), "+v"(cv[j + 1]));
+    if (row < p.M) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (c0 + 8 * j < p.N) p.C[row * p.ldc + c0 + 8 * j] = cv[j];
+    }
+  }
 }
 
 // ------------------------------------------------------------------ pack / dequant
@@ -827,6 +1006,24 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
   p.A = A; p.lda = lda; p.B = B; p.ldb = ldb; p.C = C; p.ldc = ldc;
   p.b_trans = (int)b_trans;
   p.lower_only = (int)lower_only;
+  // row-major operands, K a multiple of 16, 16-byte aligned A rows and 32-bit copy
+  // offsets: the LDS-ring kernel
+  const bool ring_ok = !b_trans && !lower_only && K > 0 && K % RK == 0 &&
+                       (reinterpret_cast<uintptr_t>(A) & 15) == 0 && lda % 2 == 0 &&
+                       (reinterpret_cast<uintptr_t>(B) & 7) == 0 &&
+                       (int64_t)(RT - 1) * lda * 8 + RK * 8 < ((int64_t)1 << 31) &&
+                       (int64_t)(RK - 1) * ldb * 8 + RT * 8 < ((int64_t)1 << 31);
+  // below about 512 tiles of 128 x 128 (two rounds of two work-groups per CU on 256
+  // CUs) the 64 x 64 kernel's finer grid is measured faster
+  const int64_t ring_tiles = ((M + RT - 1) / RT) * ((N + RT - 1) / RT);
+  if (ring_ok && tile == 0 && ring_tiles >= 512) {
+    p.tiles_n = (int)((N + RT - 1) / RT);
+    const int64_t g = ring_tiles;
+    prof_begin(s, name);
+    hipLaunchKernelGGL(k_dgemm_ring, dim3((unsigned)g), dim3(64 * RWAVES), 0, s, p);
+    prof_end(s);
+    return last_launch_error();
+  }
   const int DT = tile == 128 ? 128 : 64;
   const int tiles_m = (int)((M + DT - 1) / DT), tiles_n = (int)((N + DT - 1) / DT);
   p.tiles_n = tiles_n;
