@@ -5,9 +5,10 @@ One step = the whole pass on one layer with its inputs resident in HBM:
     ->  clip + grid + OPTQ 2-bit rounding (fp64)  ->  W^ = P_l D^ P_prev^T
 on the Llama-2-7B-shaped up_proj layer (11008 x 4096 bf16, X 262,144 x 4096 bf16,
 frames r = 1.1: K_out x K_in = 12112 x 4512, block 128).  Inputs are synthetic and
-seeded (fq_inputs).
+seeded (fq_inputs).  --streams 2 forms D on a second stream while the main stream
+factors H~.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--streams 1|2] [--no-cpu-baseline]
 
 Prints one JSON line.  value = quantized weights per second (d_out * d_in / step time).
 "roofline" is the dominant kernel's algorithmic throughput against its MFMA peak, timed
@@ -187,6 +188,10 @@ def main():
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--layer", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
+                    help="2: D is formed on a second stream while the main stream factors "
+                         "H~ (measured within 0.5%% of one stream: the contractions take "
+                         "every CU); the kernel-timer region always uses one")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="device-to-device copy of this many MiB before the warmup, as the "
                          "known-size reference for hardware byte counters")
@@ -214,10 +219,12 @@ def main():
     n = dev["X"].shape[0]
     bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block)
     stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream() if args.streams == 2 else None
 
-    def step():
+    def step(two=args.streams == 2):
         quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], bufs, block=wl.block,
-                       damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream)
+                       damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream,
+                       side_stream=side if two else None)
 
     if args.copy_probe_mib > 0:
         nb = args.copy_probe_mib << 20
@@ -241,13 +248,14 @@ def main():
     ms = (t1 - t0) * 1000.0 / args.steps
     print(f"[bench] {args.steps} timed steps: {ms:.2f} ms/step", file=sys.stderr, flush=True)
     # second timed region with the per-launch kernel timers (HIP events on the launch
-    # stream around every kernel): the per-kernel breakdown and the roofline come from it
+    # stream around every kernel): the per-kernel breakdown and the roofline come from it.
+    # One stream here, so that no two timed kernels overlap.
     fq.fq_profile_reset()
     fq.fq_profile_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step()
+        step(two=False)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     fq.fq_profile_enable(False)
@@ -317,6 +325,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 3),
         "ms_per_step_with_kernel_timers": round(ms_timed, 3),
+        "kernel_timer_streams": 1,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -328,7 +337,7 @@ def main():
                                f"(r={wl.r}, rho={wl.rho}), {wl.bits}-bit, block {wl.block}, "
                                f"damp {wl.damp}, clip {wl.clip_sigmas} sigma",
                    "d_out": L.d_out, "d_in": L.d_in, "n_tokens": n, "K_out": K_out,
-                   "K_in": K_in},
+                   "K_in": K_in, "streams": args.streams},
         "roofline": roof,
         "contraction_mfma_frac": None if contraction_frac is None else round(contraction_frac, 4),
         "contraction_mfma_executed_frac": None if contraction_exec is None else round(contraction_exec, 4),

@@ -15,14 +15,20 @@
  *   fq_frame_synthesis     Theta^ = P_l D^ P_prev^T (Alg. 1 return value; appendix
  *                          "Computational Complexity during Inference")
  *
+ * fq_quantize_frames is also available as its two phases, fq_quantize_prepare (the part
+ * that reads H~ only: damping and the Cholesky factor) and fq_quantize_apply (the part
+ * that reads D), so that the factorization can run on one stream while D is still being
+ * formed on another.
+ *
  * Conventions shared by every call
  *  - Matrices are row-major.  Every array argument is a DEVICE pointer owned by the
  *    caller; the library never allocates device memory.  Each call that needs scratch
  *    space takes a caller-provided workspace `ws` of at least the size returned by its
  *    *_workspace_bytes query (16-byte aligned).
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are stream-ordered and
- *    asynchronous, except fq_quantize_frames, which synchronizes `stream` once at its end
- *    to report the positive-definiteness and finiteness checks.
+ *    asynchronous, except fq_quantize_frames and fq_quantize_apply, which synchronize
+ *    `stream` once at their end to report the positive-definiteness and finiteness
+ *    checks.
  *  - Arguments are validated before anything is launched; on failure the call returns
  *    FQ_ERR_INVALID_ARG (or FQ_ERR_UNSUPPORTED / FQ_ERR_WORKSPACE_TOO_SMALL) and
  *    fq_last_error() describes the problem.  No exception crosses the boundary.
@@ -112,6 +118,28 @@ fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int6
                              double clip_sigmas, uint32_t* codes, float* scale, float* zero,
                              void* ws, size_t ws_bytes);
 size_t fq_quantize_frames_workspace_bytes(int64_t K_out, int64_t K_in, int block);
+
+/*
+ * fq_quantize_frames in two phases sharing one workspace (sized by
+ * fq_quantize_frames_workspace_bytes(K_out, K_in, block)); prepare + apply on the same
+ * workspace gives bit-identical outputs to fq_quantize_frames.
+ *   fq_quantize_prepare  reads Ht only: dead columns, damping (step 3 above) and the
+ *                        Cholesky factor, into ws.  Asynchronous; its checks are reported
+ *                        by the following fq_quantize_apply.
+ *   fq_quantize_apply    reads D and the factor in ws: clip, grid and rounding (steps 1-3),
+ *                        then synchronizes `stream` and reports the checks of both phases.
+ * apply must be ordered after prepare (same stream, or an event the caller records on
+ * prepare's stream and makes apply's stream wait for), with the same K_out, K_in, block
+ * and workspace.  apply does not modify the factor: one prepare serves any number of
+ * applies in stream order (layers that share their input, and so H~, share it too);
+ * apply calls on one workspace must not overlap.  Errors as for fq_quantize_frames; the
+ * H~ checks of prepare are reported by every apply that follows it.
+ */
+fq_status fq_quantize_prepare(void* stream, const float* Ht, int64_t K_out, int64_t K_in,
+                              int block, double damp, void* ws, size_t ws_bytes);
+fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t K_in,
+                            int bits, int block, double clip_sigmas, uint32_t* codes,
+                            float* scale, float* zero, void* ws, size_t ws_bytes);
 
 /*
  * Synthesis of the dequantized layer (Alg. 1 return value; appendix "Computational

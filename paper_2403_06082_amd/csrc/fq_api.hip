@@ -476,32 +476,29 @@ size_t fq_quantize_frames_workspace_bytes(int64_t K_out, int64_t K_in, int block
   return quant_layout(K_out, K_in, block, nullptr, nullptr);
 }
 
-fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int64_t K_out,
-                             int64_t K_in, int bits, int block, double damp, double clip_sigmas,
-                             uint32_t* codes, float* scale, float* zero, void* ws,
-                             size_t ws_bytes) {
-  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
-  if (bits != 2) return fail(FQ_ERR_UNSUPPORTED, "only bits = 2 is implemented");
-  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
-  if (!(damp >= 0.0) || !isfinite(damp)) return fail(FQ_ERR_INVALID_ARG, "damp must be finite and >= 0");
-  if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
-  if (K_out == 0 || K_in == 0) return FQ_OK;
-  if (!D || !Ht || !codes || !scale || !zero) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
-  const size_t need = quant_layout(K_out, K_in, block, nullptr, nullptr);
-  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_quantize_frames_workspace_bytes()");
-  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
-  QuantScratch Q;
-  quant_layout(K_out, K_in, block, base, &Q);
+// the H~ phase: dead columns, damping, the reversed Cholesky factor R (no sync)
+static fq_status quantize_prepare(hipStream_t s, const float* Ht, int64_t K_in, double damp,
+                                  QuantScratch& Q) {
   hipError_t e;
   prof_begin(s, "q_init");
   hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, Q.flags, 4);
   prof_end(s);
-  if ((e = q_stats(D, K_out, K_in, clip_sigmas, Q, s)) != hipSuccess) return hip_fail(e, "stats");
   if ((e = q_hdiag_build(Ht, K_in, damp, Q, s)) != hipSuccess) return hip_fail(e, "hessian prep");
   if ((e = q_cholesky(Q.A, K_in, Q.linv, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
   if ((e = q_reverse_upper(Q.A, K_in, Q.R, Q.inv_rdiag, s)) != hipSuccess) return hip_fail(e, "reverse");
+  return FQ_OK;
+}
+
+// the D phase: clip, grid, rounding with error feedback, packing; then sync and checks
+static fq_status quantize_apply(hipStream_t s, const float* D, int64_t K_out, int64_t K_in,
+                                int bits, int block, double clip_sigmas, uint32_t* codes,
+                                float* scale, float* zero, QuantScratch& Q) {
+  hipError_t e;
+  // this call's own D check (the H~ checks of the prepare phase stay in flags[0..1])
+  prof_begin(s, "q_init");
+  hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, Q.flags + 2, 1);
+  prof_end(s);
+  if ((e = q_stats(D, K_out, K_in, clip_sigmas, Q, s)) != hipSuccess) return hip_fail(e, "stats");
   if ((e = q_clip_grid(D, K_out, K_in, bits, Q, scale, zero, s)) != hipSuccess) return hip_fail(e, "clip/grid");
   const int64_t ldr = res_width(K_in, block);
   const int64_t cw = chunk_width(block), sw = span_width(block);
@@ -528,9 +525,73 @@ fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int6
   if ((e = hipMemcpyAsync(flags, Q.flags, sizeof(flags), hipMemcpyDeviceToHost, s)) != hipSuccess)
     return hip_fail(e, "flag copy");
   if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(e, "stream sync");
-  if (flags[1]) return fail(FQ_ERR_NONFINITE, "D or Ht holds NaN or Inf");
+  if (flags[2]) return fail(FQ_ERR_NONFINITE, "D holds NaN or Inf");
+  if (flags[1]) return fail(FQ_ERR_NONFINITE, "Ht holds NaN or Inf");
   if (flags[0]) return fail(FQ_ERR_NOT_POSITIVE_DEFINITE, "damped Ht is not positive definite");
   return FQ_OK;
+}
+
+static fq_status quantize_ws_check(int64_t K_out, int64_t K_in, int block, void* ws,
+                                   size_t ws_bytes) {
+  const size_t need = quant_layout(K_out, K_in, block, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_quantize_frames_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  return FQ_OK;
+}
+
+static QuantScratch quantize_scratch(int64_t K_out, int64_t K_in, int block, void* ws) {
+  char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+  QuantScratch Q;
+  quant_layout(K_out, K_in, block, base, &Q);
+  return Q;
+}
+
+fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int64_t K_out,
+                             int64_t K_in, int bits, int block, double damp, double clip_sigmas,
+                             uint32_t* codes, float* scale, float* zero, void* ws,
+                             size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (bits != 2) return fail(FQ_ERR_UNSUPPORTED, "only bits = 2 is implemented");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (!(damp >= 0.0) || !isfinite(damp)) return fail(FQ_ERR_INVALID_ARG, "damp must be finite and >= 0");
+  if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!D || !Ht || !codes || !scale || !zero) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  if ((st = quantize_prepare(s, Ht, K_in, damp, Q)) != FQ_OK) return st;
+  return quantize_apply(s, D, K_out, K_in, bits, block, clip_sigmas, codes, scale, zero, Q);
+}
+
+fq_status fq_quantize_prepare(void* stream, const float* Ht, int64_t K_out, int64_t K_in,
+                              int block, double damp, void* ws, size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (!(damp >= 0.0) || !isfinite(damp)) return fail(FQ_ERR_INVALID_ARG, "damp must be finite and >= 0");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!Ht) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  return quantize_prepare((hipStream_t)stream, Ht, K_in, damp, Q);
+}
+
+fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t K_in, int bits,
+                            int block, double clip_sigmas, uint32_t* codes, float* scale,
+                            float* zero, void* ws, size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (bits != 2) return fail(FQ_ERR_UNSUPPORTED, "only bits = 2 is implemented");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!D || !codes || !scale || !zero) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  return quantize_apply((hipStream_t)stream, D, K_out, K_in, bits, block, clip_sigmas, codes,
+                        scale, zero, Q);
 }
 
 // ================================================================ S4: synthesis

@@ -75,7 +75,7 @@ __global__ __launch_bounds__(256) void k_moments(const float* __restrict__ D, in
       acc += d * d;
     }
   }
-  if (bad) flags[1] = 1;
+  if (bad) flags[2] = 1;                 // D non-finite (flags[1]: H~ non-finite)
   const double s = block_sum<256>(acc, sh);
   if (threadIdx.x == 0) red[blockIdx.x] = s;
 }

@@ -30,6 +30,8 @@ SIGNATURES = {
     "fq_quantize_frames": (_i, [_vp, _vp, _vp, _i64, _i64, _i, _i, _d, _d, _vp, _vp, _vp, _vp,
                                 _sz]),
     "fq_quantize_frames_workspace_bytes": (_sz, [_i64, _i64, _i]),
+    "fq_quantize_prepare": (_i, [_vp, _vp, _i64, _i64, _i, _d, _vp, _sz]),
+    "fq_quantize_apply": (_i, [_vp, _vp, _i64, _i64, _i, _i, _d, _vp, _vp, _vp, _vp, _sz]),
     "fq_frame_synthesis": (_i, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp,
                                 _sz]),
     "fq_frame_synthesis_workspace_bytes": (_sz, [_i64, _i64, _i64, _i64]),
@@ -176,6 +178,34 @@ def fq_quantize_frames(D, Ht, codes, scale, zero, bits: int = 2, block: int = 12
     _check(lib().fq_quantize_frames(_stream(stream), _ptr(D), _ptr(Ht), K_out, K_in, bits, block,
                                     float(damp), float(clip_sigmas), _ptr(codes), _ptr(scale),
                                     _ptr(zero), wp, wb))
+    return codes, scale, zero
+
+
+def fq_quantize_prepare(Ht, K_out: int, ws, block: int = 128, damp: float = 0.01,
+                        stream=None):
+    """H~ phase of fq_quantize_frames (damping, Cholesky factor) into the workspace ws."""
+    torch = _torch()
+    K_in = Ht.shape[0]
+    _dev(Ht, "Ht", torch.float32, (K_in, K_in))
+    _dev(ws, "ws", torch.uint8)
+    _check(lib().fq_quantize_prepare(_stream(stream), _ptr(Ht), int(K_out), K_in, block,
+                                     float(damp), _ptr(ws), ws.numel()))
+    return ws
+
+
+def fq_quantize_apply(D, codes, scale, zero, ws, bits: int = 2, block: int = 128,
+                      clip_sigmas: float = 2.0, stream=None):
+    """D phase of fq_quantize_frames, after fq_quantize_prepare on the same workspace."""
+    torch = _torch()
+    K_out, K_in = D.shape
+    _dev(D, "D", torch.float32)
+    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    _dev(ws, "ws", torch.uint8)
+    _check(lib().fq_quantize_apply(_stream(stream), _ptr(D), K_out, K_in, bits, block,
+                                   float(clip_sigmas), _ptr(codes), _ptr(scale), _ptr(zero),
+                                   _ptr(ws), ws.numel()))
     return codes, scale, zero
 
 

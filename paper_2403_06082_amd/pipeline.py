@@ -6,6 +6,10 @@
     W_hat  = fq_frame_synthesis(codes, ...)
 
 Workspaces are allocated once per call site with torch and reused.
+
+With a second stream (side_stream), D = P_out^T W P_in is formed there while the main
+stream factors the damped H~ (fq_quantize_prepare): the Cholesky factorization, a chain
+of small dependent kernels, then overlaps the D contractions.  Outputs are identical.
 """
 from __future__ import annotations
 
@@ -34,6 +38,7 @@ class LayerBuffers:
         self.ws_a = torch.empty(_fq.fq_frame_analysis_workspace_bytes(dt[w_dtype], d_out, d_in,
                                                                       K_out, K_in),
                                 dtype=u8, device=device)
+        self.ws_a2 = None      # second analysis workspace, for the two-stream order
         self.ws_q = torch.empty(_fq.fq_quantize_frames_workspace_bytes(K_out, K_in, block),
                                 dtype=u8, device=device)
         self.ws_s = torch.empty(_fq.fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in),
@@ -41,8 +46,11 @@ class LayerBuffers:
 
 
 def quantize_layer(W, X, P_out, P_in, bufs: LayerBuffers, H=None, Ht=None, bits=2, block=128,
-                   damp=0.01, clip_sigmas=2.0, stream=None):
+                   damp=0.01, clip_sigmas=2.0, stream=None, side_stream=None):
     """Run the pass; returns bufs (H, D, Ht, codes, scale, zero, W_hat filled in)."""
+    if side_stream is not None:
+        return _quantize_layer_two_streams(W, X, P_out, P_in, bufs, H, Ht, bits, block, damp,
+                                           clip_sigmas, stream, side_stream)
     if H is None:
         _fq.fq_hessian_accumulate(X, bufs.H, ws=bufs.ws_h, stream=stream)
         H = bufs.H
@@ -55,4 +63,32 @@ def quantize_layer(W, X, P_out, P_in, bufs: LayerBuffers, H=None, Ht=None, bits=
                            damp=damp, clip_sigmas=clip_sigmas, ws=bufs.ws_q, stream=stream)
     _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
                            ws=bufs.ws_s, stream=stream)
+    return bufs
+
+
+def _quantize_layer_two_streams(W, X, P_out, P_in, bufs, H, Ht, bits, block, damp,
+                                clip_sigmas, stream, side):
+    import torch
+    main = torch.cuda.current_stream() if stream is None else stream
+    if bufs.ws_a2 is None:
+        bufs.ws_a2 = torch.empty_like(bufs.ws_a)
+    if H is None and Ht is None:
+        _fq.fq_hessian_accumulate(X, bufs.H, ws=bufs.ws_h, stream=main)
+        H = bufs.H
+    if Ht is None:
+        _fq.fq_frame_analysis(W, P_out, P_in, H, None, bufs.Ht, ws=bufs.ws_a, stream=main)
+        Ht = bufs.Ht
+    # D on the side stream, started once H~ is done (so that it does not delay H~)
+    ready = torch.cuda.Event()
+    ready.record(main)
+    side.wait_event(ready)
+    _fq.fq_frame_analysis(W, P_out, P_in, None, bufs.D, None, ws=bufs.ws_a2, stream=side)
+    d_done = torch.cuda.Event()
+    d_done.record(side)
+    _fq.fq_quantize_prepare(Ht, bufs.D.shape[0], bufs.ws_q, block=block, damp=damp, stream=main)
+    main.wait_event(d_done)
+    _fq.fq_quantize_apply(bufs.D, bufs.codes, bufs.scale, bufs.zero, bufs.ws_q, bits=bits,
+                          block=block, clip_sigmas=clip_sigmas, stream=main)
+    _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
+                           ws=bufs.ws_s, stream=main)
     return bufs

@@ -75,6 +75,18 @@ def test_invalid_arguments_rejected_before_launch(L):
     assert L.fq_quantize_frames(*args, 2, 128, 0.01, 0.0, *outs) == 1
     assert L.fq_quantize_frames(*args, 2, 128, 0.01, float("nan"), *outs) == 1
     assert L.fq_quantize_frames(*args, 2, 128, 0.01, 2.0, *outs) == 5
+    # the two phases check the same arguments in the same order
+    assert L.fq_quantize_prepare(n, ctypes.c_void_p(64), 4, 4, 0, 0.01, n, 0) == 1
+    assert L.fq_quantize_prepare(n, ctypes.c_void_p(64), 4, 4, 128, float("inf"), n, 0) == 1
+    assert L.fq_quantize_prepare(n, n, 4, 4, 128, 0.01, n, 0) == 1
+    assert L.fq_quantize_prepare(n, ctypes.c_void_p(64), 4, 4, 128, 0.01, n, 0) == 5
+    aouts = (ctypes.c_void_p(64), ctypes.c_void_p(64), ctypes.c_void_p(64), n, 0)
+    assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 3, 128, 2.0, *aouts) == 2
+    assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 2, 128, -2.0, *aouts) == 1
+    assert L.fq_quantize_apply(n, ctypes.c_void_p(64), -4, 4, 2, 128, 2.0, *aouts) == 1
+    assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 2, 128, 2.0, *aouts) == 5
     # empty problems are no-ops
     assert L.fq_quantize_frames(n, n, n, 0, 5, 2, 128, 0.01, 2.0, n, n, n, n, 0) == 0
+    assert L.fq_quantize_prepare(n, n, 0, 5, 128, 0.01, n, 0) == 0
+    assert L.fq_quantize_apply(n, n, 5, 0, 2, 128, 2.0, n, n, n, n, 0) == 0
     assert L.fq_frame_synthesis(n, n, n, n, 5, 5, n, 0, n, 5, n, n, 0) == 0

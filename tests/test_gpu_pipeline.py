@@ -84,3 +84,83 @@ def test_pipeline_tiny256():
 
 def test_pipeline_vitb():
     run_workload("vitb")
+
+
+@pytest.mark.parametrize("key", ["tiny256", "vitb"])
+def test_two_stream_order_is_bit_identical(key):
+    """D formed on a second stream while the main stream factors H~ (prepare / apply)
+    gives exactly the outputs of the one-stream order."""
+    torch = need_gpu()
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    wl = WORKLOADS[key]
+    L = wl.layers[0]
+    X = upload(gen.make_x(wl, L.d_in), wl.x_dtype)
+    Po64, Pi64 = gen.make_frames(wl, 0)
+    P_out, P_in = torch.from_numpy(gen.frame_f32(Po64)).cuda(), torch.from_numpy(gen.frame_f32(Pi64)).cuda()
+    W = upload(gen.make_weight(wl, 0), wl.w_dtype)
+    K_out, K_in = P_out.shape[1], P_in.shape[1]
+    outs = []
+    side = torch.cuda.Stream()
+    for two in (False, True, True):
+        bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, X.shape[0], wl.block)
+        quantize_layer(W, X, P_out, P_in, bufs, block=wl.block, damp=wl.damp,
+                       clip_sigmas=wl.clip_sigmas, side_stream=side if two else None)
+        torch.cuda.synchronize()
+        outs.append({k: getattr(bufs, k).cpu().numpy() for k in
+                     ("H", "D", "Ht", "codes", "scale", "zero", "W_hat")})
+    for o in outs[1:]:
+        for k, v in o.items():
+            np.testing.assert_array_equal(v, outs[0][k], err_msg=k)
+
+
+def test_prepare_apply_match_fused_call():
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    rng = np.random.default_rng(12)
+    K_out, K_in = 300, 200
+    A = rng.standard_normal((400, K_in))
+    Ht = torch.from_numpy((A.T @ A).astype(np.float32)).cuda()
+    Ht = (Ht + Ht.T) / 2
+    D = torch.from_numpy((rng.standard_normal((K_out, K_in)) * 0.02).astype(np.float32)).cuda()
+    res = []
+    for split in (False, True):
+        codes = torch.empty((K_out, (K_in + 15) // 16), dtype=torch.int32, device="cuda")
+        scale = torch.empty((K_out,), dtype=torch.float32, device="cuda")
+        zero = torch.empty((K_out,), dtype=torch.float32, device="cuda")
+        ws = torch.full((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), 0xFF,
+                        dtype=torch.uint8, device="cuda")
+        if split:
+            s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+            fq.fq_quantize_prepare(Ht, K_out, ws, stream=s1)
+            ev = torch.cuda.Event()
+            ev.record(s1)
+            s2.wait_event(ev)
+            fq.fq_quantize_apply(D, codes, scale, zero, ws, stream=s2)
+        else:
+            fq.fq_quantize_frames(D, Ht, codes, scale, zero, ws=ws)
+        torch.cuda.synchronize()
+        res.append((codes.cpu().numpy(), scale.cpu().numpy(), zero.cpu().numpy()))
+    for a, b in zip(res[0], res[1]):
+        np.testing.assert_array_equal(a, b)
+    # one factor, several applies: a non-finite D is reported by its own apply only
+    ws = torch.empty((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), dtype=torch.uint8,
+                     device="cuda")
+    fq.fq_quantize_prepare(Ht, K_out, ws)
+    Dn = D.clone()
+    Dn[7, 3] = float("nan")
+    with pytest.raises(fq.FQError) as ei:
+        fq.fq_quantize_apply(Dn, codes, scale, zero, ws)
+    assert ei.value.status == 4
+    for _ in range(2):
+        fq.fq_quantize_apply(D, codes, scale, zero, ws)
+        torch.cuda.synchronize()
+        for a, b in zip(res[0], (codes.cpu().numpy(), scale.cpu().numpy(), zero.cpu().numpy())):
+            np.testing.assert_array_equal(a, b)
+    # a non-positive-definite H~ found by prepare is reported by apply
+    bad = -torch.eye(K_in, dtype=torch.float32, device="cuda")
+    ws = torch.empty((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), dtype=torch.uint8,
+                     device="cuda")
+    fq.fq_quantize_prepare(bad, K_out, ws, damp=0.0)
+    with pytest.raises(fq.FQError) as ei:
+        fq.fq_quantize_apply(D, codes, scale, zero, ws)
+    assert ei.value.status == 3
