@@ -30,8 +30,11 @@ static fq_status hip_fail(hipError_t e, const char* where) {
 
 hipError_t last_launch_error() { return hipGetLastError(); }
 
-// kernel of the fp64 update GEMM: 0 = LDS ring where it applies (FQ_DGEMM_TILE=64|128
-// selects the register-staged kernel with that tile, for comparison)
+// kernel of the fp64 update GEMMs: by default the LDS-ring kernel for the updates beyond
+// a span (large: K_out x 512 x the rest) and the 64 x 64 kernel for those inside a span
+// (K_out x 128 x at most 384); FQ_DGEMM_TILE=64|128 puts every update on the
+// register-staged kernel with that tile, for comparison
+
 static int dgemm_tile_from_env() {
   const char* v = getenv("FQ_DGEMM_TILE");
   const int t = v ? atoi(v) : 0;
@@ -510,13 +513,14 @@ static fq_status quantize_apply(hipStream_t s, const float* D, int64_t K_out, in
         return hip_fail(e, "rounding block");
       if (i2 < s2) {
         e = dgemm(K_out, s2 - i2, i2 - i1, 1.0, 1.0, Q.res + (i1 - s1), ldr, Q.R + i1 * K_in + i2,
-                  K_in, false, Q.Y + i2, K_in, false, s, "gptq_update", g_dgemm_tile);
+                  K_in, false, Q.Y + i2, K_in, false, s, "gptq_update_span",
+                  g_dgemm_tile ? g_dgemm_tile : 64);
         if (e != hipSuccess) return hip_fail(e, "in-span update");
       }
     }
     if (s2 < K_in) {
       e = dgemm(K_out, K_in - s2, s2 - s1, 1.0, 1.0, Q.res, ldr, Q.R + s1 * K_in + s2, K_in, false,
-                Q.Y + s2, K_in, false, s, "gptq_update", g_dgemm_tile);
+                Q.Y + s2, K_in, false, s, "gptq_update_lazy", g_dgemm_tile);
       if (e != hipSuccess) return hip_fail(e, "lazy update");
     }
   }

@@ -105,7 +105,8 @@ hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int 
 //   lower_only: only tiles with tile_row >= tile_col (for the Cholesky update)
 //   tile: 64 or 128 (register-staged kernel with that tile edge), or 0: the 128 x 128
 //         LDS-ring kernel where its layout rules hold (row-major operands, K % 16 == 0,
-//         16-byte aligned A rows), else the 64 kernel
+//         16-byte aligned A rows), else the 64 kernel.  The ring kernel is the faster one
+//         from about 512 of its tiles up (two rounds of two work-groups per CU).
 hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, const double* A,
                  int64_t lda, const double* B, int64_t ldb, bool b_trans, double* C, int64_t ldc,
                  bool lower_only, hipStream_t s, const char* name, int tile);

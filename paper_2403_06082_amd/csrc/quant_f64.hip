@@ -1013,10 +1013,8 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
                        (reinterpret_cast<uintptr_t>(B) & 7) == 0 &&
                        (int64_t)(RT - 1) * lda * 8 + RK * 8 < ((int64_t)1 << 31) &&
                        (int64_t)(RK - 1) * ldb * 8 + RT * 8 < ((int64_t)1 << 31);
-  // below about 512 tiles of 128 x 128 (two rounds of two work-groups per CU on 256
-  // CUs) the 64 x 64 kernel's finer grid is measured faster
   const int64_t ring_tiles = ((M + RT - 1) / RT) * ((N + RT - 1) / RT);
-  if (ring_ok && tile == 0 && ring_tiles >= 512) {
+  if (ring_ok && tile == 0) {
     p.tiles_n = (int)((N + RT - 1) / RT);
     const int64_t g = ring_tiles;
     prof_begin(s, name);
