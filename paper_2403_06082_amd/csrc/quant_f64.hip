@@ -378,18 +378,16 @@ __global__ __launch_bounds__(256) void k_clip_grid(const float* __restrict__ D, 
 }
 
 // ------------------------------------------------------------------ rounding block
-// Columns [i1, i1 + b) (b <= 128) of every row.  512 threads = 8 waves; each wave is four
-// 16-lane DPP rows ("groups"); a group owns 2 rows of D and lane g of the group holds
-// columns 8g .. 8g+7 of the block for both rows.  At column j every lane evaluates the
-// rounding on its own copy of column j, the owner lane (g = j / 8) keeps the code and
-// the residual D_j - D^_j, the residual is broadcast inside the group with a DPP row
-// broadcast, and every lane folds it into its columns with row j of R (from LDS).
+// Columns [i1, i1 + b) (b <= 128) of every row.  768 threads = 12 waves (three per SIMD:
+// the column chain is latency bound, so more rows in flight per CU rather than more work
+// per lane); each wave is four 16-lane DPP rows ("groups"), a group owns GRK rows of D.
 constexpr int GB = 128;
-constexpr int GTH = 384;
-constexpr int GROWS = GTH / 16 * 2;   // 48 rows per work-group (253 groups for 12112 rows)
+constexpr int GRK = 1;                 // rows per 16-lane group
+constexpr int GTH = 768;
+constexpr int GROWS = GTH / 16 * GRK;  // 48 rows per work-group (253 groups for 12112 rows)
 
 // Column-sequential rounding of one chunk of at most GB columns.  A group of 16 lanes
-// holds 2 rows; lane g owns columns g + 16 cc (cc < 8), so the lanes of a group read a
+// holds GRK rows; lane g owns columns g + 16 cc (cc < 8), so the lanes of a group read a
 // row of R as 16 consecutive doubles (no bank conflicts) and load / store rows of Y, D,
 // codes and residuals contiguously.  Column j is rounded by its owner lane j % 16, its
 // residual broadcast to the group with a DPP row broadcast, and every lane folds it into
@@ -403,9 +401,9 @@ __device__ __forceinline__ double row_bcast(double v) {
 }
 
 struct RoundState {
-  double y[2][8], d0[2][8], rr[2][8];
-  uint32_t q[2][2];            // the 8 codes of each row, one byte each
-  double s[2], is[2], z[2];
+  double y[GRK][8], d0[GRK][8], rr[GRK][8];
+  uint32_t q[GRK][2];          // the 8 codes of each row, one byte each
+  double s[GRK], is[GRK], z[GRK];
 };
 
 // column J; rn: row J of R at this lane's columns, irj: 1 / R_JJ
@@ -423,9 +421,9 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
       for (int cc = 0; cc < 8; ++cc) rnext[cc] = Rs[(J + 1) * GB + g + 16 * cc];
       irn = ird[J + 1];
     }
-    double e[2];
+    double e[GRK];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < GRK; ++k) {
       // t = w / scale in code units; the code relative to the zero point is
       // clamp(rne(t), -zero, maxq - zero) (the zero point is an integer)
       const double t = st.y[k][C] * (irj * st.is[k]);
@@ -438,16 +436,15 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
       e[k] = row_bcast<O>(ek);
     }
 #pragma unroll
-    for (int cc = 0; cc < 8; ++cc) {
-      st.y[0][cc] += e[0] * rn[cc];
-      st.y[1][cc] += e[1] * rn[cc];
-    }
+    for (int cc = 0; cc < 8; ++cc)
+#pragma unroll
+      for (int k = 0; k < GRK; ++k) st.y[k][cc] += e[k] * rn[cc];
     // pin the updated values here: otherwise the compiler sinks each update to the column
     // that reads it and keeps every broadcast residual alive
 #pragma unroll
-    for (int cc = 0; cc < 8; cc += 2)
-      asm volatile("" : "+v"(st.y[0][cc]), "+v"(st.y[0][cc + 1]), "+v"(st.y[1][cc]),
-                   "+v"(st.y[1][cc + 1]));
+    for (int k = 0; k < GRK; ++k)
+#pragma unroll
+      for (int cc = 0; cc < 8; cc += 2) asm volatile("" : "+v"(st.y[k][cc]), "+v"(st.y[k][cc + 1]));
     if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, ird, b, g, maxq, rnext, irn);
   }
 }
@@ -485,18 +482,18 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   const int lane = threadIdx.x & 63;
   const int g = lane & 15;                         // position inside the 16-lane group
   const int grp = threadIdx.x >> 4;                // group index in the work-group
-  const int64_t r0 = (int64_t)blockIdx.x * GROWS + grp * 2;
+  const int64_t r0 = (int64_t)blockIdx.x * GROWS + grp * GRK;
   const double lo_b = scal[2], hi_b = scal[3];
 
   RoundState st;
   {
-    double yv[2][8];
-    float dv[2][8];
+    double yv[GRK][8];
+    float dv[GRK][8];
     uint8_t dd[8];
 #pragma unroll
     for (int cc = 0; cc < 8; ++cc) dd[cc] = dead[i1 + min(g + 16 * cc, b - 1)];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < GRK; ++k) {
       const int64_t r = min(r0 + k, rows - 1);
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) {
@@ -506,7 +503,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
       }
     }
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < GRK; ++k) {
       const int64_t r = r0 + k;
       const bool ok = r < rows;
       const int64_t rc = ok ? r : rows - 1;
@@ -531,7 +528,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   round_col<0>(st, Rs, ird, b, g, (double)maxq, rn, ird[0]);
 
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < GRK; ++k) {
     const int64_t r = r0 + k;
     if (r >= rows) continue;
 #pragma unroll
