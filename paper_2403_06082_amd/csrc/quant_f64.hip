@@ -406,20 +406,22 @@ struct RoundState {
   double s[GRK], is[GRK], z[GRK];
 };
 
-// column J; rn: row J of R at this lane's columns, irj: 1 / R_JJ
+// column J; rn: row J of R at this lane's columns, irj: 1 / R_JJ; rn1, irj1: the same for
+// column J + 1 (rows of R are read from LDS two columns ahead)
 template <int J>
 __device__ __forceinline__ void round_col(RoundState& st, const double* __restrict__ Rs,
                                           const double* __restrict__ ird, int b, int g,
-                                          double maxq, const double (&rn)[8], double irj) {
+                                          double maxq, const double (&rn)[8], double irj,
+                                          const double (&rn1)[8], double irj1) {
   if constexpr (J < GB) {
     if (J >= b) return;
     constexpr int O = J & 15, C = J >> 4;
     double rnext[8];
     double irn = 0.0;
-    if constexpr (J + 1 < GB) {   // next row of R and pivot, read while column J is rounded
+    if constexpr (J + 2 < GB) {
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) rnext[cc] = Rs[(J + 1) * GB + g + 16 * cc];
-      irn = ird[J + 1];
+      for (int cc = 0; cc < 8; ++cc) rnext[cc] = Rs[(J + 2) * GB + g + 16 * cc];
+      irn = ird[J + 2];
     }
     double e[GRK];
 #pragma unroll
@@ -445,7 +447,7 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
     for (int k = 0; k < GRK; ++k)
 #pragma unroll
       for (int cc = 0; cc < 8; cc += 2) asm volatile("" : "+v"(st.y[k][cc]), "+v"(st.y[k][cc + 1]));
-    if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, ird, b, g, maxq, rnext, irn);
+    if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, ird, b, g, maxq, rn1, irj1, rnext, irn);
   }
 }
 
@@ -525,7 +527,10 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   double rn[8];
 #pragma unroll
   for (int cc = 0; cc < 8; ++cc) rn[cc] = Rs[g + 16 * cc];
-  round_col<0>(st, Rs, ird, b, g, (double)maxq, rn, ird[0]);
+  double rn1[8];
+#pragma unroll
+  for (int cc = 0; cc < 8; ++cc) rn1[cc] = Rs[GB + g + 16 * cc];
+  round_col<0>(st, Rs, ird, b, g, (double)maxq, rn, ird[0], rn1, ird[1]);
 
 #pragma unroll
   for (int k = 0; k < GRK; ++k) {
