@@ -865,19 +865,40 @@ __global__ __launch_bounds__(256) void k_syrk_reduce(const float* __restrict__ p
   const int tidx = blockIdx.x >> 4;
   const int i0 = tm * BM + sr * 64, j0 = tn * BN + sc * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int r = ty; r < 64; r += 4) {
-    const int i = i0 + r, j = j0 + tx;
-    double sum = 0.0;
-    const int64_t off = (int64_t)tidx * (BM * BN) + (int64_t)(sr * 64 + r) * BN + sc * 64 + tx;
-    for (int s = 0; s < ksplit; ++s) sum += (double)part[(int64_t)s * ntiles * (BM * BN) + off];
-    float v = 0.f;
-    if (i < N && j < N) {
-      const int ii = i <= j ? i : j, jj = i <= j ? j : i;
-      if (accumulate) sum += (double)H[(int64_t)ii * ldh + jj];
-      v = (float)sum;
-      if (i <= j) H[(int64_t)i * ldh + j] = v;
+  // sums: 4 consecutive columns per thread (16-byte loads), the splits in order, four
+  // loads in flight at a time
+  const int c4 = (threadIdx.x & 15) * 4, rq = threadIdx.x >> 4;
+  const int64_t sstride = (int64_t)ntiles * (BM * BN);
+  for (int r = rq; r < 64; r += 16) {
+    const float* p0 = part + (int64_t)tidx * (BM * BN) + (int64_t)(sr * 64 + r) * BN + sc * 64 + c4;
+    double sum[4] = {0.0, 0.0, 0.0, 0.0};
+    int s = 0;
+    for (; s + 4 <= ksplit; s += 4) {
+      float4 v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p0 + (s + q) * sstride);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sum[0] += v[q].x; sum[1] += v[q].y; sum[2] += v[q].z; sum[3] += v[q].w;
+      }
     }
-    tr[r][tx] = v;
+    for (; s < ksplit; ++s) {
+      const float4 v = *reinterpret_cast<const float4*>(p0 + s * sstride);
+      sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+    }
+    const int i = i0 + r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = j0 + c4 + q;
+      float v = 0.f;
+      if (i < N && j < N) {
+        const int ii = i <= j ? i : j, jj = i <= j ? j : i;
+        if (accumulate) sum[q] += (double)H[(int64_t)ii * ldh + jj];
+        v = (float)sum[q];
+        if (i <= j) H[(int64_t)i * ldh + j] = v;
+      }
+      tr[r][c4 + q] = v;
+    }
   }
   __syncthreads();
   // transposed write: element (i0 + c, j0 + r') -> H[j0 + r'][i0 + c]

@@ -65,8 +65,8 @@ __global__ __launch_bounds__(256) void k_moments(const float* __restrict__ D, in
   const double mu = mode ? scal[0] : 0.0;
   double acc = 0.0;
   bool bad = false;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)RED_BLOCKS * 256) {
-    const double x = (double)D[e];
+  auto add = [&](float xf) {
+    const double x = (double)xf;
     if (mode == 0) {
       bad |= !isfinite(x);
       acc += x;
@@ -74,7 +74,17 @@ __global__ __launch_bounds__(256) void k_moments(const float* __restrict__ D, in
       const double d = x - mu;
       acc += d * d;
     }
+  };
+  const int64_t stride = (int64_t)RED_BLOCKS * 256;
+  // 16-byte loads over the aligned bulk, then the remainder one by one
+  const int64_t n4 = ((reinterpret_cast<uintptr_t>(D) & 15) == 0) ? n / 4 : 0;
+  const float4* D4 = reinterpret_cast<const float4*>(D);
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n4; e += stride) {
+    const float4 v = D4[e];
+    add(v.x); add(v.y); add(v.z); add(v.w);
   }
+  for (int64_t e = 4 * n4 + (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += stride)
+    add(D[e]);
   if (bad) flags[2] = 1;                 // D non-finite (flags[1]: H~ non-finite)
   const double s = block_sum<256>(acc, sh);
   if (threadIdx.x == 0) red[blockIdx.x] = s;
