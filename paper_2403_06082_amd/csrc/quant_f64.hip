@@ -350,8 +350,25 @@ __global__ __launch_bounds__(256) void k_clip_grid(const float* __restrict__ D, 
   const int64_t r = blockIdx.x;
   const double lo_b = scal[2], hi_b = scal[3];
   const float* row = D + r * cols;
+  // the row is read once: the first CK of each thread's elements stay in registers for
+  // the second pass (rows up to 256 CK columns), the rest are read again
+  constexpr int CK = 24;
+  float keep[CK];
+#pragma unroll
+  for (int q = 0; q < CK; ++q) {
+    const int64_t j = threadIdx.x + 256 * q;
+    keep[q] = row[j < cols ? j : cols - 1];
+  }
   double mn = 0.0, mx = 0.0;   // min(0, .), max(0, .)
-  for (int64_t j = threadIdx.x; j < cols; j += 256) {
+#pragma unroll
+  for (int q = 0; q < CK; ++q) {
+    if (threadIdx.x + 256 * q < cols) {
+      const double x = fmin(fmax((double)keep[q], lo_b), hi_b);
+      mn = fmin(mn, x);
+      mx = fmax(mx, x);
+    }
+  }
+  for (int64_t j = threadIdx.x + 256 * CK; j < cols; j += 256) {
     const double x = fmin(fmax((double)row[j], lo_b), hi_b);
     mn = fmin(mn, x);
     mx = fmax(mx, x);
@@ -381,7 +398,15 @@ __global__ __launch_bounds__(256) void k_clip_grid(const float* __restrict__ D, 
     zero64[r] = z;
   }
   double* yrow = Y + r * cols;
-  for (int64_t j = threadIdx.x; j < cols; j += 256) {
+#pragma unroll
+  for (int q = 0; q < CK; ++q) {
+    const int64_t j = threadIdx.x + 256 * q;
+    if (j < cols) {
+      const double x = dead[j] ? 0.0 : fmin(fmax((double)keep[q], lo_b), hi_b);
+      yrow[j] = x * rdiag[j];
+    }
+  }
+  for (int64_t j = threadIdx.x + 256 * CK; j < cols; j += 256) {
     const double x = dead[j] ? 0.0 : fmin(fmax((double)row[j], lo_b), hi_b);
     yrow[j] = x * rdiag[j];
   }
