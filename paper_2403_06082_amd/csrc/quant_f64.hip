@@ -437,7 +437,6 @@ __device__ __forceinline__ double row_bcast(double v) {
 
 struct RoundState {
   double y[GRK][8], d0[GRK][8], rr[GRK][8];
-  uint32_t q[GRK][2];          // the 8 codes of each row, one byte each
   double s[GRK], is[GRK], z[GRK];
 };
 
@@ -468,7 +467,6 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
       const double ek = fma(-st.s[k], qz, st.d0[k][C]);
       if (g == O) {
         st.rr[k][C] = ek;
-        st.q[k][C >> 2] |= (uint32_t)(qz + st.z[k]) << (8 * (C & 3));
       }
       e[k] = row_bcast<O>(ek);
     }
@@ -547,7 +545,6 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
       st.s[k] = ok ? scale64[rc] : 1.0;
       st.is[k] = 1.0 / st.s[k];
       st.z[k] = ok ? zero64[rc] : 0.0;
-      st.q[k][0] = st.q[k][1] = 0;
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) {
         const bool in = ok && g + 16 * cc < b;
@@ -575,7 +572,10 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     for (int cc = 0; cc < 8; ++cc) {
       const int c = g + 16 * cc;
       if (c < b) {
-        codes8[r * cols + i1 + c] = (uint8_t)(st.q[k][cc >> 2] >> (8 * (cc & 3)));
+        // the code from the kept residual: e = fma(-s, qz, d0) is exact to within an ulp
+        // of e, so (d0 - e) / s is qz to within 2^-50 and rounds back to it
+        const double qz = rint((st.d0[k][cc] - st.rr[k][cc]) * st.is[k]);
+        codes8[r * cols + i1 + c] = (uint8_t)(qz + st.z[k]);
         res[r * ld_res + res_col0 + c] = st.rr[k][cc];
       }
     }
