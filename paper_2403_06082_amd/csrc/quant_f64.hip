@@ -605,6 +605,7 @@ struct DgemmArgs {
   const double* B; int64_t ldb;
   double* C; int64_t ldc;
   int b_trans, lower_only, tiles_n;
+  int b16;                    // B 16-byte aligned with an even ldb (ring kernel)
 };
 
 // One K step (16) of the DT x DT tile's operands: each of the 256 threads fetches DT / 16
@@ -794,7 +795,10 @@ __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
   // A copy i (i = 0, 1) of this wave: rows 8 (2 wave + i) + lane / 8, k pair c ^ (r & 7)
   // at chunk c = lane % 8.  B copy i: k-row 2 wave + i / 4, columns 32 (i % 4) + 0..31,
   // column n at position n ^ 8 (k-row & 3); offsets clamp at the last column.
-  uint32_t ga[2], gb[2], gl[2];
+  uint32_t ga[2], gb[2];
+  // clamp limit of this wave's first B k-row (the last column of the matrix); the second
+  // k-row's is ldb further
+  const uint32_t gl0 = (uint32_t)((2 * wave * p.ldb + (p.N - 1 - n0)) * 8 + 4 * (lane & 1));
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = 8 * (2 * wave + i) + (lane >> 3), c = lane & 7;
@@ -803,26 +807,38 @@ __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
     const int kr = 2 * wave + i;
     const int nl = (lane >> 1) ^ (8 * (kr & 3));
     gb[i] = (uint32_t)((kr * p.ldb + nl) * 8 + 4 * (lane & 1));
-    gl[i] = (uint32_t)((kr * p.ldb + (p.N - 1 - n0)) * 8 + 4 * (lane & 1));
   }
   const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void*)ring;
   const char* srcA = reinterpret_cast<const char*>(p.A + m0 * p.lda);
   const char* srcB = reinterpret_cast<const char*>(p.B + n0);
   const int64_t stepA = RK * 8, stepB = (int64_t)RK * p.ldb * 8;
+  const bool bx4 = p.b16 && n0 + RT <= p.N;
   auto issue = [&](int s) {
     const uint32_t slot = ring_lds + (uint32_t)((s & 1) * RSLOT);
     const char* a = srcA + s * stepA;
     const char* b = srcB + s * stepB;
 #pragma unroll
     for (int i = 0; i < 2; ++i) lds_copy16(a, ga[i], slot + (2 * wave + i) * 1024);
-    // the clamped offsets are formed here at every step (opaque copies of the bases keep
-    // the compiler from holding all eight in registers)
-    uint32_t b0 = gb[0], b1 = gb[1], l0 = gl[0], l1 = gl[1];
-    asm volatile("" : "+v"(b0), "+v"(b1), "+v"(l0), "+v"(l1));
+    if (bx4) {
+      // interior column tile: whole k-rows of B in 16-byte pieces (column pairs stay
+      // together under the swizzle)
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      lds_copy4(b, min((i < 4 ? b0 : b1) + 256 * (i & 3), i < 4 ? l0 : l1),
-                slot + RA_BYTES + (8 * wave + i) * 256);
+      for (int i = 0; i < 2; ++i) {
+        const int kr = 2 * wave + i;
+        const uint32_t off = (uint32_t)((kr * p.ldb + ((2 * lane) ^ (8 * (kr & 3)))) * 8);
+        lds_copy16(b, off, slot + RA_BYTES + kr * 1024);
+      }
+    } else {
+      // the clamped offsets are formed here at every step (opaque copies of the bases
+      // keep the compiler from holding all eight in registers)
+      uint32_t b0 = gb[0], b1 = gb[1], l0 = gl0;
+      asm volatile("" : "+v"(b0), "+v"(b1), "+v"(l0));
+      const uint32_t l1 = l0 + (uint32_t)(p.ldb * 8);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        lds_copy4(b, min((i < 4 ? b0 : b1) + 256 * (i & 3), i < 4 ? l0 : l1),
+                  slot + RA_BYTES + (8 * wave + i) * 256);
+    }
   };
   auto barrier = [] {
     asm volatile("" ::: "memory");
@@ -1043,6 +1059,7 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
   p.A = A; p.lda = lda; p.B = B; p.ldb = ldb; p.C = C; p.ldc = ldc;
   p.b_trans = (int)b_trans;
   p.lower_only = (int)lower_only;
+  p.b16 = ((reinterpret_cast<uintptr_t>(B) & 15) == 0) && ldb % 2 == 0;
   // row-major operands, K a multiple of 16, 16-byte aligned A rows and 32-bit copy
   // offsets: the LDS-ring kernel
   const bool ring_ok = !b_trans && !lower_only && K > 0 && K % RK == 0 &&
