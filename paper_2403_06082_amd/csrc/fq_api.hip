@@ -34,7 +34,6 @@ hipError_t last_launch_error() { return hipGetLastError(); }
 // a span (large: K_out x 512 x the rest) and the 64 x 64 kernel for those inside a span
 // (K_out x 128 x at most 384); FQ_DGEMM_TILE=64|128 puts every update on the
 // register-staged kernel with that tile, for comparison
-
 static int dgemm_tile_from_env() {
   const char* v = getenv("FQ_DGEMM_TILE");
   const int t = v ? atoi(v) : 0;

@@ -15,7 +15,6 @@
 
 namespace fq {
 
-typedef double doublex4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
