@@ -585,10 +585,28 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
     tloc = bb - split * p.tcount;
     int t = p.tile0 + tloc;
     if (SYM) {
-      int row = 0, cnt = p.tiles_n;
-      while (t >= cnt) { t -= cnt; ++row; --cnt; }
-      tm = row;
-      tn = row + t;
+      // upper tiles in super-blocks of 8 x 8 tiles (diagonal ones triangular), each walked
+      // row by row: the work-groups that run together on an XCD read few distinct
+      // operand blocks
+      const int nsb = (p.tiles_n + 7) / 8;
+      int I = 0, J = 0;
+      for (;;) {
+        const int nr = min(8, p.tiles_n - 8 * I), nc = min(8, p.tiles_n - 8 * J);
+        const int cnt = (I == J) ? nr * (nr + 1) / 2 : nr * nc;
+        if (t < cnt || (I == nsb - 1 && J == nsb - 1)) break;
+        t -= cnt;
+        if (++J == nsb) { ++I; J = I; }
+      }
+      if (I == J) {
+        int r = 0, cnt = min(8, p.tiles_n - 8 * I);
+        while (t >= cnt) { t -= cnt; ++r; --cnt; }
+        tm = 8 * I + r;
+        tn = tm + t;
+      } else {
+        const int nc = min(8, p.tiles_n - 8 * J);
+        tm = 8 * I + t / nc;
+        tn = 8 * J + t % nc;
+      }
     } else {
       const int G = 8;
       const int g = t / (G * p.tiles_n);
