@@ -145,7 +145,12 @@ def _quantize(torch, fq, D, Ht, block, **kw):
 
 @pytest.mark.parametrize("K_out,d_in,k_in,block", [(70, 64, 18, 128), (300, 136, 37, 7),
                                                    (130, 200, 55, 128), (200, 256, 70, 200),
-                                                   (64, 96, 25, 1)])
+                                                   (64, 96, 25, 1),
+                                                   # K_in = 1100: two updates beyond a
+                                                   # 512-column span on the LDS-ring
+                                                   # kernel (interior and clamped edge
+                                                   # column tiles, ragged rows)
+                                                   (300, 1024, 275, 128)])
 def test_quantize_teacher_forced(K_out, d_in, k_in, block):
     torch = need_gpu()
     fq = _fq()
@@ -157,6 +162,22 @@ def test_quantize_teacher_forced(K_out, d_in, k_in, block):
     assert ties <= 2
     # the packed layout carries nothing beyond K_in
     assert cg.shape == D.shape
+
+
+def test_quantize_odd_row_length():
+    """K_in = 1101: the rows of R have an odd length, so the LDS-ring kernel copies B a
+    dword per lane in every column tile."""
+    torch = need_gpu()
+    fq = _fq()
+    rng = np.random.default_rng(1101)
+    A = rng.standard_normal((600, 1101))
+    A[:, 3] *= 20.0
+    Ht = (A.T @ A).astype(np.float32)
+    Ht = np.triu(Ht) + np.triu(Ht, 1).T            # exactly symmetric
+    D = (rng.standard_normal((260, 1101)) * 0.02 + 0.001).astype(np.float32)
+    cg, sg, zg = _quantize(torch, fq, D, Ht, 128)
+    r = replay_rows(D, Ht, cg, block=128)
+    assert check_codes(r, cg, sg, zg) <= 2
 
 
 def test_quantize_identity_hessian_is_rtn():
