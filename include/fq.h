@@ -155,6 +155,26 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
 size_t fq_frame_synthesis_workspace_bytes(int64_t K_out, int64_t K_in, int64_t d_out,
                                           int64_t d_in);
 
+/*
+ * Layer outputs straight from the stored codes and the frames, without forming Theta^
+ * (appendix "Computational Complexity during Inference"):
+ *   Y = X Theta^T = ((X P_in) (codes - zero)^T diag(scale)) P_out^T
+ *   X      device, n_tokens x d_in, element type xt (FQ_F32 / FQ_F16 / FQ_BF16), row
+ *          stride ldx >= d_in (elements).
+ *   codes/scale/zero  as produced by fq_quantize_frames (K_out x K_in codes).
+ *   P_out  device fp32 d_out x K_out;  P_in device fp32 d_in x K_in.
+ *   Y      device fp32, n_tokens x d_out, row-major.
+ * Meant for decode and small batches: every frame and the codes are streamed once per
+ * block of 8 tokens (for large token counts form Theta^ with fq_frame_synthesis and use a
+ * GEMM).  fp32 arithmetic with fp32 accumulation.
+ */
+fq_status fq_frame_apply(void* stream, const void* X, int xt, int64_t n_tokens, int64_t ldx,
+                         int64_t d_in, const uint32_t* codes, const float* scale,
+                         const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
+                         int64_t d_out, const float* P_in, float* Y, void* ws,
+                         size_t ws_bytes);
+size_t fq_frame_apply_workspace_bytes(int64_t d_in, int64_t K_out, int64_t K_in);
+
 /* Status text and the calling thread's last error message (never NULL). */
 const char* fq_status_string(int status);
 const char* fq_last_error(void);

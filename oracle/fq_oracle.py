@@ -266,6 +266,14 @@ def synthesis(codes, scale, zero, P_out, P_in):
     return np.asarray(P_out, dtype=np.float64) @ Dhat @ np.asarray(P_in, dtype=np.float64).T
 
 
+def frame_apply(X, codes, scale, zero, P_out, P_in):
+    """Layer outputs of the quantized layer, Y = X Theta^T with Theta^ = P_l D^ P_prev^T
+    (appendix "Computational Complexity during Inference": the output is produced from the
+    stored codes and the two frames).  X: tokens x d_in; Y: tokens x d_out."""
+    Wh = synthesis(codes, scale, zero, P_out, P_in)
+    return np.asarray(X, dtype=np.float64) @ Wh.T
+
+
 # --------------------------------------------------------------------------- pipeline
 def quantize_frames(D, Ht, bits=2, block=128, damp=0.01, clip_sigmas=2.0,
                     forced_codes=None, tie_eps=TIE_EPS):

@@ -6,7 +6,7 @@ package holds the sources, the build script and a thin ctypes binding.
 from .fq import (  # noqa: F401
     FQ_F32, FQ_F16, FQ_BF16, FQError, lib,
     fq_hessian_accumulate, fq_frame_analysis, fq_quantize_frames, fq_frame_synthesis,
-    fq_quantize_prepare, fq_quantize_apply,
+    fq_quantize_prepare, fq_quantize_apply, fq_frame_apply, fq_frame_apply_workspace_bytes,
     fq_hessian_workspace_bytes, fq_frame_analysis_workspace_bytes,
     fq_quantize_frames_workspace_bytes, fq_frame_synthesis_workspace_bytes,
     fq_profile_enable, fq_profile_reset, fq_profile_query,

@@ -598,6 +598,43 @@ fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t
 }
 
 // ================================================================ S4: synthesis
+size_t fq_frame_apply_workspace_bytes(int64_t d_in, int64_t K_out, int64_t K_in) {
+  if (!dim_ok(d_in) || !dim_ok(K_out) || !dim_ok(K_in)) return 0;
+  return apply_scratch_floats(d_in, K_out, K_in, nullptr, nullptr) * sizeof(float) + 256;
+}
+
+fq_status fq_frame_apply(void* stream, const void* X, int xt, int64_t n_tokens, int64_t ldx,
+                         int64_t d_in, const uint32_t* codes, const float* scale,
+                         const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
+                         int64_t d_out, const float* P_in, float* Y, void* ws,
+                         size_t ws_bytes) {
+  if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (!dim_ok(n_tokens) || !dim_ok(d_in) || !dim_ok(K_out) || !dim_ok(K_in) || !dim_ok(d_out))
+    return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
+  if (K_out < d_out || K_in < d_in)
+    return fail(FQ_ERR_INVALID_ARG, "a frame needs K >= d (K_out >= d_out, K_in >= d_in)");
+  if (ldx < d_in) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d_in");
+  if (n_tokens == 0 || d_out == 0) return FQ_OK;
+  if (!Y) return fail(FQ_ERR_INVALID_ARG, "NULL Y");
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e;
+  if (d_in == 0 || K_out == 0 || K_in == 0) {
+    e = fill_zero_f32(Y, (int)n_tokens, (int)d_out, d_out, s);
+    return e == hipSuccess ? FQ_OK : hip_fail(e, "zero Y");
+  }
+  if (!X || !codes || !scale || !zero || !P_out || !P_in) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  const size_t need = fq_frame_apply_workspace_bytes(d_in, K_out, K_in);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_apply_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  float* base = (float*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+  ApplyScratch w;
+  apply_scratch_floats(d_in, K_out, K_in, &w, base);
+  if ((e = frame_apply(X, xt, n_tokens, ldx, d_in, codes, scale, zero, K_out, K_in, P_out, d_out,
+                       P_in, Y, w, s)) != hipSuccess)
+    return hip_fail(e, "frame apply");
+  return FQ_OK;
+}
+
 size_t fq_frame_synthesis_workspace_bytes(int64_t K_out, int64_t K_in, int64_t d_out,
                                           int64_t d_in) {
   if (!dim_ok(K_out) || !dim_ok(K_in) || !dim_ok(d_out) || !dim_ok(d_in)) return 0;

@@ -71,6 +71,23 @@ hipError_t split_bf16_pad(const void* in, int in_type, int64_t ld_in, int rows, 
                           int rows_out, hipStream_t s);
 hipError_t fill_zero_f32(float* p, int rows, int cols, int64_t ld, hipStream_t s);
 
+// ---------------------------------------------------------------- layer outputs from codes
+// Y = X Theta^T from the packed codes and the frames, tokens in blocks of APPLY_NT.
+constexpr int APPLY_NT = 8;
+struct ApplyScratch {
+  float* part;   // split-K partials of U = X P_in
+  float* U;      // APPLY_NT x pad16(K_in)
+  float* V;      // APPLY_NT x K_out
+};
+// floats of scratch (and, with base, the carve-up); base 256-byte aligned
+size_t apply_scratch_floats(int64_t d_in, int64_t K_out, int64_t K_in, ApplyScratch* w,
+                            float* base);
+// X: n x d_in (row stride ldx, element type xt: 0 f32, 1 f16, 2 bf16); Y: n x d_out fp32
+hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_in,
+                       const uint32_t* codes, const float* scale, const float* zero,
+                       int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,
+                       const float* P_in, float* Y, const ApplyScratch& w, hipStream_t s);
+
 // ---------------------------------------------------------------- fp64 path
 struct QuantScratch {
   double* Y;          // K_out x K_in working matrix (scaled pre-rounding values)

@@ -1,0 +1,345 @@
+// Layer outputs straight from the stored codes and the two frames (appendix
+// "Computational Complexity during Inference"): Y = X Theta^T with
+// Theta^ = P_out diag(scale) (q - zero) P_in^T, taken in the order
+//   U = X P_in            (tokens x K_in)
+//   V = U (q - zero)^T S  (tokens x K_out; the 2-bit codes decoded on the fly)
+//   Y = V P_out^T         (tokens x d_out)
+// for small token counts (decode, small batches), where every step streams its operand
+// from HBM once: P_in (d_in x K_in fp32), the packed codes, P_out (d_out x K_out fp32).
+// Tokens go through in blocks of at most 8; all arithmetic is fp32 with fp32
+// accumulation (the split-K partials of U are summed in fp64).
+#include "fq_internal.h"
+
+#include <algorithm>
+
+namespace fq {
+namespace {
+
+constexpr int AT = 256;        // threads per work-group in every kernel here
+constexpr int UCH = 4096;      // columns of U staged in LDS at a time by the code kernel
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T v);
+template <>
+__device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <>
+__device__ __forceinline__ float to_f32<uint16_t>(uint16_t v) {   // bf16
+  return __uint_as_float((uint32_t)v << 16);
+}
+template <>
+__device__ __forceinline__ float to_f32<_Float16>(_Float16 v) { return (float)v; }
+
+// ---- step 1: part[s][t][j] = sum over k in split s of X[t][k] P_in[k][j]
+// grid (ceil(K_in / (4 AT)), ksplit); a thread owns 4 consecutive columns.
+template <typename XT, int NT, bool VEC>
+__global__ __launch_bounds__(AT) void k_apply_in(const XT* __restrict__ X, int64_t ldx, int nt,
+                                                 int64_t d_in, const float* __restrict__ P,
+                                                 int64_t K_in, int kper,
+                                                 float* __restrict__ part) {
+  __shared__ float xs[NT][256];
+  const int s = blockIdx.y;
+  const int64_t k0 = (int64_t)s * kper;
+  const int kn = (int)min((int64_t)kper, d_in - k0);
+  for (int e = threadIdx.x; e < NT * kper; e += AT) {
+    const int t = e / kper, k = e % kper;
+    xs[t][k] = (t < nt && k < kn) ? to_f32<XT>(X[t * ldx + k0 + k]) : 0.f;
+  }
+  __syncthreads();
+  const int64_t j = ((int64_t)blockIdx.x * AT + threadIdx.x) * 4;
+  if (j >= K_in) return;
+  float acc[NT][4];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[t][q] = 0.f;
+  const float* p = P + k0 * K_in + j;
+  for (int k = 0; k < kn; ++k, p += K_in) {
+    float v[4];
+    if (VEC) {
+      const float4 w = *reinterpret_cast<const float4*>(p);
+      v[0] = w.x; v[1] = w.y; v[2] = w.z; v[3] = w.w;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = (j + q < K_in) ? p[q] : 0.f;
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float x = xs[t][k];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[t][q] = fmaf(x, v[q], acc[t][q]);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (j + q < K_in) part[((int64_t)s * NT + t) * K_in + j + q] = acc[t][q];
+}
+
+// U[t][j] = sum over the splits (fp64), zero for t >= nt; U has ldu >= K_in columns,
+// columns [K_in, ldu) zero.
+__global__ __launch_bounds__(AT) void k_apply_in_reduce(const float* __restrict__ part, int nt_blk,
+                                                        int nt, int ksplit, int64_t K_in,
+                                                        int64_t ldu, float* __restrict__ U) {
+  const int64_t total = (int64_t)nt_blk * ldu;
+  for (int64_t e = (int64_t)blockIdx.x * AT + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * AT) {
+    const int t = (int)(e / ldu);
+    const int64_t j = e - t * ldu;
+    double acc = 0.0;
+    if (t < nt && j < K_in)
+      for (int s = 0; s < ksplit; ++s) acc += part[((int64_t)s * nt_blk + t) * K_in + j];
+    U[e] = (float)acc;
+  }
+}
+
+// ---- step 2: V[t][i] = scale_i sum_j U[t][j] (q_ij - zero_i)
+// A work-group owns 16 rows (4 per wave); U goes through LDS UCH columns at a time; a
+// lane takes code words w = lane, lane + 64, ... of its wave's 4 rows, decodes each word
+// once (q - zero, small integers, exact) and applies it to every token.
+template <int NT>
+__global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U, int64_t ldu,
+                                                    const uint32_t* __restrict__ codes,
+                                                    int64_t K_out, int64_t nwords,
+                                                    const float* __restrict__ scale,
+                                                    const float* __restrict__ zero,
+                                                    float* __restrict__ V) {
+  __shared__ __attribute__((aligned(16))) float us[NT][UCH];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row0 = (int64_t)blockIdx.x * 16 + wave * 4;
+  float acc[4][NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r][t] = 0.f;
+  const uint32_t* crow[4];
+  float zr[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t i = min(row0 + r, K_out - 1);
+    crow[r] = codes + i * nwords;
+    zr[r] = zero[i];
+  }
+  for (int64_t c0 = 0; c0 < ldu; c0 += UCH) {
+    const int cn = (int)min((int64_t)UCH, ldu - c0);        // multiple of 16
+    __syncthreads();
+    for (int e = threadIdx.x * 4; e < NT * UCH; e += AT * 4) {
+      const int t = e / UCH, c = e % UCH;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (c < cn) v = *reinterpret_cast<const float4*>(U + t * ldu + c0 + c);
+      *reinterpret_cast<float4*>(&us[t][c]) = v;
+    }
+    __syncthreads();
+    const int64_t w0 = c0 / 16;
+    for (int w = lane; w < cn / 16; w += 64) {
+      float q[4][16];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t word = (w0 + w < nwords) ? crow[r][w0 + w] : 0u;
+#pragma unroll
+        for (int b = 0; b < 16; ++b) q[r][b] = (float)((word >> (2 * b)) & 3u) - zr[r];
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        float u[16];
+#pragma unroll
+        for (int b = 0; b < 16; b += 4) {
+          const float4 v = *reinterpret_cast<const float4*>(&us[t][16 * w + b]);
+          u[b] = v.x; u[b + 1] = v.y; u[b + 2] = v.z; u[b + 3] = v.w;
+        }
+#pragma unroll
+        for (int b = 0; b < 16; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[r][t] = fmaf(u[b], q[r][b], acc[r][t]);
+      }
+    }
+  }
+  // wave sums
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r][t] += __shfl_xor(acc[r][t], o);
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t i = row0 + r;
+      if (i < K_out) {
+        const float s = scale[i];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) V[t * K_out + i] = s * acc[r][t];
+      }
+    }
+  }
+}
+
+// ---- step 3: Y[t][o] = sum_i V[t][i] P_out[o][i]
+// A work-group owns 4 output rows; a thread owns 4 consecutive columns of every 4 AT-wide
+// chunk of P_out's rows.
+template <int NT, bool VEC>
+__global__ __launch_bounds__(AT) void k_apply_out(const float* __restrict__ V, int nt,
+                                                  const float* __restrict__ P, int64_t K_out,
+                                                  int64_t d_out, float* __restrict__ Y,
+                                                  int64_t ldy) {
+  __shared__ float red[AT / 64][4][NT];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t o0 = (int64_t)blockIdx.x * 4;
+  float acc[4][NT];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[r][t] = 0.f;
+  const float* prow[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) prow[r] = P + min(o0 + r, d_out - 1) * K_out;
+  for (int64_t i = (int64_t)threadIdx.x * 4; i < K_out; i += AT * 4) {
+    float v[NT][4];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      if (VEC) {
+        const float4 w = *reinterpret_cast<const float4*>(V + t * K_out + i);
+        v[t][0] = w.x; v[t][1] = w.y; v[t][2] = w.z; v[t][3] = w.w;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[t][q] = (i + q < K_out) ? V[t * K_out + i + q] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float p[4];
+      if (VEC) {
+        const float4 w = *reinterpret_cast<const float4*>(prow[r] + i);
+        p[0] = w.x; p[1] = w.y; p[2] = w.z; p[3] = w.w;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) p[q] = (i + q < K_out) ? prow[r][i + q] : 0.f;
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[r][t] = fmaf(v[t][q], p[q], acc[r][t]);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[r][t] += __shfl_xor(acc[r][t], o);
+  if (lane == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) red[wave][r][t] = acc[r][t];
+  __syncthreads();
+  if (threadIdx.x < 4 * NT) {
+    const int r = threadIdx.x / NT, t = threadIdx.x % NT;
+    const int64_t o = o0 + r;
+    if (o < d_out && t < nt) {
+      float sum = 0.f;
+#pragma unroll
+      for (int w = 0; w < AT / 64; ++w) sum += red[w][r][t];
+      Y[t * ldy + o] = sum;
+    }
+  }
+}
+
+int64_t rup16(int64_t x) { return (x + 15) / 16 * 16; }
+
+// splits of d_in for step 1: about 64 (enough work-groups to fill the CUs), at least 32
+// rows each, at most 256 rows each (the LDS copy of the tokens' X slice)
+int apply_ksplit(int64_t d_in) {
+  int64_t ks = 64;
+  while (ks > 1 && d_in / ks < 32) ks >>= 1;
+  if ((d_in + ks - 1) / ks > 256) ks = (d_in + 255) / 256;
+  return (int)ks;
+}
+
+template <int NT>
+hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
+                       const uint32_t* codes, const float* scale, const float* zero,
+                       int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,
+                       const float* P_in, float* Y, const ApplyScratch& w, hipStream_t s) {
+  const int ks = apply_ksplit(d_in);
+  const int kper = (int)((d_in + ks - 1) / ks);
+  const int ks_eff = (int)((d_in + kper - 1) / kper);
+  const int64_t ldu = rup16(K_in);
+  const bool vin = (K_in % 4 == 0) && ((reinterpret_cast<uintptr_t>(P_in) & 15) == 0);
+  const bool vout = (K_out % 4 == 0) && ((reinterpret_cast<uintptr_t>(P_out) & 15) == 0);
+  const dim3 gin((unsigned)((K_in + 4 * AT - 1) / (4 * AT)), (unsigned)ks_eff);
+  prof_begin(s, "apply_in");
+#define FQ_APPLY_IN(XT)                                                                          \
+  if (vin) hipLaunchKernelGGL((k_apply_in<XT, NT, true>), gin, dim3(AT), 0, s,                    \
+                              (const XT*)X, ldx, nt, d_in, P_in, K_in, kper, w.part);            \
+  else hipLaunchKernelGGL((k_apply_in<XT, NT, false>), gin, dim3(AT), 0, s,                       \
+                          (const XT*)X, ldx, nt, d_in, P_in, K_in, kper, w.part);
+  if (xt == 0) { FQ_APPLY_IN(float) }
+  else if (xt == 1) { FQ_APPLY_IN(_Float16) }
+  else { FQ_APPLY_IN(uint16_t) }
+#undef FQ_APPLY_IN
+  const int64_t tot = (int64_t)NT * ldu;
+  hipLaunchKernelGGL(k_apply_in_reduce, dim3((unsigned)std::min<int64_t>((tot + AT - 1) / AT, 4096)),
+                     dim3(AT), 0, s, w.part, NT, nt, ks_eff, K_in, ldu, w.U);
+  prof_end(s);
+  prof_begin(s, "apply_codes");
+  hipLaunchKernelGGL(k_apply_codes<NT>, dim3((unsigned)((K_out + 15) / 16)), dim3(AT), 0, s,
+                     w.U, ldu, codes, K_out, (K_in + 15) / 16, scale, zero, w.V);
+  prof_end(s);
+  prof_begin(s, "apply_out");
+  if (vout)
+    hipLaunchKernelGGL((k_apply_out<NT, true>), dim3((unsigned)((d_out + 3) / 4)), dim3(AT), 0, s,
+                       w.V, nt, P_out, K_out, d_out, Y, d_out);
+  else
+    hipLaunchKernelGGL((k_apply_out<NT, false>), dim3((unsigned)((d_out + 3) / 4)), dim3(AT), 0,
+                       s, w.V, nt, P_out, K_out, d_out, Y, d_out);
+  prof_end(s);
+  return last_launch_error();
+}
+
+}  // namespace
+
+size_t apply_scratch_floats(int64_t d_in, int64_t K_out, int64_t K_in, ApplyScratch* w,
+                            float* base) {
+  const int ks = apply_ksplit(d_in);
+  const int64_t kper = (d_in + ks - 1) / ks;
+  const int64_t ks_eff = (d_in + kper - 1) / kper;
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    float* p = base ? base + off : nullptr;
+    off += (n + 63) / 64 * 64;
+    return p;
+  };
+  ApplyScratch l{};
+  l.part = take((size_t)ks_eff * APPLY_NT * K_in);
+  l.U = take((size_t)APPLY_NT * rup16(K_in));
+  l.V = take((size_t)APPLY_NT * K_out);
+  if (w) *w = l;
+  return off;
+}
+
+hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_in,
+                       const uint32_t* codes, const float* scale, const float* zero,
+                       int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,
+                       const float* P_in, float* Y, const ApplyScratch& w, hipStream_t s) {
+  const int esz = xt == 0 ? 4 : 2;
+  for (int64_t t0 = 0; t0 < n; t0 += APPLY_NT) {
+    const int nt = (int)std::min<int64_t>(APPLY_NT, n - t0);
+    const void* Xb = static_cast<const char*>(X) + t0 * ldx * esz;
+    float* Yb = Y + t0 * d_out;
+    hipError_t e;
+    if (nt == 1)
+      e = apply_block<1>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+    else if (nt == 2)
+      e = apply_block<2>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+    else if (nt <= 4)
+      e = apply_block<4>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+    else
+      e = apply_block<8>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace fq

@@ -35,6 +35,9 @@ SIGNATURES = {
     "fq_frame_synthesis": (_i, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp,
                                 _sz]),
     "fq_frame_synthesis_workspace_bytes": (_sz, [_i64, _i64, _i64, _i64]),
+    "fq_frame_apply": (_i, [_vp, _vp, _i, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _i64,
+                            _vp, _vp, _vp, _sz]),
+    "fq_frame_apply_workspace_bytes": (_sz, [_i64, _i64, _i64]),
     "fq_status_string": (ctypes.c_char_p, [_i]),
     "fq_last_error": (ctypes.c_char_p, []),
     "fq_profile_enable": (None, [_i]),
@@ -243,3 +246,34 @@ def fq_profile_query(prefix: str = ""):
     if lib().fq_profile_query(prefix.encode(), ctypes.byref(n), ctypes.byref(ms)) != 0:
         raise FQError(6, "event query failed")
     return n.value, ms.value
+
+
+def fq_frame_apply_workspace_bytes(d_in, K_out, K_in) -> int:
+    return lib().fq_frame_apply_workspace_bytes(d_in, K_out, K_in)
+
+
+def fq_frame_apply(X, codes, scale, zero, P_out, P_in, Y=None, ws=None, stream=None):
+    """Y = X Theta^T from the codes and the frames (small token counts)."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be 2-D with unit column stride")
+    n, d_in = X.shape
+    if not X.is_cuda:
+        raise ValueError("X must be a device tensor")
+    K_out, K_in = P_out.shape[1], P_in.shape[1]
+    d_out = P_out.shape[0]
+    if P_in.shape[0] != d_in:
+        raise ValueError("P_in must have d_in rows")
+    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    _dev(P_out, "P_out", torch.float32)
+    _dev(P_in, "P_in", torch.float32)
+    if Y is None:
+        Y = torch.empty((n, d_out), dtype=torch.float32, device=X.device)
+    _dev(Y, "Y", torch.float32, (n, d_out))
+    ws, wp, wb = _ws(fq_frame_apply_workspace_bytes(d_in, K_out, K_in), ws, X.device)
+    _check(lib().fq_frame_apply(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), d_in,
+                                _ptr(codes), _ptr(scale), _ptr(zero), K_out, K_in, _ptr(P_out),
+                                d_out, _ptr(P_in), _ptr(Y), wp, wb))
+    return Y

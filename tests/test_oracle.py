@@ -249,6 +249,36 @@ def test_synthesis_inverts_analysis_at_r1():
     np.testing.assert_allclose(D2, O.dequant(codes, scale, zero), atol=1e-12)
 
 
+def test_frame_apply_identity_frames_brute_force():
+    """With identity frames the layer output is the plain quantized matmul, written out
+    entry by entry here; with random frames it matches the product taken in the other
+    association and is linear in X."""
+    rng = np.random.default_rng(31)
+    n, K_out, K_in = 3, 5, 7
+    codes = rng.integers(0, 4, size=(K_out, K_in))
+    scale = rng.uniform(0.01, 0.2, K_out)
+    zero = rng.integers(0, 4, K_out).astype(np.float64)
+    X = rng.standard_normal((n, K_in))
+    Y = O.frame_apply(X, codes, scale, zero, np.eye(K_out), np.eye(K_in))
+    for t in range(n):
+        for o in range(K_out):
+            acc = 0.0
+            for j in range(K_in):
+                acc += X[t, j] * scale[o] * (codes[o, j] - zero[o])
+            assert abs(Y[t, o] - acc) < 1e-12
+    d_out, d_in = 4, 6
+    P_out = rng.standard_normal((d_out, K_out))
+    P_in = rng.standard_normal((d_in, K_in))
+    X = rng.standard_normal((n, d_in))
+    Y = O.frame_apply(X, codes, scale, zero, P_out, P_in)
+    Dh = scale[:, None] * (codes - zero[:, None])
+    np.testing.assert_allclose(Y, ((X @ P_in) @ Dh.T) @ P_out.T, rtol=1e-12, atol=1e-12)
+    X2 = rng.standard_normal((n, d_in))
+    np.testing.assert_allclose(O.frame_apply(2 * X - X2, codes, scale, zero, P_out, P_in),
+                               2 * Y - O.frame_apply(X2, codes, scale, zero, P_out, P_in),
+                               rtol=1e-12, atol=1e-12)
+
+
 def test_output_loss_bound_and_pipeline():
     """||(Theta - Theta^) X^T|| <= ||(D - D^) C|| for the unclipped D; equality at
     r_out = 1 (P_l has unit singular values)."""
