@@ -14,7 +14,9 @@ Prints one JSON line.  value = quantized weights per second (d_out * d_in / step
 "roofline" is the dominant kernel's algorithmic throughput against its MFMA peak, timed
 with HIP events on its own launch stream inside the timed region; "kernels" lists every
 kernel group the same way.  "cpu_baseline" is the float64 CPU oracle timed on a bounded
-sample of the same workload on this host, extrapolated stage by stage.
+sample of the same workload on this host, extrapolated stage by stage.  "inference" times
+the quantized layer's outputs for 1 and 8 tokens (fq_frame_apply on the pass's own codes)
+against HBM bandwidth, with its own roofline and CPU-oracle baseline.
 """
 from __future__ import annotations
 
@@ -169,13 +171,117 @@ def cpu_baseline(wl, li, host, budget_rows=1024, sample_tokens=8192):
             "stage_seconds": {k: round(v, 3) for k, v in t.items()}}
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed byte-counter profile, or None when
+def apply_bytes(nt, d_out, d_in, K_out, K_in, x_bytes):
+    """Algorithmic HBM bytes of one fq_frame_apply call per kernel group: every operand
+    read once per block of up to 8 tokens (P_in, codes + scale + zero, P_out), X read
+    and Y written once."""
+    blocks = -(-nt // 8)
+    nwords = -(-K_in // 16)
+    return {"apply_in": blocks * d_in * K_in * 4 + nt * d_in * x_bytes,
+            "apply_codes": blocks * (K_out * nwords * 4 + 2 * K_out * 4),
+            "apply_out": blocks * d_out * K_out * 4 + nt * d_out * 4}
+
+
+def inference_bench(fq, torch, dev, bufs, L, K_out, K_in, tokens=(1, 8), iters=200):
+    """Layer outputs Y = X Theta^T from the pass's own codes and the frames (fq_frame_apply),
+    for 1 and 8 tokens (rows of the calibration activations), timed with HIP events on the
+    launch stream; per-kernel times from the library's kernel timers in a second run."""
+    stream = torch.cuda.current_stream()
+    ws = torch.empty(fq.fq_frame_apply_workspace_bytes(L.d_in, K_out, K_in), dtype=torch.uint8,
+                     device="cuda")
+    x_bytes = dev["X"].element_size()
+    rows = []
+    for nt in tokens:
+        X = dev["X"][:nt]
+        Y = torch.empty((nt, L.d_out), dtype=torch.float32, device="cuda")
+
+        def call():
+            fq.fq_frame_apply(X, bufs.codes, bufs.scale, bufs.zero, dev["P_out"], dev["P_in"],
+                              Y=Y, ws=ws, stream=stream)
+
+        for _ in range(10):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / iters
+        fq.fq_profile_reset()
+        fq.fq_profile_enable(True)
+        for _ in range(iters):
+            call()
+        torch.cuda.synchronize()
+        fq.fq_profile_enable(False)
+        nbytes = apply_bytes(nt, L.d_out, L.d_in, K_out, K_in, x_bytes)
+        kern = {}
+        for name, b in nbytes.items():
+            cnt, tot = fq.fq_profile_query(name)
+            k_us = tot * 1e3 / iters
+            kern[name] = {"launches_per_call": cnt / iters, "us_per_call": round(k_us, 2),
+                          "algorithmic_bytes": b, "GB/s": round(b / k_us / 1e3, 1)}
+        fq.fq_profile_reset()
+        total = sum(nbytes.values())
+        rows.append({"tokens": nt, "us_per_call": round(us, 2),
+                     "tokens_per_s": round(nt / (us / 1e6), 1),
+                     "algorithmic_bytes": total, "GB/s": round(total / us / 1e3, 1),
+                     "frac_of_hbm_peak": round(total / us / 1e3 / PEAK["hbm"], 4),
+                     "kernels": kern})
+        print(f"[bench] frame_apply {nt} token(s): {us:.1f} us/call", file=sys.stderr, flush=True)
+    k1 = rows[0]["kernels"]["apply_out"]
+    roof = {"bound": "hbm", "kernel": "apply_out", "tokens": rows[0]["tokens"],
+            "achieved": k1["GB/s"], "peak": PEAK["hbm"], "unit": "GB/s",
+            "frac": round(k1["GB/s"] / PEAK["hbm"], 4), "traffic": measured_traffic("apply_out", "traffic_apply_out.json"),
+            "avg_launch_us": k1["us_per_call"], "algorithmic_per_launch": k1["algorithmic_bytes"]}
+    return {"op": "fq_frame_apply: Y = X Theta^T straight from the 2-bit codes and the two "
+                  "fp32 frames (Theta^ never formed): U = X P_in, V = U (q - zero)^T diag(scale), "
+                  "Y = V P_out^T",
+            "workload": f"the benchmark layer ({L.d_out}x{L.d_in}, K {K_out}x{K_in}), codes of "
+                        f"the pass just timed, X = first rows of its bf16 activations",
+            "dtype": "fp32 (fp32 accumulation; split-K partials summed in fp64)",
+            "per_tokens": rows, "roofline": roof}
+
+
+def cpu_inference_baseline(host, codes, scale, zero, wl, li, sample_rows=512):
+    """The oracle's layer output for one token on `sample_rows` sampled output channels;
+    its row-proportional part is scaled to all channels, the dequantization counted once."""
+    import oracle as O
+    from fq_inputs import gen
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    L = wl.layers[li]
+    K_in = host["P_in"].shape[1]
+    q = O.unpack2(codes.view(np.uint32), K_in)
+    sc, z = scale.astype(np.float64), zero.astype(np.float64)
+    X1 = gen.storage_to_f32(host["X"][:1], wl.x_dtype).astype(np.float64)
+    rows = np.sort(np.random.default_rng(1).choice(L.d_out, size=min(sample_rows, L.d_out),
+                                                    replace=False))
+    s0 = time.perf_counter()
+    O.dequant(q, sc, z)
+    t_dq = time.perf_counter() - s0
+    s0 = time.perf_counter()
+    O.frame_apply(X1, q, sc, z, host["P_out"][rows], host["P_in"])
+    t_rows = time.perf_counter() - s0
+    total = t_dq + (t_rows - t_dq) * (L.d_out / len(rows))
+    return {"value": round(1.0 / total, 4), "unit": "tokens/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"float64 numpy oracle frame_apply for 1 token on {len(rows)} of {L.d_out} "
+                       f"output channels ({t_rows:.2f} s), the part beyond the dequantization "
+                       f"({t_dq:.2f} s, counted once) scaled to all channels: {total:.1f} s")}
+
+
+def measured_traffic(kernel, fname="traffic.json"):
+    """HBM bytes per launch of `kernel` from a committed byte-counter profile, or None when
     there is none or the kernel source changed since it was taken."""
     import hashlib
     here = os.path.dirname(os.path.abspath(__file__))
     try:
-        with open(os.path.join(here, "profiles", "traffic.json")) as f:
+        with open(os.path.join(here, "profiles", fname)) as f:
             t = json.load(f)
         if t.get("kernel") != kernel:
             return None
@@ -353,9 +459,14 @@ def main():
         "kernels": kernels,
         "kernel_ms_total_per_step": round(tot_all / args.steps, 3),
     }
+    inf = inference_bench(fq, torch, dev, bufs, L, K_out, K_in)
+    out["inference"] = inf
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
+        inf["cpu_baseline"] = cpu_inference_baseline(host, bufs.codes.cpu().numpy(),
+                                                     bufs.scale.cpu().numpy(),
+                                                     bufs.zero.cpu().numpy(), wl, li)
     print(json.dumps(out), flush=True)
 
 

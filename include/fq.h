@@ -157,16 +157,23 @@ size_t fq_frame_synthesis_workspace_bytes(int64_t K_out, int64_t K_in, int64_t d
 
 /*
  * Layer outputs straight from the stored codes and the frames, without forming Theta^
- * (appendix "Computational Complexity during Inference"):
+ * (Sec. 3 "Inference Procedure": the inputs go to their frame representation through the
+ * analysis operator P_prev^T, through the quantized D^, and back through the synthesis
+ * operator P_l; Theta^ as in the appendix "Computational Complexity during Inference"):
  *   Y = X Theta^T = ((X P_in) (codes - zero)^T diag(scale)) P_out^T
  *   X      device, n_tokens x d_in, element type xt (FQ_F32 / FQ_F16 / FQ_BF16), row
  *          stride ldx >= d_in (elements).
  *   codes/scale/zero  as produced by fq_quantize_frames (K_out x K_in codes).
  *   P_out  device fp32 d_out x K_out;  P_in device fp32 d_in x K_in.
- *   Y      device fp32, n_tokens x d_out, row-major.
+ *   Y      device fp32, n_tokens x d_out, row-major (written; never read).
+ *   ws     caller workspace of fq_frame_apply_workspace_bytes(d_in, K_out, K_in) bytes,
+ *          16-byte aligned; its contents on entry do not matter.
  * Meant for decode and small batches: every frame and the codes are streamed once per
  * block of 8 tokens (for large token counts form Theta^ with fq_frame_synthesis and use a
- * GEMM).  fp32 arithmetic with fp32 accumulation.
+ * GEMM).  fp32 arithmetic with fp32 accumulation.  n_tokens == 0 or d_out == 0 is a
+ * no-op; d_in, K_out or K_in == 0 writes Y = 0.  Errors (before any launch):
+ * FQ_ERR_INVALID_ARG (xt, a dimension outside [0, 2^30), K < d, ldx < d_in, a NULL
+ * array), FQ_ERR_WORKSPACE_TOO_SMALL; FQ_ERR_HIP if a launch fails.
  */
 fq_status fq_frame_apply(void* stream, const void* X, int xt, int64_t n_tokens, int64_t ldx,
                          int64_t d_in, const uint32_t* codes, const float* scale,

@@ -267,9 +267,9 @@ def synthesis(codes, scale, zero, P_out, P_in):
 
 
 def frame_apply(X, codes, scale, zero, P_out, P_in):
-    """Layer outputs of the quantized layer, Y = X Theta^T with Theta^ = P_l D^ P_prev^T
-    (appendix "Computational Complexity during Inference": the output is produced from the
-    stored codes and the two frames).  X: tokens x d_in; Y: tokens x d_out."""
+    """Layer outputs of the quantized layer (Sec. 3 "Inference Procedure"), by their plain
+    definition Y = X Theta^T with Theta^ = P_l D^ P_prev^T (appendix "Computational
+    Complexity during Inference").  X: tokens x d_in; Y: tokens x d_out."""
     Wh = synthesis(codes, scale, zero, P_out, P_in)
     return np.asarray(X, dtype=np.float64) @ Wh.T
 

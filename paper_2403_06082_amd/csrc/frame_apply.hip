@@ -1,6 +1,7 @@
-// Layer outputs straight from the stored codes and the two frames (appendix
-// "Computational Complexity during Inference"): Y = X Theta^T with
-// Theta^ = P_out diag(scale) (q - zero) P_in^T, taken in the order
+// Layer outputs straight from the stored codes and the two frames: Y = X Theta^T with
+// Theta^ = P_out diag(scale) (q - zero) P_in^T (appendix "Computational Complexity during
+// Inference"), taken in the order of Sec. 3 "Inference Procedure" (analysis operator on
+// the inputs, the quantized D^, synthesis operator):
 //   U = X P_in            (tokens x K_in)
 //   V = U (q - zero)^T S  (tokens x K_out; the 2-bit codes decoded on the fly)
 //   Y = V P_out^T         (tokens x d_out)
@@ -16,7 +17,6 @@ namespace fq {
 namespace {
 
 constexpr int AT = 256;        // threads per work-group in every kernel here
-constexpr int UCH = 4096;      // columns of U staged in LDS at a time by the code kernel
 
 template <typename T>
 __device__ __forceinline__ float to_f32(T v);
@@ -77,26 +77,38 @@ __global__ __launch_bounds__(AT) void k_apply_in(const XT* __restrict__ X, int64
 }
 
 // U[t][j] = sum over the splits (fp64), zero for t >= nt; U has ldu >= K_in columns,
-// columns [K_in, ldu) zero.
+// columns [K_in, ldu) zero.  grid (ldu / 64, NT): a work-group owns 64 columns of one
+// token; its 4 waves sum every 4th split and combine through LDS in a fixed order.
 __global__ __launch_bounds__(AT) void k_apply_in_reduce(const float* __restrict__ part, int nt_blk,
                                                         int nt, int ksplit, int64_t K_in,
                                                         int64_t ldu, float* __restrict__ U) {
-  const int64_t total = (int64_t)nt_blk * ldu;
-  for (int64_t e = (int64_t)blockIdx.x * AT + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * AT) {
-    const int t = (int)(e / ldu);
-    const int64_t j = e - t * ldu;
-    double acc = 0.0;
-    if (t < nt && j < K_in)
-      for (int s = 0; s < ksplit; ++s) acc += part[((int64_t)s * nt_blk + t) * K_in + j];
-    U[e] = (float)acc;
+  __shared__ double red[AT / 64][64];
+  const int lane = threadIdx.x & 63, g = threadIdx.x >> 6;
+  const int t = blockIdx.y;
+  const int64_t j = (int64_t)blockIdx.x * 64 + lane;
+  double acc = 0.0;
+  if (t < nt && j < K_in) {
+    const float* p = part + (int64_t)t * K_in + j;
+    const int64_t step = (int64_t)nt_blk * K_in;
+#pragma unroll 8
+    for (int s = g; s < ksplit; s += AT / 64) acc += p[s * step];
   }
+  red[g][lane] = acc;
+  __syncthreads();
+  if (g == 0 && j < ldu)
+    U[(int64_t)t * ldu + j] = (float)(red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane]);
 }
 
-// ---- step 2: V[t][i] = scale_i sum_j U[t][j] (q_ij - zero_i)
-// A work-group owns 16 rows (4 per wave); U goes through LDS UCH columns at a time; a
-// lane takes code words w = lane, lane + 64, ... of its wave's 4 rows, decodes each word
-// once (q - zero, small integers, exact) and applies it to every token.
+// ---- step 2: V[t][i] = scale_i (sum_j U[t][j] q_ij - zero_i sum_j U[t][j])
+// (the same sum as sum_j U[t][j] (q_ij - zero_i); both forms have error bounds of the
+// same size, since |q|, |q - zero| <= 3).  A work-group owns 16 rows (4 per wave); U goes
+// through LDS UCH(NT) columns at a time (at most 32 KB), and the work-group sums each token's U
+// while staging it.  A lane takes code words w = lane, lane + 64, ... of its wave's 4
+// rows (loaded for the whole chunk before the chunk of U is staged).  A word is spread
+// into bytes, (word >> 2b) & 0x03030303 holding the codes of columns b, b+4, b+8, b+12,
+// and each byte converts to float in one instruction.  In LDS, group g (4 columns) of
+// word w sits at group (g + w/2) mod 4 of the word's 16 columns, so that 8 lanes reading
+// the same group of consecutive words cover all banks.
 template <int NT>
 __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U, int64_t ldu,
                                                     const uint32_t* __restrict__ codes,
@@ -104,96 +116,130 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
                                                     const float* __restrict__ scale,
                                                     const float* __restrict__ zero,
                                                     float* __restrict__ V) {
+  constexpr int UCH = NT == 1 ? 4096 : 8192 / NT;   // columns per chunk (at most 32 KB)
+  constexpr int WPL = UCH / (16 * 64);       // code words per lane and row in a chunk
+  constexpr int SPT = UCH / (4 * AT);        // staging rounds per token
   __shared__ __attribute__((aligned(16))) float us[NT][UCH];
+  __shared__ float usum_w[AT / 64][NT];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t row0 = (int64_t)blockIdx.x * 16 + wave * 4;
-  float acc[4][NT];
+  float acc[4][NT], tsum[NT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int t = 0; t < NT; ++t) {
+    tsum[t] = 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) acc[r][t] = 0.f;
-  const uint32_t* crow[4];
-  float zr[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int64_t i = min(row0 + r, K_out - 1);
-    crow[r] = codes + i * nwords;
-    zr[r] = zero[i];
   }
+  const uint32_t* crow[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) crow[r] = codes + min(row0 + r, K_out - 1) * nwords;
   for (int64_t c0 = 0; c0 < ldu; c0 += UCH) {
     const int cn = (int)min((int64_t)UCH, ldu - c0);        // multiple of 16
-    __syncthreads();
-    for (int e = threadIdx.x * 4; e < NT * UCH; e += AT * 4) {
-      const int t = e / UCH, c = e % UCH;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (c < cn) v = *reinterpret_cast<const float4*>(U + t * ldu + c0 + c);
-      *reinterpret_cast<float4*>(&us[t][c]) = v;
-    }
-    __syncthreads();
+    const int nw = cn / 16;
     const int64_t w0 = c0 / 16;
-    for (int w = lane; w < cn / 16; w += 64) {
-      float q[4][16];
+    uint32_t wd[4][WPL];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t word = (w0 + w < nwords) ? crow[r][w0 + w] : 0u;
+    for (int k = 0; k < WPL; ++k) {
+      const int w = lane + 64 * k;
 #pragma unroll
-        for (int b = 0; b < 16; ++b) q[r][b] = (float)((word >> (2 * b)) & 3u) - zr[r];
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        float u[16];
-#pragma unroll
-        for (int b = 0; b < 16; b += 4) {
-          const float4 v = *reinterpret_cast<const float4*>(&us[t][16 * w + b]);
-          u[b] = v.x; u[b + 1] = v.y; u[b + 2] = v.z; u[b + 3] = v.w;
-        }
-#pragma unroll
-        for (int b = 0; b < 16; ++b)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[r][t] = fmaf(u[b], q[r][b], acc[r][t]);
-      }
+      for (int r = 0; r < 4; ++r) wd[r][k] = (w < nw) ? crow[r][w0 + w] : 0u;
     }
-  }
-  // wave sums
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
+    __syncthreads();
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r][t] += __shfl_xor(acc[r][t], o);
+      for (int m = 0; m < SPT; ++m) {
+        const int c = (m * AT + (int)threadIdx.x) * 4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (c < cn) v = *reinterpret_cast<const float4*>(U + t * ldu + c0 + c);
+        tsum[t] += (v.x + v.y) + (v.z + v.w);
+        const int w = c >> 4, g = (c >> 2) & 3;
+        *reinterpret_cast<float4*>(&us[t][16 * w + 4 * ((g + (w >> 1)) & 3)]) = v;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < WPL; ++k) {
+      const int w = lane + 64 * k;
+      if (w >= nw) break;
+      uint32_t y[4][4];                       // byte g of y[r][b]: code of column 4g + b
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          y[r][b] = (wd[r][k] >> (2 * b)) & 0x03030303u;
+          asm volatile("" : "+v"(y[r][b]));   // keep the bytes: one conversion per code
+        }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float q[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) q[r][b] = (float)((y[r][b] >> (8 * g)) & 0xffu);
+        const int pg = (g + (w >> 1)) & 3;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const float4 v = *reinterpret_cast<const float4*>(&us[t][16 * w + 4 * pg]);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            acc[r][t] = fmaf(v.x, q[r][0], acc[r][t]);
+            acc[r][t] = fmaf(v.y, q[r][1], acc[r][t]);
+            acc[r][t] = fmaf(v.z, q[r][2], acc[r][t]);
+            acc[r][t] = fmaf(v.w, q[r][3], acc[r][t]);
+          }
+        }
+      }
+    }
   }
+  // token sums of U over the work-group, row sums over each wave
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      tsum[t] += __shfl_xor(tsum[t], o);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r][t] += __shfl_xor(acc[r][t], o);
+    }
+  }
+  if (lane == 0)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) usum_w[wave][t] = tsum[t];
+  __syncthreads();
   if (lane == 0) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int64_t i = row0 + r;
       if (i < K_out) {
-        const float s = scale[i];
+        const float s = scale[i], z = zero[i];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) V[t * K_out + i] = s * acc[r][t];
+        for (int t = 0; t < NT; ++t) {
+          const float us_t = (usum_w[0][t] + usum_w[1][t]) + (usum_w[2][t] + usum_w[3][t]);
+          V[t * K_out + i] = s * fmaf(-z, us_t, acc[r][t]);
+        }
       }
     }
   }
 }
 
 // ---- step 3: Y[t][o] = sum_i V[t][i] P_out[o][i]
-// A work-group owns 4 output rows; a thread owns 4 consecutive columns of every 4 AT-wide
-// chunk of P_out's rows.
-template <int NT, bool VEC>
+// A work-group owns R output rows; a thread owns 4 consecutive columns of every 4 AT-wide
+// chunk of P_out's rows (each V element is read once per work-group).
+template <int NT, int R, bool VEC>
 __global__ __launch_bounds__(AT) void k_apply_out(const float* __restrict__ V, int nt,
                                                   const float* __restrict__ P, int64_t K_out,
                                                   int64_t d_out, float* __restrict__ Y,
                                                   int64_t ldy) {
-  __shared__ float red[AT / 64][4][NT];
+  __shared__ float red[AT / 64][R][NT];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t o0 = (int64_t)blockIdx.x * 4;
-  float acc[4][NT];
+  const int64_t o0 = (int64_t)blockIdx.x * R;
+  float acc[R][NT];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[r][t] = 0.f;
-  const float* prow[4];
+  const float* prow[R];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) prow[r] = P + min(o0 + r, d_out - 1) * K_out;
+  for (int r = 0; r < R; ++r) prow[r] = P + min(o0 + r, d_out - 1) * K_out;
   for (int64_t i = (int64_t)threadIdx.x * 4; i < K_out; i += AT * 4) {
     float v[NT][4];
 #pragma unroll
@@ -207,7 +253,7 @@ __global__ __launch_bounds__(AT) void k_apply_out(const float* __restrict__ V, i
       }
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < R; ++r) {
       float p[4];
       if (VEC) {
         const float4 w = *reinterpret_cast<const float4*>(prow[r] + i);
@@ -225,16 +271,16 @@ __global__ __launch_bounds__(AT) void k_apply_out(const float* __restrict__ V, i
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1)
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[r][t] += __shfl_xor(acc[r][t], o);
   if (lane == 0)
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int t = 0; t < NT; ++t) red[wave][r][t] = acc[r][t];
   __syncthreads();
-  if (threadIdx.x < 4 * NT) {
+  if (threadIdx.x < R * NT) {
     const int r = threadIdx.x / NT, t = threadIdx.x % NT;
     const int64_t o = o0 + r;
     if (o < d_out && t < nt) {
@@ -279,21 +325,20 @@ hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
   else if (xt == 1) { FQ_APPLY_IN(_Float16) }
   else { FQ_APPLY_IN(uint16_t) }
 #undef FQ_APPLY_IN
-  const int64_t tot = (int64_t)NT * ldu;
-  hipLaunchKernelGGL(k_apply_in_reduce, dim3((unsigned)std::min<int64_t>((tot + AT - 1) / AT, 4096)),
-                     dim3(AT), 0, s, w.part, NT, nt, ks_eff, K_in, ldu, w.U);
+  hipLaunchKernelGGL(k_apply_in_reduce, dim3((unsigned)(ldu / 64 + (ldu % 64 != 0)), NT), dim3(AT), 0, s,
+                     w.part, NT, nt, ks_eff, K_in, ldu, w.U);
   prof_end(s);
   prof_begin(s, "apply_codes");
   hipLaunchKernelGGL(k_apply_codes<NT>, dim3((unsigned)((K_out + 15) / 16)), dim3(AT), 0, s,
                      w.U, ldu, codes, K_out, (K_in + 15) / 16, scale, zero, w.V);
   prof_end(s);
   prof_begin(s, "apply_out");
+  constexpr int R = NT >= 4 ? 8 : 4;
+  const dim3 gout((unsigned)((d_out + R - 1) / R));
   if (vout)
-    hipLaunchKernelGGL((k_apply_out<NT, true>), dim3((unsigned)((d_out + 3) / 4)), dim3(AT), 0, s,
-                       w.V, nt, P_out, K_out, d_out, Y, d_out);
+    hipLaunchKernelGGL((k_apply_out<NT, R, true>), gout, dim3(AT), 0, s, w.V, nt, P_out, K_out, d_out, Y, d_out);
   else
-    hipLaunchKernelGGL((k_apply_out<NT, false>), dim3((unsigned)((d_out + 3) / 4)), dim3(AT), 0,
-                       s, w.V, nt, P_out, K_out, d_out, Y, d_out);
+    hipLaunchKernelGGL((k_apply_out<NT, R, false>), gout, dim3(AT), 0, s, w.V, nt, P_out, K_out, d_out, Y, d_out);
   prof_end(s);
   return last_launch_error();
 }
