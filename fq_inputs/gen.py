@@ -139,6 +139,20 @@ def make_frames(wl: Workload, li: int, dtype=np.float64):
     return P_out, P_in
 
 
+def frame_factors(wl: Workload, d: int, tag: int, index: int = 0):
+    """(k, rho, R1, R2): the construction parameters of make_frame(wl, d, tag, index), whose
+    rotation is R1 (x) R2 with exactly these (float64) factors."""
+    k = frame_k(wl, d)
+    R1, R2 = tff.rotation_factors(d, np.random.SeedSequence([wl.seed, tag, index]))
+    return k, wl.rho, R1, R2
+
+
+def layer_frame_factors(wl: Workload, li: int):
+    """frame_factors of (P_out, P_in) of layer li, as make_frames builds them."""
+    L = wl.layers[li]
+    return frame_factors(wl, L.d_out, TAG_POUT, li), frame_factors(wl, L.d_in, TAG_PIN, 0)
+
+
 def frame_f32(P: np.ndarray) -> np.ndarray:
     """The frame as the float32 matrix handed to the device (RNE from float64)."""
     return np.ascontiguousarray(P, dtype=np.float32)

@@ -182,6 +182,61 @@ fq_status fq_frame_apply(void* stream, const void* X, int xt, int64_t n_tokens, 
                          size_t ws_bytes);
 size_t fq_frame_apply_workspace_bytes(int64_t d_in, int64_t K_out, int64_t K_in);
 
+/*
+ * A real tight fusion frame given by its construction instead of a dense matrix (Sec. 2.2
+ * "Constructing TFFs"; appendix "Synopsis of Construction of Tight Fusion Frames"):
+ *   P = (R1 (x) R2) T / sqrt(k),  d x (k rho), Parseval (P P^T = I),
+ * T's column block s < k (rho columns) being the realified subspace s of the complex
+ * (k, rho/2, d/2) frame built by spectral tetris and modulation by the k-th roots of
+ * unity (complex coordinate j = real pair (2j, 2j+1), complex column c = real pair
+ * (2c, 2c+1)), and R1 (x) R2 mapping a vector read row-major as a d1 x d2 matrix M to
+ * R1 M R2^T.  Supported: d and rho even, d divisible by rho (the base frame's rows are
+ * then blocks of m = d / rho ones), m <= k <= 3968, d1 d2 = d, d2 <= 4096.  R1, R2: device fp32,
+ * row-major, owned by the caller.  The transforms below cost d (d1 + d2) + 2 d k FMAs per
+ * vector and read no d x K matrix.
+ */
+typedef struct fq_tff {
+  int64_t d, k, rho;
+  const float* R1;
+  int64_t d1;
+  const float* R2;
+  int64_t d2;
+} fq_tff;
+
+/*
+ * Analysis operator on n vectors (Sec. 2 "Operators in Fusion Frames"): U = X P, i.e. row
+ * t of U is P^T x_t.  X device n x d, element type xt, row stride ldx >= d; U device fp32
+ * n x (k rho), row-major.  ws: fq_tff_analysis_workspace_bytes(n, frame) bytes, 16-byte
+ * aligned.  Errors: FQ_ERR_INVALID_ARG (xt, sizes, ldx, NULL arrays, a frame outside the
+ * supported set), FQ_ERR_UNSUPPORTED (d not divisible by rho, k > 3968, d2 > 4096),
+ * FQ_ERR_WORKSPACE_TOO_SMALL, FQ_ERR_HIP.
+ */
+fq_status fq_tff_analysis(void* stream, const void* X, int xt, int64_t n, int64_t ldx,
+                          const fq_tff* frame, float* U, void* ws, size_t ws_bytes);
+size_t fq_tff_analysis_workspace_bytes(int64_t n, const fq_tff* frame);
+
+/*
+ * Synthesis operator (the adjoint, same passage): Y = V P^T, row t of Y is P v_t.  V device
+ * fp32 n x (k rho); Y device fp32 n x d.  Same workspace rule and errors as the analysis.
+ */
+fq_status fq_tff_synthesis(void* stream, const float* V, int64_t n, const fq_tff* frame,
+                           float* Y, void* ws, size_t ws_bytes);
+size_t fq_tff_synthesis_workspace_bytes(int64_t n, const fq_tff* frame);
+
+/*
+ * fq_frame_apply with both frames given by their construction (Sec. 3 "Inference
+ * Procedure"): Y = ((X P_in) (codes - zero)^T diag(scale)) P_out^T, where P_in is
+ * frame_in (d = d_in, K_in = k rho) and P_out is frame_out (d = d_out, K_out = k rho).
+ * Reads the codes once per block of 8 tokens and no frame matrix.  X, codes, scale, zero,
+ * Y as in fq_frame_apply; ws: fq_frame_apply_tff_workspace_bytes(frame_out, frame_in).
+ * Errors as fq_frame_apply and fq_tff_analysis.
+ */
+fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_tokens,
+                             int64_t ldx, const uint32_t* codes, const float* scale,
+                             const float* zero, const fq_tff* frame_out,
+                             const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes);
+size_t fq_frame_apply_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
+
 /* Status text and the calling thread's last error message (never NULL). */
 const char* fq_status_string(int status);
 const char* fq_last_error(void);

@@ -33,6 +33,20 @@ import scipy.linalg as sla
 TIE_EPS = 1e-6
 
 
+# --------------------------------------------------------------------------- operators
+def frame_analysis_vectors(X, P):
+    """Analysis operator of the fusion frame on each row x of X (Sec. 2 "Operators in Fusion
+    Frames"): the dot products of x with every column of P = [w_1 P_1 ... w_k P_k], i.e. the
+    rows P^T x, stacked: U = X P.  X: n x d; U: n x (k rho)."""
+    return np.asarray(X, dtype=np.float64) @ np.asarray(P, dtype=np.float64)
+
+
+def frame_synthesis_vectors(U, P):
+    """Synthesis operator (the adjoint of the analysis operator, same passage) on each row
+    u of U: sum_i w_i P_i u_i = P u, stacked: Y = U P^T.  U: n x (k rho); Y: n x d."""
+    return np.asarray(U, dtype=np.float64) @ np.asarray(P, dtype=np.float64).T
+
+
 # --------------------------------------------------------------------------- stage 1
 def hessian(X_chunks) -> np.ndarray:
     """Calibration Hessian H = X^T X = A_prev A_prev^T (Sec. 3, proxy loss: the FF-space

@@ -693,4 +693,165 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   return FQ_OK;
 }
 
+// ================================================================ structured frames
+static bool tff_dims_ok(const fq_tff* f) {
+  return f && f->d > 0 && f->k > 0 && f->rho > 0 && dim_ok(f->d) && dim_ok(f->k) &&
+         dim_ok(f->rho) && f->d % 2 == 0 && f->rho % 2 == 0 && f->d % f->rho == 0 &&
+         f->d / f->rho <= f->k && f->k <= TFF_MAX_K && f->rho <= 131070 &&
+         f->k * f->rho < DIM_MAX && f->d1 > 0 && f->d2 > 0 && f->d1 * f->d2 == f->d &&
+         f->d2 <= TFF_MAX_D2;
+}
+
+static fq_status tff_check(const fq_tff* f, const char* which, TffDev* out) {
+  char msg[160];
+  auto bad = [&](fq_status st, const char* why) {
+    snprintf(msg, sizeof msg, "%s: %s", which, why);
+    return fail(st, msg);
+  };
+  if (!f) return bad(FQ_ERR_INVALID_ARG, "NULL frame");
+  if (f->d <= 0 || f->k <= 0 || f->rho <= 0 || !dim_ok(f->d) || !dim_ok(f->k) || !dim_ok(f->rho))
+    return bad(FQ_ERR_INVALID_ARG, "d, k and rho must be in [1, 2^30)");
+  if (f->d % 2 || f->rho % 2) return bad(FQ_ERR_INVALID_ARG, "d and rho must be even (a realified complex frame)");
+  if (f->d1 <= 0 || f->d2 <= 0 || f->d1 * f->d2 != f->d) return bad(FQ_ERR_INVALID_ARG, "d1 * d2 must equal d");
+  if (!f->R1 || !f->R2) return bad(FQ_ERR_INVALID_ARG, "NULL rotation factor");
+  if (f->d % f->rho) return bad(FQ_ERR_UNSUPPORTED, "d must be divisible by rho");
+  if (f->d / f->rho > f->k) return bad(FQ_ERR_INVALID_ARG, "d / rho must not exceed k (the modulation is not tight otherwise)");
+  if (f->k > TFF_MAX_K || f->rho > 131070) return bad(FQ_ERR_UNSUPPORTED, "k above 3968 or rho above 131070");
+  if (f->d2 > TFF_MAX_D2) return bad(FQ_ERR_UNSUPPORTED, "d2 above 4096");
+  if (f->k * f->rho >= DIM_MAX) return bad(FQ_ERR_INVALID_ARG, "k * rho must be below 2^30");
+  out->d = f->d; out->k = f->k; out->rho = f->rho; out->m = f->d / f->rho;
+  out->R1 = f->R1; out->d1 = (int)f->d1; out->R2 = f->R2; out->d2 = (int)f->d2;
+  return FQ_OK;
+}
+
+struct TffLayout { float* a; float* r2t; };
+
+static size_t tff_layout(int64_t n, const fq_tff* f, void* base, TffLayout* L) {
+  const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(n, TFF_CHUNK));
+  Carver c(base);
+  TffLayout l{};
+  l.a = c.take<float>((size_t)(chunk * f->d));
+  l.r2t = c.take<float>((size_t)(f->d2 * f->d2));
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+struct ApplyTffLayout { float* y; float* U; float* V; float* z; float* r2t; };
+
+static size_t apply_tff_layout(const fq_tff* fo, const fq_tff* fi, void* base, ApplyTffLayout* L) {
+  const int64_t K_in = fi->k * fi->rho, K_out = fo->k * fo->rho;
+  Carver c(base);
+  ApplyTffLayout l{};
+  l.y = c.take<float>((size_t)(APPLY_NT * fi->d));
+  l.U = c.take<float>((size_t)(APPLY_NT * ((K_in + 15) / 16 * 16)));
+  l.V = c.take<float>((size_t)(APPLY_NT * K_out));
+  l.z = c.take<float>((size_t)(APPLY_NT * fo->d));
+  l.r2t = c.take<float>((size_t)(fo->d2 * fo->d2));
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+size_t fq_tff_analysis_workspace_bytes(int64_t n, const fq_tff* frame) {
+  if (!dim_ok(n) || !tff_dims_ok(frame)) return 0;
+  return tff_layout(n, frame, nullptr, nullptr);
+}
+
+size_t fq_tff_synthesis_workspace_bytes(int64_t n, const fq_tff* frame) {
+  return fq_tff_analysis_workspace_bytes(n, frame);
+}
+
+size_t fq_frame_apply_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in) {
+  if (!tff_dims_ok(frame_out) || !tff_dims_ok(frame_in)) return 0;
+  return apply_tff_layout(frame_out, frame_in, nullptr, nullptr);
+}
+
+fq_status fq_tff_analysis(void* stream, const void* X, int xt, int64_t n, int64_t ldx,
+                          const fq_tff* frame, float* U, void* ws, size_t ws_bytes) {
+  if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (!dim_ok(n)) return fail(FQ_ERR_INVALID_ARG, "n must be in [0, 2^30)");
+  TffDev F;
+  fq_status st = tff_check(frame, "frame", &F);
+  if (st != FQ_OK) return st;
+  if (ldx < F.d) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d");
+  if (n == 0) return FQ_OK;
+  if (!X || !U) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  if (ws_bytes < tff_layout(n, frame, nullptr, nullptr)) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_tff_analysis_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  TffLayout L;
+  tff_layout(n, frame, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  hipError_t e;
+  const int esz = xt == FQ_F32 ? 4 : 2;
+  const int64_t K = F.k * F.rho;
+  for (int64_t t0 = 0; t0 < n; t0 += TFF_CHUNK) {
+    const int64_t nc = std::min<int64_t>(TFF_CHUNK, n - t0);
+    if ((e = tff_analysis((const char*)X + t0 * ldx * esz, xt, ldx, nc, F, L.a, U + t0 * K, K,
+                          s)) != hipSuccess)
+      return hip_fail(e, "tff analysis");
+  }
+  return FQ_OK;
+}
+
+fq_status fq_tff_synthesis(void* stream, const float* V, int64_t n, const fq_tff* frame,
+                           float* Y, void* ws, size_t ws_bytes) {
+  if (!dim_ok(n)) return fail(FQ_ERR_INVALID_ARG, "n must be in [0, 2^30)");
+  TffDev F;
+  fq_status st = tff_check(frame, "frame", &F);
+  if (st != FQ_OK) return st;
+  if (n == 0) return FQ_OK;
+  if (!V || !Y) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  if (ws_bytes < tff_layout(n, frame, nullptr, nullptr)) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_tff_synthesis_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  if (((uintptr_t)V & 7) != 0) return fail(FQ_ERR_INVALID_ARG, "V must be 8-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  TffLayout L;
+  tff_layout(n, frame, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  hipError_t e;
+  if ((e = tff_transpose_r2(F, L.r2t, s)) != hipSuccess) return hip_fail(e, "transpose R2");
+  const int64_t K = F.k * F.rho;
+  for (int64_t t0 = 0; t0 < n; t0 += TFF_CHUNK) {
+    const int64_t nc = std::min<int64_t>(TFF_CHUNK, n - t0);
+    if ((e = tff_synthesis(V + t0 * K, K, nc, F, L.r2t, L.a, Y + t0 * F.d, F.d, s)) != hipSuccess)
+      return hip_fail(e, "tff synthesis");
+  }
+  return FQ_OK;
+}
+
+fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_tokens,
+                             int64_t ldx, const uint32_t* codes, const float* scale,
+                             const float* zero, const fq_tff* frame_out,
+                             const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes) {
+  if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (!dim_ok(n_tokens)) return fail(FQ_ERR_INVALID_ARG, "n_tokens must be in [0, 2^30)");
+  TffDev Fo, Fi;
+  fq_status st = tff_check(frame_out, "frame_out", &Fo);
+  if (st != FQ_OK) return st;
+  if ((st = tff_check(frame_in, "frame_in", &Fi)) != FQ_OK) return st;
+  if (ldx < Fi.d) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d_in");
+  if (n_tokens == 0) return FQ_OK;
+  if (!X || !codes || !scale || !zero || !Y) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  if (ws_bytes < apply_tff_layout(frame_out, frame_in, nullptr, nullptr))
+    return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_apply_tff_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  ApplyTffLayout L;
+  apply_tff_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  const int64_t K_in = Fi.k * Fi.rho, K_out = Fo.k * Fo.rho;
+  const int64_t ldu = (K_in + 15) / 16 * 16;
+  hipError_t e;
+  if ((e = tff_transpose_r2(Fo, L.r2t, s)) != hipSuccess) return hip_fail(e, "transpose R2");
+  const int esz = xt == FQ_F32 ? 4 : 2;
+  for (int64_t t0 = 0; t0 < n_tokens; t0 += APPLY_NT) {
+    const int nt = (int)std::min<int64_t>(APPLY_NT, n_tokens - t0);
+    if ((e = tff_analysis((const char*)X + t0 * ldx * esz, xt, ldx, nt, Fi, L.y, L.U, ldu, s)) !=
+        hipSuccess)
+      return hip_fail(e, "tff analysis");
+    if ((e = apply_codes(L.U, ldu, nt, codes, K_out, (K_in + 15) / 16, scale, zero, L.V, s)) != hipSuccess)
+      return hip_fail(e, "apply codes");
+    if ((e = tff_synthesis(L.V, K_out, nt, Fo, L.r2t, L.z, Y + t0 * Fo.d, Fo.d, s)) != hipSuccess)
+      return hip_fail(e, "tff synthesis");
+  }
+  return FQ_OK;
+}
+
 }  // extern "C"

@@ -83,6 +83,33 @@ struct ApplyScratch {
 size_t apply_scratch_floats(int64_t d_in, int64_t K_out, int64_t K_in, ApplyScratch* w,
                             float* base);
 // X: n x d_in (row stride ldx, element type xt: 0 f32, 1 f16, 2 bf16); Y: n x d_out fp32
+// V (rows [0, tokens-per-block) with tokens-per-block = 1, 2, 4 or 8 >= nt) = scale *
+// (U (codes - zero)^T) for U with ldu = 16 * ceil(K_in / 16) columns, zero beyond K_in.
+hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* codes,
+                       int64_t K_out, int64_t nwords, const float* scale, const float* zero,
+                       float* V, hipStream_t s);
+// ---------------------------------------------------------------- structured frames
+// A validated tight fusion frame given by its construction (see tff_apply.hip):
+// m = d / rho, R1 d1 x d1 and R2 d2 x d2 device fp32, d1 d2 = d.
+struct TffDev {
+  int64_t d, k, rho, m;
+  const float* R1;
+  int d1;
+  const float* R2;
+  int d2;
+};
+constexpr int64_t TFF_MAX_K = 3968;       // twiddles + one block of a vector within 64 KB of LDS
+constexpr int64_t TFF_MAX_D2 = 4096;     // one row of the rotation's d1 x d2 view in LDS
+constexpr int64_t TFF_CHUNK = 256;        // vectors per pass of the stand-alone transforms
+// U (n x ldu, ldu >= k rho, columns beyond k rho set to 0) = X P; y: n x d scratch
+hipError_t tff_analysis(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F,
+                        float* y, float* U, int64_t ldu, hipStream_t s);
+// R2t (d2 x d2) = R2^T, read by tff_synthesis
+hipError_t tff_transpose_r2(const TffDev& F, float* R2t, hipStream_t s);
+// Y (n x ldy) = V P^T with V n x ldv (ldv even), R2t from tff_transpose_r2; z: n x d scratch
+hipError_t tff_synthesis(const float* V, int64_t ldv, int64_t n, const TffDev& F,
+                         const float* R2t, float* z, float* Y, int64_t ldy, hipStream_t s);
+
 hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_in,
                        const uint32_t* codes, const float* scale, const float* zero,
                        int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,

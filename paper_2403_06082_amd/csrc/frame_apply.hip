@@ -18,6 +18,12 @@ namespace {
 
 constexpr int AT = 256;        // threads per work-group in every kernel here
 
+// Work-group barrier for LDS traffic only: waits for this wave's LDS operations, not for
+// its global loads (a fenced __syncthreads would also drain every load in flight).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 template <typename T>
 __device__ __forceinline__ float to_f32(T v);
 template <>
@@ -111,12 +117,12 @@ __global__ __launch_bounds__(AT) void k_apply_in_reduce(const float* __restrict_
 // the same group of consecutive words cover all banks.
 template <int NT>
 __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U, int64_t ldu,
-                                                    const uint32_t* __restrict__ codes,
+                                                    const uint32_t* codes,   // not restrict: its loads must stay before the barriers
                                                     int64_t K_out, int64_t nwords,
                                                     const float* __restrict__ scale,
                                                     const float* __restrict__ zero,
                                                     float* __restrict__ V) {
-  constexpr int UCH = NT == 1 ? 4096 : 8192 / NT;   // columns per chunk (at most 32 KB)
+  constexpr int UCH = NT <= 4 ? 2048 : 8192 / NT;    // columns per chunk (at most 32 KB)
   constexpr int WPL = UCH / (16 * 64);       // code words per lane and row in a chunk
   constexpr int SPT = UCH / (4 * AT);        // staging rounds per token
   __shared__ __attribute__((aligned(16))) float us[NT][UCH];
@@ -133,30 +139,49 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
   const uint32_t* crow[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) crow[r] = codes + min(row0 + r, K_out - 1) * nwords;
-  for (int64_t c0 = 0; c0 < ldu; c0 += UCH) {
-    const int cn = (int)min((int64_t)UCH, ldu - c0);        // multiple of 16
-    const int nw = cn / 16;
-    const int64_t w0 = c0 / 16;
-    uint32_t wd[4][WPL];
+  // code words of a chunk: 4 rows x WPL words per lane (clamped loads, unconditional)
+  auto load_words = [&](uint32_t (&dst)[4][WPL], int64_t c0) {
+    const int nw = (int)(min((int64_t)UCH, ldu - c0) / 16);
 #pragma unroll
     for (int k = 0; k < WPL; ++k) {
       const int w = lane + 64 * k;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) wd[r][k] = (w < nw) ? crow[r][w0 + w] : 0u;
+      for (int r = 0; r < 4; ++r) dst[r][k] = crow[r][c0 / 16 + min(w, nw - 1)];
     }
-    __syncthreads();
+  };
+  uint32_t wd[4][WPL], wn[4][WPL] = {};
+  for (int64_t c0 = 0; c0 < ldu; c0 += UCH) {
+    const int cn = (int)min((int64_t)UCH, ldu - c0);        // multiple of 16
+    const int nw = cn / 16;
+    lds_barrier();                          // the previous chunk's reads of us are done
+    float4 uv[NT][SPT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int m = 0; m < SPT; ++m) {
+        const int c = (m * AT + (int)threadIdx.x) * 4;   // unconditional load, clamped
+        uv[t][m] = *reinterpret_cast<const float4*>(U + t * ldu + c0 + min(c, cn - 4));
+      }
+    // the first chunk's words are loaded after its U, so that storing U into LDS waits for
+    // U alone; later chunks' words were loaded one chunk ahead
+    if (c0 == 0) load_words(wd, 0);
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int m = 0; m < SPT; ++m) {
         const int c = (m * AT + (int)threadIdx.x) * 4;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (c < cn) v = *reinterpret_cast<const float4*>(U + t * ldu + c0 + c);
+        const uint32_t keep = c < cn ? 0xffffffffu : 0u;      // a mask, not a branch: the
+        const float4 u4 = uv[t][m];                            // load stays unconditional
+        const float4 v = make_float4(__uint_as_float(__float_as_uint(u4.x) & keep),
+                                     __uint_as_float(__float_as_uint(u4.y) & keep),
+                                     __uint_as_float(__float_as_uint(u4.z) & keep),
+                                     __uint_as_float(__float_as_uint(u4.w) & keep));
         tsum[t] += (v.x + v.y) + (v.z + v.w);
         const int w = c >> 4, g = (c >> 2) & 3;
         *reinterpret_cast<float4*>(&us[t][16 * w + 4 * ((g + (w >> 1)) & 3)]) = v;
       }
-    __syncthreads();
+    lds_barrier();
+    if (c0 + UCH < ldu) load_words(wn, c0 + UCH);   // in flight during this chunk's work
 #pragma unroll
     for (int k = 0; k < WPL; ++k) {
       const int w = lane + 64 * k;
@@ -190,6 +215,10 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
         }
       }
     }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int k = 0; k < WPL; ++k) wd[r][k] = wn[r][k];
   }
   // token sums of U over the work-group, row sums over each wave
 #pragma unroll
@@ -344,6 +373,19 @@ hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
 }
 
 }  // namespace
+
+hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* codes,
+                       int64_t K_out, int64_t nwords, const float* scale, const float* zero,
+                       float* V, hipStream_t s) {
+  const dim3 g((unsigned)((K_out + 15) / 16));
+  prof_begin(s, "apply_codes");
+  if (nt == 1) hipLaunchKernelGGL(k_apply_codes<1>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+  else if (nt == 2) hipLaunchKernelGGL(k_apply_codes<2>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+  else if (nt <= 4) hipLaunchKernelGGL(k_apply_codes<4>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+  else hipLaunchKernelGGL(k_apply_codes<8>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+  prof_end(s);
+  return last_launch_error();
+}
 
 size_t apply_scratch_floats(int64_t d_in, int64_t K_out, int64_t K_in, ApplyScratch* w,
                             float* base) {

@@ -19,6 +19,17 @@ STATUS = {0: "FQ_OK", 1: "FQ_ERR_INVALID_ARG", 2: "FQ_ERR_UNSUPPORTED",
           3: "FQ_ERR_NOT_POSITIVE_DEFINITE", 4: "FQ_ERR_NONFINITE",
           5: "FQ_ERR_WORKSPACE_TOO_SMALL", 6: "FQ_ERR_HIP"}
 
+
+
+class TFF(ctypes.Structure):
+    """struct fq_tff: a tight fusion frame given by (d, k, rho) and its rotation factors."""
+    _fields_ = [("d", ctypes.c_int64), ("k", ctypes.c_int64), ("rho", ctypes.c_int64),
+                ("R1", ctypes.c_void_p), ("d1", ctypes.c_int64),
+                ("R2", ctypes.c_void_p), ("d2", ctypes.c_int64)]
+
+
+_tp = ctypes.POINTER(TFF)
+
 # exported symbols of include/fq.h: name -> (restype, argtypes)
 _vp, _i64, _i, _sz, _d = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t, ctypes.c_double
 SIGNATURES = {
@@ -38,6 +49,13 @@ SIGNATURES = {
     "fq_frame_apply": (_i, [_vp, _vp, _i, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _i64,
                             _vp, _vp, _vp, _sz]),
     "fq_frame_apply_workspace_bytes": (_sz, [_i64, _i64, _i64]),
+    "fq_tff_analysis": (_i, [_vp, _vp, _i, _i64, _i64, _tp, _vp, _vp, _sz]),
+    "fq_tff_analysis_workspace_bytes": (_sz, [_i64, _tp]),
+    "fq_tff_synthesis": (_i, [_vp, _vp, _i64, _tp, _vp, _vp, _sz]),
+    "fq_tff_synthesis_workspace_bytes": (_sz, [_i64, _tp]),
+    "fq_frame_apply_tff": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _vp, _vp, _tp, _tp, _vp, _vp,
+                                _sz]),
+    "fq_frame_apply_tff_workspace_bytes": (_sz, [_tp, _tp]),
     "fq_status_string": (ctypes.c_char_p, [_i]),
     "fq_last_error": (ctypes.c_char_p, []),
     "fq_profile_enable": (None, [_i]),
@@ -276,4 +294,94 @@ def fq_frame_apply(X, codes, scale, zero, P_out, P_in, Y=None, ws=None, stream=N
     _check(lib().fq_frame_apply(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), d_in,
                                 _ptr(codes), _ptr(scale), _ptr(zero), K_out, K_in, _ptr(P_out),
                                 d_out, _ptr(P_in), _ptr(Y), wp, wb))
+    return Y
+
+
+class Frame:
+    """A tight fusion frame by its construction: dimension d, k subspaces of dimension rho,
+    rotation factors R1 (d1 x d1) and R2 (d2 x d2) as fp32 device tensors, d1 * d2 = d.
+    Keeps the factor tensors alive while the descriptor is in use."""
+
+    def __init__(self, d, k, rho, R1, R2):
+        torch = _torch()
+        _dev(R1, "R1", torch.float32)
+        _dev(R2, "R2", torch.float32)
+        if R1.dim() != 2 or R1.shape[0] != R1.shape[1] or R2.dim() != 2 or R2.shape[0] != R2.shape[1]:
+            raise ValueError("R1 and R2 must be square")
+        self.d, self.k, self.rho = int(d), int(k), int(rho)
+        self.R1, self.R2 = R1, R2
+        self.c = TFF(self.d, self.k, self.rho, R1.data_ptr(), R1.shape[0], R2.data_ptr(),
+                     R2.shape[0])
+
+    @property
+    def K(self):
+        return self.k * self.rho
+
+
+def fq_tff_analysis_workspace_bytes(n, frame: Frame) -> int:
+    return lib().fq_tff_analysis_workspace_bytes(n, ctypes.byref(frame.c))
+
+
+def fq_tff_synthesis_workspace_bytes(n, frame: Frame) -> int:
+    return lib().fq_tff_synthesis_workspace_bytes(n, ctypes.byref(frame.c))
+
+
+def fq_frame_apply_tff_workspace_bytes(frame_out: Frame, frame_in: Frame) -> int:
+    return lib().fq_frame_apply_tff_workspace_bytes(ctypes.byref(frame_out.c),
+                                                    ctypes.byref(frame_in.c))
+
+
+def fq_tff_analysis(X, frame: Frame, U=None, ws=None, stream=None):
+    """U = X P (rows P^T x) with P given by its construction."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1 or not X.is_cuda:
+        raise ValueError("X must be a 2-D device tensor with unit column stride")
+    n = X.shape[0]
+    if X.shape[1] != frame.d:
+        raise ValueError("X must have d columns")
+    if U is None:
+        U = torch.empty((n, frame.K), dtype=torch.float32, device=X.device)
+    _dev(U, "U", torch.float32, (n, frame.K))
+    ws, wp, wb = _ws(fq_tff_analysis_workspace_bytes(n, frame), ws, X.device)
+    _check(lib().fq_tff_analysis(_stream(stream), _ptr(X), _dt(X), n, X.stride(0),
+                                 ctypes.byref(frame.c), _ptr(U), wp, wb))
+    return U
+
+
+def fq_tff_synthesis(V, frame: Frame, Y=None, ws=None, stream=None):
+    """Y = V P^T (rows P v) with P given by its construction."""
+    torch = _torch()
+    _dev(V, "V", torch.float32)
+    if V.dim() != 2 or V.shape[1] != frame.K:
+        raise ValueError("V must be n x (k rho)")
+    n = V.shape[0]
+    if Y is None:
+        Y = torch.empty((n, frame.d), dtype=torch.float32, device=V.device)
+    _dev(Y, "Y", torch.float32, (n, frame.d))
+    ws, wp, wb = _ws(fq_tff_synthesis_workspace_bytes(n, frame), ws, V.device)
+    _check(lib().fq_tff_synthesis(_stream(stream), _ptr(V), n, ctypes.byref(frame.c), _ptr(Y),
+                                  wp, wb))
+    return Y
+
+
+def fq_frame_apply_tff(X, codes, scale, zero, frame_out: Frame, frame_in: Frame, Y=None, ws=None,
+                       stream=None):
+    """Y = X Theta^T from the codes, both frames given by their construction."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1 or not X.is_cuda:
+        raise ValueError("X must be a 2-D device tensor with unit column stride")
+    n, d_in = X.shape
+    if d_in != frame_in.d:
+        raise ValueError("X must have frame_in.d columns")
+    K_out, K_in = frame_out.K, frame_in.K
+    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    if Y is None:
+        Y = torch.empty((n, frame_out.d), dtype=torch.float32, device=X.device)
+    _dev(Y, "Y", torch.float32, (n, frame_out.d))
+    ws, wp, wb = _ws(fq_frame_apply_tff_workspace_bytes(frame_out, frame_in), ws, X.device)
+    _check(lib().fq_frame_apply_tff(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), _ptr(codes),
+                                    _ptr(scale), _ptr(zero), ctypes.byref(frame_out.c),
+                                    ctypes.byref(frame_in.c), _ptr(Y), wp, wb))
     return Y

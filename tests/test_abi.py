@@ -90,3 +90,38 @@ def test_invalid_arguments_rejected_before_launch(L):
     assert L.fq_quantize_prepare(n, n, 0, 5, 128, 0.01, n, 0) == 0
     assert L.fq_quantize_apply(n, n, 5, 0, 2, 128, 2.0, n, n, n, n, 0) == 0
     assert L.fq_frame_synthesis(n, n, n, n, 5, 5, n, 0, n, 5, n, n, 0) == 0
+
+
+def test_tff_frames_validated_before_launch(L):
+    """Structured frames: the workspace query answers 0 and every entry point returns its
+    status before any launch for frames outside the supported set."""
+    from paper_2403_06082_amd.fq import TFF
+    p, n = ctypes.c_void_p(64), None
+    good = TFF(4096, 282, 16, 64, 64, 64, 64)
+    assert L.fq_tff_analysis_workspace_bytes(1, ctypes.byref(good)) >= 4096 * 4
+    assert L.fq_frame_apply_tff_workspace_bytes(ctypes.byref(good), ctypes.byref(good)) > 0
+    cases = [
+        (TFF(4096, 282, 15, 64, 64, 64, 64), 1),     # odd rho
+        (TFF(4096, 282, 24, 64, 64, 64, 64), 2),     # d not divisible by rho
+        (TFF(4096, 200, 16, 64, 64, 64, 64), 1),     # d / rho > k: modulation not tight
+        (TFF(4096, 282, 16, 64, 64, 64, 32), 1),     # d1 d2 != d
+        (TFF(4096, 282, 16, None, 64, 64, 64), 1),   # NULL rotation factor
+        (TFF(4096, 4000, 2, 64, 64, 64, 64), 2),     # k above the LDS limit
+        (TFF(8192, 600, 16, 64, 1, 64, 8192), 2),    # d2 above the LDS limit
+    ]
+    for f, st in cases:
+        fp = ctypes.byref(f)
+        if f.R1 is not None:
+            assert L.fq_tff_analysis_workspace_bytes(1, fp) == 0
+        assert L.fq_tff_analysis(n, p, 0, 1, 4096, fp, p, p, 1 << 30) == st
+        assert L.fq_tff_synthesis(n, p, 1, fp, p, p, 1 << 30) == st
+        assert L.fq_frame_apply_tff(n, p, 0, 1, 4096, p, p, p, fp, ctypes.byref(good), p, p,
+                                    1 << 30) == st
+        assert b"frame" in L.fq_last_error()
+    # ldx < d, bad dtype, empty input, too small a workspace
+    gp = ctypes.byref(good)
+    assert L.fq_tff_analysis(n, p, 0, 1, 4095, gp, p, p, 1 << 30) == 1
+    assert L.fq_tff_analysis(n, p, 5, 1, 4096, gp, p, p, 1 << 30) == 1
+    assert L.fq_tff_analysis(n, n, 0, 0, 4096, gp, n, n, 0) == 0
+    assert L.fq_tff_analysis(n, p, 0, 1, 4096, gp, p, p, 64) == 5
+    assert L.fq_frame_apply_tff(n, p, 0, 1, 4096, p, p, p, gp, gp, p, p, 64) == 5

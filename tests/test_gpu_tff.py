@@ -1,0 +1,169 @@
+"""Structured frames on the device (fq_tff_analysis, fq_tff_synthesis, fq_frame_apply_tff)
+against the oracle's operators applied with the dense float64 frame that the input
+generator builds from the same (k, rho, d) and rotation seed.
+
+Tolerance (relative Frobenius): the device takes the rotation factors in fp32 and each
+step is an fp32 sum (d1 + d2 terms for the rotation, m or k terms for the DFT blocks) with
+fp32 twiddles, a few x 2^-24 sqrt(terms) per step: 1e-5 on small shapes; 1e-4 for the
+layer outputs at the Llama-7B up_proj shape, the bound the pass's outputs are held to.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from fq_inputs import WORKLOADS, gen, tff
+from fq_testutil import need_gpu, upload, rel_fro
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [(136, 37, 4), (200, 55, 4), (264, 72, 4), (64, 16, 4)]
+
+
+def _frame(torch, fq, d, k, rho, seed):
+    P = tff.parseval_frame(k, rho, d, np.random.SeedSequence(seed))
+    R1, R2 = tff.rotation_factors(d, np.random.SeedSequence(seed))
+    F = fq.Frame(d, k, rho, torch.from_numpy(R1.astype(np.float32)).cuda(),
+                 torch.from_numpy(R2.astype(np.float32)).cuda())
+    return F, P
+
+
+@pytest.mark.parametrize("xdt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", SMALL)
+@pytest.mark.parametrize("n", [1, 5, 300])
+def test_tff_analysis_parity(xdt, shape, n):
+    """U = X P for ragged shapes (d1 x d2 = 8 x 17, 10 x 20, 12 x 22, 8 x 8) and 300
+    vectors (two passes of 256)."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    d, k, rho = shape
+    F, P = _frame(torch, fq, d, k, rho, d + k)
+    rng = np.random.default_rng(n + d)
+    Xs = gen.to_device_storage(rng.standard_normal((n, d)).astype(np.float32), xdt)
+    U = fq.fq_tff_analysis(upload(Xs, xdt), F)
+    torch.cuda.synchronize()
+    Uo = O.frame_analysis_vectors(gen.storage_to_f32(Xs, xdt), P)
+    assert rel_fro(U.cpu().numpy(), Uo) < 1e-5
+
+
+@pytest.mark.parametrize("shape", SMALL)
+@pytest.mark.parametrize("n", [1, 7, 260])
+def test_tff_synthesis_parity(shape, n):
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    d, k, rho = shape
+    F, P = _frame(torch, fq, d, k, rho, d + k)
+    rng = np.random.default_rng(2 * n + d)
+    V = rng.standard_normal((n, k * rho)).astype(np.float32)
+    ws = torch.full((fq.fq_tff_synthesis_workspace_bytes(n, F),), 0xFF, dtype=torch.uint8,
+                    device="cuda")
+    Y = fq.fq_tff_synthesis(torch.from_numpy(V).cuda(), F, ws=ws)
+    torch.cuda.synchronize()
+    Yo = O.frame_synthesis_vectors(V.astype(np.float64), P)
+    assert rel_fro(Y.cpu().numpy(), Yo) < 1e-5
+
+
+def test_tff_round_trip_and_strided_input():
+    """Synthesis after analysis gives X back (Parseval frame); X as a column slice."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    F, _ = _frame(torch, fq, 200, 55, 4, 9)
+    rng = np.random.default_rng(3)
+    wide = torch.from_numpy(rng.standard_normal((9, 232)).astype(np.float32)).cuda()
+    X = wide[:, :200]
+    Y = fq.fq_tff_synthesis(fq.fq_tff_analysis(X, F), F)
+    torch.cuda.synchronize()
+    assert rel_fro(Y.cpu().numpy(), X.cpu().numpy()) < 1e-5
+
+
+def _codes(rng, K_out, K_in):
+    codes = rng.integers(0, 4, size=(K_out, K_in))
+    scale = rng.uniform(0.01, 0.1, K_out).astype(np.float32)
+    zero = rng.integers(0, 4, K_out).astype(np.float32)
+    return codes, scale, zero
+
+
+@pytest.mark.parametrize("xdt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("n", [1, 3, 8, 11])
+def test_frame_apply_tff_parity(xdt, n):
+    """K_in = 148 (a partial code word), K_out = 220; every token-block size and two
+    blocks; a NaN-filled workspace."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    Fo, Po = _frame(torch, fq, 200, 55, 4, 5)
+    Fi, Pi = _frame(torch, fq, 136, 37, 4, 6)
+    rng = np.random.default_rng(7 * n + len(xdt))
+    codes, scale, zero = _codes(rng, 220, 148)
+    Xs = gen.to_device_storage(rng.standard_normal((n, 136)).astype(np.float32), xdt)
+    ws = torch.full((fq.fq_frame_apply_tff_workspace_bytes(Fo, Fi),), 0xFF, dtype=torch.uint8,
+                    device="cuda")
+    words = torch.from_numpy(O.pack2(codes).view(np.int32)).cuda()
+    Y = fq.fq_frame_apply_tff(upload(Xs, xdt), words, torch.from_numpy(scale).cuda(),
+                              torch.from_numpy(zero).cuda(), Fo, Fi, ws=ws)
+    torch.cuda.synchronize()
+    Yo = O.frame_apply(gen.storage_to_f32(Xs, xdt), codes, scale.astype(np.float64),
+                       zero.astype(np.float64), Po, Pi)
+    assert Y.shape == (n, 200)
+    assert rel_fro(Y.cpu().numpy(), Yo) < 1e-5
+
+
+def test_frame_apply_tff_matches_dense_frames():
+    """Same outputs as fq_frame_apply with the fp32 dense frames."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    Fo, Po = _frame(torch, fq, 520, 143, 4, 11)
+    Fi, Pi = _frame(torch, fq, 264, 72, 4, 12)
+    rng = np.random.default_rng(13)
+    codes, scale, zero = _codes(rng, Fo.K, Fi.K)
+    words = torch.from_numpy(O.pack2(codes).view(np.int32)).cuda()
+    sc, ze = torch.from_numpy(scale).cuda(), torch.from_numpy(zero).cuda()
+    X = torch.from_numpy(rng.standard_normal((6, 264)).astype(np.float32)).cuda()
+    Yt = fq.fq_frame_apply_tff(X, words, sc, ze, Fo, Fi)
+    Yd = fq.fq_frame_apply(X, words, sc, ze, torch.from_numpy(gen.frame_f32(Po)).cuda(),
+                           torch.from_numpy(gen.frame_f32(Pi)).cuda())
+    torch.cuda.synchronize()
+    assert rel_fro(Yt.cpu().numpy(), Yd.cpu().numpy().astype(np.float64)) < 1e-5
+
+
+def test_frame_apply_tff_empty_and_errors():
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    Fo, _ = _frame(torch, fq, 64, 16, 4, 1)
+    Fi, _ = _frame(torch, fq, 64, 16, 4, 2)
+    words = torch.zeros((64, 4), dtype=torch.int32, device="cuda")
+    sc = torch.ones(64, device="cuda")
+    X = torch.zeros((0, 64), device="cuda")
+    assert fq.fq_frame_apply_tff(X, words, sc, sc, Fo, Fi).shape == (0, 64)
+    with pytest.raises(ValueError):
+        fq.fq_frame_apply_tff(torch.zeros((2, 63), device="cuda"), words, sc, sc, Fo, Fi)
+    bad = fq.Frame(64, 15, 4, Fo.R1, Fo.R2)          # d / rho = 16 > k = 15
+    with pytest.raises(fq.FQError):
+        fq.fq_tff_analysis(torch.zeros((2, 64), device="cuda"), bad)
+
+
+@pytest.mark.parametrize("n", [1, 8])
+def test_frame_apply_tff_llama7b_up_sampled(n):
+    """The Llama-2-7B up_proj frames (d_out 11008 = 86 x 128, k 757; d_in 4096 = 64 x 64,
+    k 282; rho 16) in the launch configuration the benchmark times; 64 sampled output
+    channels against the oracle with the dense float64 frames."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    wl = WORKLOADS["llama7b"]
+    (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, 1)
+    Fo = fq.Frame(11008, ko, ro, torch.from_numpy(R1o.astype(np.float32)).cuda(),
+                  torch.from_numpy(R2o.astype(np.float32)).cuda())
+    Fi = fq.Frame(4096, ki, ri, torch.from_numpy(R1i.astype(np.float32)).cuda(),
+                  torch.from_numpy(R2i.astype(np.float32)).cuda())
+    Po, Pi = gen.make_frames(wl, 1)
+    rng = np.random.default_rng(50 + n)
+    codes, scale, zero = _codes(rng, Fo.K, Fi.K)
+    Xs = gen.to_device_storage(rng.standard_normal((n, 4096)).astype(np.float32), "bf16")
+    words = torch.from_numpy(O.pack2(codes).view(np.int32)).cuda()
+    Y = fq.fq_frame_apply_tff(upload(Xs, "bf16"), words, torch.from_numpy(scale).cuda(),
+                              torch.from_numpy(zero).cuda(), Fo, Fi)
+    torch.cuda.synchronize()
+    Yg = Y.cpu().numpy()
+    rows = np.sort(rng.choice(11008, 64, replace=False))
+    Yo = O.frame_apply(gen.storage_to_f32(Xs, "bf16"), codes, scale.astype(np.float64),
+                       zero.astype(np.float64), Po[rows], Pi)
+    assert rel_fro(Yg[:, rows], Yo) < 1e-4
+    assert np.isfinite(Yg).all()

@@ -249,6 +249,36 @@ def test_synthesis_inverts_analysis_at_r1():
     np.testing.assert_allclose(D2, O.dequant(codes, scale, zero), atol=1e-12)
 
 
+def test_frame_operators_parseval_and_adjoint():
+    """For a Parseval fusion frame the frame operator (synthesis after analysis) is the
+    identity and analysis preserves the norm; synthesis is the adjoint of analysis
+    (<P^T x, u> = <x, P u>); analysis after synthesis is the orthogonal projection onto
+    the range of P^T (idempotent, and the identity on analysed vectors).  An orthonormal
+    basis (k = 1, rho = d, no rotation) gives U = X, written out entry by entry."""
+    rng = _rng(41)
+    P = tff.parseval_frame(37, 4, 136, np.random.SeedSequence(6))      # 136 x 148, r > 1
+    X = rng.standard_normal((5, 136))
+    U = O.frame_analysis_vectors(X, P)
+    assert U.shape == (5, 148)
+    np.testing.assert_allclose(O.frame_synthesis_vectors(U, P), X, atol=1e-12)
+    np.testing.assert_allclose(np.linalg.norm(U, axis=1), np.linalg.norm(X, axis=1), rtol=1e-12)
+    V = rng.standard_normal((5, 148))
+    Y = O.frame_synthesis_vectors(V, P)
+    np.testing.assert_allclose(np.sum(U * V, axis=1), np.sum(X * Y, axis=1), rtol=1e-10)
+    proj = O.frame_analysis_vectors(Y, P)
+    np.testing.assert_allclose(O.frame_analysis_vectors(O.frame_synthesis_vectors(proj, P), P),
+                               proj, atol=1e-12)
+    np.testing.assert_allclose(O.frame_analysis_vectors(O.frame_synthesis_vectors(U, P), P), U,
+                               atol=1e-12)
+    assert np.linalg.norm(proj - V) > 0.1          # r > 1: a proper projection
+    E = tff.parseval_frame(1, 6, 6, rotate=False)
+    Xs = rng.standard_normal((2, 6))
+    Ue = O.frame_analysis_vectors(Xs, E)
+    for t in range(2):
+        for j in range(6):
+            assert abs(Ue[t, j] - Xs[t, j]) < 1e-15
+
+
 def test_frame_apply_identity_frames_brute_force():
     """With identity frames the layer output is the plain quantized matmul, written out
     entry by entry here; with random frames it matches the product taken in the other
