@@ -182,6 +182,87 @@ def apply_bytes(nt, d_out, d_in, K_out, K_in, x_bytes):
             "apply_out": blocks * d_out * K_out * 4 + nt * d_out * 4}
 
 
+def apply_tff_bytes(nt, d_out, d_in, K_out, K_in, x_bytes, rot_floats):
+    """Algorithmic HBM bytes of one fq_frame_apply_tff call: the codes + scale + zero once
+    per block of up to 8 tokens, the rotation factors, X read and Y written once (the frames
+    themselves are never read)."""
+    blocks = -(-nt // 8)
+    nwords = -(-K_in // 16)
+    return (blocks * (K_out * nwords * 4 + 2 * K_out * 4) + rot_floats * 4 + nt * d_in * x_bytes
+            + nt * d_out * 4)
+
+
+def _time_calls(torch, call, stream, iters):
+    for _ in range(10):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(iters):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / iters
+
+
+def _kernel_us(fq, torch, call, names, iters):
+    fq.fq_profile_reset()
+    fq.fq_profile_enable(True)
+    for _ in range(iters):
+        call()
+    torch.cuda.synchronize()
+    fq.fq_profile_enable(False)
+    out = {}
+    for name in names:
+        cnt, tot = fq.fq_profile_query(name)
+        out[name] = {"launches_per_call": cnt / iters, "us_per_call": round(tot * 1e3 / iters, 2)}
+    fq.fq_profile_reset()
+    return out
+
+
+def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), iters=200):
+    """fq_frame_apply_tff: the same layer outputs with both frames applied from their
+    construction (rotation factors + DFT blocks), for 1 and 8 tokens."""
+    from fq_inputs import gen
+    L = wl.layers[li]
+    (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, li)
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    Fo = fq.Frame(L.d_out, ko, ro, up(R1o), up(R2o))
+    Fi = fq.Frame(L.d_in, ki, ri, up(R1i), up(R2i))
+    assert (Fo.K, Fi.K) == (K_out, K_in)
+    rot_floats = sum(r.size for r in (R1o, R2o, R1i, R2i))
+    stream = torch.cuda.current_stream()
+    ws = torch.empty(fq.fq_frame_apply_tff_workspace_bytes(Fo, Fi), dtype=torch.uint8, device="cuda")
+    rows = []
+    for nt in tokens:
+        X = dev["X"][:nt]
+        Y = torch.empty((nt, L.d_out), dtype=torch.float32, device="cuda")
+
+        def call():
+            fq.fq_frame_apply_tff(X, bufs.codes, bufs.scale, bufs.zero, Fo, Fi, Y=Y, ws=ws,
+                                  stream=stream)
+
+        us = _time_calls(torch, call, stream, iters)
+        kern = _kernel_us(fq, torch, call, ("tff_rotate", "tff_dft", "apply_codes"), iters)
+        b = apply_tff_bytes(nt, L.d_out, L.d_in, K_out, K_in, dev["X"].element_size(), rot_floats)
+        kc = kern["apply_codes"]
+        kc["algorithmic_bytes"] = -(-nt // 8) * (K_out * (-(-K_in // 16)) * 4 + 2 * K_out * 4)
+        kc["GB/s"] = round(kc["algorithmic_bytes"] / kc["us_per_call"] / 1e3, 1)
+        rows.append({"tokens": nt, "us_per_call": round(us, 2),
+                     "tokens_per_s": round(nt / (us / 1e6), 1), "algorithmic_bytes": b,
+                     "GB/s": round(b / us / 1e3, 1), "kernels": kern})
+        print(f"[bench] frame_apply_tff {nt} token(s): {us:.1f} us/call", file=sys.stderr, flush=True)
+    return {"op": "fq_frame_apply_tff: the same outputs with P_in and P_l applied from their "
+                  "construction (Kronecker rotation factors + length-k DFT blocks); no frame "
+                  "matrix is read",
+            "frames": {"out": {"d": L.d_out, "k": ko, "rho": ro, "d1": R1o.shape[0], "d2": R2o.shape[0]},
+                       "in": {"d": L.d_in, "k": ki, "rho": ri, "d1": R1i.shape[0], "d2": R2i.shape[0]}},
+            "per_tokens": rows,
+            "note": "about 7.6e7 FMAs per token (5.5e7 in the code GEMV) and 13.8 MB of codes "
+                    "per block of 8 tokens: bound by launch and memory latency at 1 token, by "
+                    "the code kernel's VALU work at 8"}
+
+
 def inference_bench(fq, torch, dev, bufs, L, K_out, K_in, tokens=(1, 8), iters=200):
     """Layer outputs Y = X Theta^T from the pass's own codes and the frames (fq_frame_apply),
     for 1 and 8 tokens (rows of the calibration activations), timed with HIP events on the
@@ -460,6 +541,7 @@ def main():
         "kernel_ms_total_per_step": round(tot_all / args.steps, 3),
     }
     inf = inference_bench(fq, torch, dev, bufs, L, K_out, K_in)
+    inf["structured"] = structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in)
     out["inference"] = inf
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)

@@ -110,7 +110,8 @@ __global__ __launch_bounds__(AT) void k_apply_in_reduce(const float* __restrict_
 // same size, since |q|, |q - zero| <= 3).  A work-group owns 16 rows (4 per wave); U goes
 // through LDS UCH(NT) columns at a time (at most 32 KB), and the work-group sums each token's U
 // while staging it.  A lane takes code words w = lane, lane + 64, ... of its wave's 4
-// rows (loaded for the whole chunk before the chunk of U is staged).  A word is spread
+// rows; the first chunk's words are loaded right after its U, each later chunk's words one
+// chunk ahead, and LDS-only barriers keep them in flight meanwhile.  A word is spread
 // into bytes, (word >> 2b) & 0x03030303 holding the codes of columns b, b+4, b+8, b+12,
 // and each byte converts to float in one instruction.  In LDS, group g (4 columns) of
 // word w sits at group (g + w/2) mod 4 of the word's 16 columns, so that 8 lanes reading
@@ -122,7 +123,9 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
                                                     const float* __restrict__ scale,
                                                     const float* __restrict__ zero,
                                                     float* __restrict__ V) {
-  constexpr int UCH = NT <= 4 ? 2048 : 8192 / NT;    // columns per chunk (at most 32 KB)
+  // columns per chunk (at most 32 KB of LDS; 2048 for up to 4 tokens keeps the code words
+  // of two chunks in registers)
+  constexpr int UCH = NT <= 4 ? 2048 : 8192 / NT;
   constexpr int WPL = UCH / (16 * 64);       // code words per lane and row in a chunk
   constexpr int SPT = UCH / (4 * AT);        // staging rounds per token
   __shared__ __attribute__((aligned(16))) float us[NT][UCH];
@@ -357,10 +360,8 @@ hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
   hipLaunchKernelGGL(k_apply_in_reduce, dim3((unsigned)(ldu / 64 + (ldu % 64 != 0)), NT), dim3(AT), 0, s,
                      w.part, NT, nt, ks_eff, K_in, ldu, w.U);
   prof_end(s);
-  prof_begin(s, "apply_codes");
-  hipLaunchKernelGGL(k_apply_codes<NT>, dim3((unsigned)((K_out + 15) / 16)), dim3(AT), 0, s,
-                     w.U, ldu, codes, K_out, (K_in + 15) / 16, scale, zero, w.V);
-  prof_end(s);
+  if (hipError_t e = apply_codes(w.U, ldu, nt, codes, K_out, (K_in + 15) / 16, scale, zero, w.V, s); e != hipSuccess)
+    return e;
   prof_begin(s, "apply_out");
   constexpr int R = NT >= 4 ? 8 : 4;
   const dim3 gout((unsigned)((d_out + R - 1) / R));
@@ -379,10 +380,13 @@ hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* code
                        float* V, hipStream_t s) {
   const dim3 g((unsigned)((K_out + 15) / 16));
   prof_begin(s, "apply_codes");
-  if (nt == 1) hipLaunchKernelGGL(k_apply_codes<1>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
-  else if (nt == 2) hipLaunchKernelGGL(k_apply_codes<2>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
-  else if (nt <= 4) hipLaunchKernelGGL(k_apply_codes<4>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
-  else hipLaunchKernelGGL(k_apply_codes<8>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+#define FQ_CODES(N)                                                                              \
+  hipLaunchKernelGGL(k_apply_codes<N>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+  if (nt == 1) { FQ_CODES(1) }
+  else if (nt == 2) { FQ_CODES(2) }
+  else if (nt <= 4) { FQ_CODES(4) }
+  else { FQ_CODES(8) }
+#undef FQ_CODES
   prof_end(s);
   return last_launch_error();
 }
