@@ -237,6 +237,31 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
                              const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes);
 size_t fq_frame_apply_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
 
+/*
+ * Rounding of the frame representation of activations to act_bits-bit integers (appendix
+ * "FrameQuant for Activation Quantization?"): per token t (row of U),
+ * Delta_t = max_j |U_tj| / (2^(act_bits-1) - 1) and Cq_tj = round(U_tj / Delta_t), with
+ * IEEE fp32 divisions and ties to even; a zero row gives Delta_t = 0 and Cq_t = 0.
+ *   U device fp32 n x K row-major; Cq device int8 n x K row-major; delta device fp32 n.
+ *   act_bits in [2, 8].  No workspace.  Errors: FQ_ERR_INVALID_ARG, FQ_ERR_HIP.
+ */
+fq_status fq_act_quantize(void* stream, const float* U, int64_t n, int64_t K, int act_bits,
+                          int8_t* Cq, float* delta);
+
+/*
+ * fq_frame_apply_tff with the inputs' frame representation C = X P_in rounded per token as
+ * fq_act_quantize does (same appendix): Y = (Delta C^ (codes - zero)^T diag(scale)) P_out^T,
+ * where the products with the codes run exactly in integer arithmetic (int32 sums of
+ * int8 x 2-bit terms).  Arguments and errors as fq_frame_apply_tff, plus act_bits in
+ * [2, 8]; ws: fq_frame_apply_tff_actq_workspace_bytes(frame_out, frame_in) bytes.
+ */
+fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n_tokens,
+                                  int64_t ldx, const uint32_t* codes, const float* scale,
+                                  const float* zero, const fq_tff* frame_out,
+                                  const fq_tff* frame_in, int act_bits, float* Y, void* ws,
+                                  size_t ws_bytes);
+size_t fq_frame_apply_tff_actq_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
+
 /* Status text and the calling thread's last error message (never NULL). */
 const char* fq_status_string(int status);
 const char* fq_last_error(void);

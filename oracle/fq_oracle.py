@@ -288,6 +288,35 @@ def frame_apply(X, codes, scale, zero, P_out, P_in):
     return np.asarray(X, dtype=np.float64) @ Wh.T
 
 
+# --------------------------------------------------------------------------- activations
+def activation_rtn(C, bits: int = 8):
+    """Round-to-nearest of the frame representation of activations (appendix "FrameQuant
+    for Activation Quantization?": C^ = round(C / Delta_C), Delta_C = max|C| /
+    (2^(N-1) - 1)), one Delta per token (row of C: the per-token form the same passage
+    names as the one that admits integer matrix products).  The decision is taken in
+    float32, the precision the device computes C in: Delta = float32(max|C_t|) / float32(qmax)
+    and C / Delta are float32 divisions; ties go to even.  A token with max|C_t| = 0 gets
+    Delta = 0 and C^ = 0.  Returns (C^ as int64, Delta as float32)."""
+    C = np.asarray(C, dtype=np.float32)
+    qmax = np.float32(2 ** (bits - 1) - 1)
+    mx = np.max(np.abs(C), axis=1) if C.shape[1] else np.zeros(C.shape[0], np.float32)
+    delta = (mx / qmax).astype(np.float32)
+    Cq = np.zeros(C.shape, dtype=np.int64)
+    nz = delta > 0
+    Cq[nz] = np.rint(C[nz] / delta[nz, None]).astype(np.int64)
+    return Cq, delta
+
+
+def frame_apply_rtn_activations(C, codes, scale, zero, P_out, bits: int = 8):
+    """Layer outputs from the rounded frame representation of the inputs (same appendix;
+    Sec. 3 "Inference Procedure" for the rest): C^, Delta = activation_rtn(C), then
+    V = Delta * C^ (q - zero)^T diag(scale) and Y = V P_l^T, in float64.  C: tokens x K_in
+    (the analysis X P_prev as the device computed it)."""
+    Cq, delta = activation_rtn(C, bits)
+    V = (delta.astype(np.float64)[:, None] * Cq.astype(np.float64)) @ dequant(codes, scale, zero).T
+    return V @ np.asarray(P_out, dtype=np.float64).T
+
+
 # --------------------------------------------------------------------------- pipeline
 def quantize_frames(D, Ht, bits=2, block=128, damp=0.01, clip_sigmas=2.0,
                     forced_codes=None, tie_eps=TIE_EPS):

@@ -854,4 +854,77 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
   return FQ_OK;
 }
 
+// ================================================================ rounded activations
+fq_status fq_act_quantize(void* stream, const float* U, int64_t n, int64_t K, int act_bits,
+                          int8_t* Cq, float* delta) {
+  if (act_bits < 2 || act_bits > 8) return fail(FQ_ERR_INVALID_ARG, "act_bits must be in [2, 8]");
+  if (!dim_ok(n) || !dim_ok(K)) return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
+  if (n == 0) return FQ_OK;
+  if (!U || !Cq || !delta) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  hipError_t e = act_quantize(U, K, n, K, act_bits, Cq, K, false, delta, nullptr, (hipStream_t)stream);
+  return e == hipSuccess ? FQ_OK : hip_fail(e, "activation rounding");
+}
+
+struct ApplyActqLayout { ApplyTffLayout base; int8_t* Cq; float* delta; int* csum; };
+
+static size_t apply_actq_layout(const fq_tff* fo, const fq_tff* fi, void* base, ApplyActqLayout* L) {
+  ApplyActqLayout l{};
+  const size_t head = apply_tff_layout(fo, fi, base, &l.base);      // includes 256 of slack
+  const int64_t nwords = (fi->k * fi->rho + 15) / 16;
+  Carver c(base ? (char*)base + head : nullptr);
+  l.Cq = c.take<int8_t>((size_t)(APPLY_NT * 16 * nwords));
+  l.delta = c.take<float>(APPLY_NT);
+  l.csum = c.take<int>(APPLY_NT);
+  if (L) *L = l;
+  return head + c.off + 256;
+}
+
+size_t fq_frame_apply_tff_actq_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in) {
+  if (!tff_dims_ok(frame_out) || !tff_dims_ok(frame_in)) return 0;
+  return apply_actq_layout(frame_out, frame_in, nullptr, nullptr);
+}
+
+fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n_tokens,
+                                  int64_t ldx, const uint32_t* codes, const float* scale,
+                                  const float* zero, const fq_tff* frame_out,
+                                  const fq_tff* frame_in, int act_bits, float* Y, void* ws,
+                                  size_t ws_bytes) {
+  if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (act_bits < 2 || act_bits > 8) return fail(FQ_ERR_INVALID_ARG, "act_bits must be in [2, 8]");
+  if (!dim_ok(n_tokens)) return fail(FQ_ERR_INVALID_ARG, "n_tokens must be in [0, 2^30)");
+  TffDev Fo, Fi;
+  fq_status st = tff_check(frame_out, "frame_out", &Fo);
+  if (st != FQ_OK) return st;
+  if ((st = tff_check(frame_in, "frame_in", &Fi)) != FQ_OK) return st;
+  if (ldx < Fi.d) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d_in");
+  if (n_tokens == 0) return FQ_OK;
+  if (!X || !codes || !scale || !zero || !Y) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  if (ws_bytes < apply_actq_layout(frame_out, frame_in, nullptr, nullptr))
+    return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_apply_tff_actq_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  ApplyActqLayout L;
+  apply_actq_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  const int64_t K_in = Fi.k * Fi.rho, K_out = Fo.k * Fo.rho;
+  const int64_t ldu = (K_in + 15) / 16 * 16, nwords = (K_in + 15) / 16;
+  hipError_t e;
+  if ((e = tff_transpose_r2(Fo, L.base.r2t, s)) != hipSuccess) return hip_fail(e, "transpose R2");
+  const int esz = xt == FQ_F32 ? 4 : 2;
+  for (int64_t t0 = 0; t0 < n_tokens; t0 += APPLY_NT) {
+    const int nt = (int)std::min<int64_t>(APPLY_NT, n_tokens - t0);
+    if ((e = tff_analysis((const char*)X + t0 * ldx * esz, xt, ldx, nt, Fi, L.base.y, L.base.U, ldu, s)) !=
+        hipSuccess)
+      return hip_fail(e, "tff analysis");
+    if ((e = act_quantize(L.base.U, ldu, nt, K_in, act_bits, L.Cq, 16 * nwords, true, L.delta, L.csum, s)) !=
+        hipSuccess)
+      return hip_fail(e, "activation rounding");
+    if ((e = apply_codes_i8(L.Cq, 16 * nwords, L.delta, L.csum, nt, codes, K_out, nwords, scale, zero,
+                            L.base.V, s)) != hipSuccess)
+      return hip_fail(e, "apply codes");
+    if ((e = tff_synthesis(L.base.V, K_out, nt, Fo, L.base.r2t, L.base.z, Y + t0 * Fo.d, Fo.d, s)) != hipSuccess)
+      return hip_fail(e, "tff synthesis");
+  }
+  return FQ_OK;
+}
+
 }  // extern "C"

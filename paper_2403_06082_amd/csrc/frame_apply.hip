@@ -253,6 +253,163 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
   }
 }
 
+// ---- rounded activations (appendix "FrameQuant for Activation Quantization?"): per token
+// t, Delta_t = max_j |U[t][j]| / qmax and Cq[t][j] = round(U[t][j] / Delta_t) (IEEE fp32
+// divisions, ties to even; Delta_t = 0 gives a zero row).  One 1024-thread work-group per
+// token.
+// PERM stores each 16-column word's bytes in the order of the spread code words: column
+// 16w + 4g + b at byte 16w + 4b + g (columns [K, ldc) zero); otherwise column j at byte j.
+// csum (optional) receives sum_j Cq[t][j].
+constexpr int QT = 1024;       // threads per token in the activation rounding kernel
+
+template <bool PERM>
+__global__ __launch_bounds__(QT) void k_act_quantize(const float* __restrict__ U, int64_t ldu,
+                                                     int64_t K, float qmax,
+                                                     int8_t* __restrict__ Cq, int64_t ldc,
+                                                     float* __restrict__ delta,
+                                                     int* __restrict__ csum) {
+  __shared__ float wmax[QT / 64];
+  __shared__ int wsum[QT / 64];
+  const int64_t t = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float* u = U + t * ldu;
+  float mx = 0.f;
+#pragma unroll 4
+  for (int64_t j = threadIdx.x; j < K; j += QT) mx = fmaxf(mx, fabsf(u[j]));
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if (lane == 0) wmax[wave] = mx;
+  __syncthreads();
+  mx = 0.f;
+#pragma unroll
+  for (int w = 0; w < QT / 64; ++w) mx = fmaxf(mx, wmax[w]);
+  const float dl = mx / qmax;
+  int sum = 0;
+#pragma unroll 4
+  for (int64_t j = threadIdx.x; j < ldc; j += QT) {
+    int q = 0;
+    if (j < K && dl > 0.f) q = (int)rintf(u[j] / dl);
+    sum += q;
+    const int64_t dst = PERM ? (j & ~(int64_t)15) + 4 * (j & 3) + ((j >> 2) & 3) : j;
+    Cq[t * ldc + dst] = (int8_t)q;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+  if (lane == 0) wsum[wave] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    delta[t] = dl;
+    if (csum) {
+      int total = 0;
+      for (int w = 0; w < QT / 64; ++w) total += wsum[w];
+      csum[t] = total;
+    }
+  }
+}
+
+// V[t][i] = scale_i Delta_t (sum_j Cq[t][j] q_ij - zero_i sum_j Cq[t][j]), the dot product
+// exact in int32 (|sum| <= 3 * 127 * K_in).  Same work split as k_apply_codes: 16 rows per
+// work-group, 4 per wave, lanes over code words; Cq (PERM layout, ldc = 16 nwords bytes)
+// goes through LDS CW words at a time, and each word's spread codes meet the matching 4
+// dwords of Cq in 4 v_dot4 per row and token.
+template <int NT>
+__global__ __launch_bounds__(AT) void k_apply_codes_i8(const int8_t* __restrict__ Cq,
+                                                       int64_t ldc,
+                                                       const float* __restrict__ delta,
+                                                       const int* __restrict__ csum,
+                                                       const uint32_t* codes, int64_t K_out,
+                                                       int64_t nwords,
+                                                       const float* __restrict__ scale,
+                                                       const float* __restrict__ zero,
+                                                       float* __restrict__ V) {
+  constexpr int CW = NT >= 8 ? 128 : 256;    // words per chunk (NT * CW * 16 bytes <= 16 KB)
+  constexpr int WPL = CW / 64;               // code words per lane and row in a chunk
+  __shared__ uint4 cs[NT][CW];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row0 = (int64_t)blockIdx.x * 16 + wave * 4;
+  int acc[4][NT];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[r][t] = 0;
+  const uint32_t* crow[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) crow[r] = codes + min(row0 + r, K_out - 1) * nwords;
+  auto load_words = [&](uint32_t (&dst)[4][WPL], int64_t w0) {
+    const int nw = (int)min((int64_t)CW, nwords - w0);
+#pragma unroll
+    for (int k = 0; k < WPL; ++k) {
+      const int w = lane + 64 * k;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[r][k] = crow[r][w0 + min(w, nw - 1)];
+    }
+  };
+  uint32_t wd[4][WPL], wn[4][WPL] = {};
+  const uint4* src = reinterpret_cast<const uint4*>(Cq);
+  const int64_t ldq = ldc / 16;              // uint4 per token row
+  for (int64_t w0 = 0; w0 < nwords; w0 += CW) {
+    const int nw = (int)min((int64_t)CW, nwords - w0);
+    lds_barrier();                          // the previous chunk's reads of cs are done
+    uint4 cv[NT * CW / AT];
+#pragma unroll
+    for (int e = 0; e < NT * CW / AT; ++e) {
+      const int f = e * AT + (int)threadIdx.x, t = f / CW, w = f - t * CW;
+      cv[e] = src[t * ldq + w0 + min(w, nw - 1)];
+    }
+    if (w0 == 0) load_words(wd, 0);
+#pragma unroll
+    for (int e = 0; e < NT * CW / AT; ++e) {
+      const int f = e * AT + (int)threadIdx.x, t = f / CW, w = f - t * CW;
+      cs[t][w] = cv[e];
+    }
+    lds_barrier();
+    if (w0 + CW < nwords) load_words(wn, w0 + CW);   // in flight during this chunk's work
+#pragma unroll
+    for (int k = 0; k < WPL; ++k) {
+      const int w = lane + 64 * k;
+      if (w >= nw) break;
+      uint32_t y[4][4];                     // byte g of y[r][b]: code of column 4g + b
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) y[r][b] = (wd[r][k] >> (2 * b)) & 0x03030303u;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const uint4 d = cs[t][w];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][0], (int)d.x, acc[r][t], false);
+          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][1], (int)d.y, acc[r][t], false);
+          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][2], (int)d.z, acc[r][t], false);
+          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][3], (int)d.w, acc[r][t], false);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int k = 0; k < WPL; ++k) wd[r][k] = wn[r][k];
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r][t] += __shfl_xor(acc[r][t], o);
+  if (lane == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t i = row0 + r;
+      if (i < K_out) {
+        const float sc = scale[i], z = zero[i];
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          V[t * K_out + i] = sc * delta[t] * fmaf(-z, (float)csum[t], (float)acc[r][t]);
+      }
+    }
+  }
+}
+
 // ---- step 3: Y[t][o] = sum_i V[t][i] P_out[o][i]
 // A work-group owns R output rows; a thread owns 4 consecutive columns of every 4 AT-wide
 // chunk of P_out's rows (each V element is read once per work-group).
@@ -387,6 +544,36 @@ hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* code
   else if (nt <= 4) { FQ_CODES(4) }
   else { FQ_CODES(8) }
 #undef FQ_CODES
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t act_quantize(const float* U, int64_t ldu, int64_t n, int64_t K, int bits,
+                        int8_t* Cq, int64_t ldc, bool perm, float* delta, int* csum,
+                        hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const float qmax = (float)((1 << (bits - 1)) - 1);
+  prof_begin(s, "act_quantize");
+  if (perm)
+    hipLaunchKernelGGL(k_act_quantize<true>, dim3((unsigned)n), dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
+  else
+    hipLaunchKernelGGL(k_act_quantize<false>, dim3((unsigned)n), dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t apply_codes_i8(const int8_t* Cq, int64_t ldc, const float* delta, const int* csum,
+                          int nt, const uint32_t* codes, int64_t K_out, int64_t nwords,
+                          const float* scale, const float* zero, float* V, hipStream_t s) {
+  const dim3 g((unsigned)((K_out + 15) / 16));
+  prof_begin(s, "apply_codes");
+#define FQ_CODES_I8(N) \
+  hipLaunchKernelGGL(k_apply_codes_i8<N>, g, dim3(AT), 0, s, Cq, ldc, delta, csum, codes, K_out, nwords, scale, zero, V);
+  if (nt == 1) { FQ_CODES_I8(1) }
+  else if (nt == 2) { FQ_CODES_I8(2) }
+  else if (nt <= 4) { FQ_CODES_I8(4) }
+  else { FQ_CODES_I8(8) }
+#undef FQ_CODES_I8
   prof_end(s);
   return last_launch_error();
 }

@@ -56,6 +56,10 @@ SIGNATURES = {
     "fq_frame_apply_tff": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _vp, _vp, _tp, _tp, _vp, _vp,
                                 _sz]),
     "fq_frame_apply_tff_workspace_bytes": (_sz, [_tp, _tp]),
+    "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
+    "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _vp, _vp, _tp, _tp, _i, _vp,
+                                     _vp, _sz]),
+    "fq_frame_apply_tff_actq_workspace_bytes": (_sz, [_tp, _tp]),
     "fq_status_string": (ctypes.c_char_p, [_i]),
     "fq_last_error": (ctypes.c_char_p, []),
     "fq_profile_enable": (None, [_i]),
@@ -384,4 +388,51 @@ def fq_frame_apply_tff(X, codes, scale, zero, frame_out: Frame, frame_in: Frame,
     _check(lib().fq_frame_apply_tff(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), _ptr(codes),
                                     _ptr(scale), _ptr(zero), ctypes.byref(frame_out.c),
                                     ctypes.byref(frame_in.c), _ptr(Y), wp, wb))
+    return Y
+
+
+def fq_act_quantize(U, act_bits=8, Cq=None, delta=None, stream=None):
+    """Per-token rounding of U (n x K fp32) to act_bits-bit integers: (Cq int8, delta)."""
+    torch = _torch()
+    _dev(U, "U", torch.float32)
+    if U.dim() != 2:
+        raise ValueError("U must be 2-D")
+    n, K = U.shape
+    if Cq is None:
+        Cq = torch.empty((n, K), dtype=torch.int8, device=U.device)
+    if delta is None:
+        delta = torch.empty((n,), dtype=torch.float32, device=U.device)
+    _dev(Cq, "Cq", torch.int8, (n, K))
+    _dev(delta, "delta", torch.float32, (n,))
+    _check(lib().fq_act_quantize(_stream(stream), _ptr(U), n, K, act_bits, _ptr(Cq), _ptr(delta)))
+    return Cq, delta
+
+
+def fq_frame_apply_tff_actq_workspace_bytes(frame_out: Frame, frame_in: Frame) -> int:
+    return lib().fq_frame_apply_tff_actq_workspace_bytes(ctypes.byref(frame_out.c),
+                                                         ctypes.byref(frame_in.c))
+
+
+def fq_frame_apply_tff_actq(X, codes, scale, zero, frame_out: Frame, frame_in: Frame, act_bits=8,
+                            Y=None, ws=None, stream=None):
+    """fq_frame_apply_tff with the inputs' frame representation rounded per token to
+    act_bits-bit integers and the code products in integer arithmetic."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1 or not X.is_cuda:
+        raise ValueError("X must be a 2-D device tensor with unit column stride")
+    n, d_in = X.shape
+    if d_in != frame_in.d:
+        raise ValueError("X must have frame_in.d columns")
+    K_out, K_in = frame_out.K, frame_in.K
+    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    if Y is None:
+        Y = torch.empty((n, frame_out.d), dtype=torch.float32, device=X.device)
+    _dev(Y, "Y", torch.float32, (n, frame_out.d))
+    ws, wp, wb = _ws(fq_frame_apply_tff_actq_workspace_bytes(frame_out, frame_in), ws, X.device)
+    _check(lib().fq_frame_apply_tff_actq(_stream(stream), _ptr(X), _dt(X), n, X.stride(0),
+                                         _ptr(codes), _ptr(scale), _ptr(zero),
+                                         ctypes.byref(frame_out.c), ctypes.byref(frame_in.c),
+                                         act_bits, _ptr(Y), wp, wb))
     return Y

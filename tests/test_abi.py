@@ -125,3 +125,17 @@ def test_tff_frames_validated_before_launch(L):
     assert L.fq_tff_analysis(n, n, 0, 0, 4096, gp, n, n, 0) == 0
     assert L.fq_tff_analysis(n, p, 0, 1, 4096, gp, p, p, 64) == 5
     assert L.fq_frame_apply_tff(n, p, 0, 1, 4096, p, p, p, gp, gp, p, p, 64) == 5
+
+
+def test_act_quantize_arguments(L):
+    p, n = ctypes.c_void_p(64), None
+    assert L.fq_act_quantize(n, p, 4, 8, 1, p, p) == 1
+    assert L.fq_act_quantize(n, p, 4, 8, 9, p, p) == 1
+    assert L.fq_act_quantize(n, n, 0, 8, 8, n, n) == 0
+    assert L.fq_act_quantize(n, n, 4, 8, 8, p, p) == 1
+    from paper_2403_06082_amd.fq import TFF
+    good = ctypes.byref(TFF(4096, 282, 16, 64, 64, 64, 64))
+    assert L.fq_frame_apply_tff_actq_workspace_bytes(good, good) > \
+        L.fq_frame_apply_tff_workspace_bytes(good, good)
+    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, p, p, good, good, 9, p, p, 1 << 30) == 1
+    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, p, p, good, good, 8, p, p, 64) == 5

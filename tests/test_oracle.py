@@ -279,6 +279,50 @@ def test_frame_operators_parseval_and_adjoint():
             assert abs(Ue[t, j] - Xs[t, j]) < 1e-15
 
 
+def test_activation_rtn_hand_cases_and_bounds():
+    """Hand case: row [1, -0.5, 0.25, 0] at 8 bits has Delta = 1/127 and rounds to
+    [127, -64 (a tie: -63.5 goes to even), 32, 0]; at 6 bits qmax is 31.  For random rows
+    the largest magnitude maps to +-qmax, every |C^| <= qmax, and |C - Delta C^| <= Delta/2;
+    a zero row stays zero.  The layer output from C^ equals the product written out with
+    the rounded values, and tends to the unrounded output as the bit width grows."""
+    Cq, d = O.activation_rtn(np.array([[1.0, -0.5, 0.25, 0.0]], np.float32), 8)
+    assert d[0] == np.float32(1.0) / np.float32(127.0)
+    np.testing.assert_array_equal(Cq[0], [127, -64, 32, 0])
+    Cq6, d6 = O.activation_rtn(np.array([[2.0, -1.0]], np.float32), 6)
+    assert d6[0] == np.float32(2.0) / np.float32(31.0)
+    np.testing.assert_array_equal(Cq6[0], [31, -16])
+    rng = _rng(5)
+    C = rng.standard_normal((6, 300)).astype(np.float32)
+    C[3] = 0.0
+    for bits in (6, 8):
+        qmax = 2 ** (bits - 1) - 1
+        Cq, d = O.activation_rtn(C, bits)
+        assert np.all(np.abs(Cq) <= qmax)
+        for t in (0, 1, 2, 4, 5):
+            assert np.abs(Cq[t]).max() == qmax
+            assert np.all(np.abs(C[t] - d[t] * Cq[t]) <= d[t] / 2 * (1 + 1e-6))
+        assert d[3] == 0 and not Cq[3].any()
+    K_out, K_in, d_out = 5, 7, 4
+    codes = rng.integers(0, 4, size=(K_out, K_in))
+    scale = rng.uniform(0.01, 0.2, K_out)
+    zero = rng.integers(0, 4, K_out).astype(np.float64)
+    P_out = rng.standard_normal((d_out, K_out))
+    Cs = rng.standard_normal((2, K_in)).astype(np.float32)
+    Y = O.frame_apply_rtn_activations(Cs, codes, scale, zero, P_out, 8)
+    Cq, d = O.activation_rtn(Cs, 8)
+    for t in range(2):
+        for o in range(d_out):
+            acc = 0.0
+            for i in range(K_out):
+                v = sum(d[t] * Cq[t, j] * scale[i] * (codes[i, j] - zero[i]) for j in range(K_in))
+                acc += v * P_out[o, i]
+            assert abs(Y[t, o] - acc) < 1e-9
+    exact = (Cs.astype(np.float64) @ O.dequant(codes, scale, zero).T) @ P_out.T
+    e8 = np.abs(Y - exact).max()
+    e16 = np.abs(O.frame_apply_rtn_activations(Cs, codes, scale, zero, P_out, 16) - exact).max()
+    assert e16 < e8 / 50
+
+
 def test_frame_apply_identity_frames_brute_force():
     """With identity frames the layer output is the plain quantized matmul, written out
     entry by entry here; with random frames it matches the product taken in the other
