@@ -252,12 +252,34 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
                      "tokens_per_s": round(nt / (us / 1e6), 1), "algorithmic_bytes": b,
                      "GB/s": round(b / us / 1e3, 1), "kernels": kern})
         print(f"[bench] frame_apply_tff {nt} token(s): {us:.1f} us/call", file=sys.stderr, flush=True)
+    # the same with the frame representation of the inputs rounded to 8-bit integers
+    wsq = torch.empty(fq.fq_frame_apply_tff_actq_workspace_bytes(Fo, Fi), dtype=torch.uint8,
+                      device="cuda")
+    qrows = []
+    for nt in tokens:
+        X = dev["X"][:nt]
+        Y = torch.empty((nt, L.d_out), dtype=torch.float32, device="cuda")
+
+        def callq():
+            fq.fq_frame_apply_tff_actq(X, bufs.codes, bufs.scale, bufs.zero, Fo, Fi, 8, Y=Y, ws=wsq,
+                                       stream=stream)
+
+        us = _time_calls(torch, callq, stream, iters)
+        kern = _kernel_us(fq, torch, callq, ("tff_rotate", "tff_dft", "act_quantize", "apply_codes"),
+                          iters)
+        qrows.append({"tokens": nt, "us_per_call": round(us, 2),
+                      "tokens_per_s": round(nt / (us / 1e6), 1), "kernels": kern})
+        print(f"[bench] frame_apply_tff_actq (8-bit activations) {nt} token(s): {us:.1f} us/call",
+              file=sys.stderr, flush=True)
     return {"op": "fq_frame_apply_tff: the same outputs with P_in and P_l applied from their "
                   "construction (Kronecker rotation factors + length-k DFT blocks); no frame "
                   "matrix is read",
             "frames": {"out": {"d": L.d_out, "k": ko, "rho": ro, "d1": R1o.shape[0], "d2": R2o.shape[0]},
                        "in": {"d": L.d_in, "k": ki, "rho": ri, "d1": R1i.shape[0], "d2": R2i.shape[0]}},
             "per_tokens": rows,
+            "int8_activations": {"op": "fq_frame_apply_tff_actq, act_bits 8: the analysis output "
+                                       "rounded per token to int8, code products exact in int32 "
+                                       "(v_dot4)", "per_tokens": qrows},
             "note": "about 7.6e7 FMAs per token (5.5e7 in the code GEMV) and 13.8 MB of codes "
                     "per block of 8 tokens: bound by launch and memory latency at 1 token, by "
                     "the code kernel's VALU work at 8"}
