@@ -13,6 +13,8 @@
 // R comes from a lower Cholesky M of J H J (J reverses the index order): R = J M J.
 #include "fq_internal.h"
 
+#include <algorithm>
+
 namespace fq {
 
 
@@ -995,22 +997,44 @@ hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& 
   return last_launch_error();
 }
 
+// Lower Cholesky factor in place, two-level right-looking: panels of CHOL_PANEL columns are
+// factored block by block (64 columns: the diagonal block by k_potrf64, the rows below by
+// the block's inverse, and the rest of the panel's columns updated at rank 64), then the
+// trailing matrix right of the panel receives one rank-CHOL_PANEL update.  The trailing
+// matrix is thus read and written once per panel instead of once per 64 columns.  Entries
+// above the diagonal inside a panel pick up finite values that are never read.
+constexpr int64_t CHOL_PANEL = 256;
+
 hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s) {
-  for (int64_t k0 = 0; k0 < K; k0 += 64) {
-    const int kb = (int)((K - k0) < 64 ? (K - k0) : 64);
-    prof_begin(s, "chol_potrf");
-    hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(128), 0, s, A, K, k0, kb, Z, flags);
-    prof_end(s);
-    const int64_t rest = K - k0 - kb;
-    if (rest > 0) {
-      // panel below the block: X = A[k0+kb:, k0:k0+kb] L_kk^{-T}, in place (each output tile
-      // reads only its own rows of the panel, all of them before it writes)
+  for (int64_t j0 = 0; j0 < K; j0 += CHOL_PANEL) {
+    const int64_t jb = std::min<int64_t>(CHOL_PANEL, K - j0);
+    for (int64_t k0 = j0; k0 < j0 + jb; k0 += 64) {
+      const int kb = (int)std::min<int64_t>(64, j0 + jb - k0);
+      prof_begin(s, "chol_potrf");
+      hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(128), 0, s, A, K, k0, kb, Z, flags);
+      prof_end(s);
+      const int64_t rest = K - k0 - kb;
+      if (rest <= 0) continue;
+      // column block below the diagonal block: X = A[k0+kb:, k0:k0+kb] L_kk^{-T}, in place
+      // (each output tile reads only its own rows, all of them before it writes)
       double* P = A + (k0 + kb) * K + k0;
       hipError_t e = dgemm(rest, kb, kb, 1.0, 0.0, P, K, Z, 64, true, P, K, false, s,
                            "chol_trsm", 64);
       if (e != hipSuccess) return e;
-      e = dgemm(rest, rest, kb, -1.0, 1.0, P, K, P, K, true, A + (k0 + kb) * K + (k0 + kb), K,
-                true, s, "chol_syrk", 64);
+      // the panel's remaining columns, every row below: A[k0+kb:, k0+kb:j0+jb] -= X X[:w]^T
+      const int64_t w = j0 + jb - (k0 + kb);
+      if (w > 0) {
+        e = dgemm(rest, w, kb, -1.0, 1.0, P, K, P, K, true, A + (k0 + kb) * K + (k0 + kb), K,
+                  false, s, "chol_syrk", 64);
+        if (e != hipSuccess) return e;
+      }
+    }
+    // trailing matrix (lower triangle) right of the panel, at rank jb
+    const int64_t rest = K - j0 - jb;
+    if (rest > 0) {
+      const double* Pp = A + (j0 + jb) * K + j0;
+      hipError_t e = dgemm(rest, rest, jb, -1.0, 1.0, Pp, K, Pp, K, true,
+                           A + (j0 + jb) * K + (j0 + jb), K, true, s, "chol_syrk", 64);
       if (e != hipSuccess) return e;
     }
   }
