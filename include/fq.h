@@ -238,6 +238,19 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
 size_t fq_frame_apply_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
 
 /*
+ * The dense frame P (d x k rho, fp32, row stride ldp >= k rho) generated on the device from
+ * its construction (the appendix on constructing TFFs; the storage appendix notes that only
+ * (k, rho, d) and the rotation need be kept): column s rho + 2c + e of P is the rotated
+ * realified vector of subspace s, base-frame row c, real (e = 0) or imaginary (e = 1) part,
+ * scaled to a Parseval frame; same conventions and supported set as fq_tff_analysis.
+ * ws: fq_tff_materialize_workspace_bytes(frame) bytes, 16-byte aligned.  Errors as
+ * fq_tff_analysis.
+ */
+fq_status fq_tff_materialize(void* stream, const fq_tff* frame, float* P, int64_t ldp, void* ws,
+                             size_t ws_bytes);
+size_t fq_tff_materialize_workspace_bytes(const fq_tff* frame);
+
+/*
  * Rounding of the frame representation of activations to act_bits-bit integers (appendix
  * "FrameQuant for Activation Quantization?"): per token t (row of U),
  * Delta_t = max_j |U_tj| / (2^(act_bits-1) - 1) and Cq_tj = round(U_tj / Delta_t), with

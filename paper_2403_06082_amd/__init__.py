@@ -10,6 +10,7 @@ from .fq import (  # noqa: F401
     Frame, fq_tff_analysis, fq_tff_synthesis, fq_frame_apply_tff, fq_tff_analysis_workspace_bytes,
     fq_tff_synthesis_workspace_bytes, fq_frame_apply_tff_workspace_bytes,
     fq_act_quantize, fq_frame_apply_tff_actq, fq_frame_apply_tff_actq_workspace_bytes,
+    fq_tff_materialize, fq_tff_materialize_workspace_bytes,
     fq_hessian_workspace_bytes, fq_frame_analysis_workspace_bytes,
     fq_quantize_frames_workspace_bytes, fq_frame_synthesis_workspace_bytes,
     fq_profile_enable, fq_profile_reset, fq_profile_query,

@@ -927,4 +927,45 @@ fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n
   return FQ_OK;
 }
 
+// ================================================================ dense frame on the device
+static constexpr int64_t TFF_MAT_COLS = 512;   // frame columns per pass of the materialisation
+
+static size_t tff_mat_layout(const fq_tff* f, void* base, float** Z, float** Pt, float** R2t) {
+  Carver c(base);
+  const int64_t nc = std::min<int64_t>(TFF_MAT_COLS, f->k * f->rho);
+  float* z = c.take<float>((size_t)(nc * f->d));
+  float* pt = c.take<float>((size_t)(nc * f->d));
+  float* r = c.take<float>((size_t)(f->d2 * f->d2));
+  if (Z) *Z = z;
+  if (Pt) *Pt = pt;
+  if (R2t) *R2t = r;
+  return c.off + 256;
+}
+
+size_t fq_tff_materialize_workspace_bytes(const fq_tff* frame) {
+  if (!tff_dims_ok(frame)) return 0;
+  return tff_mat_layout(frame, nullptr, nullptr, nullptr, nullptr);
+}
+
+fq_status fq_tff_materialize(void* stream, const fq_tff* frame, float* P, int64_t ldp, void* ws,
+                             size_t ws_bytes) {
+  TffDev F;
+  fq_status st = tff_check(frame, "frame", &F);
+  if (st != FQ_OK) return st;
+  const int64_t K = F.k * F.rho;
+  if (ldp < K) return fail(FQ_ERR_INVALID_ARG, "ldp must be >= k * rho");
+  if (!P) return fail(FQ_ERR_INVALID_ARG, "NULL P");
+  if (ws_bytes < tff_mat_layout(frame, nullptr, nullptr, nullptr, nullptr))
+    return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_tff_materialize_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  float *Z, *Pt, *R2t;
+  tff_mat_layout(frame, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &Z, &Pt, &R2t);
+  hipError_t e;
+  if ((e = tff_transpose_r2(F, R2t, s)) != hipSuccess) return hip_fail(e, "transpose R2");
+  if ((e = tff_materialize(F, R2t, Z, Pt, std::min<int64_t>(TFF_MAT_COLS, K), P, ldp, s)) != hipSuccess)
+    return hip_fail(e, "materialize");
+  return FQ_OK;
+}
+
 }  // extern "C"

@@ -104,6 +104,10 @@ constexpr int64_t TFF_CHUNK = 256;        // vectors per pass of the stand-alone
 // U (n x ldu, ldu >= k rho, columns beyond k rho set to 0) = X P; y: n x d scratch
 hipError_t tff_analysis(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F,
                         float* y, float* U, int64_t ldu, hipStream_t s);
+// P (d x k rho, row stride ldp) of the frame, nc_max columns at a time; R2t from
+// tff_transpose_r2; Z, Pt: nc_max x d scratch each
+hipError_t tff_materialize(const TffDev& F, const float* R2t, float* Z, float* Pt, int64_t nc_max,
+                           float* P, int64_t ldp, hipStream_t s);
 // R2t (d2 x d2) = R2^T, read by tff_synthesis
 hipError_t tff_transpose_r2(const TffDev& F, float* R2t, hipStream_t s);
 // Y (n x ldy) = V P^T with V n x ldv (ldv even), R2t from tff_transpose_r2; z: n x d scratch

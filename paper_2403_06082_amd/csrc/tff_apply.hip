@@ -214,6 +214,50 @@ unsigned blocks_for(int64_t total) { return (unsigned)((total + TT - 1) / TT); }
 
 size_t rot_lds(int d2) { return (size_t)(d2 + (d2 < RT ? RT / d2 : 1) * d2) * sizeof(float); }
 
+// Columns c0 .. c0 + nc - 1 of T / sqrt(k) as rows of Z (nc x d, complex pairs): column
+// s rho + 2c + e is zero outside the m-block c, where complex coordinate c m + j holds
+// k^(-1/2) w^((c m + j) s) (e = 0) or i k^(-1/2) w^((c m + j) s) (e = 1).  One thread per
+// complex coordinate; the phase index (c m + j) s mod k is exact in 64-bit integers.
+__global__ __launch_bounds__(TT) void k_tff_columns(int64_t c0, int64_t nc, int64_t d, int k,
+                                                    int rho, int m, float scale,
+                                                    float* __restrict__ Z) {
+  const int64_t dc = d / 2;
+  const int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x;
+  if (e >= nc * dc) return;
+  const int64_t r = e / dc, j = e - r * dc;
+  const int64_t col = c0 + r;
+  const int64_t sidx = col / rho;
+  const int within = (int)(col - sidx * rho), c = within >> 1, odd = within & 1;
+  float2 v = make_float2(0.f, 0.f);
+  if (j / m == c) {
+    const int64_t t = (j % k) * (sidx % k) % k;
+    float sn, cs;
+    sincospif(2.0f * (float)t / (float)k, &sn, &cs);
+    v = odd ? make_float2(-sn * scale, cs * scale) : make_float2(cs * scale, sn * scale);
+  }
+  *reinterpret_cast<float2*>(Z + r * d + 2 * j) = v;
+}
+
+// P[i][c0 + r] = Pt[r][i] for r < nc, i < d: 32 x 32 tiles through LDS.
+// grid (ceil(nc / 32) * ceil(d / 32)).
+__global__ __launch_bounds__(TT) void k_scatter_columns(const float* __restrict__ Pt, int64_t nc,
+                                                        int64_t d, float* __restrict__ P,
+                                                        int64_t ldp, int64_t c0) {
+  __shared__ float tile[32][33];
+  const int64_t nbi = (d + 31) / 32;
+  const int64_t br = blockIdx.x / nbi, bi = blockIdx.x - br * nbi;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t r = br * 32 + q, i = bi * 32 + tx;
+    tile[q][tx] = (r < nc && i < d) ? Pt[r * d + i] : 0.f;
+  }
+  __syncthreads();
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t i = bi * 32 + q, r = br * 32 + tx;
+    if (i < d && r < nc) P[i * ldp + c0 + r] = tile[tx][q];
+  }
+}
+
 }  // namespace
 
 hipError_t tff_analysis(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F,
@@ -258,6 +302,28 @@ hipError_t tff_synthesis(const float* V, int64_t ldv, int64_t n, const TffDev& F
   hipLaunchKernelGGL((k_rotate<float, false>), gr, dim3(RT), rot_lds(F.d2), s,
                      (const float*)z, F.d, F.R1, R2t, F.d1, F.d2, Y, ldy);
   prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t tff_materialize(const TffDev& F, const float* R2t, float* Z, float* Pt, int64_t nc_max,
+                           float* P, int64_t ldp, hipStream_t s) {
+  const int64_t K = F.k * F.rho;
+  const float scale = (float)(1.0 / std::sqrt((double)F.k));
+  for (int64_t c0 = 0; c0 < K; c0 += nc_max) {
+    const int64_t nc = std::min(nc_max, K - c0);
+    prof_begin(s, "tff_columns");
+    hipLaunchKernelGGL(k_tff_columns, dim3(blocks_for(nc * (F.d / 2))), dim3(TT), 0, s, c0, nc, F.d,
+                       (int)F.k, (int)F.rho, (int)F.m, scale, Z);
+    prof_end(s);
+    prof_begin(s, "tff_rotate");
+    hipLaunchKernelGGL((k_rotate<float, false>), dim3((unsigned)(nc * F.d1)), dim3(RT), rot_lds(F.d2), s,
+                       (const float*)Z, F.d, F.R1, R2t, F.d1, F.d2, Pt, F.d);
+    prof_end(s);
+    prof_begin(s, "tff_columns");
+    const int64_t g = ((nc + 31) / 32) * ((F.d + 31) / 32);
+    hipLaunchKernelGGL(k_scatter_columns, dim3((unsigned)g), dim3(TT), 0, s, Pt, nc, F.d, P, ldp, c0);
+    prof_end(s);
+  }
   return last_launch_error();
 }
 

@@ -56,6 +56,8 @@ SIGNATURES = {
     "fq_frame_apply_tff": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _vp, _vp, _tp, _tp, _vp, _vp,
                                 _sz]),
     "fq_frame_apply_tff_workspace_bytes": (_sz, [_tp, _tp]),
+    "fq_tff_materialize": (_i, [_vp, _tp, _vp, _i64, _vp, _sz]),
+    "fq_tff_materialize_workspace_bytes": (_sz, [_tp]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _vp, _vp, _tp, _tp, _i, _vp,
                                      _vp, _sz]),
@@ -436,3 +438,20 @@ def fq_frame_apply_tff_actq(X, codes, scale, zero, frame_out: Frame, frame_in: F
                                          ctypes.byref(frame_out.c), ctypes.byref(frame_in.c),
                                          act_bits, _ptr(Y), wp, wb))
     return Y
+
+
+def fq_tff_materialize_workspace_bytes(frame: Frame) -> int:
+    return lib().fq_tff_materialize_workspace_bytes(ctypes.byref(frame.c))
+
+
+def fq_tff_materialize(frame: Frame, P=None, ws=None, stream=None):
+    """The dense frame P (d x k rho fp32) generated on the device from its construction."""
+    torch = _torch()
+    dev = frame.R1.device
+    if P is None:
+        P = torch.empty((frame.d, frame.K), dtype=torch.float32, device=dev)
+    _dev(P, "P", torch.float32, (frame.d, frame.K))
+    ws, wp, wb = _ws(fq_tff_materialize_workspace_bytes(frame), ws, dev)
+    _check(lib().fq_tff_materialize(_stream(stream), ctypes.byref(frame.c), _ptr(P), P.stride(0),
+                                    wp, wb))
+    return P

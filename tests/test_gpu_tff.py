@@ -167,3 +167,40 @@ def test_frame_apply_tff_llama7b_up_sampled(n):
                        zero.astype(np.float64), Po[rows], Pi)
     assert rel_fro(Yg[:, rows], Yo) < 1e-4
     assert np.isfinite(Yg).all()
+
+
+@pytest.mark.parametrize("shape", SMALL + [(520, 143, 4)])
+def test_tff_materialize_matches_construction(shape):
+    """The dense frame generated on the device equals the input generator's float64 frame
+    (relative Frobenius <= 1e-6, entries within 1e-6), and is Parseval (P P^T = I)."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    d, k, rho = shape
+    F, P = _frame(torch, fq, d, k, rho, d + 3 * k)
+    ws = torch.full((fq.fq_tff_materialize_workspace_bytes(F),), 0xFF, dtype=torch.uint8,
+                    device="cuda")
+    Pd = fq.fq_tff_materialize(F, ws=ws)
+    torch.cuda.synchronize()
+    Pg = Pd.cpu().numpy().astype(np.float64)
+    assert rel_fro(Pg, P) < 1e-6
+    assert np.abs(Pg - P).max() < 1e-6
+    assert np.abs(Pg @ Pg.T - np.eye(d)).max() < 1e-5
+
+
+def test_tff_materialize_llama7b_up_frames():
+    """Both frames of the Llama-7B up_proj layer (11008 x 12112 and 4096 x 4512; more than
+    one pass of 512 columns) against the input generator's float64 frames."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    wl = WORKLOADS["llama7b"]
+    (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, 1)
+    Po, Pi = gen.make_frames(wl, 1)
+    for d, k, rho, R1, R2, Pref in ((11008, ko, ro, R1o, R2o, Po), (4096, ki, ri, R1i, R2i, Pi)):
+        F = fq.Frame(d, k, rho, torch.from_numpy(R1.astype(np.float32)).cuda(),
+                     torch.from_numpy(R2.astype(np.float32)).cuda())
+        Pd = fq.fq_tff_materialize(F)
+        torch.cuda.synchronize()
+        Pg = Pd.cpu().numpy()
+        assert rel_fro(Pg, Pref) < 1e-6
+        assert np.abs(Pg - Pref).max() < 1e-6
+        del Pd
