@@ -94,7 +94,9 @@ def make_inputs(wl, li):
     t0 = time.time()
     Xs = gen.make_x(wl, L.d_in)
     Ws = gen.make_weight(wl, li)
+    tf = time.time()
     Po64, Pi64 = gen.make_frames(wl, li)
+    frames_host_s = time.time() - tf
     Po, Pi = gen.frame_f32(Po64), gen.frame_f32(Pi64)
     del Po64, Pi64
 
@@ -106,7 +108,7 @@ def make_inputs(wl, li):
 
     dev = dict(X=up(Xs, wl.x_dtype), W=up(Ws, wl.w_dtype), P_out=up(Po, "f32"),
                P_in=up(Pi, "f32"))
-    host = dict(X=Xs, W=Ws, P_out=Po, P_in=Pi)
+    host = dict(X=Xs, W=Ws, P_out=Po, P_in=Pi, frames_host_s=frames_host_s)
     print(f"[bench] inputs generated and uploaded in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
     return dev, host
@@ -283,6 +285,36 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
             "note": "about 7.6e7 FMAs per token (5.5e7 in the code GEMV) and 13.8 MB of codes "
                     "per block of 8 tokens: bound by launch and memory latency at 1 token, by "
                     "the code kernel's VALU work at 8"}
+
+
+def frame_generation_bench(fq, torch, dev, wl, li, host, iters=5):
+    """Both dense frames of the layer generated on the device from (k, rho, d) and their
+    rotation factors (fq_tff_materialize), timed with HIP events, checked against the
+    frames the pass used (generated on the host in float64 and rounded to float32)."""
+    from fq_inputs import gen
+    L = wl.layers[li]
+    out = {}
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    stream = torch.cuda.current_stream()
+    for name, d, (k, rho, R1, R2) in zip(("P_out", "P_in"), (L.d_out, L.d_in),
+                                         gen.layer_frame_factors(wl, li)):
+        F = fq.Frame(d, k, rho, up(R1), up(R2))
+        P = torch.empty((d, F.K), dtype=torch.float32, device="cuda")
+        ws = torch.empty(fq.fq_tff_materialize_workspace_bytes(F), dtype=torch.uint8, device="cuda")
+        fq.fq_tff_materialize(F, P=P, ws=ws, stream=stream)
+        torch.cuda.synchronize()
+        err = float((P - dev[name]).abs().max())
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            fq.fq_tff_materialize(F, P=P, ws=ws, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out[name] = {"shape": [d, F.K], "ms": round(e0.elapsed_time(e1) / iters, 3),
+                     "max_abs_diff_vs_host_frame": err}
+        del P, ws
+    out["host_float64_seconds_both"] = round(host["frames_host_s"], 2)
+    return out
 
 
 def inference_bench(fq, torch, dev, bufs, L, K_out, K_in, tokens=(1, 8), iters=200):
@@ -565,6 +597,7 @@ def main():
     inf = inference_bench(fq, torch, dev, bufs, L, K_out, K_in)
     inf["structured"] = structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in)
     out["inference"] = inf
+    out["frame_generation"] = frame_generation_bench(fq, torch, dev, wl, li, host)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
