@@ -9,7 +9,7 @@
  *
  *   fq_hessian_accumulate  H   = X^T X over calibration tokens (Sec. 3, proxy loss)
  *   fq_frame_analysis      D   = P_l^T Theta P_prev,  H~ = P_prev^T H P_prev (Alg. 1 step 1)
- *   fq_quantize_frames     2-bit codes of D with OPTQ-style Hessian-aware rounding and
+ *   fq_quantize_frames     2-bit (or 3/4-bit) codes of D with OPTQ-style Hessian-aware rounding and
  *                          Cholesky error feedback after a mu +/- c*sigma clip
  *                          (Alg. 1 steps 2-5)
  *   fq_frame_synthesis     Theta^ = P_l D^ P_prev^T (Alg. 1 return value; appendix
@@ -104,10 +104,12 @@ size_t fq_frame_analysis_workspace_bytes(int wt, int64_t d_out, int64_t d_in, in
  *     All of step 3 runs in fp64.
  *   D       device fp32 K_out x K_in (read only).
  *   Ht      device fp32 K_in x K_in symmetric (the lower triangle is read).
- *   bits    2 (other widths return FQ_ERR_UNSUPPORTED).
+ *   bits    2, 3 or 4 (other widths return FQ_ERR_UNSUPPORTED; the 3- and 4-bit grids
+ *           are those of the paper's appendix on segmentation and detection models).
  *   block   >= 1.
- *   codes   device uint32, K_out x ceil(K_in / 16): column j of row i sits in bits
- *           2*(j mod 16) .. 2*(j mod 16)+1 of word floor(j / 16) of row i; pad bits are 0.
+ *   codes   device uint32, K_out x ceil(K_in / cpw), cpw = floor(32 / bits) codes per word
+ *           (16, 10, 8): column j of row i sits in bits b*(j mod cpw) .. b*(j mod cpw)+b-1
+ *           of word floor(j / cpw) of row i (b = bits); pad bits are 0.
  *   scale, zero  device fp32, K_out each (zero is integer valued; bias = -scale * zero).
  * Returns FQ_ERR_NOT_POSITIVE_DEFINITE when the damped H~ is not positive definite
  * (e.g. damp = 0 with K_in > rank H~) and FQ_ERR_NONFINITE when D or H~ holds NaN/Inf;
@@ -152,6 +154,13 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
                              const float* zero, int64_t K_out, int64_t K_in,
                              const float* P_out, int64_t d_out, const float* P_in,
                              int64_t d_in, float* W_hat, void* ws, size_t ws_bytes);
+/* fq_frame_synthesis for codes of `bits` bits (2, 3 or 4; packed as fq_quantize_frames
+ * packs them); fq_frame_synthesis is this with bits = 2.  Same workspace. */
+fq_status fq_frame_synthesis_nbit(void* stream, const uint32_t* codes, int bits,
+                                  const float* scale, const float* zero, int64_t K_out,
+                                  int64_t K_in, const float* P_out, int64_t d_out,
+                                  const float* P_in, int64_t d_in, float* W_hat, void* ws,
+                                  size_t ws_bytes);
 size_t fq_frame_synthesis_workspace_bytes(int64_t K_out, int64_t K_in, int64_t d_out,
                                           int64_t d_in);
 

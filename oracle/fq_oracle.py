@@ -272,6 +272,33 @@ def unpack2(words, n: int) -> np.ndarray:
     return c.reshape(w.shape[0], -1)[:, :n].astype(np.int64)
 
 
+def codes_per_word(bits: int) -> int:
+    """b-bit codes per uint32 word: floor(32 / b) (16, 10, 8 for 2, 3, 4 bits)."""
+    return 32 // bits
+
+
+def pack_bits(codes, bits: int) -> np.ndarray:
+    """b-bit codes -> uint32 words, floor(32/b) codes per word, row-major; column j sits in
+    bits b*(j mod cpw) .. b*(j mod cpw)+b-1 of word floor(j / cpw); pad bits are zero (the
+    storage appendix keeps the codes of D^ plus a per-row scale and bias)."""
+    cpw = codes_per_word(bits)
+    c = np.asarray(codes, dtype=np.uint64)
+    rows, n = c.shape
+    nw = (n + cpw - 1) // cpw
+    padded = np.zeros((rows, nw * cpw), dtype=np.uint64)
+    padded[:, :n] = c
+    shifts = (bits * np.arange(cpw, dtype=np.uint64))[None, None, :]
+    return np.bitwise_or.reduce(padded.reshape(rows, nw, cpw) << shifts, axis=2).astype(np.uint32)
+
+
+def unpack_bits(words, n: int, bits: int) -> np.ndarray:
+    cpw = codes_per_word(bits)
+    w = np.asarray(words, dtype=np.uint64)
+    shifts = (bits * np.arange(cpw, dtype=np.uint64))[None, None, :]
+    c = (w[:, :, None] >> shifts) & np.uint64((1 << bits) - 1)
+    return c.reshape(w.shape[0], -1)[:, :n].astype(np.int64)
+
+
 # --------------------------------------------------------------------------- stage 4
 def synthesis(codes, scale, zero, P_out, P_in):
     """Reconstructed weights Theta^ = P_l D^ P_prev^T (Alg. 1 return value without the

@@ -523,7 +523,9 @@ static fq_status quantize_apply(hipStream_t s, const float* D, int64_t K_out, in
       if (e != hipSuccess) return hip_fail(e, "lazy update");
     }
   }
-  if ((e = q_pack2(Q.codes8, K_out, K_in, codes, s)) != hipSuccess) return hip_fail(e, "pack");
+  if ((e = bits == 2 ? q_pack2(Q.codes8, K_out, K_in, codes, s)
+                    : q_pack_nbit(Q.codes8, K_out, K_in, bits, codes, s)) != hipSuccess)
+    return hip_fail(e, "pack");
   int flags[4] = {0, 0, 0, 0};
   if ((e = hipMemcpyAsync(flags, Q.flags, sizeof(flags), hipMemcpyDeviceToHost, s)) != hipSuccess)
     return hip_fail(e, "flag copy");
@@ -554,7 +556,7 @@ fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int6
                              uint32_t* codes, float* scale, float* zero, void* ws,
                              size_t ws_bytes) {
   if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
-  if (bits != 2) return fail(FQ_ERR_UNSUPPORTED, "only bits = 2 is implemented");
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
   if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
   if (!(damp >= 0.0) || !isfinite(damp)) return fail(FQ_ERR_INVALID_ARG, "damp must be finite and >= 0");
   if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
@@ -585,7 +587,7 @@ fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t
                             int block, double clip_sigmas, uint32_t* codes, float* scale,
                             float* zero, void* ws, size_t ws_bytes) {
   if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
-  if (bits != 2) return fail(FQ_ERR_UNSUPPORTED, "only bits = 2 is implemented");
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
   if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
   if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
   if (K_out == 0 || K_in == 0) return FQ_OK;
@@ -645,6 +647,16 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
                              const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
                              int64_t d_out, const float* P_in, int64_t d_in, float* W_hat,
                              void* ws, size_t ws_bytes) {
+  return fq_frame_synthesis_nbit(stream, codes, 2, scale, zero, K_out, K_in, P_out, d_out, P_in,
+                                 d_in, W_hat, ws, ws_bytes);
+}
+
+fq_status fq_frame_synthesis_nbit(void* stream, const uint32_t* codes, int bits,
+                                  const float* scale, const float* zero, int64_t K_out,
+                                  int64_t K_in, const float* P_out, int64_t d_out,
+                                  const float* P_in, int64_t d_in, float* W_hat, void* ws,
+                                  size_t ws_bytes) {
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
   if (!dim_ok(K_out) || !dim_ok(K_in) || !dim_ok(d_out) || !dim_ok(d_in))
     return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
   if (K_out < d_out || K_in < d_in)
@@ -664,7 +676,7 @@ fq_status fq_frame_synthesis(void* stream, const uint32_t* codes, const float* s
   char* base = (char*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
   SynLayout L;
   synthesis_layout(K_out, K_in, d_out, d_in, base, &L);
-  if ((e = dequant_bf16(codes, zero, K_out, K_in, L.q, L.ki, L.ko, s)) != hipSuccess)
+  if ((e = dequant_nbit_bf16(codes, bits, zero, K_out, K_in, L.q, L.ki, L.ko, s)) != hipSuccess)
     return hip_fail(e, "dequant");
   if ((e = split_bf16_pad(P_out, 0, K_out, (int)d_out, (int)K_out, scale, L.pl_hi, L.pl_lo, L.ko, (int)d_out, s)) != hipSuccess)
     return hip_fail(e, "split P_out");

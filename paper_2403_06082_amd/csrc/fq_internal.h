@@ -172,6 +172,13 @@ hipError_t q_pack2(const uint8_t* codes8, int64_t rows, int64_t cols, uint32_t* 
                    hipStream_t s);
 // out[r * ld_out + c] = code[r][c] - zero[r] (bf16) on a rows_out x ld_out plane, zero
 // outside rows x cols; ld_out a multiple of 16 (and 16-byte aligned rows).
+// 3- and 4-bit codes: floor(32 / bits) per uint32 word (2-bit: q_pack2 / dequant_bf16)
+hipError_t q_pack_nbit(const uint8_t* codes8, int64_t rows, int64_t cols, int bits,
+                       uint32_t* out, hipStream_t s);
+// dequant_bf16 for any of 2, 3, 4 bits
+hipError_t dequant_nbit_bf16(const uint32_t* codes, int bits, const float* zero, int64_t rows,
+                             int64_t cols, u16* out, int64_t ld_out, int64_t rows_out,
+                             hipStream_t s);
 hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
                         u16* out, int64_t ld_out, int64_t rows_out, hipStream_t s);
 

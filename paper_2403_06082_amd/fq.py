@@ -21,6 +21,12 @@ STATUS = {0: "FQ_OK", 1: "FQ_ERR_INVALID_ARG", 2: "FQ_ERR_UNSUPPORTED",
 
 
 
+def words_per_row(K_in: int, bits: int = 2) -> int:
+    """uint32 words of one row of packed codes: floor(32 / bits) codes per word."""
+    cpw = 32 // bits
+    return (K_in + cpw - 1) // cpw
+
+
 class TFF(ctypes.Structure):
     """struct fq_tff: a tight fusion frame given by (d, k, rho) and its rotation factors."""
     _fields_ = [("d", ctypes.c_int64), ("k", ctypes.c_int64), ("rho", ctypes.c_int64),
@@ -46,6 +52,8 @@ SIGNATURES = {
     "fq_frame_synthesis": (_i, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp,
                                 _sz]),
     "fq_frame_synthesis_workspace_bytes": (_sz, [_i64, _i64, _i64, _i64]),
+    "fq_frame_synthesis_nbit": (_i, [_vp, _vp, _i, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64,
+                                     _vp, _vp, _sz]),
     "fq_frame_apply": (_i, [_vp, _vp, _i, _i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _vp, _i64,
                             _vp, _vp, _vp, _sz]),
     "fq_frame_apply_workspace_bytes": (_sz, [_i64, _i64, _i64]),
@@ -193,12 +201,12 @@ def fq_frame_analysis(W, P_out, P_in, H=None, D=None, Ht=None, ws=None, stream=N
 
 def fq_quantize_frames(D, Ht, codes, scale, zero, bits: int = 2, block: int = 128,
                        damp: float = 0.01, clip_sigmas: float = 2.0, ws=None, stream=None):
-    """2-bit codes (K_out, ceil(K_in/16)) int32 view of uint32 words, scale/zero (K_out,)."""
+    """codes (K_out, words_per_row(K_in, bits)) int32 view of uint32 words, scale/zero (K_out,)."""
     torch = _torch()
     K_out, K_in = D.shape
     _dev(D, "D", torch.float32)
     _dev(Ht, "Ht", torch.float32, (K_in, K_in))
-    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
     _dev(scale, "scale", torch.float32, (K_out,))
     _dev(zero, "zero", torch.float32, (K_out,))
     ws, wp, wb = _ws(fq_quantize_frames_workspace_bytes(K_out, K_in, block), ws, D.device)
@@ -226,7 +234,7 @@ def fq_quantize_apply(D, codes, scale, zero, ws, bits: int = 2, block: int = 128
     torch = _torch()
     K_out, K_in = D.shape
     _dev(D, "D", torch.float32)
-    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
     _dev(scale, "scale", torch.float32, (K_out,))
     _dev(zero, "zero", torch.float32, (K_out,))
     _dev(ws, "ws", torch.uint8)
@@ -236,12 +244,12 @@ def fq_quantize_apply(D, codes, scale, zero, ws, bits: int = 2, block: int = 128
     return codes, scale, zero
 
 
-def fq_frame_synthesis(codes, scale, zero, P_out, P_in, W_hat, ws=None, stream=None):
-    """W_hat = P_out diag(scale) (codes - zero) P_in^T."""
+def fq_frame_synthesis(codes, scale, zero, P_out, P_in, W_hat, ws=None, stream=None, bits=2):
+    """W_hat = P_out diag(scale) (codes - zero) P_in^T (codes of 2, 3 or 4 bits)."""
     torch = _torch()
     K_out, K_in = P_out.shape[1], P_in.shape[1]
     d_out, d_in = P_out.shape[0], P_in.shape[0]
-    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
     _dev(scale, "scale", torch.float32, (K_out,))
     _dev(zero, "zero", torch.float32, (K_out,))
     _dev(P_out, "P_out", torch.float32)
@@ -249,9 +257,9 @@ def fq_frame_synthesis(codes, scale, zero, P_out, P_in, W_hat, ws=None, stream=N
     _dev(W_hat, "W_hat", torch.float32, (d_out, d_in))
     ws, wp, wb = _ws(fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in), ws,
                      W_hat.device)
-    _check(lib().fq_frame_synthesis(_stream(stream), _ptr(codes), _ptr(scale), _ptr(zero), K_out,
-                                    K_in, _ptr(P_out), d_out, _ptr(P_in), d_in, _ptr(W_hat), wp,
-                                    wb))
+    _check(lib().fq_frame_synthesis_nbit(_stream(stream), _ptr(codes), bits, _ptr(scale),
+                                         _ptr(zero), K_out, K_in, _ptr(P_out), d_out, _ptr(P_in),
+                                         d_in, _ptr(W_hat), wp, wb))
     return W_hat
 
 

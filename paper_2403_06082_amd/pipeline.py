@@ -20,13 +20,15 @@ class LayerBuffers:
     """Device outputs and workspaces for one layer shape (reused across calls)."""
 
     def __init__(self, d_out, d_in, K_out, K_in, w_dtype, x_dtype, n_tokens, block=128,
-                 device="cuda"):
+                 device="cuda", bits=2):
         import torch
         f32 = torch.float32
         self.H = torch.empty((d_in, d_in), dtype=f32, device=device)
         self.D = torch.empty((K_out, K_in), dtype=f32, device=device)
         self.Ht = torch.empty((K_in, K_in), dtype=f32, device=device)
-        self.codes = torch.empty((K_out, (K_in + 15) // 16), dtype=torch.int32, device=device)
+        self.bits = bits
+        self.codes = torch.empty((K_out, _fq.words_per_row(K_in, bits)), dtype=torch.int32,
+                                 device=device)
         self.scale = torch.empty((K_out,), dtype=f32, device=device)
         self.zero = torch.empty((K_out,), dtype=f32, device=device)
         self.W_hat = torch.empty((d_out, d_in), dtype=f32, device=device)
@@ -62,7 +64,7 @@ def quantize_layer(W, X, P_out, P_in, bufs: LayerBuffers, H=None, Ht=None, bits=
     _fq.fq_quantize_frames(bufs.D, Ht, bufs.codes, bufs.scale, bufs.zero, bits=bits, block=block,
                            damp=damp, clip_sigmas=clip_sigmas, ws=bufs.ws_q, stream=stream)
     _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
-                           ws=bufs.ws_s, stream=stream)
+                           ws=bufs.ws_s, stream=stream, bits=bits)
     return bufs
 
 
@@ -90,5 +92,5 @@ def _quantize_layer_two_streams(W, X, P_out, P_in, bufs, H, Ht, bits, block, dam
     _fq.fq_quantize_apply(bufs.D, bufs.codes, bufs.scale, bufs.zero, bufs.ws_q, bits=bits,
                           block=block, clip_sigmas=clip_sigmas, stream=main)
     _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
-                           ws=bufs.ws_s, stream=main)
+                           ws=bufs.ws_s, stream=main, bits=bits)
     return bufs

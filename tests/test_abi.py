@@ -69,7 +69,8 @@ def test_invalid_arguments_rejected_before_launch(L):
     # unsupported bit width, bad block, bad damp / clip
     args = (n, ctypes.c_void_p(64), ctypes.c_void_p(64), 4, 4)
     outs = (ctypes.c_void_p(64), ctypes.c_void_p(64), ctypes.c_void_p(64), n, 0)
-    assert L.fq_quantize_frames(*args, 3, 128, 0.01, 2.0, *outs) == 2
+    assert L.fq_quantize_frames(*args, 5, 128, 0.01, 2.0, *outs) == 2
+    assert L.fq_quantize_frames(*args, 1, 128, 0.01, 2.0, *outs) == 2
     assert L.fq_quantize_frames(*args, 2, 0, 0.01, 2.0, *outs) == 1
     assert L.fq_quantize_frames(*args, 2, 128, -1.0, 2.0, *outs) == 1
     assert L.fq_quantize_frames(*args, 2, 128, 0.01, 0.0, *outs) == 1
@@ -81,7 +82,7 @@ def test_invalid_arguments_rejected_before_launch(L):
     assert L.fq_quantize_prepare(n, n, 4, 4, 128, 0.01, n, 0) == 1
     assert L.fq_quantize_prepare(n, ctypes.c_void_p(64), 4, 4, 128, 0.01, n, 0) == 5
     aouts = (ctypes.c_void_p(64), ctypes.c_void_p(64), ctypes.c_void_p(64), n, 0)
-    assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 3, 128, 2.0, *aouts) == 2
+    assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 5, 128, 2.0, *aouts) == 2
     assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 2, 128, -2.0, *aouts) == 1
     assert L.fq_quantize_apply(n, ctypes.c_void_p(64), -4, 4, 2, 128, 2.0, *aouts) == 1
     assert L.fq_quantize_apply(n, ctypes.c_void_p(64), 4, 4, 2, 128, 2.0, *aouts) == 5

@@ -236,6 +236,26 @@ def test_pack_layout_hand_case():
 
 
 # ----------------------------------------------------------------------------- synthesis
+def test_pack_bits_hand_cases():
+    """3-bit: codes 0..7, 0..2 of one row fill word 0 as sum_j c_j 8^j (10 codes, top two
+    bits zero) and word 1 with the last code; 4-bit: eight codes per word as hex digits;
+    2-bit agrees with the 16-per-word packing; unpacking inverts packing for every width."""
+    c3 = np.array([[0, 1, 2, 3, 4, 5, 6, 7, 0, 1, 2]])
+    w3 = O.pack_bits(c3, 3)
+    assert w3.shape == (1, 2)
+    assert int(w3[0, 0]) == sum(int(v) << (3 * j) for j, v in enumerate(c3[0, :10]))
+    assert int(w3[0, 0]) >> 30 == 0 and int(w3[0, 1]) == 2
+    c4 = np.array([[1, 2, 3, 4, 5, 6, 7, 15, 9]])
+    w4 = O.pack_bits(c4, 4)
+    assert int(w4[0, 0]) == 0xF7654321 and int(w4[0, 1]) == 9
+    rng = _rng(9)
+    c2 = rng.integers(0, 4, (3, 37))
+    np.testing.assert_array_equal(O.pack_bits(c2, 2), O.pack2(c2))
+    for bits in (2, 3, 4):
+        c = rng.integers(0, 1 << bits, (4, 53))
+        np.testing.assert_array_equal(O.unpack_bits(O.pack_bits(c, bits), 53, bits), c)
+
+
 def test_synthesis_inverts_analysis_at_r1():
     """With r = 1 both frames are orthogonal, so analysis(synthesis(D^)) = D^ exactly."""
     P_out = tff.parseval_frame(6, 4, 24, np.random.SeedSequence(1))   # K = d = 24
