@@ -134,7 +134,8 @@ def _ff_problem(rng, K_out, d_in, k_in, rho=4, n=600):
 
 def _quantize(torch, fq, D, Ht, block, **kw):
     K_out, K_in = D.shape
-    codes = torch.empty((K_out, (K_in + 15) // 16), dtype=torch.int32, device="cuda")
+    codes = torch.empty((K_out, fq.fq.words_per_row(K_in, kw.get("bits", 2))), dtype=torch.int32,
+                        device="cuda")
     scale = torch.empty((K_out,), dtype=torch.float32, device="cuda")
     zero = torch.empty((K_out,), dtype=torch.float32, device="cuda")
     fq.fq_quantize_frames(torch.from_numpy(D).cuda(), torch.from_numpy(Ht).cuda(), codes, scale,
@@ -220,7 +221,7 @@ def test_quantize_errors():
         _quantize(torch, fq, Dn, Ht, 128)
     assert ei.value.status == 4
     with pytest.raises(fq.FQError) as ei:
-        _quantize(torch, fq, D, Ht, 128, bits=3)
+        _quantize(torch, fq, D, Ht, 128, bits=5)
     assert ei.value.status == 2
 
 
