@@ -204,3 +204,47 @@ def test_tff_materialize_llama7b_up_frames():
         assert rel_fro(Pg, Pref) < 1e-6
         assert np.abs(Pg - Pref).max() < 1e-6
         del Pd
+
+
+@pytest.mark.parametrize("key", ["llama70b_r1.0", "llama70b_r1.1"])
+def test_tff_llama70b_down_largest_frames(key):
+    """The largest frames of the workloads: Llama-2-70B down_proj, d_in 28672 = 128 x 224
+    (k 1792 at r = 1.0, 1971 at r = 1.1; rho 16) and d_out 8192.  The materialized P_in
+    equals the input generator's float64 construction on three subspaces at each end; the
+    structured layer outputs (1 and 8 tokens, and 8-bit activations against the oracle on
+    the device's own analysis) agree with the dense path run on the materialized frames."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    wl = WORKLOADS[key]
+    L = wl.layers[0]
+    (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, 0)
+    up = lambda a: torch.from_numpy(a.astype(np.float32)).cuda()
+    Fo = fq.Frame(L.d_out, ko, ro, up(R1o), up(R2o))
+    Fi = fq.Frame(L.d_in, ki, ri, up(R1i), up(R2i))
+    Pi = fq.fq_tff_materialize(Fi)
+    Po = fq.fq_tff_materialize(Fo)
+    torch.cuda.synchronize()
+    scale_f = np.sqrt(L.d_in / (ki * ri))
+    for s0 in (0, ki - 3):
+        T = tff.real_tff_basis(ki, ri, L.d_in, range(s0, s0 + 3)) * scale_f
+        ref = tff.apply_rotation(R1i, R2i, T)
+        got = Pi[:, s0 * ri:(s0 + 3) * ri].cpu().numpy()
+        assert rel_fro(got, ref) < 1e-6
+    rng = np.random.default_rng(7)
+    codes, scale, zero = _codes(rng, Fo.K, Fi.K)
+    words = torch.from_numpy(O.pack2(codes).view(np.int32)).cuda()
+    sc, ze = torch.from_numpy(scale).cuda(), torch.from_numpy(zero).cuda()
+    for n in (1, 8):
+        X = up(rng.standard_normal((n, L.d_in)))
+        Yt = fq.fq_frame_apply_tff(X, words, sc, ze, Fo, Fi)
+        Yd = fq.fq_frame_apply(X, words, sc, ze, Po, Pi)
+        Yq = fq.fq_frame_apply_tff_actq(X, words, sc, ze, Fo, Fi, 8)
+        U = fq.fq_tff_analysis(X, Fi)
+        torch.cuda.synchronize()
+        assert rel_fro(Yt.cpu().numpy(), Yd.cpu().numpy().astype(np.float64)) < 1e-5
+        rows = np.sort(rng.choice(L.d_out, 32, replace=False))
+        Yo = O.frame_apply_rtn_activations(U.cpu().numpy(), codes, scale.astype(np.float64),
+                                           zero.astype(np.float64),
+                                           Po[rows].cpu().numpy().astype(np.float64), 8)
+        assert rel_fro(Yq.cpu().numpy()[:, rows], Yo) < 1e-4
+    del Pi, Po
