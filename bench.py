@@ -287,6 +287,33 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
                     "the code kernel's VALU work at 8"}
 
 
+def grid_variants_bench(torch, dev, wl, L, K_out, K_in, n, steps):
+    """The same pass with 3- and 4-bit grids (one warmup, then `steps` timed passes each;
+    one stream), as quantized weights per second."""
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    out = {}
+    for bits in (3, 4):
+        b = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
+                         bits=bits)
+
+        def run():
+            quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], b, bits=bits,
+                           block=wl.block, damp=wl.damp, clip_sigmas=wl.clip_sigmas)
+
+        run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            run()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        out[f"bits{bits}"] = {"ms_per_step": round(ms, 3),
+                              "weights_per_s": round(L.d_out * L.d_in / (ms / 1e3), 1)}
+        print(f"[bench] {bits}-bit pass: {ms:.2f} ms/step", file=sys.stderr, flush=True)
+        del b
+    return out
+
+
 def frame_generation_bench(fq, torch, dev, wl, li, host, iters=5):
     """Both dense frames of the layer generated on the device from (k, rho, d) and their
     rotation factors (fq_tff_materialize), timed with HIP events, checked against the
@@ -598,6 +625,7 @@ def main():
     inf["structured"] = structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in)
     out["inference"] = inf
     out["frame_generation"] = frame_generation_bench(fq, torch, dev, wl, li, host)
+    out["grid_variants"] = grid_variants_bench(torch, dev, wl, L, K_out, K_in, n, args.steps)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
