@@ -274,14 +274,16 @@ fq_status fq_act_quantize(void* stream, const float* U, int64_t n, int64_t K, in
  * fq_frame_apply_tff with the inputs' frame representation C = X P_in rounded per token as
  * fq_act_quantize does (same appendix): Y = (Delta C^ (codes - zero)^T diag(scale)) P_out^T,
  * where the products with the codes run exactly in integer arithmetic (int32 sums of
- * int8 x 2-bit terms).  Arguments and errors as fq_frame_apply_tff, plus act_bits in
- * [2, 8]; ws: fq_frame_apply_tff_actq_workspace_bytes(frame_out, frame_in) bytes.
+ * int8 x b-bit terms).  Arguments and errors as fq_frame_apply_tff, plus bits, the code
+ * width (2 or 4, packed as fq_quantize_frames packs them; 3 returns FQ_ERR_UNSUPPORTED),
+ * and act_bits in [2, 8] (the appendix reports W4/A4); ws:
+ * fq_frame_apply_tff_actq_workspace_bytes(frame_out, frame_in) bytes (any code width).
  */
 fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n_tokens,
-                                  int64_t ldx, const uint32_t* codes, const float* scale,
-                                  const float* zero, const fq_tff* frame_out,
-                                  const fq_tff* frame_in, int act_bits, float* Y, void* ws,
-                                  size_t ws_bytes);
+                                  int64_t ldx, const uint32_t* codes, int bits,
+                                  const float* scale, const float* zero,
+                                  const fq_tff* frame_out, const fq_tff* frame_in, int act_bits,
+                                  float* Y, void* ws, size_t ws_bytes);
 size_t fq_frame_apply_tff_actq_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
 
 /* Status text and the calling thread's last error message (never NULL). */

@@ -873,7 +873,7 @@ fq_status fq_act_quantize(void* stream, const float* U, int64_t n, int64_t K, in
   if (!dim_ok(n) || !dim_ok(K)) return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
   if (n == 0) return FQ_OK;
   if (!U || !Cq || !delta) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
-  hipError_t e = act_quantize(U, K, n, K, act_bits, Cq, K, false, delta, nullptr, (hipStream_t)stream);
+  hipError_t e = act_quantize(U, K, n, K, act_bits, Cq, K, 0, delta, nullptr, (hipStream_t)stream);
   return e == hipSuccess ? FQ_OK : hip_fail(e, "activation rounding");
 }
 
@@ -897,11 +897,12 @@ size_t fq_frame_apply_tff_actq_workspace_bytes(const fq_tff* frame_out, const fq
 }
 
 fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n_tokens,
-                                  int64_t ldx, const uint32_t* codes, const float* scale,
-                                  const float* zero, const fq_tff* frame_out,
-                                  const fq_tff* frame_in, int act_bits, float* Y, void* ws,
-                                  size_t ws_bytes) {
+                                  int64_t ldx, const uint32_t* codes, int bits,
+                                  const float* scale, const float* zero,
+                                  const fq_tff* frame_out, const fq_tff* frame_in, int act_bits,
+                                  float* Y, void* ws, size_t ws_bytes) {
   if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
+  if (bits != 2 && bits != 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2 or 4 (3-bit codes do not spread into bytes)");
   if (act_bits < 2 || act_bits > 8) return fail(FQ_ERR_INVALID_ARG, "act_bits must be in [2, 8]");
   if (!dim_ok(n_tokens)) return fail(FQ_ERR_INVALID_ARG, "n_tokens must be in [0, 2^30)");
   TffDev Fo, Fi;
@@ -918,7 +919,8 @@ fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n
   ApplyActqLayout L;
   apply_actq_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
   const int64_t K_in = Fi.k * Fi.rho, K_out = Fo.k * Fo.rho;
-  const int64_t ldu = (K_in + 15) / 16 * 16, nwords = (K_in + 15) / 16;
+  const int cpw = 32 / bits;
+  const int64_t ldu = (K_in + 15) / 16 * 16, nwords = (K_in + cpw - 1) / cpw;
   hipError_t e;
   if ((e = tff_transpose_r2(Fo, L.base.r2t, s)) != hipSuccess) return hip_fail(e, "transpose R2");
   const int esz = xt == FQ_F32 ? 4 : 2;
@@ -927,11 +929,11 @@ fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n
     if ((e = tff_analysis((const char*)X + t0 * ldx * esz, xt, ldx, nt, Fi, L.base.y, L.base.U, ldu, s)) !=
         hipSuccess)
       return hip_fail(e, "tff analysis");
-    if ((e = act_quantize(L.base.U, ldu, nt, K_in, act_bits, L.Cq, 16 * nwords, true, L.delta, L.csum, s)) !=
+    if ((e = act_quantize(L.base.U, ldu, nt, K_in, act_bits, L.Cq, cpw * nwords, cpw, L.delta, L.csum, s)) !=
         hipSuccess)
       return hip_fail(e, "activation rounding");
-    if ((e = apply_codes_i8(L.Cq, 16 * nwords, L.delta, L.csum, nt, codes, K_out, nwords, scale, zero,
-                            L.base.V, s)) != hipSuccess)
+    if ((e = apply_codes_i8(L.Cq, cpw * nwords, L.delta, L.csum, nt, bits, codes, K_out, nwords, scale,
+                            zero, L.base.V, s)) != hipSuccess)
       return hip_fail(e, "apply codes");
     if ((e = tff_synthesis(L.base.V, K_out, nt, Fo, L.base.r2t, L.base.z, Y + t0 * Fo.d, Fo.d, s)) != hipSuccess)
       return hip_fail(e, "tff synthesis");

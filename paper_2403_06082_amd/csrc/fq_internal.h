@@ -115,14 +115,15 @@ hipError_t tff_synthesis(const float* V, int64_t ldv, int64_t n, const TffDev& F
                          const float* R2t, float* z, float* Y, int64_t ldy, hipStream_t s);
 
 // Per-token rounding of U (n x ldu, K columns) to bits-bit integers: Cq (n x ldc bytes;
-// perm: each 16-column word in the byte order of the spread code words), delta (n), and
-// when csum is not NULL the row sums of Cq (n).
+// perm_cpw 16 or 8: each code word's columns in the byte order of 2- or 4-bit spread code
+// words, 0: natural order), delta (n), and when csum is not NULL the row sums of Cq (n).
 hipError_t act_quantize(const float* U, int64_t ldu, int64_t n, int64_t K, int bits,
-                        int8_t* Cq, int64_t ldc, bool perm, float* delta, int* csum,
+                        int8_t* Cq, int64_t ldc, int perm_cpw, float* delta, int* csum,
                         hipStream_t s);
-// V as apply_codes, from rounded activations (perm layout, ldc = 16 * nwords bytes)
+// V as apply_codes, from rounded activations and codes of `bits` = 2 or 4 bits
+// (ldc = (32 / bits) * nwords bytes)
 hipError_t apply_codes_i8(const int8_t* Cq, int64_t ldc, const float* delta, const int* csum,
-                          int nt, const uint32_t* codes, int64_t K_out, int64_t nwords,
+                          int nt, int bits, const uint32_t* codes, int64_t K_out, int64_t nwords,
                           const float* scale, const float* zero, float* V, hipStream_t s);
 hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_in,
                        const uint32_t* codes, const float* scale, const float* zero,

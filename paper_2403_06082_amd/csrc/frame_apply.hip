@@ -257,12 +257,13 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
 // t, Delta_t = max_j |U[t][j]| / qmax and Cq[t][j] = round(U[t][j] / Delta_t) (IEEE fp32
 // divisions, ties to even; Delta_t = 0 gives a zero row).  One 1024-thread work-group per
 // token.
-// PERM stores each 16-column word's bytes in the order of the spread code words: column
-// 16w + 4g + b at byte 16w + 4b + g (columns [K, ldc) zero); otherwise column j at byte j.
+// CPW > 0 stores each CPW-column code word's bytes in the order of the spread code words
+// (NB = CPW / 4 dwords per word): column CPW w + NB g + b at byte CPW w + 4b + g (columns
+// [K, ldc) zero); CPW = 0 stores column j at byte j.
 // csum (optional) receives sum_j Cq[t][j].
 constexpr int QT = 1024;       // threads per token in the activation rounding kernel
 
-template <bool PERM>
+template <int CPW>
 __global__ __launch_bounds__(QT) void k_act_quantize(const float* __restrict__ U, int64_t ldu,
                                                      int64_t K, float qmax,
                                                      int8_t* __restrict__ Cq, int64_t ldc,
@@ -290,7 +291,12 @@ __global__ __launch_bounds__(QT) void k_act_quantize(const float* __restrict__ U
     int q = 0;
     if (j < K && dl > 0.f) q = (int)rintf(u[j] / dl);
     sum += q;
-    const int64_t dst = PERM ? (j & ~(int64_t)15) + 4 * (j & 3) + ((j >> 2) & 3) : j;
+    int64_t dst = j;
+    if (CPW > 0) {
+      constexpr int NB = CPW > 0 ? CPW / 4 : 1;
+      const int r = (int)(j % CPW);
+      dst = (j - r) + 4 * (r % NB) + r / NB;
+    }
     Cq[t * ldc + dst] = (int8_t)q;
   }
 #pragma unroll
@@ -307,12 +313,22 @@ __global__ __launch_bounds__(QT) void k_act_quantize(const float* __restrict__ U
   }
 }
 
-// V[t][i] = scale_i Delta_t (sum_j Cq[t][j] q_ij - zero_i sum_j Cq[t][j]), the dot product
-// exact in int32 (|sum| <= 3 * 127 * K_in).  Same work split as k_apply_codes: 16 rows per
-// work-group, 4 per wave, lanes over code words; Cq (PERM layout, ldc = 16 nwords bytes)
-// goes through LDS CW words at a time, and each word's spread codes meet the matching 4
-// dwords of Cq in 4 v_dot4 per row and token.
-template <int NT>
+template <int B> struct CqWord;                         // one code word's Cq bytes
+template <> struct CqWord<2> { typedef uint4 type; };   // 16 columns
+template <> struct CqWord<4> { typedef uint2 type; };   // 8 columns
+__device__ __forceinline__ uint32_t dw(const uint4& d, int b) {
+  return b == 0 ? d.x : b == 1 ? d.y : b == 2 ? d.z : d.w;
+}
+__device__ __forceinline__ uint32_t dw(const uint2& d, int b) { return b == 0 ? d.x : d.y; }
+
+// V[t][i] = scale_i Delta_t (sum_j Cq[t][j] q_ij - zero_i sum_j Cq[t][j]) for BITS-bit codes
+// (2 or 4), the dot product exact in int32 (|sum| <= (2^BITS - 1) * 127 * K_in) and
+// converted to float at the end.  Same work split as k_apply_codes: 16 rows per
+// work-group, 4 per wave, lanes over code words; Cq (layout of k_act_quantize with
+// CPW = 32 / BITS, ldc = CPW nwords bytes) goes through LDS CW words at a time, and each
+// word's spread codes meet the matching NB = CPW / 4 dwords of Cq in NB v_dot4 per row and
+// token.
+template <int NT, int BITS>
 __global__ __launch_bounds__(AT) void k_apply_codes_i8(const int8_t* __restrict__ Cq,
                                                        int64_t ldc,
                                                        const float* __restrict__ delta,
@@ -322,9 +338,12 @@ __global__ __launch_bounds__(AT) void k_apply_codes_i8(const int8_t* __restrict_
                                                        const float* __restrict__ scale,
                                                        const float* __restrict__ zero,
                                                        float* __restrict__ V) {
-  constexpr int CW = NT >= 8 ? 128 : 256;    // words per chunk (NT * CW * 16 bytes <= 16 KB)
+  typedef typename CqWord<BITS>::type WT;
+  constexpr int CPW = 32 / BITS, NB = CPW / 4;
+  constexpr uint32_t MASK = BITS == 2 ? 0x03030303u : 0x0F0F0F0Fu;
+  constexpr int CW = NT >= 8 ? 128 : 256;    // words per chunk (NT * CW * CPW bytes <= 16 KB)
   constexpr int WPL = CW / 64;               // code words per lane and row in a chunk
-  __shared__ uint4 cs[NT][CW];
+  __shared__ WT cs[NT][CW];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t row0 = (int64_t)blockIdx.x * 16 + wave * 4;
   int acc[4][NT];
@@ -345,12 +364,12 @@ __global__ __launch_bounds__(AT) void k_apply_codes_i8(const int8_t* __restrict_
     }
   };
   uint32_t wd[4][WPL], wn[4][WPL] = {};
-  const uint4* src = reinterpret_cast<const uint4*>(Cq);
-  const int64_t ldq = ldc / 16;              // uint4 per token row
+  const WT* src = reinterpret_cast<const WT*>(Cq);
+  const int64_t ldq = ldc / CPW;             // words per token row
   for (int64_t w0 = 0; w0 < nwords; w0 += CW) {
     const int nw = (int)min((int64_t)CW, nwords - w0);
     lds_barrier();                          // the previous chunk's reads of cs are done
-    uint4 cv[NT * CW / AT];
+    WT cv[NT * CW / AT];
 #pragma unroll
     for (int e = 0; e < NT * CW / AT; ++e) {
       const int f = e * AT + (int)threadIdx.x, t = f / CW, w = f - t * CW;
@@ -368,21 +387,19 @@ __global__ __launch_bounds__(AT) void k_apply_codes_i8(const int8_t* __restrict_
     for (int k = 0; k < WPL; ++k) {
       const int w = lane + 64 * k;
       if (w >= nw) break;
-      uint32_t y[4][4];                     // byte g of y[r][b]: code of column 4g + b
+      uint32_t y[4][NB];                    // byte g of y[r][b]: code of column NB g + b
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) y[r][b] = (wd[r][k] >> (2 * b)) & 0x03030303u;
+        for (int b = 0; b < NB; ++b) y[r][b] = (wd[r][k] >> (BITS * b)) & MASK;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const uint4 d = cs[t][w];
+        const WT d = cs[t][w];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][0], (int)d.x, acc[r][t], false);
-          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][1], (int)d.y, acc[r][t], false);
-          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][2], (int)d.z, acc[r][t], false);
-          acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][3], (int)d.w, acc[r][t], false);
-        }
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[r][t] = __builtin_amdgcn_sdot4((int)y[r][b], (int)dw(d, b), acc[r][t], false);
       }
     }
 #pragma unroll
@@ -549,30 +566,37 @@ hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* code
 }
 
 hipError_t act_quantize(const float* U, int64_t ldu, int64_t n, int64_t K, int bits,
-                        int8_t* Cq, int64_t ldc, bool perm, float* delta, int* csum,
+                        int8_t* Cq, int64_t ldc, int perm_cpw, float* delta, int* csum,
                         hipStream_t s) {
   if (n == 0) return hipSuccess;
   const float qmax = (float)((1 << (bits - 1)) - 1);
+  const dim3 g((unsigned)n);
   prof_begin(s, "act_quantize");
-  if (perm)
-    hipLaunchKernelGGL(k_act_quantize<true>, dim3((unsigned)n), dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
+  if (perm_cpw == 16)
+    hipLaunchKernelGGL(k_act_quantize<16>, g, dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
+  else if (perm_cpw == 8)
+    hipLaunchKernelGGL(k_act_quantize<8>, g, dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
   else
-    hipLaunchKernelGGL(k_act_quantize<false>, dim3((unsigned)n), dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
+    hipLaunchKernelGGL(k_act_quantize<0>, g, dim3(QT), 0, s, U, ldu, K, qmax, Cq, ldc, delta, csum);
   prof_end(s);
   return last_launch_error();
 }
 
 hipError_t apply_codes_i8(const int8_t* Cq, int64_t ldc, const float* delta, const int* csum,
-                          int nt, const uint32_t* codes, int64_t K_out, int64_t nwords,
+                          int nt, int bits, const uint32_t* codes, int64_t K_out, int64_t nwords,
                           const float* scale, const float* zero, float* V, hipStream_t s) {
   const dim3 g((unsigned)((K_out + 15) / 16));
   prof_begin(s, "apply_codes");
-#define FQ_CODES_I8(N) \
-  hipLaunchKernelGGL(k_apply_codes_i8<N>, g, dim3(AT), 0, s, Cq, ldc, delta, csum, codes, K_out, nwords, scale, zero, V);
-  if (nt == 1) { FQ_CODES_I8(1) }
-  else if (nt == 2) { FQ_CODES_I8(2) }
-  else if (nt <= 4) { FQ_CODES_I8(4) }
-  else { FQ_CODES_I8(8) }
+#define FQ_CODES_I8(N, B) \
+  hipLaunchKernelGGL((k_apply_codes_i8<N, B>), g, dim3(AT), 0, s, Cq, ldc, delta, csum, codes, K_out, nwords, scale, zero, V);
+#define FQ_CODES_I8_NT(B)                 \
+  if (nt == 1) { FQ_CODES_I8(1, B) }      \
+  else if (nt == 2) { FQ_CODES_I8(2, B) } \
+  else if (nt <= 4) { FQ_CODES_I8(4, B) } \
+  else { FQ_CODES_I8(8, B) }
+  if (bits == 4) { FQ_CODES_I8_NT(4) }
+  else { FQ_CODES_I8_NT(2) }
+#undef FQ_CODES_I8_NT
 #undef FQ_CODES_I8
   prof_end(s);
   return last_launch_error();

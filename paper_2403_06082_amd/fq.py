@@ -67,8 +67,8 @@ SIGNATURES = {
     "fq_tff_materialize": (_i, [_vp, _tp, _vp, _i64, _vp, _sz]),
     "fq_tff_materialize_workspace_bytes": (_sz, [_tp]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
-    "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _vp, _vp, _tp, _tp, _i, _vp,
-                                     _vp, _sz]),
+    "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
+                                     _vp, _vp, _sz]),
     "fq_frame_apply_tff_actq_workspace_bytes": (_sz, [_tp, _tp]),
     "fq_status_string": (ctypes.c_char_p, [_i]),
     "fq_last_error": (ctypes.c_char_p, []),
@@ -424,7 +424,7 @@ def fq_frame_apply_tff_actq_workspace_bytes(frame_out: Frame, frame_in: Frame) -
 
 
 def fq_frame_apply_tff_actq(X, codes, scale, zero, frame_out: Frame, frame_in: Frame, act_bits=8,
-                            Y=None, ws=None, stream=None):
+                            Y=None, ws=None, stream=None, bits=2):
     """fq_frame_apply_tff with the inputs' frame representation rounded per token to
     act_bits-bit integers and the code products in integer arithmetic."""
     torch = _torch()
@@ -434,7 +434,7 @@ def fq_frame_apply_tff_actq(X, codes, scale, zero, frame_out: Frame, frame_in: F
     if d_in != frame_in.d:
         raise ValueError("X must have frame_in.d columns")
     K_out, K_in = frame_out.K, frame_in.K
-    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
     _dev(scale, "scale", torch.float32, (K_out,))
     _dev(zero, "zero", torch.float32, (K_out,))
     if Y is None:
@@ -442,7 +442,7 @@ def fq_frame_apply_tff_actq(X, codes, scale, zero, frame_out: Frame, frame_in: F
     _dev(Y, "Y", torch.float32, (n, frame_out.d))
     ws, wp, wb = _ws(fq_frame_apply_tff_actq_workspace_bytes(frame_out, frame_in), ws, X.device)
     _check(lib().fq_frame_apply_tff_actq(_stream(stream), _ptr(X), _dt(X), n, X.stride(0),
-                                         _ptr(codes), _ptr(scale), _ptr(zero),
+                                         _ptr(codes), bits, _ptr(scale), _ptr(zero),
                                          ctypes.byref(frame_out.c), ctypes.byref(frame_in.c),
                                          act_bits, _ptr(Y), wp, wb))
     return Y

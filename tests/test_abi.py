@@ -138,5 +138,6 @@ def test_act_quantize_arguments(L):
     good = ctypes.byref(TFF(4096, 282, 16, 64, 64, 64, 64))
     assert L.fq_frame_apply_tff_actq_workspace_bytes(good, good) > \
         L.fq_frame_apply_tff_workspace_bytes(good, good)
-    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, p, p, good, good, 9, p, p, 1 << 30) == 1
-    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, p, p, good, good, 8, p, p, 64) == 5
+    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, 2, p, p, good, good, 9, p, p, 1 << 30) == 1
+    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, 3, p, p, good, good, 8, p, p, 1 << 30) == 2
+    assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, 2, p, p, good, good, 8, p, p, 64) == 5

@@ -44,25 +44,27 @@ def test_act_quantize_bit_exact(bits):
     np.testing.assert_array_equal(Cq.cpu().numpy().astype(np.int64), Co)
 
 
-@pytest.mark.parametrize("bits", [8, 6])
+@pytest.mark.parametrize("cbits,bits", [(2, 8), (2, 6), (4, 4), (4, 8)])
 @pytest.mark.parametrize("xdt", ["f32", "bf16"])
 @pytest.mark.parametrize("n", [1, 3, 8, 11])
-def test_frame_apply_tff_actq_parity(bits, xdt, n):
+def test_frame_apply_tff_actq_parity(cbits, bits, xdt, n):
+    """2-bit codes with 8- and 6-bit activations, 4-bit codes with 4- and 8-bit activations
+    (the appendix's W4/A4); K_in = 148 (partial code words for both widths)."""
     torch = need_gpu()
     import paper_2403_06082_amd as fq
     Fo, Po = _frame(torch, fq, 200, 55, 4, 5)
     Fi, _ = _frame(torch, fq, 136, 37, 4, 6)
-    rng = np.random.default_rng(3 * n + bits + len(xdt))
-    codes = rng.integers(0, 4, size=(220, 148))
+    rng = np.random.default_rng(3 * n + bits + len(xdt) + 7 * cbits)
+    codes = rng.integers(0, 1 << cbits, size=(220, 148))
     scale = rng.uniform(0.01, 0.1, 220).astype(np.float32)
-    zero = rng.integers(0, 4, 220).astype(np.float32)
+    zero = rng.integers(0, 1 << cbits, 220).astype(np.float32)
     Xs = gen.to_device_storage(rng.standard_normal((n, 136)).astype(np.float32), xdt)
     X = upload(Xs, xdt)
     ws = torch.full((fq.fq_frame_apply_tff_actq_workspace_bytes(Fo, Fi),), 0xFF, dtype=torch.uint8,
                     device="cuda")
-    words = torch.from_numpy(O.pack2(codes).view(np.int32)).cuda()
+    words = torch.from_numpy(O.pack_bits(codes, cbits).view(np.int32)).cuda()
     Y = fq.fq_frame_apply_tff_actq(X, words, torch.from_numpy(scale).cuda(),
-                                   torch.from_numpy(zero).cuda(), Fo, Fi, bits, ws=ws)
+                                   torch.from_numpy(zero).cuda(), Fo, Fi, bits, ws=ws, bits=cbits)
     U = fq.fq_tff_analysis(X, Fi)
     torch.cuda.synchronize()
     Yo = O.frame_apply_rtn_activations(U.cpu().numpy(), codes, scale.astype(np.float64),
