@@ -287,9 +287,12 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
                     "the code kernel's VALU work at 8"}
 
 
-def grid_variants_bench(torch, dev, wl, L, K_out, K_in, n, steps):
+def grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, steps, iters=200):
     """The same pass with 3- and 4-bit grids (one warmup, then `steps` timed passes each;
-    one stream), as quantized weights per second."""
+    one stream), as quantized weights per second; then the 4-bit codes of that pass run
+    through the integer inference path at 4-bit activations (W4/A4), 1 and 8 tokens."""
+    import paper_2403_06082_amd as fq
+    from fq_inputs import gen
     from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
     out = {}
     for bits in (3, 4):
@@ -310,6 +313,30 @@ def grid_variants_bench(torch, dev, wl, L, K_out, K_in, n, steps):
         out[f"bits{bits}"] = {"ms_per_step": round(ms, 3),
                               "weights_per_s": round(L.d_out * L.d_in / (ms / 1e3), 1)}
         print(f"[bench] {bits}-bit pass: {ms:.2f} ms/step", file=sys.stderr, flush=True)
+        if bits == 4:
+            (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, li)
+            up = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+            Fo = fq.Frame(L.d_out, ko, ro, up(R1o), up(R2o))
+            Fi = fq.Frame(L.d_in, ki, ri, up(R1i), up(R2i))
+            stream = torch.cuda.current_stream()
+            ws = torch.empty(fq.fq_frame_apply_tff_actq_workspace_bytes(Fo, Fi), dtype=torch.uint8,
+                             device="cuda")
+            rows = []
+            for nt in (1, 8):
+                X = dev["X"][:nt]
+                Y = torch.empty((nt, L.d_out), dtype=torch.float32, device="cuda")
+
+                def call():
+                    fq.fq_frame_apply_tff_actq(X, b.codes, b.scale, b.zero, Fo, Fi, 4, Y=Y, ws=ws,
+                                               stream=stream, bits=4)
+
+                us = _time_calls(torch, call, stream, iters)
+                rows.append({"tokens": nt, "us_per_call": round(us, 2),
+                             "tokens_per_s": round(nt / (us / 1e6), 1)})
+                print(f"[bench] W4/A4 structured inference {nt} token(s): {us:.1f} us/call",
+                      file=sys.stderr, flush=True)
+            out["w4a4_inference"] = {"op": "fq_frame_apply_tff_actq, bits 4, act_bits 4, on the "
+                                           "4-bit pass's codes", "per_tokens": rows}
         del b
     return out
 
@@ -625,7 +652,7 @@ def main():
     inf["structured"] = structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in)
     out["inference"] = inf
     out["frame_generation"] = frame_generation_bench(fq, torch, dev, wl, li, host)
-    out["grid_variants"] = grid_variants_bench(torch, dev, wl, L, K_out, K_in, n, args.steps)
+    out["grid_variants"] = grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, args.steps)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
