@@ -260,6 +260,48 @@ fq_status fq_tff_materialize(void* stream, const fq_tff* frame, float* P, int64_
 size_t fq_tff_materialize_workspace_bytes(const fq_tff* frame);
 
 /*
+ * S2 with both frames given by their construction (Alg. 1 step 1 and the proxy loss of
+ * Sec. 3, with P = (R1 (x) R2) T / sqrt(k) of Sec. 2.2 and the appendix on constructing
+ * TFFs): D = P_out^T W P_in and Ht = P_in^T H P_in, the same results as fq_frame_analysis
+ * with the materialized frames, computed without them.  Each two-sided product is two
+ * row transforms (rotation, then the per-block DFT as batched MFMA products) with a
+ * transpose between them: 2 d k + d (d1 + d2) multiply-adds per row and side instead of
+ * d k rho.
+ *   W          device, d_out x d_in row-major (d_out = frame_out->d, d_in = frame_in->d),
+ *              element type wt (FQ_F32, FQ_F16, FQ_BF16); may be NULL when D is NULL.
+ *   H          device fp32 d_in x d_in (symmetric); may be NULL when Ht is NULL.
+ *   D          device fp32 K_out x K_in (K = k rho) or NULL.
+ *   Ht         device fp32 K_in x K_in or NULL; written as (B + B^T) / 2 of the computed
+ *              product B, so exactly symmetric.
+ * Frames as fq_tff_analysis; in addition d <= 2^21 and K <= 2^21 (else
+ * FQ_ERR_UNSUPPORTED).  ws: fq_frame_analysis_tff_workspace_bytes(wt, frame_out,
+ * frame_in) bytes, 16-byte aligned.  Stream-ordered; errors as fq_frame_analysis.
+ */
+fq_status fq_frame_analysis_tff(void* stream, const void* W, int wt, const fq_tff* frame_out,
+                                const fq_tff* frame_in, const float* H, float* D, float* Ht,
+                                void* ws, size_t ws_bytes);
+size_t fq_frame_analysis_tff_workspace_bytes(int wt, const fq_tff* frame_out,
+                                             const fq_tff* frame_in);
+
+/*
+ * S4 with both frames given by their construction (Alg. 1 return value; the appendix on
+ * inference cost): W_hat = P_out diag(scale)(Q - zero) P_in^T from the packed codes of
+ * `bits` bits (2, 3 or 4; packed as fq_quantize_frames packs them), the same result as
+ * fq_frame_synthesis_nbit with the materialized frames.  Two row syntheses (per-block DFT
+ * as batched MFMA products, then the rotation) with a gather between them.
+ *   codes, scale, zero  as fq_frame_synthesis_nbit, K_out = frame_out->k rho,
+ *                       K_in = frame_in->k rho.
+ *   W_hat               device fp32 frame_out->d x frame_in->d.
+ * Frames and limits as fq_frame_analysis_tff.  ws: fq_frame_synthesis_tff_workspace_bytes
+ * (frame_out, frame_in) bytes, 16-byte aligned.  Stream-ordered; errors as
+ * fq_frame_synthesis.
+ */
+fq_status fq_frame_synthesis_tff(void* stream, const uint32_t* codes, int bits,
+                                 const float* scale, const float* zero, const fq_tff* frame_out,
+                                 const fq_tff* frame_in, float* W_hat, void* ws, size_t ws_bytes);
+size_t fq_frame_synthesis_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
+
+/*
  * Rounding of the frame representation of activations to act_bits-bit integers (appendix
  * "FrameQuant for Activation Quantization?"): per token t (row of U),
  * Delta_t = max_j |U_tj| / (2^(act_bits-1) - 1) and Cq_tj = round(U_tj / Delta_t), with

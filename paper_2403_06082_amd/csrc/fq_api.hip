@@ -982,4 +982,180 @@ fq_status fq_tff_materialize(void* stream, const fq_tff* frame, float* P, int64_
   return FQ_OK;
 }
 
+// ================================================================ structured S2 / S4
+static constexpr int64_t TFFP_MAX = (int64_t)1 << 21;   // d and K limit of the structured pass
+
+static fq_status tffp_check(const fq_tff* f, const char* which, TffDev* F) {
+  fq_status st = tff_check(f, which, F);
+  if (st != FQ_OK) return st;
+  if (F->d > TFFP_MAX || F->k * F->rho > TFFP_MAX) {
+    char msg[128];
+    snprintf(msg, sizeof msg, "%s: d and k * rho must not exceed 2^21 here", which);
+    return fail(FQ_ERR_UNSUPPORTED, msg);
+  }
+  return FQ_OK;
+}
+
+static TffDev tff_dev_of(const fq_tff* f) {
+  TffDev F;
+  F.d = f->d; F.k = f->k; F.rho = f->rho; F.m = f->d / f->rho;
+  F.R1 = f->R1; F.d1 = (int)f->d1; F.R2 = f->R2; F.d2 = (int)f->d2;
+  return F;
+}
+
+static bool tffp_dims_ok(const fq_tff* f) {
+  return tff_dims_ok(f) && f->d <= TFFP_MAX && f->k * f->rho <= TFFP_MAX;
+}
+
+// F_c planes of both frames, then the stage buffers (the largest stage of each).
+struct TffAnaLayout {
+  u16 *fi_hi, *fi_lo, *fo_hi, *fo_lo;   // F_c planes of frame_in / frame_out
+  float* tmp;                           // rotation scratch, aliased with the DFT output
+  u16 *y_hi, *y_lo;                     // rotated rows, block order
+  float* mid;                           // (W P_in)^T or (H P_in)^T
+};
+
+static size_t tff_ana_layout(const fq_tff* fo, const fq_tff* fi, void* base, TffAnaLayout* L) {
+  const TffDev Fo = tff_dev_of(fo), Fi = tff_dev_of(fi);
+  const TffPassGeom go = tff_pass_geom(Fo), gi = tff_pass_geom(Fi);
+  const int64_t d_out = fo->d, d_in = fi->d, K_out = fo->k * fo->rho, K_in = fi->k * fi->rho;
+  const int64_t tmp = std::max({d_out * std::max(d_in, K_in), K_in * std::max(d_out, K_out),
+                                d_in * std::max(d_in, K_in), K_in * std::max(d_in, K_in)});
+  const int64_t yp = std::max({d_out * gi.nb * gi.pm, K_in * go.nb * go.pm,
+                               std::max(d_in, K_in) * gi.nb * gi.pm});
+  const int64_t mid = K_in * std::max(d_out, d_in);
+  Carver c(base);
+  TffAnaLayout l{};
+  l.fi_hi = c.take<u16>((size_t)(gi.nb * gi.pm * gi.pk));
+  l.fi_lo = c.take<u16>((size_t)(gi.nb * gi.pm * gi.pk));
+  l.fo_hi = c.take<u16>((size_t)(go.nb * go.pm * go.pk));
+  l.fo_lo = c.take<u16>((size_t)(go.nb * go.pm * go.pk));
+  l.tmp = c.take<float>((size_t)tmp);
+  l.y_hi = c.take<u16>((size_t)yp);
+  l.y_lo = c.take<u16>((size_t)yp);
+  l.mid = c.take<float>((size_t)mid);
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+size_t fq_frame_analysis_tff_workspace_bytes(int wt, const fq_tff* frame_out,
+                                             const fq_tff* frame_in) {
+  if (wt < 0 || wt > 2 || !tffp_dims_ok(frame_out) || !tffp_dims_ok(frame_in)) return 0;
+  return tff_ana_layout(frame_out, frame_in, nullptr, nullptr);
+}
+
+fq_status fq_frame_analysis_tff(void* stream, const void* W, int wt, const fq_tff* frame_out,
+                                const fq_tff* frame_in, const float* H, float* D, float* Ht,
+                                void* ws, size_t ws_bytes) {
+  if (wt < FQ_F32 || wt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "wt must be FQ_F32, FQ_F16 or FQ_BF16");
+  TffDev Fo, Fi;
+  fq_status st = tffp_check(frame_out, "frame_out", &Fo);
+  if (st != FQ_OK) return st;
+  if ((st = tffp_check(frame_in, "frame_in", &Fi)) != FQ_OK) return st;
+  if (D && !W) return fail(FQ_ERR_INVALID_ARG, "W is required for D");
+  if (Ht && !H) return fail(FQ_ERR_INVALID_ARG, "H is required for Ht");
+  const size_t need = tff_ana_layout(frame_out, frame_in, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_analysis_tff_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  if (!D && !Ht) return FQ_OK;
+  hipStream_t s = (hipStream_t)stream;
+  TffAnaLayout L;
+  tff_ana_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  const int64_t K_out = Fo.k * Fo.rho, K_in = Fi.k * Fi.rho;
+  hipError_t e;
+  if ((e = tff_dft_blocks(Fi, L.fi_hi, L.fi_lo, s)) != hipSuccess) return hip_fail(e, "frame_in blocks");
+  if (D) {
+    if ((e = tff_dft_blocks(Fo, L.fo_hi, L.fo_lo, s)) != hipSuccess) return hip_fail(e, "frame_out blocks");
+    // (W P_in)^T: K_in x d_out
+    if ((e = tff_rows_analysis_t(W, wt, Fi.d, Fo.d, Fi, L.fi_hi, L.fi_lo, L.tmp, L.y_hi, L.y_lo,
+                                 L.tmp, L.mid, Fo.d, s)) != hipSuccess)
+      return hip_fail(e, "analysis of the rows of W");
+    // D = ((W P_in)^T P_out)^T: K_out x K_in
+    if ((e = tff_rows_analysis_t(L.mid, FQ_F32, Fo.d, K_in, Fo, L.fo_hi, L.fo_lo, L.tmp, L.y_hi,
+                                 L.y_lo, L.tmp, D, K_in, s)) != hipSuccess)
+      return hip_fail(e, "analysis of the columns of W P_in");
+  }
+  if (Ht) {
+    // (H P_in)^T: K_in x d_in, then Ht = ((H P_in)^T P_in)^T, symmetrized
+    if ((e = tff_rows_analysis_t(H, FQ_F32, Fi.d, Fi.d, Fi, L.fi_hi, L.fi_lo, L.tmp, L.y_hi,
+                                 L.y_lo, L.tmp, L.mid, Fi.d, s)) != hipSuccess)
+      return hip_fail(e, "analysis of the rows of H");
+    if ((e = tff_rows_analysis_t(L.mid, FQ_F32, Fi.d, K_in, Fi, L.fi_hi, L.fi_lo, L.tmp, L.y_hi,
+                                 L.y_lo, L.tmp, Ht, K_in, s)) != hipSuccess)
+      return hip_fail(e, "analysis of the columns of H P_in");
+    if ((e = sym_average(Ht, K_in, K_in, s)) != hipSuccess) return hip_fail(e, "symmetrize Ht");
+  }
+  (void)K_out;
+  return FQ_OK;
+}
+
+struct TffSynLayout {
+  u16 *fi_hi, *fi_lo, *fo_hi, *fo_lo;
+  u16* v1;              // codes - zero, block order of frame_in (K_out rows)
+  u16 *v2_hi, *v2_lo;   // scaled (Q - zero) P_in^T transposed, block order of frame_out
+  float *z, *tmp, *mid;
+};
+
+static size_t tff_syn_layout(const fq_tff* fo, const fq_tff* fi, void* base, TffSynLayout* L) {
+  const TffDev Fo = tff_dev_of(fo), Fi = tff_dev_of(fi);
+  const TffPassGeom go = tff_pass_geom(Fo), gi = tff_pass_geom(Fi);
+  const int64_t d_out = fo->d, d_in = fi->d, K_out = fo->k * fo->rho;
+  const int64_t big = std::max(K_out * d_in, d_in * d_out);
+  Carver c(base);
+  TffSynLayout l{};
+  l.fi_hi = c.take<u16>((size_t)(gi.nb * gi.pm * gi.pk));
+  l.fi_lo = c.take<u16>((size_t)(gi.nb * gi.pm * gi.pk));
+  l.fo_hi = c.take<u16>((size_t)(go.nb * go.pm * go.pk));
+  l.fo_lo = c.take<u16>((size_t)(go.nb * go.pm * go.pk));
+  l.v1 = c.take<u16>((size_t)(K_out * gi.nb * gi.pk));
+  l.v2_hi = c.take<u16>((size_t)(d_in * go.nb * go.pk));
+  l.v2_lo = c.take<u16>((size_t)(d_in * go.nb * go.pk));
+  l.z = c.take<float>((size_t)big);
+  l.tmp = c.take<float>((size_t)big);
+  l.mid = c.take<float>((size_t)big);
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+size_t fq_frame_synthesis_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in) {
+  if (!tffp_dims_ok(frame_out) || !tffp_dims_ok(frame_in)) return 0;
+  return tff_syn_layout(frame_out, frame_in, nullptr, nullptr);
+}
+
+fq_status fq_frame_synthesis_tff(void* stream, const uint32_t* codes, int bits,
+                                 const float* scale, const float* zero, const fq_tff* frame_out,
+                                 const fq_tff* frame_in, float* W_hat, void* ws, size_t ws_bytes) {
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
+  TffDev Fo, Fi;
+  fq_status st = tffp_check(frame_out, "frame_out", &Fo);
+  if (st != FQ_OK) return st;
+  if ((st = tffp_check(frame_in, "frame_in", &Fi)) != FQ_OK) return st;
+  if (!codes || !scale || !zero || !W_hat) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  const size_t need = tff_syn_layout(frame_out, frame_in, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_synthesis_tff_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  TffSynLayout L;
+  tff_syn_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  const int64_t K_out = Fo.k * Fo.rho;
+  hipError_t e;
+  if ((e = tff_dft_blocks(Fi, L.fi_hi, L.fi_lo, s)) != hipSuccess) return hip_fail(e, "frame_in blocks");
+  if ((e = tff_dft_blocks(Fo, L.fo_hi, L.fo_lo, s)) != hipSuccess) return hip_fail(e, "frame_out blocks");
+  // M = (Q - zero) P_in^T: K_out x d_in
+  if ((e = tff_dequant_gather(codes, bits, zero, K_out, Fi, L.v1, s)) != hipSuccess)
+    return hip_fail(e, "dequant");
+  if ((e = tff_rows_synthesis(L.v1, nullptr, K_out, Fi, L.fi_hi, L.fi_lo, L.z, L.tmp, L.mid,
+                              Fi.d, s)) != hipSuccess)
+    return hip_fail(e, "synthesis of the code rows");
+  // W_hat^T = (diag(scale) M)^T P_out^T: d_in x d_out, then transposed
+  if ((e = tff_gather_rows(L.mid, Fi.d, Fi.d, scale, Fo, L.v2_hi, L.v2_lo, s)) != hipSuccess)
+    return hip_fail(e, "gather");
+  if ((e = tff_rows_synthesis(L.v2_hi, L.v2_lo, Fi.d, Fo, L.fo_hi, L.fo_lo, L.z, L.tmp, L.mid,
+                              Fo.d, s)) != hipSuccess)
+    return hip_fail(e, "synthesis of the columns");
+  if ((e = transpose_f32(L.mid, Fi.d, Fo.d, Fo.d, W_hat, Fi.d, s)) != hipSuccess)
+    return hip_fail(e, "transpose");
+  return FQ_OK;
+}
+
 }  // extern "C"

@@ -46,6 +46,10 @@ struct GemmDesc {
   int ksplit = 1;                // EPI_PARTIAL only
   const char* name = "gemm";     // kernel-timer label
   int64_t ldc_pad = 0;           // EPI_SPLIT: output columns [N, ldc_pad) are zeroed
+  // batch > 1 (EPI_F32 only): products z < batch read A + z bsa, B + z bsb and write
+  // C + z bsc (element strides; bsa and bsb multiples of 8)
+  int batch = 1;
+  int64_t bsa = 0, bsb = 0, bsc = 0;
 };
 
 // Workspace bytes needed by EPI_PARTIAL for an N x N symmetric product split ksplit ways.
@@ -110,6 +114,34 @@ hipError_t tff_materialize(const TffDev& F, const float* R2t, float* Z, float* P
                            float* P, int64_t ldp, hipStream_t s);
 // R2t (d2 x d2) = R2^T, read by tff_synthesis
 hipError_t tff_transpose_r2(const TffDev& F, float* R2t, hipStream_t s);
+
+// Structured analysis / synthesis of whole matrices (tff_pass.hip).  Block geometry of a
+// frame: nb = rho / 2 blocks of m2 = 2m real coordinates (padded to pm) and k2 = 2k
+// frame coordinates (padded to pk), pads multiples of 32.
+struct TffPassGeom { int64_t nb, m2, pm, k2, pk; };
+TffPassGeom tff_pass_geom(const TffDev& F);
+// F_c for all blocks: bf16 (hi, lo) planes of nb x pm x pk each
+hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s);
+// out (K x n at stride ldout) = (X P)^T for n rows of X (element type xt, stride ldx).
+// Scratch: tmp / O one fp32 buffer of max(n d, n K) (they may alias), Y pair planes of
+// n x nb pm each.
+hipError_t tff_rows_analysis_t(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F,
+                               const u16* Fhi, const u16* Flo, float* tmp, u16* Yhi, u16* Ylo,
+                               float* O, float* out, int64_t ldout, hipStream_t s);
+// V planes (n x nb pk, block order) from M (K x n, stride ldm) with row q scaled by scale[q]
+hipError_t tff_gather_rows(const float* M, int64_t ldm, int64_t n, const float* scale,
+                           const TffDev& F, u16* hi, u16* lo, hipStream_t s);
+// V plane (rows x nb pk, block order) = codes - zero, exact bf16
+hipError_t tff_dequant_gather(const uint32_t* codes, int bits, const float* zero, int64_t rows,
+                              const TffDev& F, u16* V, hipStream_t s);
+// out (n x d at stride ldout) = V P^T from block-order planes (Vlo may be NULL); Z, tmp:
+// n x d fp32 scratch each
+hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const TffDev& F,
+                              const u16* Fhi, const u16* Flo, float* Z, float* tmp, float* out,
+                              int64_t ldout, hipStream_t s);
+hipError_t transpose_f32(const float* in, int64_t rows, int64_t cols, int64_t ldin, float* out,
+                         int64_t ldout, hipStream_t s);
+hipError_t sym_average(float* X, int64_t n, int64_t ld, hipStream_t s);
 // Y (n x ldy) = V P^T with V n x ldv (ldv even), R2t from tff_transpose_r2; z: n x d scratch
 hipError_t tff_synthesis(const float* V, int64_t ldv, int64_t n, const TffDev& F,
                          const float* R2t, float* z, float* Y, int64_t ldy, hipStream_t s);

@@ -461,6 +461,7 @@ struct AParams {
   float* part;
   int tile0, tcount;    // this launch covers tiles [tile0, tile0 + tcount) (x ksplit)
   int ra, rb;           // row extents the operand loads are clamped to (see gemm_run)
+  int64_t bsa, bsb, bsc;  // element strides of A, B and C between the products of a batch
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -643,13 +644,14 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
 
   // Operand origins of each pass for this work-group's K range; inside a pass the stage
   // origin advances by a fixed byte step, so the issue path is pointer increments only.
+  const int64_t bz = blockIdx.y;                 // product of a batch (0 when unbatched)
   auto a_origin = [&](int sel) {
-    const u16* a = sel ? p.a1 : p.a0;
+    const u16* a = (sel ? p.a1 : p.a0) + bz * p.bsa;
     return reinterpret_cast<const char*>(AMN ? a + (int64_t)kbeg * p.lda + m0
                                              : a + (int64_t)m0 * p.lda + kbeg);
   };
   auto b_origin = [&](int sel) {
-    const u16* b = sel ? p.b1 : p.b0;
+    const u16* b = (sel ? p.b1 : p.b0) + bz * p.bsb;
     return reinterpret_cast<const char*>(BMN ? b + (int64_t)kbeg * p.ldb + n0
                                              : b + (int64_t)n0 * p.ldb + kbeg);
   };
@@ -803,7 +805,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
         } else if (EPI == EPI_TAIL) {
           p.part[((int64_t)split * p.tcount + tloc) * (BM * BN) + rl * BN + cl] = x;
         } else if (EPI == EPI_F32) {
-          if (col < p.N) p.c[(int64_t)row * p.ldc + col] = x;
+          if (col < p.N) p.c[bz * p.bsc + (int64_t)row * p.ldc + col] = x;
         } else if (EPI == EPI_SPLIT) {
           if (col < p.ldc_pad) {
             const bool in = col < p.N;
@@ -1102,7 +1104,9 @@ size_t gemm_partial_bytes(int N, int ksplit) {
 }
 
 hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
-  if (d.M <= 0 || d.N <= 0) return hipSuccess;
+  if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
+  if (d.batch > 1 && (d.epi != EPI_F32 || d.batch > 65535 || d.bsa % 8 || d.bsb % 8))
+    return hipErrorInvalidValue;
   KParams p{};
   p.M = d.M; p.N = d.N; p.K = d.K;
   p.a0 = d.a[0]; p.a1 = d.a[1] ? d.a[1] : d.a[0];
@@ -1149,9 +1153,11 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     q.ksplit = p.ksplit; q.k_per_split = p.k_per_split; q.part = partial;
     q.ra = d.a_kmajor ? d.M : m8;
     q.rb = d.b_kmajor ? d.N : n8;
+    q.bsa = d.bsa; q.bsb = d.bsb; q.bsc = d.bsc;
+    const unsigned nbatch = (unsigned)d.batch;
     prof_begin(s, d.name);
 #define FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, E, G)                                                        \
-    hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, E, 8>), dim3(G), dim3(512), 0, s, q);
+    hipLaunchKernelGGL((k_gemm_async<AMN, BMN, F16, E, 8>), dim3(G, nbatch), dim3(512), 0, s, q);
 #define FQ_LAUNCH_ASYNC(AMN, BMN, F16, E, G)                                                           \
     switch (E) {                                                                                        \
       case EPI_F32: FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, EPI_F32, G) break;                                 \
@@ -1183,7 +1189,7 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     if (ts > ksteps / 4) ts = ksteps / 4;
     const int kps = ts > 0 ? (ksteps + ts - 1) / ts : 0;   // k-steps per slice
     if (kps > 0) ts = (ksteps + kps - 1) / kps;              // no empty slice
-    const bool use_tail = partial && rounds >= 2 && tail <= cus / 2 && ts >= 2 &&
+    const bool use_tail = partial && d.batch == 1 && rounds >= 2 && tail <= cus / 2 && ts >= 2 &&
                           (d.epi == EPI_F32 || d.epi == EPI_SPLIT) &&
                           (size_t)tail * ts * BM * BN * sizeof(float) <= gemm_tail_bytes();
     if (use_tail) {
@@ -1210,6 +1216,7 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     prof_end(s);
     return last_launch_error();
   }
+  if (d.batch != 1) return hipErrorInvalidValue;   // batches run on the asynchronous path only
   prof_begin(s, d.name);
   bool ok;
   if (d.a_kmajor && d.b_kmajor) {

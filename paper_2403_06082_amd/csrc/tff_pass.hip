@@ -1,0 +1,477 @@
+// The analysis D = P_out^T W P_in, H~ = P_in^T H P_in and the synthesis
+// W^ = P_out diag(scale)(Q - zero) P_in^T with both frames applied from their
+// construction P = (R1 (x) R2) T / sqrt(k) (Sec. 2.2 and the appendix on constructing
+// TFFs; the appendix on inference cost counts this route), for whole weight matrices.
+//
+// Every two-sided product is two passes of a one-sided row transform with a transpose
+// between them: D^T = (W P_in)^T P_out, so D is the transposed row analysis (by P_out) of
+// the transposed row analysis (by P_in) of W.  A row transform has two parts:
+//  - the rotation R1^T M R2 (analysis) or R1 M R2^T (synthesis) of each row read as a
+//    d1 x d2 matrix M: two batched small products on the vector ALU (k_rot_step);
+//  - the DFT part, which acts on the rho/2 blocks of 2m real coordinates separately:
+//    block c of an analysed row is y_c F_c with F_c the real 2m x 2k matrix
+//      F_c[2j][2s] = F_c[2j+1][2s+1] = cos(phi) / sqrt(k),
+//      F_c[2j][2s+1] = -sin(phi) / sqrt(k),  F_c[2j+1][2s] = sin(phi) / sqrt(k),
+//      phi = 2 pi ((c m + j) s mod k) / k,
+//    (conj(w^((cm+j)s)) times the complex coordinate, realified), and a synthesised row is
+//    v_c F_c^T.  All rows of all blocks are one batch of rho/2 MFMA products (bf16 pairs,
+//    fp32 accumulation), 2 d k multiply-adds per row instead of the dense d k rho.
+// Block c of an analysed row fills frame columns s rho + 2c + e (e = 0, 1); the gathers
+// below move between that order and the block order of the products.
+#include "fq_internal.h"
+
+#include <cmath>
+
+namespace fq {
+namespace {
+
+constexpr int TT = 256;
+constexpr int RB = 64;       // rotation output tile (RB x RB per work-group of one wave)
+constexpr int RK = 16;       // rotation k step
+
+template <typename T>
+__device__ __forceinline__ float ldx_f32(const T* p);
+template <>
+__device__ __forceinline__ float ldx_f32<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float ldx_f32<uint16_t>(const uint16_t* p) {   // bf16
+  return __uint_as_float((uint32_t)*p << 16);
+}
+template <>
+__device__ __forceinline__ float ldx_f32<_Float16>(const _Float16* p) { return (float)*p; }
+
+__device__ __forceinline__ uint32_t rne_bf16(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+struct RotOut {
+  float* f; int64_t ldf;               // fp32 rows (row t at f + t ldf)
+  u16* hi; u16* lo; int64_t ldp;       // bf16 pair rows in block layout (row t at + t ldp)
+  int bw, pb;                          // block layout: coordinate p sits at (p / bw) pb + p % bw
+};
+
+// One factor of the rotation for n vectors, each read as a d1 x d2 row-major matrix X_t:
+// XL: C_t = X_t S (S d2 x d2), else C_t = S X_t (S d1 x d1); S(a, b) = S[b][a] when ST.
+// A work-group (one wave) owns a 64 x 64 tile of one C_t, 8 x 8 outputs per lane, fp32
+// FMAs over k steps of 16 staged in LDS.  grid (n * ceil(d1/64) * ceil(d2/64)).
+// OUT 0: fp32 rows; OUT 1: bf16 (hi, lo) rows in block layout.
+template <typename XT, bool XL, bool ST, int OUT>
+__global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64_t ldx,
+                                                 const float* __restrict__ S, int d1, int d2,
+                                                 RotOut o) {
+  __shared__ __attribute__((aligned(16))) float As[RK][RB + 4];
+  __shared__ __attribute__((aligned(16))) float Bs[RK][RB + 4];
+  const int tr = (d1 + RB - 1) / RB, tc = (d2 + RB - 1) / RB;
+  const int64_t blk = blockIdx.x;
+  const int64_t t = blk / (tr * tc);
+  const int rem = (int)(blk - t * (tr * tc));
+  const int i0 = (rem / tc) * RB, j0 = (rem % tc) * RB;
+  const int lane = threadIdx.x;
+  const int tx = lane & 7, ty = lane >> 3;
+  const int Kd = XL ? d2 : d1;
+  const XT* x = X + t * ldx;
+  float acc[8][8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[r][q] = 0.f;
+  for (int k0 = 0; k0 < Kd; k0 += RK) {
+#pragma unroll 4
+    for (int pass = 0; pass < 16; ++pass) {
+      // A(i, k): row-contiguous in k unless it is S^T of the left factor
+      int ii, ka;
+      if (XL || !ST) { const int e = pass * 64 + lane; ka = e & 15; ii = e >> 4; }
+      else { ii = lane; ka = pass; }
+      const int gi = i0 + ii, gka = k0 + ka;
+      float av = 0.f;
+      if (gi < d1 && gka < Kd) {
+        if (XL) av = ldx_f32<XT>(x + (int64_t)gi * d2 + gka);
+        else av = ST ? S[(int64_t)gka * d1 + gi] : S[(int64_t)gi * d1 + gka];
+      }
+      As[ka][ii] = av;
+      // B(k, j): row-contiguous in j unless it is S^T of the right factor
+      int jj, kb;
+      if (!XL || !ST) { jj = lane; kb = pass; }
+      else { const int e = pass * 64 + lane; kb = e & 15; jj = e >> 4; }
+      const int gj = j0 + jj, gkb = k0 + kb;
+      float bv = 0.f;
+      if (gj < d2 && gkb < Kd) {
+        if (!XL) bv = ldx_f32<XT>(x + (int64_t)gkb * d2 + gj);
+        else bv = ST ? S[(int64_t)gj * d2 + gkb] : S[(int64_t)gkb * d2 + gj];
+      }
+      Bs[kb][jj] = bv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < RK; ++kk) {
+      const float4 a0 = *reinterpret_cast<const float4*>(&As[kk][ty * 8]);
+      const float4 a1 = *reinterpret_cast<const float4*>(&As[kk][ty * 8 + 4]);
+      const float4 b0 = *reinterpret_cast<const float4*>(&Bs[kk][tx * 8]);
+      const float4 b1 = *reinterpret_cast<const float4*>(&Bs[kk][tx * 8 + 4]);
+      const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const float b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[r][q] = fmaf(a[r], b[q], acc[r][q]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int i = i0 + ty * 8 + r;
+    if (i >= d1) continue;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int j = j0 + tx * 8 + q;
+      if (j >= d2) continue;
+      const int64_t p = (int64_t)i * d2 + j;
+      if (OUT == 0) {
+        o.f[t * o.ldf + p] = acc[r][q];
+      } else {
+        const int64_t c = p / o.bw;
+        const int64_t idx = t * o.ldp + c * o.pb + (p - c * o.bw);
+        const uint32_t h = rne_bf16(acc[r][q]);
+        o.hi[idx] = (u16)h;
+        o.lo[idx] = (u16)rne_bf16(acc[r][q] - __uint_as_float(h << 16));
+      }
+    }
+  }
+}
+
+// Block-layout pad columns [bw, pb) of every block of n rows set to 0 (both planes).
+__global__ __launch_bounds__(TT) void k_zero_pads(u16* hi, u16* lo, int64_t n, int64_t ldp,
+                                                  int nb, int bw, int pb) {
+  const int w = pb - bw;
+  const int64_t total = n * nb * w;
+  for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * TT) {
+    const int64_t r = e / ((int64_t)nb * w);
+    const int64_t q = e - r * nb * w;
+    const int64_t c = q / w, x = q - c * w;
+    const int64_t idx = r * ldp + c * pb + bw + x;
+    hi[idx] = 0;
+    if (lo) lo[idx] = 0;
+  }
+}
+
+// F_c for c < rho/2 as bf16 (hi, lo) planes [c][pm][pk] (rows 2j + e, columns 2s + e'),
+// zero outside 2m x 2k.  One thread per entry.
+__global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm, int pk,
+                                                   float scale, u16* __restrict__ hi,
+                                                   u16* __restrict__ lo) {
+  const int64_t total = (int64_t)nb * pm * pk;
+  for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * TT) {
+    const int64_t c = e / ((int64_t)pm * pk);
+    const int64_t rc = e - c * pm * pk;
+    const int row = (int)(rc / pk), col = (int)(rc - (int64_t)(rc / pk) * pk);
+    float v = 0.f;
+    if (row < 2 * m && col < 2 * k) {
+      const int64_t j = row >> 1, s = col >> 1;
+      const int64_t ph = ((c * m + j) % k) * s % k;
+      float sn, cs;
+      sincospif(2.0f * (float)ph / (float)k, &sn, &cs);
+      const int er = row & 1, ec = col & 1;
+      v = (er == ec) ? cs : (er ? sn : -sn);
+      v *= scale;
+    }
+    const uint32_t h = rne_bf16(v);
+    hi[e] = (u16)h;
+    lo[e] = (u16)rne_bf16(v - __uint_as_float(h << 16));
+  }
+}
+
+// out[(p/2) rho + 2c + (p&1)][t] = O[c][t][p] for p < 2k, t < n (O blocks of n x ldo);
+// 32 x 32 tiles through LDS.  grid (ceil(2k/32) * ceil(n/32), rho/2).
+__global__ __launch_bounds__(TT) void k_gather_t(const float* __restrict__ O, int64_t n,
+                                                 int64_t ldo, int k2, int rho,
+                                                 float* __restrict__ out, int64_t ldout) {
+  __shared__ float tile[32][33];
+  const int c = blockIdx.y;
+  const int npb = (k2 + 31) / 32;
+  const int64_t tb = blockIdx.x / npb;
+  const int pbk = (int)(blockIdx.x - tb * npb);
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const float* Oc = O + (int64_t)c * n * ldo;
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t t = tb * 32 + q;
+    const int p = pbk * 32 + tx;
+    tile[q][tx] = (t < n && p < k2) ? Oc[t * ldo + p] : 0.f;
+  }
+  __syncthreads();
+  for (int q = ty; q < 32; q += 8) {
+    const int p = pbk * 32 + q;
+    const int64_t t = tb * 32 + tx;
+    if (p < k2 && t < n) out[((int64_t)(p >> 1) * rho + 2 * c + (p & 1)) * ldout + t] = tile[tx][q];
+  }
+}
+
+// V[t][c pk + p] = scale[q] M[q][t], q = (p/2) rho + 2c + (p&1), as bf16 (hi, lo) for
+// p < 2k, t < n; 0 for p in [2k, pk).  M is K x n (rows q at stride ldm); scale may be
+// NULL (1).  grid (ceil(pk/32) * ceil(n/32), rho/2).
+__global__ __launch_bounds__(TT) void k_gather(const float* __restrict__ M, int64_t ldm, int64_t n,
+                                               const float* __restrict__ scale, int k2, int pk,
+                                               int rho, u16* __restrict__ hi,
+                                               u16* __restrict__ lo, int64_t ldv) {
+  __shared__ float tile[32][33];
+  const int c = blockIdx.y;
+  const int npb = pk / 32;
+  const int64_t tb = blockIdx.x / npb;
+  const int pbk = (int)(blockIdx.x - tb * npb);
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int q = ty; q < 32; q += 8) {
+    const int p = pbk * 32 + q;
+    const int64_t t = tb * 32 + tx;
+    float v = 0.f;
+    if (p < k2 && t < n) {
+      const int64_t row = (int64_t)(p >> 1) * rho + 2 * c + (p & 1);
+      v = M[row * ldm + t];
+      if (scale) v *= scale[row];
+    }
+    tile[q][tx] = v;
+  }
+  __syncthreads();
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t t = tb * 32 + q;
+    const int p = pbk * 32 + tx;
+    if (t < n) {
+      const float v = tile[tx][q];
+      const uint32_t h = rne_bf16(v);
+      const int64_t idx = t * ldv + (int64_t)c * pk + p;
+      hi[idx] = (u16)h;
+      lo[idx] = (u16)rne_bf16(v - __uint_as_float(h << 16));
+    }
+  }
+}
+
+// V[r][c pk + p] = code(r, q) - zero[r] as bf16 (small integers, exact), q as in k_gather,
+// for r < rows; 0 for p in [2k, pk).  codes: cpw = floor(32 / bits) per word, row-major.
+// One thread per output element.
+__global__ __launch_bounds__(TT) void k_dequant_gather(const uint32_t* __restrict__ codes,
+                                                       int bits, const float* __restrict__ zero,
+                                                       int64_t rows, int64_t K, int k2, int pk,
+                                                       int rho, int nb, u16* __restrict__ V,
+                                                       int64_t ldv) {
+  const int cpw = 32 / bits;
+  const uint32_t mask = (1u << bits) - 1u;
+  const int64_t nw = (K + cpw - 1) / cpw;
+  const int64_t per = (int64_t)nb * pk;
+  const int64_t total = rows * per;
+  for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * TT) {
+    const int64_t r = e / per;
+    const int64_t rc = e - r * per;
+    const int c = (int)(rc / pk), p = (int)(rc - (int64_t)c * pk);
+    uint32_t h = 0;
+    if (p < k2) {
+      const int64_t q = (int64_t)(p >> 1) * rho + 2 * c + (p & 1);
+      const int64_t w = q / cpw;
+      const uint32_t code = (codes[r * nw + w] >> (bits * (int)(q - w * cpw))) & mask;
+      h = __float_as_uint((float)code - zero[r]) >> 16;
+    }
+    V[r * ldv + rc] = (u16)h;
+  }
+}
+
+// out[j][i] = in[i][j] for i < rows, j < cols; 32 x 32 tiles through LDS.
+__global__ __launch_bounds__(TT) void k_transpose_rect(const float* __restrict__ in, int64_t rows,
+                                                       int64_t cols, int64_t ldin,
+                                                       float* __restrict__ out, int64_t ldout) {
+  __shared__ float tile[32][33];
+  const int64_t ncb = (cols + 31) / 32;
+  const int64_t bi = blockIdx.x / ncb, bj = blockIdx.x - bi * ncb;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t i = bi * 32 + q, j = bj * 32 + tx;
+    tile[q][tx] = (i < rows && j < cols) ? in[i * ldin + j] : 0.f;
+  }
+  __syncthreads();
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t j = bj * 32 + q, i = bi * 32 + tx;
+    if (i < rows && j < cols) out[j * ldout + i] = tile[tx][q];
+  }
+}
+
+// X = (X + X^T) / 2 in place (n x n at stride ld): work-group (bi, bj), bi <= bj, owns the
+// tiles (bi, bj) and (bj, bi).  grid (T, T), T = ceil(n / 32); bi > bj return at once.
+__global__ __launch_bounds__(TT) void k_sym_average(float* __restrict__ X, int64_t n, int64_t ld) {
+  __shared__ float a[32][33], b[32][33];
+  const int64_t bi = blockIdx.x, bj = blockIdx.y;
+  if (bi > bj) return;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t i = bi * 32 + q, j = bj * 32 + tx;
+    a[q][tx] = (i < n && j < n) ? X[i * ld + j] : 0.f;
+    const int64_t i2 = bj * 32 + q, j2 = bi * 32 + tx;
+    b[q][tx] = (i2 < n && j2 < n) ? X[i2 * ld + j2] : 0.f;
+  }
+  __syncthreads();
+  for (int q = ty; q < 32; q += 8) {
+    const int64_t i = bi * 32 + q, j = bj * 32 + tx;
+    if (i < n && j < n) X[i * ld + j] = 0.5f * (a[q][tx] + b[tx][q]);
+    const int64_t i2 = bj * 32 + q, j2 = bi * 32 + tx;
+    if (i2 < n && j2 < n) X[i2 * ld + j2] = 0.5f * (b[q][tx] + a[tx][q]);
+  }
+}
+
+unsigned grid_1d(int64_t total) {
+  const int64_t g = (total + TT - 1) / TT;
+  return (unsigned)(g < 65536 ? (g > 0 ? g : 1) : 65536);
+}
+
+// The two rotation factors of n rows.  Analysis: tmp = X R2, then R1^T tmp into `o`;
+// synthesis: tmp = X R2^T, then R1 tmp into `o`.  xt: 0 f32, 1 f16, 2 bf16 (first factor
+// only; tmp is fp32).
+template <int OUT>
+hipError_t rotate_rows(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F, bool synth,
+                       float* tmp, const RotOut& o, hipStream_t s) {
+  const int64_t tiles = (int64_t)((F.d1 + RB - 1) / RB) * ((F.d2 + RB - 1) / RB);
+  const dim3 g((unsigned)(n * tiles));
+  RotOut ot{};
+  ot.f = tmp; ot.ldf = F.d;
+  prof_begin(s, "tffp_rotate");
+  if (synth) {
+    hipLaunchKernelGGL((k_rot_step<float, true, true, 0>), g, dim3(64), 0, s, (const float*)X, ldx, F.R2, F.d1, F.d2, ot);
+    hipLaunchKernelGGL((k_rot_step<float, false, false, OUT>), g, dim3(64), 0, s, (const float*)tmp, F.d, F.R1, F.d1, F.d2, o);
+  } else {
+    if (xt == 0)
+      hipLaunchKernelGGL((k_rot_step<float, true, false, 0>), g, dim3(64), 0, s, (const float*)X, ldx, F.R2, F.d1, F.d2, ot);
+    else if (xt == 1)
+      hipLaunchKernelGGL((k_rot_step<_Float16, true, false, 0>), g, dim3(64), 0, s, (const _Float16*)X, ldx, F.R2, F.d1, F.d2, ot);
+    else
+      hipLaunchKernelGGL((k_rot_step<uint16_t, true, false, 0>), g, dim3(64), 0, s, (const uint16_t*)X, ldx, F.R2, F.d1, F.d2, ot);
+    hipLaunchKernelGGL((k_rot_step<float, false, true, OUT>), g, dim3(64), 0, s, (const float*)tmp, F.d, F.R1, F.d1, F.d2, o);
+  }
+  prof_end(s);
+  return last_launch_error();
+}
+
+}  // namespace
+
+TffPassGeom tff_pass_geom(const TffDev& F) {
+  TffPassGeom g;
+  g.nb = F.rho / 2;
+  g.m2 = 2 * F.m;
+  g.pm = (g.m2 + 31) / 32 * 32;
+  g.k2 = 2 * F.k;
+  g.pk = (g.k2 + 31) / 32 * 32;
+  return g;
+}
+
+hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s) {
+  const TffPassGeom g = tff_pass_geom(F);
+  prof_begin(s, "tffp_blocks");
+  hipLaunchKernelGGL(k_dft_blocks, dim3(grid_1d(g.nb * g.pm * g.pk)), dim3(TT), 0, s, (int)F.k,
+                     (int)F.m, (int)g.nb, (int)g.pm, (int)g.pk,
+                     (float)(1.0 / std::sqrt((double)F.k)), hi, lo);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t tff_rows_analysis_t(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F,
+                               const u16* Fhi, const u16* Flo, float* tmp, u16* Yhi, u16* Ylo,
+                               float* O, float* out, int64_t ldout, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const TffPassGeom g = tff_pass_geom(F);
+  const int64_t ldy = g.nb * g.pm;
+  RotOut o{};
+  o.hi = Yhi; o.lo = Ylo; o.ldp = ldy; o.bw = (int)g.m2; o.pb = (int)g.pm;
+  hipError_t e;
+  if (g.pm > g.m2) {
+    prof_begin(s, "tffp_rotate");
+    hipLaunchKernelGGL(k_zero_pads, dim3(grid_1d(n * g.nb * (g.pm - g.m2))), dim3(TT), 0, s, Yhi, Ylo,
+                       n, ldy, (int)g.nb, (int)g.m2, (int)g.pm);
+    prof_end(s);
+  }
+  if ((e = rotate_rows<1>(X, xt, ldx, n, F, false, tmp, o, s)) != hipSuccess) return e;
+  // O[c] (n x 2k) = Y[:, c pm .. c pm + pm) F_c, all blocks in one batch
+  GemmDesc d;
+  d.M = (int)n; d.N = (int)g.k2; d.K = (int)g.pm;
+  d.a[0] = Yhi; d.a[1] = Ylo; d.lda = ldy; d.a_kmajor = true;
+  d.b[0] = Fhi; d.b[1] = Flo; d.ldb = g.pk; d.b_kmajor = false;
+  d.npass = 3;
+  d.pa[0] = 0; d.pb[0] = 0; d.pa[1] = 0; d.pb[1] = 1; d.pa[2] = 1; d.pb[2] = 0;
+  d.epi = EPI_F32; d.c = O; d.ldc = g.k2;
+  d.batch = (int)g.nb; d.bsa = g.pm; d.bsb = g.pm * g.pk; d.bsc = n * g.k2;
+  d.name = "tffp_dft";
+  if ((e = gemm_run(d, nullptr, s)) != hipSuccess) return e;
+  prof_begin(s, "tffp_gather");
+  const int64_t ntb = (n + 31) / 32;
+  hipLaunchKernelGGL(k_gather_t, dim3((unsigned)(ntb * ((g.k2 + 31) / 32)), (unsigned)g.nb), dim3(TT), 0, s,
+                     (const float*)O, n, g.k2, (int)g.k2, (int)F.rho, out, ldout);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t tff_gather_rows(const float* M, int64_t ldm, int64_t n, const float* scale,
+                           const TffDev& F, u16* hi, u16* lo, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const TffPassGeom g = tff_pass_geom(F);
+  prof_begin(s, "tffp_gather");
+  hipLaunchKernelGGL(k_gather, dim3((unsigned)(((n + 31) / 32) * (g.pk / 32)), (unsigned)g.nb), dim3(TT), 0, s,
+                     M, ldm, n, scale, (int)g.k2, (int)g.pk, (int)F.rho, hi, lo, g.nb * g.pk);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t tff_dequant_gather(const uint32_t* codes, int bits, const float* zero, int64_t rows,
+                              const TffDev& F, u16* V, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  const TffPassGeom g = tff_pass_geom(F);
+  prof_begin(s, "tffp_gather");
+  hipLaunchKernelGGL(k_dequant_gather, dim3(grid_1d(rows * g.nb * g.pk)), dim3(TT), 0, s, codes, bits,
+                     zero, rows, F.k * F.rho, (int)g.k2, (int)g.pk, (int)F.rho, (int)g.nb, V,
+                     g.nb * g.pk);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const TffDev& F,
+                              const u16* Fhi, const u16* Flo, float* Z, float* tmp, float* out,
+                              int64_t ldout, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const TffPassGeom g = tff_pass_geom(F);
+  // Z[:, c 2m .. (c+1) 2m) = V_c F_c^T, all blocks in one batch
+  GemmDesc d;
+  d.M = (int)n; d.N = (int)g.m2; d.K = (int)g.pk;
+  d.a[0] = Vhi; d.a[1] = Vlo; d.lda = g.nb * g.pk; d.a_kmajor = true;
+  d.b[0] = Fhi; d.b[1] = Flo; d.ldb = g.pk; d.b_kmajor = true;
+  if (Vlo) {
+    d.npass = 3;
+    d.pa[0] = 0; d.pb[0] = 0; d.pa[1] = 0; d.pb[1] = 1; d.pa[2] = 1; d.pb[2] = 0;
+  } else {
+    d.npass = 2;
+    d.pa[0] = 0; d.pb[0] = 0; d.pa[1] = 0; d.pb[1] = 1;
+  }
+  d.epi = EPI_F32; d.c = Z; d.ldc = F.d;
+  d.batch = (int)g.nb; d.bsa = g.pk; d.bsb = g.pm * g.pk; d.bsc = g.m2;
+  d.name = "tffp_dft";
+  hipError_t e;
+  if ((e = gemm_run(d, nullptr, s)) != hipSuccess) return e;
+  RotOut o{};
+  o.f = out; o.ldf = ldout;
+  return rotate_rows<0>(Z, 0, F.d, n, F, true, tmp, o, s);
+}
+
+hipError_t transpose_f32(const float* in, int64_t rows, int64_t cols, int64_t ldin, float* out,
+                         int64_t ldout, hipStream_t s) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  prof_begin(s, "tffp_gather");
+  hipLaunchKernelGGL(k_transpose_rect, dim3((unsigned)(((rows + 31) / 32) * ((cols + 31) / 32))), dim3(TT), 0, s,
+                     in, rows, cols, ldin, out, ldout);
+  prof_end(s);
+  return last_launch_error();
+}
+
+hipError_t sym_average(float* X, int64_t n, int64_t ld, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const unsigned T = (unsigned)((n + 31) / 32);
+  prof_begin(s, "tffp_gather");
+  hipLaunchKernelGGL(k_sym_average, dim3(T, T), dim3(TT), 0, s, X, n, ld);
+  prof_end(s);
+  return last_launch_error();
+}
+
+}  // namespace fq

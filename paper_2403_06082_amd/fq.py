@@ -66,6 +66,10 @@ SIGNATURES = {
     "fq_frame_apply_tff_workspace_bytes": (_sz, [_tp, _tp]),
     "fq_tff_materialize": (_i, [_vp, _tp, _vp, _i64, _vp, _sz]),
     "fq_tff_materialize_workspace_bytes": (_sz, [_tp]),
+    "fq_frame_analysis_tff": (_i, [_vp, _vp, _i, _tp, _tp, _vp, _vp, _vp, _vp, _sz]),
+    "fq_frame_analysis_tff_workspace_bytes": (_sz, [_i, _tp, _tp]),
+    "fq_frame_synthesis_tff": (_i, [_vp, _vp, _i, _vp, _vp, _tp, _tp, _vp, _vp, _sz]),
+    "fq_frame_synthesis_tff_workspace_bytes": (_sz, [_tp, _tp]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
                                      _vp, _vp, _sz]),
@@ -463,3 +467,52 @@ def fq_tff_materialize(frame: Frame, P=None, ws=None, stream=None):
     _check(lib().fq_tff_materialize(_stream(stream), ctypes.byref(frame.c), _ptr(P), P.stride(0),
                                     wp, wb))
     return P
+
+
+def fq_frame_analysis_tff_workspace_bytes(wt: int, frame_out: Frame, frame_in: Frame) -> int:
+    return lib().fq_frame_analysis_tff_workspace_bytes(wt, ctypes.byref(frame_out.c),
+                                                       ctypes.byref(frame_in.c))
+
+
+def fq_frame_analysis_tff(W, frame_out: Frame, frame_in: Frame, H=None, D=None, Ht=None, ws=None,
+                          stream=None):
+    """D = P_out^T W P_in and Ht = P_in^T H P_in (each optional), both frames given by their
+    construction.  W: (frame_out.d, frame_in.d) f32/f16/bf16 or None when D is None."""
+    torch = _torch()
+    d_out, d_in = frame_out.d, frame_in.d
+    if W is not None:
+        _dev(W, "W", None, (d_out, d_in))
+    _dev(H, "H", torch.float32, (d_in, d_in))
+    _dev(D, "D", torch.float32, (frame_out.K, frame_in.K))
+    _dev(Ht, "Ht", torch.float32, (frame_in.K, frame_in.K))
+    dev = next(t.device for t in (W, H, D, Ht) if t is not None)
+    wt = _dt(W) if W is not None else 0
+    ws, wp, wb = _ws(fq_frame_analysis_tff_workspace_bytes(wt, frame_out, frame_in), ws, dev)
+    _check(lib().fq_frame_analysis_tff(_stream(stream), _ptr(W), wt, ctypes.byref(frame_out.c),
+                                       ctypes.byref(frame_in.c), _ptr(H), _ptr(D), _ptr(Ht), wp,
+                                       wb))
+    return D, Ht
+
+
+def fq_frame_synthesis_tff_workspace_bytes(frame_out: Frame, frame_in: Frame) -> int:
+    return lib().fq_frame_synthesis_tff_workspace_bytes(ctypes.byref(frame_out.c),
+                                                        ctypes.byref(frame_in.c))
+
+
+def fq_frame_synthesis_tff(codes, scale, zero, frame_out: Frame, frame_in: Frame, W_hat=None,
+                           ws=None, stream=None, bits=2):
+    """W_hat = P_out diag(scale) (codes - zero) P_in^T, both frames given by their
+    construction (codes of 2, 3 or 4 bits)."""
+    torch = _torch()
+    K_out, K_in = frame_out.K, frame_in.K
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    if W_hat is None:
+        W_hat = torch.empty((frame_out.d, frame_in.d), dtype=torch.float32, device=codes.device)
+    _dev(W_hat, "W_hat", torch.float32, (frame_out.d, frame_in.d))
+    ws, wp, wb = _ws(fq_frame_synthesis_tff_workspace_bytes(frame_out, frame_in), ws, codes.device)
+    _check(lib().fq_frame_synthesis_tff(_stream(stream), _ptr(codes), bits, _ptr(scale),
+                                        _ptr(zero), ctypes.byref(frame_out.c),
+                                        ctypes.byref(frame_in.c), _ptr(W_hat), wp, wb))
+    return W_hat

@@ -128,6 +128,37 @@ def test_tff_frames_validated_before_launch(L):
     assert L.fq_frame_apply_tff(n, p, 0, 1, 4096, p, p, p, gp, gp, p, p, 64) == 5
 
 
+def test_structured_pass_arguments(L):
+    """fq_frame_analysis_tff / fq_frame_synthesis_tff: frames, sizes, bits, NULL arrays and
+    the workspace are checked before any launch."""
+    from paper_2403_06082_amd.fq import TFF
+    p, n = ctypes.c_void_p(64), None
+    good = TFF(4096, 282, 16, 64, 64, 64, 64)
+    gp = ctypes.byref(good)
+    need_a = L.fq_frame_analysis_tff_workspace_bytes(2, gp, gp)
+    need_s = L.fq_frame_synthesis_tff_workspace_bytes(gp, gp)
+    assert need_a >= 4512 * 4512 * 4 and need_s >= 4096 * 4512 * 4
+    assert L.fq_frame_analysis_tff_workspace_bytes(3, gp, gp) == 0
+    big = TFF(1 << 22, 3968, 2048, 64, 1 << 11, 64, 1 << 11)     # d above 2^21, else valid
+    bp = ctypes.byref(big)
+    assert L.fq_frame_analysis_tff_workspace_bytes(2, bp, gp) == 0
+    assert L.fq_frame_analysis_tff(n, p, 2, bp, gp, p, p, p, p, 1 << 40) == 2
+    assert L.fq_frame_synthesis_tff(n, p, 2, p, p, gp, bp, p, p, 1 << 40) == 2
+    bad = ctypes.byref(TFF(4096, 282, 15, 64, 64, 64, 64))
+    assert L.fq_frame_analysis_tff(n, p, 2, bad, gp, p, p, p, p, 1 << 40) == 1
+    assert b"frame_out" in L.fq_last_error()
+    assert L.fq_frame_analysis_tff(n, p, 5, gp, gp, p, p, p, p, 1 << 40) == 1    # bad dtype
+    assert L.fq_frame_analysis_tff(n, n, 2, gp, gp, p, p, p, p, need_a) == 1     # W NULL with D
+    assert L.fq_frame_analysis_tff(n, p, 2, gp, gp, n, p, p, p, need_a) == 1     # H NULL with Ht
+    assert L.fq_frame_analysis_tff(n, p, 2, gp, gp, p, p, p, p, need_a - 1) == 5
+    assert L.fq_frame_analysis_tff(n, n, 2, gp, gp, n, n, n, p, need_a) == 0     # nothing asked
+    assert L.fq_frame_synthesis_tff(n, p, 5, p, p, gp, gp, p, p, need_s) == 2    # bits
+    assert L.fq_frame_synthesis_tff(n, p, 2, p, p, gp, bad, p, p, need_s) == 1
+    assert b"frame_in" in L.fq_last_error()
+    assert L.fq_frame_synthesis_tff(n, n, 2, p, p, gp, gp, p, p, need_s) == 1    # codes NULL
+    assert L.fq_frame_synthesis_tff(n, p, 2, p, p, gp, gp, p, p, need_s - 1) == 5
+
+
 def test_act_quantize_arguments(L):
     p, n = ctypes.c_void_p(64), None
     assert L.fq_act_quantize(n, p, 4, 8, 1, p, p) == 1
