@@ -33,11 +33,15 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "quantized weights/sec per layer (Llama-7B-shaped 11008×4096); MFMA % of peak"
-PEAK = {"bf16": 2500.0, "f64": 78.6, "hbm": 8000.0}    # TFLOP/s, TFLOP/s, GB/s
+PEAK = {"bf16": 2500.0, "f32": 157.3, "f64": 78.6, "hbm": 8000.0}   # TFLOP/s ..., GB/s
 
 
-def algorithmic_work(n, d_out, d_in, K_out, K_in, block):
-    """Algorithmic flops (bytes for the memory-bound kernels) per launch group and step."""
+def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, rot=None):
+    """Algorithmic flops (bytes for the memory-bound kernels) per launch group and step.
+    With structured frames (rho, and rot = (d1_out + d2_out, d1_in + d2_in)): the per-block
+    DFT products, 4 d k flops per transformed row (k = K / rho), and the rotations,
+    2 d (d1 + d2) flops per row, over the rows each stage transforms (D: d_out rows of W,
+    then K_in columns; Ht: d_in, then K_in; W_hat: K_out code rows, then d_in columns)."""
     gptq_upd = 0
     for o1 in range(0, K_in, block):
         o2 = min(o1 + block, K_in)
@@ -55,7 +59,15 @@ def algorithmic_work(n, d_out, d_in, K_out, K_in, block):
         kb = min(64, K_in - k0)
         rest = K_in - k0 - kb
         chol += rest * (rest + 1) * kb          # lower-triangle rank-kb update, 2 flops/FMA
+    extra = {}
+    if rho is not None:
+        k_out, k_in = K_out // rho, K_in // rho
+        rows_in = d_out + d_in + K_in + K_out        # rows transformed by the input frame
+        rows_out = K_in + d_in                       # rows transformed by the output frame
+        extra["tffp_dft"] = ("bf16", 4 * d_in * k_in * rows_in + 4 * d_out * k_out * rows_out)
+        extra["tffp_rotate"] = ("f32", 2 * d_in * rot[1] * rows_in + 2 * d_out * rot[0] * rows_out)
     return {
+        **extra,
         "gemm_hessian": ("bf16", n * d_in * (d_in + 1)),
         "gemm_analysis_w1": ("bf16", 2 * K_out * d_out * d_in),
         "gemm_analysis_w2": ("bf16", 2 * K_out * d_in * K_in),
@@ -82,7 +94,8 @@ def mfma_passes(w_dtype):
 
 
 KERNEL_GROUPS = ["gemm_hessian", "gemm_analysis_w1", "gemm_analysis_w2", "gemm_analysis_h1",
-                 "gemm_analysis_h2", "gemm_synthesis_1", "gemm_synthesis_2", "gptq_update",
+                 "gemm_analysis_h2", "gemm_synthesis_1", "gemm_synthesis_2", "tffp_rotate",
+                 "tffp_blocks", "tffp_dft", "tffp_gather", "gptq_update",
                  "gptq_update_lazy", "gptq_update_span", "gptq_block", "chol_syrk", "chol_potrf", "chol_trsm", "q_", "split_bf16",
                  "syrk_reduce", "dequant", "pack2"]
 
@@ -287,7 +300,7 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
                     "the code kernel's VALU work at 8"}
 
 
-def grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, steps, iters=200):
+def grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, steps, iters=200, frames=None):
     """The same pass with 3- and 4-bit grids (one warmup, then `steps` timed passes each;
     one stream), as quantized weights per second; then the 4-bit codes of that pass run
     through the integer inference path at 4-bit activations (W4/A4), 1 and 8 tokens."""
@@ -297,7 +310,7 @@ def grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, steps, iters=200)
     out = {}
     for bits in (3, 4):
         b = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
-                         bits=bits)
+                         bits=bits, frames=frames)
 
         def run():
             quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], b, bits=bits,
@@ -494,6 +507,10 @@ def main():
                     help="2: D is formed on a second stream while the main stream factors "
                          "H~ (measured within 0.5%% of one stream: the contractions take "
                          "every CU); the kernel-timer region always uses one")
+    ap.add_argument("--frames", default="structured", choices=("structured", "dense"),
+                    help="how the pass applies the frames in the analysis and the synthesis: "
+                         "from their construction (default) or as the dense d x K matrices; "
+                         "the other way is timed beside it")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="device-to-device copy of this many MiB before the warmup, as the "
                          "known-size reference for hardware byte counters")
@@ -507,7 +524,7 @@ def main():
     import torch
     import paper_2403_06082_amd as fq
     from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
-    from fq_inputs import WORKLOADS
+    from fq_inputs import WORKLOADS, gen
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -519,7 +536,13 @@ def main():
     dev, host = make_inputs(wl, li)
     K_out, K_in = dev["P_out"].shape[1], dev["P_in"].shape[1]
     n = dev["X"].shape[0]
-    bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block)
+    (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, li)
+    upf = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    tff_frames = (fq.Frame(L.d_out, ko, ro, upf(R1o), upf(R2o)),
+                  fq.Frame(L.d_in, ki, ri, upf(R1i), upf(R2i)))
+    frames = tff_frames if args.frames == "structured" else None
+    bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
+                        frames=frames)
     stream = torch.cuda.current_stream()
     side = torch.cuda.Stream() if args.streams == 2 else None
 
@@ -565,7 +588,9 @@ def main():
     print(f"[bench] {args.steps} steps with kernel timers: {ms_timed:.2f} ms/step", file=sys.stderr,
           flush=True)
 
-    work = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block)
+    rot = (R1o.shape[0] + R2o.shape[0], R1i.shape[0] + R2i.shape[0])
+    work = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block,
+                            rho=wl.rho if frames is not None else None, rot=rot)
     passes = mfma_passes(wl.w_dtype)
     kernels = {}
     for name in KERNEL_GROUPS:
@@ -641,18 +666,42 @@ def main():
                                f"(r={wl.r}, rho={wl.rho}), {wl.bits}-bit, block {wl.block}, "
                                f"damp {wl.damp}, clip {wl.clip_sigmas} sigma",
                    "d_out": L.d_out, "d_in": L.d_in, "n_tokens": n, "K_out": K_out,
-                   "K_in": K_in, "streams": args.streams},
+                   "K_in": K_in, "streams": args.streams, "frames": args.frames},
         "roofline": roof,
         "contraction_mfma_frac": None if contraction_frac is None else round(contraction_frac, 4),
         "contraction_mfma_executed_frac": None if contraction_exec is None else round(contraction_exec, 4),
         "kernels": kernels,
         "kernel_ms_total_per_step": round(tot_all / args.steps, 3),
     }
+    # the pass with the frames applied the other way, same inputs (one warmup, `steps` timed)
+    other = "dense" if args.frames == "structured" else "structured"
+    ob = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
+                      frames=tff_frames if other == "structured" else None)
+
+    def ostep():
+        quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], ob, block=wl.block,
+                       damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream)
+
+    ostep()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ostep()
+    torch.cuda.synchronize()
+    oms = (time.perf_counter() - t0) * 1000.0 / args.steps
+    out["other_frames"] = {"frames": other, "ms_per_step": round(oms, 3),
+                           "weights_per_s": round(L.d_out * L.d_in / (oms / 1e3), 1),
+                           "codes_differing_frac_vs_headline_pass": float(sum(
+                               (((ob.codes >> (2 * j)) & 3) != ((bufs.codes >> (2 * j)) & 3))
+                               .sum().item() for j in range(16)) / (K_out * K_in))}
+    print(f"[bench] pass with {other} frames: {oms:.2f} ms/step", file=sys.stderr, flush=True)
+    del ob
     inf = inference_bench(fq, torch, dev, bufs, L, K_out, K_in)
     inf["structured"] = structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in)
     out["inference"] = inf
     out["frame_generation"] = frame_generation_bench(fq, torch, dev, wl, li, host)
-    out["grid_variants"] = grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, args.steps)
+    out["grid_variants"] = grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, args.steps,
+                                               frames=frames)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)

@@ -7,7 +7,7 @@
 // between them: D^T = (W P_in)^T P_out, so D is the transposed row analysis (by P_out) of
 // the transposed row analysis (by P_in) of W.  A row transform has two parts:
 //  - the rotation R1^T M R2 (analysis) or R1 M R2^T (synthesis) of each row read as a
-//    d1 x d2 matrix M: two batched small products on the vector ALU (k_rot_step);
+//    d1 x d2 matrix M: two batched small products on fp32 MFMA (k_rot_step);
 //  - the DFT part, which acts on the rho/2 blocks of 2m real coordinates separately:
 //    block c of an analysed row is y_c F_c with F_c the real 2m x 2k matrix
 //      F_c[2j][2s] = F_c[2j+1][2s+1] = cos(phi) / sqrt(k),
@@ -24,6 +24,8 @@
 
 namespace fq {
 namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int TT = 256;
 constexpr int RB = 64;       // rotation output tile (RB x RB per work-group of one wave)
@@ -53,9 +55,10 @@ struct RotOut {
 
 // One factor of the rotation for n vectors, each read as a d1 x d2 row-major matrix X_t:
 // XL: C_t = X_t S (S d2 x d2), else C_t = S X_t (S d1 x d1); S(a, b) = S[b][a] when ST.
-// A work-group (one wave) owns a 64 x 64 tile of one C_t, 8 x 8 outputs per lane, fp32
-// FMAs over k steps of 16 staged in LDS.  grid (n * ceil(d1/64) * ceil(d2/64)).
-// OUT 0: fp32 rows; OUT 1: bf16 (hi, lo) rows in block layout.
+// A work-group (one wave) owns a 64 x 64 tile of one C_t as 2 x 2 blocks of
+// v_mfma_f32_32x32x2_f32 (fp32 operands and sums), over k steps of 16 staged in LDS.
+// grid (n * ceil(d1/64) * ceil(d2/64)).  OUT 0: fp32 rows; OUT 1: bf16 (hi, lo) rows in
+// block layout.
 template <typename XT, bool XL, bool ST, int OUT>
 __global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64_t ldx,
                                                  const float* __restrict__ S, int d1, int d2,
@@ -68,14 +71,16 @@ __global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64
   const int rem = (int)(blk - t * (tr * tc));
   const int i0 = (rem / tc) * RB, j0 = (rem % tc) * RB;
   const int lane = threadIdx.x;
-  const int tx = lane & 7, ty = lane >> 3;
+  const int lo = lane & 31, hi = lane >> 5;
   const int Kd = XL ? d2 : d1;
   const XT* x = X + t * ldx;
-  float acc[8][8];
+  floatx16 acc[2][2];
 #pragma unroll
-  for (int r = 0; r < 8; ++r)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[r][q] = 0.f;
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
   for (int k0 = 0; k0 < Kd; k0 += RK) {
 #pragma unroll 4
     for (int pass = 0; pass < 16; ++pass) {
@@ -103,38 +108,41 @@ __global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64
       Bs[kb][jj] = bv;
     }
     __syncthreads();
+    // lane l supplies A(32 a + l % 32, kk + l / 32) and B(kk + l / 32, 32 b + l % 32)
 #pragma unroll
-    for (int kk = 0; kk < RK; ++kk) {
-      const float4 a0 = *reinterpret_cast<const float4*>(&As[kk][ty * 8]);
-      const float4 a1 = *reinterpret_cast<const float4*>(&As[kk][ty * 8 + 4]);
-      const float4 b0 = *reinterpret_cast<const float4*>(&Bs[kk][tx * 8]);
-      const float4 b1 = *reinterpret_cast<const float4*>(&Bs[kk][tx * 8 + 4]);
-      const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      const float b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-#pragma unroll
-      for (int r = 0; r < 8; ++r)
-#pragma unroll
-        for (int q = 0; q < 8; ++q) acc[r][q] = fmaf(a[r], b[q], acc[r][q]);
+    for (int kk = 0; kk < RK; kk += 2) {
+      const float a0 = As[kk + hi][lo], a1 = As[kk + hi][32 + lo];
+      const float b0 = Bs[kk + hi][lo], b1 = Bs[kk + hi][32 + lo];
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
     }
     __syncthreads();
   }
+  // 32 x 32 accumulator layout: value v of lane l is row 8 (v / 4) + 4 (l / 32) + v % 4,
+  // column l % 32 of its block
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const int i = i0 + ty * 8 + r;
-    if (i >= d1) continue;
+  for (int a = 0; a < 2; ++a) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int j = j0 + tx * 8 + q;
-      if (j >= d2) continue;
-      const int64_t p = (int64_t)i * d2 + j;
-      if (OUT == 0) {
-        o.f[t * o.ldf + p] = acc[r][q];
-      } else {
-        const int64_t c = p / o.bw;
-        const int64_t idx = t * o.ldp + c * o.pb + (p - c * o.bw);
-        const uint32_t h = rne_bf16(acc[r][q]);
-        o.hi[idx] = (u16)h;
-        o.lo[idx] = (u16)rne_bf16(acc[r][q] - __uint_as_float(h << 16));
+    for (int v = 0; v < 16; ++v) {
+      const int i = i0 + 32 * a + 8 * (v >> 2) + 4 * hi + (v & 3);
+      if (i >= d1) continue;
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int j = j0 + 32 * b + lo;
+        if (j >= d2) continue;
+        const float val = acc[a][b][v];
+        const int64_t p = (int64_t)i * d2 + j;
+        if (OUT == 0) {
+          o.f[t * o.ldf + p] = val;
+        } else {
+          const int64_t c = p / o.bw;
+          const int64_t idx = t * o.ldp + c * o.pb + (p - c * o.bw);
+          const uint32_t h = rne_bf16(val);
+          o.hi[idx] = (u16)h;
+          o.lo[idx] = (u16)rne_bf16(val - __uint_as_float(h << 16));
+        }
       }
     }
   }

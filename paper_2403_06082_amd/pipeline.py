@@ -7,6 +7,10 @@
 
 Workspaces are allocated once per call site with torch and reused.
 
+With frames given by their construction (LayerBuffers(..., frames=(F_out, F_in)), fq.Frame
+objects), the analysis and the synthesis are fq_frame_analysis_tff / fq_frame_synthesis_tff
+and the dense P_out, P_in are not read (pass None).
+
 With a second stream (side_stream), D = P_out^T W P_in is formed there while the main
 stream factors the damped H~ (fq_quantize_prepare): the Cholesky factorization, a chain
 of small dependent kernels, then overlaps the D contractions.  Outputs are identical.
@@ -20,7 +24,7 @@ class LayerBuffers:
     """Device outputs and workspaces for one layer shape (reused across calls)."""
 
     def __init__(self, d_out, d_in, K_out, K_in, w_dtype, x_dtype, n_tokens, block=128,
-                 device="cuda", bits=2):
+                 device="cuda", bits=2, frames=None):
         import torch
         f32 = torch.float32
         self.H = torch.empty((d_in, d_in), dtype=f32, device=device)
@@ -37,14 +41,39 @@ class LayerBuffers:
         u8 = torch.uint8
         self.ws_h = torch.empty(_fq.fq_hessian_workspace_bytes(dt[x_dtype], n_tokens, d_in),
                                 dtype=u8, device=device)
-        self.ws_a = torch.empty(_fq.fq_frame_analysis_workspace_bytes(dt[w_dtype], d_out, d_in,
-                                                                      K_out, K_in),
-                                dtype=u8, device=device)
+        self.frames = frames
+        if frames is None:
+            na = _fq.fq_frame_analysis_workspace_bytes(dt[w_dtype], d_out, d_in, K_out, K_in)
+            ns = _fq.fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in)
+        else:
+            fo, fi = frames
+            if (fo.d, fi.d, fo.K, fi.K) != (d_out, d_in, K_out, K_in):
+                raise ValueError("frames do not match the layer shape")
+            na = _fq.fq_frame_analysis_tff_workspace_bytes(dt[w_dtype], fo, fi)
+            ns = _fq.fq_frame_synthesis_tff_workspace_bytes(fo, fi)
+        self.ws_a = torch.empty(na, dtype=u8, device=device)
         self.ws_a2 = None      # second analysis workspace, for the two-stream order
         self.ws_q = torch.empty(_fq.fq_quantize_frames_workspace_bytes(K_out, K_in, block),
                                 dtype=u8, device=device)
-        self.ws_s = torch.empty(_fq.fq_frame_synthesis_workspace_bytes(K_out, K_in, d_out, d_in),
-                                dtype=u8, device=device)
+        self.ws_s = torch.empty(ns, dtype=u8, device=device)
+
+
+def _analysis(W, P_out, P_in, bufs, H, D, Ht, ws, stream):
+    if bufs.frames is None:
+        _fq.fq_frame_analysis(W, P_out, P_in, H, D, Ht, ws=ws, stream=stream)
+    else:
+        _fq.fq_frame_analysis_tff(W if D is not None else None, bufs.frames[0], bufs.frames[1],
+                                  H, D, Ht, ws=ws, stream=stream)
+
+
+def _synthesis(P_out, P_in, bufs, bits, stream):
+    if bufs.frames is None:
+        _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
+                               ws=bufs.ws_s, stream=stream, bits=bits)
+    else:
+        _fq.fq_frame_synthesis_tff(bufs.codes, bufs.scale, bufs.zero, bufs.frames[0],
+                                   bufs.frames[1], bufs.W_hat, ws=bufs.ws_s, stream=stream,
+                                   bits=bits)
 
 
 def quantize_layer(W, X, P_out, P_in, bufs: LayerBuffers, H=None, Ht=None, bits=2, block=128,
@@ -57,14 +86,13 @@ def quantize_layer(W, X, P_out, P_in, bufs: LayerBuffers, H=None, Ht=None, bits=
         _fq.fq_hessian_accumulate(X, bufs.H, ws=bufs.ws_h, stream=stream)
         H = bufs.H
     if Ht is None:
-        _fq.fq_frame_analysis(W, P_out, P_in, H, bufs.D, bufs.Ht, ws=bufs.ws_a, stream=stream)
+        _analysis(W, P_out, P_in, bufs, H, bufs.D, bufs.Ht, bufs.ws_a, stream)
         Ht = bufs.Ht
     else:
-        _fq.fq_frame_analysis(W, P_out, P_in, None, bufs.D, None, ws=bufs.ws_a, stream=stream)
+        _analysis(W, P_out, P_in, bufs, None, bufs.D, None, bufs.ws_a, stream)
     _fq.fq_quantize_frames(bufs.D, Ht, bufs.codes, bufs.scale, bufs.zero, bits=bits, block=block,
                            damp=damp, clip_sigmas=clip_sigmas, ws=bufs.ws_q, stream=stream)
-    _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
-                           ws=bufs.ws_s, stream=stream, bits=bits)
+    _synthesis(P_out, P_in, bufs, bits, stream)
     return bufs
 
 
@@ -78,19 +106,18 @@ def _quantize_layer_two_streams(W, X, P_out, P_in, bufs, H, Ht, bits, block, dam
         _fq.fq_hessian_accumulate(X, bufs.H, ws=bufs.ws_h, stream=main)
         H = bufs.H
     if Ht is None:
-        _fq.fq_frame_analysis(W, P_out, P_in, H, None, bufs.Ht, ws=bufs.ws_a, stream=main)
+        _analysis(W, P_out, P_in, bufs, H, None, bufs.Ht, bufs.ws_a, main)
         Ht = bufs.Ht
     # D on the side stream, started once H~ is done (so that it does not delay H~)
     ready = torch.cuda.Event()
     ready.record(main)
     side.wait_event(ready)
-    _fq.fq_frame_analysis(W, P_out, P_in, None, bufs.D, None, ws=bufs.ws_a2, stream=side)
+    _analysis(W, P_out, P_in, bufs, None, bufs.D, None, bufs.ws_a2, side)
     d_done = torch.cuda.Event()
     d_done.record(side)
     _fq.fq_quantize_prepare(Ht, bufs.D.shape[0], bufs.ws_q, block=block, damp=damp, stream=main)
     main.wait_event(d_done)
     _fq.fq_quantize_apply(bufs.D, bufs.codes, bufs.scale, bufs.zero, bufs.ws_q, bits=bits,
                           block=block, clip_sigmas=clip_sigmas, stream=main)
-    _fq.fq_frame_synthesis(bufs.codes, bufs.scale, bufs.zero, P_out, P_in, bufs.W_hat,
-                           ws=bufs.ws_s, stream=main, bits=bits)
+    _synthesis(P_out, P_in, bufs, bits, main)
     return bufs

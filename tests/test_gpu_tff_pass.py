@@ -162,3 +162,37 @@ def test_tff_pass_llama7b_up_full_size():
     got_w = Wt.cpu().numpy()[ri_, ci_]
     scale_w = float(torch.linalg.norm(Wd.double())) / np.sqrt(L.d_out * L.d_in)
     assert np.max(np.abs(got_w - ref_w)) < 1e-4 * scale_w
+
+
+@pytest.mark.parametrize("two_streams", [False, True])
+def test_pipeline_with_structured_frames(two_streams):
+    """The whole pass with frames given by their construction: D and Ht against the oracle,
+    the codes replayed row by row on the device's own D and Ht (bit-exact outside the
+    near-tie window), W_hat against the oracle's synthesis of the device's codes."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    from fq_testutil import replay_rows, check_codes, unpack_codes
+    d_out, d_in = 520, 264
+    Fo, Po = _frame(torch, fq, d_out, 143, 4, 51)
+    Fi, Pi = _frame(torch, fq, d_in, 72, 4, 52)
+    rng = np.random.default_rng(53)
+    Wn = (rng.standard_normal((d_out, d_in)) * 0.02).astype(np.float32)
+    Xn = rng.standard_normal((700, d_in)).astype(np.float32)
+    Xn[:, 5] *= 30.0
+    W, X = torch.from_numpy(Wn).cuda(), torch.from_numpy(Xn).cuda()
+    b = LayerBuffers(d_out, d_in, Fo.K, Fi.K, torch.float32, torch.float32, 700,
+                     frames=(Fo, Fi))
+    side = torch.cuda.Stream() if two_streams else None
+    quantize_layer(W, X, None, None, b, side_stream=side)
+    torch.cuda.synchronize()
+    Hg = b.H.cpu().numpy()
+    Do, Hto = O.frame_analysis(Wn, Po, Pi, Hg)
+    Dg, Htg = b.D.cpu().numpy(), b.Ht.cpu().numpy()
+    assert rel_fro(Dg, Do) < 1e-5 and rel_fro(Htg, Hto) < 1e-5
+    cg = unpack_codes(b.codes, Fi.K)
+    r = replay_rows(Dg, Htg, cg)
+    check_codes(r, cg, b.scale.cpu().numpy(), b.zero.cpu().numpy())
+    Who = O.synthesis(cg, b.scale.cpu().numpy().astype(np.float64),
+                      b.zero.cpu().numpy().astype(np.float64), Po, Pi)
+    assert rel_fro(b.W_hat.cpu().numpy(), Who) < 1e-5
