@@ -28,7 +28,7 @@ namespace {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int TT = 256;
-constexpr int RB = 64;       // rotation output tile (RB x RB per work-group of one wave)
+constexpr int RB = 64;       // rotation output tile (RB x RB per wave)
 constexpr int RK = 16;       // rotation k step
 
 template <typename T>
@@ -53,27 +53,89 @@ struct RotOut {
   int bw, pb;                          // block layout: coordinate p sits at (p / bw) pb + p % bw
 };
 
+// 4 consecutive elements at p as floats (16 bytes for fp32, 8 for the 16-bit types)
+template <typename T>
+__device__ __forceinline__ float4 ld4_f32(const T* p);
+template <>
+__device__ __forceinline__ float4 ld4_f32<float>(const float* p) {
+  return *reinterpret_cast<const float4*>(p);
+}
+template <>
+__device__ __forceinline__ float4 ld4_f32<uint16_t>(const uint16_t* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+}
+template <>
+__device__ __forceinline__ float4 ld4_f32<_Float16>(const _Float16* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  const _Float16* h = reinterpret_cast<const _Float16*>(&u);
+  return make_float4((float)h[0], (float)h[1], (float)h[2], (float)h[3]);
+}
+
+typedef float RotTile[RK][RB + 4];
+
+// Stage the RK x RB tile T(k, q) = base[q ld + k] (KC) or base[k ld + q] (!KC), k0 <= k <
+// k0 + RK, q0 <= q < q0 + RB, into L[k - k0][q - q0]; entries with k >= kext or q >= qext
+// are 0.  The tile is 256 runs of 4 elements contiguous in memory; thread r of nthr takes
+// runs r, r + nthr, ...  A run is one 16- (8-) byte load when vec (rows aligned) and it
+// lies inside the extents, else element by element.
+template <typename T, bool KC>
+__device__ __forceinline__ void stage_tile(const T* __restrict__ base, int64_t ld, int k0, int kext,
+                                           int q0, int qext, bool vec, RotTile& L, int r,
+                                           int nthr) {
+  for (int u = r; u < 256; u += nthr) {
+    if (KC) {
+      const int q = u >> 2, kq = (u & 3) * 4;
+      const int gq = q0 + q, gk = k0 + kq;
+      const T* src = base + (int64_t)gq * ld + gk;
+      if (vec && gq < qext && gk + 3 < kext) {
+        const float4 v = ld4_f32<T>(src);
+        L[kq][q] = v.x; L[kq + 1][q] = v.y; L[kq + 2][q] = v.z; L[kq + 3][q] = v.w;
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          L[kq + c][q] = (gq < qext && gk + c < kext) ? ldx_f32<T>(src + c) : 0.f;
+      }
+    } else {
+      const int k = u >> 4, qq = (u & 15) * 4;
+      const int gk = k0 + k, gq = q0 + qq;
+      const T* src = base + (int64_t)gk * ld + gq;
+      if (vec && gk < kext && gq + 3 < qext) {
+        *reinterpret_cast<float4*>(&L[k][qq]) = ld4_f32<T>(src);
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          L[k][qq + c] = (gk < kext && gq + c < qext) ? ldx_f32<T>(src + c) : 0.f;
+      }
+    }
+  }
+}
+
 // One factor of the rotation for n vectors, each read as a d1 x d2 row-major matrix X_t:
 // XL: C_t = X_t S (S d2 x d2), else C_t = S X_t (S d1 x d1); S(a, b) = S[b][a] when ST.
-// A work-group (one wave) owns a 64 x 64 tile of one C_t as 2 x 2 blocks of
-// v_mfma_f32_32x32x2_f32 (fp32 operands and sums), over k steps of 16 staged in LDS.
-// grid (n * ceil(d1/64) * ceil(d2/64)).  OUT 0: fp32 rows; OUT 1: bf16 (hi, lo) rows in
-// block layout.
+// A work-group of 4 waves owns one 64 x 64 output tile for 4 consecutive vectors (one per
+// wave) and stages the tile of S they share once per k step of 16.  Each wave forms its
+// tile as 2 x 2 blocks of v_mfma_f32_32x32x2_f32 (fp32 operands and sums).  grid
+// (ceil(n/4) * ceil(d1/64) * ceil(d2/64)).  vx / vs: rows of X / S allow 4-element loads.
+// OUT 0: fp32 rows; OUT 1: bf16 (hi, lo) rows in block layout.
 template <typename XT, bool XL, bool ST, int OUT>
-__global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64_t ldx,
-                                                 const float* __restrict__ S, int d1, int d2,
-                                                 RotOut o) {
-  __shared__ __attribute__((aligned(16))) float As[RK][RB + 4];
-  __shared__ __attribute__((aligned(16))) float Bs[RK][RB + 4];
+__global__ __launch_bounds__(256) void k_rot_step(const XT* __restrict__ X, int64_t ldx, int64_t n,
+                                                  const float* __restrict__ S, int d1, int d2,
+                                                  int vx, int vs, RotOut o) {
+  __shared__ __attribute__((aligned(16))) RotTile Sh;
+  __shared__ __attribute__((aligned(16))) RotTile Xw[4];
   const int tr = (d1 + RB - 1) / RB, tc = (d2 + RB - 1) / RB;
   const int64_t blk = blockIdx.x;
-  const int64_t t = blk / (tr * tc);
-  const int rem = (int)(blk - t * (tr * tc));
+  const int64_t tg = blk / (tr * tc);
+  const int rem = (int)(blk - tg * (tr * tc));
   const int i0 = (rem / tc) * RB, j0 = (rem % tc) * RB;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lo = lane & 31, hi = lane >> 5;
+  const int64_t t = tg * 4 + wave;
+  const bool live = t < n;
   const int Kd = XL ? d2 : d1;
-  const XT* x = X + t * ldx;
+  const XT* x = X + (live ? t : 0) * ldx;
   floatx16 acc[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -81,33 +143,22 @@ __global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+  RotTile& Xt = Xw[wave];
   for (int k0 = 0; k0 < Kd; k0 += RK) {
-#pragma unroll 4
-    for (int pass = 0; pass < 16; ++pass) {
-      // A(i, k): row-contiguous in k unless it is S^T of the left factor
-      int ii, ka;
-      if (XL || !ST) { const int e = pass * 64 + lane; ka = e & 15; ii = e >> 4; }
-      else { ii = lane; ka = pass; }
-      const int gi = i0 + ii, gka = k0 + ka;
-      float av = 0.f;
-      if (gi < d1 && gka < Kd) {
-        if (XL) av = ldx_f32<XT>(x + (int64_t)gi * d2 + gka);
-        else av = ST ? S[(int64_t)gka * d1 + gi] : S[(int64_t)gi * d1 + gka];
-      }
-      As[ka][ii] = av;
-      // B(k, j): row-contiguous in j unless it is S^T of the right factor
-      int jj, kb;
-      if (!XL || !ST) { jj = lane; kb = pass; }
-      else { const int e = pass * 64 + lane; kb = e & 15; jj = e >> 4; }
-      const int gj = j0 + jj, gkb = k0 + kb;
-      float bv = 0.f;
-      if (gj < d2 && gkb < Kd) {
-        if (!XL) bv = ldx_f32<XT>(x + (int64_t)gkb * d2 + gj);
-        else bv = ST ? S[(int64_t)gj * d2 + gkb] : S[(int64_t)gkb * d2 + gj];
-      }
-      Bs[kb][jj] = bv;
+    // shared operand: B = S (XL) with q = j, or A = S (!XL) with q = i
+    if (XL) {
+      if (ST) stage_tile<float, true>(S, d2, k0, Kd, j0, d2, vs, Sh, tid, 256);
+      else stage_tile<float, false>(S, d2, k0, Kd, j0, d2, vs, Sh, tid, 256);
+    } else {
+      if (ST) stage_tile<float, false>(S, d1, k0, Kd, i0, d1, vs, Sh, tid, 256);
+      else stage_tile<float, true>(S, d1, k0, Kd, i0, d1, vs, Sh, tid, 256);
     }
+    // this wave's vector: A = X_t (XL, contiguous in k) or B = X_t (!XL, contiguous in j)
+    if (XL) stage_tile<XT, true>(x, d2, k0, Kd, i0, live ? d1 : 0, vx, Xt, lane, 64);
+    else stage_tile<XT, false>(x, d2, k0, Kd, j0, live ? d2 : 0, vx, Xt, lane, 64);
     __syncthreads();
+    const RotTile& As = XL ? Xt : Sh;
+    const RotTile& Bs = XL ? Sh : Xt;
     // lane l supplies A(32 a + l % 32, kk + l / 32) and B(kk + l / 32, 32 b + l % 32)
 #pragma unroll
     for (int kk = 0; kk < RK; kk += 2) {
@@ -120,6 +171,7 @@ __global__ __launch_bounds__(64) void k_rot_step(const XT* __restrict__ X, int64
     }
     __syncthreads();
   }
+  if (!live) return;
   // 32 x 32 accumulator layout: value v of lane l is row 8 (v / 4) + 4 (l / 32) + v % 4,
   // column l % 32 of its block
 #pragma unroll
@@ -336,21 +388,27 @@ template <int OUT>
 hipError_t rotate_rows(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F, bool synth,
                        float* tmp, const RotOut& o, hipStream_t s) {
   const int64_t tiles = (int64_t)((F.d1 + RB - 1) / RB) * ((F.d2 + RB - 1) / RB);
-  const dim3 g((unsigned)(n * tiles));
+  const dim3 g((unsigned)((n + 3) / 4 * tiles)), b(256);
   RotOut ot{};
   ot.f = tmp; ot.ldf = F.d;
+  auto al = [](const void* p, int bytes) { return ((uintptr_t)p % bytes) == 0; };
+  const int esz = xt == 0 ? 4 : 2;
+  const int vx = (F.d2 % 4 == 0 && ldx % 4 == 0 && al(X, 4 * esz)) ? 1 : 0;
+  const int vt = (F.d2 % 4 == 0 && al(tmp, 16)) ? 1 : 0;      // tmp rows are d floats
+  const int vs2 = (F.d2 % 4 == 0 && al(F.R2, 16)) ? 1 : 0;
+  const int vs1 = (F.d1 % 4 == 0 && al(F.R1, 16)) ? 1 : 0;
   prof_begin(s, "tffp_rotate");
   if (synth) {
-    hipLaunchKernelGGL((k_rot_step<float, true, true, 0>), g, dim3(64), 0, s, (const float*)X, ldx, F.R2, F.d1, F.d2, ot);
-    hipLaunchKernelGGL((k_rot_step<float, false, false, OUT>), g, dim3(64), 0, s, (const float*)tmp, F.d, F.R1, F.d1, F.d2, o);
+    hipLaunchKernelGGL((k_rot_step<float, true, true, 0>), g, b, 0, s, (const float*)X, ldx, n, F.R2, F.d1, F.d2, vx, vs2, ot);
+    hipLaunchKernelGGL((k_rot_step<float, false, false, OUT>), g, b, 0, s, (const float*)tmp, F.d, n, F.R1, F.d1, F.d2, vt, vs1, o);
   } else {
     if (xt == 0)
-      hipLaunchKernelGGL((k_rot_step<float, true, false, 0>), g, dim3(64), 0, s, (const float*)X, ldx, F.R2, F.d1, F.d2, ot);
+      hipLaunchKernelGGL((k_rot_step<float, true, false, 0>), g, b, 0, s, (const float*)X, ldx, n, F.R2, F.d1, F.d2, vx, vs2, ot);
     else if (xt == 1)
-      hipLaunchKernelGGL((k_rot_step<_Float16, true, false, 0>), g, dim3(64), 0, s, (const _Float16*)X, ldx, F.R2, F.d1, F.d2, ot);
+      hipLaunchKernelGGL((k_rot_step<_Float16, true, false, 0>), g, b, 0, s, (const _Float16*)X, ldx, n, F.R2, F.d1, F.d2, vx, vs2, ot);
     else
-      hipLaunchKernelGGL((k_rot_step<uint16_t, true, false, 0>), g, dim3(64), 0, s, (const uint16_t*)X, ldx, F.R2, F.d1, F.d2, ot);
-    hipLaunchKernelGGL((k_rot_step<float, false, true, OUT>), g, dim3(64), 0, s, (const float*)tmp, F.d, F.R1, F.d1, F.d2, o);
+      hipLaunchKernelGGL((k_rot_step<uint16_t, true, false, 0>), g, b, 0, s, (const uint16_t*)X, ldx, n, F.R2, F.d1, F.d2, vx, vs2, ot);
+    hipLaunchKernelGGL((k_rot_step<float, false, true, OUT>), g, b, 0, s, (const float*)tmp, F.d, n, F.R1, F.d1, F.d2, vt, vs1, o);
   }
   prof_end(s);
   return last_launch_error();
