@@ -5,10 +5,13 @@ One step = the whole pass on one layer with its inputs resident in HBM:
     ->  clip + grid + OPTQ 2-bit rounding (fp64)  ->  W^ = P_l D^ P_prev^T
 on the Llama-2-7B-shaped up_proj layer (11008 x 4096 bf16, X 262,144 x 4096 bf16,
 frames r = 1.1: K_out x K_in = 12112 x 4512, block 128).  Inputs are synthetic and
-seeded (fq_inputs).  --streams 2 forms D on a second stream while the main stream
-factors H~.
+seeded (fq_inputs).  The frames are applied from their construction (rotation and
+per-block DFT; --frames dense multiplies by the d x K matrices instead, and the pass with
+the other choice is timed beside the headline).  With --streams 2 (the default) D is
+formed on a second stream while the main stream factors H~.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--streams 1|2] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--streams 1|2]
+                    [--frames structured|dense] [--no-cpu-baseline]
 
 Prints one JSON line.  value = quantized weights per second (d_out * d_in / step time).
 "roofline" is the dominant kernel's algorithmic throughput against its MFMA peak, timed
@@ -503,10 +506,10 @@ def main():
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--layer", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
-                    help="2: D is formed on a second stream while the main stream factors "
-                         "H~ (measured within 0.5%% of one stream: the contractions take "
-                         "every CU); the kernel-timer region always uses one")
+    ap.add_argument("--streams", type=int, default=2, choices=(1, 2),
+                    help="2 (default): D is formed on a second stream while the main stream "
+                         "factors H~ (the factorization is a chain of small kernels that leaves "
+                         "most CUs idle); 1: one stream.  The kernel-timer region always uses one")
     ap.add_argument("--frames", default="structured", choices=("structured", "dense"),
                     help="how the pass applies the frames in the analysis and the synthesis: "
                          "from their construction (default) or as the dense d x K matrices; "

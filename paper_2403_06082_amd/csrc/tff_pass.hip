@@ -217,29 +217,40 @@ __global__ __launch_bounds__(TT) void k_zero_pads(u16* hi, u16* lo, int64_t n, i
 }
 
 // F_c for c < rho/2 as bf16 (hi, lo) planes [c][pm][pk] (rows 2j + e, columns 2s + e'),
-// zero outside 2m x 2k.  One thread per entry.
+// zero outside 2m x 2k.  One thread per 2 x 2 entry block (c, j, s): one phase, four
+// entries, 32-bit stores (pm and pk are even).
 __global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm, int pk,
                                                    float scale, u16* __restrict__ hi,
                                                    u16* __restrict__ lo) {
-  const int64_t total = (int64_t)nb * pm * pk;
+  const int hm = pm / 2, hk = pk / 2;
+  const int64_t total = (int64_t)nb * hm * hk;
   for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * TT) {
-    const int64_t c = e / ((int64_t)pm * pk);
-    const int64_t rc = e - c * pm * pk;
-    const int row = (int)(rc / pk), col = (int)(rc - (int64_t)(rc / pk) * pk);
-    float v = 0.f;
-    if (row < 2 * m && col < 2 * k) {
-      const int64_t j = row >> 1, s = col >> 1;
-      const int64_t ph = ((c * m + j) % k) * s % k;
-      float sn, cs;
+    const int64_t c = e / ((int64_t)hm * hk);
+    const int64_t rc = e - c * hm * hk;
+    const int j = (int)(rc / hk), sx = (int)(rc - (int64_t)j * hk);
+    float cs = 0.f, sn = 0.f;
+    if (j < m && sx < k) {
+      const int64_t ph = ((c * m + j) % k) * sx % k;
       sincospif(2.0f * (float)ph / (float)k, &sn, &cs);
-      const int er = row & 1, ec = col & 1;
-      v = (er == ec) ? cs : (er ? sn : -sn);
-      v *= scale;
+      cs *= scale;
+      sn *= scale;
     }
-    const uint32_t h = rne_bf16(v);
-    hi[e] = (u16)h;
-    lo[e] = (u16)rne_bf16(v - __uint_as_float(h << 16));
+    // rows 2j (x) and 2j + 1 (y); columns 2s (re) and 2s + 1 (im)
+    const float v00 = cs, v01 = -sn, v10 = sn, v11 = cs;
+    auto pair = [](float a, float b, uint32_t& h, uint32_t& l) {
+      const uint32_t ha = rne_bf16(a), hb = rne_bf16(b);
+      h = ha | (hb << 16);
+      l = rne_bf16(a - __uint_as_float(ha << 16)) | (rne_bf16(b - __uint_as_float(hb << 16)) << 16);
+    };
+    uint32_t h0, l0, h1, l1;
+    pair(v00, v01, h0, l0);
+    pair(v10, v11, h1, l1);
+    const int64_t r0 = (c * pm + 2 * j) * pk + 2 * sx;
+    *reinterpret_cast<uint32_t*>(hi + r0) = h0;
+    *reinterpret_cast<uint32_t*>(lo + r0) = l0;
+    *reinterpret_cast<uint32_t*>(hi + r0 + pk) = h1;
+    *reinterpret_cast<uint32_t*>(lo + r0 + pk) = l1;
   }
 }
 
@@ -308,30 +319,36 @@ __global__ __launch_bounds__(TT) void k_gather(const float* __restrict__ M, int6
 
 // V[r][c pk + p] = code(r, q) - zero[r] as bf16 (small integers, exact), q as in k_gather,
 // for r < rows; 0 for p in [2k, pk).  codes: cpw = floor(32 / bits) per word, row-major.
-// One thread per output element.
+// One thread per (r, s) pair slot s < pk / 2: the rho codes of subspace s (frame columns
+// s rho .. s rho + rho - 1) go to column pair s of every block, one 32-bit store each.
 __global__ __launch_bounds__(TT) void k_dequant_gather(const uint32_t* __restrict__ codes,
                                                        int bits, const float* __restrict__ zero,
-                                                       int64_t rows, int64_t K, int k2, int pk,
+                                                       int64_t rows, int64_t K, int k, int pk,
                                                        int rho, int nb, u16* __restrict__ V,
                                                        int64_t ldv) {
   const int cpw = 32 / bits;
   const uint32_t mask = (1u << bits) - 1u;
   const int64_t nw = (K + cpw - 1) / cpw;
-  const int64_t per = (int64_t)nb * pk;
-  const int64_t total = rows * per;
+  const int hk = pk / 2;
+  const int64_t total = rows * hk;
   for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * TT) {
-    const int64_t r = e / per;
-    const int64_t rc = e - r * per;
-    const int c = (int)(rc / pk), p = (int)(rc - (int64_t)c * pk);
-    uint32_t h = 0;
-    if (p < k2) {
-      const int64_t q = (int64_t)(p >> 1) * rho + 2 * c + (p & 1);
-      const int64_t w = q / cpw;
-      const uint32_t code = (codes[r * nw + w] >> (bits * (int)(q - w * cpw))) & mask;
-      h = __float_as_uint((float)code - zero[r]) >> 16;
+    const int64_t r = e / hk;
+    const int sx = (int)(e - r * hk);
+    const uint32_t* row = codes + r * nw;
+    const float z = zero[r];
+    u16* dst = V + r * ldv + 2 * sx;
+    for (int c = 0; c < nb; ++c) {
+      uint32_t v = 0;
+      if (sx < k) {
+        const int64_t q = (int64_t)sx * rho + 2 * c;
+        const int64_t w0 = q / cpw, w1 = (q + 1) / cpw;
+        const uint32_t c0 = (row[w0] >> (bits * (int)(q - w0 * cpw))) & mask;
+        const uint32_t c1 = (row[w1] >> (bits * (int)(q + 1 - w1 * cpw))) & mask;
+        v = (__float_as_uint((float)c0 - z) >> 16) | (__float_as_uint((float)c1 - z) & 0xFFFF0000u);
+      }
+      *reinterpret_cast<uint32_t*>(dst + (int64_t)c * pk) = v;
     }
-    V[r * ldv + rc] = (u16)h;
   }
 }
 
@@ -429,7 +446,7 @@ TffPassGeom tff_pass_geom(const TffDev& F) {
 hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s) {
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_blocks");
-  hipLaunchKernelGGL(k_dft_blocks, dim3(grid_1d(g.nb * g.pm * g.pk)), dim3(TT), 0, s, (int)F.k,
+  hipLaunchKernelGGL(k_dft_blocks, dim3(grid_1d(g.nb * (g.pm / 2) * (g.pk / 2))), dim3(TT), 0, s, (int)F.k,
                      (int)F.m, (int)g.nb, (int)g.pm, (int)g.pk,
                      (float)(1.0 / std::sqrt((double)F.k)), hi, lo);
   prof_end(s);
@@ -487,8 +504,8 @@ hipError_t tff_dequant_gather(const uint32_t* codes, int bits, const float* zero
   if (rows == 0) return hipSuccess;
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_gather");
-  hipLaunchKernelGGL(k_dequant_gather, dim3(grid_1d(rows * g.nb * g.pk)), dim3(TT), 0, s, codes, bits,
-                     zero, rows, F.k * F.rho, (int)g.k2, (int)g.pk, (int)F.rho, (int)g.nb, V,
+  hipLaunchKernelGGL(k_dequant_gather, dim3(grid_1d(rows * (g.pk / 2))), dim3(TT), 0, s, codes, bits,
+                     zero, rows, F.k * F.rho, (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V,
                      g.nb * g.pk);
   prof_end(s);
   return last_launch_error();
