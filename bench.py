@@ -514,6 +514,10 @@ def main():
                     help="how the pass applies the frames in the analysis and the synthesis: "
                          "from their construction (default) or as the dense d x K matrices; "
                          "the other way is timed beside it")
+    ap.add_argument("--pass-only", action="store_true",
+                    help="time the pass only (no pass with the other frames, no inference, frame "
+                         "generation or grid variants): the kernel trace then covers exactly "
+                         "the warmup, timed and kernel-timer passes")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="device-to-device copy of this many MiB before the warmup, as the "
                          "known-size reference for hardware byte counters")
@@ -676,6 +680,9 @@ def main():
         "kernels": kernels,
         "kernel_ms_total_per_step": round(tot_all / args.steps, 3),
     }
+    if args.pass_only:
+        print(json.dumps(out), flush=True)
+        return
     # the pass with the frames applied the other way, same inputs (one warmup, `steps` timed)
     other = "dense" if args.frames == "structured" else "structured"
     ob = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
