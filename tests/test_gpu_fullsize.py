@@ -1,6 +1,8 @@
 """Parity at the full workload sizes, in the launch configuration the benchmark times
-(one LayerBuffers per layer shape, the four ABI calls in order, H computed from all of X),
-checked on sampled outputs the oracle can compute one by one:
+(one LayerBuffers per layer shape, the four ABI calls in order, H computed from all of X;
+frames applied from their construction, D formed on a second stream while the first
+factors H~; two layers also with the dense frames on one stream), checked on sampled
+outputs the oracle can compute one by one:
   H      : the principal submatrix on 64 random channels plus every outlier channel;
   D      : 16 random rows, P_out[:, r]^T W P_in;
   H~     : in full, P_in^T H P_in from the device's H (stage isolation); for the
@@ -49,7 +51,7 @@ def _calibration(key):
     return _X[key]
 
 
-def fullsize_layer(key, li, n_code_rows=48, replay=True):
+def fullsize_layer(key, li, n_code_rows=48, replay=True, frames="structured"):
     torch = need_gpu()
     from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
     wl = WORKLOADS[key]
@@ -62,13 +64,22 @@ def fullsize_layer(key, li, n_code_rows=48, replay=True):
     W = upload(Ws, wl.w_dtype)
     K_out, K_in = Po.shape[1], Pi.shape[1]
     _log(f"frames and weight built in {time.time() - t:.1f}s (K_out {K_out}, K_in {K_in})")
-    bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, X.shape[0], wl.block)
+    F = None
+    side = None
+    if frames == "structured":
+        import paper_2403_06082_amd as fq
+        (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, li)
+        up = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+        F = (fq.Frame(L.d_out, ko, ro, up(R1o), up(R2o)), fq.Frame(L.d_in, ki, ri, up(R1i), up(R2i)))
+        side = torch.cuda.Stream()
+    bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, X.shape[0], wl.block,
+                        frames=F)
     P_out, P_in = torch.from_numpy(Po).cuda(), torch.from_numpy(Pi).cuda()
     t = time.time()
     quantize_layer(W, X, P_out, P_in, bufs, block=wl.block, damp=wl.damp,
-                   clip_sigmas=wl.clip_sigmas)
+                   clip_sigmas=wl.clip_sigmas, side_stream=side)
     torch.cuda.synchronize()
-    _log(f"device pass done in {time.time() - t:.1f}s")
+    _log(f"device pass ({frames} frames) done in {time.time() - t:.1f}s")
     rng = np.random.default_rng([li, K_out, K_in])
 
     # stage 1: principal submatrix of H on sampled channels
@@ -164,9 +175,17 @@ def test_fullsize_llama7b_up():
     fullsize_layer("llama7b", 1)
 
 
+def test_fullsize_llama7b_up_dense_frames():
+    fullsize_layer("llama7b", 1, frames="dense")
+
+
 def test_fullsize_llama70b_r10_down():
     fullsize_layer("llama70b_r1.0", 0, n_code_rows=128, replay=False)
 
 
 def test_fullsize_llama70b_r11_down():
     fullsize_layer("llama70b_r1.1", 0, n_code_rows=128, replay=False)
+
+
+def test_fullsize_llama70b_r11_down_dense_frames():
+    fullsize_layer("llama70b_r1.1", 0, n_code_rows=128, replay=False, frames="dense")
