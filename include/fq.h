@@ -273,7 +273,7 @@ size_t fq_tff_materialize_workspace_bytes(const fq_tff* frame);
  *   D          device fp32 K_out x K_in (K = k rho) or NULL.
  *   Ht         device fp32 K_in x K_in or NULL; written as (B + B^T) / 2 of the computed
  *              product B, so exactly symmetric.
- * Frames as fq_tff_analysis; in addition d <= 2^21 and K <= 2^21 (else
+ * Frames as fq_tff_analysis; in addition d <= 2^21 and K <= 65535 * 32 (else
  * FQ_ERR_UNSUPPORTED).  ws: fq_frame_analysis_tff_workspace_bytes(wt, frame_out,
  * frame_in) bytes, 16-byte aligned.  Stream-ordered; errors as fq_frame_analysis.
  */

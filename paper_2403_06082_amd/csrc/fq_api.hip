@@ -983,14 +983,15 @@ fq_status fq_tff_materialize(void* stream, const fq_tff* frame, float* P, int64_
 }
 
 // ================================================================ structured S2 / S4
-static constexpr int64_t TFFP_MAX = (int64_t)1 << 21;   // d and K limit of the structured pass
+static constexpr int64_t TFFP_MAX = (int64_t)1 << 21;   // d limit of the structured pass
+static constexpr int64_t TFFP_MAX_K = (int64_t)65535 * 32; // K limit (32-tiles per grid axis)
 
 static fq_status tffp_check(const fq_tff* f, const char* which, TffDev* F) {
   fq_status st = tff_check(f, which, F);
   if (st != FQ_OK) return st;
-  if (F->d > TFFP_MAX || F->k * F->rho > TFFP_MAX) {
+  if (F->d > TFFP_MAX || F->k * F->rho > TFFP_MAX_K) {
     char msg[128];
-    snprintf(msg, sizeof msg, "%s: d and k * rho must not exceed 2^21 here", which);
+    snprintf(msg, sizeof msg, "%s: d must not exceed 2^21 and k * rho 65535 * 32 here", which);
     return fail(FQ_ERR_UNSUPPORTED, msg);
   }
   return FQ_OK;
@@ -1004,7 +1005,7 @@ static TffDev tff_dev_of(const fq_tff* f) {
 }
 
 static bool tffp_dims_ok(const fq_tff* f) {
-  return tff_dims_ok(f) && f->d <= TFFP_MAX && f->k * f->rho <= TFFP_MAX;
+  return tff_dims_ok(f) && f->d <= TFFP_MAX && f->k * f->rho <= TFFP_MAX_K;
 }
 
 // F_c planes of both frames, then the stage buffers (the largest stage of each).
@@ -1061,7 +1062,7 @@ fq_status fq_frame_analysis_tff(void* stream, const void* W, int wt, const fq_tf
   hipStream_t s = (hipStream_t)stream;
   TffAnaLayout L;
   tff_ana_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
-  const int64_t K_out = Fo.k * Fo.rho, K_in = Fi.k * Fi.rho;
+  const int64_t K_in = Fi.k * Fi.rho;
   hipError_t e;
   if ((e = tff_dft_blocks(Fi, L.fi_hi, L.fi_lo, s)) != hipSuccess) return hip_fail(e, "frame_in blocks");
   if (D) {
@@ -1085,7 +1086,6 @@ fq_status fq_frame_analysis_tff(void* stream, const void* W, int wt, const fq_tf
       return hip_fail(e, "analysis of the columns of H P_in");
     if ((e = sym_average(Ht, K_in, K_in, s)) != hipSuccess) return hip_fail(e, "symmetrize Ht");
   }
-  (void)K_out;
   return FQ_OK;
 }
 

@@ -144,6 +144,9 @@ def test_structured_pass_arguments(L):
     assert L.fq_frame_analysis_tff_workspace_bytes(2, bp, gp) == 0
     assert L.fq_frame_analysis_tff(n, p, 2, bp, gp, p, p, p, p, 1 << 40) == 2
     assert L.fq_frame_synthesis_tff(n, p, 2, p, p, gp, bp, p, p, 1 << 40) == 2
+    wide = ctypes.byref(TFF(1 << 20, 3968, 1024, 64, 256, 64, 4096))   # K = 3968 * 1024 > 65535 * 32
+    assert L.fq_frame_analysis_tff_workspace_bytes(2, wide, gp) == 0
+    assert L.fq_frame_analysis_tff(n, p, 2, wide, gp, p, p, p, p, 1 << 40) == 2
     bad = ctypes.byref(TFF(4096, 282, 15, 64, 64, 64, 64))
     assert L.fq_frame_analysis_tff(n, p, 2, bad, gp, p, p, p, p, 1 << 40) == 1
     assert b"frame_out" in L.fq_last_error()
