@@ -683,6 +683,24 @@ def main():
     if args.pass_only:
         print(json.dumps(out), flush=True)
         return
+    # the pass without S1: H given (it is shared by layers that read the same input, such
+    # as q/k/v or gate/up), same frames and streams
+    def gstep():
+        quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], bufs, H=bufs.H,
+                       block=wl.block, damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream,
+                       side_stream=side)
+
+    gstep()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        gstep()
+    torch.cuda.synchronize()
+    gms = (time.perf_counter() - t0) * 1000.0 / args.steps
+    out["pass_given_H"] = {"ms_per_step": round(gms, 3),
+                           "weights_per_s": round(L.d_out * L.d_in / (gms / 1e3), 1),
+                           "note": "S2 -> S4 with H from the headline pass"}
+    print(f"[bench] pass with H given: {gms:.2f} ms/step", file=sys.stderr, flush=True)
     # the pass with the frames applied the other way, same inputs (one warmup, `steps` timed)
     other = "dense" if args.frames == "structured" else "structured"
     ob = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,

@@ -14,6 +14,7 @@
 #include "fq_internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace fq {
 
@@ -1005,7 +1006,36 @@ hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& 
 // above the diagonal inside a panel pick up finite values that are never read.
 constexpr int64_t CHOL_PANEL = 256;
 
+namespace {
+// Auxiliary stream and events of the look-ahead factorization, one set per device, made on
+// first use (default priority).  The mutex also keeps the event records and waits of one
+// factorization from interleaving with another's.
+struct CholAux {
+  hipStream_t s2 = nullptr;
+  hipEvent_t chain = nullptr, upd = nullptr;
+  bool ok = false, init = false;
+};
+std::mutex g_chol_mu;
+CholAux g_chol_aux[64];
+
+CholAux* chol_aux() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  CholAux& a = g_chol_aux[dev];
+  if (!a.init) {
+    a.init = true;
+    a.ok = hipStreamCreateWithFlags(&a.s2, hipStreamNonBlocking) == hipSuccess &&
+           hipEventCreateWithFlags(&a.chain, hipEventDisableTiming) == hipSuccess &&
+           hipEventCreateWithFlags(&a.upd, hipEventDisableTiming) == hipSuccess;
+  }
+  return a.ok ? &a : nullptr;
+}
+}  // namespace
+
 hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_chol_mu);
+  CholAux* aux = chol_aux();
+  bool pending = false;            // a trailing update is in flight on the auxiliary stream
   for (int64_t j0 = 0; j0 < K; j0 += CHOL_PANEL) {
     const int64_t jb = std::min<int64_t>(CHOL_PANEL, K - j0);
     for (int64_t k0 = j0; k0 < j0 + jb; k0 += 64) {
@@ -1029,14 +1059,47 @@ hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s
         if (e != hipSuccess) return e;
       }
     }
-    // trailing matrix (lower triangle) right of the panel, at rank jb
-    const int64_t rest = K - j0 - jb;
-    if (rest > 0) {
-      const double* Pp = A + (j0 + jb) * K + j0;
-      hipError_t e = dgemm(rest, rest, jb, -1.0, 1.0, Pp, K, Pp, K, true,
-                           A + (j0 + jb) * K + (j0 + jb), K, true, s, "chol_syrk", 64);
+    // rank-jb update of the trailing matrix right of the panel, in two parts (look-ahead):
+    // (a) the next panel's columns, on this stream, which the next panel's factorization
+    //     needs; (b) everything right of the next panel, on the auxiliary stream, beside
+    //     the next panel's factorization (which touches only its own columns).  (a) of the
+    //     next panel waits for (b) of this one, which updated the same columns.
+    const int64_t j1 = j0 + jb;
+    const int64_t rest = K - j1;
+    if (rest <= 0) continue;
+    const int64_t jb1 = std::min<int64_t>(CHOL_PANEL, rest);
+    const int64_t j2 = j1 + jb1, rest2 = K - j2;
+    hipError_t e;
+    if (aux && pending) {
+      if ((e = hipStreamWaitEvent(s, aux->upd, 0)) != hipSuccess) return e;
+      pending = false;
+    }
+    // (a): rows j1.., columns [j1, j2) (a full rectangle: the upper triangle of the next
+    // diagonal block is never read)
+    const double* Pa = A + j1 * K + j0;
+    e = dgemm(rest, jb1, jb, -1.0, 1.0, Pa, K, Pa, K, true, A + j1 * K + j1, K, false, s,
+              "chol_syrk", 64);
+    if (e != hipSuccess) return e;
+    if (rest2 <= 0) continue;
+    // (b): rows j2.., columns [j2, K) (lower triangle)
+    const double* Pb = A + j2 * K + j0;
+    if (aux) {
+      if ((e = hipEventRecord(aux->chain, s)) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(aux->s2, aux->chain, 0)) != hipSuccess) return e;
+      e = dgemm(rest2, rest2, jb, -1.0, 1.0, Pb, K, Pb, K, true, A + j2 * K + j2, K, true,
+                aux->s2, "chol_syrk", 64);
+      if (e != hipSuccess) return e;
+      if ((e = hipEventRecord(aux->upd, aux->s2)) != hipSuccess) return e;
+      pending = true;
+    } else {
+      e = dgemm(rest2, rest2, jb, -1.0, 1.0, Pb, K, Pb, K, true, A + j2 * K + j2, K, true, s,
+                "chol_syrk", 64);
       if (e != hipSuccess) return e;
     }
+  }
+  if (aux && pending) {
+    hipError_t e = hipStreamWaitEvent(s, aux->upd, 0);
+    if (e != hipSuccess) return e;
   }
   return last_launch_error();
 }
