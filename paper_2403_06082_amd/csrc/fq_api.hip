@@ -126,11 +126,6 @@ static size_t hessian_layout(int xt, int64_t n, int64_t d, void* ws, HessLayout*
 
 static int64_t rup32(int64_t x) { return (x + 31) / 32 * 32; }
 
-// Operand planes of the analysis, every one stored K-contiguous and zero-padded in K to a
-// multiple of 32 (the layout the asynchronous MFMA kernel reads):
-//   pot  = P_out^T  [K_out x pad(d_out)]    wt = W^T  [d_in x pad(d_out)]
-//   t    = P_out^T W [K_out x pad(d_in)]    pit = P_in^T [K_in x pad(d_in)]
-//   h    = H [d_in x pad(d_in)]             gt = P_in^T H [K_in x pad(d_in)]
 // Analysis planes.  Every product reads both operands with the reduction index as the
 // row (row-contiguous in the other index), so each operand is the caller's array as laid
 // out, split into bf16 planes with rows and columns zero-padded:
