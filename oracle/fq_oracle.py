@@ -368,3 +368,70 @@ def quantize_layer(W, X_chunks, P_out, P_in, bits=2, block=128, damp=0.01,
     r["packed"] = pack2(r["codes"])
     r["W_hat"] = synthesis(r["codes"], r["scale"], r["zero"], P_out, P_in)
     return r
+
+
+# --------------------------------------------------------------------------- seeded rotation
+# The rotation factors of a frame drawn from a 64-bit seed (Sec. 2.2 and the appendix on
+# constructing TFFs take a random rotation; the storage appendix keeps only (k, rho, d)
+# and what regenerates the rotation).  Recipe (a reading: the paper names no generator):
+#   * Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11), key = (seed mod 2^32,
+#     seed div 2^32), counter = (p mod 2^32, p div 2^32, f, 0) for pair p of factor f;
+#   * its 4 output words (x0, x1, x2, x3) give u1 from (x0, x1) and u2 from (x2, x3):
+#     u = (2^21 x_odd + floor(x_even / 2^11) + 1/2) / 2^53, in (0, 1);
+#   * Box-Muller: entries 2p and 2p + 1 of the row-major n x n matrix G are
+#     sqrt(-2 ln u1) cos(2 pi u2) and sqrt(-2 ln u1) sin(2 pi u2);
+#   * the factor is Q of G = Q R with R's diagonal made positive (the signs of R's
+#     diagonal moved into Q), a Haar-distributed orthogonal matrix.
+PHILOX_M = (0xD2511F53, 0xCD9E8D57)
+PHILOX_W = (0x9E3779B9, 0xBB67AE85)
+
+
+def philox4x32_10(counters, key):
+    """Philox4x32 with 10 rounds on an (N, 4) array of uint32 counters and a key of two
+    uint32 words (Salmon et al., SC'11): each round multiplies words 0 and 2 by the two
+    multipliers, mixes the halves of the products with words 1, 3 and the key, and the
+    key is bumped by the two Weyl constants between rounds."""
+    c = np.asarray(counters, dtype=np.uint64).reshape(-1, 4).copy()
+    k0, k1 = np.uint64(key[0]), np.uint64(key[1])
+    mask = np.uint64(0xFFFFFFFF)
+    for _ in range(10):
+        p0 = np.uint64(PHILOX_M[0]) * c[:, 0]
+        p1 = np.uint64(PHILOX_M[1]) * c[:, 2]
+        hi0, lo0 = p0 >> np.uint64(32), p0 & mask
+        hi1, lo1 = p1 >> np.uint64(32), p1 & mask
+        c = np.stack([(hi1 ^ c[:, 1] ^ k0) & mask, lo1, (hi0 ^ c[:, 3] ^ k1) & mask, lo0], axis=1)
+        k0 = (k0 + np.uint64(PHILOX_W[0])) & mask
+        k1 = (k1 + np.uint64(PHILOX_W[1])) & mask
+    return c.astype(np.uint32)
+
+
+def seeded_gaussian(seed: int, f: int, n: int) -> np.ndarray:
+    """The n x n Gaussian matrix of factor f drawn from `seed` by the recipe above."""
+    total = n * n
+    npair = (total + 1) // 2
+    p = np.arange(npair, dtype=np.uint64)
+    ctr = np.stack([p & np.uint64(0xFFFFFFFF), p >> np.uint64(32),
+                    np.full(npair, f, np.uint64), np.zeros(npair, np.uint64)], axis=1)
+    x = philox4x32_10(ctr, (seed & 0xFFFFFFFF, seed >> 32)).astype(np.uint64)
+
+    def unif(lo_w, hi_w):
+        m = (hi_w << np.uint64(21)) | (lo_w >> np.uint64(11))
+        return (m.astype(np.float64) + 0.5) / 2.0 ** 53
+
+    u1, u2 = unif(x[:, 0], x[:, 1]), unif(x[:, 2], x[:, 3])
+    rad = np.sqrt(-2.0 * np.log(u1))
+    g = np.empty(2 * npair)
+    g[0::2] = rad * np.cos(2.0 * np.pi * u2)
+    g[1::2] = rad * np.sin(2.0 * np.pi * u2)
+    return g[:total].reshape(n, n)
+
+
+def seeded_haar(seed: int, f: int, n: int) -> np.ndarray:
+    """Factor f (0: R1, 1: R2) of the rotation drawn from `seed`: Q of the QR of the
+    seeded Gaussian matrix with R's diagonal made positive (LAPACK QR; the positive-
+    diagonal QR is unique, so any QR algorithm gives the same Q)."""
+    G = seeded_gaussian(seed, f, n)
+    Q, R = np.linalg.qr(G)
+    sg = np.sign(np.diag(R))
+    sg[sg == 0] = 1.0
+    return Q * sg[None, :]

@@ -4,6 +4,7 @@ Each check is chosen so that a plausible slip in the oracle (a dropped term, a w
 sign or index, a transposed operand) fails at least one of them.
 """
 import itertools
+import os
 
 import numpy as np
 import pytest
@@ -415,3 +416,50 @@ def test_tail_pre_rounding_matches_replay():
         bad[:, 3] = (bad[:, 3] + 1) % 4
         w_bad = O.gptq_tail_pre_rounding(Dc, O.dequant(bad, s, z), Ht, 9)
         assert np.abs(w_bad / s[:, None] - r["t"][:, 9:]).max() > 1e-3
+
+
+# ---------------------------------------------------------------- seeded rotation factors
+def _kat_rows():
+    path = os.path.join(os.path.dirname(__file__), "golden", "philox4x32_10_kat.txt")
+    rows = []
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            w = [int(x, 16) for x in line.split()]
+            rows.append((w[0:4], w[4:6], w[6:10]))
+    return rows
+
+
+def test_philox_known_answers():
+    """The oracle's Philox4x32-10 reproduces the generator's published known-answer
+    vectors (tests/golden/philox4x32_10_kat.txt)."""
+    rows = _kat_rows()
+    assert len(rows) == 3
+    for ctr, key, out in rows:
+        np.testing.assert_array_equal(O.philox4x32_10([ctr], key)[0], np.array(out, np.uint32))
+
+
+def test_seeded_gaussian_moments_and_streams():
+    """Box-Muller over the generator: mean, variance and fourth moment of N(0, 1) within
+    5 standard errors on 2.5e5 draws; factors 0 and 1 and different seeds give different
+    matrices; the matrix of an n x n factor is the leading part of the pair stream (odd n)."""
+    G = O.seeded_gaussian(7, 0, 500).ravel()
+    n = G.size
+    assert abs(G.mean()) < 5 / np.sqrt(n)
+    assert abs(G.var() - 1.0) < 5 * np.sqrt(2.0 / n)
+    assert abs(np.mean(G ** 4) - 3.0) < 5 * np.sqrt(96.0 / n)
+    assert not np.allclose(O.seeded_gaussian(7, 0, 9), O.seeded_gaussian(7, 1, 9))
+    assert not np.allclose(O.seeded_gaussian(7, 0, 9), O.seeded_gaussian(8, 0, 9))
+    a, b = O.seeded_gaussian(3, 1, 5).ravel(), O.seeded_gaussian(3, 1, 7).ravel()
+    np.testing.assert_array_equal(a, b[:25])
+
+
+@pytest.mark.parametrize("n", [1, 2, 17, 86, 128])
+def test_seeded_haar_is_the_positive_qr_factor(n):
+    """Q is orthogonal and Q^T G is upper triangular with a positive diagonal: the unique
+    QR with positive R, whatever algorithm formed it."""
+    G = O.seeded_gaussian(11, 1, n)
+    Q = O.seeded_haar(11, 1, n)
+    np.testing.assert_allclose(Q.T @ Q, np.eye(n), atol=1e-12)
+    R = Q.T @ G
+    np.testing.assert_allclose(np.tril(R, -1), 0.0, atol=1e-10)
+    assert np.all(np.diag(R) > 0)
