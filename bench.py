@@ -382,7 +382,21 @@ def frame_generation_bench(fq, torch, dev, wl, li, host, iters=5):
         torch.cuda.synchronize()
         out[name] = {"shape": [d, F.K], "ms": round(e0.elapsed_time(e1) / iters, 3),
                      "max_abs_diff_vs_host_frame": err}
-        del P, ws
+        # the same layer's rotation factors drawn on the device from a seed
+        d1, d2 = R1.shape[0], R2.shape[0]
+        wsr = torch.empty(fq.fq_tff_rotation_factors_workspace_bytes(d1, d2), dtype=torch.uint8,
+                          device="cuda")
+        S1 = torch.empty((d1, d1), dtype=torch.float32, device="cuda")
+        S2 = torch.empty((d2, d2), dtype=torch.float32, device="cuda")
+        fq.fq_tff_rotation_factors(wl.seed, d1, d2, R1=S1, R2=S2, ws=wsr, stream=stream)
+        e0.record(stream)
+        for _ in range(iters):
+            fq.fq_tff_rotation_factors(wl.seed, d1, d2, R1=S1, R2=S2, ws=wsr, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out[name]["seeded_factors"] = {"d1": d1, "d2": d2,
+                                       "ms": round(e0.elapsed_time(e1) / iters, 3)}
+        del P, ws, wsr
     out["host_float64_seconds_both"] = round(host["frames_host_s"], 2)
     return out
 

@@ -302,6 +302,24 @@ fq_status fq_frame_synthesis_tff(void* stream, const uint32_t* codes, int bits,
 size_t fq_frame_synthesis_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
 
 /*
+ * The two rotation factors of a frame drawn on the device from a 64-bit seed (Sec. 2.2 and
+ * the appendix on constructing TFFs take a random rotation; the storage appendix keeps
+ * only (k, rho, d) and what regenerates it).  The paper names no generator; the recipe:
+ * Philox4x32-10 (Salmon et al., SC'11) with key = the seed's two 32-bit halves and
+ * counter = (pair index, factor index (0: R1, 1: R2), 0), two uniforms of 53 bits per
+ * output, Box-Muller to an n x n Gaussian matrix G (row-major), and the factor is Q of
+ * the QR of G with R's diagonal positive (a Haar-distributed orthogonal matrix), formed
+ * by fp64 Householder reflections and stored in fp32.
+ *   R1, R2   device fp32 d1 x d1 and d2 x d2, row-major, written; usable as fq_tff.R1/R2.
+ * 1 <= d1, d2 <= 1024 (larger: FQ_ERR_UNSUPPORTED).  ws:
+ * fq_tff_rotation_factors_workspace_bytes(d1, d2) bytes, 16-byte aligned.  Stream-ordered;
+ * one work-group forms each factor (about n^3 fp64 operations, milliseconds at n = 224).
+ */
+fq_status fq_tff_rotation_factors(void* stream, uint64_t seed, int64_t d1, int64_t d2, float* R1,
+                                  float* R2, void* ws, size_t ws_bytes);
+size_t fq_tff_rotation_factors_workspace_bytes(int64_t d1, int64_t d2);
+
+/*
  * Rounding of the frame representation of activations to act_bits-bit integers (appendix
  * "FrameQuant for Activation Quantization?"): per token t (row of U),
  * Delta_t = max_j |U_tj| / (2^(act_bits-1) - 1) and Cq_tj = round(U_tj / Delta_t), with

@@ -1153,4 +1153,40 @@ fq_status fq_frame_synthesis_tff(void* stream, const uint32_t* codes, int bits,
   return FQ_OK;
 }
 
+// ================================================================ seeded rotation factors
+static size_t seed_layout(int64_t n, void* base, double** G, double** V, double** ab) {
+  Carver c(base);
+  double* g = c.take<double>((size_t)(n * n));
+  double* v = c.take<double>((size_t)(n * n));
+  double* a = c.take<double>((size_t)(2 * n));
+  if (G) *G = g;
+  if (V) *V = v;
+  if (ab) *ab = a;
+  return c.off + 256;
+}
+
+size_t fq_tff_rotation_factors_workspace_bytes(int64_t d1, int64_t d2) {
+  if (d1 < 1 || d2 < 1 || d1 > TFF_SEED_MAX_N || d2 > TFF_SEED_MAX_N) return 0;
+  return seed_layout(std::max(d1, d2), nullptr, nullptr, nullptr, nullptr);
+}
+
+fq_status fq_tff_rotation_factors(void* stream, uint64_t seed, int64_t d1, int64_t d2, float* R1,
+                                  float* R2, void* ws, size_t ws_bytes) {
+  if (d1 < 1 || d2 < 1) return fail(FQ_ERR_INVALID_ARG, "d1 and d2 must be >= 1");
+  if (d1 > TFF_SEED_MAX_N || d2 > TFF_SEED_MAX_N)
+    return fail(FQ_ERR_UNSUPPORTED, "seeded factors are drawn for d1, d2 <= 1024");
+  if (!R1 || !R2) return fail(FQ_ERR_INVALID_ARG, "NULL R1 or R2");
+  const int64_t n = std::max(d1, d2);
+  if (ws_bytes < seed_layout(n, nullptr, nullptr, nullptr, nullptr))
+    return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_tff_rotation_factors_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  double *G, *V, *ab;
+  seed_layout(n, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &G, &V, &ab);
+  hipError_t e;
+  if ((e = tff_seeded_factor(seed, 0, (int)d1, G, V, ab, R1, s)) != hipSuccess) return hip_fail(e, "R1");
+  if ((e = tff_seeded_factor(seed, 1, (int)d2, G, V, ab, R2, s)) != hipSuccess) return hip_fail(e, "R2");
+  return FQ_OK;
+}
+
 }  // extern "C"

@@ -142,6 +142,12 @@ hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const T
 hipError_t transpose_f32(const float* in, int64_t rows, int64_t cols, int64_t ldin, float* out,
                          int64_t ldout, hipStream_t s);
 hipError_t sym_average(float* X, int64_t n, int64_t ld, hipStream_t s);
+
+// Seeded Haar factor f (tff_seed.hip): out (n x n fp32) from seed; G, V: n x n fp64
+// scratch each, ab: 2n fp64
+constexpr int64_t TFF_SEED_MAX_N = 1024;
+hipError_t tff_seeded_factor(uint64_t seed, int f, int n, double* G, double* V, double* ab,
+                             float* out, hipStream_t s);
 // Y (n x ldy) = V P^T with V n x ldv (ldv even), R2t from tff_transpose_r2; z: n x d scratch
 hipError_t tff_synthesis(const float* V, int64_t ldv, int64_t n, const TffDev& F,
                          const float* R2t, float* z, float* Y, int64_t ldy, hipStream_t s);

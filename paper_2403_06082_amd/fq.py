@@ -70,6 +70,8 @@ SIGNATURES = {
     "fq_frame_analysis_tff_workspace_bytes": (_sz, [_i, _tp, _tp]),
     "fq_frame_synthesis_tff": (_i, [_vp, _vp, _i, _vp, _vp, _tp, _tp, _vp, _vp, _sz]),
     "fq_frame_synthesis_tff_workspace_bytes": (_sz, [_tp, _tp]),
+    "fq_tff_rotation_factors": (_i, [_vp, ctypes.c_uint64, _i64, _i64, _vp, _vp, _vp, _sz]),
+    "fq_tff_rotation_factors_workspace_bytes": (_sz, [_i64, _i64]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
                                      _vp, _vp, _sz]),
@@ -516,3 +518,24 @@ def fq_frame_synthesis_tff(codes, scale, zero, frame_out: Frame, frame_in: Frame
                                         _ptr(zero), ctypes.byref(frame_out.c),
                                         ctypes.byref(frame_in.c), _ptr(W_hat), wp, wb))
     return W_hat
+
+
+def fq_tff_rotation_factors_workspace_bytes(d1: int, d2: int) -> int:
+    return lib().fq_tff_rotation_factors_workspace_bytes(d1, d2)
+
+
+def fq_tff_rotation_factors(seed: int, d1: int, d2: int, R1=None, R2=None, ws=None, stream=None,
+                            device="cuda"):
+    """(R1, R2): the rotation factors (d1 x d1, d2 x d2 fp32) drawn on the device from a
+    64-bit seed."""
+    torch = _torch()
+    if R1 is None:
+        R1 = torch.empty((d1, d1), dtype=torch.float32, device=device)
+    if R2 is None:
+        R2 = torch.empty((d2, d2), dtype=torch.float32, device=device)
+    _dev(R1, "R1", torch.float32, (d1, d1))
+    _dev(R2, "R2", torch.float32, (d2, d2))
+    ws, wp, wb = _ws(fq_tff_rotation_factors_workspace_bytes(d1, d2), ws, R1.device)
+    _check(lib().fq_tff_rotation_factors(_stream(stream), ctypes.c_uint64(seed & (2 ** 64 - 1)),
+                                         d1, d2, _ptr(R1), _ptr(R2), wp, wb))
+    return R1, R2

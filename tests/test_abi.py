@@ -162,6 +162,19 @@ def test_structured_pass_arguments(L):
     assert L.fq_frame_synthesis_tff(n, p, 2, p, p, gp, gp, p, p, need_s - 1) == 5
 
 
+def test_rotation_factor_arguments(L):
+    p, n = ctypes.c_void_p(64), None
+    need = L.fq_tff_rotation_factors_workspace_bytes(86, 128)
+    assert need >= 2 * 128 * 128 * 8
+    assert L.fq_tff_rotation_factors_workspace_bytes(0, 4) == 0
+    assert L.fq_tff_rotation_factors_workspace_bytes(4, 1025) == 0
+    assert L.fq_tff_rotation_factors(n, 7, 0, 4, p, p, p, need) == 1
+    assert L.fq_tff_rotation_factors(n, 7, 4, 1025, p, p, p, 1 << 40) == 2
+    assert L.fq_tff_rotation_factors(n, 7, 86, 128, n, p, p, need) == 1
+    assert L.fq_tff_rotation_factors(n, 7, 86, 128, p, p, p, need - 1) == 5
+    assert L.fq_tff_rotation_factors(n, 7, 86, 128, p, p, n, need) == 1
+
+
 def test_act_quantize_arguments(L):
     p, n = ctypes.c_void_p(64), None
     assert L.fq_act_quantize(n, p, 4, 8, 1, p, p) == 1
