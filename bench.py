@@ -658,7 +658,8 @@ def main():
     roof["avg_launch_ms"] = round(avg_ms, 4)
     roof["algorithmic_per_launch"] = per_launch
 
-    # spec contraction fraction: Hessian + analysis contractions at bf16 peak
+    # contraction fraction of S1 + S2 (the Hessian and, with dense frames, the analysis
+    # contractions) at bf16 peak
     contr = [k for k in kernels if k.startswith("gemm_hessian") or k.startswith("gemm_analysis")]
     c_flops = sum(work[k][1] for k in contr)
     c_ms = sum(kernels[k]["ms_per_step"] for k in contr)
