@@ -261,6 +261,21 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
                                   stream=stream)
 
         us = _time_calls(torch, call, stream, iters)
+        # the same call captured once into a HIP graph and replayed (no host launch work
+        # per kernel); the replay's output must equal the eager call's
+        call()
+        torch.cuda.synchronize()
+        Y_eager = Y.clone()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fq.fq_frame_apply_tff(X, bufs.codes, bufs.scale, bufs.zero, Fo, Fi, Y=Y, ws=ws,
+                                  stream=torch.cuda.current_stream())
+        Y.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        graph_equal = bool(torch.equal(Y, Y_eager))
+        us_graph = _time_calls(torch, graph.replay, stream, iters)
+        del graph
         kern = _kernel_us(fq, torch, call, ("tff_rotate", "tff_dft", "apply_codes"), iters)
         b = apply_tff_bytes(nt, L.d_out, L.d_in, K_out, K_in, dev["X"].element_size(), rot_floats)
         kc = kern["apply_codes"]
@@ -268,8 +283,12 @@ def structured_bench(fq, torch, dev, bufs, wl, li, K_out, K_in, tokens=(1, 8), i
         kc["GB/s"] = round(kc["algorithmic_bytes"] / kc["us_per_call"] / 1e3, 1)
         rows.append({"tokens": nt, "us_per_call": round(us, 2),
                      "tokens_per_s": round(nt / (us / 1e6), 1), "algorithmic_bytes": b,
-                     "GB/s": round(b / us / 1e3, 1), "kernels": kern})
-        print(f"[bench] frame_apply_tff {nt} token(s): {us:.1f} us/call", file=sys.stderr, flush=True)
+                     "GB/s": round(b / us / 1e3, 1), "kernels": kern,
+                     "hip_graph": {"us_per_call": round(us_graph, 2),
+                                   "tokens_per_s": round(nt / (us_graph / 1e6), 1),
+                                   "output_equals_eager": graph_equal}})
+        print(f"[bench] frame_apply_tff {nt} token(s): {us:.1f} us/call, {us_graph:.1f} us "
+              f"replayed from a HIP graph", file=sys.stderr, flush=True)
     # the same with the frame representation of the inputs rounded to 8-bit integers
     wsq = torch.empty(fq.fq_frame_apply_tff_actq_workspace_bytes(Fo, Fi), dtype=torch.uint8,
                       device="cuda")
