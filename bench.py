@@ -372,6 +372,24 @@ def grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, steps, iters=200,
                       file=sys.stderr, flush=True)
             out["w4a4_inference"] = {"op": "fq_frame_apply_tff_actq, bits 4, act_bits 4, on the "
                                            "4-bit pass's codes", "per_tokens": rows}
+            wsf = torch.empty(fq.fq_frame_apply_tff_workspace_bytes(Fo, Fi), dtype=torch.uint8,
+                              device="cuda")
+            frows = []
+            for nt in (1, 8):
+                X = dev["X"][:nt]
+                Y = torch.empty((nt, L.d_out), dtype=torch.float32, device="cuda")
+
+                def callf():
+                    fq.fq_frame_apply_tff(X, b.codes, b.scale, b.zero, Fo, Fi, Y=Y, ws=wsf,
+                                          stream=stream, bits=4)
+
+                us = _time_calls(torch, callf, stream, iters)
+                frows.append({"tokens": nt, "us_per_call": round(us, 2),
+                              "tokens_per_s": round(nt / (us / 1e6), 1)})
+                print(f"[bench] W4 structured inference (float activations) {nt} token(s): "
+                      f"{us:.1f} us/call", file=sys.stderr, flush=True)
+            out["w4_inference"] = {"op": "fq_frame_apply_tff, bits 4, on the 4-bit pass's codes",
+                                   "per_tokens": frows}
         del b
     return out
 

@@ -245,6 +245,19 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
                              const float* zero, const fq_tff* frame_out,
                              const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes);
 size_t fq_frame_apply_tff_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
+/* fq_frame_apply and fq_frame_apply_tff for codes of `bits` bits (2 or 4, packed as
+ * fq_quantize_frames packs them: codes K_out x ceil(K_in / (32 / bits)) words; the
+ * appendix on segmentation and detection models quantizes at 4 bits); the 2-bit calls
+ * are these with bits = 2.  Same workspaces.  Other widths: FQ_ERR_UNSUPPORTED. */
+fq_status fq_frame_apply_nbit(void* stream, const void* X, int xt, int64_t n_tokens, int64_t ldx,
+                              int64_t d_in, const uint32_t* codes, int bits, const float* scale,
+                              const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
+                              int64_t d_out, const float* P_in, float* Y, void* ws,
+                              size_t ws_bytes);
+fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n_tokens,
+                                  int64_t ldx, const uint32_t* codes, int bits, const float* scale,
+                                  const float* zero, const fq_tff* frame_out,
+                                  const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes);
 
 /*
  * The dense frame P (d x k rho, fp32, row stride ldp >= k rho) generated on the device from

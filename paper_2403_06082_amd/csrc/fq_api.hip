@@ -605,6 +605,16 @@ fq_status fq_frame_apply(void* stream, const void* X, int xt, int64_t n_tokens, 
                          const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
                          int64_t d_out, const float* P_in, float* Y, void* ws,
                          size_t ws_bytes) {
+  return fq_frame_apply_nbit(stream, X, xt, n_tokens, ldx, d_in, codes, 2, scale, zero, K_out,
+                             K_in, P_out, d_out, P_in, Y, ws, ws_bytes);
+}
+
+fq_status fq_frame_apply_nbit(void* stream, const void* X, int xt, int64_t n_tokens, int64_t ldx,
+                              int64_t d_in, const uint32_t* codes, int bits, const float* scale,
+                              const float* zero, int64_t K_out, int64_t K_in, const float* P_out,
+                              int64_t d_out, const float* P_in, float* Y, void* ws,
+                              size_t ws_bytes) {
+  if (bits != 2 && bits != 4) return fail(FQ_ERR_UNSUPPORTED, "the float inference kernels take 2- or 4-bit codes");
   if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
   if (!dim_ok(n_tokens) || !dim_ok(d_in) || !dim_ok(K_out) || !dim_ok(K_in) || !dim_ok(d_out))
     return fail(FQ_ERR_INVALID_ARG, "dimensions must be in [0, 2^30)");
@@ -626,8 +636,8 @@ fq_status fq_frame_apply(void* stream, const void* X, int xt, int64_t n_tokens, 
   float* base = (float*)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
   ApplyScratch w;
   apply_scratch_floats(d_in, K_out, K_in, &w, base);
-  if ((e = frame_apply(X, xt, n_tokens, ldx, d_in, codes, scale, zero, K_out, K_in, P_out, d_out,
-                       P_in, Y, w, s)) != hipSuccess)
+  if ((e = frame_apply(X, xt, n_tokens, ldx, d_in, codes, bits, scale, zero, K_out, K_in, P_out,
+                       d_out, P_in, Y, w, s)) != hipSuccess)
     return hip_fail(e, "frame apply");
   return FQ_OK;
 }
@@ -828,6 +838,15 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
                              int64_t ldx, const uint32_t* codes, const float* scale,
                              const float* zero, const fq_tff* frame_out,
                              const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes) {
+  return fq_frame_apply_tff_nbit(stream, X, xt, n_tokens, ldx, codes, 2, scale, zero, frame_out,
+                                 frame_in, Y, ws, ws_bytes);
+}
+
+fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n_tokens,
+                                  int64_t ldx, const uint32_t* codes, int bits, const float* scale,
+                                  const float* zero, const fq_tff* frame_out,
+                                  const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes) {
+  if (bits != 2 && bits != 4) return fail(FQ_ERR_UNSUPPORTED, "the float inference kernels take 2- or 4-bit codes");
   if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
   if (!dim_ok(n_tokens)) return fail(FQ_ERR_INVALID_ARG, "n_tokens must be in [0, 2^30)");
   TffDev Fo, Fi;
@@ -853,7 +872,8 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
     if ((e = tff_analysis((const char*)X + t0 * ldx * esz, xt, ldx, nt, Fi, L.y, L.U, ldu, s)) !=
         hipSuccess)
       return hip_fail(e, "tff analysis");
-    if ((e = apply_codes(L.U, ldu, nt, codes, K_out, (K_in + 15) / 16, scale, zero, L.V, s)) != hipSuccess)
+    const int64_t nwords = bits == 2 ? (K_in + 15) / 16 : (K_in + 7) / 8;
+    if ((e = apply_codes(L.U, ldu, nt, codes, K_out, nwords, scale, zero, L.V, s, bits)) != hipSuccess)
       return hip_fail(e, "apply codes");
     if ((e = tff_synthesis(L.V, K_out, nt, Fo, L.r2t, L.z, Y + t0 * Fo.d, Fo.d, s)) != hipSuccess)
       return hip_fail(e, "tff synthesis");

@@ -89,9 +89,10 @@ size_t apply_scratch_floats(int64_t d_in, int64_t K_out, int64_t K_in, ApplyScra
 // X: n x d_in (row stride ldx, element type xt: 0 f32, 1 f16, 2 bf16); Y: n x d_out fp32
 // V (rows [0, tokens-per-block) with tokens-per-block = 1, 2, 4 or 8 >= nt) = scale *
 // (U (codes - zero)^T) for U with ldu = 16 * ceil(K_in / 16) columns, zero beyond K_in.
+// bits: 2 or 4 (nwords = ceil(K_in / 16) or ceil(K_in / 8) per code row)
 hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* codes,
                        int64_t K_out, int64_t nwords, const float* scale, const float* zero,
-                       float* V, hipStream_t s);
+                       float* V, hipStream_t s, int bits = 2);
 // ---------------------------------------------------------------- structured frames
 // A validated tight fusion frame given by its construction (see tff_apply.hip):
 // m = d / rho, R1 d1 x d1 and R2 d2 x d2 device fp32, d1 d2 = d.
@@ -164,7 +165,7 @@ hipError_t apply_codes_i8(const int8_t* Cq, int64_t ldc, const float* delta, con
                           int nt, int bits, const uint32_t* codes, int64_t K_out, int64_t nwords,
                           const float* scale, const float* zero, float* V, hipStream_t s);
 hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_in,
-                       const uint32_t* codes, const float* scale, const float* zero,
+                       const uint32_t* codes, int bits, const float* scale, const float* zero,
                        int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,
                        const float* P_in, float* Y, const ApplyScratch& w, hipStream_t s);
 

@@ -115,8 +115,11 @@ __global__ __launch_bounds__(AT) void k_apply_in_reduce(const float* __restrict_
 // into bytes, (word >> 2b) & 0x03030303 holding the codes of columns b, b+4, b+8, b+12,
 // and each byte converts to float in one instruction.  In LDS, group g (4 columns) of
 // word w sits at group (g + w/2) mod 4 of the word's 16 columns, so that 8 lanes reading
-// the same group of consecutive words cover all banks.
-template <int NT>
+// the same group of consecutive words cover all banks.  BITS = 4: 8 codes per word,
+// (word >> 4b) & 0x0F0F0F0F holds the codes of columns 2g + b (byte g), U sits in LDS in
+// column order (a word's 8 columns are 32 bytes, so 8 lanes on consecutive words cover
+// all banks without the rotation).
+template <int NT, int BITS>
 __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U, int64_t ldu,
                                                     const uint32_t* codes,   // not restrict: its loads must stay before the barriers
                                                     int64_t K_out, int64_t nwords,
@@ -126,7 +129,8 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
   // columns per chunk (at most 32 KB of LDS; 2048 for up to 4 tokens keeps the code words
   // of two chunks in registers)
   constexpr int UCH = NT <= 4 ? 2048 : 8192 / NT;
-  constexpr int WPL = UCH / (16 * 64);       // code words per lane and row in a chunk
+  constexpr int CPW = BITS == 2 ? 16 : 8;    // codes per word
+  constexpr int WPL = UCH / (CPW * 64);      // code words per lane and row in a chunk
   constexpr int SPT = UCH / (4 * AT);        // staging rounds per token
   __shared__ __attribute__((aligned(16))) float us[NT][UCH];
   __shared__ float usum_w[AT / 64][NT];
@@ -142,20 +146,23 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
   const uint32_t* crow[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) crow[r] = codes + min(row0 + r, K_out - 1) * nwords;
-  // code words of a chunk: 4 rows x WPL words per lane (clamped loads, unconditional)
+  // code words of a chunk: 4 rows x WPL words per lane (clamped loads, unconditional; with
+  // 4-bit codes the padded U row can reach one word past a code row, whose columns carry
+  // U = 0, so the index is clamped into the row)
   auto load_words = [&](uint32_t (&dst)[4][WPL], int64_t c0) {
-    const int nw = (int)(min((int64_t)UCH, ldu - c0) / 16);
+    const int nw = (int)(min((int64_t)UCH, ldu - c0) / CPW);
 #pragma unroll
     for (int k = 0; k < WPL; ++k) {
       const int w = lane + 64 * k;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) dst[r][k] = crow[r][c0 / 16 + min(w, nw - 1)];
+      for (int r = 0; r < 4; ++r)
+        dst[r][k] = crow[r][min(c0 / CPW + min(w, nw - 1), nwords - 1)];
     }
   };
   uint32_t wd[4][WPL], wn[4][WPL] = {};
   for (int64_t c0 = 0; c0 < ldu; c0 += UCH) {
     const int cn = (int)min((int64_t)UCH, ldu - c0);        // multiple of 16
-    const int nw = cn / 16;
+    const int nw = cn / CPW;
     lds_barrier();                          // the previous chunk's reads of us are done
     float4 uv[NT][SPT];
 #pragma unroll
@@ -180,8 +187,12 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
                                      __uint_as_float(__float_as_uint(u4.z) & keep),
                                      __uint_as_float(__float_as_uint(u4.w) & keep));
         tsum[t] += (v.x + v.y) + (v.z + v.w);
-        const int w = c >> 4, g = (c >> 2) & 3;
-        *reinterpret_cast<float4*>(&us[t][16 * w + 4 * ((g + (w >> 1)) & 3)]) = v;
+        if constexpr (BITS == 2) {
+          const int w = c >> 4, g = (c >> 2) & 3;
+          *reinterpret_cast<float4*>(&us[t][16 * w + 4 * ((g + (w >> 1)) & 3)]) = v;
+        } else {
+          *reinterpret_cast<float4*>(&us[t][c]) = v;
+        }
       }
     lds_barrier();
     if (c0 + UCH < ldu) load_words(wn, c0 + UCH);   // in flight during this chunk's work
@@ -189,6 +200,37 @@ __global__ __launch_bounds__(AT) void k_apply_codes(const float* __restrict__ U,
     for (int k = 0; k < WPL; ++k) {
       const int w = lane + 64 * k;
       if (w >= nw) break;
+      if constexpr (BITS == 4) {
+        uint32_t y[4][2];                     // byte g of y[r][b]: code of column 2g + b
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            y[r][b] = (wd[r][k] >> (4 * b)) & 0x0F0F0F0Fu;
+            asm volatile("" : "+v"(y[r][b]));
+          }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {          // columns 4h .. 4h + 3 of the word: bytes 2h, 2h + 1
+          float q[4][4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+              q[r][x] = (float)((y[r][x & 1] >> (8 * (2 * h + (x >> 1)))) & 0xffu);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            const float4 v = *reinterpret_cast<const float4*>(&us[t][8 * w + 4 * h]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              acc[r][t] = fmaf(v.x, q[r][0], acc[r][t]);
+              acc[r][t] = fmaf(v.y, q[r][1], acc[r][t]);
+              acc[r][t] = fmaf(v.z, q[r][2], acc[r][t]);
+              acc[r][t] = fmaf(v.w, q[r][3], acc[r][t]);
+            }
+          }
+        }
+        continue;
+      }
       uint32_t y[4][4];                       // byte g of y[r][b]: code of column 4g + b
 #pragma unroll
       for (int r = 0; r < 4; ++r)
@@ -511,7 +553,7 @@ int apply_ksplit(int64_t d_in) {
 
 template <int NT>
 hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
-                       const uint32_t* codes, const float* scale, const float* zero,
+                       const uint32_t* codes, int bits, const float* scale, const float* zero,
                        int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,
                        const float* P_in, float* Y, const ApplyScratch& w, hipStream_t s) {
   const int ks = apply_ksplit(d_in);
@@ -534,7 +576,8 @@ hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
   hipLaunchKernelGGL(k_apply_in_reduce, dim3((unsigned)(ldu / 64 + (ldu % 64 != 0)), NT), dim3(AT), 0, s,
                      w.part, NT, nt, ks_eff, K_in, ldu, w.U);
   prof_end(s);
-  if (hipError_t e = apply_codes(w.U, ldu, nt, codes, K_out, (K_in + 15) / 16, scale, zero, w.V, s); e != hipSuccess)
+  const int cpw = bits == 2 ? 16 : 8;
+  if (hipError_t e = apply_codes(w.U, ldu, nt, codes, K_out, (K_in + cpw - 1) / cpw, scale, zero, w.V, s, bits); e != hipSuccess)
     return e;
   prof_begin(s, "apply_out");
   constexpr int R = NT >= 4 ? 8 : 4;
@@ -551,15 +594,19 @@ hipError_t apply_block(const void* X, int xt, int64_t ldx, int nt, int64_t d_in,
 
 hipError_t apply_codes(const float* U, int64_t ldu, int nt, const uint32_t* codes,
                        int64_t K_out, int64_t nwords, const float* scale, const float* zero,
-                       float* V, hipStream_t s) {
+                       float* V, hipStream_t s, int bits) {
+  if (bits != 2 && bits != 4) return hipErrorInvalidValue;
   const dim3 g((unsigned)((K_out + 15) / 16));
   prof_begin(s, "apply_codes");
-#define FQ_CODES(N)                                                                              \
-  hipLaunchKernelGGL(k_apply_codes<N>, g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
-  if (nt == 1) { FQ_CODES(1) }
-  else if (nt == 2) { FQ_CODES(2) }
-  else if (nt <= 4) { FQ_CODES(4) }
-  else { FQ_CODES(8) }
+#define FQ_CODES(N, B)                                                                           \
+  hipLaunchKernelGGL((k_apply_codes<N, B>), g, dim3(AT), 0, s, U, ldu, codes, K_out, nwords, scale, zero, V);
+#define FQ_CODES_NT(B)                                                                           \
+  if (nt == 1) { FQ_CODES(1, B) }                                                                \
+  else if (nt == 2) { FQ_CODES(2, B) }                                                           \
+  else if (nt <= 4) { FQ_CODES(4, B) }                                                           \
+  else { FQ_CODES(8, B) }
+  if (bits == 2) { FQ_CODES_NT(2) } else { FQ_CODES_NT(4) }
+#undef FQ_CODES_NT
 #undef FQ_CODES
   prof_end(s);
   return last_launch_error();
@@ -622,7 +669,7 @@ size_t apply_scratch_floats(int64_t d_in, int64_t K_out, int64_t K_in, ApplyScra
 }
 
 hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_in,
-                       const uint32_t* codes, const float* scale, const float* zero,
+                       const uint32_t* codes, int bits, const float* scale, const float* zero,
                        int64_t K_out, int64_t K_in, const float* P_out, int64_t d_out,
                        const float* P_in, float* Y, const ApplyScratch& w, hipStream_t s) {
   const int esz = xt == 0 ? 4 : 2;
@@ -632,13 +679,13 @@ hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_
     float* Yb = Y + t0 * d_out;
     hipError_t e;
     if (nt == 1)
-      e = apply_block<1>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+      e = apply_block<1>(Xb, xt, ldx, nt, d_in, codes, bits, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
     else if (nt == 2)
-      e = apply_block<2>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+      e = apply_block<2>(Xb, xt, ldx, nt, d_in, codes, bits, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
     else if (nt <= 4)
-      e = apply_block<4>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+      e = apply_block<4>(Xb, xt, ldx, nt, d_in, codes, bits, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
     else
-      e = apply_block<8>(Xb, xt, ldx, nt, d_in, codes, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
+      e = apply_block<8>(Xb, xt, ldx, nt, d_in, codes, bits, scale, zero, K_out, K_in, P_out, d_out, P_in, Yb, w, s);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

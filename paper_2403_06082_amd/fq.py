@@ -71,6 +71,10 @@ SIGNATURES = {
     "fq_frame_synthesis_tff": (_i, [_vp, _vp, _i, _vp, _vp, _tp, _tp, _vp, _vp, _sz]),
     "fq_frame_synthesis_tff_workspace_bytes": (_sz, [_tp, _tp]),
     "fq_tff_rotation_factors": (_i, [_vp, ctypes.c_uint64, _i64, _i64, _vp, _vp, _vp, _sz]),
+    "fq_frame_apply_nbit": (_i, [_vp, _vp, _i, _i64, _i64, _i64, _vp, _i, _vp, _vp, _i64, _i64,
+                                 _vp, _i64, _vp, _vp, _vp, _sz]),
+    "fq_frame_apply_tff_nbit": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _vp,
+                                     _vp, _sz]),
     "fq_tff_rotation_factors_workspace_bytes": (_sz, [_i64, _i64]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
@@ -290,8 +294,8 @@ def fq_frame_apply_workspace_bytes(d_in, K_out, K_in) -> int:
     return lib().fq_frame_apply_workspace_bytes(d_in, K_out, K_in)
 
 
-def fq_frame_apply(X, codes, scale, zero, P_out, P_in, Y=None, ws=None, stream=None):
-    """Y = X Theta^T from the codes and the frames (small token counts)."""
+def fq_frame_apply(X, codes, scale, zero, P_out, P_in, Y=None, ws=None, stream=None, bits=2):
+    """Y = X Theta^T from the codes (2 or 4 bits) and the frames (small token counts)."""
     torch = _torch()
     if X.dim() != 2 or X.stride(1) != 1:
         raise ValueError("X must be 2-D with unit column stride")
@@ -302,7 +306,7 @@ def fq_frame_apply(X, codes, scale, zero, P_out, P_in, Y=None, ws=None, stream=N
     d_out = P_out.shape[0]
     if P_in.shape[0] != d_in:
         raise ValueError("P_in must have d_in rows")
-    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
     _dev(scale, "scale", torch.float32, (K_out,))
     _dev(zero, "zero", torch.float32, (K_out,))
     _dev(P_out, "P_out", torch.float32)
@@ -311,9 +315,9 @@ def fq_frame_apply(X, codes, scale, zero, P_out, P_in, Y=None, ws=None, stream=N
         Y = torch.empty((n, d_out), dtype=torch.float32, device=X.device)
     _dev(Y, "Y", torch.float32, (n, d_out))
     ws, wp, wb = _ws(fq_frame_apply_workspace_bytes(d_in, K_out, K_in), ws, X.device)
-    _check(lib().fq_frame_apply(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), d_in,
-                                _ptr(codes), _ptr(scale), _ptr(zero), K_out, K_in, _ptr(P_out),
-                                d_out, _ptr(P_in), _ptr(Y), wp, wb))
+    _check(lib().fq_frame_apply_nbit(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), d_in,
+                                     _ptr(codes), bits, _ptr(scale), _ptr(zero), K_out, K_in,
+                                     _ptr(P_out), d_out, _ptr(P_in), _ptr(Y), wp, wb))
     return Y
 
 
@@ -385,8 +389,8 @@ def fq_tff_synthesis(V, frame: Frame, Y=None, ws=None, stream=None):
 
 
 def fq_frame_apply_tff(X, codes, scale, zero, frame_out: Frame, frame_in: Frame, Y=None, ws=None,
-                       stream=None):
-    """Y = X Theta^T from the codes, both frames given by their construction."""
+                       stream=None, bits=2):
+    """Y = X Theta^T from the codes (2 or 4 bits), both frames given by their construction."""
     torch = _torch()
     if X.dim() != 2 or X.stride(1) != 1 or not X.is_cuda:
         raise ValueError("X must be a 2-D device tensor with unit column stride")
@@ -394,16 +398,17 @@ def fq_frame_apply_tff(X, codes, scale, zero, frame_out: Frame, frame_in: Frame,
     if d_in != frame_in.d:
         raise ValueError("X must have frame_in.d columns")
     K_out, K_in = frame_out.K, frame_in.K
-    _dev(codes, "codes", torch.int32, (K_out, (K_in + 15) // 16))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
     _dev(scale, "scale", torch.float32, (K_out,))
     _dev(zero, "zero", torch.float32, (K_out,))
     if Y is None:
         Y = torch.empty((n, frame_out.d), dtype=torch.float32, device=X.device)
     _dev(Y, "Y", torch.float32, (n, frame_out.d))
     ws, wp, wb = _ws(fq_frame_apply_tff_workspace_bytes(frame_out, frame_in), ws, X.device)
-    _check(lib().fq_frame_apply_tff(_stream(stream), _ptr(X), _dt(X), n, X.stride(0), _ptr(codes),
-                                    _ptr(scale), _ptr(zero), ctypes.byref(frame_out.c),
-                                    ctypes.byref(frame_in.c), _ptr(Y), wp, wb))
+    _check(lib().fq_frame_apply_tff_nbit(_stream(stream), _ptr(X), _dt(X), n, X.stride(0),
+                                         _ptr(codes), bits, _ptr(scale), _ptr(zero),
+                                         ctypes.byref(frame_out.c), ctypes.byref(frame_in.c),
+                                         _ptr(Y), wp, wb))
     return Y
 
 
