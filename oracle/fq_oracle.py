@@ -229,13 +229,25 @@ def gptq_tail_pre_rounding(Dc, dq, Ht, first: int, damp: float = 0.01):
     D[:, dead] = 0.0
     n = H.shape[0]
     p = n - first
-    A = H[::-1, ::-1]                                   # J H~ J
-    L11 = np.linalg.cholesky(A[:p, :p])
-    L21 = sla.solve_triangular(L11, A[p:, :p].T, lower=True).T
-    Lp = np.vstack([L11, L21])                          # leading p columns of L
-    Mt = Lp[::-1, ::-1]                                 # columns first..n-1 of M
-    E = (D - np.asarray(dq, dtype=np.float64)) @ Mt     # E_j for j >= first
-    diag = Mt[first + np.arange(p), np.arange(p)]
+    A = np.ascontiguousarray(H[::-1, ::-1])             # J H~ J
+    del H
+    # LAPACK's Cholesky on the leading block (symmetric, so its transpose is the same
+    # matrix in column-major order and is factored in place; the upper triangle of the
+    # result is not part of the factor)
+    L11, info = sla.lapack.dpotrf(A[:p, :p].T, lower=1, clean=1, overwrite_a=1)
+    if info != 0:
+        raise np.linalg.LinAlgError("damped H~ is not positive definite")
+    if p < n:
+        L21 = sla.solve_triangular(L11, A[p:, :p].T, lower=True).T
+        Lp = np.vstack([L11, L21])                      # leading p columns of L
+    else:
+        Lp = L11
+    del A
+    # columns first..n-1 of M are Mt = Lp[::-1, ::-1], so E = X Mt with X = D - DQ is
+    # (X[:, ::-1] Lp)[:, ::-1]: the product reads Lp in its stored order
+    X = D - np.asarray(dq, dtype=np.float64)
+    E = (np.ascontiguousarray(X[:, ::-1]) @ Lp)[:, ::-1]   # E_j for j >= first
+    diag = Lp[n - 1 - first - np.arange(p), p - 1 - np.arange(p)]
     return np.asarray(dq, dtype=np.float64)[:, first:] + E / diag[None, :]
 
 
@@ -249,6 +261,29 @@ def proxy_loss(D, Dhat, H):
     """L(D^) = tr((D - D^) H (D - D^)^T) (Sec. 3, proxy loss in FF space)."""
     R = np.asarray(D, dtype=np.float64) - np.asarray(Dhat, dtype=np.float64)
     return float(np.einsum("ij,jk,ik->", R, H, R))
+
+
+# --------------------------------------------------------------------------- filter
+def wiener_row_gains(D, Dhat, Ht):
+    """Diagonal approximation of the Wiener (linear MMSE) filter at synthesis (appendix
+    "LMMSE estimation from fusion frame measurements"; Sec. 3 "Robustness of Fusion
+    Frames" (b)).  The layer output is Z = P_l D C (C = P_prev^T A_prev, H~ = C C^T); the
+    filter replaces the synthesis P_l D^ C by F D^ C.  Reading: F = P_l diag(g), one gain
+    per frame-coefficient row, each minimising the row's share of the output error on the
+    calibration set, ||(D_i - g_i D^_i) C||^2, i.e.
+        g_i = (D H~ D^^T)_ii / (D^ H~ D^^T)_ii,
+    with D the unclipped analysis output (the only D with P_l D C = Theta A_prev).  A
+    row with (D^ H~ D^^T)_ii = 0 keeps g_i = 1.  The gains fold into the stored per-row
+    scale (scale_i g_i), so synthesis and inference are unchanged."""
+    D = np.asarray(D, dtype=np.float64)
+    Dh = np.asarray(Dhat, dtype=np.float64)
+    M = Dh @ np.asarray(Ht, dtype=np.float64)            # D^ H~
+    num = np.einsum("ij,ij->i", D, M)
+    den = np.einsum("ij,ij->i", Dh, M)
+    g = np.ones(D.shape[0])
+    ok = den != 0
+    g[ok] = num[ok] / den[ok]
+    return g
 
 
 # --------------------------------------------------------------------------- stage 3e

@@ -114,6 +114,32 @@ def test_U_is_cholesky_of_inverse_and_ul_identity():
     np.testing.assert_allclose(J @ np.linalg.inv(M) @ J, U, rtol=1e-9, atol=1e-12)
 
 
+def test_damped_hessian_hand_cases():
+    """OPTQ's conditioning, by hand: the dead fix first (a zero diagonal entry becomes 1),
+    then damp times the mean of that fixed diagonal on every diagonal entry; off-diagonal
+    entries are untouched.  The cases tell the mean from the trace or the maximum, and
+    the mean after the dead fix from the mean before it."""
+    Hd, dead = O.damped_hessian(np.diag([0.0, 2.0, 4.0]), 0.01)
+    lam = 0.01 * 7.0 / 3.0                       # mean of diag(1, 2, 4)
+    np.testing.assert_array_equal(dead, [True, False, False])
+    np.testing.assert_allclose(Hd, np.diag([1.0 + lam, 2.0 + lam, 4.0 + lam]), rtol=0, atol=1e-15)
+    Ht = np.array([[4.0, 1.0, 0.0], [1.0, 2.0, 0.0], [0.0, 0.0, 0.0]])
+    Hd, dead = O.damped_hessian(Ht, 0.1)
+    lam = 0.1 * (4.0 + 2.0 + 1.0) / 3.0
+    np.testing.assert_array_equal(dead, [False, False, True])
+    np.testing.assert_allclose(Hd, [[4.0 + lam, 1.0, 0.0], [1.0, 2.0 + lam, 0.0],
+                                    [0.0, 0.0, 1.0 + lam]], rtol=0, atol=1e-15)
+    # no dead column: damp * trace / n
+    Hd, dead = O.damped_hessian(np.array([[2.0, -1.0], [-1.0, 6.0]]), 0.5)
+    assert not dead.any()
+    np.testing.assert_allclose(Hd, [[4.0, -1.0], [-1.0, 8.0]], rtol=0, atol=1e-15)
+    # the input is not modified, and gptq_prepare factors exactly this matrix
+    Ht0 = Ht.copy()
+    U, dead, Hd = O.gptq_prepare(Ht, 0.1)
+    np.testing.assert_array_equal(Ht, Ht0)
+    np.testing.assert_allclose(np.linalg.inv(U.T @ U), Hd, rtol=1e-12, atol=1e-12)
+
+
 def test_identity_hessian_is_rtn():
     rng = _rng(5)
     D = rng.standard_normal((5, 12))
@@ -416,6 +442,99 @@ def test_tail_pre_rounding_matches_replay():
         bad[:, 3] = (bad[:, 3] + 1) % 4
         w_bad = O.gptq_tail_pre_rounding(Dc, O.dequant(bad, s, z), Ht, 9)
         assert np.abs(w_bad / s[:, None] - r["t"][:, 9:]).max() > 1e-3
+
+
+def test_tail_pre_rounding_matches_literal_optq_at_scale():
+    """The same consistency property against the literal OPTQ (U = chol(H~^-1), lazy
+    blocks of 128) at a frame-shaped size: K_in = 1120 = 70 subspaces of 16 over d = 1024,
+    H~ = P^T (X^T X) P singular (rank 1024) before damping, condition about 4e4 after it,
+    outlier channels in X, clipped D.  From column 0 (every column of the row), from the
+    middle and for the last column, the pre-rounding values agree to 1e-9 code units and
+    every code is the nearest grid point of its value."""
+    rng = _rng(31)
+    d, rho, k = 1024, 16, 70
+    P = tff.parseval_frame(k, rho, d, np.random.SeedSequence(5))
+    X = rng.standard_normal((2048, d))
+    X[:, [3, 500, 901]] *= 50.0
+    W = rng.standard_normal((6, d)) * 0.02
+    D, Ht = O.frame_analysis(W, np.eye(6), P, O.hessian(X))
+    assert np.linalg.matrix_rank(Ht) < Ht.shape[0]
+    mu, sigma, lo, hi = O.clip_bounds(D, 2.0)
+    Dc = O.apply_clip(D, lo, hi)
+    s, z = O.row_grid(Dc)
+    U, dead, _ = O.gptq_prepare(Ht, 0.01)
+    r = O.gptq(Dc, U, s, z, 2, 128, dead)
+    dq = O.dequant(r["codes"], s, z)
+    for first in (0, 517, Ht.shape[0] - 1):
+        w = O.gptq_tail_pre_rounding(Dc, dq, Ht, first)
+        np.testing.assert_allclose(w / s[:, None], r["t"][:, first:], rtol=0, atol=1e-9)
+        q, _ = O.rtn_codes(w, s[:, None], z[:, None])
+        np.testing.assert_array_equal(q, r["codes"][:, first:])
+    bad = r["codes"].copy()
+    bad[:, 40] = (bad[:, 40] + 2) % 4
+    w_bad = O.gptq_tail_pre_rounding(Dc, O.dequant(bad, s, z), Ht, 0)
+    assert np.abs(w_bad / s[:, None] - r["t"]).max() > 1e-2
+
+
+# ----------------------------------------------------------------------------- filter
+def test_wiener_gains_closed_forms():
+    """g = 1 when nothing is quantized; g = 1/c when D^ = c D; a zero row keeps g = 1."""
+    rng = _rng(40)
+    X = rng.standard_normal((50, 12))
+    Ht = O.hessian(X)
+    D = rng.standard_normal((5, 12))
+    np.testing.assert_allclose(O.wiener_row_gains(D, D, Ht), 1.0, rtol=1e-13)
+    c = np.array([0.5, 2.0, -3.0, 1.0, 7.0])
+    np.testing.assert_allclose(O.wiener_row_gains(D, c[:, None] * D, Ht), 1.0 / c, rtol=1e-12)
+    Dh = D.copy()
+    Dh[2] = 0.0
+    assert O.wiener_row_gains(D, Dh, Ht)[2] == 1.0
+
+
+def test_wiener_gains_minimise_row_output_error_brute_force():
+    """Each g_i minimises ||(D_i - g D^_i) C||^2 computed from C itself (not from H~):
+    a fine scan around g_i and random trial gains never do better, and the minimum value
+    matches the closed form ||D_i C||^2 - (D_i C . D^_i C)^2 / ||D^_i C||^2."""
+    rng = _rng(41)
+    C = rng.standard_normal((10, 40))                 # K_in x tokens
+    C[3] *= 20.0
+    Ht = C @ C.T
+    D = rng.standard_normal((4, 10))
+    Dh = np.round(D * 2.0) / 2.0                      # a coarse quantization of D
+    g = O.wiener_row_gains(D, Dh, Ht)
+    for i in range(4):
+        f = lambda gg: float(np.sum(((D[i] - gg * Dh[i]) @ C) ** 2))
+        best = f(g[i])
+        for gg in np.concatenate([g[i] + np.linspace(-0.05, 0.05, 201), rng.uniform(-2, 3, 50)]):
+            assert f(gg) >= best * (1 - 1e-12)
+        a, b = D[i] @ C, Dh[i] @ C
+        assert best == pytest.approx(a @ a - (a @ b) ** 2 / (b @ b), rel=1e-9)
+
+
+def test_wiener_filtered_layer_loss():
+    """On a quantized layer the filtered proxy loss never exceeds the unfiltered one, the
+    layer-output error stays below the filtered proxy loss (P_l P_l^T = I), and at r_out
+    = 1 (P_l orthogonal) the two are equal, so the filter lowers the output error itself."""
+    rng = _rng(42)
+    for k_out in (9, 8):                              # r_out = 36/32 and 1
+        P_out, P_in = _frames(32, 24, k_out, 7)
+        W = rng.standard_normal((32, 24)) * 0.02
+        X = rng.standard_normal((300, 24))
+        X[:, 5] *= 20.0
+        r = O.quantize_layer(W, X, P_out, P_in, bits=2, block=8)
+        Dh = O.dequant(r["codes"], r["scale"], r["zero"])
+        g = O.wiener_row_gains(r["D"], Dh, r["Ht"])
+        C = P_in.T @ X.T
+        base = np.sum(((r["D"] - Dh) @ C) ** 2)
+        filt = np.sum(((r["D"] - g[:, None] * Dh) @ C) ** 2)
+        assert filt <= base
+        Wg = O.synthesis(r["codes"], r["scale"] * g, r["zero"], P_out, P_in)
+        out = np.sum(((W - Wg) @ X.T) ** 2)
+        assert out <= filt * (1 + 1e-10)
+        if k_out == 8:
+            assert out == pytest.approx(filt, rel=1e-9)
+            out0 = np.sum(((W - r["W_hat"]) @ X.T) ** 2)
+            assert out < out0
 
 
 # ---------------------------------------------------------------- seeded rotation factors
