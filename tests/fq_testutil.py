@@ -63,14 +63,23 @@ def replay_rows(D_gpu: np.ndarray, Ht_gpu: np.ndarray, codes_gpu: np.ndarray, ro
     return r
 
 
-def check_codes(r, codes_gpu, scale_gpu, zero_gpu):
+def check_codes(r, codes_gpu, scale_gpu, zero_gpu, words=None):
     """Codes bit-exact outside the near-tie window; scale/zero equal to the oracle's.
     The device arrays hold every row, or only the replayed rows when the replay was made
-    with codes_are_rows."""
+    with codes_are_rows.  words: the device's packed 2-bit words (same rows as codes_gpu),
+    then compared bit for bit, pad bits included, with the oracle's packing of the
+    replayed codes."""
     sel = slice(None) if r.get("codes_are_rows") else r["rows"]
     cg = codes_gpu[sel]
     mism = (r["codes"] != cg) & ~r["tie"]
     np.testing.assert_allclose(scale_gpu[sel], r["scale"], rtol=2e-7, atol=0)
     np.testing.assert_array_equal(zero_gpu[sel], r["zero"])
     assert int(mism.sum()) == 0, f"{int(mism.sum())} code mismatches outside near ties"
+    if words is not None:
+        np.testing.assert_array_equal(np.asarray(words).view(np.uint32)[sel], O.pack2(r["codes"]))
     return int(r["tie"].sum())
+
+
+def words_of(codes_t) -> np.ndarray:
+    """The device's packed code words as uint32."""
+    return codes_t.cpu().numpy().view(np.uint32)

@@ -8,10 +8,13 @@ outputs the oracle can compute one by one:
   H~     : in full, P_in^T H P_in from the device's H (stage isolation); for the
            Llama-70B-shaped layer the principal submatrix on 64 random frame columns;
   codes  : teacher-forced replay of 48 random rows on the device's D and H~; for the
-           Llama-70B-shaped layer (K_in 28672 / 31536, beyond a host factorization in a
-           test) scale / zero of 128 random rows exactly, and the rounding property of the
-           last four 128-column blocks: each code is the grid point nearest to its
-           pre-rounding value given the device's earlier codes (exact outside near ties);
+           Llama-70B-shaped layer (K_in 28672 / 31536, where the literal OPTQ's inverse
+           factor is too slow for a test) scale / zero of 128 random rows exactly, and
+           the rounding property over every column of those rows: each code is the grid
+           point nearest to its pre-rounding value given the device's earlier codes
+           (exact outside near ties), with the pre-rounding values from one host
+           Cholesky factorization of the damped H~; either way the device's packed words
+           of those rows equal the packing of the replayed codes bit for bit;
   W_hat  : 16 random rows, P_out[i, :] D^ P_in^T from the device's codes;
   Y      : those output channels of X W_hat^T on 512 random tokens.
 Tolerances are those of the small-shape tests (see test_gpu_stages): 1e-5 relative
@@ -116,17 +119,22 @@ def fullsize_layer(key, li, n_code_rows=48, replay=True, frames="structured"):
     # stage 3: codes of sampled rows
     rows_q = np.sort(rng.choice(K_out, n_code_rows, replace=False))
     rq = torch.from_numpy(rows_q).cuda()
-    cg_rows = unpack_codes(bufs.codes.index_select(0, rq), K_in)
+    words_rows = bufs.codes.index_select(0, rq).cpu().numpy().view(np.uint32)
+    cg_rows = O.unpack2(words_rows, K_in)
     sg, zg = bufs.scale.cpu().numpy(), bufs.zero.cpu().numpy()
     if replay:
         r = replay_rows(Dg, Htg, cg_rows, rows=rows_q, block=wl.block, damp=wl.damp,
                         clip_sigmas=wl.clip_sigmas, codes_are_rows=True)
         ties = check_codes(r, cg_rows, sg[rows_q], zg[rows_q])
+        replayed = r["codes"]
         _log(f"codes ok on {n_code_rows} rows ({ties} near ties)")
     else:
-        ties = _check_code_tail(wl, Dg, Htg, rows_q, cg_rows, sg[rows_q], zg[rows_q], 4 * wl.block)
-        _log(f"scale/zero and last {4 * wl.block} columns ok on {n_code_rows} rows "
-             f"({ties} near ties)")
+        t = time.time()
+        ties, replayed = _check_codes_all_columns(wl, Dg, Htg, rows_q, cg_rows, sg[rows_q],
+                                                  zg[rows_q])
+        _log(f"scale/zero and all {K_in} columns ok on {n_code_rows} rows ({ties} near ties; "
+             f"host check {time.time() - t:.1f}s)")
+    np.testing.assert_array_equal(words_rows, O.pack2(replayed))
     del Dg, Htg
 
     # stage 4 and layer outputs, from the device's codes
@@ -143,9 +151,12 @@ def fullsize_layer(key, li, n_code_rows=48, replay=True, frames="structured"):
     return ties
 
 
-def _check_code_tail(wl, Dg, Htg, rows, codes, scale, zero, tail):
+def _check_codes_all_columns(wl, Dg, Htg, rows, codes, scale, zero):
     """scale / zero of the given rows against the oracle's clip and grid, then the
-    rounding property on the last `tail` columns given the device's earlier codes."""
+    rounding property of every column given the device's earlier codes (Alg. 1 step 4:
+    each code is the grid point nearest to its pre-rounding value).  Equivalent to a
+    teacher-forced replay: a row passes exactly when the replay, fed the device's codes
+    at near ties, reproduces every code.  Returns (near ties, the replayed codes)."""
     D = np.asarray(Dg, dtype=np.float64)
     mu, sigma, lo_b, hi_b = O.clip_bounds(D, wl.clip_sigmas)
     Dc = O.apply_clip(D[rows], lo_b, hi_b)
@@ -154,13 +165,12 @@ def _check_code_tail(wl, Dg, Htg, rows, codes, scale, zero, tail):
     np.testing.assert_allclose(scale, s_o, rtol=2e-7, atol=0)
     np.testing.assert_array_equal(zero, z_o)
     dq = O.dequant(codes, s_o, z_o)
-    first = Dc.shape[1] - tail
-    w = O.gptq_tail_pre_rounding(Dc, dq, Htg, first, wl.damp)
+    w = O.gptq_tail_pre_rounding(Dc, dq, Htg, 0, wl.damp)
     q, t = O.rtn_codes(w, s_o[:, None], z_o[:, None], wl.bits)
     tie = O.near_tie(t)
-    mism = (q != codes[:, first:]) & ~tie
-    assert int(mism.sum()) == 0, f"{int(mism.sum())} tail codes are not the nearest grid point"
-    return int(tie.sum())
+    mism = (q != codes) & ~tie
+    assert int(mism.sum()) == 0, f"{int(mism.sum())} codes are not the nearest grid point"
+    return int(tie.sum()), np.where(tie, codes, q).astype(np.int64)
 
 
 def test_fullsize_opt1b3_fc1():

@@ -54,7 +54,7 @@ def run_workload(key, independent=True):
         cg = unpack_codes(bufs.codes, K_in)
         sg, zg = bufs.scale.cpu().numpy(), bufs.zero.cpu().numpy()
         r = replay_rows(Dg, Htg, cg, block=wl.block, damp=wl.damp, clip_sigmas=wl.clip_sigmas)
-        ties = check_codes(r, cg, sg, zg)
+        ties = check_codes(r, cg, sg, zg, words=bufs.codes.cpu().numpy())
         # stage 4 and layer outputs, from the replayed codes
         Wh_o = O.synthesis(r["codes"], r["scale"], r["zero"], Po, Pi)
         Whg = bufs.W_hat.cpu().numpy()

@@ -141,7 +141,8 @@ def _quantize(torch, fq, D, Ht, block, **kw):
     fq.fq_quantize_frames(torch.from_numpy(D).cuda(), torch.from_numpy(Ht).cuda(), codes, scale,
                           zero, block=block, **kw)
     torch.cuda.synchronize()
-    return unpack_codes(codes, K_in), scale.cpu().numpy(), zero.cpu().numpy()
+    w = codes.cpu().numpy().view(np.uint32)
+    return O.unpack2(w, K_in), scale.cpu().numpy(), zero.cpu().numpy(), w
 
 
 @pytest.mark.parametrize("K_out,d_in,k_in,block", [(70, 64, 18, 128), (300, 136, 37, 7),
@@ -157,12 +158,10 @@ def test_quantize_teacher_forced(K_out, d_in, k_in, block):
     fq = _fq()
     rng = np.random.default_rng(K_out + block)
     D, Ht = _ff_problem(rng, K_out, d_in, k_in)
-    cg, sg, zg = _quantize(torch, fq, D, Ht, block)
+    cg, sg, zg, words = _quantize(torch, fq, D, Ht, block)
     r = replay_rows(D, Ht, cg, block=block)
-    ties = check_codes(r, cg, sg, zg)
+    ties = check_codes(r, cg, sg, zg, words=words)
     assert ties <= 2
-    # the packed layout carries nothing beyond K_in
-    assert cg.shape == D.shape
 
 
 def test_quantize_odd_row_length():
@@ -176,9 +175,9 @@ def test_quantize_odd_row_length():
     Ht = (A.T @ A).astype(np.float32)
     Ht = np.triu(Ht) + np.triu(Ht, 1).T            # exactly symmetric
     D = (rng.standard_normal((260, 1101)) * 0.02 + 0.001).astype(np.float32)
-    cg, sg, zg = _quantize(torch, fq, D, Ht, 128)
+    cg, sg, zg, words = _quantize(torch, fq, D, Ht, 128)
     r = replay_rows(D, Ht, cg, block=128)
-    assert check_codes(r, cg, sg, zg) <= 2
+    assert check_codes(r, cg, sg, zg, words=words) <= 2
 
 
 def test_quantize_identity_hessian_is_rtn():
@@ -187,12 +186,14 @@ def test_quantize_identity_hessian_is_rtn():
     rng = np.random.default_rng(2)
     D = (rng.standard_normal((90, 77)) * 0.05 + 0.002).astype(np.float32)
     Ht = np.eye(77, dtype=np.float32)
-    cg, sg, zg = _quantize(torch, fq, D, Ht, 128)
+    cg, sg, zg, words = _quantize(torch, fq, D, Ht, 128)
     mu, sigma, lo, hi = O.clip_bounds(D.astype(np.float64))
     Dc = O.apply_clip(D.astype(np.float64), lo, hi)
     s, z = O.row_grid(Dc)
     q, _ = O.rtn_codes(Dc, s[:, None], z[:, None])
     np.testing.assert_array_equal(cg, q)
+    # K_in = 77: the last word of every row holds 13 codes and 3 zero pad fields
+    np.testing.assert_array_equal(words, O.pack2(q))
 
 
 def test_quantize_no_clip_and_dead_column():
@@ -202,9 +203,9 @@ def test_quantize_no_clip_and_dead_column():
     D, Ht = _ff_problem(rng, 50, 64, 18)
     Ht[5, :] = 0
     Ht[:, 5] = 0
-    cg, sg, zg = _quantize(torch, fq, D, Ht, 16, clip_sigmas=float("inf"))
+    cg, sg, zg, words = _quantize(torch, fq, D, Ht, 16, clip_sigmas=float("inf"))
     r = replay_rows(D, Ht, cg, block=16, clip_sigmas=float("inf"))
-    check_codes(r, cg, sg, zg)
+    check_codes(r, cg, sg, zg, words=words)       # K_in = 72: half-filled last words
 
 
 def test_quantize_errors():

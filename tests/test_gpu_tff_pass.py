@@ -192,7 +192,7 @@ def test_pipeline_with_structured_frames(two_streams):
     assert rel_fro(Dg, Do) < 1e-5 and rel_fro(Htg, Hto) < 1e-5
     cg = unpack_codes(b.codes, Fi.K)
     r = replay_rows(Dg, Htg, cg)
-    check_codes(r, cg, b.scale.cpu().numpy(), b.zero.cpu().numpy())
+    check_codes(r, cg, b.scale.cpu().numpy(), b.zero.cpu().numpy(), words=b.codes.cpu().numpy())
     Who = O.synthesis(cg, b.scale.cpu().numpy().astype(np.float64),
                       b.zero.cpu().numpy().astype(np.float64), Po, Pi)
     assert rel_fro(b.W_hat.cpu().numpy(), Who) < 1e-5
