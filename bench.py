@@ -39,12 +39,35 @@ METRIC = "quantized weights/sec per layer (Llama-7B-shaped 11008×4096); MFMA % 
 PEAK = {"bf16": 2500.0, "f32": 157.3, "f64": 78.6, "hbm": 8000.0}   # TFLOP/s ..., GB/s
 
 
-def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, rot=None):
-    """Algorithmic flops (bytes for the memory-bound kernels) per launch group and step.
-    With structured frames (rho, and rot = (d1_out + d2_out, d1_in + d2_in)): the per-block
-    DFT products, 4 d k flops per transformed row (k = K / rho), and the rotations,
-    2 d (d1 + d2) flops per row, over the rows each stage transforms (D: d_out rows of W,
-    then K_in columns; Ht: d_in, then K_in; W_hat: K_out code rows, then d_in columns)."""
+def _tff_geom(d, K, rho):
+    """Block geometry of a frame as the structured pass lays it out: nb = rho/2 blocks of
+    2m real coordinates padded to pm and 2k frame coordinates padded to pk (multiples of
+    32); the rotation factors d1 x d2 (d1 <= d2, d1 as close to sqrt(d) as possible)."""
+    k, m = K // rho, d // rho
+    d1 = max(a for a in range(1, int(d ** 0.5) + 1) if d % a == 0)
+    return dict(k=k, m=m, nb=rho // 2, pm=-(-2 * m // 32) * 32, pk=-(-2 * k // 32) * 32,
+                d1=d1, d2=d // d1)
+
+
+def _rot_exec(g):
+    """fp32 MFMA flops issued per vector by the two rotation steps (64 x 64 output tiles,
+    k steps of 16): X R2 with k = d2, then R1^T (.) with k = d1."""
+    p64 = lambda x: -(-x // 64) * 64
+    p16 = lambda x: -(-x // 16) * 16
+    return 2 * p64(g["d1"]) * p64(g["d2"]) * (p16(g["d2"]) + p16(g["d1"]))
+
+
+def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, w_dtype="bf16"):
+    """Work per kernel group and step: (peak kind, algorithmic amount, executed amount).
+    Contractions count flops (one pass of the useful product for 'algorithmic'; every
+    bf16 pass of a split product for 'executed'), streaming kernels bytes.
+    With structured frames (rho given) the per-block DFT products cost 4 d k flops per
+    transformed row (executed: 2 nb pm pk per row and pass, the padded block layout) and
+    the rotations 2 d (d1 + d2) flops per row (executed: the padded 64 x 64 tiles).  The
+    analysis (_an) transforms d_out rows of W, d_in rows of H and K_in rows of H P_in by
+    the input frame, then K_in rows of W P_in by the output frame; the synthesis (_syn)
+    transforms K_out code rows by the input frame (2 passes: exact codes), then d_in rows
+    by the output frame."""
     gptq_upd = 0
     for o1 in range(0, K_in, block):
         o2 = min(o1 + block, K_in)
@@ -57,50 +80,102 @@ def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, rot=None):
     span = block * -(-512 // block)
     gptq_lazy = sum(2 * K_out * (min(s1 + span, K_in) - s1) * (K_in - min(s1 + span, K_in))
                     for s1 in range(0, K_in, span))
-    chol = 0
-    for k0 in range(0, K_in, 64):
-        kb = min(64, K_in - k0)
-        rest = K_in - k0 - kb
-        chol += rest * (rest + 1) * kb          # lower-triangle rank-kb update, 2 flops/FMA
-    extra = {}
+    chol = K_in ** 3 // 3                   # the factorization: n^3 / 3 flops
+    work = {}
     if rho is not None:
-        k_out, k_in = K_out // rho, K_in // rho
-        rows_in = d_out + d_in + K_in + K_out        # rows transformed by the input frame
-        rows_out = K_in + d_in                       # rows transformed by the output frame
-        extra["tffp_dft"] = ("bf16", 4 * d_in * k_in * rows_in + 4 * d_out * k_out * rows_out)
-        extra["tffp_rotate"] = ("f32", 2 * d_in * rot[1] * rows_in + 2 * d_out * rot[0] * rows_out)
-    return {
-        **extra,
-        "gemm_hessian": ("bf16", n * d_in * (d_in + 1)),
-        "gemm_analysis_w1": ("bf16", 2 * K_out * d_out * d_in),
-        "gemm_analysis_w2": ("bf16", 2 * K_out * d_in * K_in),
-        "gemm_analysis_h1": ("bf16", 2 * d_in * d_in * K_in),
-        "gemm_analysis_h2": ("bf16", K_in * (K_in + 1) * d_in),
-        "gemm_synthesis_1": ("bf16", 2 * d_out * K_out * K_in),
-        "gemm_synthesis_2": ("bf16", 2 * d_out * K_in * d_in),
-        "gptq_update": ("f64", gptq_upd),
-        "gptq_update_lazy": ("f64", gptq_lazy),
-        "gptq_update_span": ("f64", gptq_upd - gptq_lazy),
-        "chol_syrk": ("f64", chol),
-        "gptq_block": ("f64", K_out * K_in * 128),     # in-block FMAs (upper bound)
-        "pack2": ("hbm", K_out * K_in + K_out * ((K_in + 15) // 16) * 4),
-    }
+        gi, go = _tff_geom(d_in, K_in, rho), _tff_geom(d_out, K_out, rho)
+        dft_i = lambda rows, passes: (4 * d_in * gi["k"] * rows,
+                                      passes * 2 * gi["nb"] * gi["pm"] * gi["pk"] * rows)
+        dft_o = lambda rows, passes: (4 * d_out * go["k"] * rows,
+                                      passes * 2 * go["nb"] * go["pm"] * go["pk"] * rows)
+        rot_i = lambda rows: (2 * d_in * (gi["d1"] + gi["d2"]) * rows, _rot_exec(gi) * rows)
+        rot_o = lambda rows: (2 * d_out * (go["d1"] + go["d2"]) * rows, _rot_exec(go) * rows)
+        add = lambda a, b: (a[0] + b[0], a[1] + b[1])
+        a1, a2 = dft_i(d_out + d_in + K_in, 3), dft_o(K_in, 3)
+        work["tffp_dft_an"] = ("bf16",) + add(a1, a2)
+        work["tffp_dft_syn"] = ("bf16",) + add(dft_i(K_out, 2), dft_o(d_in, 3))
+        work["tffp_rotate_an"] = ("f32",) + add(rot_i(d_out + d_in + K_in), rot_o(K_in))
+        work["tffp_rotate_syn"] = ("f32",) + add(rot_i(K_out), rot_o(d_in))
+    hess_tiles = (-(-d_in // 256)) * (-(-d_in // 256) + 1) // 2
+    passes = {"gemm_hessian": 1, "gemm_analysis_w1": 2 if w_dtype == "bf16" else 3,
+              "gemm_analysis_w2": 3, "gemm_analysis_h1": 3, "gemm_analysis_h2": 3,
+              "gemm_synthesis_1": 2, "gemm_synthesis_2": 3}
+    dense = {"gemm_hessian": n * d_in * (d_in + 1),
+             "gemm_analysis_w1": 2 * K_out * d_out * d_in,
+             "gemm_analysis_w2": 2 * K_out * d_in * K_in,
+             "gemm_analysis_h1": 2 * d_in * d_in * K_in,
+             "gemm_analysis_h2": K_in * (K_in + 1) * d_in,
+             "gemm_synthesis_1": 2 * d_out * K_out * K_in,
+             "gemm_synthesis_2": 2 * d_out * K_in * d_in}
+    for k, v in dense.items():
+        ex = passes[k] * v
+        if k == "gemm_hessian":        # upper 256 x 256 tiles of the symmetric product
+            ex = hess_tiles * 256 * 256 * 2 * n
+        work[k] = ("bf16", v, ex)
+    work.update({
+        "gptq_update": ("f64", gptq_upd, gptq_upd),
+        "gptq_update_lazy": ("f64", gptq_lazy, gptq_lazy),
+        "gptq_update_span": ("f64", gptq_upd - gptq_lazy, gptq_upd - gptq_lazy),
+        "chol": ("f64", chol, None),
+        "gptq_block": ("f64", K_out * K_in * 128, None),     # in-block FMAs (upper bound)
+        "pack2": ("hbm", K_out * K_in + K_out * ((K_in + 15) // 16) * 4, None),
+    })
+    return work
 
 
-def mfma_passes(w_dtype):
-    """bf16 MFMA passes per product: an fp32 operand is a bf16 (hi, lo) pair; a product
-    takes 3 passes (hi.hi + hi.lo + lo.hi), 2 when one side is exact in one bf16 plane
-    (bf16 weights, codes - zero), 1 for the Hessian of 16-bit calibration data."""
-    return {"gemm_hessian": 1, "gemm_analysis_w1": 2 if w_dtype == "bf16" else 3,
-            "gemm_analysis_w2": 3, "gemm_analysis_h1": 3, "gemm_analysis_h2": 3,
-            "gemm_synthesis_1": 2, "gemm_synthesis_2": 3}
-
+# contraction groups of the spec MFMA target: S1 and the frame transforms of S2
+# (analysis) and S4 (synthesis)
+CONTRACTIONS_S2 = ["gemm_analysis_w1", "gemm_analysis_w2", "gemm_analysis_h1",
+                   "gemm_analysis_h2", "tffp_dft_an", "tffp_rotate_an"]
+CONTRACTIONS_S4 = ["gemm_synthesis_1", "gemm_synthesis_2", "tffp_dft_syn", "tffp_rotate_syn"]
 
 KERNEL_GROUPS = ["gemm_hessian", "gemm_analysis_w1", "gemm_analysis_w2", "gemm_analysis_h1",
-                 "gemm_analysis_h2", "gemm_synthesis_1", "gemm_synthesis_2", "tffp_rotate",
-                 "tffp_blocks", "tffp_dft", "tffp_gather", "gptq_update",
-                 "gptq_update_lazy", "gptq_update_span", "gptq_block", "chol_syrk", "chol_potrf", "chol_trsm", "q_", "split_bf16",
-                 "syrk_reduce", "dequant", "pack2"]
+                 "gemm_analysis_h2", "gemm_synthesis_1", "gemm_synthesis_2", "tffp_rotate_an",
+                 "tffp_rotate_syn", "tffp_blocks", "tffp_dft_an", "tffp_dft_syn", "tffp_gather",
+                 "gptq_update", "gptq_update_lazy", "gptq_update_span", "gptq_block", "chol",
+                 "chol_syrk", "chol_potrf", "chol_trsm", "q_", "split_bf16", "syrk_reduce",
+                 "dequant", "pack2"]
+
+
+def kernel_table(fq, work, steps):
+    """Per kernel group: launches, ms per step and, where the work is defined, the rate
+    against its own peak (algorithmic and executed), from the library's kernel timers."""
+    kernels = {}
+    for name in KERNEL_GROUPS:
+        cnt, tot = fq.fq_profile_query(name)
+        if cnt == 0:
+            continue
+        e = {"launches_per_step": cnt / steps, "ms_per_step": round(tot / steps, 4)}
+        if name in work:
+            kind, amount, executed = work[name]
+            sec = tot / steps / 1000.0
+            if kind == "hbm":
+                e["GB/s"] = round(amount / sec / 1e9, 1)
+                e["frac_of_peak"] = round(amount / sec / 1e9 / PEAK["hbm"], 4)
+            else:
+                e["peak"] = kind
+                e["TFLOP/s"] = round(amount / sec / 1e12, 2)
+                e["frac_of_peak"] = round(amount / sec / 1e12 / PEAK[kind], 4)
+                if executed is not None and executed != amount:
+                    e["executed_TFLOP/s"] = round(executed / sec / 1e12, 2)
+                    e["executed_frac_of_peak"] = round(executed / sec / 1e12 / PEAK[kind], 4)
+        kernels[name] = e
+    return kernels
+
+
+def contraction_summary(kernels, work, groups):
+    """Combined MFMA fraction of several contraction groups, each against its own dtype's
+    peak: (sum of work / peak) / (sum of time), i.e. the time the work takes at peak rate
+    over the time it took.  Algorithmic and executed (every bf16 pass) separately."""
+    used = [g for g in groups if g in kernels and g in work]
+    t = sum(kernels[g]["ms_per_step"] for g in used) / 1e3
+    if t <= 0:
+        return None
+    alg = sum(work[g][1] / (PEAK[work[g][0]] * 1e12) for g in used)
+    exe = sum((work[g][2] if work[g][2] is not None else work[g][1]) / (PEAK[work[g][0]] * 1e12)
+              for g in used)
+    return {"groups": used, "ms_per_step": round(t * 1e3, 4), "algorithmic_frac": round(alg / t, 4),
+            "executed_frac": round(exe / t, 4)}
 
 
 def make_inputs(wl, li):
@@ -130,62 +205,70 @@ def make_inputs(wl, li):
     return dev, host
 
 
-def cpu_baseline(wl, li, host, budget_rows=1024, sample_tokens=8192):
-    """Time the oracle on a bounded sample of the same layer and extrapolate per stage:
-    H over one 8,192-token chunk (x n / 8192); D, OPTQ and W^ on `budget_rows` sampled
-    rows (x rows / budget_rows); H~ and the factor U in full."""
-    import oracle as O
-    from fq_inputs import gen
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        cores = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+        return max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
     except Exception:
-        cores = len(os.sched_getaffinity(0))
+        return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(wl, li, host, chunk=8192):
+    """The float64 oracle's whole pass on the same layer and inputs, nothing sampled or
+    extrapolated: H over every calibration token (chunks of `chunk` tokens upcast to
+    float64), D and H~ with the dense float64-exact frames, OPTQ's preparation (literal
+    U = chol(H~^-1)), clip, grid and rounding of every row, packing, and W^."""
+    import oracle as O
+    from fq_inputs import gen
     L = wl.layers[li]
-    n = wl.n_tokens
     X = host["X"]
+    n = X.shape[0]
+    t = {}
+    s0 = time.perf_counter()
+    H = O.hessian(gen.storage_to_f32(X[c:c + chunk], wl.x_dtype) for c in range(0, n, chunk))
+    t["hessian"] = time.perf_counter() - s0
     W64 = gen.storage_to_f32(host["W"], wl.w_dtype).astype(np.float64)
     Po = host["P_out"].astype(np.float64)
     Pi = host["P_in"].astype(np.float64)
-    K_out, K_in = Po.shape[1], Pi.shape[1]
-    rng = np.random.default_rng(0)
-    t = {}
     s0 = time.perf_counter()
-    Xc = gen.storage_to_f32(X[:sample_tokens], wl.x_dtype).astype(np.float64)
-    H = O.hessian(Xc) * (n / sample_tokens)
-    t["hessian"] = (time.perf_counter() - s0) * (n / sample_tokens)
-    rows = np.sort(rng.choice(K_out, size=min(budget_rows, K_out), replace=False))
+    D, _ = O.frame_analysis(W64, Po, Pi, None)
+    t["analysis_D"] = time.perf_counter() - s0
     s0 = time.perf_counter()
-    D_rows = (Po[:, rows].T @ W64) @ Pi
-    t["analysis_D"] = (time.perf_counter() - s0) * (K_out / len(rows))
-    s0 = time.perf_counter()
-    _, Ht = O.frame_analysis(np.zeros((1, L.d_in)), np.zeros((1, 1)), Pi, H)
+    _, Ht = O.frame_analysis(W64[:0], Po[:0, :0], Pi, H)
     t["analysis_Ht"] = time.perf_counter() - s0
     s0 = time.perf_counter()
     U, dead, _ = O.gptq_prepare(Ht, wl.damp)
     t["factor"] = time.perf_counter() - s0
     s0 = time.perf_counter()
-    mu, sigma, lo, hi = O.clip_bounds(D_rows, wl.clip_sigmas)
-    Dc = O.apply_clip(D_rows, lo, hi)
-    sc, z = O.row_grid(Dc)
+    mu, sigma, lo, hi = O.clip_bounds(D, wl.clip_sigmas)
+    Dc = O.apply_clip(D, lo, hi)
+    sc, z = O.row_grid(Dc, wl.bits)
     r = O.gptq(Dc, U, sc, z, wl.bits, wl.block, dead)
+    t["clip_grid_optq"] = time.perf_counter() - s0
+    s0 = time.perf_counter()
     O.pack2(r["codes"])
-    t["gptq"] = (time.perf_counter() - s0) * (K_out / len(rows))
-    orow = np.sort(rng.choice(L.d_out, size=min(budget_rows, L.d_out), replace=False))
-    Dh = O.dequant(r["codes"], sc, z)
-    # rows of W^ = (P_l[rows, :] D^) P_prev^T; the sampled rows of D^ stand in for all of it
+    t["pack"] = time.perf_counter() - s0
     s0 = time.perf_counter()
-    Mr = Po[orow][:, rows] @ Dh
-    t["synthesis_1"] = (time.perf_counter() - s0) * (L.d_out / len(orow)) * (K_out / len(rows))
-    s0 = time.perf_counter()
-    _ = Mr @ Pi.T
-    t["synthesis_2"] = (time.perf_counter() - s0) * (L.d_out / len(orow))
+    O.synthesis(r["codes"], sc, z, Po, Pi)
+    t["synthesis"] = time.perf_counter() - s0
     total = sum(t.values())
-    return {"value": L.d_out * L.d_in / total, "unit": "weights/s", "cores": int(cores),
-            "kind": "oracle",
-            "sample": (f"float64 numpy oracle: H on {sample_tokens} of {n} tokens (x{n // sample_tokens}); "
-                       f"D, OPTQ and synthesis on {len(rows)} of {K_out} FF rows (scaled to all rows); "
-                       f"H~ and its Cholesky factor in full; extrapolated total {total:.1f} s"),
+    return {"value": L.d_out * L.d_in / total, "unit": "weights/s", "cores": int(_blas_threads()),
+            "kind": "oracle", "cpu_model": _cpu_model(),
+            "sample": (f"the whole pass on the benchmark layer, nothing sampled: H over all {n} "
+                       f"tokens, D and H~, OPTQ on all {D.shape[0]} x {D.shape[1]} frame "
+                       f"coefficients, pack, W^ ({total:.1f} s in float64 numpy/LAPACK)"),
+            "seconds": round(total, 2),
             "stage_seconds": {k: round(v, 3) for k, v in t.items()}}
 
 
@@ -549,14 +632,134 @@ def measured_traffic(kernel, fname="traffic.json"):
         return None
 
 
+def roofline_of(kernels, work):
+    """The dominant kernel group with a defined algorithmic count ("gptq_update" sums its
+    _lazy and _span launches, which run on two different kernels; "chol" has no single
+    kernel), against its own peak."""
+    cands = [k for k in kernels if k in work and k not in ("gptq_update", "chol")]
+    dom = max(cands, key=lambda k: kernels[k]["ms_per_step"])
+    kind, amount, _ = work[dom]
+    launches = kernels[dom]["launches_per_step"]
+    avg_ms = kernels[dom]["ms_per_step"] / launches
+    per_launch = amount / launches
+    if kind == "hbm":
+        roof = {"bound": "hbm", "achieved": round(per_launch / (avg_ms / 1e3) / 1e9, 1),
+                "peak": PEAK["hbm"], "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": round(per_launch / (avg_ms / 1e3) / 1e12, 2),
+                "peak": PEAK[kind], "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["kernel"] = dom
+    roof["avg_launch_ms"] = round(avg_ms, 4)
+    roof["algorithmic_per_launch"] = per_launch
+    return roof
+
+
+def timed_steps(torch, step, steps):
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1000.0 / steps
+
+
+def profiled_steps(torch, fq, step, steps, work):
+    """`steps` more passes under the kernel timers (one stream): (ms per step, kernel
+    table, total kernel ms per step)."""
+    fq.fq_profile_reset()
+    fq.fq_profile_enable(True)
+    ms = timed_steps(torch, step, steps)
+    fq.fq_profile_enable(False)
+    kernels = kernel_table(fq, work, steps)
+    _, tot = fq.fq_profile_query("")
+    fq.fq_profile_reset()
+    return ms, kernels, tot / steps
+
+
+def contraction_block(kernels, work):
+    return {"S1_S2": contraction_summary(kernels, work, ["gemm_hessian"] + CONTRACTIONS_S2),
+            "S1_S2_S4": contraction_summary(kernels, work,
+                                            ["gemm_hessian"] + CONTRACTIONS_S2 + CONTRACTIONS_S4),
+            "S2_S4": contraction_summary(kernels, work, CONTRACTIONS_S2 + CONTRACTIONS_S4)}
+
+
+CONFIG_LAYERS = [("tiny256", 0), ("vitb", 0), ("vitb", 1), ("opt1b3", 0), ("llama7b", 0),
+                 ("llama7b", 1), ("llama70b_r1.0", 0), ("llama70b_r1.1", 0)]
+
+
+def configs_bench(torch, fq, headline, steps_small=5, steps_big=3):
+    """Every workload layer through the same pass (structured frames, two streams): ms per
+    step and weights per second from HIP-synchronized wall time around `steps` passes
+    after one warmup, then one pass under the kernel timers for the dominant kernel's
+    roofline and the contraction fractions.  The headline layer's entry repeats the
+    headline figures.  GPU only (the oracle is timed on the headline layer alone)."""
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    from fq_inputs import WORKLOADS, gen
+    out = {}
+    for key, li in CONFIG_LAYERS:
+        wl = WORKLOADS[key]
+        L = wl.layers[li]
+        name = f"{key}:{L.name}"
+        if (key, li) == headline[0]:
+            out[name] = headline[1]
+            continue
+        t0 = time.time()
+        Xs = gen.make_x(wl, L.d_in)
+        X = torch.from_numpy(Xs)
+        X = (X.view(torch.bfloat16) if wl.x_dtype == "bf16" else X).cuda()
+        del Xs
+        Ws = gen.make_weight(wl, li)
+        W = torch.from_numpy(Ws)
+        W = (W.view(torch.bfloat16) if wl.w_dtype == "bf16" else W).cuda()
+        (ko, ro, R1o, R2o), (ki, ri, R1i, R2i) = gen.layer_frame_factors(wl, li)
+        up = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+        F = (fq.Frame(L.d_out, ko, ro, up(R1o), up(R2o)), fq.Frame(L.d_in, ki, ri, up(R1i), up(R2i)))
+        K_out, K_in = F[0].K, F[1].K
+        n = X.shape[0]
+        bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, n, wl.block, frames=F)
+        side = torch.cuda.Stream()
+        stream = torch.cuda.current_stream()
+
+        def step(two=True):
+            quantize_layer(W, X, None, None, bufs, block=wl.block, damp=wl.damp,
+                           clip_sigmas=wl.clip_sigmas, stream=stream,
+                           side_stream=side if two else None)
+
+        steps = steps_big if K_in > 10000 else steps_small
+        step()
+        ms = timed_steps(torch, step, steps)
+        work = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block, rho=wl.rho,
+                                w_dtype=wl.w_dtype)
+        ms_t, kernels, _ = profiled_steps(torch, fq, lambda: step(False), 1, work)
+        roof = roofline_of(kernels, work)
+        e = {"workload": f"{key} {L.name}: W {L.d_out}x{L.d_in} {wl.w_dtype}, X {n}x{L.d_in} "
+                         f"{wl.x_dtype}, K {K_out}x{K_in} (r={wl.r}, rho={wl.rho}), {wl.bits}-bit, "
+                         f"block {wl.block}",
+             "ms_per_step": round(ms, 3), "steps": steps,
+             "weights_per_s": round(L.d_out * L.d_in / (ms / 1e3), 1),
+             "roofline": roof, "contractions": contraction_block(kernels, work),
+             "kernel_ms": {k: v["ms_per_step"] for k, v in kernels.items()}}
+        out[name] = e
+        print(f"[bench] config {name}: {ms:.2f} ms/step ({e['weights_per_s']:.3g} weights/s), "
+              f"dominant {roof['kernel']} at {roof['frac']:.3f} of peak "
+              f"({time.time() - t0:.1f}s with input generation)", file=sys.stderr, flush=True)
+        del bufs, X, W, F
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama7b")
     ap.add_argument("--layer", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload section (every other layer shape)")
     ap.add_argument("--streams", type=int, default=2, choices=(1, 2),
                     help="2 (default): D is formed on a second stream while the main stream "
                          "factors H~ (the factorization is a chain of small kernels that leaves "
@@ -567,8 +770,8 @@ def main():
                          "the other way is timed beside it")
     ap.add_argument("--pass-only", action="store_true",
                     help="time the pass only (no pass with the other frames, no inference, frame "
-                         "generation or grid variants): the kernel trace then covers exactly "
-                         "the warmup, timed and kernel-timer passes")
+                         "generation, grid variants or other workloads): the kernel trace then "
+                         "covers exactly the warmup, timed and kernel-timer passes")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="device-to-device copy of this many MiB before the warmup, as the "
                          "known-size reference for hardware byte counters")
@@ -621,88 +824,21 @@ def main():
     for i in range(args.warmup):
         step()
         print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
     # timed region: the pass alone
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1000.0 / args.steps
+    ms = timed_steps(torch, step, args.steps)
     print(f"[bench] {args.steps} timed steps: {ms:.2f} ms/step", file=sys.stderr, flush=True)
     # second timed region with the per-launch kernel timers (HIP events on the launch
     # stream around every kernel): the per-kernel breakdown and the roofline come from it.
-    # One stream here, so that no two timed kernels overlap.
-    fq.fq_profile_reset()
-    fq.fq_profile_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(two=False)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    fq.fq_profile_enable(False)
-    ms_timed = (t1 - t0) * 1000.0 / args.steps
+    # One stream here (the library keeps its own look-ahead on the caller's stream while
+    # the timers are on), so that no two timed kernels overlap.
+    work = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block,
+                            rho=wl.rho if frames is not None else None, w_dtype=wl.w_dtype)
+    ms_timed, kernels, k_total = profiled_steps(torch, fq, lambda: step(False), args.steps, work)
     print(f"[bench] {args.steps} steps with kernel timers: {ms_timed:.2f} ms/step", file=sys.stderr,
           flush=True)
-
-    rot = (R1o.shape[0] + R2o.shape[0], R1i.shape[0] + R2i.shape[0])
-    work = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block,
-                            rho=wl.rho if frames is not None else None, rot=rot)
-    passes = mfma_passes(wl.w_dtype)
-    kernels = {}
-    for name in KERNEL_GROUPS:
-        cnt, tot = fq.fq_profile_query(name)
-        if cnt == 0:
-            continue
-        e = {"launches_per_step": cnt / args.steps, "ms_per_step": round(tot / args.steps, 4)}
-        if name in work:
-            kind, amount = work[name]
-            per_step_s = tot / args.steps / 1000.0
-            if kind == "hbm":
-                e["GB/s"] = round(amount / per_step_s / 1e9, 1)
-                e["frac_of_peak"] = round(amount / per_step_s / 1e9 / PEAK["hbm"], 4)
-            else:
-                e["TFLOP/s"] = round(amount / per_step_s / 1e12, 2)
-                e["frac_of_peak"] = round(amount / per_step_s / 1e12 / PEAK[kind], 4)
-                e["peak"] = kind
-                if name in passes:
-                    # MFMA work actually executed: every bf16 pass of the split product
-                    e["passes"] = passes[name]
-                    e["executed_TFLOP/s"] = round(amount * passes[name] / per_step_s / 1e12, 2)
-                    e["executed_frac_of_peak"] = round(amount * passes[name] / per_step_s / 1e12 / PEAK[kind], 4)
-        kernels[name] = e
-    cnt_all, tot_all = fq.fq_profile_query("")
-    fq.fq_profile_reset()
-
-    # dominant kernel with a defined algorithmic count ("gptq_update" is the sum of its
-    # _lazy and _span launches, which run on two different kernels)
-    dom = max((k for k in kernels if k in work and k != "gptq_update"),
-              key=lambda k: kernels[k]["ms_per_step"])
-    kind, amount = work[dom]
-    launches = kernels[dom]["launches_per_step"]
-    avg_ms = kernels[dom]["ms_per_step"] / launches
-    per_launch = amount / launches
-    if kind == "hbm":
-        roof = {"bound": "hbm", "achieved": round(per_launch / (avg_ms / 1e3) / 1e9, 1),
-                "peak": PEAK["hbm"], "unit": "GB/s"}
-    else:
-        roof = {"bound": "mfma", "achieved": round(per_launch / (avg_ms / 1e3) / 1e12, 2),
-                "peak": PEAK[kind], "unit": "TFLOP/s"}
-    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic(dom)
-    roof["kernel"] = dom
-    roof["avg_launch_ms"] = round(avg_ms, 4)
-    roof["algorithmic_per_launch"] = per_launch
-
-    # contraction fraction of S1 + S2 (the Hessian and, with dense frames, the analysis
-    # contractions) at bf16 peak
-    contr = [k for k in kernels if k.startswith("gemm_hessian") or k.startswith("gemm_analysis")]
-    c_flops = sum(work[k][1] for k in contr)
-    c_ms = sum(kernels[k]["ms_per_step"] for k in contr)
-    contraction_frac = c_flops / (c_ms / 1e3) / 1e12 / PEAK["bf16"] if c_ms > 0 else None
-    c_exec = sum(work[k][1] * passes[k] for k in contr)
-    contraction_exec = c_exec / (c_ms / 1e3) / 1e12 / PEAK["bf16"] if c_ms > 0 else None
+    roof = roofline_of(kernels, work)
+    roof["traffic"] = measured_traffic(roof["kernel"])
+    contr = contraction_block(kernels, work)
 
     out = {
         "metric": METRIC,
@@ -717,7 +853,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 MFMA (fp32 acc) + fp64",
+        "dtype": "bf16 MFMA (fp32 acc) + fp32 MFMA (rotations) + fp64",
         "data": "synthetic (seeded; Gaussian weights with 1% x10 outliers, Gaussian "
                 "activations with 8 channels x100)",
         "config": {"workload": f"{wl.key} {L.name}_proj: W {L.d_out}x{L.d_in} {wl.w_dtype}, "
@@ -727,10 +863,13 @@ def main():
                    "d_out": L.d_out, "d_in": L.d_in, "n_tokens": n, "K_out": K_out,
                    "K_in": K_in, "streams": args.streams, "frames": args.frames},
         "roofline": roof,
-        "contraction_mfma_frac": None if contraction_frac is None else round(contraction_frac, 4),
-        "contraction_mfma_executed_frac": None if contraction_exec is None else round(contraction_exec, 4),
+        # combined MFMA fraction of the Hessian and the frame-transform contractions of
+        # the analysis (S1 + S2), each group against its own dtype's peak
+        "contraction_mfma_frac": contr["S1_S2"]["algorithmic_frac"] if contr["S1_S2"] else None,
+        "contraction_mfma_executed_frac": contr["S1_S2"]["executed_frac"] if contr["S1_S2"] else None,
+        "contractions": contr,
         "kernels": kernels,
-        "kernel_ms_total_per_step": round(tot_all / args.steps, 3),
+        "kernel_ms_total_per_step": round(k_total, 3),
     }
     if args.pass_only:
         print(json.dumps(out), flush=True)
@@ -743,17 +882,13 @@ def main():
                        side_stream=side)
 
     gstep()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        gstep()
-    torch.cuda.synchronize()
-    gms = (time.perf_counter() - t0) * 1000.0 / args.steps
+    gms = timed_steps(torch, gstep, args.steps)
     out["pass_given_H"] = {"ms_per_step": round(gms, 3),
                            "weights_per_s": round(L.d_out * L.d_in / (gms / 1e3), 1),
                            "note": "S2 -> S4 with H from the headline pass"}
     print(f"[bench] pass with H given: {gms:.2f} ms/step", file=sys.stderr, flush=True)
-    # the pass with the frames applied the other way, same inputs (one warmup, `steps` timed)
+    # the pass with the frames applied the other way, same inputs (one warmup, `steps`
+    # timed, then `steps` under the kernel timers)
     other = "dense" if args.frames == "structured" else "structured"
     ob = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
                       frames=tff_frames if other == "structured" else None)
@@ -763,17 +898,17 @@ def main():
                        damp=wl.damp, clip_sigmas=wl.clip_sigmas, stream=stream)
 
     ostep()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        ostep()
-    torch.cuda.synchronize()
-    oms = (time.perf_counter() - t0) * 1000.0 / args.steps
+    oms = timed_steps(torch, ostep, args.steps)
+    owork = algorithmic_work(n, L.d_out, L.d_in, K_out, K_in, wl.block,
+                             rho=wl.rho if other == "structured" else None, w_dtype=wl.w_dtype)
+    _, okern, _ = profiled_steps(torch, fq, ostep, args.steps, owork)
     out["other_frames"] = {"frames": other, "ms_per_step": round(oms, 3),
                            "weights_per_s": round(L.d_out * L.d_in / (oms / 1e3), 1),
                            "codes_differing_frac_vs_headline_pass": float(sum(
                                (((ob.codes >> (2 * j)) & 3) != ((bufs.codes >> (2 * j)) & 3))
-                               .sum().item() for j in range(16)) / (K_out * K_in))}
+                               .sum().item() for j in range(16)) / (K_out * K_in)),
+                           "contractions": contraction_block(okern, owork),
+                           "kernels": okern}
     print(f"[bench] pass with {other} frames: {oms:.2f} ms/step", file=sys.stderr, flush=True)
     del ob
     inf = inference_bench(fq, torch, dev, bufs, L, K_out, K_in)
@@ -783,11 +918,22 @@ def main():
     out["grid_variants"] = grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, args.steps,
                                                frames=frames)
     if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        print("[bench] timing the CPU oracle on the whole pass", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
+        print(f"[bench] CPU oracle: {out['cpu_baseline']['seconds']} s", file=sys.stderr,
+              flush=True)
         inf["cpu_baseline"] = cpu_inference_baseline(host, bufs.codes.cpu().numpy(),
                                                      bufs.scale.cpu().numpy(),
                                                      bufs.zero.cpu().numpy(), wl, li)
+    if not args.no_configs:
+        headline = ((args.workload, li),
+                    {"workload": out["config"]["workload"], "ms_per_step": out["ms_per_step"],
+                     "steps": args.steps, "weights_per_s": out["value"], "roofline": roof,
+                     "contractions": contr, "note": "the headline pass above"})
+        del bufs, dev, host
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        out["configs"] = configs_bench(torch, fq, headline)
     print(json.dumps(out), flush=True)
 
 

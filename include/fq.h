@@ -365,7 +365,9 @@ const char* fq_last_error(void);
 
 /*
  * Kernel timing (tracing).  While enabled, every kernel the library launches is
- * bracketed with HIP events on the stream it runs on.  fq_profile_query synchronizes
+ * bracketed with HIP events on the stream it runs on, and work the library would
+ * otherwise put on its own auxiliary stream (the factorization's look-ahead) runs on the
+ * caller's stream, so that timed kernels of one call never overlap.  fq_profile_query synchronizes
  * those events and returns the launch count and total milliseconds of kernels whose name
  * starts with `prefix` (all kernels for ""), since the last reset.  Not thread-safe.
  */

@@ -70,6 +70,8 @@ void prof_begin(hipStream_t s, const char* name) {
   g_prof.push_back(r);
 }
 
+bool prof_enabled() { return g_prof_on; }
+
 void prof_end(hipStream_t s) {
   if (!g_prof_on) return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
@@ -842,26 +844,28 @@ fq_status fq_frame_apply_tff(void* stream, const void* X, int xt, int64_t n_toke
                                  frame_in, Y, ws, ws_bytes);
 }
 
-fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n_tokens,
-                                  int64_t ldx, const uint32_t* codes, int bits, const float* scale,
-                                  const float* zero, const fq_tff* frame_out,
-                                  const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes) {
+// checks shared by fq_frame_apply_tff_nbit and its allocation-free variant (no launch)
+static fq_status apply_tff_check(const void* X, int xt, int64_t n_tokens, int64_t ldx,
+                                 const uint32_t* codes, int bits, const float* scale,
+                                 const float* zero, const fq_tff* frame_out,
+                                 const fq_tff* frame_in, float* Y, TffDev* Fo, TffDev* Fi) {
   if (bits != 2 && bits != 4) return fail(FQ_ERR_UNSUPPORTED, "the float inference kernels take 2- or 4-bit codes");
   if (xt < FQ_F32 || xt > FQ_BF16) return fail(FQ_ERR_INVALID_ARG, "xt must be FQ_F32, FQ_F16 or FQ_BF16");
   if (!dim_ok(n_tokens)) return fail(FQ_ERR_INVALID_ARG, "n_tokens must be in [0, 2^30)");
-  TffDev Fo, Fi;
-  fq_status st = tff_check(frame_out, "frame_out", &Fo);
+  fq_status st = tff_check(frame_out, "frame_out", Fo);
   if (st != FQ_OK) return st;
-  if ((st = tff_check(frame_in, "frame_in", &Fi)) != FQ_OK) return st;
-  if (ldx < Fi.d) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d_in");
+  if ((st = tff_check(frame_in, "frame_in", Fi)) != FQ_OK) return st;
+  if (ldx < Fi->d) return fail(FQ_ERR_INVALID_ARG, "ldx must be >= d_in");
   if (n_tokens == 0) return FQ_OK;
   if (!X || !codes || !scale || !zero || !Y) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
-  if (ws_bytes < apply_tff_layout(frame_out, frame_in, nullptr, nullptr))
-    return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_apply_tff_workspace_bytes()");
-  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
-  hipStream_t s = (hipStream_t)stream;
-  ApplyTffLayout L;
-  apply_tff_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  return FQ_OK;
+}
+
+// the launches of fq_frame_apply_tff_nbit on a carved scratch area (256-byte aligned)
+static fq_status apply_tff_launch(hipStream_t s, const void* X, int xt, int64_t n_tokens,
+                                  int64_t ldx, const uint32_t* codes, int bits,
+                                  const float* scale, const float* zero, const TffDev& Fo,
+                                  const TffDev& Fi, float* Y, const ApplyTffLayout& L) {
   const int64_t K_in = Fi.k * Fi.rho, K_out = Fo.k * Fo.rho;
   const int64_t ldu = (K_in + 15) / 16 * 16;
   hipError_t e;
@@ -879,6 +883,23 @@ fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n
       return hip_fail(e, "tff synthesis");
   }
   return FQ_OK;
+}
+
+fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n_tokens,
+                                  int64_t ldx, const uint32_t* codes, int bits, const float* scale,
+                                  const float* zero, const fq_tff* frame_out,
+                                  const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes) {
+  TffDev Fo, Fi;
+  fq_status st = apply_tff_check(X, xt, n_tokens, ldx, codes, bits, scale, zero, frame_out,
+                                 frame_in, Y, &Fo, &Fi);
+  if (st != FQ_OK || n_tokens == 0) return st;
+  if (ws_bytes < apply_tff_layout(frame_out, frame_in, nullptr, nullptr))
+    return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_frame_apply_tff_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  ApplyTffLayout L;
+  apply_tff_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  return apply_tff_launch((hipStream_t)stream, X, xt, n_tokens, ldx, codes, bits, scale, zero,
+                          Fo, Fi, Y, L);
 }
 
 // ================================================================ rounded activations

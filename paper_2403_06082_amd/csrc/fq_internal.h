@@ -14,6 +14,9 @@ typedef uint16_t u16;
 // bracket it with events on the launch stream.
 void prof_begin(hipStream_t s, const char* name);
 void prof_end(hipStream_t s);
+// whether the kernel timer is on (work that would otherwise go to an auxiliary stream
+// then stays on the caller's stream, so that no two timed kernels overlap)
+bool prof_enabled();
 hipError_t last_launch_error();
 
 // ---------------------------------------------------------------- bf16 MFMA GEMM engine

@@ -1034,7 +1034,9 @@ CholAux* chol_aux() {
 
 hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_chol_mu);
-  CholAux* aux = chol_aux();
+  // under the kernel timer every part runs on the caller's stream (timed intervals must
+  // not overlap)
+  CholAux* aux = prof_enabled() ? nullptr : chol_aux();
   bool pending = false;            // a trailing update is in flight on the auxiliary stream
   for (int64_t j0 = 0; j0 < K; j0 += CHOL_PANEL) {
     const int64_t jb = std::min<int64_t>(CHOL_PANEL, K - j0);

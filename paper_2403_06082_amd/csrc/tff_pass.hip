@@ -403,7 +403,7 @@ unsigned grid_1d(int64_t total) {
 // only; tmp is fp32).
 template <int OUT>
 hipError_t rotate_rows(const void* X, int xt, int64_t ldx, int64_t n, const TffDev& F, bool synth,
-                       float* tmp, const RotOut& o, hipStream_t s) {
+                       float* tmp, const RotOut& o, hipStream_t s, const char* name) {
   const int64_t tiles = (int64_t)((F.d1 + RB - 1) / RB) * ((F.d2 + RB - 1) / RB);
   const dim3 g((unsigned)((n + 3) / 4 * tiles)), b(256);
   RotOut ot{};
@@ -414,7 +414,7 @@ hipError_t rotate_rows(const void* X, int xt, int64_t ldx, int64_t n, const TffD
   const int vt = (F.d2 % 4 == 0 && al(tmp, 16)) ? 1 : 0;      // tmp rows are d floats
   const int vs2 = (F.d2 % 4 == 0 && al(F.R2, 16)) ? 1 : 0;
   const int vs1 = (F.d1 % 4 == 0 && al(F.R1, 16)) ? 1 : 0;
-  prof_begin(s, "tffp_rotate");
+  prof_begin(s, name);
   if (synth) {
     hipLaunchKernelGGL((k_rot_step<float, true, true, 0>), g, b, 0, s, (const float*)X, ldx, n, F.R2, F.d1, F.d2, vx, vs2, ot);
     hipLaunchKernelGGL((k_rot_step<float, false, false, OUT>), g, b, 0, s, (const float*)tmp, F.d, n, F.R1, F.d1, F.d2, vt, vs1, o);
@@ -463,12 +463,13 @@ hipError_t tff_rows_analysis_t(const void* X, int xt, int64_t ldx, int64_t n, co
   o.hi = Yhi; o.lo = Ylo; o.ldp = ldy; o.bw = (int)g.m2; o.pb = (int)g.pm;
   hipError_t e;
   if (g.pm > g.m2) {
-    prof_begin(s, "tffp_rotate");
+    prof_begin(s, "tffp_gather");
     hipLaunchKernelGGL(k_zero_pads, dim3(grid_1d(n * g.nb * (g.pm - g.m2))), dim3(TT), 0, s, Yhi, Ylo,
                        n, ldy, (int)g.nb, (int)g.m2, (int)g.pm);
     prof_end(s);
   }
-  if ((e = rotate_rows<1>(X, xt, ldx, n, F, false, tmp, o, s)) != hipSuccess) return e;
+  if ((e = rotate_rows<1>(X, xt, ldx, n, F, false, tmp, o, s, "tffp_rotate_an")) != hipSuccess)
+    return e;
   // O[c] (n x 2k) = Y[:, c pm .. c pm + pm) F_c, all blocks in one batch
   GemmDesc d;
   d.M = (int)n; d.N = (int)g.k2; d.K = (int)g.pm;
@@ -478,7 +479,7 @@ hipError_t tff_rows_analysis_t(const void* X, int xt, int64_t ldx, int64_t n, co
   d.pa[0] = 0; d.pb[0] = 0; d.pa[1] = 0; d.pb[1] = 1; d.pa[2] = 1; d.pb[2] = 0;
   d.epi = EPI_F32; d.c = O; d.ldc = g.k2;
   d.batch = (int)g.nb; d.bsa = g.pm; d.bsb = g.pm * g.pk; d.bsc = n * g.k2;
-  d.name = "tffp_dft";
+  d.name = "tffp_dft_an";
   if ((e = gemm_run(d, nullptr, s)) != hipSuccess) return e;
   prof_begin(s, "tffp_gather");
   const int64_t ntb = (n + 31) / 32;
@@ -530,12 +531,12 @@ hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const T
   }
   d.epi = EPI_F32; d.c = Z; d.ldc = F.d;
   d.batch = (int)g.nb; d.bsa = g.pk; d.bsb = g.pm * g.pk; d.bsc = g.m2;
-  d.name = "tffp_dft";
+  d.name = "tffp_dft_syn";
   hipError_t e;
   if ((e = gemm_run(d, nullptr, s)) != hipSuccess) return e;
   RotOut o{};
   o.f = out; o.ldf = ldout;
-  return rotate_rows<0>(Z, 0, F.d, n, F, true, tmp, o, s);
+  return rotate_rows<0>(Z, 0, F.d, n, F, true, tmp, o, s, "tffp_rotate_syn");
 }
 
 hipError_t transpose_f32(const float* in, int64_t rows, int64_t cols, int64_t ldin, float* out,
