@@ -260,6 +260,29 @@ fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n
                                   const fq_tff* frame_in, float* Y, void* ws, size_t ws_bytes);
 
 /*
+ * fq_frame_apply_tff_nbit without a workspace argument and without any allocation, for
+ * callers that cannot allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  The scratch space is a device array of
+ * FQ_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held until the process ends;
+ * its address is looked up on the first call on each device (the stream must belong to
+ * the current device).  The call allocates nothing (no hipMalloc, no library routine that
+ * allocates) and needs nothing cleared: the array keeps the last call's contents, and
+ * every scratch value an output depends on is written earlier in the same call.  Calls
+ * on one GPU share its array, so calls that overlap on
+ * one GPU (different streams, or host threads without ordering) race and give undefined
+ * outputs; order them on one stream.  Arguments, results and errors as
+ * fq_frame_apply_tff_nbit; frames whose fq_frame_apply_tff_workspace_bytes exceeds
+ * FQ_NOALLOC_SCRATCH_BYTES + 256 return FQ_ERR_UNSUPPORTED before any launch (16 MiB
+ * covers frames with 8 (d_in + d_out + K_in + K_out) + d2_out^2 floats up to 4 Mi, e.g.
+ * d_in = 28672, d_out = 8192, r = 1.1).
+ */
+#define FQ_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+fq_status fq_frame_apply_tff_noalloc(void* stream, const void* X, int xt, int64_t n_tokens,
+                                     int64_t ldx, const uint32_t* codes, int bits,
+                                     const float* scale, const float* zero,
+                                     const fq_tff* frame_out, const fq_tff* frame_in, float* Y);
+
+/*
  * The dense frame P (d x k rho, fp32, row stride ldp >= k rho) generated on the device from
  * its construction (the appendix on constructing TFFs; the storage appendix notes that only
  * (k, rho, d) and the rotation need be kept): column s rho + 2c + e of P is the rotated

@@ -254,6 +254,33 @@ __global__ void k_zero_i32(int* p, int n) {
 
 using namespace fq;
 
+// ---------------------------------------------------------------- allocation-free scratch
+// The scratch area of fq_frame_apply_tff_noalloc: a device array in the library's code
+// object, held by every GPU the library runs on until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it only stands in for the symbol); its
+// device address is looked up once per device with hipGetSymbolAddress, with that device
+// current, and kept here.
+static __device__ __align__(256) char scratch[FQ_NOALLOC_SCRATCH_BYTES];
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[64];
+
+static fq_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return fail(FQ_ERR_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(FQ_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return FQ_OK;
+}
+
 extern "C" {
 
 const char* fq_status_string(int st) {
@@ -898,6 +925,26 @@ fq_status fq_frame_apply_tff_nbit(void* stream, const void* X, int xt, int64_t n
   if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
   ApplyTffLayout L;
   apply_tff_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  return apply_tff_launch((hipStream_t)stream, X, xt, n_tokens, ldx, codes, bits, scale, zero,
+                          Fo, Fi, Y, L);
+}
+
+fq_status fq_frame_apply_tff_noalloc(void* stream, const void* X, int xt, int64_t n_tokens,
+                                     int64_t ldx, const uint32_t* codes, int bits,
+                                     const float* scale, const float* zero,
+                                     const fq_tff* frame_out, const fq_tff* frame_in, float* Y) {
+  TffDev Fo, Fi;
+  fq_status st = apply_tff_check(X, xt, n_tokens, ldx, codes, bits, scale, zero, frame_out,
+                                 frame_in, Y, &Fo, &Fi);
+  if (st != FQ_OK || n_tokens == 0) return st;
+  // the carve-up starts at the array's (256-byte aligned) base and must end inside it
+  if (apply_tff_layout(frame_out, frame_in, nullptr, nullptr) - 256 > FQ_NOALLOC_SCRATCH_BYTES)
+    return fail(FQ_ERR_UNSUPPORTED, "the frames need more scratch than FQ_NOALLOC_SCRATCH_BYTES "
+                                    "(use fq_frame_apply_tff_nbit with a caller workspace)");
+  void* base = nullptr;
+  if ((st = scratch_of_current_device(&base)) != FQ_OK) return st;
+  ApplyTffLayout L;
+  apply_tff_layout(frame_out, frame_in, base, &L);
   return apply_tff_launch((hipStream_t)stream, X, xt, n_tokens, ldx, codes, bits, scale, zero,
                           Fo, Fi, Y, L);
 }

@@ -75,6 +75,8 @@ SIGNATURES = {
                                  _vp, _i64, _vp, _vp, _vp, _sz]),
     "fq_frame_apply_tff_nbit": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _vp,
                                      _vp, _sz]),
+    "fq_frame_apply_tff_noalloc": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp,
+                                        _vp]),
     "fq_tff_rotation_factors_workspace_bytes": (_sz, [_i64, _i64]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
@@ -409,6 +411,29 @@ def fq_frame_apply_tff(X, codes, scale, zero, frame_out: Frame, frame_in: Frame,
                                          _ptr(codes), bits, _ptr(scale), _ptr(zero),
                                          ctypes.byref(frame_out.c), ctypes.byref(frame_in.c),
                                          _ptr(Y), wp, wb))
+    return Y
+
+
+def fq_frame_apply_tff_noalloc(X, codes, scale, zero, frame_out: Frame, frame_in: Frame, Y,
+                               stream=None, bits=2):
+    """fq_frame_apply_tff without a workspace: the library's own per-device scratch array
+    (FQ_NOALLOC_SCRATCH_BYTES) is used and nothing is allocated; Y (n x d_out fp32) is the
+    caller's.  Calls that overlap on one GPU race on that array."""
+    torch = _torch()
+    if X.dim() != 2 or X.stride(1) != 1 or not X.is_cuda:
+        raise ValueError("X must be a 2-D device tensor with unit column stride")
+    n, d_in = X.shape
+    if d_in != frame_in.d:
+        raise ValueError("X must have frame_in.d columns")
+    K_out, K_in = frame_out.K, frame_in.K
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    _dev(Y, "Y", torch.float32, (n, frame_out.d))
+    _check(lib().fq_frame_apply_tff_noalloc(_stream(stream), _ptr(X), _dt(X), n, X.stride(0),
+                                            _ptr(codes), bits, _ptr(scale), _ptr(zero),
+                                            ctypes.byref(frame_out.c), ctypes.byref(frame_in.c),
+                                            _ptr(Y)))
     return Y
 
 
