@@ -405,6 +405,91 @@ def quantize_layer(W, X_chunks, P_out, P_in, bits=2, block=128, damp=0.01,
     return r
 
 
+# --------------------------------------------------------------------------- frame choice
+def spectral_tetris_untf(rho_c: int, d_c: int):
+    """Spectral tetris (appendix "Synopsis of Construction of Tight Fusion Frames"): a
+    rho_c x d_c matrix F whose d_c columns are unit vectors and whose rows are orthogonal
+    with squared norm d_c / rho_c (a unit-norm tight frame for C^rho_c), or None when the
+    construction does not go through.  Rows are filled left to right; a row takes 1s while
+    it still lacks at least 1 of squared norm; a remainder 0 < x < 1 is placed with the
+    2 x 2 block [[sqrt(x/2), sqrt(x/2)], [sqrt(1-x/2), -sqrt(1-x/2)]] on this row and the
+    next, which then lacks 2 - x less.  The bookkeeping is exact (fractions)."""
+    from fractions import Fraction
+    if rho_c < 1 or d_c < rho_c:
+        return None
+    F = np.zeros((rho_c, d_c))
+    target = Fraction(d_c, rho_c)
+    j = 0
+    given = Fraction(0)                 # squared norm the row already has from a block
+    for r in range(rho_c):
+        need = target - given
+        given = Fraction(0)
+        if need < 0:
+            return None
+        while need >= 1:
+            if j >= d_c:
+                return None
+            F[r, j] = 1.0
+            j += 1
+            need -= 1
+        if need > 0:
+            if r + 1 >= rho_c or j + 2 > d_c:
+                return None
+            a, b = np.sqrt(float(need) / 2.0), np.sqrt(1.0 - float(need) / 2.0)
+            F[r, j], F[r, j + 1] = a, a
+            F[r + 1, j], F[r + 1, j + 1] = b, -b
+            j += 2
+            given = 2 - need
+    return F if j == d_c else None
+
+
+def modulated_frame_is_tight(F, k: int, tol: float = 1e-9) -> bool:
+    """The fusion frame of Sec. 2.2 built from F: subspace s (s < k) is spanned by the rows
+    of F multiplied entrywise by (w^(j s))_j, w = exp(2 pi i / k).  By definition it is a
+    tight fusion frame when each subspace's rows, divided by sqrt(d_c / rho_c), form an
+    orthonormal basis and the sum of the k orthogonal projections is (k rho_c / d_c) I."""
+    rho_c, d_c = F.shape
+    jj = np.arange(d_c)
+    S = np.zeros((d_c, d_c), dtype=np.complex128)
+    for s in range(k):
+        B = F * np.exp(2j * np.pi * s * jj / k)[None, :] / np.sqrt(d_c / rho_c)
+        if np.abs(B @ B.conj().T - np.eye(rho_c)).max() > tol:
+            return False
+        S += B.conj().T @ B
+    return np.abs(S - (k * rho_c / d_c) * np.eye(d_c)).max() <= tol
+
+
+def tff_frame_valid(d: int, k: int, rho: int) -> bool:
+    """A real (k, rho, d) frame by realification of the complex (k, rho/2, d/2) one exists
+    by this construction when d and rho are even, spectral tetris goes through for
+    (rho/2, d/2) and the modulation is tight (checked by its definition)."""
+    if d % 2 or rho % 2 or k < 1 or d < 2 or rho < 2:
+        return False
+    F = spectral_tetris_untf(rho // 2, d // 2)
+    return F is not None and modulated_frame_is_tight(F, k)
+
+
+def untf_max_row_support(F) -> int:
+    """Length of the longest run of columns from a row's first nonzero to its last."""
+    best = 0
+    for row in F:
+        nz = np.flatnonzero(row)
+        best = max(best, int(nz[-1] - nz[0] + 1))
+    return best
+
+
+def tff_choose_k(d: int, r: float, rho: int, valid=None) -> int:
+    """The constructible frame nearest a requested redundancy r = k rho / d (Sec. 2.2
+    remarks: take a valid (k, rho), else a lower redundancy): k = round(r d / rho), ties to
+    even, lowered until valid.  valid: the validity test (default: by definition, small d
+    only); returns 0 when no k >= 1 is valid."""
+    valid = valid or tff_frame_valid
+    k = int(round(r * d / rho))
+    while k >= 1 and not valid(d, k, rho):
+        k -= 1
+    return max(k, 0)
+
+
 # --------------------------------------------------------------------------- seeded rotation
 # The rotation factors of a frame drawn from a 64-bit seed (Sec. 2.2 and the appendix on
 # constructing TFFs take a random rotation; the storage appendix keeps only (k, rho, d)

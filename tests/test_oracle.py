@@ -537,6 +537,51 @@ def test_wiener_filtered_layer_loss():
             assert out < out0
 
 
+# ----------------------------------------------------------------------------- frame choice
+def test_spectral_tetris_untf_and_the_5_4_11_frame():
+    """The oracle's spectral tetris against the appendix's (5, 4, 11) frame F (with the
+    corrections recorded in the golden file): unit columns, orthogonal rows of squared
+    norm 11/4, and the printed entries."""
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "tff_5_4_11.json")))
+    F = O.spectral_tetris_untf(4, 11)
+    np.testing.assert_allclose(np.sum(F ** 2, axis=0), 1.0, atol=1e-15)
+    np.testing.assert_allclose(F @ F.T, 11 / 4 * np.eye(4), atol=1e-14)
+    v = np.array(g["F_sq8_signed"], dtype=float)
+    np.testing.assert_allclose(F, np.sign(v) * np.sqrt(np.abs(v) / 8.0), atol=1e-12)
+    assert O.spectral_tetris_untf(5, 4) is None          # fewer vectors than dimensions
+
+
+def test_frame_validity_pins():
+    """The (k, rho, d) triples the paper and the workloads fix: (16, 18, 256) is not
+    tight (a row of its frame spans 17 columns), (18, 16, 256) is; Example 1's frame
+    (k = 3 subspaces of C^1 in C^2, realified: rho = 2, d = 4) is; the appendix's complex
+    (5, 4, 11) frame (real rho = 8, d = 22) is, with k = 4 it is not."""
+    assert not O.tff_frame_valid(256, 16, 18)
+    assert O.tff_frame_valid(256, 18, 16)
+    assert O.tff_frame_valid(4, 3, 2)
+    assert O.tff_frame_valid(22, 5, 8)
+    assert not O.tff_frame_valid(22, 4, 8)
+    assert O.untf_max_row_support(O.spectral_tetris_untf(9, 128)) == 17
+    # lowering k only lengthens no support, so (rho, d) = (18, 256) has no valid k <= 16
+    assert O.tff_choose_k(256, 1.125, 18) == 0 and O.tff_choose_k(256, 1.125, 16) == 18
+    assert O.tff_choose_k(22, 1.9, 8) == 5 and O.tff_choose_k(22, 1.1, 8) == 0
+
+
+def test_support_rule_equals_tightness_brute_force():
+    """The support rule (longest row support <= k) decides tightness exactly, on every
+    small complex triple: tightness checked by its definition (orthonormal subspace bases,
+    frame operator a multiple of I)."""
+    for rho_c in range(1, 7):
+        for d_c in range(rho_c, 3 * rho_c + 3):
+            F = O.spectral_tetris_untf(rho_c, d_c)
+            if F is None:
+                continue
+            sup = O.untf_max_row_support(F)
+            for k in range(1, d_c + 3):
+                assert O.modulated_frame_is_tight(F, k) == (sup <= k), (rho_c, d_c, k)
+
+
 # ---------------------------------------------------------------- seeded rotation factors
 def _kat_rows():
     path = os.path.join(os.path.dirname(__file__), "golden", "philox4x32_10_kat.txt")
