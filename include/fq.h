@@ -356,6 +356,28 @@ fq_status fq_tff_rotation_factors(void* stream, uint64_t seed, int64_t d1, int64
 size_t fq_tff_rotation_factors_workspace_bytes(int64_t d1, int64_t d2);
 
 /*
+ * Choice of a constructible frame (Sec. 2.2 "Constructing TFFs" and the appendix on
+ * constructing TFFs: spectral tetris builds a unit-norm tight frame of d/2 vectors in
+ * C^(rho/2), whose modulation by the k-th roots of unity is a tight fusion frame exactly
+ * when no row of that frame has two support columns congruent mod k; with rows supported
+ * on runs of consecutive columns, when its longest row support is at most k; realified
+ * this is a real (k, rho, d) frame).  Host functions, no device work.
+ *   fq_tff_frame_valid  1 if (d, k, rho) passes that rule (d, rho even, spectral tetris
+ *                       succeeds for (rho/2, d/2)), else 0.
+ *   fq_tff_choose       the frame of redundancy r = k rho / d closest to the request that is
+ *                       constructible: k = round(r d / rho) (ties to even), lowered until
+ *                       valid (the paper lowers the redundancy when a (k, rho) is not
+ *                       valid); and the split d = d1 d2 of its Kronecker rotation (d1 the
+ *                       largest divisor of d not above sqrt(d)).  d1 / d2 may be NULL.
+ *                       Errors: FQ_ERR_INVALID_ARG (d or rho odd or < 2, r not > 0),
+ *                       FQ_ERR_UNSUPPORTED (no valid k >= 1).
+ * With the factors drawn by fq_tff_rotation_factors(seed, d1, d2), (d, k, rho, seed) is
+ * all a frame needs to be regenerated (the storage appendix).
+ */
+int fq_tff_frame_valid(int64_t d, int64_t k, int64_t rho);
+fq_status fq_tff_choose(int64_t d, double r, int64_t rho, int64_t* k, int64_t* d1, int64_t* d2);
+
+/*
  * Rounding of the frame representation of activations to act_bits-bit integers (appendix
  * "FrameQuant for Activation Quantization?"): per token t (row of U),
  * Delta_t = max_j |U_tj| / (2^(act_bits-1) - 1) and Cq_tj = round(U_tj / Delta_t), with
@@ -381,6 +403,33 @@ fq_status fq_frame_apply_tff_actq(void* stream, const void* X, int xt, int64_t n
                                   const fq_tff* frame_out, const fq_tff* frame_in, int act_bits,
                                   float* Y, void* ws, size_t ws_bytes);
 size_t fq_frame_apply_tff_actq_workspace_bytes(const fq_tff* frame_out, const fq_tff* frame_in);
+
+/*
+ * Diagonal Wiener (linear MMSE) filter at synthesis (appendix "LMMSE estimation from fusion
+ * frame measurements"; Sec. 3 "Robustness of Fusion Frames" (b)): the layer output
+ * Z = P_l D C (C = P_prev^T A_prev) is estimated from the quantized coefficients as
+ * F D^ C instead of P_l D^ C.  The paper uses a diagonal approximation of the filter and
+ * does not print it; the reading implemented here is F = P_l diag(g) with one gain per
+ * frame-coefficient row, each minimising that row's share ||(D_i - g_i D^_i) C||^2 of the
+ * output error on the calibration set:
+ *   g_i = (D H~ D^^T)_ii / (D^ H~ D^^T)_ii,   D^ = diag(scale) (codes - zero),
+ * and g_i = 1 where the denominator is 0.  The gains fold into the stored scale
+ * (scale_i g_i), so every synthesis and inference call applies the filter unchanged.
+ *   D      device fp32 K_out x K_in: the unclipped analysis output (as fq_frame_analysis
+ *          wrote it; fq_quantize_frames does not modify it).
+ *   Ht     device fp32 K_in x K_in: the undamped H~ of the calibration set (symmetric).
+ *   codes, bits, scale, zero: as fq_quantize_frames wrote them (bits 2, 3 or 4).
+ *   gain   device fp32 K_out, written.
+ *   scale_out  device fp32 K_out or NULL: fp32(g_i scale_i); may be the same array as scale.
+ * D^ H~ runs on bf16 MFMA (the codes exact, H~ as a bf16 pair: relative error about 2^-17)
+ * with fp32 accumulation; the row sums are fp64.  ws: fq_wiener_gains_workspace_bytes
+ * (K_out, K_in) bytes, 16-byte aligned.  Errors: FQ_ERR_INVALID_ARG (dimensions, NULL
+ * arrays), FQ_ERR_UNSUPPORTED (bits), FQ_ERR_WORKSPACE_TOO_SMALL, FQ_ERR_HIP.
+ */
+fq_status fq_wiener_gains(void* stream, const float* D, const float* Ht, const uint32_t* codes,
+                          int bits, const float* scale, const float* zero, int64_t K_out,
+                          int64_t K_in, float* gain, float* scale_out, void* ws, size_t ws_bytes);
+size_t fq_wiener_gains_workspace_bytes(int64_t K_out, int64_t K_in);
 
 /* Status text and the calling thread's last error message (never NULL). */
 const char* fq_status_string(int status);

@@ -14,8 +14,9 @@ from .fq import (  # noqa: F401
     fq_tff_materialize, fq_tff_materialize_workspace_bytes,
     fq_frame_analysis_tff, fq_frame_analysis_tff_workspace_bytes,
     fq_frame_synthesis_tff, fq_frame_synthesis_tff_workspace_bytes,
-    fq_tff_rotation_factors, fq_tff_rotation_factors_workspace_bytes,
+    fq_tff_rotation_factors, fq_tff_rotation_factors_workspace_bytes, fq_tff_choose,
+    fq_tff_frame_valid,
     fq_hessian_workspace_bytes, fq_frame_analysis_workspace_bytes,
     fq_quantize_frames_workspace_bytes, fq_frame_synthesis_workspace_bytes,
-    fq_profile_enable, fq_profile_reset, fq_profile_query,
+    fq_profile_enable, fq_profile_reset, fq_profile_query, fq_wiener_gains,
 )

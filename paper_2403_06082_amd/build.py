@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libfq.so")
 BUILD = os.path.join(PKG, "_build")
 ARCH = os.environ.get("FQ_OFFLOAD_ARCH", "gfx950")
-SOURCES = ["gemm_bf16.hip", "quant_f64.hip", "frame_apply.hip", "tff_apply.hip", "codes_nbit.hip", "tff_pass.hip", "tff_seed.hip", "fq_api.hip"]
+SOURCES = ["gemm_bf16.hip", "quant_f64.hip", "frame_apply.hip", "tff_apply.hip", "codes_nbit.hip", "tff_pass.hip", "tff_seed.hip", "wiener.hip", "fq_api.hip"]
 
 
 def hipcc() -> str:

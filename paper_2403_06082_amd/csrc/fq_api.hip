@@ -203,7 +203,7 @@ static size_t quant_layout(int64_t K_out, int64_t K_in, int block, void* ws, Qua
   q.scale64 = c.take<double>((size_t)K_out);
   q.zero64 = c.take<double>((size_t)K_out);
   q.inv_rdiag = c.take<double>((size_t)2 * K_in);
-  q.linv = c.take<double>(64 * 64);
+  q.lslots = c.take<double>(2 * 64 * 64);
   q.dead = c.take<uint8_t>((size_t)K_in);
   q.flags = c.take<int>(4);
   if (Q) *Q = q;
@@ -510,7 +510,7 @@ static fq_status quantize_prepare(hipStream_t s, const float* Ht, int64_t K_in, 
   hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, Q.flags, 4);
   prof_end(s);
   if ((e = q_hdiag_build(Ht, K_in, damp, Q, s)) != hipSuccess) return hip_fail(e, "hessian prep");
-  if ((e = q_cholesky(Q.A, K_in, Q.linv, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
+  if ((e = q_cholesky(Q.A, K_in, Q.lslots, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
   if ((e = q_reverse_upper(Q.A, K_in, Q.R, Q.inv_rdiag, s)) != hipSuccess) return hip_fail(e, "reverse");
   return FQ_OK;
 }
@@ -736,6 +736,76 @@ fq_status fq_frame_synthesis_nbit(void* stream, const uint32_t* codes, int bits,
   g2.epi = EPI_F32; g2.c = W_hat; g2.ldc = d_in;
   g2.name = "gemm_synthesis_2";
   if ((e = gemm_run(g2, L.tailp, s)) != hipSuccess) return hip_fail(e, "synthesis gemm 2");
+  return FQ_OK;
+}
+
+// ================================================================ diagonal Wiener filter
+// Planes: q = codes - zero [pad(K_out) x pad(K_in)] (exact bf16, rows read as the
+// reduction index's rows of A), h = H~ bf16 pair [pad(K_in) x pad8(K_in)], E = q H~ fp32
+// [K_out x K_in].
+struct WienerLayout {
+  u16 *q, *h_hi, *h_lo;
+  float* E;
+  int64_t ko, ki, ki8;
+  float* tailp;
+};
+
+static size_t wiener_layout(int64_t K_out, int64_t K_in, void* ws, WienerLayout* L) {
+  Carver c(ws);
+  WienerLayout l{};
+  l.ko = rup32(K_out);
+  l.ki = rup32(K_in);
+  l.ki8 = (K_in + 7) / 8 * 8;
+  l.q = c.take<u16>((size_t)l.ko * l.ki);
+  l.h_hi = c.take<u16>((size_t)l.ki * l.ki8);
+  l.h_lo = c.take<u16>((size_t)l.ki * l.ki8);
+  l.E = c.take<float>((size_t)K_out * K_in);
+  l.tailp = gemm_tiles(K_out, K_in) > kTailMinTiles ? c.take<float>(gemm_tail_bytes() / sizeof(float))
+                                                    : nullptr;
+  if (L) *L = l;
+  return c.off + 256;
+}
+
+size_t fq_wiener_gains_workspace_bytes(int64_t K_out, int64_t K_in) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return 0;
+  return wiener_layout(K_out, K_in, nullptr, nullptr);
+}
+
+fq_status fq_wiener_gains(void* stream, const float* D, const float* Ht, const uint32_t* codes,
+                          int bits, const float* scale, const float* zero, int64_t K_out,
+                          int64_t K_in, float* gain, float* scale_out, void* ws, size_t ws_bytes) {
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (K_out == 0) return FQ_OK;
+  if (!gain || !scale) return fail(FQ_ERR_INVALID_ARG, "NULL gain or scale");
+  if (K_in > 0 && (!D || !Ht || !codes || !zero)) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  const size_t need = wiener_layout(K_out, K_in, nullptr, nullptr);
+  if (ws_bytes < need) return fail(FQ_ERR_WORKSPACE_TOO_SMALL, "workspace smaller than fq_wiener_gains_workspace_bytes()");
+  if (!ws || !aligned16(ws)) return fail(FQ_ERR_INVALID_ARG, "workspace is NULL or not 16-byte aligned");
+  hipStream_t s = (hipStream_t)stream;
+  WienerLayout L;
+  wiener_layout(K_out, K_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
+  hipError_t e;
+  if (K_in > 0) {
+    if ((e = dequant_nbit_bf16(codes, bits, zero, K_out, K_in, L.q, L.ki, L.ko, s)) != hipSuccess)
+      return hip_fail(e, "dequant");
+    if ((e = split_bf16_pad(Ht, 0, K_in, (int)K_in, (int)K_in, nullptr, L.h_hi, L.h_lo, L.ki8,
+                            (int)L.ki, s)) != hipSuccess)
+      return hip_fail(e, "split Ht");
+    // E = q H~  (K_out x K_in): A(m, k) = q[m ki + k], B(k, n) = h[k ki8 + n]; q is exact,
+    // so the two passes q h_hi + q h_lo carry H~ to its bf16-pair precision
+    GemmDesc g;
+    g.M = (int)K_out; g.N = (int)K_in; g.K = (int)L.ki;
+    g.a[0] = L.q; g.lda = L.ki; g.a_kmajor = true;
+    g.b[0] = L.h_hi; g.b[1] = L.h_lo; g.ldb = L.ki8; g.b_kmajor = false;
+    g.npass = 2;
+    g.pa[0] = 0; g.pb[0] = 0; g.pa[1] = 0; g.pb[1] = 1;
+    g.epi = EPI_F32; g.c = L.E; g.ldc = K_in;
+    g.name = "gemm_wiener";
+    if ((e = gemm_run(g, L.tailp, s)) != hipSuccess) return hip_fail(e, "wiener gemm");
+  }
+  if ((e = wiener_rows(D, L.E, L.q, L.ki, K_out, K_in, scale, gain, scale_out, s)) != hipSuccess)
+    return hip_fail(e, "wiener rows");
   return FQ_OK;
 }
 
@@ -1251,6 +1321,69 @@ static size_t seed_layout(int64_t n, void* base, double** G, double** V, double*
   if (V) *V = v;
   if (ab) *ab = a;
   return c.off + 256;
+}
+
+// ================================================================ frame choice
+// Longest row support of the unit-norm tight frame that spectral tetris builds for d_c
+// vectors in C^rho_c (the appendix on constructing TFFs), in exact integer arithmetic with
+// squared norms in units of 1 / rho_c: every row must reach d_c units; a 1 adds rho_c; a
+// remainder 0 < x < rho_c closes the row with the 2 x 2 block T(x / rho_c), which also puts
+// 2 rho_c - x units into the next row over the same two columns.  A row's support is the
+// run of columns from its first entry (the previous row's block, if any) to its last.
+// Returns false when the construction fails (a block overfills a row, the last row has a
+// remainder, or the columns do not come out at d_c).
+static bool st_max_support(int64_t rho_c, int64_t d_c, int64_t* maxsup) {
+  if (rho_c < 1 || d_c < rho_c) return false;
+  int64_t col = 0, carry = 0, block_col = 0, best = 0;
+  for (int64_t r = 0; r < rho_c; ++r) {
+    int64_t need = d_c - carry;
+    if (need < 0) return false;
+    const int64_t start = carry > 0 ? block_col : col;
+    carry = 0;
+    const int64_t ones = need / rho_c;
+    col += ones;
+    need -= ones * rho_c;
+    if (need > 0) {
+      if (r + 1 >= rho_c) return false;
+      block_col = col;
+      col += 2;
+      carry = 2 * rho_c - need;
+    }
+    best = std::max(best, col - start);
+  }
+  if (col != d_c) return false;
+  *maxsup = best;
+  return true;
+}
+
+int fq_tff_frame_valid(int64_t d, int64_t k, int64_t rho) {
+  if (d < 2 || rho < 2 || k < 1 || d % 2 || rho % 2 || !dim_ok(d) || !dim_ok(k) || !dim_ok(rho))
+    return 0;
+  int64_t sup = 0;
+  if (!st_max_support(rho / 2, d / 2, &sup)) return 0;
+  // the modulation by the k-th roots of unity is tight exactly when no row has two support
+  // columns congruent mod k; a support is a run of consecutive columns
+  return sup <= k ? 1 : 0;
+}
+
+fq_status fq_tff_choose(int64_t d, double r, int64_t rho, int64_t* k, int64_t* d1, int64_t* d2) {
+  if (!k) return fail(FQ_ERR_INVALID_ARG, "NULL k");
+  if (d < 2 || rho < 2 || d % 2 || rho % 2 || !dim_ok(d) || !dim_ok(rho))
+    return fail(FQ_ERR_INVALID_ARG, "d and rho must be even and in [2, 2^30)");
+  if (!(r > 0.0) || !isfinite(r)) return fail(FQ_ERR_INVALID_ARG, "r must be finite and > 0");
+  const double k0 = nearbyint(r * (double)d / (double)rho);     // ties to even
+  if (!(k0 >= 1.0) || k0 >= (double)DIM_MAX) return fail(FQ_ERR_UNSUPPORTED, "no k >= 1 at this redundancy");
+  int64_t kk = (int64_t)k0;
+  while (kk >= 1 && !fq_tff_frame_valid(d, kk, rho)) --kk;
+  if (kk < 1) return fail(FQ_ERR_UNSUPPORTED, "no valid (k, rho) at or below this redundancy");
+  *k = kk;
+  // rotation factors: d1 the largest divisor of d not above sqrt(d), d2 = d / d1
+  int64_t best = 1;
+  for (int64_t a = 1; a * a <= d; ++a)
+    if (d % a == 0) best = a;
+  if (d1) *d1 = best;
+  if (d2) *d2 = d / best;
+  return FQ_OK;
 }
 
 size_t fq_tff_rotation_factors_workspace_bytes(int64_t d1, int64_t d2) {

@@ -184,7 +184,7 @@ struct QuantScratch {
   double* scale64;    // K_out
   double* zero64;     // K_out
   double* inv_rdiag;  // K_in
-  double* linv;       // 64 x 64: inverse of the current diagonal block of the factor
+  double* lslots;     // 2 x 64 x 64: factors of the last two diagonal blocks
   uint8_t* dead;      // K_in
   int* flags;         // [0] not PD, [1] non-finite
 };
@@ -193,8 +193,8 @@ hipError_t q_stats(const float* D, int64_t rows, int64_t cols, double clip_sigma
                    QuantScratch& w, hipStream_t s);
 hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& w,
                          hipStream_t s);
-// Blocked lower Cholesky of A (K x K, in place); Z: 64 x 64 doubles of scratch.
-hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s);
+// Blocked lower Cholesky of A (K x K, in place); Lslots: 2 x 64 x 64 doubles of scratch.
+hipError_t q_cholesky(double* A, int64_t K, double* Lslots, int* flags, hipStream_t s);
 hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rdiag,
                            hipStream_t s);
 hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, QuantScratch& w,
@@ -224,5 +224,13 @@ hipError_t dequant_nbit_bf16(const uint32_t* codes, int bits, const float* zero,
                              hipStream_t s);
 hipError_t dequant_bf16(const uint32_t* codes, const float* zero, int64_t rows, int64_t cols,
                         u16* out, int64_t ld_out, int64_t rows_out, hipStream_t s);
+
+// ---------------------------------------------------------------- diagonal Wiener filter
+// gain_i = (D_i . E_i) / (scale_i (Q_i . E_i)) (1 where the denominator is 0) with E = Q H~,
+// Q the bf16 plane of codes - zero (row stride ldq); scale_out (may alias scale or be
+// NULL) = gain * scale.
+hipError_t wiener_rows(const float* D, const float* E, const u16* Q, int64_t ldq, int64_t K_out,
+                       int64_t K_in, const float* scale, float* gain, float* scale_out,
+                       hipStream_t s);
 
 }  // namespace fq

@@ -264,57 +264,182 @@ __device__ __forceinline__ void zinv_step(double (&z)[64], const double (*col)[6
   }
 }
 
-// Factor the kb x kb diagonal block at (k0, k0) in place (lower) and write its inverse to
-// Z (64 x 64 row-major, lower; rows and columns beyond kb are the identity).  Rows of the
-// block beyond kb are identity rows.  Entries above the diagonal pick up finite values in
-// registers that are never written back, which keeps the update loop free of masks.
-// Two waves: wave 0 factors (one row per lane), wave 1 forms the inverse alongside.
-__global__ __launch_bounds__(128) void k_potrf64(double* __restrict__ A, int64_t lda, int64_t k0,
-                                                 int kb, double* __restrict__ Z, int* flags) {
-  __shared__ double Lrow[64][65];      // row-major copy of the factor for the global store
-  __shared__ __attribute__((aligned(16))) double col[2][64];
-  __shared__ double invd[64];
-  const int r = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  if (wave == 0) {
-    // all 64 loads of a thread in flight at once, unconditional (indices clamped into the
-    // block, the unwanted values replaced afterwards), coalesced row by row
-    const int rc = r < kb ? r : kb - 1;
-    double ld[64];
+// ---- one block column of the factorization in one launch (left-looking inside a panel).
+// Block column [k0, k0 + kb) (kb <= 64) of the panel that starts at column j0 <= k0, every
+// update from earlier panels already applied.  Work-group 0 owns the diagonal block's rows;
+// the rows below, in slabs of 64 from k0 + kb, are dealt to work-groups 1 .. gridDim.x - 1
+// (slab q to work-group 1 + q mod (gridDim.x - 1)).  Each work-group of 4 waves:
+//  1. brings the diagonal block up to date with the panel's earlier columns [j0, k0)
+//     (left-looking, fp64 MFMA, a 32 x 32 quadrant per wave):  B -= L[k0:, j0:k0] L[k0:, j0:k0]^T
+//  2. factors it (wave 0, one row per lane) while wave 1 forms its inverse, redundantly in
+//     every work-group, so that no work-group waits for another;
+//  3. work-group 0 stores L_kk to the slot Lout (every work-group reads the diagonal block
+//     of A, so it must stay unchanged during this launch) and moves the previous block's
+//     factor from its slot Lprev into A (rows this launch does not read); every other
+//     work-group, for each of its slabs, applies the same left-looking update to the slab's
+//     rows of the block column and stores X = B L_kk^-T (MFMA).
+// All reads are of columns finished by earlier launches or of the block column before it
+// is written, and every work-group writes only its own rows of A: no ordering between
+// work-groups is needed.
+constexpr int CB = 64, CBP = 65;     // block edge, LDS row pitch (conflict-free fragments)
+
+// acc (a 32 x 32 quadrant of a 64 x 64 product per wave) = sum over k in [j0, k0) of
+// L[r0 + i][k] L[d0 + j][k] for the rows r0 .. r0 + nr and d0 .. d0 + nd (zero beyond)
+__device__ __forceinline__ void chol_left_update(const double* __restrict__ A, int64_t lda,
+                                                 int64_t j0, int64_t k0, int64_t r0, int nr,
+                                                 int64_t d0, int nd, double (*Ls)[CB + 8],
+                                                 double (*Ld)[CB + 8], double (&acc)[4][4],
+                                                 int tid, int arow, int bcol, int kq) {
 #pragma unroll
-    for (int i = 0; i < 64; ++i) ld[i] = A[(k0 + (i < kb ? i : kb - 1)) * lda + k0 + rc];
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int i = 0; i < 64; ++i) Lrow[i][r] = (i < kb && r <= i) ? ld[i] : ((i == r) ? 1.0 : 0.0);
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int64_t kk0 = j0; kk0 < k0; kk0 += 16) {
+    {  // thread t stages row t / 4, 4 consecutive k, of both operands (k-major)
+      const int r = tid >> 2, kq4 = (tid & 3) * 4;
+      const int64_t rd = d0 + min(r, nd - 1), rr = r0 + min(r, nr - 1);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        Ld[kq4 + c][r] = (r < nd) ? A[rd * lda + kk0 + kq4 + c] : 0.0;
+        Ls[kq4 + c][r] = (r < nr) ? A[rr * lda + kk0 + kq4 + c] : 0.0;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; kk += 4) {
+      double af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = Ls[kk + kq][arow + 8 * i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bf[j] = Ld[kk + kq][bcol + 8 * j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
   }
+}
+
+__global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int64_t lda, int64_t K,
+                                                    int64_t j0, int64_t k0, int kb,
+                                                    double* __restrict__ Lout,
+                                                    const double* __restrict__ Lprev,
+                                                    int64_t kp0, int kpb,
+                                                    int* __restrict__ flags) {
+  __shared__ double Dg[CB][CBP];                       // diagonal block, then L_kk
+  __shared__ double Sg[CB][CBP];                       // a slab's rows of the block column
+  __shared__ double Zs[CB][CBP];                       // L_kk^-1 (Zs[k][c] = (L^-1)[k][c])
+  __shared__ double Ls[16][CB + 8], Ld[16][CB + 8];    // update staging, k-major
+  __shared__ __attribute__((aligned(16))) double col[2][64];     // broadcast column of L
+  __shared__ double invd[64];                                    // 1 / L_jj
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int w = blockIdx.x;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int blk = (lane >> 2) & 3, bi = blk >> 1, bj = blk & 1, q4 = lane & 3, kq = lane >> 4;
+  const int arow = wm * 32 + 4 * bi + q4;
+  const int bcol = wn * 32 + 4 * bj + q4;
+  const int r0 = wm * 32 + 4 * bi + kq, c0 = wn * 32 + 4 * bj + q4;   // accumulator origin
+  double acc[4][4];
+
+  // ---- 1. the diagonal block, updated, as the factorization expects it: lower part,
+  // identity rows and columns beyond kb, zero above the diagonal
+  chol_left_update(A, lda, j0, k0, k0, kb, k0, kb, Ls, Ld, acc, tid, arow, bcol, kq);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + 8 * i, c = c0 + 8 * j;
+      const double a = A[(k0 + min(r, kb - 1)) * lda + k0 + min(c, kb - 1)];
+      Dg[r][c] = (r < kb && c <= r) ? a - acc[i][j] : (r == c ? 1.0 : 0.0);
+    }
   __syncthreads();
+
+  // ---- 2. factor (wave 0) and inverse (wave 1); waves 2, 3 meet the same 64 barriers
   if (wave == 0) {
+    const int r = lane;
     double a[64];
 #pragma unroll
-    for (int c = 0; c < 64; ++c) a[c] = Lrow[r][c];
+    for (int c = 0; c < 64; ++c) a[c] = Dg[r][c];
     bool notpd = false;
     pf_scale<0>(a, col[0], invd, r, notpd);
     __syncthreads();                       // matches the first barrier of the inverse
     pf_step<0>(a, col, invd, r, notpd);
-    if (notpd && r == 0) flags[0] = 1;
-    // row-major copy for the store (zero above the diagonal), written without conflicts
+    if (notpd && r == 0 && w == 0) flags[0] = 1;
 #pragma unroll
-    for (int c = 0; c < 64; ++c) Lrow[r][c] = (c <= r) ? a[c] : 0.0;
-  } else {
+    for (int c = 0; c < 64; ++c) Dg[r][c] = (c <= r) ? a[c] : 0.0;
+  } else if (wave == 1) {
+    const int r = lane;
     double z[64];
 #pragma unroll
     for (int k = 0; k < 64; ++k) z[k] = (k == r) ? 1.0 : 0.0;
     zinv_step<0>(z, col, invd);
-    // Z[k][r] = z[k]: one row of Z per instruction across the wave (coalesced)
 #pragma unroll
-    for (int k = 0; k < 64; ++k) Z[k * 64 + r] = z[k];
+    for (int k = 0; k < 64; ++k) Zs[k][r] = z[k];
+  } else {
+    for (int i = 0; i < 64; ++i) __syncthreads();
   }
   __syncthreads();
-  if (wave == 0) {
-    // row i of the factor, zeros above the diagonal (the upper triangle of a diagonal
-    // block is never read)
+
+  // ---- 3. L_kk to its slot and the previous factor into A, or the slabs' rows of L
+  if (w == 0) {
+    for (int e = tid; e < CB * CB; e += 256) {
+      const int i = e >> 6, c = e & 63;
+      Lout[e] = Dg[i][c];
+      if (Lprev && i < kpb && c < kpb) A[(kp0 + i) * lda + kp0 + c] = Lprev[e];
+    }
+    return;
+  }
+  const int64_t below = K - k0 - kb;
+  const int64_t nslab = (below + CB - 1) / CB;
+  for (int64_t q = w - 1; q < nslab; q += gridDim.x - 1) {
+    const int64_t rs = k0 + kb + CB * q;
+    const int nr = (int)min<int64_t>(CB, K - rs);
+    chol_left_update(A, lda, j0, k0, rs, nr, k0, kb, Ls, Ld, acc, tid, arow, bcol, kq);
 #pragma unroll
-    for (int i = 0; i < 64; ++i)
-      if (i < kb && r < kb) A[(k0 + i) * lda + k0 + r] = Lrow[i][r];
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = r0 + 8 * i, c = c0 + 8 * j;
+        const double b = A[(rs + min(r, nr - 1)) * lda + k0 + min(c, kb - 1)];
+        Sg[r][c] = (r < nr && c < kb) ? b - acc[i][j] : 0.0;
+      }
+    __syncthreads();
+    // X[r][c] = sum_k Sg[r][k] Zs[c][k]  (A = Sg, B(k, c) = Zs[c][k])
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+    for (int kk = 0; kk < CB; kk += 4) {
+      double af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) af[i] = Sg[arow + 8 * i][kk + kq];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bf[j] = Zs[bcol + 8 * j][kk + kq];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = r0 + 8 * i, c = c0 + 8 * j;
+        if (r < nr && c < kb) A[(rs + r) * lda + k0 + c] = acc[i][j];
+      }
+    __syncthreads();          // Sg is reused by the next slab
+  }
+}
+
+// The last diagonal block's factor from its slot into A (k_chol_block moves every other).
+__global__ __launch_bounds__(256) void k_chol_last(double* __restrict__ A, int64_t lda,
+                                                   const double* __restrict__ L, int64_t k0, int kb) {
+  for (int e = threadIdx.x; e < CB * CB; e += 256) {
+    const int i = e >> 6, c = e & 63;
+    if (i < kb && c < kb) A[(k0 + i) * lda + k0 + c] = L[e];
   }
 }
 
@@ -736,8 +861,11 @@ __global__ __launch_bounds__(256) void k_dgemm(DgemmArgs p) {
 }
 
 // ------------------------------------------------------------------ fp64 GEMM, LDS ring
-// C = beta C + alpha A B for row-major A (M x K, rows 16-byte aligned) and B (K x N),
-// K a multiple of 16: the trailing updates of the rounding.  Tile 128 x 128, 8 waves of
+// C = beta C + alpha A op(B) for row-major A (M x K, rows 16-byte aligned) and B (K x N,
+// or with BT op(B)(k, n) = B[n ldb + k], rows 16-byte aligned), K a multiple of 16: the
+// trailing updates of the rounding and of the Cholesky factorization (BT, LOWER: only the
+// tiles on or below the diagonal, a diagonal tile computed and stored in full).  Tile
+// 128 x 128, 8 waves of
 // 32 x 64 built from 8 x 8 sub-tiles of the 2 x 2 block arrangement above; two
 // work-groups per CU (four waves per SIMD).  The waves copy each K step of 16 straight
 // from global memory into LDS (A in 16-byte pieces, rows clamped to M; B one dword per
@@ -770,26 +898,36 @@ __device__ __forceinline__ void lds_copy4(const char* base, uint32_t off, uint32
                : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
 }
 
+template <bool BT, bool LOWER>
 __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
   __shared__ __attribute__((aligned(16))) char ring[RST * RSLOT];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;          // 32-row group, 64-column half
   // work-group -> tile: contiguous ranges per XCD (ids are dealt round-robin to 8), then
-  // groups of 8 tile-rows walked column by column
+  // groups of 8 tile-rows walked column by column (LOWER: the lower tiles row by row)
   int tm, tn;
   {
     const int nb = gridDim.x, b = blockIdx.x;
     const int per = nb / 8, rem = nb % 8;
     const int xcd = b % 8, idx = b / 8;
     const int t = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
-    const int tiles_m = (int)((p.M + RT - 1) / RT);
-    const int g = t / (8 * p.tiles_n);
-    const int first = g * 8;
-    const int gs = min(8, tiles_m - first);
-    const int in = t - g * 8 * p.tiles_n;
-    tm = first + in % gs;
-    tn = in / gs;
+    if (LOWER) {
+      // t = tm (tm + 1) / 2 + tn, tn <= tm
+      int r = (int)((sqrt(8.0 * (double)t + 1.0) - 1.0) * 0.5);
+      while ((r + 1) * (r + 2) / 2 <= t) ++r;
+      while (r * (r + 1) / 2 > t) --r;
+      tm = r;
+      tn = t - r * (r + 1) / 2;
+    } else {
+      const int tiles_m = (int)((p.M + RT - 1) / RT);
+      const int g = t / (8 * p.tiles_n);
+      const int first = g * 8;
+      const int gs = min(8, tiles_m - first);
+      const int in = t - g * 8 * p.tiles_n;
+      tm = first + in % gs;
+      tn = in / gs;
+    }
   }
   const int64_t m0 = (int64_t)tm * RT, n0 = (int64_t)tn * RT;
   const int nst = (int)(p.K / RK);
@@ -806,14 +944,20 @@ __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
     const int r = 8 * (2 * wave + i) + (lane >> 3), c = lane & 7;
     const int64_t gr = min(m0 + r, p.M - 1) - m0;
     ga[i] = (uint32_t)((gr * p.lda + 2 * (c ^ (r & 7))) * 8);
-    const int kr = 2 * wave + i;
-    const int nl = (lane >> 1) ^ (8 * (kr & 3));
-    gb[i] = (uint32_t)((kr * p.ldb + nl) * 8 + 4 * (lane & 1));
+    if (BT) {
+      // op(B) rows n (B's rows) are copied like A's rows, clamped to N
+      const int64_t gn = min(n0 + r, p.N - 1) - n0;
+      gb[i] = (uint32_t)((gn * p.ldb + 2 * (c ^ (r & 7))) * 8);
+    } else {
+      const int kr = 2 * wave + i;
+      const int nl = (lane >> 1) ^ (8 * (kr & 3));
+      gb[i] = (uint32_t)((kr * p.ldb + nl) * 8 + 4 * (lane & 1));
+    }
   }
   const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void*)ring;
   const char* srcA = reinterpret_cast<const char*>(p.A + m0 * p.lda);
-  const char* srcB = reinterpret_cast<const char*>(p.B + n0);
-  const int64_t stepA = RK * 8, stepB = (int64_t)RK * p.ldb * 8;
+  const char* srcB = reinterpret_cast<const char*>(BT ? p.B + n0 * p.ldb : p.B + n0);
+  const int64_t stepA = RK * 8, stepB = BT ? (int64_t)RK * 8 : (int64_t)RK * p.ldb * 8;
   const bool bx4 = p.b16 && n0 + RT <= p.N;
   auto issue = [&](int s) {
     const uint32_t slot = ring_lds + (uint32_t)((s & 1) * RSLOT);
@@ -821,7 +965,10 @@ __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
     const char* b = srcB + s * stepB;
 #pragma unroll
     for (int i = 0; i < 2; ++i) lds_copy16(a, ga[i], slot + (2 * wave + i) * 1024);
-    if (bx4) {
+    if (BT) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) lds_copy16(b, gb[i], slot + RA_BYTES + (2 * wave + i) * 1024);
+    } else if (bx4) {
       // interior column tile: whole k-rows of B in 16-byte pieces (column pairs stay
       // together under the swizzle)
 #pragma unroll
@@ -856,9 +1003,18 @@ __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
   uint32_t xa[4], xb[4];
 #pragma unroll
   for (int t = 0; t < 4; ++t) xa[t] = base_a + 8 * ((4 * t + kq) ^ (2 * ra7));
+  if (BT) {
+    // op(B) slot laid out like A's: column n at byte 128 n, k at position k ^ 2 (n & 7);
+    // sub-tile j adds 1024 j (8 columns), k group t uses xb[t]
+    const int rb7 = 4 * bj + q4;
+    const uint32_t base_b = (uint32_t)(RA_BYTES + (wn * 64 + rb7) * 128);
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    xb[j] = (uint32_t)(RA_BYTES + kq * 1024 + (wn * 64 + 4 * bj + q4) * 8 + 64 * (j ^ kq));
+    for (int t = 0; t < 4; ++t) xb[t] = base_b + 8 * ((4 * t + kq) ^ (2 * rb7));
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      xb[j] = (uint32_t)(RA_BYTES + kq * 1024 + (wn * 64 + 4 * bj + q4) * 8 + 64 * (j ^ kq));
+  }
 
   double acc[4][8];
 #pragma unroll
@@ -878,9 +1034,14 @@ __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
       double af[4], bfv[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const double*>(slot + xa[t] + 1024 * i);
+      if (BT) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        bfv[j] = *reinterpret_cast<const double*>(slot + xb[j & 3] + 256 * (j >> 2) + 4096 * t);
+        for (int j = 0; j < 8; ++j) bfv[j] = *reinterpret_cast<const double*>(slot + xb[t] + 1024 * j);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          bfv[j] = *reinterpret_cast<const double*>(slot + xb[j & 3] + 256 * (j >> 2) + 4096 * t);
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -998,13 +1159,16 @@ hipError_t q_hdiag_build(const float* Ht, int64_t K, double damp, QuantScratch& 
   return last_launch_error();
 }
 
-// Lower Cholesky factor in place, two-level right-looking: panels of CHOL_PANEL columns are
-// factored block by block (64 columns: the diagonal block by k_potrf64, the rows below by
-// the block's inverse, and the rest of the panel's columns updated at rank 64), then the
-// trailing matrix right of the panel receives one rank-CHOL_PANEL update.  The trailing
-// matrix is thus read and written once per panel instead of once per 64 columns.  Entries
-// above the diagonal inside a panel pick up finite values that are never read.
-constexpr int64_t CHOL_PANEL = 256;
+// Lower Cholesky factor in place, in panels of CHOL_PANEL columns: inside a panel each
+// 64-column block column is one k_chol_block launch (left-looking over the panel's earlier
+// columns, the diagonal block factored in every work-group, the rows below solved through
+// the block's inverse); after a panel the trailing matrix right of it receives one
+// rank-CHOL_PANEL update.  Entries above the diagonal inside the trailing matrix pick up
+// finite values that are never read.
+#ifndef FQ_CHOL_PANEL
+#define FQ_CHOL_PANEL 128
+#endif
+constexpr int64_t CHOL_PANEL = FQ_CHOL_PANEL;
 
 namespace {
 // Auxiliary stream and events of the look-ahead factorization, one set per device, made on
@@ -1032,34 +1196,32 @@ CholAux* chol_aux() {
 }
 }  // namespace
 
-hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s) {
+hipError_t q_cholesky(double* A, int64_t K, double* Lslots, int* flags, hipStream_t s) {
   std::lock_guard<std::mutex> lock(g_chol_mu);
   // under the kernel timer every part runs on the caller's stream (timed intervals must
   // not overlap)
   CholAux* aux = prof_enabled() ? nullptr : chol_aux();
   bool pending = false;            // a trailing update is in flight on the auxiliary stream
+  int64_t nblk = 0, kp0 = 0;       // blocks launched; the previous block's column and width
+  int kpb = 0;
   for (int64_t j0 = 0; j0 < K; j0 += CHOL_PANEL) {
     const int64_t jb = std::min<int64_t>(CHOL_PANEL, K - j0);
-    for (int64_t k0 = j0; k0 < j0 + jb; k0 += 64) {
-      const int kb = (int)std::min<int64_t>(64, j0 + jb - k0);
-      prof_begin(s, "chol_potrf");
-      hipLaunchKernelGGL(k_potrf64, dim3(1), dim3(128), 0, s, A, K, k0, kb, Z, flags);
+    for (int64_t k0 = j0; k0 < j0 + jb; k0 += CB) {
+      const int kb = (int)std::min<int64_t>(CB, j0 + jb - k0);
+      // one work-group per slab of 64 rows below, at most 255 (more slabs are dealt round
+      // robin): every work-group factors the diagonal block, so more than one round of
+      // work-groups per compute unit would repeat that latency
+      const int64_t below = K - k0 - kb;
+      const unsigned grid = (unsigned)(1 + std::min<int64_t>((below + CB - 1) / CB, 255));
+      double* Lout = Lslots + (nblk & 1) * CB * CB;
+      const double* Lprev = nblk > 0 ? Lslots + ((nblk - 1) & 1) * CB * CB : nullptr;
+      prof_begin(s, "chol_block");
+      hipLaunchKernelGGL(k_chol_block, dim3(grid), dim3(256), 0, s, A, K, K, j0, k0, kb, Lout,
+                         Lprev, kp0, kpb, flags);
       prof_end(s);
-      const int64_t rest = K - k0 - kb;
-      if (rest <= 0) continue;
-      // column block below the diagonal block: X = A[k0+kb:, k0:k0+kb] L_kk^{-T}, in place
-      // (each output tile reads only its own rows, all of them before it writes)
-      double* P = A + (k0 + kb) * K + k0;
-      hipError_t e = dgemm(rest, kb, kb, 1.0, 0.0, P, K, Z, 64, true, P, K, false, s,
-                           "chol_trsm", 64);
-      if (e != hipSuccess) return e;
-      // the panel's remaining columns, every row below: A[k0+kb:, k0+kb:j0+jb] -= X X[:w]^T
-      const int64_t w = j0 + jb - (k0 + kb);
-      if (w > 0) {
-        e = dgemm(rest, w, kb, -1.0, 1.0, P, K, P, K, true, A + (k0 + kb) * K + (k0 + kb), K,
-                  false, s, "chol_syrk", 64);
-        if (e != hipSuccess) return e;
-      }
+      ++nblk;
+      kp0 = k0;
+      kpb = kb;
     }
     // rank-jb update of the trailing matrix right of the panel, in two parts (look-ahead):
     // (a) the next panel's columns, on this stream, which the next panel's factorization
@@ -1083,25 +1245,33 @@ hipError_t q_cholesky(double* A, int64_t K, double* Z, int* flags, hipStream_t s
               "chol_syrk", 64);
     if (e != hipSuccess) return e;
     if (rest2 <= 0) continue;
-    // (b): rows j2.., columns [j2, K) (lower triangle)
+    // (b): rows j2.., columns [j2, K), tiles on or below the diagonal (the LDS-ring kernel
+    // where its layout rules hold and the matrix is large enough to fill the device)
     const double* Pb = A + j2 * K + j0;
+    const int tile_b = rest2 >= 384 ? 0 : 64;
+    hipStream_t sb = s;
     if (aux) {
       if ((e = hipEventRecord(aux->chain, s)) != hipSuccess) return e;
       if ((e = hipStreamWaitEvent(aux->s2, aux->chain, 0)) != hipSuccess) return e;
-      e = dgemm(rest2, rest2, jb, -1.0, 1.0, Pb, K, Pb, K, true, A + j2 * K + j2, K, true,
-                aux->s2, "chol_syrk", 64);
-      if (e != hipSuccess) return e;
+      sb = aux->s2;
+    }
+    e = dgemm(rest2, rest2, jb, -1.0, 1.0, Pb, K, Pb, K, true, A + j2 * K + j2, K, true, sb,
+              "chol_syrk", tile_b);
+    if (e != hipSuccess) return e;
+    if (aux) {
       if ((e = hipEventRecord(aux->upd, aux->s2)) != hipSuccess) return e;
       pending = true;
-    } else {
-      e = dgemm(rest2, rest2, jb, -1.0, 1.0, Pb, K, Pb, K, true, A + j2 * K + j2, K, true, s,
-                "chol_syrk", 64);
-      if (e != hipSuccess) return e;
     }
   }
   if (aux && pending) {
     hipError_t e = hipStreamWaitEvent(s, aux->upd, 0);
     if (e != hipSuccess) return e;
+  }
+  if (nblk > 0) {
+    prof_begin(s, "chol_block");
+    hipLaunchKernelGGL(k_chol_last, dim3(1), dim3(256), 0, s, A, K,
+                       Lslots + ((nblk - 1) & 1) * CB * CB, kp0, kpb);
+    prof_end(s);
   }
   return last_launch_error();
 }
@@ -1150,17 +1320,26 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
   p.b16 = ((reinterpret_cast<uintptr_t>(B) & 15) == 0) && ldb % 2 == 0;
   // row-major operands, K a multiple of 16, 16-byte aligned A rows and 32-bit copy
   // offsets: the LDS-ring kernel
-  const bool ring_ok = !b_trans && !lower_only && K > 0 && K % RK == 0 &&
+  // b_trans: op(B) rows are B's rows, copied in 16-byte pieces like A's (16-byte aligned);
+  // lower_only: square C, tiles on or below the diagonal
+  const bool ring_ok = K > 0 && K % RK == 0 && (!lower_only || (b_trans && M == N)) &&
                        (reinterpret_cast<uintptr_t>(A) & 15) == 0 && lda % 2 == 0 &&
-                       (reinterpret_cast<uintptr_t>(B) & 7) == 0 &&
-                       (int64_t)(RT - 1) * lda * 8 + RK * 8 < ((int64_t)1 << 31) &&
-                       (int64_t)(RK - 1) * ldb * 8 + RT * 8 < ((int64_t)1 << 31);
-  const int64_t ring_tiles = ((M + RT - 1) / RT) * ((N + RT - 1) / RT);
+                       (b_trans ? ((reinterpret_cast<uintptr_t>(B) & 15) == 0 && ldb % 2 == 0 &&
+                                   (int64_t)(RT - 1) * ldb * 8 + RK * 8 < ((int64_t)1 << 31))
+                                : ((reinterpret_cast<uintptr_t>(B) & 7) == 0 &&
+                                   (int64_t)(RK - 1) * ldb * 8 + RT * 8 < ((int64_t)1 << 31))) &&
+                       (int64_t)(RT - 1) * lda * 8 + RK * 8 < ((int64_t)1 << 31);
   if (ring_ok && tile == 0) {
+    const int64_t tm_ = (M + RT - 1) / RT;
     p.tiles_n = (int)((N + RT - 1) / RT);
-    const int64_t g = ring_tiles;
+    const int64_t g = lower_only ? tm_ * (tm_ + 1) / 2 : tm_ * p.tiles_n;
     prof_begin(s, name);
-    hipLaunchKernelGGL(k_dgemm_ring, dim3((unsigned)g), dim3(64 * RWAVES), 0, s, p);
+    if (!b_trans)
+      hipLaunchKernelGGL((k_dgemm_ring<false, false>), dim3((unsigned)g), dim3(64 * RWAVES), 0, s, p);
+    else if (!lower_only)
+      hipLaunchKernelGGL((k_dgemm_ring<true, false>), dim3((unsigned)g), dim3(64 * RWAVES), 0, s, p);
+    else
+      hipLaunchKernelGGL((k_dgemm_ring<true, true>), dim3((unsigned)g), dim3(64 * RWAVES), 0, s, p);
     prof_end(s);
     return last_launch_error();
   }

@@ -79,6 +79,11 @@ SIGNATURES = {
                                         _vp]),
     "fq_tff_rotation_factors_workspace_bytes": (_sz, [_i64, _i64]),
     "fq_act_quantize": (_i, [_vp, _vp, _i64, _i64, _i, _vp, _vp]),
+    "fq_wiener_gains": (_i, [_vp, _vp, _vp, _vp, _i, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _sz]),
+    "fq_wiener_gains_workspace_bytes": (_sz, [_i64, _i64]),
+    "fq_tff_frame_valid": (_i, [_i64, _i64, _i64]),
+    "fq_tff_choose": (_i, [_i64, _d, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
+                           ctypes.POINTER(_i64)]),
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
                                      _vp, _vp, _sz]),
     "fq_frame_apply_tff_actq_workspace_bytes": (_sz, [_tp, _tp]),
@@ -275,6 +280,30 @@ def fq_frame_synthesis(codes, scale, zero, P_out, P_in, W_hat, ws=None, stream=N
     return W_hat
 
 
+def fq_wiener_gains(D, Ht, codes, scale, zero, gain=None, scale_out=None, ws=None, stream=None,
+                    bits=2):
+    """Per-row gains of the diagonal Wiener filter, g_i = (D H~ D^^T)_ii / (D^ H~ D^^T)_ii
+    (D the unclipped analysis output, H~ undamped); scale_out (optional, may be scale)
+    receives scale * g.  Returns gain."""
+    torch = _torch()
+    _dev(D, "D", torch.float32)
+    if D.dim() != 2:
+        raise ValueError("D must be 2-D")
+    K_out, K_in = D.shape
+    _dev(Ht, "Ht", torch.float32, (K_in, K_in))
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    if gain is None:
+        gain = torch.empty((K_out,), dtype=torch.float32, device=D.device)
+    _dev(gain, "gain", torch.float32, (K_out,))
+    _dev(scale_out, "scale_out", torch.float32, (K_out,))
+    ws, wp, wb = _ws(lib().fq_wiener_gains_workspace_bytes(K_out, K_in), ws, D.device)
+    _check(lib().fq_wiener_gains(_stream(stream), _ptr(D), _ptr(Ht), _ptr(codes), bits, _ptr(scale),
+                                 _ptr(zero), K_out, K_in, _ptr(gain), _ptr(scale_out), wp, wb))
+    return gain
+
+
 # ------------------------------------------------------------------ kernel timer
 def fq_profile_enable(on: bool = True):
     lib().fq_profile_enable(int(bool(on)))
@@ -342,6 +371,15 @@ class Frame:
     @property
     def K(self):
         return self.k * self.rho
+
+    @classmethod
+    def from_seed(cls, d, r, rho, seed, stream=None, device="cuda"):
+        """The constructible frame nearest redundancy r (fq_tff_choose: k lowered until the
+        modulation is tight) with its rotation factors drawn on the device from a 64-bit
+        seed (fq_tff_rotation_factors): (d, r, rho, seed) regenerate the whole frame."""
+        k, d1, d2 = fq_tff_choose(d, r, rho)
+        R1, R2 = fq_tff_rotation_factors(seed, d1, d2, stream=stream, device=device)
+        return cls(d, k, rho, R1, R2)
 
 
 def fq_tff_analysis_workspace_bytes(n, frame: Frame) -> int:
@@ -548,6 +586,20 @@ def fq_frame_synthesis_tff(codes, scale, zero, frame_out: Frame, frame_in: Frame
                                         _ptr(zero), ctypes.byref(frame_out.c),
                                         ctypes.byref(frame_in.c), _ptr(W_hat), wp, wb))
     return W_hat
+
+
+def fq_tff_frame_valid(d: int, k: int, rho: int) -> bool:
+    """Whether the modulated spectral-tetris frame (k, rho, d) is tight (host check)."""
+    return bool(lib().fq_tff_frame_valid(d, k, rho))
+
+
+def fq_tff_choose(d: int, r: float, rho: int):
+    """(k, d1, d2): the constructible frame nearest redundancy r = k rho / d (k lowered until
+    valid) and the split d = d1 d2 of its Kronecker rotation (host computation)."""
+    k, d1, d2 = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().fq_tff_choose(d, float(r), rho, ctypes.byref(k), ctypes.byref(d1),
+                               ctypes.byref(d2)))
+    return k.value, d1.value, d2.value
 
 
 def fq_tff_rotation_factors_workspace_bytes(d1: int, d2: int) -> int:

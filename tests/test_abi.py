@@ -188,3 +188,41 @@ def test_act_quantize_arguments(L):
     assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, 2, p, p, good, good, 9, p, p, 1 << 30) == 1
     assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, 3, p, p, good, good, 8, p, p, 1 << 30) == 2
     assert L.fq_frame_apply_tff_actq(n, p, 0, 1, 4096, p, 2, p, p, good, good, 8, p, p, 64) == 5
+
+
+def test_frame_choice_matches_the_oracle(L):
+    """fq_tff_frame_valid against the oracle's definition of tightness on every small real
+    triple, and fq_tff_choose against the oracle's choice (support rule at the workloads'
+    sizes) and against the frames the workloads use."""
+    import numpy as np
+    import oracle as O
+    from fq_inputs import WORKLOADS, configs
+    for rho in range(2, 13, 2):
+        for d in range(rho, 3 * rho + 6, 2):
+            for k in range(1, d // 2 + 3):
+                assert L.fq_tff_frame_valid(d, k, rho) == int(O.tff_frame_valid(d, k, rho)), (d, k, rho)
+    assert L.fq_tff_frame_valid(256, 16, 18) == 0 and L.fq_tff_frame_valid(256, 18, 16) == 1
+    assert L.fq_tff_frame_valid(21, 5, 8) == 0 and L.fq_tff_frame_valid(22, 5, 7) == 0
+
+    def support_valid(d, k, rho):
+        F = O.spectral_tetris_untf(rho // 2, d // 2)
+        return F is not None and O.untf_max_row_support(F) <= k
+
+    k, d1, d2 = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    for wl in WORKLOADS.values():
+        for lay in wl.layers:
+            for d in (lay.d_out, lay.d_in):
+                if d in wl.k_override:
+                    continue
+                assert L.fq_tff_choose(d, wl.r, wl.rho, ctypes.byref(k), ctypes.byref(d1),
+                                       ctypes.byref(d2)) == 0
+                assert k.value == O.tff_choose_k(d, wl.r, wl.rho, support_valid)
+                assert k.value == configs.frame_k(wl, d)
+                assert d1.value * d2.value == d and d1.value <= d2.value
+    # the 256 x 256 layer's stated (k, rho) = (16, 18): no k <= 16 is valid with rho = 18
+    assert L.fq_tff_choose(256, 1.125, 18, ctypes.byref(k), None, None) == 2
+    assert L.fq_tff_choose(256, 1.125, 16, ctypes.byref(k), None, None) == 0 and k.value == 18
+    assert L.fq_tff_choose(22, 1.9, 8, ctypes.byref(k), None, None) == 0 and k.value == 5
+    assert L.fq_tff_choose(22, 1.1, 8, ctypes.byref(k), None, None) == 2
+    assert L.fq_tff_choose(255, 1.1, 16, ctypes.byref(k), None, None) == 1
+    assert L.fq_tff_choose(256, -1.0, 16, ctypes.byref(k), None, None) == 1

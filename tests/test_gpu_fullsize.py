@@ -15,6 +15,7 @@ outputs the oracle can compute one by one:
            (exact outside near ties), with the pre-rounding values from one host
            Cholesky factorization of the damped H~; either way the device's packed words
            of those rows equal the packing of the replayed codes bit for bit;
+  gains  : the diagonal Wiener gains of 16 of those rows (layers with the replay);
   W_hat  : 16 random rows, P_out[i, :] D^ P_in^T from the device's codes;
   Y      : those output channels of X W_hat^T on 512 random tokens.
 Tolerances are those of the small-shape tests (see test_gpu_stages): 1e-5 relative
@@ -135,6 +136,16 @@ def fullsize_layer(key, li, n_code_rows=48, replay=True, frames="structured"):
         _log(f"scale/zero and all {K_in} columns ok on {n_code_rows} rows ({ties} near ties; "
              f"host check {time.time() - t:.1f}s)")
     np.testing.assert_array_equal(words_rows, O.pack2(replayed))
+    if replay:
+        # diagonal Wiener gains on the same rows (the device's D, H~ and codes)
+        import paper_2403_06082_amd as fq
+        g = fq.fq_wiener_gains(bufs.D, bufs.Ht, bufs.codes, bufs.scale, bufs.zero)
+        rw = rows_q[:16]
+        Dh = O.dequant(replayed[:16], sg[rw].astype(np.float64), zg[rw].astype(np.float64))
+        go = O.wiener_row_gains(Dg[rw].astype(np.float64), Dh, Htg.astype(np.float64))
+        np.testing.assert_allclose(g.cpu().numpy()[rw], go, rtol=2e-5, atol=0)
+        del g
+        _log("Wiener gains ok on 16 rows")
     del Dg, Htg
 
     # stage 4 and layer outputs, from the device's codes

@@ -61,3 +61,44 @@ def test_frame_from_seed(d, k, rho):
     T = tff.parseval_frame(k, rho, d, rotate=False)
     Po = tff.apply_rotation(O.seeded_haar(seed, 0, d1), O.seeded_haar(seed, 1, d2), T)
     assert rel_fro(P.cpu().numpy(), Po) < 1e-5
+
+
+def test_pass_with_frames_from_seed():
+    """The whole pass with both frames regenerated from (d, r, rho, seed) alone
+    (fq.Frame.from_seed: fq_tff_choose, then fq_tff_rotation_factors): D and H~ against the
+    oracle's products with the dense frames built from the oracle's own seeded factors, the
+    codes replayed row by row on the device's D and H~, W^ against the oracle's synthesis
+    of the device's codes."""
+    torch = need_gpu()
+    import paper_2403_06082_amd as fq
+    from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
+    from fq_testutil import replay_rows, check_codes, unpack_codes
+    d_out, d_in, r, rho, seed = 520, 264, 1.1, 4, 2 ** 33 + 7
+    Fo = fq.Frame.from_seed(d_out, r, rho, seed)
+    Fi = fq.Frame.from_seed(d_in, r, rho, seed + 1)
+    torch.cuda.synchronize()
+
+    def dense(F, s):
+        d1, d2 = F.R1.shape[0], F.R2.shape[0]
+        T = tff.parseval_frame(F.k, F.rho, F.d, rotate=False)
+        return tff.apply_rotation(O.seeded_haar(s, 0, d1), O.seeded_haar(s, 1, d2), T)
+
+    assert (Fo.k, Fi.k) == (O.tff_choose_k(d_out, r, rho), O.tff_choose_k(d_in, r, rho)) == (143, 73)
+    Po, Pi = dense(Fo, seed), dense(Fi, seed + 1)
+    rng = np.random.default_rng(61)
+    Wn = (rng.standard_normal((d_out, d_in)) * 0.02).astype(np.float32)
+    Xn = rng.standard_normal((900, d_in)).astype(np.float32)
+    Xn[:, 7] *= 30.0
+    W, X = torch.from_numpy(Wn).cuda(), torch.from_numpy(Xn).cuda()
+    b = LayerBuffers(d_out, d_in, Fo.K, Fi.K, torch.float32, torch.float32, 900, frames=(Fo, Fi))
+    quantize_layer(W, X, None, None, b, side_stream=torch.cuda.Stream())
+    torch.cuda.synchronize()
+    Do, Hto = O.frame_analysis(Wn, Po, Pi, b.H.cpu().numpy())
+    Dg, Htg = b.D.cpu().numpy(), b.Ht.cpu().numpy()
+    assert rel_fro(Dg, Do) < 1e-5 and rel_fro(Htg, Hto) < 1e-5
+    cg = unpack_codes(b.codes, Fi.K)
+    r_ = replay_rows(Dg, Htg, cg)
+    check_codes(r_, cg, b.scale.cpu().numpy(), b.zero.cpu().numpy(), words=b.codes.cpu().numpy())
+    Who = O.synthesis(cg, b.scale.cpu().numpy().astype(np.float64),
+                      b.zero.cpu().numpy().astype(np.float64), Po, Pi)
+    assert rel_fro(b.W_hat.cpu().numpy(), Who) < 1e-5
