@@ -583,6 +583,36 @@ def inference_bench(fq, torch, dev, bufs, L, K_out, K_in, tokens=(1, 8), iters=2
             "per_tokens": rows, "roofline": roof}
 
 
+def wiener_bench(fq, torch, bufs, K_out, K_in, steps):
+    """The diagonal Wiener gains of the headline layer (fq_wiener_gains on the pass's own
+    D, H~ and codes), timed with HIP events on the launch stream; the product (q - zero) H~
+    runs as 2 bf16 passes of 2 K_out K_in^2 flops each."""
+    stream = torch.cuda.current_stream()
+    ws = torch.empty(fq.lib().fq_wiener_gains_workspace_bytes(K_out, K_in), dtype=torch.uint8,
+                     device="cuda")
+    g = torch.empty((K_out,), dtype=torch.float32, device="cuda")
+    so = torch.empty_like(g)
+
+    def call():
+        fq.fq_wiener_gains(bufs.D, bufs.Ht, bufs.codes, bufs.scale, bufs.zero, gain=g,
+                           scale_out=so, ws=ws, stream=stream)
+
+    us = _time_calls(torch, call, stream, max(steps, 5))
+    kern = _kernel_us(fq, torch, call, ("gemm_wiener", "wiener_rows", "dequant", "split_bf16"),
+                      max(steps, 5))
+    flops = 2.0 * K_out * K_in * K_in
+    gu = kern["gemm_wiener"]["us_per_call"]
+    kern["gemm_wiener"]["TFLOP/s"] = round(flops / (gu * 1e-6) / 1e12, 1)
+    kern["gemm_wiener"]["frac_of_bf16_peak"] = round(flops / (gu * 1e-6) / 1e12 / PEAK["bf16"], 4)
+    kern["gemm_wiener"]["executed_frac_of_bf16_peak"] = round(2 * flops / (gu * 1e-6) / 1e12 / PEAK["bf16"], 4)
+    gh = g.cpu()
+    print(f"[bench] Wiener gains: {us / 1e3:.2f} ms/call", file=sys.stderr, flush=True)
+    return {"op": "fq_wiener_gains: per-row gains of the diagonal Wiener filter from D, H~ and "
+                  "the codes, folded into the scale", "ms_per_call": round(us / 1e3, 3),
+            "gain_range": [round(float(gh.min()), 4), round(float(gh.max()), 4)],
+            "kernels": kern}
+
+
 def cpu_inference_baseline(host, codes, scale, zero, wl, li, sample_rows=512):
     """The oracle's layer output for one token on `sample_rows` sampled output channels;
     its row-proportional part is scaled to all channels, the dequantization counted once."""
@@ -917,6 +947,7 @@ def main():
     out["frame_generation"] = frame_generation_bench(fq, torch, dev, wl, li, host)
     out["grid_variants"] = grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, args.steps,
                                                frames=frames)
+    out["wiener_filter"] = wiener_bench(fq, torch, bufs, K_out, K_in, args.steps)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on the whole pass", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
