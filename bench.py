@@ -718,7 +718,7 @@ CONFIG_LAYERS = [("tiny256", 0), ("vitb", 0), ("vitb", 1), ("opt1b3", 0), ("llam
                  ("llama7b", 1), ("llama70b_r1.0", 0), ("llama70b_r1.1", 0)]
 
 
-def configs_bench(torch, fq, headline, steps_small=5, steps_big=3):
+def configs_bench(torch, fq, headline, side, steps_small=5, steps_big=3):
     """Every workload layer through the same pass (structured frames, two streams): ms per
     step and weights per second from HIP-synchronized wall time around `steps` passes
     after one warmup, then one pass under the kernel timers for the dominant kernel's
@@ -748,7 +748,6 @@ def configs_bench(torch, fq, headline, steps_small=5, steps_big=3):
         K_out, K_in = F[0].K, F[1].K
         n = X.shape[0]
         bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, n, wl.block, frames=F)
-        side = torch.cuda.Stream()
         stream = torch.cuda.current_stream()
 
         def step(two=True):
@@ -794,6 +793,10 @@ def main():
                     help="2 (default): D is formed on a second stream while the main stream "
                          "factors H~ (the factorization is a chain of small kernels that leaves "
                          "most CUs idle); 1: one stream.  The kernel-timer region always uses one")
+    ap.add_argument("--reserve-cus", type=int, default=128,
+                    help="with two streams, the second is made by fq_side_stream_create and its "
+                         "kernels stay off this many compute units, which the factorization's "
+                         "chain keeps for itself (0: an ordinary second stream)")
     ap.add_argument("--frames", default="structured", choices=("structured", "dense"),
                     help="how the pass applies the frames in the analysis and the synthesis: "
                          "from their construction (default) or as the dense d x K matrices; "
@@ -821,6 +824,10 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     fq.lib()
+    # everything runs on a non-blocking stream of its own: the side stream that
+    # fq_side_stream_create makes synchronizes with the legacy default stream, so work on
+    # the default stream would not overlap it
+    torch.cuda.set_stream(torch.cuda.Stream())
     wl = WORKLOADS[args.workload]
     li = args.layer
     L = wl.layers[li]
@@ -835,7 +842,8 @@ def main():
     bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, dev["W"].dtype, dev["X"].dtype, n, wl.block,
                         frames=frames)
     stream = torch.cuda.current_stream()
-    side = torch.cuda.Stream() if args.streams == 2 else None
+    side_handle = fq.SideStream(args.reserve_cus) if args.streams == 2 else None
+    side = side_handle.stream if side_handle is not None else None
 
     def step(two=args.streams == 2):
         quantize_layer(dev["W"], dev["X"], dev["P_out"], dev["P_in"], bufs, block=wl.block,
@@ -891,7 +899,9 @@ def main():
                                f"(r={wl.r}, rho={wl.rho}), {wl.bits}-bit, block {wl.block}, "
                                f"damp {wl.damp}, clip {wl.clip_sigmas} sigma",
                    "d_out": L.d_out, "d_in": L.d_in, "n_tokens": n, "K_out": K_out,
-                   "K_in": K_in, "streams": args.streams, "frames": args.frames},
+                   "K_in": K_in, "streams": args.streams,
+                   "side_stream_reserved_cus": args.reserve_cus if args.streams == 2 else None,
+                   "frames": args.frames},
         "roofline": roof,
         # combined MFMA fraction of the Hessian and the frame-transform contractions of
         # the analysis (S1 + S2), each group against its own dtype's peak
@@ -964,7 +974,7 @@ def main():
         del bufs, dev, host
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        out["configs"] = configs_bench(torch, fq, headline)
+        out["configs"] = configs_bench(torch, fq, headline, side if side is not None else torch.cuda.Stream())
     print(json.dumps(out), flush=True)
 
 

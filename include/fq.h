@@ -144,6 +144,26 @@ fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t
                             float* scale, float* zero, void* ws, size_t ws_bytes);
 
 /*
+ * A stream for the work a caller runs beside fq_quantize_prepare (the analysis of W, which
+ * only fq_quantize_apply needs).  The factorization that prepare launches is a chain of
+ * small dependent kernels that keeps a fraction of the device busy at a time; beside it on
+ * an ordinary stream, a kernel with many work-groups takes every compute unit, and each link
+ * of the chain then waits for units to drain.  Kernels queued on a stream made here run on
+ * every compute unit but `reserve_cus` of them (the first ones in the order of the device's
+ * CU mask, hipExtStreamCreateWithCUMask), which stay free for the chain.
+ *   reserve_cus  in [0, n_cu / 2], n_cu the current device's compute-unit count; 0 makes an
+ *                ordinary non-blocking stream.
+ *   *stream      receives the new hipStream_t of the current device (default priority);
+ *                release it with fq_side_stream_destroy.
+ * A stream with a CU mask synchronizes with the legacy default stream (NULL) as a blocking
+ * stream does: the work it runs beside must be queued on another stream, or the two
+ * serialize.
+ * Errors: FQ_ERR_INVALID_ARG (reserve_cus out of range, stream NULL), FQ_ERR_HIP.
+ */
+fq_status fq_side_stream_create(int reserve_cus, void** stream);
+fq_status fq_side_stream_destroy(void* stream);
+
+/*
  * Synthesis of the dequantized layer (Alg. 1 return value; appendix "Computational
  * Complexity during Inference"):  W_hat = P_out * diag(scale) * (codes - zero) * P_in^T.
  *   codes/scale/zero  as produced by fq_quantize_frames.

@@ -18,5 +18,5 @@ from .fq import (  # noqa: F401
     fq_tff_frame_valid,
     fq_hessian_workspace_bytes, fq_frame_analysis_workspace_bytes,
     fq_quantize_frames_workspace_bytes, fq_frame_synthesis_workspace_bytes,
-    fq_profile_enable, fq_profile_reset, fq_profile_query, fq_wiener_gains,
+    fq_profile_enable, fq_profile_reset, fq_profile_query, fq_wiener_gains, SideStream,
 )

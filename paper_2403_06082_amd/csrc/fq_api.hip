@@ -623,6 +623,35 @@ fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t
                         scale, zero, Q);
 }
 
+// A stream kept off the first reserve_cus compute units (bit c of the mask = unit c).
+fq_status fq_side_stream_create(int reserve_cus, void** stream) {
+  if (!stream) return fail(FQ_ERR_INVALID_ARG, "stream is NULL");
+  *stream = nullptr;
+  int dev = 0, n_cu = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "compute-unit count");
+  if (reserve_cus < 0 || reserve_cus > n_cu / 2)
+    return fail(FQ_ERR_INVALID_ARG, "reserve_cus must be in [0, compute units / 2]");
+  hipStream_t s = nullptr;
+  if (reserve_cus == 0) {
+    e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+  } else {
+    std::vector<uint32_t> mask((size_t)(n_cu + 31) / 32, 0u);
+    for (int c = reserve_cus; c < n_cu; ++c) mask[(size_t)c / 32] |= 1u << (c % 32);
+    e = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
+  }
+  if (e != hipSuccess) return hip_fail(e, "stream creation");
+  *stream = s;
+  return FQ_OK;
+}
+
+fq_status fq_side_stream_destroy(void* stream) {
+  if (!stream) return fail(FQ_ERR_INVALID_ARG, "stream is NULL");
+  const hipError_t e = hipStreamDestroy((hipStream_t)stream);
+  return e == hipSuccess ? FQ_OK : hip_fail(e, "stream destruction");
+}
+
 // ================================================================ S4: synthesis
 size_t fq_frame_apply_workspace_bytes(int64_t d_in, int64_t K_out, int64_t K_in) {
   if (!dim_ok(d_in) || !dim_ok(K_out) || !dim_ok(K_in)) return 0;

@@ -87,6 +87,8 @@ SIGNATURES = {
     "fq_frame_apply_tff_actq": (_i, [_vp, _vp, _i, _i64, _i64, _vp, _i, _vp, _vp, _tp, _tp, _i,
                                      _vp, _vp, _sz]),
     "fq_frame_apply_tff_actq_workspace_bytes": (_sz, [_tp, _tp]),
+    "fq_side_stream_create": (_i, [_i, ctypes.POINTER(_vp)]),
+    "fq_side_stream_destroy": (_i, [_vp]),
     "fq_status_string": (ctypes.c_char_p, [_i]),
     "fq_last_error": (ctypes.c_char_p, []),
     "fq_profile_enable": (None, [_i]),
@@ -259,6 +261,28 @@ def fq_quantize_apply(D, codes, scale, zero, ws, bits: int = 2, block: int = 128
                                    float(clip_sigmas), _ptr(codes), _ptr(scale), _ptr(zero),
                                    _ptr(ws), ws.numel()))
     return codes, scale, zero
+
+
+class SideStream:
+    """A stream from fq_side_stream_create (kernels kept off `reserve_cus` compute units),
+    usable wherever a torch stream is (`.stream` is a torch.cuda.ExternalStream).  Released
+    with the object."""
+
+    def __init__(self, reserve_cus: int = 128, device=None):
+        torch = _torch()
+        dev = torch.device("cuda", torch.cuda.current_device() if device is None else device)
+        self._h = None
+        with torch.cuda.device(dev):
+            h = ctypes.c_void_p()
+            _check(lib().fq_side_stream_create(int(reserve_cus), ctypes.byref(h)))
+        self._h = h.value
+        self.reserve_cus = int(reserve_cus)
+        self.stream = torch.cuda.ExternalStream(self._h, device=dev)
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.fq_side_stream_destroy(ctypes.c_void_p(self._h))
+            self._h = None
 
 
 def fq_frame_synthesis(codes, scale, zero, P_out, P_in, W_hat, ws=None, stream=None, bits=2):

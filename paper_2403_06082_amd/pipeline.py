@@ -14,6 +14,9 @@ and the dense P_out, P_in are not read (pass None).
 With a second stream (side_stream), D = P_out^T W P_in is formed there while the main
 stream factors the damped H~ (fq_quantize_prepare): the Cholesky factorization, a chain
 of small dependent kernels, then overlaps the D contractions.  Outputs are identical.
+A side stream from fq.SideStream keeps the D kernels off part of the device, so that the
+chain always finds free compute units; it synchronizes with the legacy default stream, so
+the main stream must then be another stream (torch.cuda.Stream()).
 """
 from __future__ import annotations
 

@@ -89,7 +89,8 @@ def test_pipeline_vitb():
 @pytest.mark.parametrize("key", ["tiny256", "vitb"])
 def test_two_stream_order_is_bit_identical(key):
     """D formed on a second stream while the main stream factors H~ (prepare / apply)
-    gives exactly the outputs of the one-stream order."""
+    gives exactly the outputs of the one-stream order, also when the second stream is kept
+    off part of the device (fq_side_stream_create)."""
     torch = need_gpu()
     from paper_2403_06082_amd.pipeline import LayerBuffers, quantize_layer
     wl = WORKLOADS[key]
@@ -100,17 +101,42 @@ def test_two_stream_order_is_bit_identical(key):
     W = upload(gen.make_weight(wl, 0), wl.w_dtype)
     K_out, K_in = P_out.shape[1], P_in.shape[1]
     outs = []
-    side = torch.cuda.Stream()
-    for two in (False, True, True):
+    import paper_2403_06082_amd as fq
+    part = fq.SideStream(128)         # kernels kept off 128 compute units
+    sides = {0: None, 1: torch.cuda.Stream(), 2: torch.cuda.Stream(), 3: part.stream}
+    for two in (0, 1, 2, 3):
         bufs = LayerBuffers(L.d_out, L.d_in, K_out, K_in, W.dtype, X.dtype, X.shape[0], wl.block)
         quantize_layer(W, X, P_out, P_in, bufs, block=wl.block, damp=wl.damp,
-                       clip_sigmas=wl.clip_sigmas, side_stream=side if two else None)
+                       clip_sigmas=wl.clip_sigmas, side_stream=sides[two])
         torch.cuda.synchronize()
         outs.append({k: getattr(bufs, k).cpu().numpy() for k in
                      ("H", "D", "Ht", "codes", "scale", "zero", "W_hat")})
     for o in outs[1:]:
         for k, v in o.items():
             np.testing.assert_array_equal(v, outs[0][k], err_msg=k)
+
+
+def test_side_stream_create_and_errors():
+    """fq_side_stream_create: a usable stream for reserves across [0, CUs / 2]; a reserve
+    out of range and a NULL handle are refused."""
+    torch = need_gpu()
+    import ctypes
+    import paper_2403_06082_amd as fq
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    for reserve in (0, 1, n_cu // 4, n_cu // 2):
+        print(f"reserve {reserve} of {n_cu}", flush=True)
+        s = fq.SideStream(reserve)
+        x = torch.arange(1 << 20, dtype=torch.float32, device="cuda")
+        with torch.cuda.stream(s.stream):
+            y = x * 2.0 + 1.0
+        s.stream.synchronize()
+        assert torch.equal(y, x * 2.0 + 1.0)
+        del s
+    h = ctypes.c_void_p()
+    for bad in (-1, n_cu // 2 + 1, n_cu):
+        assert fq.lib().fq_side_stream_create(bad, ctypes.byref(h)) == 1
+    assert fq.lib().fq_side_stream_create(0, None) == 1
+    assert fq.lib().fq_side_stream_destroy(None) == 1
 
 
 def test_prepare_apply_match_fused_call():
