@@ -50,11 +50,24 @@ def _tff_geom(d, K, rho):
 
 
 def _rot_exec(g):
-    """fp32 MFMA flops issued per vector by the two rotation steps (64 x 64 output tiles,
-    k steps of 16): X R2 with k = d2, then R1^T (.) with k = d1."""
-    p64 = lambda x: -(-x // 64) * 64
+    """fp32 MFMA flops issued per vector by the rotation.  Fused kernel (d1 <= 128,
+    d2 % 4 == 0, the operands within LDS): rows padded to 16 (5 and 7 tiles of 16 to 6 and
+    8), k of the first factor padded to 16, output columns in blocks of 64 (128 when
+    d2 >= 128); both factors on those padded shapes.  Otherwise the two-step kernels: 64 x 64
+    output tiles, k steps of 16."""
     p16 = lambda x: -(-x // 16) * 16
-    return 2 * p64(g["d1"]) * p64(g["d2"]) * (p16(g["d2"]) + p16(g["d1"]))
+    d1, d2 = g["d1"], g["d2"]
+    mt = p16(d1) // 16
+    mt = {5: 6, 7: 8}.get(mt, mt)
+    m, k2 = 16 * mt, p16(d2)
+    bj = 128 if k2 >= 128 else 64
+    lds = (m * (max(k2, bj) + 4) + bj * (k2 + 4) + m * (m + 4)) * 4
+    maxq = 16 if bj == 64 else 8
+    if d1 <= 128 and d2 % 4 == 0 and d1 * (d2 // 4) <= (bj * 4) * maxq and lds <= 160 * 1024:
+        cols = -(-d2 // bj) * bj
+        return 2 * m * cols * (k2 + m)
+    p64 = lambda x: -(-x // 64) * 64
+    return 2 * p64(d1) * p64(d2) * (p16(d2) + p16(d1))
 
 
 def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, w_dtype="bf16"):

@@ -393,6 +393,284 @@ __global__ __launch_bounds__(TT) void k_sym_average(float* __restrict__ X, int64
   }
 }
 
+// ---- both rotation factors of a row in one work-group.
+// out_t = A X_t B with X_t the d1 x d2 view of row t; analysis: A = R1^T, B = R2; synthesis:
+// A = R1, B = R2^T.  A work-group of NW waves takes FR_NV consecutive rows and one block of
+// BJ = 16 NW output columns; wave w forms the 16 columns [16 w, 16 w + 16) of the block for
+// every output row, with v_mfma_f32_16x16x4_f32 on 16 x 16 tiles:
+//  step A  T = X_t B[:, cols], K = d2.  Inside a chunk of 16 k values, at step s lane l
+//          supplies k = kc + 4 (l / 16) + s (a permutation of the k order, the same for both
+//          operands), so each lane reads its operands for four steps as one 16-byte run.
+//  step B  out[:, cols] = A T, K = d1.  The accumulator of tile mt of step A holds, in lane
+//          l and value v, T[16 mt + 4 (l / 16) + v][col l % 16]: in the same k order this is
+//          exactly the B operand of step B at step v, so T stays in registers.
+// X_t, B[:, block] (transposed) and A sit in LDS with k contiguous; the next row's X is
+// fetched into registers while the current one is multiplied.  The output block goes
+// through LDS (the space of X_t) and leaves in runs of 8 consecutive elements per lane.
+#ifndef FR_ROWS
+#define FR_ROWS 4
+#endif
+constexpr int FR_NV = FR_ROWS;   // rows per work-group
+constexpr int FR_MAXQ = 16;      // pieces of 4 elements of a row per thread
+
+__host__ __device__ constexpr int fr_pad16(int x) { return (x + 15) / 16 * 16; }
+__host__ __device__ inline int fr_waves(int d2) { return fr_pad16(d2) >= 128 ? 8 : 4; }
+__host__ __device__ inline int fr_mt(int d1) {    // 16-row tiles of d1 (5 -> 6, 7 -> 8)
+  const int m = fr_pad16(d1) / 16;
+  return m == 5 ? 6 : (m == 7 ? 8 : m);
+}
+
+// LDS floats of the fused kernel for d1 x d2
+__host__ __device__ inline int64_t fr_lds_floats(int d1, int d2) {
+  const int64_t m = 16 * fr_mt(d1), k = fr_pad16(d2), bj = 16 * fr_waves(d2);
+  const int64_t pxo = (k > bj ? k : bj) + 4;
+  return m * pxo + bj * (k + 4) + m * (m + 4);
+}
+
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// a row's pieces held raw while in flight (16 bytes for fp32, 8 for the 16-bit types);
+// converted to fp32 when stored to LDS
+template <typename XT> struct FrRaw { typedef uint2 T; };
+template <> struct FrRaw<float> { typedef float4 T; };
+__device__ __forceinline__ float4 fr_cvt(float4 v, const float*) { return v; }
+__device__ __forceinline__ float4 fr_cvt(uint2 u, const uint16_t*) {   // bf16
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+}
+__device__ __forceinline__ float4 fr_cvt(uint2 u, const _Float16*) {
+  const _Float16* h = reinterpret_cast<const _Float16*>(&u);
+  return make_float4((float)h[0], (float)h[1], (float)h[2], (float)h[3]);
+}
+
+template <typename XT, bool SYN, int OUT, int MT, int NQ, int NW>
+__global__ __launch_bounds__(64 * NW) void k_rot_fused(const XT* __restrict__ X, int64_t ldx,
+                                                       int64_t n, const float* __restrict__ R1,
+                                                       const float* __restrict__ R2, int d1,
+                                                       int d2, int vout, RotOut o) {
+  extern __shared__ __attribute__((aligned(16))) float fr_lds[];
+  constexpr int M = 16 * MT;                   // d1 padded
+  constexpr int BJ = 16 * NW;                  // output columns per work-group
+  constexpr int NT = 64 * NW;                  // threads
+  const int K2 = fr_pad16(d2);                 // d2 padded (k of step A)
+  const int PX = K2 + 4, PA = M + 4;           // row pitches (floats): 16-byte reads of 16
+  constexpr int PO = BJ + 4;                   // rows at one k fall on distinct banks
+  const int PXO = (K2 > BJ ? K2 : BJ) + 4;
+  float* Xs = fr_lds;                          // [M][PX]   X_t (i, k); later [M][PO] output
+  float* Bs = Xs + M * PXO;                    // [BJ][PX]  B[k][jb BJ + j] at (j, k)
+  float* As = Bs + BJ * PX;                    // [M][PA]   A[i][k]
+  const int njb = (d2 + BJ - 1) / BJ;
+  const int jb = (int)(blockIdx.x % njb);
+  const int64_t t0 = (int64_t)(blockIdx.x / njb) * FR_NV;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c = lane & 15, g = lane >> 4;
+
+  // resident operands: A (d1 x d1) and the block's columns of B, zero padded
+  for (int e = tid; e < M * M; e += NT) {
+    const int i = e / M, k = e - i * M;
+    float v = 0.f;
+    if (i < d1 && k < d1) v = SYN ? R1[(int64_t)i * d1 + k] : R1[(int64_t)k * d1 + i];
+    As[i * PA + k] = v;
+  }
+  for (int e = tid; e < BJ * K2; e += NT) {
+    const int j = e / K2, k = e - j * K2;
+    const int jj = jb * BJ + j;
+    float v = 0.f;
+    if (jj < d2 && k < d2) v = SYN ? R2[(int64_t)jj * d2 + k] : R2[(int64_t)k * d2 + jj];
+    Bs[j * PX + k] = v;
+  }
+
+  // the row's d1 x d2 values in pieces of 4 (d2 % 4 == 0, so a piece stays in one row of
+  // the view): piece e = tid + NT q covers elements 4 e .. 4 e + 3, i.e.
+  // (i, k) = (4 e / d2, 4 e mod d2); its LDS offset is computed once
+  typedef typename FrRaw<XT>::T Raw;
+  const int qrow = d2 / 4;
+  const int nq = d1 * qrow;
+  int loff[NQ];
+  {
+    int i = tid / qrow, r = tid - (tid / qrow) * qrow;
+    const int di = NT / qrow, dr = NT - (NT / qrow) * qrow;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      loff[q] = i * PX + 4 * r;
+      i += di;
+      r += dr;
+      if (r >= qrow) { r -= qrow; ++i; }
+    }
+  }
+  Raw pre[NQ];
+  auto fetch = [&](int64_t t) {
+    const Raw* x = reinterpret_cast<const Raw*>(X + t * ldx);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+      if (tid + NT * q < nq) pre[q] = x[tid + NT * q];
+  };
+  if (t0 < n) fetch(t0);
+
+  // zero padding of X_t: rows d1 .. M once (the output block, staged in the same space,
+  // covers rows < d1 only when BJ <= K2); columns d2 .. K2 of rows < d1 before every row
+  const bool stage_fits = BJ <= K2;
+  for (int e = tid; e < (M - d1) * K2; e += NT) Xs[d1 * PX + (e / K2) * PX + e % K2] = 0.f;
+  const int kpad = K2 - d2;
+
+  for (int v = 0; v < FR_NV; ++v) {
+    const int64_t t = t0 + v;
+    if (t >= n) break;
+    __syncthreads();                 // the previous row's output has left the LDS
+    if (!stage_fits) {
+      for (int e = tid; e < M * K2; e += NT) {
+        const int i = e / K2, k = e - i * K2;
+        if (i >= d1 || k >= d2) Xs[i * PX + k] = 0.f;
+      }
+    } else if (kpad > 0) {
+      for (int e = tid; e < d1 * kpad; e += NT) Xs[(e / kpad) * PX + d2 + e % kpad] = 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+      if (tid + NT * q < nq)
+        *reinterpret_cast<float4*>(&Xs[loff[q]]) = fr_cvt(pre[q], (const XT*)nullptr);
+    __syncthreads();
+    if (v + 1 < FR_NV && t + 1 < n) fetch(t + 1);
+
+    // step A: T[:, 16 w + c] for all M rows; the MT accumulators interleave
+    floatx4 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int kc = 0; kc < K2; kc += 16) {
+      const float4 bv = *reinterpret_cast<const float4*>(&Bs[(16 * w + c) * PX + kc + 4 * g]);
+      float4 av[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        av[mt] = *reinterpret_cast<const float4*>(&Xs[(16 * mt + c) * PX + kc + 4 * g]);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt].x, bv.x, acc[mt], 0, 0, 0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt].y, bv.y, acc[mt], 0, 0, 0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt].z, bv.z, acc[mt], 0, 0, 0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[mt].w, bv.w, acc[mt], 0, 0, 0);
+    }
+    __syncthreads();                 // every wave is done with X_t
+    // step B: out[:, 16 w + c] = A T, the accumulators of step A as the B operand
+    floatx4 res[MT];
+#pragma unroll
+    for (int it = 0; it < MT; ++it) res[it] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      float4 av[MT];
+#pragma unroll
+      for (int it = 0; it < MT; ++it)
+        av[it] = *reinterpret_cast<const float4*>(&As[(16 * it + c) * PA + 16 * mt + 4 * g]);
+#pragma unroll
+      for (int it = 0; it < MT; ++it) res[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[it].x, acc[mt][0], res[it], 0, 0, 0);
+#pragma unroll
+      for (int it = 0; it < MT; ++it) res[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[it].y, acc[mt][1], res[it], 0, 0, 0);
+#pragma unroll
+      for (int it = 0; it < MT; ++it) res[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[it].z, acc[mt][2], res[it], 0, 0, 0);
+#pragma unroll
+      for (int it = 0; it < MT; ++it) res[it] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[it].w, acc[mt][3], res[it], 0, 0, 0);
+    }
+    // lane l, value r of tile it: output row 16 it + 4 g + r, block column 16 w + c
+    float* Os = Xs;
+#pragma unroll
+    for (int it = 0; it < MT; ++it)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (16 * it + 4 * g + r < d1) Os[(16 * it + 4 * g + r) * PO + 16 * w + c] = res[it][r];
+    __syncthreads();
+    // the block's rows (< d1) in runs of 8 columns: run u = (row, 8 j8) of d1 x BJ / 8
+    const int jbase = jb * BJ;
+    const int ncol = min(BJ, d2 - jbase);
+    for (int u = tid; u < d1 * (BJ / 8); u += NT) {
+      const int ii = u / (BJ / 8), j8 = (u - ii * (BJ / 8)) * 8;
+      if (j8 >= ncol) continue;
+      const float4 v0 = *reinterpret_cast<const float4*>(&Os[ii * PO + j8]);
+      const float4 v1 = *reinterpret_cast<const float4*>(&Os[ii * PO + j8 + 4]);
+      const float vv[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      const int64_t p0 = (int64_t)ii * d2 + jbase + j8;
+      if (OUT == 0) {
+        float* dst = o.f + t * o.ldf + p0;
+        if (vout && j8 + 8 <= ncol) {
+          *reinterpret_cast<float4*>(dst) = v0;
+          *reinterpret_cast<float4*>(dst + 4) = v1;
+        } else {
+          for (int e = 0; e < 8 && j8 + e < ncol; ++e) dst[e] = vv[e];
+        }
+      } else {
+        const int64_t cb = (uint32_t)p0 / (uint32_t)o.bw, pin = p0 - cb * o.bw;   // p0 < 2^31
+        const int64_t idx = t * o.ldp + cb * o.pb + pin;
+        if (vout && j8 + 8 <= ncol && pin + 8 <= o.bw) {
+          uint32_t h[4], l[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t ha = rne_bf16(vv[2 * e]), hb = rne_bf16(vv[2 * e + 1]);
+            h[e] = ha | (hb << 16);
+            l[e] = rne_bf16(vv[2 * e] - __uint_as_float(ha << 16)) |
+                   (rne_bf16(vv[2 * e + 1] - __uint_as_float(hb << 16)) << 16);
+          }
+          *reinterpret_cast<uint4*>(o.hi + idx) = make_uint4(h[0], h[1], h[2], h[3]);
+          *reinterpret_cast<uint4*>(o.lo + idx) = make_uint4(l[0], l[1], l[2], l[3]);
+        } else {
+          for (int e = 0; e < 8 && j8 + e < ncol; ++e) {
+            const int64_t pe = p0 + e, ce = (uint32_t)pe / (uint32_t)o.bw;
+            const int64_t ie = t * o.ldp + ce * o.pb + (pe - ce * o.bw);
+            const uint32_t hh = rne_bf16(vv[e]);
+            o.hi[ie] = (u16)hh;
+            o.lo[ie] = (u16)rne_bf16(vv[e] - __uint_as_float(hh << 16));
+          }
+        }
+      }
+    }
+  }
+}
+
+template <typename XT, bool SYN, int OUT>
+void launch_rot_fused(const XT* X, int64_t ldx, int64_t n, const TffDev& F, const RotOut& o,
+                      hipStream_t s) {
+  const int MT = fr_mt(F.d1), NW = fr_waves(F.d2);
+  const int njb = (F.d2 + 16 * NW - 1) / (16 * NW);
+  const dim3 g((unsigned)(njb * ((n + FR_NV - 1) / FR_NV))), b((unsigned)(64 * NW));
+  const size_t lds = (size_t)fr_lds_floats(F.d1, F.d2) * sizeof(float);
+  const bool small = (int64_t)F.d1 * (F.d2 / 4) <= 64 * NW * 4;
+  // 16-byte output runs: 8-element runs start 16-byte aligned in every destination row
+  int vout;
+  if (OUT == 0)
+    vout = (F.d2 % 8 == 0 && o.ldf % 4 == 0 && (reinterpret_cast<uintptr_t>(o.f) & 15) == 0);
+  else
+    vout = (F.d2 % 8 == 0 && o.bw % 8 == 0 && o.pb % 8 == 0 && o.ldp % 8 == 0 &&
+            (reinterpret_cast<uintptr_t>(o.hi) & 15) == 0 &&
+            (reinterpret_cast<uintptr_t>(o.lo) & 15) == 0);
+  // dynamic LDS beyond 64 KB needs the kernel's limit raised (once per instantiation)
+#define FR_LAUNCH(m, q, nw) { \
+      static const hipError_t attr = hipFuncSetAttribute( \
+          reinterpret_cast<const void*>(k_rot_fused<XT, SYN, OUT, m, q, nw>), \
+          hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024); \
+      (void)attr; \
+      hipLaunchKernelGGL((k_rot_fused<XT, SYN, OUT, m, q, nw>), g, b, lds, s, X, ldx, n, F.R1, F.R2, F.d1, F.d2, vout, o); }
+#define FR_CASE(m) case m: \
+      if (NW == 4) { if (small) FR_LAUNCH(m, 4, 4) else FR_LAUNCH(m, FR_MAXQ, 4) } \
+      else { if (small) FR_LAUNCH(m, 4, 8) else FR_LAUNCH(m, 8, 8) } \
+      break;
+  switch (MT) {
+    FR_CASE(1) FR_CASE(2) FR_CASE(3) FR_CASE(4) FR_CASE(6) FR_CASE(8)
+    default: break;
+  }
+#undef FR_CASE
+#undef FR_LAUNCH
+}
+
+// the fused kernel applies when d1 <= 128, d2 % 4 == 0, rows are aligned for 4-element
+// loads, a row fits the register prefetch and the operands fit in LDS
+bool rot_fused_ok(const TffDev& F, const void* X, int esz, int64_t ldx) {
+  const int NW = fr_waves(F.d2);
+  const int maxq = NW == 4 ? FR_MAXQ : 8;
+  return F.d1 <= 128 && F.d2 % 4 == 0 && ldx % 4 == 0 &&
+         (reinterpret_cast<uintptr_t>(X) % (4 * esz)) == 0 &&
+         (int64_t)F.d1 * (F.d2 / 4) <= (int64_t)64 * NW * maxq &&
+         fr_lds_floats(F.d1, F.d2) * 4 <= 160 * 1024;
+}
+
 unsigned grid_1d(int64_t total) {
   const int64_t g = (total + TT - 1) / TT;
   return (unsigned)(g < 65536 ? (g > 0 ? g : 1) : 65536);
@@ -415,6 +693,21 @@ hipError_t rotate_rows(const void* X, int xt, int64_t ldx, int64_t n, const TffD
   const int vs2 = (F.d2 % 4 == 0 && al(F.R2, 16)) ? 1 : 0;
   const int vs1 = (F.d1 % 4 == 0 && al(F.R1, 16)) ? 1 : 0;
   prof_begin(s, name);
+  // the pass analyses into the block layout and synthesises into fp32 rows
+  if (rot_fused_ok(F, X, esz, ldx) && synth == (OUT == 0)) {
+    if constexpr (OUT == 0) {
+      launch_rot_fused<float, true, 0>((const float*)X, ldx, n, F, o, s);
+    } else {
+      if (xt == 0)
+        launch_rot_fused<float, false, OUT>((const float*)X, ldx, n, F, o, s);
+      else if (xt == 1)
+        launch_rot_fused<_Float16, false, OUT>((const _Float16*)X, ldx, n, F, o, s);
+      else
+        launch_rot_fused<uint16_t, false, OUT>((const uint16_t*)X, ldx, n, F, o, s);
+    }
+    prof_end(s);
+    return last_launch_error();
+  }
   if (synth) {
     hipLaunchKernelGGL((k_rot_step<float, true, true, 0>), g, b, 0, s, (const float*)X, ldx, n, F.R2, F.d1, F.d2, vx, vs2, ot);
     hipLaunchKernelGGL((k_rot_step<float, false, false, OUT>), g, b, 0, s, (const float*)tmp, F.d, n, F.R1, F.d1, F.d2, vt, vs1, o);
