@@ -579,9 +579,12 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
     constexpr int O = J & 15, C = J >> 4;
     double rnext[8];
     double irn = 0.0;
+    // slots cc below (J + 2) / 16 hold columns before J + 2 in every lane: R is upper
+    // triangular there, so column J + 2 neither reads nor updates them
     if constexpr (J + 2 < GB) {
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) rnext[cc] = Rs[(J + 2) * GB + g + 16 * cc];
+      for (int cc = 0; cc < 8; ++cc)
+        if (cc >= ((J + 2) >> 4)) rnext[cc] = Rs[(J + 2) * GB + g + 16 * cc];
       irn = ird[J + 2];
     }
     double e[GRK];
@@ -597,16 +600,21 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
       }
       e[k] = row_bcast<O>(ek);
     }
+    // slots below C hold columns before J (R_Jc = 0): no update; slot C is updated in
+    // every lane (lanes whose column there is <= J add e R_Jc = 0, or touch the finished
+    // column J, which is not read again)
 #pragma unroll
     for (int cc = 0; cc < 8; ++cc)
+      if (cc >= C)
 #pragma unroll
-      for (int k = 0; k < GRK; ++k) st.y[k][cc] += e[k] * rn[cc];
+        for (int k = 0; k < GRK; ++k) st.y[k][cc] += e[k] * rn[cc];
     // pin the updated values here: otherwise the compiler sinks each update to the column
     // that reads it and keeps every broadcast residual alive
 #pragma unroll
     for (int k = 0; k < GRK; ++k)
 #pragma unroll
-      for (int cc = 0; cc < 8; cc += 2) asm volatile("" : "+v"(st.y[k][cc]), "+v"(st.y[k][cc + 1]));
+      for (int cc = 0; cc < 8; cc += 2)
+        if (cc + 1 >= C) asm volatile("" : "+v"(st.y[k][cc]), "+v"(st.y[k][cc + 1]));
     if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, ird, b, g, maxq, rn1, irj1, rnext, irn);
   }
 }
