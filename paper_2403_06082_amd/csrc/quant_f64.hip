@@ -284,7 +284,9 @@ __device__ __forceinline__ void zinv_step(double (&z)[64], const double (*col)[6
 constexpr int CB = 64, CBP = 65;     // block edge, LDS row pitch (conflict-free fragments)
 
 // acc (a 32 x 32 quadrant of a 64 x 64 product per wave) = sum over k in [j0, k0) of
-// L[r0 + i][k] L[d0 + j][k] for the rows r0 .. r0 + nr and d0 .. d0 + nd (zero beyond)
+// L[r0 + i][k] L[d0 + j][k] for the rows r0 .. r0 + nr and d0 .. d0 + nd (zero beyond).
+// k0 - j0 is a multiple of 16.  The loads of up to four chunks of 16 k are issued
+// together, so the memory latency is paid once per four chunks rather than per chunk.
 __device__ __forceinline__ void chol_left_update(const double* __restrict__ A, int64_t lda,
                                                  int64_t j0, int64_t k0, int64_t r0, int nr,
                                                  int64_t d0, int nd, double (*Ls)[CB + 8],
@@ -294,31 +296,46 @@ __device__ __forceinline__ void chol_left_update(const double* __restrict__ A, i
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
-  for (int64_t kk0 = j0; kk0 < k0; kk0 += 16) {
-    {  // thread t stages row t / 4, 4 consecutive k, of both operands (k-major)
-      const int r = tid >> 2, kq4 = (tid & 3) * 4;
-      const int64_t rd = d0 + min(r, nd - 1), rr = r0 + min(r, nr - 1);
+  // thread t stages row t / 4, 4 consecutive k, of both operands (k-major)
+  const int r = tid >> 2, kq4 = (tid & 3) * 4;
+  const int64_t rd = d0 + min(r, nd - 1), rr = r0 + min(r, nr - 1);
+  const int nch = (int)((k0 - j0) / 16);
+  for (int g0 = 0; g0 < nch; g0 += 4) {
+    double vd[4][4], vs[4][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (g0 + q < nch) {
+        const int64_t kk0 = j0 + 16 * (g0 + q);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          vd[q][c] = (r < nd) ? A[rd * lda + kk0 + kq4 + c] : 0.0;
+          vs[q][c] = (r < nr) ? A[rr * lda + kk0 + kq4 + c] : 0.0;
+        }
+      }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (g0 + q >= nch) break;
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        Ld[kq4 + c][r] = (r < nd) ? A[rd * lda + kk0 + kq4 + c] : 0.0;
-        Ls[kq4 + c][r] = (r < nr) ? A[rr * lda + kk0 + kq4 + c] : 0.0;
+        Ld[kq4 + c][r] = vd[q][c];
+        Ls[kq4 + c][r] = vs[q][c];
       }
+      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < 16; kk += 4) {
+        double af[4], bf[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = Ls[kk + kq][arow + 8 * i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bf[j] = Ld[kk + kq][bcol + 8 * j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
+      }
+      __syncthreads();
     }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < 16; kk += 4) {
-      double af[4], bf[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = Ls[kk + kq][arow + 8 * i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bf[j] = Ld[kk + kq][bcol + 8 * j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-    __syncthreads();
   }
 }
 
