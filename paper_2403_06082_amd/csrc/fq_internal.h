@@ -53,6 +53,9 @@ struct GemmDesc {
   // C + z bsc (element strides; bsa and bsb multiples of 8)
   int batch = 1;
   int64_t bsa = 0, bsb = 0, bsc = 0;
+  // EPI_F32 (asynchronous path): output row r goes to row (r / 2) rowmap + r % 2 when
+  // rowmap > 0 (the frame order of a per-block DFT product)
+  int rowmap = 0;
 };
 
 // Workspace bytes needed by EPI_PARTIAL for an N x N symmetric product split ksplit ways.

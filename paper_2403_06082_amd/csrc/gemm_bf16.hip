@@ -462,6 +462,7 @@ struct AParams {
   int tile0, tcount;    // this launch covers tiles [tile0, tile0 + tcount) (x ksplit)
   int ra, rb;           // row extents the operand loads are clamped to (see gemm_run)
   int64_t bsa, bsb, bsc;  // element strides of A, B and C between the products of a batch
+  int rowmap;             // EPI_F32: row r stored at row (r / 2) rowmap + r % 2 when > 0
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -805,7 +806,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void k_gemm_async(AParams p) {
         } else if (EPI == EPI_TAIL) {
           p.part[((int64_t)split * p.tcount + tloc) * (BM * BN) + rl * BN + cl] = x;
         } else if (EPI == EPI_F32) {
-          if (col < p.N) p.c[bz * p.bsc + (int64_t)row * p.ldc + col] = x;
+          const int64_t orow = p.rowmap > 0 ? (int64_t)(row >> 1) * p.rowmap + (row & 1) : row;
+          if (col < p.N) p.c[bz * p.bsc + orow * p.ldc + col] = x;
         } else if (EPI == EPI_SPLIT) {
           if (col < p.ldc_pad) {
             const bool in = col < p.N;
@@ -1154,6 +1156,7 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     q.ra = d.a_kmajor ? d.M : m8;
     q.rb = d.b_kmajor ? d.N : n8;
     q.bsa = d.bsa; q.bsb = d.bsb; q.bsc = d.bsc;
+    q.rowmap = d.epi == EPI_F32 ? d.rowmap : 0;
     const unsigned nbatch = (unsigned)d.batch;
     prof_begin(s, d.name);
 #define FQ_LAUNCH_ASYNC_E(AMN, BMN, F16, E, G)                                                        \
@@ -1189,7 +1192,7 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     if (ts > ksteps / 4) ts = ksteps / 4;
     const int kps = ts > 0 ? (ksteps + ts - 1) / ts : 0;   // k-steps per slice
     if (kps > 0) ts = (ksteps + kps - 1) / kps;              // no empty slice
-    const bool use_tail = partial && d.batch == 1 && rounds >= 2 && tail <= cus / 2 && ts >= 2 &&
+    const bool use_tail = partial && d.batch == 1 && d.rowmap == 0 && rounds >= 2 && tail <= cus / 2 && ts >= 2 &&
                           (d.epi == EPI_F32 || d.epi == EPI_SPLIT) &&
                           (size_t)tail * ts * BM * BN * sizeof(float) <= gemm_tail_bytes();
     if (use_tail) {
@@ -1216,7 +1219,8 @@ hipError_t gemm_run(const GemmDesc& d, float* partial, hipStream_t s) {
     prof_end(s);
     return last_launch_error();
   }
-  if (d.batch != 1) return hipErrorInvalidValue;   // batches run on the asynchronous path only
+  // batches and row maps run on the asynchronous path only
+  if (d.batch != 1 || d.rowmap != 0) return hipErrorInvalidValue;
   prof_begin(s, d.name);
   bool ok;
   if (d.a_kmajor && d.b_kmajor) {

@@ -16,8 +16,9 @@
 //    (conj(w^((cm+j)s)) times the complex coordinate, realified), and a synthesised row is
 //    v_c F_c^T.  All rows of all blocks are one batch of rho/2 MFMA products (bf16 pairs,
 //    fp32 accumulation), 2 d k multiply-adds per row instead of the dense d k rho.
-// Block c of an analysed row fills frame columns s rho + 2c + e (e = 0, 1); the gathers
-// below move between that order and the block order of the products.
+// Block c of an analysed row fills frame columns s rho + 2c + e (e = 0, 1).  The analysis
+// writes that order straight from the product's epilogue (a row map); on the synthesis
+// side the gathers below move between frame order and the block order of the products.
 #include "fq_internal.h"
 
 #include <cmath>
@@ -251,31 +252,6 @@ __global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm,
     *reinterpret_cast<uint32_t*>(lo + r0) = l0;
     *reinterpret_cast<uint32_t*>(hi + r0 + pk) = h1;
     *reinterpret_cast<uint32_t*>(lo + r0 + pk) = l1;
-  }
-}
-
-// out[(p/2) rho + 2c + (p&1)][t] = O[c][t][p] for p < 2k, t < n (O blocks of n x ldo);
-// 32 x 32 tiles through LDS.  grid (ceil(2k/32) * ceil(n/32), rho/2).
-__global__ __launch_bounds__(TT) void k_gather_t(const float* __restrict__ O, int64_t n,
-                                                 int64_t ldo, int k2, int rho,
-                                                 float* __restrict__ out, int64_t ldout) {
-  __shared__ float tile[32][33];
-  const int c = blockIdx.y;
-  const int npb = (k2 + 31) / 32;
-  const int64_t tb = blockIdx.x / npb;
-  const int pbk = (int)(blockIdx.x - tb * npb);
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  const float* Oc = O + (int64_t)c * n * ldo;
-  for (int q = ty; q < 32; q += 8) {
-    const int64_t t = tb * 32 + q;
-    const int p = pbk * 32 + tx;
-    tile[q][tx] = (t < n && p < k2) ? Oc[t * ldo + p] : 0.f;
-  }
-  __syncthreads();
-  for (int q = ty; q < 32; q += 8) {
-    const int p = pbk * 32 + q;
-    const int64_t t = tb * 32 + tx;
-    if (p < k2 && t < n) out[((int64_t)(p >> 1) * rho + 2 * c + (p & 1)) * ldout + t] = tile[tx][q];
   }
 }
 
@@ -763,23 +739,20 @@ hipError_t tff_rows_analysis_t(const void* X, int xt, int64_t ldx, int64_t n, co
   }
   if ((e = rotate_rows<1>(X, xt, ldx, n, F, false, tmp, o, s, "tffp_rotate_an")) != hipSuccess)
     return e;
-  // O[c] (n x 2k) = Y[:, c pm .. c pm + pm) F_c, all blocks in one batch
+  // block c of every analysed row t, in frame order: out[(p/2) rho + 2c + (p&1)][t] =
+  // sum_j F_c[j][p] Y[t][c pm + j], i.e. F_c^T Y_c^T per block (A = F_c read M-major,
+  // B = Y read K-major), the rows placed in frame order by the epilogue's row map
   GemmDesc d;
-  d.M = (int)n; d.N = (int)g.k2; d.K = (int)g.pm;
-  d.a[0] = Yhi; d.a[1] = Ylo; d.lda = ldy; d.a_kmajor = true;
-  d.b[0] = Fhi; d.b[1] = Flo; d.ldb = g.pk; d.b_kmajor = false;
+  d.M = (int)g.k2; d.N = (int)n; d.K = (int)g.pm;
+  d.a[0] = Fhi; d.a[1] = Flo; d.lda = g.pk; d.a_kmajor = false;
+  d.b[0] = Yhi; d.b[1] = Ylo; d.ldb = ldy; d.b_kmajor = true;
   d.npass = 3;
   d.pa[0] = 0; d.pb[0] = 0; d.pa[1] = 0; d.pb[1] = 1; d.pa[2] = 1; d.pb[2] = 0;
-  d.epi = EPI_F32; d.c = O; d.ldc = g.k2;
-  d.batch = (int)g.nb; d.bsa = g.pm; d.bsb = g.pm * g.pk; d.bsc = n * g.k2;
+  d.epi = EPI_F32; d.c = out; d.ldc = ldout; d.rowmap = (int)F.rho;
+  d.batch = (int)g.nb; d.bsa = g.pm * g.pk; d.bsb = g.pm; d.bsc = 2 * ldout;
   d.name = "tffp_dft_an";
-  if ((e = gemm_run(d, nullptr, s)) != hipSuccess) return e;
-  prof_begin(s, "tffp_gather");
-  const int64_t ntb = (n + 31) / 32;
-  hipLaunchKernelGGL(k_gather_t, dim3((unsigned)(ntb * ((g.k2 + 31) / 32)), (unsigned)g.nb), dim3(TT), 0, s,
-                     (const float*)O, n, g.k2, (int)g.k2, (int)F.rho, out, ldout);
-  prof_end(s);
-  return last_launch_error();
+  (void)O;
+  return gemm_run(d, nullptr, s);
 }
 
 hipError_t tff_gather_rows(const float* M, int64_t ldm, int64_t n, const float* scale,
