@@ -161,18 +161,16 @@ __device__ __forceinline__ double rsqrt_d(double x) {
   return y;
 }
 
-// ---- 64 x 64 diagonal-block factorization, one wave64, lane r holding row r in registers.
-// Column C: the pivot comes from lane C by readlane, every lane scales its entry of column
-// C and publishes it through LDS, then every lane applies the rank-1 update to its later
-// entries.  Ordering for latency: the update of column C is split into the 16 slots right
-// of C (applied first) and the rest; the pivot, scaling and broadcast of column C + 1 are
-// issued between the two, so the LDS round trip of column C + 1 overlaps the bulk of
-// column C's update.  Each slot still receives its updates in column order.
+// ---- 64 x 64 diagonal-block factorization and the inverse of the factor, L_kk and
+// Z = L_kk^-1, by columns: the pivot of column C comes from its row's lane by readlane,
+// the column is scaled and published through LDS, and every later column receives the
+// rank-1 update (a[k] -= L_rC L_kC).  Row C of Z is finished with column C (z_C /= L_CC)
+// and published beside it; later rows receive z_k -= L_kC z_C.
 
 // pin the listed slots: without it the compiler sinks updates into later columns and keeps
 // every broadcast value alive
-template <int LO, int HI>
-__device__ __forceinline__ void pin_slots(double (&a)[64]) {
+template <int LO, int HI, int N>
+__device__ __forceinline__ void pin_slots(double (&a)[N]) {
   if constexpr (LO < HI) {
     if constexpr (HI - LO >= 4) {
       asm volatile("" : "+v"(a[LO]), "+v"(a[LO + 1]), "+v"(a[LO + 2]), "+v"(a[LO + 3]));
@@ -184,84 +182,93 @@ __device__ __forceinline__ void pin_slots(double (&a)[64]) {
   }
 }
 
-// a[k] -= a[C] * v[k - LO] for LO <= k < HI, k > C (v: broadcast values of column C)
-template <int C, int LO, int HI, int NV>
-__device__ __forceinline__ void pf_update(double (&a)[64], const double2 (&v)[NV]) {
-  if constexpr (LO < HI) {
-    const double lc = a[C];
-#pragma unroll
-    for (int k = LO; k < HI; ++k)
-      if (k > C) a[k] -= lc * (((k - LO) & 1) ? v[(k - LO) >> 1].y : v[(k - LO) >> 1].x);
-    pin_slots<LO, HI>(a);
-  }
-}
-
-template <int LO, int HI, int NV>
-__device__ __forceinline__ void pf_read(const double* colC, double2 (&v)[NV]) {
-  const double2* cp = reinterpret_cast<const double2*>(colC + LO);
-#pragma unroll
-  for (int q = 0; q < (HI - LO) / 2; ++q) v[q] = cp[q];
-}
-
-// pivot of column C, scaled column entry of this lane, broadcast
-template <int C>
-__device__ __forceinline__ void pf_scale(double (&a)[64], double* colC, double* invd, int r,
-                                         bool& notpd) {
-  double piv = bcast_lane(a[C], C);
+// The columns are spread over the four waves of the work-group: wave W
+// holds columns [16 W, 16 W + 16) of the block (lane r = row r) and rows [16 W, 16 W + 16)
+// of Z = L^{-1} (lane j = column j).  Column C is published by its owner wave (the
+// scaled column of L, row C of Z scaled by 1 / L_CC) before the barrier of step C; after
+// it every wave applies column C to its own columns of the block and its own rows of Z.
+// The owner of column C + 1 applies column C to that column first and publishes it, then
+// the rest.  Each entry receives its updates in column order.
+template <int W, int C>
+__device__ __forceinline__ void f4_publish(double (&a)[16], double (&z)[16], int r,
+                                           double* colC, double* zrowC, double* invd,
+                                           bool& notpd) {
+  constexpr int S = C - 16 * W;
+  double piv = bcast_lane(a[S], C);
   if (!(piv > 0.0)) {
     notpd = true;
     piv = 1.0;
   }
   const double inv = rsqrt_d(piv);
-  a[C] = (r == C) ? piv * inv : a[C] * inv;
-  colC[r] = a[C];
-  if (r == C) invd[C] = inv;       // 1 / L_CC
+  a[S] = (r == C) ? piv * inv : a[S] * inv;
+  colC[r] = a[S];
+  z[S] *= inv;
+  zrowC[r] = z[S];
+  if (r == C) invd[C] = inv;
 }
 
-// entering: column C scaled and broadcast in col[C & 1], visible to the wave
-template <int C>
-__device__ __forceinline__ void pf_step(double (&a)[64], double (*col)[64], double* invd, int r,
+template <int W, int C>
+__device__ __forceinline__ void f4_step(double (&a)[16], double (&z)[16], int r,
+                                        double (*col)[64], double (*zrow)[64], double* invd,
                                         bool& notpd) {
-  constexpr int G1 = (C + 1) & ~1;
-  constexpr int E1 = G1 + 16 < 64 ? G1 + 16 : 64;
-  constexpr int N1 = (E1 - G1) / 2 > 0 ? (E1 - G1) / 2 : 1;
-  constexpr int NB = (64 - E1) / 2 > 0 ? (64 - E1) / 2 : 1;
-  double2 v1[N1], vb[NB];
-  pf_read<G1, E1>(col[C & 1], v1);
-  pf_update<C, G1, E1>(a, v1);
-  pf_read<E1, 64>(col[C & 1], vb);
-  if constexpr (C + 1 < 64) pf_scale<C + 1>(a, col[(C + 1) & 1], invd, r, notpd);
-  pf_update<C, E1, 64>(a, vb);
+  constexpr int LO = 16 * W, HI = LO + 16;
+  constexpr int K0 = (C + 1 > LO) ? C + 1 : LO;
+  if constexpr (K0 < HI) {
+    constexpr int G = K0 & ~1;
+    constexpr int NV = (HI - G) / 2;
+    const double lrc = col[C & 1][r];
+    const double zc = zrow[C & 1][r];
+    double2 v[NV];
+    const double2* cp = reinterpret_cast<const double2*>(col[C & 1] + G);
+#pragma unroll
+    for (int q = 0; q < NV; ++q) v[q] = cp[q];
+    constexpr bool NEXT = (C + 1 < 64) && ((C + 1) / 16 == W);
+    if constexpr (NEXT) {
+      constexpr int k = C + 1;
+      const double lk = ((k - G) & 1) ? v[(k - G) >> 1].y : v[(k - G) >> 1].x;
+      a[k - LO] -= lrc * lk;
+      z[k - LO] -= zc * lk;
+      f4_publish<W, C + 1>(a, z, r, col[(C + 1) & 1], zrow[(C + 1) & 1], invd, notpd);
+    }
+#pragma unroll
+    for (int k = G; k < HI; ++k) {
+      if (k > C + (NEXT ? 1 : 0)) {
+        const double lk = ((k - G) & 1) ? v[(k - G) >> 1].y : v[(k - G) >> 1].x;
+        a[k - LO] -= lrc * lk;
+        z[k - LO] -= zc * lk;
+      }
+    }
+    pin_slots<0, 16>(a);
+    pin_slots<0, 16>(z);
+  }
   if constexpr (C + 1 < 64) {
     __syncthreads();
-    pf_step<C + 1>(a, col, invd, r, notpd);
+    f4_step<W, C + 1>(a, z, r, col, zrow, invd, notpd);
   }
 }
 
-// ---- inverse of the factor, Z = L^{-1}, formed by a second wave while the first factors:
-// lane j carries column j of Z, z = e_j initially; for C = 0..63, once column C of L and
-// 1 / L_CC are published: z_C /= L_CC, then z_k -= L_kC z_C for k > C.  It reads the same
-// broadcast buffer as the factorization and meets it at the same barrier per column, so
-// the buffer of column C is not reused before both waves are done with it.
-template <int C>
-__device__ __forceinline__ void zinv_step(double (&z)[64], const double (*col)[64],
-                                          const double* invd) {
-  if constexpr (C < 64) {
-    __syncthreads();                       // column C and 1 / L_CC are visible
-    z[C] *= invd[C];
-    constexpr int G = (C + 1) & ~1;
-    constexpr int NV = (64 - G) / 2 > 0 ? (64 - G) / 2 : 1;
-    if constexpr (G < 64) {
-      double2 v[NV];
-      pf_read<G, 64>(col[C & 1], v);
-      const double zc = z[C];
+// Dg: the block (lower part, identity beyond kb); writes L (zero above the diagonal) back
+// to Dg and Z to Zs[k][c]; true when a pivot was not positive
+template <int W>
+__device__ __forceinline__ bool f4_run(double (*Dg)[65], double (*Zs)[65], int r,
+                                       double (*col)[64], double (*zrow)[64], double* invd) {
+  constexpr int LO = 16 * W;
+  double a[16], z[16];
 #pragma unroll
-      for (int k = G; k < 64; ++k)
-        if (k > C) z[k] -= zc * (((k - G) & 1) ? v[(k - G) >> 1].y : v[(k - G) >> 1].x);
-      pin_slots<G, 64>(z);
-    }
-    zinv_step<C + 1>(z, col, invd);
+  for (int i = 0; i < 16; ++i) {
+    a[i] = Dg[r][LO + i];
+    z[i] = (LO + i == r) ? 1.0 : 0.0;
   }
+  bool notpd = false;
+  if constexpr (W == 0) f4_publish<0, 0>(a, z, r, col[0], zrow[0], invd, notpd);
+  __syncthreads();
+  f4_step<W, 0>(a, z, r, col, zrow, invd, notpd);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    Dg[r][LO + i] = (LO + i <= r) ? a[i] : 0.0;
+    Zs[LO + i][r] = z[i];
+  }
+  return notpd;
 }
 
 // ---- one block column of the factorization in one launch (left-looking inside a panel).
@@ -271,8 +278,8 @@ __device__ __forceinline__ void zinv_step(double (&z)[64], const double (*col)[6
 // (slab q to work-group 1 + q mod (gridDim.x - 1)).  Each work-group of 4 waves:
 //  1. brings the diagonal block up to date with the panel's earlier columns [j0, k0)
 //     (left-looking, fp64 MFMA, a 32 x 32 quadrant per wave):  B -= L[k0:, j0:k0] L[k0:, j0:k0]^T
-//  2. factors it (wave 0, one row per lane) while wave 1 forms its inverse, redundantly in
-//     every work-group, so that no work-group waits for another;
+//  2. factors it and forms its inverse, the columns spread over the four waves (one row
+//     per lane), redundantly in every work-group, so that no work-group waits for another;
 //  3. work-group 0 stores L_kk to the slot Lout (every work-group reads the diagonal block
 //     of A, so it must stay unchanged during this launch) and moves the previous block's
 //     factor from its slot Lprev into A (rows this launch does not read); every other
@@ -350,6 +357,7 @@ __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int6
   __shared__ double Zs[CB][CBP];                       // L_kk^-1 (Zs[k][c] = (L^-1)[k][c])
   __shared__ double Ls[16][CB + 8], Ld[16][CB + 8];    // update staging, k-major
   __shared__ __attribute__((aligned(16))) double col[2][64];     // broadcast column of L
+  __shared__ __attribute__((aligned(16))) double zrow[2][64];    // broadcast row of L^-1
   __shared__ double invd[64];                                    // 1 / L_jj
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int w = blockIdx.x;
@@ -373,29 +381,14 @@ __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int6
     }
   __syncthreads();
 
-  // ---- 2. factor (wave 0) and inverse (wave 1); waves 2, 3 meet the same 64 barriers
-  if (wave == 0) {
-    const int r = lane;
-    double a[64];
-#pragma unroll
-    for (int c = 0; c < 64; ++c) a[c] = Dg[r][c];
-    bool notpd = false;
-    pf_scale<0>(a, col[0], invd, r, notpd);
-    __syncthreads();                       // matches the first barrier of the inverse
-    pf_step<0>(a, col, invd, r, notpd);
-    if (notpd && r == 0 && w == 0) flags[0] = 1;
-#pragma unroll
-    for (int c = 0; c < 64; ++c) Dg[r][c] = (c <= r) ? a[c] : 0.0;
-  } else if (wave == 1) {
-    const int r = lane;
-    double z[64];
-#pragma unroll
-    for (int k = 0; k < 64; ++k) z[k] = (k == r) ? 1.0 : 0.0;
-    zinv_step<0>(z, col, invd);
-#pragma unroll
-    for (int k = 0; k < 64; ++k) Zs[k][r] = z[k];
-  } else {
-    for (int i = 0; i < 64; ++i) __syncthreads();
+  // ---- 2. factor and inverse, the columns spread over the four waves
+  {
+    bool notpd;
+    if (wave == 0) notpd = f4_run<0>(Dg, Zs, lane, col, zrow, invd);
+    else if (wave == 1) notpd = f4_run<1>(Dg, Zs, lane, col, zrow, invd);
+    else if (wave == 2) notpd = f4_run<2>(Dg, Zs, lane, col, zrow, invd);
+    else notpd = f4_run<3>(Dg, Zs, lane, col, zrow, invd);
+    if (notpd && lane == 0 && w == 0) flags[0] = 1;
   }
   __syncthreads();
 
