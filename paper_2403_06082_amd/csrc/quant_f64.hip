@@ -346,6 +346,70 @@ __device__ __forceinline__ void chol_left_update(const double* __restrict__ A, i
   }
 }
 
+// chol_left_update for two row sets sharing the second operand: accD = sum L[d][k] L[d][k]
+// (the diagonal block's rows d0 .. d0 + nd) and accS = sum L[s][k] L[d][k] (a slab's rows
+// r0 .. r0 + nr; nr = 0: accS stays 0), one pass over the columns [j0, k0).
+__device__ __forceinline__ void chol_left_update2(const double* __restrict__ A, int64_t lda,
+                                                  int64_t j0, int64_t k0, int64_t r0, int nr,
+                                                  int64_t d0, int nd, double (*Ls)[CB + 8],
+                                                  double (*Ld)[CB + 8], double (&accD)[4][4],
+                                                  double (&accS)[4][4], int tid, int arow,
+                                                  int bcol, int kq) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      accD[i][j] = 0.0;
+      accS[i][j] = 0.0;
+    }
+  const int r = tid >> 2, kq4 = (tid & 3) * 4;
+  // every address in range, also for an empty slab (nr = 0: the diagonal rows)
+  const int64_t rd = d0 + min(r, nd - 1), rr = nr > 0 ? r0 + min(r, nr - 1) : rd;
+  const int nch = (int)((k0 - j0) / 16);
+  for (int g0 = 0; g0 < nch; g0 += 4) {
+    double vd[4][4], vs[4][4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (g0 + q < nch) {
+        const int64_t kk0 = j0 + 16 * (g0 + q);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          vd[q][c] = (r < nd) ? A[rd * lda + kk0 + kq4 + c] : 0.0;
+          vs[q][c] = (r < nr) ? A[rr * lda + kk0 + kq4 + c] : 0.0;
+        }
+      }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (g0 + q >= nch) break;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        Ld[kq4 + c][r] = vd[q][c];
+        Ls[kq4 + c][r] = vs[q][c];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int kk = 0; kk < 16; kk += 4) {
+        double ad[4], as[4], bf[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          ad[i] = Ld[kk + kq][arow + 8 * i];
+          as[i] = Ls[kk + kq][arow + 8 * i];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bf[j] = Ld[kk + kq][bcol + 8 * j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            accD[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(ad[i], bf[j], accD[i][j], 0, 0, 0);
+            accS[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(as[i], bf[j], accS[i][j], 0, 0, 0);
+          }
+      }
+      __syncthreads();
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int64_t lda, int64_t K,
                                                     int64_t j0, int64_t k0, int kb,
                                                     double* __restrict__ Lout,
@@ -367,18 +431,39 @@ __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int6
   const int bcol = wn * 32 + 4 * bj + q4;
   const int r0 = wm * 32 + 4 * bi + kq, c0 = wn * 32 + 4 * bj + q4;   // accumulator origin
   double acc[4][4];
+  const int64_t below = K - k0 - kb;
+  const int64_t nslab = (below + CB - 1) / CB;
+  // the first slab of this work-group (work-groups 1 ..): brought up to date in the same
+  // pass as the diagonal block, its values fetched with the block's, before the factor
+  const int64_t rs1 = k0 + kb + CB * (int64_t)(w - 1);
+  const int nr1 = (w >= 1 && w - 1 < nslab) ? (int)min<int64_t>(CB, K - rs1) : 0;
 
   // ---- 1. the diagonal block, updated, as the factorization expects it: lower part,
-  // identity rows and columns beyond kb, zero above the diagonal
-  chol_left_update(A, lda, j0, k0, k0, kb, k0, kb, Ls, Ld, acc, tid, arow, bcol, kq);
+  // identity rows and columns beyond kb, zero above the diagonal; the first slab's rows of
+  // the block column, updated, into Sg
+  {
+    double dv[4][4], sv[4][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = r0 + 8 * i, c = c0 + 8 * j;
-      const double a = A[(k0 + min(r, kb - 1)) * lda + k0 + min(c, kb - 1)];
-      Dg[r][c] = (r < kb && c <= r) ? a - acc[i][j] : (r == c ? 1.0 : 0.0);
-    }
+      for (int j = 0; j < 4; ++j) {
+        const int r = r0 + 8 * i, c = c0 + 8 * j;
+        dv[i][j] = A[(k0 + min(r, kb - 1)) * lda + k0 + min(c, kb - 1)];
+        // (no slab: a diagonal row, so that the address stays in range)
+        const int64_t srow = nr1 > 0 ? rs1 + min(r, nr1 - 1) : k0 + min(r, kb - 1);
+        sv[i][j] = A[srow * lda + k0 + min(c, kb - 1)];
+      }
+    double accS[4][4];
+    chol_left_update2(A, lda, j0, k0, rs1, nr1, k0, kb, Ls, Ld, acc, accS, tid, arow, bcol, kq);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = r0 + 8 * i, c = c0 + 8 * j;
+        Dg[r][c] = (r < kb && c <= r) ? dv[i][j] - acc[i][j] : (r == c ? 1.0 : 0.0);
+        Sg[r][c] = (r < nr1 && c < kb) ? sv[i][j] - accS[i][j] : 0.0;
+      }
+  }
   __syncthreads();
 
   // ---- 2. factor and inverse, the columns spread over the four waves
@@ -401,21 +486,21 @@ __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int6
     }
     return;
   }
-  const int64_t below = K - k0 - kb;
-  const int64_t nslab = (below + CB - 1) / CB;
   for (int64_t q = w - 1; q < nslab; q += gridDim.x - 1) {
     const int64_t rs = k0 + kb + CB * q;
     const int nr = (int)min<int64_t>(CB, K - rs);
-    chol_left_update(A, lda, j0, k0, rs, nr, k0, kb, Ls, Ld, acc, tid, arow, bcol, kq);
+    if (q != w - 1) {     // the first slab's rows are in Sg already
+      chol_left_update(A, lda, j0, k0, rs, nr, k0, kb, Ls, Ld, acc, tid, arow, bcol, kq);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = r0 + 8 * i, c = c0 + 8 * j;
-        const double b = A[(rs + min(r, nr - 1)) * lda + k0 + min(c, kb - 1)];
-        Sg[r][c] = (r < nr && c < kb) ? b - acc[i][j] : 0.0;
-      }
-    __syncthreads();
+        for (int j = 0; j < 4; ++j) {
+          const int r = r0 + 8 * i, c = c0 + 8 * j;
+          const double b = A[(rs + min(r, nr - 1)) * lda + k0 + min(c, kb - 1)];
+          Sg[r][c] = (r < nr && c < kb) ? b - acc[i][j] : 0.0;
+        }
+      __syncthreads();
+    }
     // X[r][c] = sum_k Sg[r][k] Zs[c][k]  (A = Sg, B(k, c) = Zs[c][k])
 #pragma unroll
     for (int i = 0; i < 4; ++i)
