@@ -626,6 +626,30 @@ def wiener_bench(fq, torch, bufs, K_out, K_in, steps):
             "kernels": kern}
 
 
+def prepare_bench(fq, torch, bufs, wl, K_out, K_in, steps):
+    """fq_quantize_prepare on the headline pass's H~ (damping, Cholesky factor, R and its
+    diagonal), timed with HIP events on the launch stream with nothing beside it: the
+    factorization's trailing updates then run on the library's auxiliary stream beside the
+    panel chain, so this is the critical path that the kernel timers (which serialize every
+    launch on one stream) overstate."""
+    stream = torch.cuda.current_stream()
+
+    def call():
+        fq.fq_quantize_prepare(bufs.Ht, K_out, bufs.ws_q, block=wl.block, damp=wl.damp,
+                               stream=stream)
+
+    us = _time_calls(torch, call, stream, max(steps, 5))
+    kern = _kernel_us(fq, torch, call, ("chol_block", "chol_syrk", "q_"), max(steps, 5))
+    flops = K_in ** 3 / 3.0
+    print(f"[bench] prepare (factorization): {us / 1e3:.2f} ms/call", file=sys.stderr,
+          flush=True)
+    return {"op": "fq_quantize_prepare: damped H~, its Cholesky factor and R (H~ = R R^T), "
+                  "trailing updates on the auxiliary stream", "K_in": K_in,
+            "ms_per_call": round(us / 1e3, 3),
+            "chol_TFLOP/s_wall": round(flops / (us * 1e-6) / 1e12, 2),
+            "kernels_serialized": kern}
+
+
 def cpu_inference_baseline(host, codes, scale, zero, wl, li, sample_rows=512):
     """The oracle's layer output for one token on `sample_rows` sampled output channels;
     its row-proportional part is scaled to all channels, the dequantization counted once."""
@@ -971,6 +995,7 @@ def main():
     out["grid_variants"] = grid_variants_bench(torch, dev, wl, li, L, K_out, K_in, n, args.steps,
                                                frames=frames)
     out["wiener_filter"] = wiener_bench(fq, torch, bufs, K_out, K_in, args.steps)
+    out["quantize_prepare"] = prepare_bench(fq, torch, bufs, wl, K_out, K_in, args.steps)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on the whole pass", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, li, host)
