@@ -1342,10 +1342,12 @@ hipError_t q_cholesky(double* A, int64_t K, double* Lslots, int* flags, hipStrea
       pending = false;
     }
     // (a): rows j1.., columns [j1, j2) (a full rectangle: the upper triangle of the next
-    // diagonal block is never read)
+    // diagonal block is never read), on 32 x 32 tiles while 64 x 64 ones would leave
+    // compute units idle (it is on the chain of dependent launches)
     const double* Pa = A + j1 * K + j0;
+    const int tile_a = ((rest + 63) / 64) * ((jb1 + 63) / 64) < 256 ? 32 : 64;
     e = dgemm(rest, jb1, jb, -1.0, 1.0, Pa, K, Pa, K, true, A + j1 * K + j1, K, false, s,
-              "chol_syrk", 64);
+              "chol_syrk", tile_a);
     if (e != hipSuccess) return e;
     if (rest2 <= 0) continue;
     // (b): rows j2.., columns [j2, K), tiles on or below the diagonal (the LDS-ring kernel
@@ -1446,12 +1448,13 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
     prof_end(s);
     return last_launch_error();
   }
-  const int DT = tile == 128 ? 128 : 64;
+  const int DT = tile == 128 ? 128 : tile == 32 ? 32 : 64;
   const int tiles_m = (int)((M + DT - 1) / DT), tiles_n = (int)((N + DT - 1) / DT);
   p.tiles_n = tiles_n;
   const int64_t grid = lower_only ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
   prof_begin(s, name);
   if (DT == 128) hipLaunchKernelGGL(k_dgemm<128>, dim3((unsigned)grid), dim3(256), 0, s, p);
+  else if (DT == 32) hipLaunchKernelGGL(k_dgemm<32>, dim3((unsigned)grid), dim3(256), 0, s, p);
   else hipLaunchKernelGGL(k_dgemm<64>, dim3((unsigned)grid), dim3(256), 0, s, p);
   prof_end(s);
   return last_launch_error();
