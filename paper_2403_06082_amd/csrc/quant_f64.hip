@@ -437,6 +437,12 @@ __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int6
   // pass as the diagonal block, its values fetched with the block's, before the factor
   const int64_t rs1 = k0 + kb + CB * (int64_t)(w - 1);
   const int nr1 = (w >= 1 && w - 1 < nslab) ? (int)min<int64_t>(CB, K - rs1) : 0;
+  // work-group 0: the previous block's factor, fetched now and stored at the end
+  double lp[CB * CB / 256];
+  if (w == 0 && Lprev) {
+#pragma unroll
+    for (int q = 0; q < CB * CB / 256; ++q) lp[q] = Lprev[tid + 256 * q];
+  }
 
   // ---- 1. the diagonal block, updated, as the factorization expects it: lower part,
   // identity rows and columns beyond kb, zero above the diagonal; the first slab's rows of
@@ -479,10 +485,11 @@ __global__ __launch_bounds__(256) void k_chol_block(double* __restrict__ A, int6
 
   // ---- 3. L_kk to its slot and the previous factor into A, or the slabs' rows of L
   if (w == 0) {
-    for (int e = tid; e < CB * CB; e += 256) {
-      const int i = e >> 6, c = e & 63;
+#pragma unroll
+    for (int q = 0; q < CB * CB / 256; ++q) {
+      const int e = tid + 256 * q, i = e >> 6, c = e & 63;
       Lout[e] = Dg[i][c];
-      if (Lprev && i < kpb && c < kpb) A[(kp0 + i) * lda + kp0 + c] = Lprev[e];
+      if (Lprev && i < kpb && c < kpb) A[(kp0 + i) * lda + kp0 + c] = lp[q];
     }
     return;
   }
