@@ -18,7 +18,8 @@
  * fq_quantize_frames is also available as its two phases, fq_quantize_prepare (the part
  * that reads H~ only: damping and the Cholesky factor) and fq_quantize_apply (the part
  * that reads D), so that the factorization can run on one stream while D is still being
- * formed on another.
+ * formed on another; apply in turn splits into fq_quantize_grid (D only: clip and grid,
+ * which can also run beside the factorization) and fq_quantize_round (the rounding).
  *
  * Conventions shared by every call
  *  - Matrices are row-major.  Every array argument is a DEVICE pointer owned by the
@@ -26,9 +27,9 @@
  *    space takes a caller-provided workspace `ws` of at least the size returned by its
  *    *_workspace_bytes query (16-byte aligned).
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are stream-ordered and
- *    asynchronous, except fq_quantize_frames and fq_quantize_apply, which synchronize
- *    `stream` once at their end to report the positive-definiteness and finiteness
- *    checks.
+ *    asynchronous, except fq_quantize_frames, fq_quantize_apply and fq_quantize_round,
+ *    which synchronize `stream` once at their end to report the positive-definiteness
+ *    and finiteness checks.
  *  - Arguments are validated before anything is launched; on failure the call returns
  *    FQ_ERR_INVALID_ARG (or FQ_ERR_UNSUPPORTED / FQ_ERR_WORKSPACE_TOO_SMALL) and
  *    fq_last_error() describes the problem.  No exception crosses the boundary.
@@ -142,6 +143,29 @@ fq_status fq_quantize_prepare(void* stream, const float* Ht, int64_t K_out, int6
 fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t K_in,
                             int bits, int block, double clip_sigmas, uint32_t* codes,
                             float* scale, float* zero, void* ws, size_t ws_bytes);
+
+/*
+ * fq_quantize_apply in its two parts, on the same workspace (apply = grid, then round;
+ * the outputs are bit-identical).  The grid reads D only, so it can run beside
+ * fq_quantize_prepare.
+ *   fq_quantize_grid   reads D only: the clip bounds from D's moments (step 1 above), the
+ *                      per-row grid (step 2, writes scale and zero) and the working copy
+ *                      of the clipped D, into ws.  Asynchronous; its check (D finite) is
+ *                      reported by the following fq_quantize_round.  It writes no part of
+ *                      ws that fq_quantize_prepare reads or writes, so the two may run on
+ *                      different streams at the same time.
+ *   fq_quantize_round  the column-sequential rounding with error feedback (step 3, Alg. 1
+ *                      step 4) and the packing into `codes`; then synchronizes `stream`
+ *                      and reports the checks of prepare and grid.  It must be ordered
+ *                      after both (same stream or events), with the same D, K_out, K_in,
+ *                      bits, block and workspace.
+ * Errors: as for fq_quantize_apply (clip_sigmas and scale/zero belong to the grid).
+ */
+fq_status fq_quantize_grid(void* stream, const float* D, int64_t K_out, int64_t K_in, int bits,
+                           int block, double clip_sigmas, float* scale, float* zero, void* ws,
+                           size_t ws_bytes);
+fq_status fq_quantize_round(void* stream, const float* D, int64_t K_out, int64_t K_in, int bits,
+                            int block, uint32_t* codes, void* ws, size_t ws_bytes);
 
 /*
  * A stream for the work a caller runs beside fq_quantize_prepare (the analysis of W, which

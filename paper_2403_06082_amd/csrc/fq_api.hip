@@ -502,12 +502,14 @@ size_t fq_quantize_frames_workspace_bytes(int64_t K_out, int64_t K_in, int block
   return quant_layout(K_out, K_in, block, nullptr, nullptr);
 }
 
-// the H~ phase: dead columns, damping, the reversed Cholesky factor R (no sync)
+// the H~ phase: dead columns, damping, the reversed Cholesky factor R (no sync).  It
+// touches only its own parts of the workspace (A, R, its diagonal, the dead mask,
+// lambda, flags[0..1]), so the D phase's first part may run beside it on another stream.
 static fq_status quantize_prepare(hipStream_t s, const float* Ht, int64_t K_in, double damp,
                                   QuantScratch& Q) {
   hipError_t e;
   prof_begin(s, "q_init");
-  hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, Q.flags, 4);
+  hipLaunchKernelGGL(k_zero_i32, dim3(1), dim3(64), 0, s, Q.flags, 2);
   prof_end(s);
   if ((e = q_hdiag_build(Ht, K_in, damp, Q, s)) != hipSuccess) return hip_fail(e, "hessian prep");
   if ((e = q_cholesky(Q.A, K_in, Q.lslots, Q.flags, s)) != hipSuccess) return hip_fail(e, "cholesky");
@@ -515,10 +517,12 @@ static fq_status quantize_prepare(hipStream_t s, const float* Ht, int64_t K_in, 
   return FQ_OK;
 }
 
-// the D phase: clip, grid, rounding with error feedback, packing; then sync and checks
-static fq_status quantize_apply(hipStream_t s, const float* D, int64_t K_out, int64_t K_in,
-                                int bits, int block, double clip_sigmas, uint32_t* codes,
-                                float* scale, float* zero, QuantScratch& Q) {
+// the D phase, first part: moments, clip, per-row grid, and the working matrix Y = the
+// clipped D (no sync).  Its own parts of the workspace: Y, the moment partials,
+// scal[0..3], scale64, zero64, flags[2]; it reads nothing the H~ phase writes.
+static fq_status quantize_grid(hipStream_t s, const float* D, int64_t K_out, int64_t K_in,
+                               int bits, double clip_sigmas, float* scale, float* zero,
+                               QuantScratch& Q) {
   hipError_t e;
   // this call's own D check (the H~ checks of the prepare phase stay in flags[0..1])
   prof_begin(s, "q_init");
@@ -526,6 +530,14 @@ static fq_status quantize_apply(hipStream_t s, const float* D, int64_t K_out, in
   prof_end(s);
   if ((e = q_stats(D, K_out, K_in, clip_sigmas, Q, s)) != hipSuccess) return hip_fail(e, "stats");
   if ((e = q_clip_grid(D, K_out, K_in, bits, Q, scale, zero, s)) != hipSuccess) return hip_fail(e, "clip/grid");
+  return FQ_OK;
+}
+
+// the D phase, second part (after both the H~ phase and the first part): rounding with
+// error feedback, packing; then sync and checks
+static fq_status quantize_round(hipStream_t s, const float* D, int64_t K_out, int64_t K_in,
+                                int bits, int block, uint32_t* codes, QuantScratch& Q) {
+  hipError_t e;
   const int64_t ldr = res_width(K_in, block);
   const int64_t cw = chunk_width(block), sw = span_width(block);
   for (int64_t s1 = 0; s1 < K_in; s1 += sw) {
@@ -591,7 +603,9 @@ fq_status fq_quantize_frames(void* stream, const float* D, const float* Ht, int6
   hipStream_t s = (hipStream_t)stream;
   QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
   if ((st = quantize_prepare(s, Ht, K_in, damp, Q)) != FQ_OK) return st;
-  return quantize_apply(s, D, K_out, K_in, bits, block, clip_sigmas, codes, scale, zero, Q);
+  if ((st = quantize_grid(s, D, K_out, K_in, bits, clip_sigmas, scale, zero, Q)) != FQ_OK)
+    return st;
+  return quantize_round(s, D, K_out, K_in, bits, block, codes, Q);
 }
 
 fq_status fq_quantize_prepare(void* stream, const float* Ht, int64_t K_out, int64_t K_in,
@@ -619,8 +633,38 @@ fq_status fq_quantize_apply(void* stream, const float* D, int64_t K_out, int64_t
   fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
   if (st != FQ_OK) return st;
   QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
-  return quantize_apply((hipStream_t)stream, D, K_out, K_in, bits, block, clip_sigmas, codes,
-                        scale, zero, Q);
+  if ((st = quantize_grid((hipStream_t)stream, D, K_out, K_in, bits, clip_sigmas, scale, zero,
+                          Q)) != FQ_OK)
+    return st;
+  return quantize_round((hipStream_t)stream, D, K_out, K_in, bits, block, codes, Q);
+}
+
+fq_status fq_quantize_grid(void* stream, const float* D, int64_t K_out, int64_t K_in, int bits,
+                           int block, double clip_sigmas, float* scale, float* zero, void* ws,
+                           size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (!(clip_sigmas > 0.0)) return fail(FQ_ERR_INVALID_ARG, "clip_sigmas must be > 0 (+inf disables the clip)");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!D || !scale || !zero) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  return quantize_grid((hipStream_t)stream, D, K_out, K_in, bits, clip_sigmas, scale, zero, Q);
+}
+
+fq_status fq_quantize_round(void* stream, const float* D, int64_t K_out, int64_t K_in, int bits,
+                            int block, uint32_t* codes, void* ws, size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!D || !codes) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  return quantize_round((hipStream_t)stream, D, K_out, K_in, bits, block, codes, Q);
 }
 
 // A stream kept off the first reserve_cus compute units (bit c of the mask = unit c).

@@ -177,9 +177,9 @@ hipError_t frame_apply(const void* X, int xt, int64_t n, int64_t ldx, int64_t d_
 
 // ---------------------------------------------------------------- fp64 path
 struct QuantScratch {
-  double* Y;          // K_out x K_in working matrix (scaled pre-rounding values)
+  double* Y;          // K_out x K_in working matrix (pre-rounding values)
   double* A;          // K_in x K_in: reversed damped H~, factored in place (lower)
-  double* R;          // K_in x K_in: upper factor, H~_damped = R R^T
+  double* R;          // K_in x K_in: R' = R diag(R)^-1, R the upper factor (H~_damped = R R^T)
   double* res;        // K_out x block residuals D - D^ of the current block
   uint8_t* codes8;    // K_out x K_in codes
   double* red;        // reduction partials

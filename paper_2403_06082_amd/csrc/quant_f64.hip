@@ -545,32 +545,39 @@ __global__ __launch_bounds__(256) void k_chol_last(double* __restrict__ A, int64
   }
 }
 
-// R[i][j] = M[K-1-i][K-1-j] (upper), rdiag / inv_rdiag.
+// The upper factor of the damped H~ = R R^T is R[i][j] = M[K-1-i][K-1-j] (M the lower
+// factor of the reversed matrix).  The rounding works with its columns scaled to a unit
+// diagonal, R' = R diag(R)^-1: with Y = (clipped D) diag(R), OPTQ's error feedback y_c +=
+// e_J R_Jc becomes u_c += e_J R'_Jc on u = y / R_cc, the unscaled pre-rounding values, so
+// the rounding reads u_J directly and the working matrix starts as the clipped D.
+// rdiag[j] = R_jj and inv_rdiag[j] = 1 / R_jj first, then R' row by row.
+__global__ __launch_bounds__(256) void k_rev_diag(const double* __restrict__ M, int64_t K,
+                                                  double* __restrict__ rdiag,
+                                                  double* __restrict__ inv_rdiag) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j < K) {
+    const double v = M[(K - 1 - j) * K + (K - 1 - j)];
+    rdiag[j] = v;
+    inv_rdiag[j] = 1.0 / v;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_reverse_upper(const double* __restrict__ M, int64_t K,
-                                                       double* __restrict__ R,
-                                                       double* __restrict__ rdiag,
-                                                       double* __restrict__ inv_rdiag) {
-  const int64_t total = K * K;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * 256) {
-    const int64_t i = e / K, j = e - i * K;
-    double v = 0.0;
-    if (i <= j) v = M[(K - 1 - i) * K + (K - 1 - j)];
-    R[e] = v;
-    if (i == j) {
-      rdiag[i] = v;
-      inv_rdiag[i] = 1.0 / v;
-    }
+                                                       const double* __restrict__ inv_rdiag,
+                                                       double* __restrict__ R) {
+  for (int64_t i = blockIdx.x; i < K; i += gridDim.x) {
+    const double* mrow = M + (K - 1 - i) * K + (K - 1);     // M[K-1-i][K-1-j] = mrow[-j]
+    double* rrow = R + i * K;
+    for (int64_t j = threadIdx.x; j < K; j += 256)
+      rrow[j] = j < i ? 0.0 : (j == i ? 1.0 : mrow[-j] * inv_rdiag[j]);
   }
 }
 
 // ------------------------------------------------------------------ clip + grid
-// One work-group per row: clip at [lo, hi], per-row min/max grid, Y = clipped D * R_jj
-// (dead columns zero).
+// One work-group per row: clip at [lo, hi], per-row min/max grid, Y = clipped D (the
+// unscaled pre-rounding values; dead columns are masked by the rounding).
 __global__ __launch_bounds__(256) void k_clip_grid(const float* __restrict__ D, int64_t cols,
                                                    int maxq, const double* __restrict__ scal,
-                                                   const uint8_t* __restrict__ dead,
-                                                   const double* __restrict__ rdiag,
                                                    double* __restrict__ Y, float* __restrict__ scale,
                                                    float* __restrict__ zero,
                                                    double* __restrict__ scale64,
@@ -630,15 +637,10 @@ __global__ __launch_bounds__(256) void k_clip_grid(const float* __restrict__ D, 
 #pragma unroll
   for (int q = 0; q < CK; ++q) {
     const int64_t j = threadIdx.x + 256 * q;
-    if (j < cols) {
-      const double x = dead[j] ? 0.0 : fmin(fmax((double)keep[q], lo_b), hi_b);
-      yrow[j] = x * rdiag[j];
-    }
+    if (j < cols) yrow[j] = fmin(fmax((double)keep[q], lo_b), hi_b);
   }
-  for (int64_t j = threadIdx.x + 256 * CK; j < cols; j += 256) {
-    const double x = dead[j] ? 0.0 : fmin(fmax((double)row[j], lo_b), hi_b);
-    yrow[j] = x * rdiag[j];
-  }
+  for (int64_t j = threadIdx.x + 256 * CK; j < cols; j += 256)
+    yrow[j] = fmin(fmax((double)row[j], lo_b), hi_b);
 }
 
 // ------------------------------------------------------------------ rounding block
@@ -655,7 +657,7 @@ constexpr int GROWS = GTH / 16 * GRK;  // 48 rows per work-group (253 groups for
 // row of R as 16 consecutive doubles (no bank conflicts) and load / store rows of Y, D,
 // codes and residuals contiguously.  Column j is rounded by its owner lane j % 16, its
 // residual broadcast to the group with a DPP row broadcast, and every lane folds it into
-// its own later columns: y_c += e_j R_jc (R_jc = 0 for c < j).
+// its own later columns: y_c += e_j R'_jc (R' = R diag(R)^-1, zero for c < j).
 template <int O>
 __device__ __forceinline__ double row_bcast(double v) {
   const long long b = __double_as_longlong(v);
@@ -669,32 +671,29 @@ struct RoundState {
   double s[GRK], is[GRK], z[GRK];
 };
 
-// column J; rn: row J of R at this lane's columns, irj: 1 / R_JJ; rn1, irj1: the same for
-// column J + 1 (rows of R are read from LDS two columns ahead)
+// column J; rn: row J of R' (unit diagonal) at this lane's columns; rn1: the same for
+// column J + 1 (rows of R' are read from LDS two columns ahead)
 template <int J>
-__device__ __forceinline__ void round_col(RoundState& st, const double* __restrict__ Rs,
-                                          const double* __restrict__ ird, int b, int g,
-                                          double maxq, const double (&rn)[8], double irj,
-                                          const double (&rn1)[8], double irj1) {
+__device__ __forceinline__ void round_col(RoundState& st, const double* __restrict__ Rs, int b,
+                                          int g, double maxq, const double (&rn)[8],
+                                          const double (&rn1)[8]) {
   if constexpr (J < GB) {
     if (J >= b) return;
     constexpr int O = J & 15, C = J >> 4;
     double rnext[8];
-    double irn = 0.0;
-    // slots cc below (J + 2) / 16 hold columns before J + 2 in every lane: R is upper
+    // slots cc below (J + 2) / 16 hold columns before J + 2 in every lane: R' is upper
     // triangular there, so column J + 2 neither reads nor updates them
     if constexpr (J + 2 < GB) {
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc)
         if (cc >= ((J + 2) >> 4)) rnext[cc] = Rs[(J + 2) * GB + g + 16 * cc];
-      irn = ird[J + 2];
     }
     double e[GRK];
 #pragma unroll
     for (int k = 0; k < GRK; ++k) {
       // t = w / scale in code units; the code relative to the zero point is
       // clamp(rne(t), -zero, maxq - zero) (the zero point is an integer)
-      const double t = st.y[k][C] * (irj * st.is[k]);
+      const double t = st.y[k][C] * st.is[k];
       const double qz = fmin(fmax(rint(t), -st.z[k]), maxq - st.z[k]);
       const double ek = fma(-st.s[k], qz, st.d0[k][C]);
       if (g == O) {
@@ -717,19 +716,18 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
 #pragma unroll
       for (int cc = 0; cc < 8; cc += 2)
         if (cc + 1 >= C) asm volatile("" : "+v"(st.y[k][cc]), "+v"(st.y[k][cc + 1]));
-    if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, ird, b, g, maxq, rn1, irj1, rnext, irn);
+    if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, b, g, maxq, rn1, rnext);
   }
 }
 
 __global__ __launch_bounds__(GTH) void k_gptq_block(
     const float* __restrict__ D, int64_t rows, int64_t cols, int i1, int b, int64_t res_col0,
     int64_t ld_res, int maxq, const double* __restrict__ scal, const uint8_t* __restrict__ dead,
-    const double* __restrict__ R, const double* __restrict__ inv_rdiag,
-    const double* __restrict__ scale64, const double* __restrict__ zero64,
-    const double* __restrict__ Y, uint8_t* __restrict__ codes8, double* __restrict__ res) {
+    const double* __restrict__ R, const double* __restrict__ scale64,
+    const double* __restrict__ zero64, const double* __restrict__ Y,
+    uint8_t* __restrict__ codes8, double* __restrict__ res) {
   __shared__ __attribute__((aligned(16))) double Rs[GB * GB];
-  __shared__ __attribute__((aligned(16))) double ird[GB];
-  // R block: Rs[rr][cc] = R[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
+  // R' block: Rs[rr][cc] = R'[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
   // issued unconditionally from a clamped in-bounds address, all of a thread's at once
   {
     constexpr int NE = GB * GB, PER = (NE + GTH - 1) / GTH, BATCH = 16;
@@ -749,7 +747,6 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
       }
     }
   }
-  if (threadIdx.x < GB) ird[threadIdx.x] = threadIdx.x < b ? inv_rdiag[i1 + threadIdx.x] : 0.0;
 
   const int lane = threadIdx.x & 63;
   const int g = lane & 15;                         // position inside the 16-lane group
@@ -785,7 +782,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) {
         const bool in = ok && g + 16 * cc < b;
-        st.y[k][cc] = in ? yv[k][cc] : 0.0;
+        st.y[k][cc] = (in && !dd[cc]) ? yv[k][cc] : 0.0;
         st.d0[k][cc] = (in && !dd[cc]) ? fmin(fmax((double)dv[k][cc], lo_b), hi_b) : 0.0;
         st.rr[k][cc] = 0.0;
       }
@@ -799,7 +796,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   double rn1[8];
 #pragma unroll
   for (int cc = 0; cc < 8; ++cc) rn1[cc] = Rs[GB + g + 16 * cc];
-  round_col<0>(st, Rs, ird, b, g, (double)maxq, rn, ird[0], rn1, ird[1]);
+  round_col<0>(st, Rs, b, g, (double)maxq, rn, rn1);
 
 #pragma unroll
   for (int k = 0; k < GRK; ++k) {
@@ -1392,8 +1389,9 @@ hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rd
                            hipStream_t s) {
   // rdiag is stored right after inv_rdiag (2 K doubles)
   prof_begin(s, "q_reverse");
-  hipLaunchKernelGGL(k_reverse_upper, dim3(grid_for(K * K, 256)), dim3(256), 0, s, A, K, R,
-                     inv_rdiag + K, inv_rdiag);
+  hipLaunchKernelGGL(k_rev_diag, dim3(grid_for(K, 256)), dim3(256), 0, s, A, K, inv_rdiag + K,
+                     inv_rdiag);
+  hipLaunchKernelGGL(k_reverse_upper, dim3(grid_for(K, 1)), dim3(256), 0, s, A, K, inv_rdiag, R);
   prof_end(s);
   return last_launch_error();
 }
@@ -1403,7 +1401,7 @@ hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, Qua
   if (rows <= 0) return hipSuccess;
   prof_begin(s, "q_clip_grid");
   hipLaunchKernelGGL(k_clip_grid, dim3(rows), dim3(256), 0, s, D, cols, (1 << bits) - 1, w.scal,
-                     w.dead, w.inv_rdiag + cols, w.Y, scale, zero, w.scale64, w.zero64);
+                     w.Y, scale, zero, w.scale64, w.zero64);
   prof_end(s);
   return last_launch_error();
 }
@@ -1414,7 +1412,7 @@ hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int 
   prof_begin(s, "gptq_block");
   hipLaunchKernelGGL(k_gptq_block, dim3(grid_for(rows, GROWS, 1 << 30)), dim3(GTH), 0, s, D, rows,
                      cols, i1, i2 - i1, (int64_t)(i1 - o1), ld_res, (1 << bits) - 1, w.scal,
-                     w.dead, w.R, w.inv_rdiag, w.scale64, w.zero64, w.Y, w.codes8, w.res);
+                     w.dead, w.R, w.scale64, w.zero64, w.Y, w.codes8, w.res);
   prof_end(s);
   return last_launch_error();
 }

@@ -49,6 +49,8 @@ SIGNATURES = {
     "fq_quantize_frames_workspace_bytes": (_sz, [_i64, _i64, _i]),
     "fq_quantize_prepare": (_i, [_vp, _vp, _i64, _i64, _i, _d, _vp, _sz]),
     "fq_quantize_apply": (_i, [_vp, _vp, _i64, _i64, _i, _i, _d, _vp, _vp, _vp, _vp, _sz]),
+    "fq_quantize_grid": (_i, [_vp, _vp, _i64, _i64, _i, _i, _d, _vp, _vp, _vp, _sz]),
+    "fq_quantize_round": (_i, [_vp, _vp, _i64, _i64, _i, _i, _vp, _vp, _sz]),
     "fq_frame_synthesis": (_i, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp,
                                 _sz]),
     "fq_frame_synthesis_workspace_bytes": (_sz, [_i64, _i64, _i64, _i64]),
@@ -261,6 +263,35 @@ def fq_quantize_apply(D, codes, scale, zero, ws, bits: int = 2, block: int = 128
                                    float(clip_sigmas), _ptr(codes), _ptr(scale), _ptr(zero),
                                    _ptr(ws), ws.numel()))
     return codes, scale, zero
+
+
+def fq_quantize_grid(D, scale, zero, ws, bits: int = 2, block: int = 128,
+                     clip_sigmas: float = 2.0, stream=None):
+    """First part of fq_quantize_apply (D only: clip bounds, per-row grid, working copy of
+    the clipped D); may run beside fq_quantize_prepare on another stream."""
+    torch = _torch()
+    K_out, K_in = D.shape
+    _dev(D, "D", torch.float32)
+    _dev(scale, "scale", torch.float32, (K_out,))
+    _dev(zero, "zero", torch.float32, (K_out,))
+    _dev(ws, "ws", torch.uint8)
+    _check(lib().fq_quantize_grid(_stream(stream), _ptr(D), K_out, K_in, bits, block,
+                                  float(clip_sigmas), _ptr(scale), _ptr(zero), _ptr(ws),
+                                  ws.numel()))
+    return scale, zero
+
+
+def fq_quantize_round(D, codes, ws, bits: int = 2, block: int = 128, stream=None):
+    """Second part of fq_quantize_apply (rounding with error feedback, packing, checks),
+    after fq_quantize_prepare and fq_quantize_grid on the same workspace."""
+    torch = _torch()
+    K_out, K_in = D.shape
+    _dev(D, "D", torch.float32)
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
+    _dev(ws, "ws", torch.uint8)
+    _check(lib().fq_quantize_round(_stream(stream), _ptr(D), K_out, K_in, bits, block,
+                                   _ptr(codes), _ptr(ws), ws.numel()))
+    return codes
 
 
 class SideStream:

@@ -11,9 +11,11 @@ With frames given by their construction (LayerBuffers(..., frames=(F_out, F_in))
 objects), the analysis and the synthesis are fq_frame_analysis_tff / fq_frame_synthesis_tff
 and the dense P_out, P_in are not read (pass None).
 
-With a second stream (side_stream), D = P_out^T W P_in is formed there while the main
-stream factors the damped H~ (fq_quantize_prepare): the Cholesky factorization, a chain
-of small dependent kernels, then overlaps the D contractions.  Outputs are identical.
+With a second stream (side_stream), D = P_out^T W P_in is formed there, followed by the
+part of the rounding that reads D only (fq_quantize_grid: clip bounds, per-row grid),
+while the main stream factors the damped H~ (fq_quantize_prepare): the Cholesky
+factorization, a chain of small dependent kernels, then overlaps the D contractions.  The
+main stream then rounds (fq_quantize_round).  Outputs are identical.
 A side stream from fq.SideStream keeps the D kernels off part of the device, so that the
 chain always finds free compute units; it synchronizes with the legacy default stream, so
 the main stream must then be another stream (torch.cuda.Stream()).
@@ -116,11 +118,12 @@ def _quantize_layer_two_streams(W, X, P_out, P_in, bufs, H, Ht, bits, block, dam
     ready.record(main)
     side.wait_event(ready)
     _analysis(W, P_out, P_in, bufs, None, bufs.D, None, bufs.ws_a2, side)
+    _fq.fq_quantize_grid(bufs.D, bufs.scale, bufs.zero, bufs.ws_q, bits=bits, block=block,
+                         clip_sigmas=clip_sigmas, stream=side)
     d_done = torch.cuda.Event()
     d_done.record(side)
     _fq.fq_quantize_prepare(Ht, bufs.D.shape[0], bufs.ws_q, block=block, damp=damp, stream=main)
     main.wait_event(d_done)
-    _fq.fq_quantize_apply(bufs.D, bufs.codes, bufs.scale, bufs.zero, bufs.ws_q, bits=bits,
-                          block=block, clip_sigmas=clip_sigmas, stream=main)
+    _fq.fq_quantize_round(bufs.D, bufs.codes, bufs.ws_q, bits=bits, block=block, stream=main)
     _synthesis(P_out, P_in, bufs, bits, main)
     return bufs

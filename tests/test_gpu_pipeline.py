@@ -149,25 +149,50 @@ def test_prepare_apply_match_fused_call():
     Ht = (Ht + Ht.T) / 2
     D = torch.from_numpy((rng.standard_normal((K_out, K_in)) * 0.02).astype(np.float32)).cuda()
     res = []
-    for split in (False, True):
+    for split in ("fused", "prepare+apply", "prepare|grid+round"):
         codes = torch.empty((K_out, (K_in + 15) // 16), dtype=torch.int32, device="cuda")
         scale = torch.empty((K_out,), dtype=torch.float32, device="cuda")
         zero = torch.empty((K_out,), dtype=torch.float32, device="cuda")
         ws = torch.full((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), 0xFF,
                         dtype=torch.uint8, device="cuda")
-        if split:
+        if split == "prepare+apply":
             s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
             fq.fq_quantize_prepare(Ht, K_out, ws, stream=s1)
             ev = torch.cuda.Event()
             ev.record(s1)
             s2.wait_event(ev)
             fq.fq_quantize_apply(D, codes, scale, zero, ws, stream=s2)
+        elif split == "prepare|grid+round":
+            # the grid beside prepare on its own stream, the rounding after both
+            s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+            fq.fq_quantize_grid(D, scale, zero, ws, stream=s2)
+            fq.fq_quantize_prepare(Ht, K_out, ws, stream=s1)
+            ev = torch.cuda.Event()
+            ev.record(s2)
+            s1.wait_event(ev)
+            fq.fq_quantize_round(D, codes, ws, stream=s1)
         else:
             fq.fq_quantize_frames(D, Ht, codes, scale, zero, ws=ws)
         torch.cuda.synchronize()
         res.append((codes.cpu().numpy(), scale.cpu().numpy(), zero.cpu().numpy()))
-    for a, b in zip(res[0], res[1]):
-        np.testing.assert_array_equal(a, b)
+    for r in res[1:]:
+        for a, b in zip(res[0], r):
+            np.testing.assert_array_equal(a, b)
+    # a non-finite D found by the grid is reported by the rounding, also when the grid ran
+    # beside prepare (prepare clears only its own checks)
+    ws = torch.empty((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), dtype=torch.uint8,
+                     device="cuda")
+    Dn = D.clone()
+    Dn[3, 7] = float("inf")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    fq.fq_quantize_grid(Dn, scale, zero, ws, stream=s2)
+    fq.fq_quantize_prepare(Ht, K_out, ws, stream=s1)
+    ev = torch.cuda.Event()
+    ev.record(s2)
+    s1.wait_event(ev)
+    with pytest.raises(fq.FQError) as ei:
+        fq.fq_quantize_round(Dn, codes, ws, stream=s1)
+    assert ei.value.status == 4
     # one factor, several applies: a non-finite D is reported by its own apply only
     ws = torch.empty((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), dtype=torch.uint8,
                      device="cuda")
