@@ -126,11 +126,12 @@ def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, w_dtype="bf16
             ex = hess_tiles * 256 * 256 * 2 * n
         work[k] = ("bf16", v, ex)
     work.update({
-        "gptq_update": ("f64", gptq_upd, gptq_upd),
+        "gptq_update": ("f64", gptq_lazy, gptq_lazy),
         "gptq_update_lazy": ("f64", gptq_lazy, gptq_lazy),
-        "gptq_update_span": ("f64", gptq_upd - gptq_lazy, gptq_upd - gptq_lazy),
         "chol": ("f64", chol, None),
-        "gptq_block": ("f64", K_out * K_in * 128, None),     # in-block FMAs (upper bound)
+        # the rounding kernel: the in-span products (the span's earlier chunks into each
+        # chunk, fp64 MFMA) plus the in-block FMAs (upper bound)
+        "gptq_block": ("f64", gptq_upd - gptq_lazy + K_out * K_in * 128, None),
         "pack2": ("hbm", K_out * K_in + K_out * ((K_in + 15) // 16) * 4, None),
     })
     return work
@@ -145,7 +146,7 @@ CONTRACTIONS_S4 = ["gemm_synthesis_1", "gemm_synthesis_2", "tffp_dft_syn", "tffp
 KERNEL_GROUPS = ["gemm_hessian", "gemm_analysis_w1", "gemm_analysis_w2", "gemm_analysis_h1",
                  "gemm_analysis_h2", "gemm_synthesis_1", "gemm_synthesis_2", "tffp_rotate_an",
                  "tffp_rotate_syn", "tffp_blocks", "tffp_dft_an", "tffp_dft_syn", "tffp_gather",
-                 "gptq_update", "gptq_update_lazy", "gptq_update_span", "gptq_block", "chol",
+                 "gptq_update", "gptq_update_lazy", "gptq_block", "chol",
                  "chol_syrk", "chol_potrf", "chol_trsm", "q_", "split_bf16", "syrk_reduce",
                  "dequant", "pack2"]
 

@@ -177,9 +177,11 @@ static size_t analysis_layout(int wt, int64_t d_out, int64_t d_in, int64_t K_out
 
 // Columns are rounded in chunks of min(block, 128) by the sequential kernel; the
 // residuals of consecutive chunks are applied to the columns right of them in spans of
-// at least 512 columns (a whole number of blocks): inside a span after every chunk,
-// beyond it once per span.  This regroups OPTQ's lazy block updates; every column still
-// receives exactly the sum of the residual terms of all earlier columns.
+// at least 512 columns (a whole number of blocks): inside a span each chunk receives
+// those of the span's earlier chunks in the rounding kernel, right before it is rounded;
+// the columns beyond the span receive the whole span's once, as one fp64 GEMM.  This
+// regroups OPTQ's lazy block updates; every column still receives exactly the sum of the
+// residual terms of all earlier columns.
 static int64_t chunk_width(int block) { return block < 128 ? block : 128; }
 static int64_t span_width(int block) {
   const int64_t b = block;
@@ -544,14 +546,11 @@ static fq_status quantize_round(hipStream_t s, const float* D, int64_t K_out, in
     const int64_t s2 = (s1 + sw < K_in) ? s1 + sw : K_in;
     for (int64_t i1 = s1; i1 < s2; i1 += cw) {
       const int64_t i2 = (i1 + cw < s2) ? i1 + cw : s2;
-      if ((e = q_gptq_block(D, K_out, K_in, (int)i1, (int)i2, (int)s1, ldr, bits, Q, s)) != hipSuccess)
+      // the rounding kernel first adds the residuals of the span's earlier chunks to
+      // this chunk's columns (the in-span update), then rounds them
+      if ((e = q_gptq_block(D, K_out, K_in, (int)i1, (int)i2, (int)s1, (int)cw, ldr, bits, Q,
+                            s)) != hipSuccess)
         return hip_fail(e, "rounding block");
-      if (i2 < s2) {
-        e = dgemm(K_out, s2 - i2, i2 - i1, 1.0, 1.0, Q.res + (i1 - s1), ldr, Q.R + i1 * K_in + i2,
-                  K_in, false, Q.Y + i2, K_in, false, s, "gptq_update_span",
-                  g_dgemm_tile ? g_dgemm_tile : 64);
-        if (e != hipSuccess) return hip_fail(e, "in-span update");
-      }
     }
     if (s2 < K_in) {
       e = dgemm(K_out, K_in - s2, s2 - s1, 1.0, 1.0, Q.res, ldr, Q.R + s1 * K_in + s2, K_in, false,

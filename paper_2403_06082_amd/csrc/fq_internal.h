@@ -203,7 +203,7 @@ hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rd
 hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, QuantScratch& w,
                        float* scale, float* zero, hipStream_t s);
 hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int i2, int o1,
-                        int64_t ld_res, int bits, QuantScratch& w, hipStream_t s);
+                        int cw, int64_t ld_res, int bits, QuantScratch& w, hipStream_t s);
 // C[M x N] = beta * C + alpha * A[M x K] * op(B)   (fp64 MFMA; beta is 0 or 1)
 //   b_trans: op(B)(k, n) = B[n * ldb + k]  else B[k * ldb + n]
 //   lower_only: only tiles with tile_row >= tile_col (for the Cholesky update)

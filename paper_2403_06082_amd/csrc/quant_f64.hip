@@ -720,34 +720,104 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
   }
 }
 
+// ---- the span's earlier chunks folded into this chunk's columns before they are rounded:
+// for each earlier chunk (in order), y += res[:, chunk] R'[chunk rows, this chunk's
+// columns], a GROWS x b x cw product on v_mfma_f64_4x4x4f64.  The operands go through LDS
+// (the R block's space, before the block is staged) in k steps of 16; every product
+// element sums its k in the fp64 GEMM's order and is added to y as that GEMM's epilogue
+// adds it, so the values are the ones the in-span GEMM would leave in Y.  Wave w forms
+// rows 8 (w % 6) .. + 8 and columns 64 (w / 6) .. + 64 (eight 8 x 8 sub-tiles).
+constexpr int SU_AP = GROWS + 8;                    // A slot: [k][row]
+constexpr int SU_BP = GB + 8;                       // B slot: [k][col]
+constexpr int SU_SLOT = 16 * SU_AP + 16 * SU_BP;
+constexpr int SU_PP = GB + 2;                       // product tile pitch
+static_assert(GTH == 768 && GROWS == 48 && GRK == 1, "span update layout assumes 48 rows, 12 waves");
+static_assert(2 * SU_SLOT + GROWS * SU_PP <= GB * GB, "span update scratch fits in the R block's LDS");
+
+__device__ __forceinline__ void su_load(const double* __restrict__ res, int64_t ld_res,
+                                        const double* __restrict__ R, int64_t cols, int64_t wr0,
+                                        int64_t rows, int64_t rrow0, int col0, int kc, int b,
+                                        int i1, int kb, double& av, double (&bv)[3]) {
+  const int t = threadIdx.x;
+  {  // A: row t / 16, k t % 16 of the chunk's residuals
+    const int row = t >> 4, k = kb + (t & 15);
+    const int64_t r = wr0 + row;
+    av = (r < rows && k < kc) ? res[r * ld_res + col0 + k] : 0.0;
+  }
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {  // B: k = e / 128, column e % 128 of R' rows of the chunk
+    const int e = t + GTH * q;
+    const int k = kb + (e >> 7), c = e & 127;
+    bv[q] = (e < 16 * GB && k < kc && c < b) ? R[(rrow0 + k) * cols + i1 + c] : 0.0;
+  }
+}
+
+__device__ __forceinline__ void su_store(double* slot, double av, const double (&bv)[3]) {
+  const int t = threadIdx.x;
+  slot[(t & 15) * SU_AP + (t >> 4)] = av;
+  double* bs = slot + 16 * SU_AP;
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const int e = t + GTH * q;
+    if (e < 16 * GB) bs[(e >> 7) * SU_BP + (e & 127)] = bv[q];
+  }
+}
+
+__device__ __forceinline__ void span_update(RoundState& st, double* lds,
+                                            const double* __restrict__ res, int64_t ld_res,
+                                            int64_t res_col0, int cw,
+                                            const double* __restrict__ R, int64_t cols, int i1,
+                                            int b, int64_t rows, int64_t wr0, int grp, int g) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int blk = (lane >> 2) & 3, bi = blk >> 1, bj = blk & 1, q4 = lane & 3, kq = lane >> 4;
+  const int arow = 8 * (w % 6) + 4 * bi + q4, bcol = 64 * (w / 6) + 4 * bj + q4;
+  double* P = lds + 2 * SU_SLOT;
+  const int64_t s1 = i1 - res_col0;
+  for (int64_t col0 = 0; col0 < res_col0; col0 += cw) {
+    const int kc = (int)min<int64_t>(cw, res_col0 - col0);
+    const int nks = (kc + 15) / 16;
+    double acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.0;
+    double av, bv[3];
+    su_load(res, ld_res, R, cols, wr0, rows, s1 + col0, (int)col0, kc, b, i1, 0, av, bv);
+    su_store(lds, av, bv);
+    __syncthreads();
+    for (int ks = 0; ks < nks; ++ks) {
+      const double* slot = lds + (ks & 1) * SU_SLOT;
+      const bool more = ks + 1 < nks;
+      if (more) su_load(res, ld_res, R, cols, wr0, rows, s1 + col0, (int)col0, kc, b, i1,
+                        16 * (ks + 1), av, bv);
+#pragma unroll
+      for (int kk = 0; kk < 16; kk += 4) {
+        const double af = slot[(kk + kq) * SU_AP + arow];
+        double bf[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) bf[j] = slot[16 * SU_AP + (kk + kq) * SU_BP + bcol + 8 * j];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af, bf[j], acc[j], 0, 0, 0);
+      }
+      if (more) su_store(lds + ((ks + 1) & 1) * SU_SLOT, av, bv);
+      __syncthreads();
+    }
+    // lane l holds row 4 bi + l / 16 and column 4 bj + l % 4 of each 8 x 8 sub-tile
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      P[(8 * (w % 6) + 4 * bi + kq) * SU_PP + 64 * (w / 6) + 4 * bj + q4 + 8 * j] = acc[j];
+    __syncthreads();
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) st.y[0][cc] += P[grp * SU_PP + g + 16 * cc];
+    __syncthreads();
+  }
+}
+
 __global__ __launch_bounds__(GTH) void k_gptq_block(
     const float* __restrict__ D, int64_t rows, int64_t cols, int i1, int b, int64_t res_col0,
-    int64_t ld_res, int maxq, const double* __restrict__ scal, const uint8_t* __restrict__ dead,
-    const double* __restrict__ R, const double* __restrict__ scale64,
-    const double* __restrict__ zero64, const double* __restrict__ Y,
-    uint8_t* __restrict__ codes8, double* __restrict__ res) {
+    int cw, int64_t ld_res, int maxq, const double* __restrict__ scal,
+    const uint8_t* __restrict__ dead, const double* __restrict__ R,
+    const double* __restrict__ scale64, const double* __restrict__ zero64,
+    const double* __restrict__ Y, uint8_t* __restrict__ codes8, double* __restrict__ res) {
   __shared__ __attribute__((aligned(16))) double Rs[GB * GB];
-  // R' block: Rs[rr][cc] = R'[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
-  // issued unconditionally from a clamped in-bounds address, all of a thread's at once
-  {
-    constexpr int NE = GB * GB, PER = (NE + GTH - 1) / GTH, BATCH = 16;
-#pragma unroll
-    for (int q0 = 0; q0 < PER; q0 += BATCH) {
-      double v[BATCH];
-#pragma unroll
-      for (int q = 0; q < BATCH; ++q) {
-        const int e = min((int)threadIdx.x + (q0 + q) * GTH, NE - 1);
-        const int rr = min(e / GB, b - 1), cc = min(e % GB, b - 1);
-        v[q] = R[(int64_t)(i1 + rr) * cols + i1 + cc];
-      }
-#pragma unroll
-      for (int q = 0; q < BATCH; ++q) {
-        const int e = (int)threadIdx.x + (q0 + q) * GTH;
-        if (q0 + q < PER && e < NE) Rs[e] = ((e / GB) < b && (e % GB) < b) ? v[q] : 0.0;
-      }
-    }
-  }
-
   const int lane = threadIdx.x & 63;
   const int g = lane & 15;                         // position inside the 16-lane group
   const int grp = threadIdx.x >> 4;                // group index in the work-group
@@ -788,6 +858,33 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
       }
     }
   }
+  // the residuals of the span's earlier chunks (dead columns receive exact zeros: R' is
+  // zero there off the diagonal)
+  if (res_col0 > 0)
+    span_update(st, Rs, res, ld_res, res_col0, cw, R, cols, i1, b, rows,
+                (int64_t)blockIdx.x * GROWS, grp, g);
+
+  // R' block: Rs[rr][cc] = R'[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
+  // issued unconditionally from a clamped in-bounds address, all of a thread's at once
+  {
+    constexpr int NE = GB * GB, PER = (NE + GTH - 1) / GTH, BATCH = 16;
+#pragma unroll
+    for (int q0 = 0; q0 < PER; q0 += BATCH) {
+      double v[BATCH];
+#pragma unroll
+      for (int q = 0; q < BATCH; ++q) {
+        const int e = min((int)threadIdx.x + (q0 + q) * GTH, NE - 1);
+        const int rr = min(e / GB, b - 1), cc = min(e % GB, b - 1);
+        v[q] = R[(int64_t)(i1 + rr) * cols + i1 + cc];
+      }
+#pragma unroll
+      for (int q = 0; q < BATCH; ++q) {
+        const int e = (int)threadIdx.x + (q0 + q) * GTH;
+        if (q0 + q < PER && e < NE) Rs[e] = ((e / GB) < b && (e % GB) < b) ? v[q] : 0.0;
+      }
+    }
+  }
+
   __syncthreads();
 
   double rn[8];
@@ -1407,11 +1504,11 @@ hipError_t q_clip_grid(const float* D, int64_t rows, int64_t cols, int bits, Qua
 }
 
 hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int i2, int o1,
-                        int64_t ld_res, int bits, QuantScratch& w, hipStream_t s) {
+                        int cw, int64_t ld_res, int bits, QuantScratch& w, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   prof_begin(s, "gptq_block");
   hipLaunchKernelGGL(k_gptq_block, dim3(grid_for(rows, GROWS, 1 << 30)), dim3(GTH), 0, s, D, rows,
-                     cols, i1, i2 - i1, (int64_t)(i1 - o1), ld_res, (1 << bits) - 1, w.scal,
+                     cols, i1, i2 - i1, (int64_t)(i1 - o1), cw, ld_res, (1 << bits) - 1, w.scal,
                      w.dead, w.R, w.scale64, w.zero64, w.Y, w.codes8, w.res);
   prof_end(s);
   return last_launch_error();
