@@ -811,6 +811,169 @@ __device__ __forceinline__ void span_update(RoundState& st, double* lds,
   }
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Global -> LDS copies (wave-uniform base + per-lane byte offset; lane l lands at
+// lds + 16 l or lds + 4 l).  Inline assembly, so that the compiler does not make every
+// later LDS read wait for them: completion is tracked by the explicit vmcnt wait.
+__device__ __forceinline__ void lds_copy16(const char* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+__device__ __forceinline__ void lds_copy4(const char* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
+               : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
+}
+
+// The same products with the operands copied global -> LDS by the DMA path
+// (global_load_lds), three k steps of 16 in flight ahead of the one being multiplied
+// (four slots), and the running sum kept in the product's register layout across the
+// span's earlier chunks (per chunk: acc = its product, then sum += acc, the order and
+// roundings of the GEMM route).  For whole 128-column chunks with 16-byte aligned rows of
+// res and R.  Slot: A rows of 128 bytes, k at position k ^ 2 (row & 7); B k-rows of 1 KB,
+// column n at position n ^ 8 (k-row & 3) (the LDS-ring kernel's layouts).  Waves 0..7
+// copy B k-rows w and w + 8, waves 8..10 two A row groups of 8 each, wave 11 nothing:
+// every copying wave has exactly two copies per step in flight.  Wave w multiplies rows
+// 16 (w / 4) .. + 16 and columns 32 (w % 4) .. + 32 (2 x 4 sub-tiles of 8 x 8: six LDS
+// reads per eight MFMAs).
+constexpr int SA_BYTES = GROWS * 128;               // 6 KB
+constexpr int SB_BYTES = 16 * 1024;                 // 16 KB
+constexpr int SS_BYTES = SA_BYTES + SB_BYTES;
+constexpr int SS_N = 4;                             // slots
+static_assert(SS_N * SS_BYTES <= GB * GB * 8 && GROWS * SU_PP * 8 <= GB * GB * 8,
+              "span update slots fit in the R block's LDS");
+
+__device__ __forceinline__ bool span_async_ok(const double* res, int64_t ld_res,
+                                              const double* R, int64_t cols, int b, int cw) {
+  return b == GB && cw == GB && (cols & 1) == 0 && (ld_res & 1) == 0 &&
+         ((reinterpret_cast<uintptr_t>(res) | reinterpret_cast<uintptr_t>(R)) & 15) == 0;
+}
+
+__device__ __forceinline__ void span_update_async(RoundState& st, double* lds,
+                                                  const double* __restrict__ res,
+                                                  int64_t ld_res, int64_t res_col0,
+                                                  const double* __restrict__ R, int64_t cols,
+                                                  const double* __restrict__ Y, int i1,
+                                                  int64_t rows, int64_t wr0, int grp, int g) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int blk = (lane >> 2) & 3, bi = blk >> 1, bj = blk & 1, q4 = lane & 3, kq = lane >> 4;
+  const int wr = w >> 2, wc = w & 3;                // 16-row group, 32-column group
+  const int ra7 = 4 * bi + q4;                      // fragment row mod 8
+  const int nst = (int)(res_col0 / 16);             // k steps (8 per earlier chunk)
+  const int64_t s1 = i1 - res_col0;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)lds;
+  // this wave's copy offsets (bytes from the step's source base)
+  uint32_t off[2];
+  const char* srcA = reinterpret_cast<const char*>(res + wr0 * ld_res);
+  const char* srcB = reinterpret_cast<const char*>(R + s1 * cols + i1);
+  if (w < 8) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int kr = w + 8 * i;
+      off[i] = (uint32_t)((kr * cols + ((2 * lane) ^ (8 * (kr & 3)))) * 8);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = 8 * (2 * (w - 8) + i) + (lane >> 3), c = lane & 7;
+      const int64_t gr = min<int64_t>(wr0 + r, rows - 1) - wr0;
+      off[i] = (uint32_t)((gr * ld_res + 2 * (c ^ (r & 7))) * 8);
+    }
+  }
+  auto issue = [&](int s) {
+    const uint32_t slot = lds0 + (uint32_t)((s % SS_N) * SS_BYTES);
+    if (w < 8) {
+      const char* b = srcB + (int64_t)s * 16 * cols * 8;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) lds_copy16(b, off[i], slot + SA_BYTES + (w + 8 * i) * 1024);
+    } else if (w < 11) {
+      const char* a = srcA + (int64_t)s * 16 * 8;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) lds_copy16(a, off[i], slot + (2 * (w - 8) + i) * 1024);
+    }
+  };
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  // fragment offsets inside a slot: A rows 16 wr + 8 i + ra7, k = 4 t + kq; B k-row
+  // 4 t + kq, columns 32 wc + 4 bj + q4 + 8 j
+  uint32_t xa[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      xa[i][t] = (uint32_t)((16 * wr + 8 * i + ra7) * 128 + 8 * ((4 * t + kq) ^ (2 * ra7)));
+  const int bc = 32 * wc + 4 * bj + q4;
+  // the running sum, from Y, in the product's layout (rows 16 wr + 8 i + 4 bi + kq,
+  // columns bc + 8 j)
+  double sum[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int64_t r = min<int64_t>(wr0 + 16 * wr + 8 * i + 4 * bi + kq, rows - 1);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sum[i][j] = Y[r * cols + i1 + bc + 8 * j];
+  }
+  double acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int s = 0; s < SS_N - 1 && s < nst; ++s) issue(s);
+  for (int s = 0; s < nst; ++s) {
+    // this step's copies landed (each wave its own, then all): at most the later issued
+    // steps (two copies each) may still be in flight
+    const int later = min(SS_N - 2, nst - 1 - s);
+    if (w < 11) {
+      if (later >= 2) __builtin_amdgcn_s_waitcnt(0x0F70 | 4);
+      else if (later == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | 2);
+      else __builtin_amdgcn_s_waitcnt(0x0F70);
+    }
+    barrier();
+    if (s + SS_N - 1 < nst) issue(s + SS_N - 1);
+    const char* slot = reinterpret_cast<const char*>(lds) + (s % SS_N) * SS_BYTES;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      double af[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) af[i] = *reinterpret_cast<const double*>(slot + xa[i][t]);
+      const int kr = 4 * t + kq;
+      double bf[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bf[j] = *reinterpret_cast<const double*>(slot + SA_BYTES + kr * 1024 +
+                                                 8 * ((bc + 8 * j) ^ (8 * (kr & 3))));
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+    if ((s & 7) == 7) {       // the end of an earlier chunk: add its product
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          sum[i][j] += acc[i][j];
+          acc[i][j] = 0.0;
+        }
+    }
+  }
+  barrier();                  // every slot read; the product tile goes over them
+  double* P = lds;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      P[(16 * wr + 8 * i + 4 * bi + kq) * SU_PP + bc + 8 * j] = sum[i][j];
+  __syncthreads();
+#pragma unroll
+  for (int cc = 0; cc < 8; ++cc) st.y[0][cc] = P[grp * SU_PP + g + 16 * cc];
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(GTH) void k_gptq_block(
     const float* __restrict__ D, int64_t rows, int64_t cols, int i1, int b, int64_t res_col0,
     int cw, int64_t ld_res, int maxq, const double* __restrict__ scal,
@@ -825,8 +988,27 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   const double lo_b = scal[2], hi_b = scal[3];
 
   RoundState st;
+  // y: this chunk's columns of Y, plus the residuals of the span's earlier chunks
+  if (res_col0 > 0 && span_async_ok(res, ld_res, R, cols, b, cw)) {
+    span_update_async(st, Rs, res, ld_res, res_col0, R, cols, Y, i1, rows,
+                      (int64_t)blockIdx.x * GROWS, grp, g);
+  } else {
+    {
+      const int64_t r = min(r0, rows - 1);
+      double yv[8];
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) yv[cc] = Y[r * cols + i1 + min(g + 16 * cc, b - 1)];
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) st.y[0][cc] = yv[cc];
+    }
+    if (res_col0 > 0)
+      span_update(st, Rs, res, ld_res, res_col0, cw, R, cols, i1, b, rows,
+                  (int64_t)blockIdx.x * GROWS, grp, g);
+  }
+  // the grid, the clipped D, and the masks: columns outside the chunk, dead columns (the
+  // products above add exact zeros there, R' being zero off the diagonal) and rows
+  // outside D hold y = 0
   {
-    double yv[GRK][8];
     float dv[GRK][8];
     uint8_t dd[8];
 #pragma unroll
@@ -835,11 +1017,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     for (int k = 0; k < GRK; ++k) {
       const int64_t r = min(r0 + k, rows - 1);
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) {
-        const int c = min(g + 16 * cc, b - 1);
-        yv[k][cc] = Y[r * cols + i1 + c];
-        dv[k][cc] = D[r * cols + i1 + c];
-      }
+      for (int cc = 0; cc < 8; ++cc) dv[k][cc] = D[r * cols + i1 + min(g + 16 * cc, b - 1)];
     }
 #pragma unroll
     for (int k = 0; k < GRK; ++k) {
@@ -852,17 +1030,12 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) {
         const bool in = ok && g + 16 * cc < b;
-        st.y[k][cc] = (in && !dd[cc]) ? yv[k][cc] : 0.0;
+        st.y[k][cc] = (in && !dd[cc]) ? st.y[k][cc] : 0.0;
         st.d0[k][cc] = (in && !dd[cc]) ? fmin(fmax((double)dv[k][cc], lo_b), hi_b) : 0.0;
         st.rr[k][cc] = 0.0;
       }
     }
   }
-  // the residuals of the span's earlier chunks (dead columns receive exact zeros: R' is
-  // zero there off the diagonal)
-  if (res_col0 > 0)
-    span_update(st, Rs, res, ld_res, res_col0, cw, R, cols, i1, b, rows,
-                (int64_t)blockIdx.x * GROWS, grp, g);
 
   // R' block: Rs[rr][cc] = R'[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
   // issued unconditionally from a clamped in-bounds address, all of a thread's at once
@@ -1088,19 +1261,6 @@ constexpr int RA_PER = RA_BYTES / 1024 / RWAVES;     // 16-byte copies per wave 
 constexpr int RB_PER = RA_BYTES / 256 / RWAVES;      // dword copies per wave and step (8)
 static_assert(RA_PER == 2 && RB_PER == 8, "copy layout below assumes 8 waves");
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Global -> LDS copies (wave-uniform base + per-lane byte offset; lane l lands at
-// lds + 16 l or lds + 4 l).  Inline assembly, so that the compiler does not make every
-// later LDS read wait for them: completion is tracked by the explicit vmcnt wait.
-__device__ __forceinline__ void lds_copy16(const char* base, uint32_t off, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
-               : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
-}
-__device__ __forceinline__ void lds_copy4(const char* base, uint32_t off, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1"
-               : : "v"(off), "s"(base), "s"(lds) : "memory", "m0");
-}
 
 template <bool BT, bool LOWER>
 __global__ __launch_bounds__(64 * RWAVES, 4) void k_dgemm_ring(DgemmArgs p) {
