@@ -27,9 +27,9 @@
  *    space takes a caller-provided workspace `ws` of at least the size returned by its
  *    *_workspace_bytes query (16-byte aligned).
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls are stream-ordered and
- *    asynchronous, except fq_quantize_frames, fq_quantize_apply and fq_quantize_round,
- *    which synchronize `stream` once at their end to report the positive-definiteness
- *    and finiteness checks.
+ *    asynchronous, except fq_quantize_frames, fq_quantize_apply, fq_quantize_round and
+ *    fq_quantize_status, which synchronize `stream` once at their end to report the
+ *    positive-definiteness and finiteness checks.
  *  - Arguments are validated before anything is launched; on failure the call returns
  *    FQ_ERR_INVALID_ARG (or FQ_ERR_UNSUPPORTED / FQ_ERR_WORKSPACE_TOO_SMALL) and
  *    fq_last_error() describes the problem.  No exception crosses the boundary.
@@ -166,6 +166,21 @@ fq_status fq_quantize_grid(void* stream, const float* D, int64_t K_out, int64_t 
                            size_t ws_bytes);
 fq_status fq_quantize_round(void* stream, const float* D, int64_t K_out, int64_t K_in, int bits,
                             int block, uint32_t* codes, void* ws, size_t ws_bytes);
+
+/*
+ * fq_quantize_round without its synchronization, for a caller that has more work for the
+ * stream (the synthesis of the codes, Alg. 1's return value) and wants the device kept
+ * busy: fq_quantize_round_async launches the rounding and the packing and returns;
+ * fq_quantize_status, called later on the same stream and workspace, synchronizes the
+ * stream and reports the checks of prepare, grid and round (the return value
+ * fq_quantize_round would have given).  Outputs written before the status call are
+ * unspecified when it reports an error.  Arguments and errors as for fq_quantize_round.
+ */
+fq_status fq_quantize_round_async(void* stream, const float* D, int64_t K_out, int64_t K_in,
+                                  int bits, int block, uint32_t* codes, void* ws,
+                                  size_t ws_bytes);
+fq_status fq_quantize_status(void* stream, int64_t K_out, int64_t K_in, int block, void* ws,
+                             size_t ws_bytes);
 
 /*
  * A stream for the work a caller runs beside fq_quantize_prepare (the analysis of W, which

@@ -6,7 +6,8 @@ package holds the sources, the build script and a thin ctypes binding.
 from .fq import (  # noqa: F401
     FQ_F32, FQ_F16, FQ_BF16, FQError, lib,
     fq_hessian_accumulate, fq_frame_analysis, fq_quantize_frames, fq_frame_synthesis,
-    fq_quantize_prepare, fq_quantize_apply, fq_quantize_grid, fq_quantize_round, fq_frame_apply,
+    fq_quantize_prepare, fq_quantize_apply, fq_quantize_grid, fq_quantize_round,
+    fq_quantize_round_async, fq_quantize_status, fq_frame_apply,
     fq_frame_apply_workspace_bytes,
     Frame, fq_tff_analysis, fq_tff_synthesis, fq_frame_apply_tff, fq_frame_apply_tff_noalloc,
     fq_tff_analysis_workspace_bytes,

@@ -536,9 +536,10 @@ static fq_status quantize_grid(hipStream_t s, const float* D, int64_t K_out, int
 }
 
 // the D phase, second part (after both the H~ phase and the first part): rounding with
-// error feedback, packing; then sync and checks
-static fq_status quantize_round(hipStream_t s, const float* D, int64_t K_out, int64_t K_in,
-                                int bits, int block, uint32_t* codes, QuantScratch& Q) {
+// error feedback and packing (no sync)
+static fq_status quantize_round_launch(hipStream_t s, const float* D, int64_t K_out,
+                                       int64_t K_in, int bits, int block, uint32_t* codes,
+                                       QuantScratch& Q) {
   hipError_t e;
   const int64_t ldr = res_width(K_in, block);
   const int64_t cw = chunk_width(block), sw = span_width(block);
@@ -561,6 +562,12 @@ static fq_status quantize_round(hipStream_t s, const float* D, int64_t K_out, in
   if ((e = bits == 2 ? q_pack2(Q.codes8, K_out, K_in, codes, s)
                     : q_pack_nbit(Q.codes8, K_out, K_in, bits, codes, s)) != hipSuccess)
     return hip_fail(e, "pack");
+  return FQ_OK;
+}
+
+// the checks of all three phases, recorded in the workspace: sync, then report
+static fq_status quantize_check(hipStream_t s, QuantScratch& Q) {
+  hipError_t e;
   int flags[4] = {0, 0, 0, 0};
   if ((e = hipMemcpyAsync(flags, Q.flags, sizeof(flags), hipMemcpyDeviceToHost, s)) != hipSuccess)
     return hip_fail(e, "flag copy");
@@ -569,6 +576,12 @@ static fq_status quantize_round(hipStream_t s, const float* D, int64_t K_out, in
   if (flags[1]) return fail(FQ_ERR_NONFINITE, "Ht holds NaN or Inf");
   if (flags[0]) return fail(FQ_ERR_NOT_POSITIVE_DEFINITE, "damped Ht is not positive definite");
   return FQ_OK;
+}
+
+static fq_status quantize_round(hipStream_t s, const float* D, int64_t K_out, int64_t K_in,
+                                int bits, int block, uint32_t* codes, QuantScratch& Q) {
+  const fq_status st = quantize_round_launch(s, D, K_out, K_in, bits, block, codes, Q);
+  return st != FQ_OK ? st : quantize_check(s, Q);
 }
 
 static fq_status quantize_ws_check(int64_t K_out, int64_t K_in, int block, void* ws,
@@ -664,6 +677,31 @@ fq_status fq_quantize_round(void* stream, const float* D, int64_t K_out, int64_t
   if (st != FQ_OK) return st;
   QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
   return quantize_round((hipStream_t)stream, D, K_out, K_in, bits, block, codes, Q);
+}
+
+fq_status fq_quantize_round_async(void* stream, const float* D, int64_t K_out, int64_t K_in,
+                                  int bits, int block, uint32_t* codes, void* ws,
+                                  size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (bits < 2 || bits > 4) return fail(FQ_ERR_UNSUPPORTED, "bits must be 2, 3 or 4");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  if (!D || !codes) return fail(FQ_ERR_INVALID_ARG, "NULL array argument");
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  return quantize_round_launch((hipStream_t)stream, D, K_out, K_in, bits, block, codes, Q);
+}
+
+fq_status fq_quantize_status(void* stream, int64_t K_out, int64_t K_in, int block, void* ws,
+                             size_t ws_bytes) {
+  if (!dim_ok(K_out) || !dim_ok(K_in)) return fail(FQ_ERR_INVALID_ARG, "K_out and K_in must be in [0, 2^30)");
+  if (block < 1) return fail(FQ_ERR_INVALID_ARG, "block must be >= 1");
+  if (K_out == 0 || K_in == 0) return FQ_OK;
+  fq_status st = quantize_ws_check(K_out, K_in, block, ws, ws_bytes);
+  if (st != FQ_OK) return st;
+  QuantScratch Q = quantize_scratch(K_out, K_in, block, ws);
+  return quantize_check((hipStream_t)stream, Q);
 }
 
 // A stream kept off the first reserve_cus compute units (bit c of the mask = unit c).

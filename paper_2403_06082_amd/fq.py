@@ -51,6 +51,8 @@ SIGNATURES = {
     "fq_quantize_apply": (_i, [_vp, _vp, _i64, _i64, _i, _i, _d, _vp, _vp, _vp, _vp, _sz]),
     "fq_quantize_grid": (_i, [_vp, _vp, _i64, _i64, _i, _i, _d, _vp, _vp, _vp, _sz]),
     "fq_quantize_round": (_i, [_vp, _vp, _i64, _i64, _i, _i, _vp, _vp, _sz]),
+    "fq_quantize_round_async": (_i, [_vp, _vp, _i64, _i64, _i, _i, _vp, _vp, _sz]),
+    "fq_quantize_status": (_i, [_vp, _i64, _i64, _i, _vp, _sz]),
     "fq_frame_synthesis": (_i, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp,
                                 _sz]),
     "fq_frame_synthesis_workspace_bytes": (_sz, [_i64, _i64, _i64, _i64]),
@@ -292,6 +294,28 @@ def fq_quantize_round(D, codes, ws, bits: int = 2, block: int = 128, stream=None
     _check(lib().fq_quantize_round(_stream(stream), _ptr(D), K_out, K_in, bits, block,
                                    _ptr(codes), _ptr(ws), ws.numel()))
     return codes
+
+
+def fq_quantize_round_async(D, codes, ws, bits: int = 2, block: int = 128, stream=None):
+    """fq_quantize_round without the synchronization: launches the rounding and packing;
+    the checks are reported by a later fq_quantize_status on the same stream."""
+    torch = _torch()
+    K_out, K_in = D.shape
+    _dev(D, "D", torch.float32)
+    _dev(codes, "codes", torch.int32, (K_out, words_per_row(K_in, bits)))
+    _dev(ws, "ws", torch.uint8)
+    _check(lib().fq_quantize_round_async(_stream(stream), _ptr(D), K_out, K_in, bits, block,
+                                         _ptr(codes), _ptr(ws), ws.numel()))
+    return codes
+
+
+def fq_quantize_status(K_out: int, K_in: int, ws, block: int = 128, stream=None):
+    """Synchronize the stream and raise FQError for the checks recorded in the workspace by
+    fq_quantize_prepare, fq_quantize_grid and fq_quantize_round_async."""
+    torch = _torch()
+    _dev(ws, "ws", torch.uint8)
+    _check(lib().fq_quantize_status(_stream(stream), int(K_out), int(K_in), block, _ptr(ws),
+                                    ws.numel()))
 
 
 class SideStream:

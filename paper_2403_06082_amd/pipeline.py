@@ -15,7 +15,9 @@ With a second stream (side_stream), D = P_out^T W P_in is formed there, followed
 part of the rounding that reads D only (fq_quantize_grid: clip bounds, per-row grid),
 while the main stream factors the damped H~ (fq_quantize_prepare): the Cholesky
 factorization, a chain of small dependent kernels, then overlaps the D contractions.  The
-main stream then rounds (fq_quantize_round).  Outputs are identical.
+main stream then rounds (fq_quantize_round_async) and synthesizes, and reads the checks
+at the end (fq_quantize_status), so that no synchronization sits between the rounding and
+the synthesis.  Outputs are identical.
 A side stream from fq.SideStream keeps the D kernels off part of the device, so that the
 chain always finds free compute units; it synchronizes with the legacy default stream, so
 the main stream must then be another stream (torch.cuda.Stream()).
@@ -95,9 +97,14 @@ def quantize_layer(W, X, P_out, P_in, bufs: LayerBuffers, H=None, Ht=None, bits=
         Ht = bufs.Ht
     else:
         _analysis(W, P_out, P_in, bufs, None, bufs.D, None, bufs.ws_a, stream)
-    _fq.fq_quantize_frames(bufs.D, Ht, bufs.codes, bufs.scale, bufs.zero, bits=bits, block=block,
-                           damp=damp, clip_sigmas=clip_sigmas, ws=bufs.ws_q, stream=stream)
+    # fq_quantize_frames in its parts, the checks read after the synthesis
+    _fq.fq_quantize_prepare(Ht, bufs.D.shape[0], bufs.ws_q, block=block, damp=damp, stream=stream)
+    _fq.fq_quantize_grid(bufs.D, bufs.scale, bufs.zero, bufs.ws_q, bits=bits, block=block,
+                         clip_sigmas=clip_sigmas, stream=stream)
+    _fq.fq_quantize_round_async(bufs.D, bufs.codes, bufs.ws_q, bits=bits, block=block,
+                                stream=stream)
     _synthesis(P_out, P_in, bufs, bits, stream)
+    _fq.fq_quantize_status(bufs.D.shape[0], bufs.D.shape[1], bufs.ws_q, block=block, stream=stream)
     return bufs
 
 
@@ -124,6 +131,9 @@ def _quantize_layer_two_streams(W, X, P_out, P_in, bufs, H, Ht, bits, block, dam
     d_done.record(side)
     _fq.fq_quantize_prepare(Ht, bufs.D.shape[0], bufs.ws_q, block=block, damp=damp, stream=main)
     main.wait_event(d_done)
-    _fq.fq_quantize_round(bufs.D, bufs.codes, bufs.ws_q, bits=bits, block=block, stream=main)
+    # the synthesis follows the rounding on the stream; the checks come after both
+    _fq.fq_quantize_round_async(bufs.D, bufs.codes, bufs.ws_q, bits=bits, block=block,
+                                stream=main)
     _synthesis(P_out, P_in, bufs, bits, main)
+    _fq.fq_quantize_status(bufs.D.shape[0], bufs.D.shape[1], bufs.ws_q, block=block, stream=main)
     return bufs

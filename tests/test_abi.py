@@ -98,12 +98,20 @@ def test_invalid_arguments_rejected_before_launch(L):
     assert L.fq_quantize_round(n, ctypes.c_void_p(64), -4, 4, 2, 128, *routs) == 1
     assert L.fq_quantize_round(n, ctypes.c_void_p(64), 4, 4, 2, 128, n, n, 0) == 1
     assert L.fq_quantize_round(n, ctypes.c_void_p(64), 4, 4, 2, 128, *routs) == 5
+    assert L.fq_quantize_round_async(n, ctypes.c_void_p(64), 4, 4, 1, 128, *routs) == 2
+    assert L.fq_quantize_round_async(n, ctypes.c_void_p(64), 4, 4, 2, 128, n, n, 0) == 1
+    assert L.fq_quantize_round_async(n, ctypes.c_void_p(64), 4, 4, 2, 128, *routs) == 5
+    assert L.fq_quantize_status(n, -1, 4, 128, n, 0) == 1
+    assert L.fq_quantize_status(n, 4, 4, 0, n, 0) == 1
+    assert L.fq_quantize_status(n, 4, 4, 128, n, 0) == 5
     # empty problems are no-ops
     assert L.fq_quantize_frames(n, n, n, 0, 5, 2, 128, 0.01, 2.0, n, n, n, n, 0) == 0
     assert L.fq_quantize_prepare(n, n, 0, 5, 128, 0.01, n, 0) == 0
     assert L.fq_quantize_apply(n, n, 5, 0, 2, 128, 2.0, n, n, n, n, 0) == 0
     assert L.fq_quantize_grid(n, n, 5, 0, 2, 128, 2.0, n, n, n, 0) == 0
     assert L.fq_quantize_round(n, n, 0, 5, 2, 128, n, n, 0) == 0
+    assert L.fq_quantize_round_async(n, n, 0, 5, 2, 128, n, n, 0) == 0
+    assert L.fq_quantize_status(n, 0, 5, 128, n, 0) == 0
     assert L.fq_frame_synthesis(n, n, n, n, 5, 5, n, 0, n, 5, n, n, 0) == 0
 
 

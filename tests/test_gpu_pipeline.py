@@ -149,7 +149,7 @@ def test_prepare_apply_match_fused_call():
     Ht = (Ht + Ht.T) / 2
     D = torch.from_numpy((rng.standard_normal((K_out, K_in)) * 0.02).astype(np.float32)).cuda()
     res = []
-    for split in ("fused", "prepare+apply", "prepare|grid+round"):
+    for split in ("fused", "prepare+apply", "prepare|grid+round", "round_async+status"):
         codes = torch.empty((K_out, (K_in + 15) // 16), dtype=torch.int32, device="cuda")
         scale = torch.empty((K_out,), dtype=torch.float32, device="cuda")
         zero = torch.empty((K_out,), dtype=torch.float32, device="cuda")
@@ -171,6 +171,11 @@ def test_prepare_apply_match_fused_call():
             ev.record(s2)
             s1.wait_event(ev)
             fq.fq_quantize_round(D, codes, ws, stream=s1)
+        elif split == "round_async+status":
+            fq.fq_quantize_prepare(Ht, K_out, ws)
+            fq.fq_quantize_grid(D, scale, zero, ws)
+            fq.fq_quantize_round_async(D, codes, ws)
+            fq.fq_quantize_status(K_out, K_in, ws)
         else:
             fq.fq_quantize_frames(D, Ht, codes, scale, zero, ws=ws)
         torch.cuda.synchronize()
@@ -192,6 +197,12 @@ def test_prepare_apply_match_fused_call():
     s1.wait_event(ev)
     with pytest.raises(fq.FQError) as ei:
         fq.fq_quantize_round(Dn, codes, ws, stream=s1)
+    assert ei.value.status == 4
+    # the same check reported by fq_quantize_status after the asynchronous rounding
+    fq.fq_quantize_grid(Dn, scale, zero, ws, stream=s1)
+    fq.fq_quantize_round_async(Dn, codes, ws, stream=s1)
+    with pytest.raises(fq.FQError) as ei:
+        fq.fq_quantize_status(K_out, K_in, ws, stream=s1)
     assert ei.value.status == 4
     # one factor, several applies: a non-finite D is reported by its own apply only
     ws = torch.empty((fq.fq_quantize_frames_workspace_bytes(K_out, K_in, 128),), dtype=torch.uint8,
