@@ -190,8 +190,8 @@ fq_status fq_quantize_status(void* stream, int64_t K_out, int64_t K_in, int bloc
  * of the chain then waits for units to drain.  Kernels queued on a stream made here run on
  * every compute unit but `reserve_cus` of them (the first ones in the order of the device's
  * CU mask, hipExtStreamCreateWithCUMask), which stay free for the chain.
- *   reserve_cus  in [0, n_cu / 2], n_cu the current device's compute-unit count; 0 makes an
- *                ordinary non-blocking stream.
+ *   reserve_cus  in [0, 3 n_cu / 4], n_cu the current device's compute-unit count; 0 makes
+ *                an ordinary non-blocking stream.
  *   *stream      receives the new hipStream_t of the current device (default priority);
  *                release it with fq_side_stream_destroy.
  * A stream with a CU mask synchronizes with the legacy default stream (NULL) as a blocking

@@ -712,8 +712,8 @@ fq_status fq_side_stream_create(int reserve_cus, void** stream) {
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return hip_fail(e, "compute-unit count");
-  if (reserve_cus < 0 || reserve_cus > n_cu / 2)
-    return fail(FQ_ERR_INVALID_ARG, "reserve_cus must be in [0, compute units / 2]");
+  if (reserve_cus < 0 || reserve_cus > 3 * n_cu / 4)
+    return fail(FQ_ERR_INVALID_ARG, "reserve_cus must be in [0, 3/4 of the compute units]");
   hipStream_t s = nullptr;
   if (reserve_cus == 0) {
     e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);

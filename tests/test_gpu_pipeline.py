@@ -123,7 +123,7 @@ def test_side_stream_create_and_errors():
     import ctypes
     import paper_2403_06082_amd as fq
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
-    for reserve in (0, 1, n_cu // 4, n_cu // 2):
+    for reserve in (0, 1, n_cu // 4, n_cu // 2, 3 * n_cu // 4):
         print(f"reserve {reserve} of {n_cu}", flush=True)
         s = fq.SideStream(reserve)
         x = torch.arange(1 << 20, dtype=torch.float32, device="cuda")
@@ -133,7 +133,7 @@ def test_side_stream_create_and_errors():
         assert torch.equal(y, x * 2.0 + 1.0)
         del s
     h = ctypes.c_void_p()
-    for bad in (-1, n_cu // 2 + 1, n_cu):
+    for bad in (-1, 3 * n_cu // 4 + 1, n_cu):
         assert fq.lib().fq_side_stream_create(bad, ctypes.byref(h)) == 1
     assert fq.lib().fq_side_stream_create(0, None) == 1
     assert fq.lib().fq_side_stream_destroy(None) == 1
