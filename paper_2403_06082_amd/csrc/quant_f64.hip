@@ -1037,9 +1037,22 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
     }
   }
 
-  // R' block: Rs[rr][cc] = R'[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere; every load is
-  // issued unconditionally from a clamped in-bounds address, all of a thread's at once
-  {
+  // R' block: Rs[rr][cc] = R'[i1 + rr][i1 + cc] for rr, cc < b, 0 elsewhere.  A whole
+  // chunk with 16-byte aligned rows goes global -> LDS by the DMA path, one copy per row,
+  // all in flight together; otherwise every load is issued unconditionally from a clamped
+  // in-bounds address, a batch of a thread's at once.
+  if (b == GB && (cols & 1) == 0 && (reinterpret_cast<uintptr_t>(R) & 15) == 0) {
+    const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)Rs;
+    // the block's first element, made wave-uniform for the copy's scalar base
+    const uint64_t bp = reinterpret_cast<uint64_t>(R + (int64_t)i1 * cols + i1);
+    const char* base = reinterpret_cast<const char*>(
+        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(bp >> 32)) << 32) |
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)bp));
+    for (int row = w; row < GB; row += GTH / 64)
+      lds_copy16(base, (uint32_t)((row * cols + 2 * lane) * 8), lds0 + (uint32_t)(row * GB * 8));
+    __builtin_amdgcn_s_waitcnt(0x0F70);               // vmcnt(0): this wave's rows landed
+  } else {
     constexpr int NE = GB * GB, PER = (NE + GTH - 1) / GTH, BATCH = 16;
 #pragma unroll
     for (int q0 = 0; q0 < PER; q0 += BATCH) {
