@@ -204,7 +204,7 @@ static size_t quant_layout(int64_t K_out, int64_t K_in, int block, void* ws, Qua
   q.scal = c.take<double>(8);
   q.scale64 = c.take<double>((size_t)K_out);
   q.zero64 = c.take<double>((size_t)K_out);
-  q.inv_rdiag = c.take<double>((size_t)2 * K_in);
+  q.inv_rdiag = c.take<double>((size_t)K_in);
   q.lslots = c.take<double>(2 * 64 * 64);
   q.dead = c.take<uint8_t>((size_t)K_in);
   q.flags = c.take<int>(4);

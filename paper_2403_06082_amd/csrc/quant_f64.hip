@@ -550,16 +550,11 @@ __global__ __launch_bounds__(256) void k_chol_last(double* __restrict__ A, int64
 // diagonal, R' = R diag(R)^-1: with Y = (clipped D) diag(R), OPTQ's error feedback y_c +=
 // e_J R_Jc becomes u_c += e_J R'_Jc on u = y / R_cc, the unscaled pre-rounding values, so
 // the rounding reads u_J directly and the working matrix starts as the clipped D.
-// rdiag[j] = R_jj and inv_rdiag[j] = 1 / R_jj first, then R' row by row.
+// inv_rdiag[j] = 1 / R_jj first, then R' row by row.
 __global__ __launch_bounds__(256) void k_rev_diag(const double* __restrict__ M, int64_t K,
-                                                  double* __restrict__ rdiag,
                                                   double* __restrict__ inv_rdiag) {
   const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (j < K) {
-    const double v = M[(K - 1 - j) * K + (K - 1 - j)];
-    rdiag[j] = v;
-    inv_rdiag[j] = 1.0 / v;
-  }
+  if (j < K) inv_rdiag[j] = 1.0 / M[(K - 1 - j) * K + (K - 1 - j)];
 }
 
 __global__ __launch_bounds__(256) void k_reverse_upper(const double* __restrict__ M, int64_t K,
@@ -1657,10 +1652,8 @@ hipError_t q_cholesky(double* A, int64_t K, double* Lslots, int* flags, hipStrea
 
 hipError_t q_reverse_upper(const double* A, int64_t K, double* R, double* inv_rdiag,
                            hipStream_t s) {
-  // rdiag is stored right after inv_rdiag (2 K doubles)
   prof_begin(s, "q_reverse");
-  hipLaunchKernelGGL(k_rev_diag, dim3(grid_for(K, 256)), dim3(256), 0, s, A, K, inv_rdiag + K,
-                     inv_rdiag);
+  hipLaunchKernelGGL(k_rev_diag, dim3(grid_for(K, 256)), dim3(256), 0, s, A, K, inv_rdiag);
   hipLaunchKernelGGL(k_reverse_upper, dim3(grid_for(K, 1)), dim3(256), 0, s, A, K, inv_rdiag, R);
   prof_end(s);
   return last_launch_error();
