@@ -1245,6 +1245,77 @@ __global__ __launch_bounds__(256) void k_dgemm(DgemmArgs p) {
   }
 }
 
+// The same product for 32 x 32 tiles and K <= 128 (the factorization's next-panel update,
+// a chain of short launches where every K step of k_dgemm would wait for its own loads):
+// the operands of every K step are fetched at the start, so that the loads overlap, then
+// staged through LDS one step at a time and multiplied in k_dgemm's order; C is read at
+// the start as well.
+constexpr int PF_STEPS = 8;
+__global__ __launch_bounds__(256) void k_dgemm32_short(DgemmArgs p) {
+  constexpr int DT = 32, WS = 2;
+  __shared__ double As[2][DK][DT + DPAD];
+  __shared__ double Bs[2][DK][DT + DPAD];
+  const int tm = blockIdx.x / p.tiles_n, tn = blockIdx.x - tm * p.tiles_n;
+  const int64_t m0 = (int64_t)tm * DT, n0 = (int64_t)tn * DT;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int blk = (lane >> 2) & 3, bi = blk >> 1, bj = blk & 1, q4 = lane & 3, kq = lane >> 4;
+  const int arow = wm * (DT / 2) + 4 * bi + q4;
+  const int bcol = wn * (DT / 2) + 4 * bj + q4;
+  const int nk = (int)((p.K + DK - 1) / DK);        // <= PF_STEPS
+  double ra[PF_STEPS][2], rb[PF_STEPS][2];
+#pragma unroll
+  for (int s = 0; s < PF_STEPS; ++s)
+    if (s < nk) dg_load<DT>(p, m0, n0, (int64_t)s * DK, ra[s], rb[s], tid);
+  // C's values too (clamped addresses; values outside the matrix are discarded)
+  const int64_t r0 = m0 + wm * (DT / 2) + 4 * bi + kq;
+  const int64_t c0 = n0 + wn * (DT / 2) + 4 * bj + q4;
+  double cv[WS][WS];
+#pragma unroll
+  for (int i = 0; i < WS; ++i)
+#pragma unroll
+    for (int j = 0; j < WS; ++j)
+      cv[i][j] = p.beta != 0.0 ? p.C[min(r0 + 8 * i, p.M - 1) * p.ldc + min(c0 + 8 * j, p.N - 1)] : 0.0;
+  double acc[WS][WS];
+#pragma unroll
+  for (int i = 0; i < WS; ++i)
+#pragma unroll
+    for (int j = 0; j < WS; ++j) acc[i][j] = 0.0;
+  // slot s & 1 was last read in step s - 2, before every wave passed the barrier of s - 1
+#pragma unroll
+  for (int s = 0; s < PF_STEPS; ++s) {
+    if (s >= nk) break;
+    dg_store<DT>(p, As[s & 1], Bs[s & 1], ra[s], rb[s], tid);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < DK; kk += 4) {
+      double af[WS], bfv[WS];
+#pragma unroll
+      for (int i = 0; i < WS; ++i) af[i] = As[s & 1][kk + kq][arow + 8 * i];
+#pragma unroll
+      for (int j = 0; j < WS; ++j) bfv[j] = Bs[s & 1][kk + kq][bcol + 8 * j];
+#pragma unroll
+      for (int i = 0; i < WS; ++i)
+#pragma unroll
+        for (int j = 0; j < WS; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f64_4x4x4f64(af[i], bfv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < WS; ++i) {
+    const int64_t row = r0 + 8 * i;
+#pragma unroll
+    for (int j = 0; j < WS; ++j) cv[i][j] = p.beta * cv[i][j] + p.alpha * acc[i][j];
+#pragma unroll
+    for (int j = 0; j < WS; j += 2) asm volatile("" : "+v"(cv[i][j]), "+v"(cv[i][j + 1]));
+    if (row < p.M) {
+#pragma unroll
+      for (int j = 0; j < WS; ++j)
+        if (c0 + 8 * j < p.N) p.C[row * p.ldc + c0 + 8 * j] = cv[i][j];
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp64 GEMM, LDS ring
 // C = beta C + alpha A op(B) for row-major A (M x K, rows 16-byte aligned) and B (K x N,
 // or with BT op(B)(k, n) = B[n ldb + k], rows 16-byte aligned), K a multiple of 16: the
@@ -1722,6 +1793,8 @@ hipError_t dgemm(int64_t M, int64_t N, int64_t K, double alpha, double beta, con
   const int64_t grid = lower_only ? (int64_t)tiles_m * (tiles_m + 1) / 2 : (int64_t)tiles_m * tiles_n;
   prof_begin(s, name);
   if (DT == 128) hipLaunchKernelGGL(k_dgemm<128>, dim3((unsigned)grid), dim3(256), 0, s, p);
+  else if (DT == 32 && !lower_only && p.K <= (int64_t)DK * PF_STEPS)
+    hipLaunchKernelGGL(k_dgemm32_short, dim3((unsigned)grid), dim3(256), 0, s, p);
   else if (DT == 32) hipLaunchKernelGGL(k_dgemm<32>, dim3((unsigned)grid), dim3(256), 0, s, p);
   else hipLaunchKernelGGL(k_dgemm<64>, dim3((unsigned)grid), dim3(256), 0, s, p);
   prof_end(s);
