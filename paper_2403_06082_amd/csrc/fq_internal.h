@@ -207,7 +207,8 @@ hipError_t q_gptq_block(const float* D, int64_t rows, int64_t cols, int i1, int 
 // C[M x N] = beta * C + alpha * A[M x K] * op(B)   (fp64 MFMA; beta is 0 or 1)
 //   b_trans: op(B)(k, n) = B[n * ldb + k]  else B[k * ldb + n]
 //   lower_only: only tiles with tile_row >= tile_col (for the Cholesky update)
-//   tile: 32, 64 or 128 (register-staged kernel with that tile edge), or 0: the 128 x 128
+//   tile: 32, 64 or 128 (register-staged kernel with that tile edge; 32 with K <= 128 and
+//         not lower_only fetches every K step at launch), or 0: the 128 x 128
 //         LDS-ring kernel where its layout rules hold (row-major operands, K % 16 == 0,
 //         16-byte aligned A rows), else the 64 kernel.  The ring kernel is the faster one
 //         from about 512 of its tiles up (two rounds of two work-groups per CU).

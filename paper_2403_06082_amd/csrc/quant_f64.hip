@@ -1098,8 +1098,7 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
 // C[M x N] = beta * C + alpha * A[M x K] * op(B).  Tile DT x DT (64 or 128), K step 16,
 // 256 threads = 2 x 2 waves of DT/2 x DT/2.  Operands are staged k-major in LDS ([k][m],
 // [k][n]) and the next K step is fetched into registers while the current one is
-// multiplied.  A and C may alias when every tile reads only the rows it writes (the
-// in-place triangular solve of the Cholesky panel).
+// multiplied.  C must not overlap A or B (tiles read operands that other tiles write).
 //
 // The products use v_mfma_f64_4x4x4f64, which on gfx950 sustains about 1.6x the fp64
 // rate of the 16x16x4 form.  One instruction is four independent 4 x 4 x 4 products
