@@ -656,8 +656,9 @@ constexpr int GROWS = GTH / 16 * GRK;  // 48 rows per work-group (253 groups for
 template <int O>
 __device__ __forceinline__ double row_bcast(double v) {
   const long long b = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xffffffffll), 0x150 + O, 0xf, 0xf, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), 0x150 + O, 0xf, 0xf, false);
+  // every lane of a row receives the source lane's value, so no lane keeps an old value
+  const int lo = __builtin_amdgcn_mov_dpp((int)(b & 0xffffffffll), 0x150 + O, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(b >> 32), 0x150 + O, 0xf, 0xf, false);
   return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
 
@@ -668,12 +669,16 @@ struct RoundState {
 
 // column J; rn: row J of R' (unit diagonal) at this lane's columns; rn1: the same for
 // column J + 1 (rows of R' are read from LDS two columns ahead)
-template <int J>
+// FULL: a whole chunk (b = GB), so that no column needs the early exit (an exit after
+// every column makes the compiler rematerialize the state's constant parts at each one)
+template <int J, bool FULL>
 __device__ __forceinline__ void round_col(RoundState& st, const double* __restrict__ Rs, int b,
                                           int g, double maxq, const double (&rn)[8],
                                           const double (&rn1)[8]) {
   if constexpr (J < GB) {
-    if (J >= b) return;
+    if constexpr (!FULL) {
+      if (J >= b) return;
+    }
     constexpr int O = J & 15, C = J >> 4;
     double rnext[8];
     // slots cc below (J + 2) / 16 hold columns before J + 2 in every lane: R' is upper
@@ -711,7 +716,7 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
 #pragma unroll
       for (int cc = 0; cc < 8; cc += 2)
         if (cc + 1 >= C) asm volatile("" : "+v"(st.y[k][cc]), "+v"(st.y[k][cc + 1]));
-    if constexpr (J + 1 < GB) round_col<J + 1>(st, Rs, b, g, maxq, rn1, rnext);
+    if constexpr (J + 1 < GB) round_col<J + 1, FULL>(st, Rs, b, g, maxq, rn1, rnext);
   }
 }
 
@@ -1074,7 +1079,8 @@ __global__ __launch_bounds__(GTH) void k_gptq_block(
   double rn1[8];
 #pragma unroll
   for (int cc = 0; cc < 8; ++cc) rn1[cc] = Rs[GB + g + 16 * cc];
-  round_col<0>(st, Rs, b, g, (double)maxq, rn, rn1);
+  if (b == GB) round_col<0, true>(st, Rs, b, g, (double)maxq, rn, rn1);
+  else round_col<0, false>(st, Rs, b, g, (double)maxq, rn, rn1);
 
 #pragma unroll
   for (int k = 0; k < GRK; ++k) {
