@@ -699,6 +699,9 @@ __device__ __forceinline__ void round_col(RoundState& st, const double* __restri
       if (g == O) {
         st.rr[k][C] = ek;
       }
+      // the select happens here (left to itself, the compiler may keep every column's
+      // residual to the end and select there, which spills)
+      asm volatile("" : "+v"(st.rr[k][C]));
       e[k] = row_bcast<O>(ek);
     }
     // slots below C hold columns before J (R_Jc = 0): no update; slot C is updated in
