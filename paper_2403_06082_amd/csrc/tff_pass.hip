@@ -297,30 +297,29 @@ __global__ __launch_bounds__(TT) void k_gather(const float* __restrict__ M, int6
 // for r < rows; 0 for p in [2k, pk).  codes: cpw = floor(32 / bits) per word, row-major.
 // One thread per (r, s) pair slot s < pk / 2: the rho codes of subspace s (frame columns
 // s rho .. s rho + rho - 1) go to column pair s of every block, one 32-bit store each.
+template <int BITS>
 __global__ __launch_bounds__(TT) void k_dequant_gather(const uint32_t* __restrict__ codes,
-                                                       int bits, const float* __restrict__ zero,
+                                                       const float* __restrict__ zero,
                                                        int64_t rows, int64_t K, int k, int pk,
                                                        int rho, int nb, u16* __restrict__ V,
                                                        int64_t ldv) {
-  const int cpw = 32 / bits;
-  const uint32_t mask = (1u << bits) - 1u;
-  const int64_t nw = (K + cpw - 1) / cpw;
-  const int hk = pk / 2;
-  const int64_t total = rows * hk;
-  for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * TT) {
-    const int64_t r = e / hk;
-    const int sx = (int)(e - r * hk);
+  // rho is even and so is the number of codes a word holds (16, 10 or 8), so the pair q,
+  // q + 1 (q = s rho + 2 c, even) never straddles a word
+  constexpr int CPW = 32 / BITS;
+  constexpr uint32_t MASK = (1u << BITS) - 1u;
+  const int64_t nw = (K + CPW - 1) / CPW;
+  const int sx = (int)(blockIdx.x * TT + threadIdx.x);   // column pair slot
+  if (sx >= pk / 2) return;
+  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
     const uint32_t* row = codes + r * nw;
     const float z = zero[r];
     u16* dst = V + r * ldv + 2 * sx;
     for (int c = 0; c < nb; ++c) {
       uint32_t v = 0;
       if (sx < k) {
-        const int64_t q = (int64_t)sx * rho + 2 * c;
-        const int64_t w0 = q / cpw, w1 = (q + 1) / cpw;
-        const uint32_t c0 = (row[w0] >> (bits * (int)(q - w0 * cpw))) & mask;
-        const uint32_t c1 = (row[w1] >> (bits * (int)(q + 1 - w1 * cpw))) & mask;
+        const int q = sx * rho + 2 * c;
+        const uint32_t w = row[q / CPW] >> (BITS * (q % CPW));
+        const uint32_t c0 = w & MASK, c1 = (w >> BITS) & MASK;
         v = (__float_as_uint((float)c0 - z) >> 16) | (__float_as_uint((float)c1 - z) & 0xFFFF0000u);
       }
       *reinterpret_cast<uint32_t*>(dst + (int64_t)c * pk) = v;
@@ -771,9 +770,16 @@ hipError_t tff_dequant_gather(const uint32_t* codes, int bits, const float* zero
   if (rows == 0) return hipSuccess;
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_gather");
-  hipLaunchKernelGGL(k_dequant_gather, dim3(grid_1d(rows * (g.pk / 2))), dim3(TT), 0, s, codes, bits,
-                     zero, rows, F.k * F.rho, (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V,
-                     g.nb * g.pk);
+  const dim3 grid((unsigned)((g.pk / 2 + TT - 1) / TT), (unsigned)(rows < 65535 ? rows : 65535));
+  if (bits == 2)
+    hipLaunchKernelGGL(k_dequant_gather<2>, grid, dim3(TT), 0, s, codes, zero, rows, F.k * F.rho,
+                       (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V, g.nb * g.pk);
+  else if (bits == 3)
+    hipLaunchKernelGGL(k_dequant_gather<3>, grid, dim3(TT), 0, s, codes, zero, rows, F.k * F.rho,
+                       (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V, g.nb * g.pk);
+  else
+    hipLaunchKernelGGL(k_dequant_gather<4>, grid, dim3(TT), 0, s, codes, zero, rows, F.k * F.rho,
+                       (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V, g.nb * g.pk);
   prof_end(s);
   return last_launch_error();
 }
