@@ -106,9 +106,11 @@ def algorithmic_work(n, d_out, d_in, K_out, K_in, block, rho=None, w_dtype="bf16
         add = lambda a, b: (a[0] + b[0], a[1] + b[1])
         a1, a2 = dft_i(d_out + d_in + K_in, 3), dft_o(K_in, 3)
         work["tffp_dft_an"] = ("bf16",) + add(a1, a2)
-        work["tffp_dft_syn"] = ("bf16",) + add(dft_i(K_out, 2), dft_o(d_in, 3))
+        # the synthesis from the left: the code matrix's K_in columns through P_out (exact
+        # integer operand: 2 passes), then the d_out rows through P_in
+        work["tffp_dft_syn"] = ("bf16",) + add(dft_o(K_in, 2), dft_i(d_out, 3))
         work["tffp_rotate_an"] = ("f32",) + add(rot_i(d_out + d_in + K_in), rot_o(K_in))
-        work["tffp_rotate_syn"] = ("f32",) + add(rot_i(K_out), rot_o(d_in))
+        work["tffp_rotate_syn"] = ("f32",) + add(rot_o(K_in), rot_i(d_out))
     hess_tiles = (-(-d_in // 256)) * (-(-d_in // 256) + 1) // 2
     passes = {"gemm_hessian": 1, "gemm_analysis_w1": 2 if w_dtype == "bf16" else 3,
               "gemm_analysis_w2": 3, "gemm_analysis_h1": 3, "gemm_analysis_h2": 3,

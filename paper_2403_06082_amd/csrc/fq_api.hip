@@ -1362,17 +1362,17 @@ struct TffSynLayout {
 static size_t tff_syn_layout(const fq_tff* fo, const fq_tff* fi, void* base, TffSynLayout* L) {
   const TffDev Fo = tff_dev_of(fo), Fi = tff_dev_of(fi);
   const TffPassGeom go = tff_pass_geom(Fo), gi = tff_pass_geom(Fi);
-  const int64_t d_out = fo->d, d_in = fi->d, K_out = fo->k * fo->rho;
-  const int64_t big = std::max(K_out * d_in, d_in * d_out);
+  const int64_t d_out = fo->d, d_in = fi->d, K_in = fi->k * fi->rho;
+  const int64_t big = std::max(K_in * d_out, d_out * d_in);
   Carver c(base);
   TffSynLayout l{};
   l.fi_hi = c.take<u16>((size_t)(gi.nb * gi.pm * gi.pk));
   l.fi_lo = c.take<u16>((size_t)(gi.nb * gi.pm * gi.pk));
   l.fo_hi = c.take<u16>((size_t)(go.nb * go.pm * go.pk));
   l.fo_lo = c.take<u16>((size_t)(go.nb * go.pm * go.pk));
-  l.v1 = c.take<u16>((size_t)(K_out * gi.nb * gi.pk));
-  l.v2_hi = c.take<u16>((size_t)(d_in * go.nb * go.pk));
-  l.v2_lo = c.take<u16>((size_t)(d_in * go.nb * go.pk));
+  l.v1 = c.take<u16>((size_t)(K_in * go.nb * go.pk));
+  l.v2_hi = c.take<u16>((size_t)(d_out * gi.nb * gi.pk));
+  l.v2_lo = c.take<u16>((size_t)(d_out * gi.nb * gi.pk));
   l.z = c.take<float>((size_t)big);
   l.tmp = c.take<float>((size_t)big);
   l.mid = c.take<float>((size_t)big);
@@ -1400,24 +1400,26 @@ fq_status fq_frame_synthesis_tff(void* stream, const uint32_t* codes, int bits,
   hipStream_t s = (hipStream_t)stream;
   TffSynLayout L;
   tff_syn_layout(frame_out, frame_in, (void*)(((uintptr_t)ws + 255) & ~(uintptr_t)255), &L);
-  const int64_t K_out = Fo.k * Fo.rho;
+  const int64_t K_in = Fi.k * Fi.rho;
   hipError_t e;
+  // W^ = P_out diag(scale) (Q - zero) P_in^T, formed from the left: the output frame's
+  // blocks carry the scale (P_out diag(scale)), so the code matrix enters as exact
+  // integers, and the last synthesis writes rows of W^ directly
   if ((e = tff_dft_blocks(Fi, L.fi_hi, L.fi_lo, s)) != hipSuccess) return hip_fail(e, "frame_in blocks");
-  if ((e = tff_dft_blocks(Fo, L.fo_hi, L.fo_lo, s)) != hipSuccess) return hip_fail(e, "frame_out blocks");
-  // M = (Q - zero) P_in^T: K_out x d_in
-  if ((e = tff_dequant_gather(codes, bits, zero, K_out, Fi, L.v1, s)) != hipSuccess)
+  if ((e = tff_dft_blocks(Fo, L.fo_hi, L.fo_lo, s, scale)) != hipSuccess)
+    return hip_fail(e, "frame_out blocks");
+  // N = (P_out diag(scale) (Q - zero))^T: K_in x d_out, from the columns of the codes
+  if ((e = tff_dequant_gather_t(codes, bits, zero, K_in, Fo, L.v1, s)) != hipSuccess)
     return hip_fail(e, "dequant");
-  if ((e = tff_rows_synthesis(L.v1, nullptr, K_out, Fi, L.fi_hi, L.fi_lo, L.z, L.tmp, L.mid,
-                              Fi.d, s)) != hipSuccess)
-    return hip_fail(e, "synthesis of the code rows");
-  // W_hat^T = (diag(scale) M)^T P_out^T: d_in x d_out, then transposed
-  if ((e = tff_gather_rows(L.mid, Fi.d, Fi.d, scale, Fo, L.v2_hi, L.v2_lo, s)) != hipSuccess)
-    return hip_fail(e, "gather");
-  if ((e = tff_rows_synthesis(L.v2_hi, L.v2_lo, Fi.d, Fo, L.fo_hi, L.fo_lo, L.z, L.tmp, L.mid,
+  if ((e = tff_rows_synthesis(L.v1, nullptr, K_in, Fo, L.fo_hi, L.fo_lo, L.z, L.tmp, L.mid,
                               Fo.d, s)) != hipSuccess)
-    return hip_fail(e, "synthesis of the columns");
-  if ((e = transpose_f32(L.mid, Fi.d, Fo.d, Fo.d, W_hat, Fi.d, s)) != hipSuccess)
-    return hip_fail(e, "transpose");
+    return hip_fail(e, "synthesis of the code columns");
+  // W^ = (N^T) P_in^T: d_out rows
+  if ((e = tff_gather_rows(L.mid, Fo.d, Fo.d, nullptr, Fi, L.v2_hi, L.v2_lo, s)) != hipSuccess)
+    return hip_fail(e, "gather");
+  if ((e = tff_rows_synthesis(L.v2_hi, L.v2_lo, Fo.d, Fi, L.fi_hi, L.fi_lo, L.z, L.tmp, W_hat,
+                              Fi.d, s)) != hipSuccess)
+    return hip_fail(e, "synthesis of the rows");
   return FQ_OK;
 }
 

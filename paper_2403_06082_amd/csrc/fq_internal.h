@@ -127,8 +127,10 @@ hipError_t tff_transpose_r2(const TffDev& F, float* R2t, hipStream_t s);
 // frame coordinates (padded to pk), pads multiples of 32.
 struct TffPassGeom { int64_t nb, m2, pm, k2, pk; };
 TffPassGeom tff_pass_geom(const TffDev& F);
-// F_c for all blocks: bf16 (hi, lo) planes of nb x pm x pk each
-hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s);
+// F_c for all blocks: bf16 (hi, lo) planes of nb x pm x pk each; with colscale (K
+// entries), the blocks of P diag(colscale)
+hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s,
+                          const float* colscale = nullptr);
 // out (K x n at stride ldout) = (X P)^T for n rows of X (element type xt, stride ldx).
 // Scratch: tmp / O one fp32 buffer of max(n d, n K) (they may alias), Y pair planes of
 // n x nb pm each.
@@ -138,16 +140,15 @@ hipError_t tff_rows_analysis_t(const void* X, int xt, int64_t ldx, int64_t n, co
 // V planes (n x nb pk, block order) from M (K x n, stride ldm) with row q scaled by scale[q]
 hipError_t tff_gather_rows(const float* M, int64_t ldm, int64_t n, const float* scale,
                            const TffDev& F, u16* hi, u16* lo, hipStream_t s);
-// V plane (rows x nb pk, block order) = codes - zero, exact bf16
-hipError_t tff_dequant_gather(const uint32_t* codes, int bits, const float* zero, int64_t rows,
-                              const TffDev& F, u16* V, hipStream_t s);
+// V plane (cols x nb pk, block order of F) = (codes - zero)^T, exact bf16: the code
+// matrix (F.k F.rho rows, cols columns) read down its columns; zero per code row
+hipError_t tff_dequant_gather_t(const uint32_t* codes, int bits, const float* zero, int64_t cols,
+                                const TffDev& F, u16* V, hipStream_t s);
 // out (n x d at stride ldout) = V P^T from block-order planes (Vlo may be NULL); Z, tmp:
 // n x d fp32 scratch each
 hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const TffDev& F,
                               const u16* Fhi, const u16* Flo, float* Z, float* tmp, float* out,
                               int64_t ldout, hipStream_t s);
-hipError_t transpose_f32(const float* in, int64_t rows, int64_t cols, int64_t ldin, float* out,
-                         int64_t ldout, hipStream_t s);
 hipError_t sym_average(float* X, int64_t n, int64_t ld, hipStream_t s);
 
 // Seeded Haar factor f (tff_seed.hip): out (n x n fp32) from seed; G, V: n x n fp64

@@ -220,8 +220,11 @@ __global__ __launch_bounds__(TT) void k_zero_pads(u16* hi, u16* lo, int64_t n, i
 // F_c for c < rho/2 as bf16 (hi, lo) planes [c][pm][pk] (rows 2j + e, columns 2s + e'),
 // zero outside 2m x 2k.  One thread per 2 x 2 entry block (c, j, s): one phase, four
 // entries, 32-bit stores (pm and pk are even).
+// colscale (may be NULL): frame vector q = s rho + 2c + e (column 2s + e of block c) scaled
+// by colscale[q], i.e. the blocks of P diag(colscale)
 __global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm, int pk,
-                                                   float scale, u16* __restrict__ hi,
+                                                   float scale, const float* __restrict__ colscale,
+                                                   int rho, u16* __restrict__ hi,
                                                    u16* __restrict__ lo) {
   const int hm = pm / 2, hk = pk / 2;
   const int64_t total = (int64_t)nb * hm * hk;
@@ -238,7 +241,12 @@ __global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm,
       sn *= scale;
     }
     // rows 2j (x) and 2j + 1 (y); columns 2s (re) and 2s + 1 (im)
-    const float v00 = cs, v01 = -sn, v10 = sn, v11 = cs;
+    float a0 = 1.f, a1 = 1.f;
+    if (colscale && sx < k) {
+      a0 = colscale[(int64_t)sx * rho + 2 * c];
+      a1 = colscale[(int64_t)sx * rho + 2 * c + 1];
+    }
+    const float v00 = cs * a0, v01 = -sn * a1, v10 = sn * a0, v11 = cs * a1;
     auto pair = [](float a, float b, uint32_t& h, uint32_t& l) {
       const uint32_t ha = rne_bf16(a), hb = rne_bf16(b);
       h = ha | (hb << 16);
@@ -293,56 +301,51 @@ __global__ __launch_bounds__(TT) void k_gather(const float* __restrict__ M, int6
   }
 }
 
-// V[r][c pk + p] = code(r, q) - zero[r] as bf16 (small integers, exact), q as in k_gather,
-// for r < rows; 0 for p in [2k, pk).  codes: cpw = floor(32 / bits) per word, row-major.
-// One thread per (r, s) pair slot s < pk / 2: the rho codes of subspace s (frame columns
-// s rho .. s rho + rho - 1) go to column pair s of every block, one 32-bit store each.
+// The codes read down their columns: V[t][c pk + 2s + e] = code(q, t) - zero[q] as bf16
+// (small integers, exact), q = s rho + 2c + e, for the code matrix's columns t < cols and
+// s < k; 0 for s in [k, pk / 2).  codes: rows x ceil(cols / cpw) words, cpw = floor(32 / bits)
+// codes a word, row-major.  A work-group takes 32 columns t and 32 pair slots s of one block
+// c: the 64 code rows through LDS, then rows of V in 128-byte pieces.
+// grid (ceil(cols / 32), ceil(pk / 64), rho / 2).
 template <int BITS>
-__global__ __launch_bounds__(TT) void k_dequant_gather(const uint32_t* __restrict__ codes,
-                                                       const float* __restrict__ zero,
-                                                       int64_t rows, int64_t K, int k, int pk,
-                                                       int rho, int nb, u16* __restrict__ V,
-                                                       int64_t ldv) {
-  // rho is even and so is the number of codes a word holds (16, 10 or 8), so the pair q,
-  // q + 1 (q = s rho + 2 c, even) never straddles a word
+__global__ __launch_bounds__(TT) void k_dequant_gather_t(const uint32_t* __restrict__ codes,
+                                                         const float* __restrict__ zero,
+                                                         int64_t cols, int k, int pk, int rho,
+                                                         u16* __restrict__ V, int64_t ldv) {
   constexpr int CPW = 32 / BITS;
   constexpr uint32_t MASK = (1u << BITS) - 1u;
-  const int64_t nw = (K + CPW - 1) / CPW;
-  const int sx = (int)(blockIdx.x * TT + threadIdx.x);   // column pair slot
-  if (sx >= pk / 2) return;
-  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
-    const uint32_t* row = codes + r * nw;
-    const float z = zero[r];
-    u16* dst = V + r * ldv + 2 * sx;
-    for (int c = 0; c < nb; ++c) {
-      uint32_t v = 0;
-      if (sx < k) {
-        const int q = sx * rho + 2 * c;
-        const uint32_t w = row[q / CPW] >> (BITS * (q % CPW));
-        const uint32_t c0 = w & MASK, c1 = (w >> BITS) & MASK;
-        v = (__float_as_uint((float)c0 - z) >> 16) | (__float_as_uint((float)c1 - z) & 0xFFFF0000u);
+  __shared__ float tile[64][33];
+  const int64_t nw = (cols + CPW - 1) / CPW;
+  const int64_t t0 = (int64_t)blockIdx.x * 32;
+  const int s0 = blockIdx.y * 32, c = blockIdx.z;
+  const int tid = threadIdx.x;
+  {  // code row i: slot s0 + i / 2, e = i % 2; this thread's 8 columns of it
+    const int i = tid >> 2, tq = (tid & 3) * 8;
+    const int sx = s0 + (i >> 1);
+    const bool in = sx < k;
+    const int64_t q = in ? (int64_t)sx * rho + 2 * c + (i & 1) : 0;
+    const uint32_t* row = codes + q * nw;
+    const float z = in ? zero[q] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int64_t t = t0 + tq + u;
+      float v = 0.f;
+      if (in && t < cols) {
+        const uint32_t w = row[t / CPW] >> (BITS * (int)(t % CPW));
+        v = (float)(w & MASK) - z;
       }
-      *reinterpret_cast<uint32_t*>(dst + (int64_t)c * pk) = v;
+      tile[i][tq + u] = v;
     }
   }
-}
-
-// out[j][i] = in[i][j] for i < rows, j < cols; 32 x 32 tiles through LDS.
-__global__ __launch_bounds__(TT) void k_transpose_rect(const float* __restrict__ in, int64_t rows,
-                                                       int64_t cols, int64_t ldin,
-                                                       float* __restrict__ out, int64_t ldout) {
-  __shared__ float tile[32][33];
-  const int64_t ncb = (cols + 31) / 32;
-  const int64_t bi = blockIdx.x / ncb, bj = blockIdx.x - bi * ncb;
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  for (int q = ty; q < 32; q += 8) {
-    const int64_t i = bi * 32 + q, j = bj * 32 + tx;
-    tile[q][tx] = (i < rows && j < cols) ? in[i * ldin + j] : 0.f;
-  }
   __syncthreads();
-  for (int q = ty; q < 32; q += 8) {
-    const int64_t j = bj * 32 + q, i = bi * 32 + tx;
-    if (i < rows && j < cols) out[j * ldout + i] = tile[tx][q];
+  const int sl = tid & 31;
+  if (s0 + sl >= pk / 2) return;
+  for (int tl = tid >> 5; tl < 32; tl += TT / 32) {
+    const int64_t t = t0 + tl;
+    if (t >= cols) break;
+    const uint32_t v = (__float_as_uint(tile[2 * sl][tl]) >> 16) |
+                       (__float_as_uint(tile[2 * sl + 1][tl]) & 0xFFFF0000u);
+    *reinterpret_cast<uint32_t*>(V + t * ldv + (int64_t)c * pk + 2 * (s0 + sl)) = v;
   }
 }
 
@@ -711,12 +714,12 @@ TffPassGeom tff_pass_geom(const TffDev& F) {
   return g;
 }
 
-hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s) {
+hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s, const float* colscale) {
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_blocks");
   hipLaunchKernelGGL(k_dft_blocks, dim3(grid_1d(g.nb * (g.pm / 2) * (g.pk / 2))), dim3(TT), 0, s, (int)F.k,
                      (int)F.m, (int)g.nb, (int)g.pm, (int)g.pk,
-                     (float)(1.0 / std::sqrt((double)F.k)), hi, lo);
+                     (float)(1.0 / std::sqrt((double)F.k)), colscale, (int)F.rho, hi, lo);
   prof_end(s);
   return last_launch_error();
 }
@@ -765,21 +768,21 @@ hipError_t tff_gather_rows(const float* M, int64_t ldm, int64_t n, const float* 
   return last_launch_error();
 }
 
-hipError_t tff_dequant_gather(const uint32_t* codes, int bits, const float* zero, int64_t rows,
-                              const TffDev& F, u16* V, hipStream_t s) {
-  if (rows == 0) return hipSuccess;
+hipError_t tff_dequant_gather_t(const uint32_t* codes, int bits, const float* zero, int64_t cols,
+                                const TffDev& F, u16* V, hipStream_t s) {
+  if (cols == 0) return hipSuccess;
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_gather");
-  const dim3 grid((unsigned)((g.pk / 2 + TT - 1) / TT), (unsigned)(rows < 65535 ? rows : 65535));
+  const dim3 grid((unsigned)((cols + 31) / 32), (unsigned)((g.pk / 2 + 31) / 32), (unsigned)g.nb);
   if (bits == 2)
-    hipLaunchKernelGGL(k_dequant_gather<2>, grid, dim3(TT), 0, s, codes, zero, rows, F.k * F.rho,
-                       (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V, g.nb * g.pk);
+    hipLaunchKernelGGL(k_dequant_gather_t<2>, grid, dim3(TT), 0, s, codes, zero, cols, (int)F.k,
+                       (int)g.pk, (int)F.rho, V, g.nb * g.pk);
   else if (bits == 3)
-    hipLaunchKernelGGL(k_dequant_gather<3>, grid, dim3(TT), 0, s, codes, zero, rows, F.k * F.rho,
-                       (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V, g.nb * g.pk);
+    hipLaunchKernelGGL(k_dequant_gather_t<3>, grid, dim3(TT), 0, s, codes, zero, cols, (int)F.k,
+                       (int)g.pk, (int)F.rho, V, g.nb * g.pk);
   else
-    hipLaunchKernelGGL(k_dequant_gather<4>, grid, dim3(TT), 0, s, codes, zero, rows, F.k * F.rho,
-                       (int)F.k, (int)g.pk, (int)F.rho, (int)g.nb, V, g.nb * g.pk);
+    hipLaunchKernelGGL(k_dequant_gather_t<4>, grid, dim3(TT), 0, s, codes, zero, cols, (int)F.k,
+                       (int)g.pk, (int)F.rho, V, g.nb * g.pk);
   prof_end(s);
   return last_launch_error();
 }
@@ -809,16 +812,6 @@ hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const T
   RotOut o{};
   o.f = out; o.ldf = ldout;
   return rotate_rows<0>(Z, 0, F.d, n, F, true, tmp, o, s, "tffp_rotate_syn");
-}
-
-hipError_t transpose_f32(const float* in, int64_t rows, int64_t cols, int64_t ldin, float* out,
-                         int64_t ldout, hipStream_t s) {
-  if (rows == 0 || cols == 0) return hipSuccess;
-  prof_begin(s, "tffp_gather");
-  hipLaunchKernelGGL(k_transpose_rect, dim3((unsigned)(((rows + 31) / 32) * ((cols + 31) / 32))), dim3(TT), 0, s,
-                     in, rows, cols, ldin, out, ldout);
-  prof_end(s);
-  return last_launch_error();
 }
 
 hipError_t sym_average(float* X, int64_t n, int64_t ld, hipStream_t s) {
