@@ -1354,8 +1354,8 @@ fq_status fq_frame_analysis_tff(void* stream, const void* W, int wt, const fq_tf
 
 struct TffSynLayout {
   u16 *fi_hi, *fi_lo, *fo_hi, *fo_lo;
-  u16* v1;              // codes - zero, block order of frame_in (K_out rows)
-  u16 *v2_hi, *v2_lo;   // scaled (Q - zero) P_in^T transposed, block order of frame_out
+  u16* v1;              // (codes - zero)^T, block order of frame_out (K_in rows)
+  u16 *v2_hi, *v2_lo;   // P_out diag(scale) (Q - zero), block order of frame_in (d_out rows)
   float *z, *tmp, *mid;
 };
 

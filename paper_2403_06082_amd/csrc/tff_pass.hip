@@ -265,19 +265,20 @@ __global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm,
 
 // V[t][c pk + p] = scale[q] M[q][t], q = (p/2) rho + 2c + (p&1), as bf16 (hi, lo) for
 // p < 2k, t < n; 0 for p in [2k, pk).  M is K x n (rows q at stride ldm); scale may be
-// NULL (1).  grid (ceil(pk/32) * ceil(n/32), rho/2).
+// NULL (1).  A work-group takes 64 p by 32 t through LDS and writes each row t of both
+// planes as 128-byte pieces (four bf16 a thread).  grid (ceil(pk/64) * ceil(n/32), rho/2).
 __global__ __launch_bounds__(TT) void k_gather(const float* __restrict__ M, int64_t ldm, int64_t n,
                                                const float* __restrict__ scale, int k2, int pk,
                                                int rho, u16* __restrict__ hi,
                                                u16* __restrict__ lo, int64_t ldv) {
-  __shared__ float tile[32][33];
+  __shared__ float tile[64][33];
   const int c = blockIdx.y;
-  const int npb = pk / 32;
+  const int npb = (pk + 63) / 64;
   const int64_t tb = blockIdx.x / npb;
   const int pbk = (int)(blockIdx.x - tb * npb);
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  for (int q = ty; q < 32; q += 8) {
-    const int p = pbk * 32 + q;
+  for (int q = ty; q < 64; q += 8) {
+    const int p = pbk * 64 + q;
     const int64_t t = tb * 32 + tx;
     float v = 0.f;
     if (p < k2 && t < n) {
@@ -288,16 +289,23 @@ __global__ __launch_bounds__(TT) void k_gather(const float* __restrict__ M, int6
     tile[q][tx] = v;
   }
   __syncthreads();
-  for (int q = ty; q < 32; q += 8) {
-    const int64_t t = tb * 32 + q;
-    const int p = pbk * 32 + tx;
-    if (t < n) {
-      const float v = tile[tx][q];
-      const uint32_t h = rne_bf16(v);
-      const int64_t idx = t * ldv + (int64_t)c * pk + p;
-      hi[idx] = (u16)h;
-      lo[idx] = (u16)rne_bf16(v - __uint_as_float(h << 16));
+  // thread: p quad pq = tid % 16 of rows t = tid / 16 and tid / 16 + 16
+  const int pq = threadIdx.x & 15;
+  const int p = pbk * 64 + 4 * pq;
+  if (p >= pk) return;
+  for (int tl = threadIdx.x >> 4; tl < 32; tl += TT / 16) {
+    const int64_t t = tb * 32 + tl;
+    if (t >= n) break;
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float v = tile[4 * pq + u][tl];
+      h[u] = rne_bf16(v);
+      l[u] = rne_bf16(v - __uint_as_float(h[u] << 16));
     }
+    const int64_t idx = t * ldv + (int64_t)c * pk + p;
+    *reinterpret_cast<uint2*>(hi + idx) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    *reinterpret_cast<uint2*>(lo + idx) = make_uint2(l[0] | (l[1] << 16), l[2] | (l[3] << 16));
   }
 }
 
@@ -762,7 +770,7 @@ hipError_t tff_gather_rows(const float* M, int64_t ldm, int64_t n, const float* 
   if (n == 0) return hipSuccess;
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_gather");
-  hipLaunchKernelGGL(k_gather, dim3((unsigned)(((n + 31) / 32) * (g.pk / 32)), (unsigned)g.nb), dim3(TT), 0, s,
+  hipLaunchKernelGGL(k_gather, dim3((unsigned)(((n + 31) / 32) * ((g.pk + 63) / 64)), (unsigned)g.nb), dim3(TT), 0, s,
                      M, ldm, n, scale, (int)g.k2, (int)g.pk, (int)F.rho, hi, lo, g.nb * g.pk);
   prof_end(s);
   return last_launch_error();
