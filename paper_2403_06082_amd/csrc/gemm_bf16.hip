@@ -887,26 +887,33 @@ __global__ __launch_bounds__(256) void k_syrk_reduce(const float* __restrict__ p
   const int tidx = blockIdx.x >> 4;
   const int i0 = tm * BM + sr * 64, j0 = tn * BN + sc * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  // sums: 4 consecutive columns per thread (16-byte loads), the splits in order, four
-  // loads in flight at a time
+  // sums: 4 consecutive columns per thread (16-byte loads), the splits in order, up to
+  // sixteen loads in flight at a time
   const int c4 = (threadIdx.x & 15) * 4, rq = threadIdx.x >> 4;
   const int64_t sstride = (int64_t)ntiles * (BM * BN);
   for (int r = rq; r < 64; r += 16) {
     const float* p0 = part + (int64_t)tidx * (BM * BN) + (int64_t)(sr * 64 + r) * BN + sc * 64 + c4;
     double sum[4] = {0.0, 0.0, 0.0, 0.0};
     int s = 0;
-    for (; s + 4 <= ksplit; s += 4) {
-      float4 v[4];
+    for (; s + 16 <= ksplit; s += 16) {
+      float4 v[16];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = *reinterpret_cast<const float4*>(p0 + (s + q) * sstride);
+      for (int q = 0; q < 16; ++q) v[q] = *reinterpret_cast<const float4*>(p0 + (s + q) * sstride);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < 16; ++q) {
         sum[0] += v[q].x; sum[1] += v[q].y; sum[2] += v[q].z; sum[3] += v[q].w;
       }
     }
-    for (; s < ksplit; ++s) {
-      const float4 v = *reinterpret_cast<const float4*>(p0 + s * sstride);
-      sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+    if (s < ksplit) {         // the rest (fewer than 16), all loaded before the sums
+      float4 v[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        if (s + q < ksplit) v[q] = *reinterpret_cast<const float4*>(p0 + (s + q) * sstride);
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        if (s + q < ksplit) {
+          sum[0] += v[q].x; sum[1] += v[q].y; sum[2] += v[q].z; sum[3] += v[q].w;
+        }
     }
     const int i = i0 + r;
 #pragma unroll
