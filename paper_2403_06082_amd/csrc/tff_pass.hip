@@ -327,22 +327,23 @@ __global__ __launch_bounds__(TT) void k_dequant_gather_t(const uint32_t* __restr
   const int64_t t0 = (int64_t)blockIdx.x * 32;
   const int s0 = blockIdx.y * 32, c = blockIdx.z;
   const int tid = threadIdx.x;
-  {  // code row i: slot s0 + i / 2, e = i % 2; this thread's 8 columns of it
+  {  // code row i: slot s0 + i / 2, e = i % 2; this thread's 8 columns of it, which lie
+     // in at most two words (a word holds at least 8 codes)
     const int i = tid >> 2, tq = (tid & 3) * 8;
     const int sx = s0 + (i >> 1);
     const bool in = sx < k;
     const int64_t q = in ? (int64_t)sx * rho + 2 * c + (i & 1) : 0;
     const uint32_t* row = codes + q * nw;
     const float z = in ? zero[q] : 0.f;
+    const int64_t ta = t0 + tq, wa = ta / CPW;
+    const uint32_t w0 = (in && ta < cols) ? row[wa] : 0u;
+    const uint32_t w1 = (in && wa + 1 < nw) ? row[wa + 1] : 0u;
+    const int off = (int)(ta - wa * CPW);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int64_t t = t0 + tq + u;
-      float v = 0.f;
-      if (in && t < cols) {
-        const uint32_t w = row[t / CPW] >> (BITS * (int)(t % CPW));
-        v = (float)(w & MASK) - z;
-      }
-      tile[i][tq + u] = v;
+      const int pos = off + u;                       // code position from word wa
+      const uint32_t w = pos < CPW ? (w0 >> (BITS * pos)) : (w1 >> (BITS * (pos - CPW)));
+      tile[i][tq + u] = (in && ta + u < cols) ? (float)(w & MASK) - z : 0.f;
     }
   }
   __syncthreads();
