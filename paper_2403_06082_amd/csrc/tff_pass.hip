@@ -382,7 +382,7 @@ __global__ __launch_bounds__(TT) void k_sym_average(float* __restrict__ X, int64
 
 // ---- both rotation factors of a row in one work-group.
 // out_t = A X_t B with X_t the d1 x d2 view of row t; analysis: A = R1^T, B = R2; synthesis:
-// A = R1, B = R2^T.  A work-group of NW waves takes FR_NV consecutive rows and one block of
+// A = R1, B = R2^T.  A work-group of NW waves takes nv consecutive rows and one block of
 // BJ = 16 NW output columns; wave w forms the 16 columns [16 w, 16 w + 16) of the block for
 // every output row, with v_mfma_f32_16x16x4_f32 on 16 x 16 tiles:
 //  step A  T = X_t B[:, cols], K = d2.  Inside a chunk of 16 k values, at step s lane l
@@ -434,7 +434,7 @@ template <typename XT, bool SYN, int OUT, int MT, int NQ, int NW>
 __global__ __launch_bounds__(64 * NW) void k_rot_fused(const XT* __restrict__ X, int64_t ldx,
                                                        int64_t n, const float* __restrict__ R1,
                                                        const float* __restrict__ R2, int d1,
-                                                       int d2, int vout, RotOut o) {
+                                                       int d2, int vout, int nv, RotOut o) {
   extern __shared__ __attribute__((aligned(16))) float fr_lds[];
   constexpr int M = 16 * MT;                   // d1 padded
   constexpr int BJ = 16 * NW;                  // output columns per work-group
@@ -448,7 +448,7 @@ __global__ __launch_bounds__(64 * NW) void k_rot_fused(const XT* __restrict__ X,
   float* As = Bs + BJ * PX;                    // [M][PA]   A[i][k]
   const int njb = (d2 + BJ - 1) / BJ;
   const int jb = (int)(blockIdx.x % njb);
-  const int64_t t0 = (int64_t)(blockIdx.x / njb) * FR_NV;
+  const int64_t t0 = (int64_t)(blockIdx.x / njb) * nv;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c = lane & 15, g = lane >> 4;
 
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(64 * NW) void k_rot_fused(const XT* __restrict__ X,
   for (int e = tid; e < (M - d1) * K2; e += NT) Xs[d1 * PX + (e / K2) * PX + e % K2] = 0.f;
   const int kpad = K2 - d2;
 
-  for (int v = 0; v < FR_NV; ++v) {
+  for (int v = 0; v < nv; ++v) {
     const int64_t t = t0 + v;
     if (t >= n) break;
     __syncthreads();                 // the previous row's output has left the LDS
@@ -517,7 +517,7 @@ __global__ __launch_bounds__(64 * NW) void k_rot_fused(const XT* __restrict__ X,
       if (tid + NT * q < nq)
         *reinterpret_cast<float4*>(&Xs[loff[q]]) = fr_cvt(pre[q], (const XT*)nullptr);
     __syncthreads();
-    if (v + 1 < FR_NV && t + 1 < n) fetch(t + 1);
+    if (v + 1 < nv && t + 1 < n) fetch(t + 1);
 
     // step A: T[:, 16 w + c] for all M rows; the MT accumulators interleave
     floatx4 acc[MT];
@@ -617,8 +617,23 @@ void launch_rot_fused(const XT* X, int64_t ldx, int64_t n, const TffDev& F, cons
                       hipStream_t s) {
   const int MT = fr_mt(F.d1), NW = fr_waves(F.d2);
   const int njb = (F.d2 + 16 * NW - 1) / (16 * NW);
-  const dim3 g((unsigned)(njb * ((n + FR_NV - 1) / FR_NV))), b((unsigned)(64 * NW));
   const size_t lds = (size_t)fr_lds_floats(F.d1, F.d2) * sizeof(float);
+  // rows per work-group: at least FR_NV (the resident factors serve them all), and as
+  // many as fill the device's work-group slots in one round when that takes fewer row
+  // times than rounds of FR_NV rows (e.g. 4512 rows of the 11008-wide frame: one round of
+  // 18 rows instead of five of 4)
+  static int n_cu = 0;
+  if (n_cu <= 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n_cu <= 0)
+      n_cu = 1;
+  }
+  const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>((int64_t)(160 * 1024) / (int64_t)lds, 32 / NW));
+  const int64_t groups = std::max<int64_t>(1, (int64_t)n_cu * per_cu / njb);   // row groups at once
+  const int nv = (int)std::max<int64_t>(FR_NV, std::min<int64_t>((n + groups - 1) / groups, 64));
+  const dim3 g((unsigned)(njb * ((n + nv - 1) / nv))), b((unsigned)(64 * NW));
   const bool small = (int64_t)F.d1 * (F.d2 / 4) <= 64 * NW * 4;
   // 16-byte output runs: 8-element runs start 16-byte aligned in every destination row
   int vout;
@@ -634,7 +649,7 @@ void launch_rot_fused(const XT* X, int64_t ldx, int64_t n, const TffDev& F, cons
           reinterpret_cast<const void*>(k_rot_fused<XT, SYN, OUT, m, q, nw>), \
           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024); \
       (void)attr; \
-      hipLaunchKernelGGL((k_rot_fused<XT, SYN, OUT, m, q, nw>), g, b, lds, s, X, ldx, n, F.R1, F.R2, F.d1, F.d2, vout, o); }
+      hipLaunchKernelGGL((k_rot_fused<XT, SYN, OUT, m, q, nw>), g, b, lds, s, X, ldx, n, F.R1, F.R2, F.d1, F.d2, vout, nv, o); }
 #define FR_CASE(m) case m: \
       if (NW == 4) { if (small) FR_LAUNCH(m, 4, 4) else FR_LAUNCH(m, FR_MAXQ, 4) } \
       else { if (small) FR_LAUNCH(m, 4, 8) else FR_LAUNCH(m, 8, 8) } \
