@@ -833,7 +833,7 @@ def main():
                     help="2 (default): D is formed on a second stream while the main stream "
                          "factors H~ (the factorization is a chain of small kernels that leaves "
                          "most CUs idle); 1: one stream.  The kernel-timer region always uses one")
-    ap.add_argument("--reserve-cus", type=int, default=128,
+    ap.add_argument("--reserve-cus", type=int, default=144,
                     help="with two streams, the second is made by fq_side_stream_create and its "
                          "kernels stay off this many compute units, which the factorization's "
                          "chain keeps for itself (0: an ordinary second stream)")

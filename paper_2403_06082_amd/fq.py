@@ -323,7 +323,7 @@ class SideStream:
     usable wherever a torch stream is (`.stream` is a torch.cuda.ExternalStream).  Released
     with the object."""
 
-    def __init__(self, reserve_cus: int = 128, device=None):
+    def __init__(self, reserve_cus: int = 144, device=None):
         torch = _torch()
         dev = torch.device("cuda", torch.cuda.current_device() if device is None else device)
         self._h = None
