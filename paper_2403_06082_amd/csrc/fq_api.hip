@@ -283,6 +283,17 @@ static fq_status scratch_of_current_device(void** out) {
   return FQ_OK;
 }
 
+// Streams made by fq_side_stream_create (their kernels share part of the device with the
+// caller's other work), so that launchers can size their grids for dynamic balancing there.
+static std::mutex g_side_mu;
+static std::vector<hipStream_t> g_side_streams;
+
+bool fq::is_side_stream(hipStream_t s) {
+  if (!s) return false;
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  return std::find(g_side_streams.begin(), g_side_streams.end(), s) != g_side_streams.end();
+}
+
 extern "C" {
 
 const char* fq_status_string(int st) {
@@ -723,12 +734,21 @@ fq_status fq_side_stream_create(int reserve_cus, void** stream) {
     e = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
   }
   if (e != hipSuccess) return hip_fail(e, "stream creation");
+  {
+    std::lock_guard<std::mutex> lock(g_side_mu);
+    g_side_streams.push_back(s);
+  }
   *stream = s;
   return FQ_OK;
 }
 
 fq_status fq_side_stream_destroy(void* stream) {
   if (!stream) return fail(FQ_ERR_INVALID_ARG, "stream is NULL");
+  {
+    std::lock_guard<std::mutex> lock(g_side_mu);
+    auto it = std::find(g_side_streams.begin(), g_side_streams.end(), (hipStream_t)stream);
+    if (it != g_side_streams.end()) g_side_streams.erase(it);
+  }
   const hipError_t e = hipStreamDestroy((hipStream_t)stream);
   return e == hipSuccess ? FQ_OK : hip_fail(e, "stream destruction");
 }

@@ -150,6 +150,9 @@ hipError_t tff_rows_synthesis(const u16* Vhi, const u16* Vlo, int64_t n, const T
                               const u16* Fhi, const u16* Flo, float* Z, float* tmp, float* out,
                               int64_t ldout, hipStream_t s);
 hipError_t sym_average(float* X, int64_t n, int64_t ld, hipStream_t s);
+// true for a stream made by fq_side_stream_create (part of the device, shared with the
+// caller's other streams)
+bool is_side_stream(hipStream_t s);
 
 // Seeded Haar factor f (tff_seed.hip): out (n x n fp32) from seed; G, V: n x n fp64
 // scratch each, ab: 2n fp64

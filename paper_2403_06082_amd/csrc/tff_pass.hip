@@ -621,7 +621,8 @@ void launch_rot_fused(const XT* X, int64_t ldx, int64_t n, const TffDev& F, cons
   // rows per work-group: at least FR_NV (the resident factors serve them all), and as
   // many as fill the device's work-group slots in one round when that takes fewer row
   // times than rounds of FR_NV rows (e.g. 4512 rows of the 11008-wide frame: one round of
-  // 18 rows instead of five of 4)
+  // 18 rows instead of five of 4).  On a side stream, which shares its compute units with
+  // the caller's other work, FR_NV, so that many short work-groups balance the load.
   static int n_cu = 0;
   if (n_cu <= 0) {
     int dev = 0;
@@ -632,7 +633,8 @@ void launch_rot_fused(const XT* X, int64_t ldx, int64_t n, const TffDev& F, cons
   }
   const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>((int64_t)(160 * 1024) / (int64_t)lds, 32 / NW));
   const int64_t groups = std::max<int64_t>(1, (int64_t)n_cu * per_cu / njb);   // row groups at once
-  const int nv = (int)std::max<int64_t>(FR_NV, std::min<int64_t>((n + groups - 1) / groups, 64));
+  const int nv = is_side_stream(s) ? FR_NV
+                                    : (int)std::max<int64_t>(FR_NV, std::min<int64_t>((n + groups - 1) / groups, 64));
   const dim3 g((unsigned)(njb * ((n + nv - 1) / nv))), b((unsigned)(64 * NW));
   const bool small = (int64_t)F.d1 * (F.d2 / 4) <= 64 * NW * 4;
   // 16-byte output runs: 8-element runs start 16-byte aligned in every destination row
