@@ -196,7 +196,9 @@ fq_status fq_quantize_status(void* stream, int64_t K_out, int64_t K_in, int bloc
  *                release it with fq_side_stream_destroy.
  * A stream with a CU mask synchronizes with the legacy default stream (NULL) as a blocking
  * stream does: the work it runs beside must be queued on another stream, or the two
- * serialize.
+ * serialize.  The library remembers the streams made here until fq_side_stream_destroy:
+ * kernels it queues on them keep many short work-groups (their compute units are shared),
+ * where on other streams it may size work-groups to fill the whole device in one round.
  * Errors: FQ_ERR_INVALID_ARG (reserve_cus out of range, stream NULL), FQ_ERR_HIP.
  */
 fq_status fq_side_stream_create(int reserve_cus, void** stream);
