@@ -226,16 +226,18 @@ __global__ __launch_bounds__(TT) void k_dft_blocks(int k, int m, int nb, int pm,
                                                    float scale, const float* __restrict__ colscale,
                                                    int rho, u16* __restrict__ hi,
                                                    u16* __restrict__ lo) {
-  const int hm = pm / 2, hk = pk / 2;
-  const int64_t total = (int64_t)nb * hm * hk;
-  for (int64_t e = (int64_t)blockIdx.x * TT + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * TT) {
-    const int64_t c = e / ((int64_t)hm * hk);
-    const int64_t rc = e - c * hm * hk;
-    const int j = (int)(rc / hk), sx = (int)(rc - (int64_t)j * hk);
+  // grid (ceil(hk / TT), hm, nb): slot sx, coordinate pair j, block c (no index division)
+  const int hk = pk / 2;
+  const int sx = (int)(blockIdx.x * TT + threadIdx.x);
+  const int j = (int)blockIdx.y;
+  const int64_t c = blockIdx.z;
+  if (sx >= hk) return;
+  {
     float cs = 0.f, sn = 0.f;
     if (j < m && sx < k) {
-      const int64_t ph = ((c * m + j) % k) * sx % k;
+      // (c m + j) mod k < k and sx < k <= 3968: the product fits 32 bits
+      const int base = (int)((c * m + j) % k);
+      const int64_t ph = (int)((uint32_t)(base * sx) % (uint32_t)k);
       sincospif(2.0f * (float)ph / (float)k, &sn, &cs);
       cs *= scale;
       sn *= scale;
@@ -743,7 +745,7 @@ TffPassGeom tff_pass_geom(const TffDev& F) {
 hipError_t tff_dft_blocks(const TffDev& F, u16* hi, u16* lo, hipStream_t s, const float* colscale) {
   const TffPassGeom g = tff_pass_geom(F);
   prof_begin(s, "tffp_blocks");
-  hipLaunchKernelGGL(k_dft_blocks, dim3(grid_1d(g.nb * (g.pm / 2) * (g.pk / 2))), dim3(TT), 0, s, (int)F.k,
+  hipLaunchKernelGGL(k_dft_blocks, dim3((unsigned)((g.pk / 2 + TT - 1) / TT), (unsigned)(g.pm / 2), (unsigned)g.nb), dim3(TT), 0, s, (int)F.k,
                      (int)F.m, (int)g.nb, (int)g.pm, (int)g.pk,
                      (float)(1.0 / std::sqrt((double)F.k)), colscale, (int)F.rho, hi, lo);
   prof_end(s);
